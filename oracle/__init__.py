@@ -1,0 +1,199 @@
+"""fp64 CPU oracle for the contracted Clebsch-Gordan products.
+
+TEST INFRASTRUCTURE ONLY: tests/, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package; the product path
+(``paper_2605_15073_amd``) never does, and the two share no code.
+
+The arithmetic lives in ``cgtp_oracle.c`` (plain C, fp64, OpenMP over nodes);
+this module only loads it with ctypes and marshals numpy arrays. See that file
+for what is computed and which passages of the paper each part follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "cgtp_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so from cgtp_oracle.c with gcc (fp64, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.run(
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+             "-o", tmp, _SRC, "-lm"],
+            check=True,
+        )
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build(force=True)
+    lib = ctypes.CDLL(_LIB)
+    i32, i64, dbl = ctypes.c_int, ctypes.c_long, ctypes.c_double
+    p = ctypes.c_void_p
+    for name in ("cgo_wigner3j", "cgo_cg", "cgo_gaunt_conj", "cgo_curl_conj_im"):
+        getattr(lib, name).restype = dbl
+        getattr(lib, name).argtypes = [i32] * 6
+    lib.cgo_kappa_inv_im.restype = dbl
+    lib.cgo_kappa_inv_im.argtypes = [i32] * 3
+    lib.cgo_real_entry.restype = dbl
+    lib.cgo_real_entry.argtypes = [i32] * 7 + [ctypes.POINTER(dbl)]
+    lib.cgo_real_table.restype = i64
+    lib.cgo_real_table.argtypes = [i32, i32, i32, p, p, p, p, i64, ctypes.POINTER(dbl)]
+    lib.cgo_real_sh.restype = None
+    lib.cgo_real_sh.argtypes = [i32, dbl, dbl, dbl, p]
+    lib.cgo_onsite.restype = i32
+    lib.cgo_onsite.argtypes = [i32, i32, i32, i64, p, p, p, p, p, p, p, p, i32]
+    lib.cgo_message_pass.restype = i32
+    lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64, p, p, p, p, p, p, p, p, p,
+                                     p, i64, p, p, i32]
+    lib.cgo_max_threads.restype = i32
+    lib.cgo_max_threads.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a), dtype=np.float64)
+
+
+def max_threads() -> int:
+    return int(_load().cgo_max_threads())
+
+
+def wigner3j(j1, j2, j3, m1, m2, m3) -> float:
+    return _load().cgo_wigner3j(j1, j2, j3, m1, m2, m3)
+
+
+def cg(l1, m1, l2, m2, l, m) -> float:
+    """<l1 m1 l2 m2 | l m> (Condon-Shortley)."""
+    return _load().cgo_cg(l1, m1, l2, m2, l, m)
+
+
+def gaunt_conj(l1, m1, l2, m2, l, m) -> float:
+    """int Y_{l1m1} Y_{l2m2} Y*_{lm} (Eq. cg-integral), complex CS basis."""
+    return _load().cgo_gaunt_conj(l1, m1, l2, m2, l, m)
+
+
+def curl_conj_im(l1, m1, l2, m2, l, m) -> float:
+    """Im int Y*_{lm} {Y_{l1m1}, Y_{l2m2}} (Eq. Q-CG); the value is purely imaginary."""
+    return _load().cgo_curl_conj_im(l1, m1, l2, m2, l, m)
+
+
+def kappa_inv_im(l1, l2, l) -> float:
+    """Im kappa^-1(l1, l2, l) of Eq. kappa-inv-closed on the parity-odd support, else 0."""
+    return _load().cgo_kappa_inv_im(l1, l2, l)
+
+
+def real_entry(kind: int, l1, m1, l2, m2, l3, m3):
+    """(value, imaginary residue) of int Y^R Y^R Y^R (kind 0) or int {Y^R, Y^R} Y^R (kind 1)."""
+    im = ctypes.c_double(0.0)
+    v = _load().cgo_real_entry(kind, l1, m1, l2, m2, l3, m3, ctypes.byref(im))
+    return v, im.value
+
+
+def real_table(kind: int, lmax_in: int, lmax_out: int | None = None):
+    """Sparse real table: (k1, k2, k3, val, max_imag). kind 0 = Gaunt GR, 1 = curl QR."""
+    lib = _load()
+    if lmax_out is None:
+        lmax_out = lmax_in
+    mi = ctypes.c_double(0.0)
+    n = lib.cgo_real_table(kind, lmax_in, lmax_out, None, None, None, None, 0, ctypes.byref(mi))
+    k1 = np.zeros(max(n, 1), np.int32)
+    k2 = np.zeros(max(n, 1), np.int32)
+    k3 = np.zeros(max(n, 1), np.int32)
+    v = np.zeros(max(n, 1), np.float64)
+    lib.cgo_real_table(kind, lmax_in, lmax_out, _ptr(k1), _ptr(k2), _ptr(k3), _ptr(v), n,
+                       ctypes.byref(mi))
+    return k1[:n], k2[:n], k3[:n], v[:n], mi.value
+
+
+def dense_table(kind: int, lmax_in: int, lmax_out: int | None = None) -> np.ndarray:
+    """Dense [(lmax_in+1)^2, (lmax_in+1)^2, (lmax_out+1)^2] real table."""
+    if lmax_out is None:
+        lmax_out = lmax_in
+    k1, k2, k3, v, _ = real_table(kind, lmax_in, lmax_out)
+    n_in, n_out = (lmax_in + 1) ** 2, (lmax_out + 1) ** 2
+    t = np.zeros((n_in, n_in, n_out))
+    t[k1, k2, k3] = v
+    return t
+
+
+def real_sh(lmax: int, unit) -> np.ndarray:
+    """Real SH of App. C Eq. realY at unit vectors [..., 3] -> [..., (lmax+1)^2]."""
+    lib = _load()
+    u = _f64(unit).reshape(-1, 3)
+    out = np.zeros((u.shape[0], (lmax + 1) ** 2))
+    row = np.zeros((lmax + 1) ** 2)
+    for i in range(u.shape[0]):
+        lib.cgo_real_sh(lmax, float(u[i, 0]), float(u[i, 1]), float(u[i, 2]), _ptr(row))
+        out[i] = row
+    return out.reshape(tuple(np.shape(unit)[:-1]) + ((lmax + 1) ** 2,))
+
+
+def onsite(lmax, A, B, U_A, U_B, U_out_even, U_out_odd, nthreads: int = 0):
+    """On-site contracted product, fp64. A, B: [N, C, L^2]; U_*: [L, C, R].
+
+    Returns (out_even, out_odd), each [N, C, L^2] float64."""
+    lib = _load()
+    A, B = _f64(A), _f64(B)
+    U_A, U_B, U_oe, U_oo = _f64(U_A), _f64(U_B), _f64(U_out_even), _f64(U_out_odd)
+    N, C, L2 = A.shape
+    R = U_A.shape[2]
+    assert L2 == (lmax + 1) ** 2 and B.shape == A.shape
+    for U in (U_A, U_B, U_oe, U_oo):
+        assert U.shape == (lmax + 1, C, R)
+    oe = np.zeros((N, C, L2))
+    oo = np.zeros((N, C, L2))
+    rc = lib.cgo_onsite(lmax, C, R, N, _ptr(A), _ptr(B), _ptr(U_A), _ptr(U_B), _ptr(U_oe),
+                        _ptr(U_oo), _ptr(oe), _ptr(oo), int(nthreads))
+    if rc != 0:
+        raise RuntimeError(f"cgo_onsite failed ({rc})")
+    return oe, oo
+
+
+def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
+                 U_out_even, U_out_odd, receivers=None, nthreads: int = 0):
+    """Message-passing contracted product, fp64, for a receiver subset.
+
+    row_ptr [N+1], col [E] (int32 CSR by receiver), edge_unit [E,3],
+    edge_radial [E,C,L], node_feat [N,C,L^2], U_*: [L,C,R].
+    Returns (out_even, out_odd), each [len(receivers), C, L^2]."""
+    lib = _load()
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    col = np.ascontiguousarray(col, dtype=np.int32)
+    eu, er, nf = _f64(edge_unit), _f64(edge_radial), _f64(node_feat)
+    U_E, U_I, U_oe, U_oo = _f64(U_E), _f64(U_I), _f64(U_out_even), _f64(U_out_odd)
+    N, C, L2 = nf.shape
+    E = col.shape[0]
+    R = U_E.shape[2]
+    assert L2 == (lmax + 1) ** 2 and row_ptr.shape[0] == N + 1
+    assert er.shape == (E, C, lmax + 1) and eu.shape == (E, 3)
+    if receivers is None:
+        receivers = np.arange(N)
+    rec = np.ascontiguousarray(receivers, dtype=np.int64)
+    oe = np.zeros((rec.shape[0], C, L2))
+    oo = np.zeros((rec.shape[0], C, L2))
+    rc = lib.cgo_message_pass(lmax, C, R, N, E, _ptr(row_ptr), _ptr(col), _ptr(eu), _ptr(er),
+                              _ptr(nf), _ptr(U_E), _ptr(U_I), _ptr(U_oe), _ptr(U_oo), _ptr(rec),
+                              rec.shape[0], _ptr(oe), _ptr(oo), int(nthreads))
+    if rc != 0:
+        raise RuntimeError(f"cgo_message_pass failed ({rc})")
+    return oe, oo

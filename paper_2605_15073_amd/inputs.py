@@ -1,0 +1,145 @@
+"""Seeded synthetic inputs for the contracted CG products.
+
+This module only draws random numbers and builds neighbour lists; it holds none
+of the method's arithmetic (no spherical harmonics, no coupling). Both the GPU
+path and the fp64 oracle consume exactly the arrays produced here.
+
+Recipe (the paper benchmarks on random atomic environments, Sec. "Numerical
+performance"; no public dataset is involved):
+
+* RNG: ``numpy.random.default_rng(seed)`` (PCG64), fp64 standard normals rounded
+  to fp32 once, so every consumer sees identical values.
+* CP factor matrices ``[L][C][R]`` per degree: N(0, 1/C).
+* Coefficients ``[N][C][L^2]``: N(0, 1), optionally scaled by 1/(2l+1) per degree.
+* Message passing: atoms uniform in a periodic cube of side (N/density)^(1/3);
+  directed edges j -> i for 0 < |r_j - r_i| < r_cut (minimum image), CSR sorted
+  by receiver i, senders ascending in a row, atoms in generator (random) order.
+  ``edge_unit`` = (r_j - r_i)/|r_j - r_i|. Radial features
+  R_{n l}(r) = sum_k W[l][n][k] g_k(r) with 8 Gaussians
+  g_k(r) = exp(-(r - k r_cut/7)^2 / (2 (r_cut/7)^2)), W ~ N(0, 1/8).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+
+def _normal(rng: np.random.Generator, shape, scale=1.0) -> np.ndarray:
+    return (rng.standard_normal(shape) * scale).astype(np.float32)
+
+
+def degree_scale(lmax: int) -> np.ndarray:
+    """1/(2l+1) for every flattened index k = l*l + l + m."""
+    return np.concatenate([np.full(2 * l + 1, 1.0 / (2 * l + 1)) for l in range(lmax + 1)])
+
+
+def cp_factors(rng: np.random.Generator, lmax: int, C: int, R: int) -> np.ndarray:
+    return _normal(rng, (lmax + 1, C, R), 1.0 / np.sqrt(C))
+
+
+def coefficients(rng: np.random.Generator, n: int, C: int, lmax: int, per_degree: bool):
+    x = rng.standard_normal((n, C, (lmax + 1) ** 2))
+    if per_degree:
+        x = x * degree_scale(lmax)[None, None, :]
+    return x.astype(np.float32)
+
+
+def onsite_inputs(n: int, lmax: int, C: int, R: int, seed: int, per_degree: bool = False,
+                  self_coupled: bool = False, distinct_out: bool = False):
+    """Draw order: A, B (skipped when B := A), U_A, U_B, U_out (, U_out_odd)."""
+    rng = np.random.default_rng(seed)
+    A = coefficients(rng, n, C, lmax, per_degree)
+    B = A if self_coupled else coefficients(rng, n, C, lmax, per_degree)
+    U_A = cp_factors(rng, lmax, C, R)
+    U_B = cp_factors(rng, lmax, C, R)
+    U_out = cp_factors(rng, lmax, C, R)
+    U_out_odd = cp_factors(rng, lmax, C, R) if distinct_out else U_out
+    return dict(A=A, B=B, U_A=U_A, U_B=U_B, U_out_even=U_out, U_out_odd=U_out_odd)
+
+
+def periodic_neighbours(pos: np.ndarray, box: float, r_cut: float):
+    """CSR (by receiver) of directed edges j -> i with 0 < |r_j - r_i|_min-image < r_cut."""
+    from scipy.spatial import cKDTree
+
+    if not r_cut < box / 2:
+        raise ValueError("r_cut must be below half the box side for minimum-image edges")
+    n = pos.shape[0]
+    tree = cKDTree(pos, boxsize=box)
+    pairs = tree.query_pairs(r_cut, output_type="ndarray")
+    if pairs.size == 0:
+        pairs = np.zeros((0, 2), dtype=np.int64)
+    recv = np.concatenate([pairs[:, 0], pairs[:, 1]])
+    send = np.concatenate([pairs[:, 1], pairs[:, 0]])
+    order = np.lexsort((send, recv))
+    recv, send = recv[order], send[order]
+    d = pos[send] - pos[recv]
+    d -= box * np.round(d / box)
+    dist = np.linalg.norm(d, axis=1)
+    keep = dist > 0
+    recv, send, d, dist = recv[keep], send[keep], d[keep], dist[keep]
+    row_ptr = np.zeros(n + 1, dtype=np.int64)
+    np.add.at(row_ptr, recv + 1, 1)
+    row_ptr = np.cumsum(row_ptr)
+    return row_ptr.astype(np.int32), send.astype(np.int32), d, dist
+
+
+def gaussian_radial(dist: np.ndarray, r_cut: float, n_basis: int = 8) -> np.ndarray:
+    mu = np.arange(n_basis) * r_cut / (n_basis - 1)
+    sigma = r_cut / (n_basis - 1)
+    return np.exp(-((dist[:, None] - mu[None, :]) ** 2) / (2 * sigma ** 2))
+
+
+def mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, density: float = 0.1,
+              r_cut: float = 5.0, n_basis: int = 8, distinct_out: bool = False):
+    """Draw order: positions, W_rad, I, U_E, U_I, U_out (, U_out_odd)."""
+    rng = np.random.default_rng(seed)
+    box = (n_atoms / density) ** (1.0 / 3.0)
+    pos = rng.uniform(0.0, box, size=(n_atoms, 3))
+    W_rad = rng.standard_normal((lmax + 1, C, n_basis)) / np.sqrt(n_basis)
+    node_feat = coefficients(rng, n_atoms, C, lmax, per_degree=False)
+    U_E = cp_factors(rng, lmax, C, R)
+    U_I = cp_factors(rng, lmax, C, R)
+    U_out = cp_factors(rng, lmax, C, R)
+    U_out_odd = cp_factors(rng, lmax, C, R) if distinct_out else U_out
+    row_ptr, col, d, dist = periodic_neighbours(pos, box, r_cut)
+    edge_unit = (d / dist[:, None]).astype(np.float32)
+    g = gaussian_radial(dist, r_cut, n_basis)                    # [E, K]
+    edge_radial = np.empty((g.shape[0], C, lmax + 1), dtype=np.float32)  # [E, C, L]
+    for l in range(lmax + 1):
+        edge_radial[:, :, l] = g @ W_rad[l].T
+    return dict(row_ptr=row_ptr, col=col, edge_unit=edge_unit, edge_radial=edge_radial,
+                node_feat=node_feat, U_E=U_E, U_I=U_I, U_out_even=U_out, U_out_odd=U_out_odd,
+                box=box, n_edges=int(col.shape[0]))
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    kind: str          # "onsite" or "mp"
+    n: int             # nodes (on-site) or atoms (message passing)
+    lmax: int
+    C: int
+    R: int
+    seed: int
+    per_degree: bool = False
+    self_coupled: bool = False
+    r_cut: float = 5.0
+
+    def make(self, **kw):
+        if self.kind == "onsite":
+            return onsite_inputs(self.n, self.lmax, self.C, self.R, self.seed,
+                                 per_degree=self.per_degree, self_coupled=self.self_coupled, **kw)
+        return mp_inputs(self.n, self.lmax, self.C, self.R, self.seed, r_cut=self.r_cut, **kw)
+
+
+# The five workloads of the benchmark plan, named by what they are.
+WORKLOADS = {
+    "onsite_n64_l2_c8": Workload("onsite_n64_l2_c8", "onsite", 64, 2, 8, 8, seed=0),
+    "onsite_ace_n2048_l4_c64": Workload("onsite_ace_n2048_l4_c64", "onsite", 2048, 4, 64, 64,
+                                        seed=1, per_degree=True, self_coupled=True),
+    "mp_10k_l6_c128": Workload("mp_10k_l6_c128", "mp", 10000, 6, 128, 128, seed=2),
+    "onsite_n4096_l12_c128": Workload("onsite_n4096_l12_c128", "onsite", 4096, 12, 128, 128,
+                                      seed=3, per_degree=True),
+    "mp_5k_l20_c64": Workload("mp_5k_l20_c64", "mp", 5000, 20, 64, 64, seed=4),
+}
