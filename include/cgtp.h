@@ -1,0 +1,179 @@
+/*
+ * cgtp.h - contracted Clebsch-Gordan tensor products on a structured
+ * Gauss-Legendre x Fourier S^2 grid, for AMD Instinct MI355X (gfx950).
+ *
+ * Method: Bochkarev, Lysogorskiy, Drautz, "Fast contracted Clebsch-Gordan tensor
+ * products for equivariant graph neural networks" (SCALE-CG). The library
+ * evaluates, for CP-factorised channel mixing (Eq. cp-decomp),
+ *
+ *   on-site (Eq. phi-cg, natural-parity inputs):
+ *     out_even = Category alpha (Gaunt product, l1+l2+l even), parity (-1)^l
+ *     out_odd  = Category beta  (surface curl / spherical Poisson bracket
+ *                {A,B} = r.(grad A x grad B), Eq. poisson-S2-x; l1+l2+l odd),
+ *                parity -(-1)^l
+ *   message passing (Eq. msgpass-parity-start, single natural-parity node slot,
+ *   edge feature R_{n l1}(r_ji) Y_{l1 m1}(rhat_ji)):
+ *     out_even/out_odd as above, summed over the neighbours j of receiver i.
+ *
+ * Both follow the structured pipelines (Sec. "Optimized computational
+ * pipelines": Eqs. struct-H..struct-phi and msgpass-tildeR..cat-beta-phi) in
+ * the real SH basis of App. C (Eq. realY, no Condon-Shortley phase):
+ *   Y_{l,m>0} = sqrt2 Pt_l^m(cos th) cos(m ph), Y_{l,0} = Pt_l^0(cos th),
+ *   Y_{l,m<0} = sqrt2 Pt_l^|m|(cos th) sin(|m| ph),
+ *   Pt_l^m = sqrt((2l+1)/(4 pi) (l-m)!/(l+m)!) P_l^m.
+ * With H1 = U_1^T X1, H2 = U_2^T X2 per degree (Eq. struct-H), the outputs are
+ *   out_even[n][k] = sum_r U_out_even[l][n][r] sum_{k1,k2} G[k1,k2,k] H1[r][k1] H2[r][k2]
+ *   out_odd [n][k] = sum_r U_out_odd [l][n][r] sum_{k1,k2} Q[k1,k2,k] H1[r][k1] H2[r][k2]
+ * where G = int Y_k1 Y_k2 Y_k (Eq. gaunt) and Q = int {Y_k1, Y_k2} Y_k (Eq. Q-def)
+ * are the real-basis Gaunt and curl tables. The prefactors f and kappa of
+ * Eqs. msgpass-cp-alpha/beta are absorbed in the learnable factors, as the paper
+ * parameterises them. The first operand of the bracket is A (on-site) or the
+ * edge field (message passing); exchanging the operands negates out_odd.
+ *
+ * Conventions for every entry point:
+ *  - All tensors are dense, row-major, contiguous, in device memory, of the
+ *    plan's dtype (fp32, or fp64 for a CGTP_F64 plan), except the int32 CSR
+ *    arrays. The flattened SH index is k = l*l + l + m, K = (lmax+1)^2 and
+ *    L = lmax+1. Factor matrices are [L][C][R]: U[l][n][r] with n the radial
+ *    channel and r the CP rank.
+ *  - The caller owns every buffer it passes. Inputs are read only. Outputs are
+ *    fully overwritten (no accumulation into existing contents).
+ *  - Calls are asynchronous on `stream` (a hipStream_t cast to void*, NULL for
+ *    the default stream): they return after enqueueing the kernels.
+ *  - Every function returns CGTP_OK (0) or a negative status; none aborts or
+ *    throws. cgtp_last_error() gives the detail of the last failure on the
+ *    calling thread. A plan is not thread-safe: use it from one host thread and
+ *    one stream at a time.
+ */
+#ifndef CGTP_H
+#define CGTP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CGTP_MAX_LMAX 24
+
+/* status codes */
+#define CGTP_OK 0
+#define CGTP_ERR_ARG (-1)         /* NULL pointer, negative size, bad descriptor */
+#define CGTP_ERR_WORKSPACE (-2)   /* caller workspace smaller than cgtp_workspace_bytes() */
+#define CGTP_ERR_CSR (-3)         /* CSR rejected (only checked with CGTP_VALIDATE_CSR) */
+#define CGTP_ERR_HIP (-4)         /* HIP runtime / launch failure; see cgtp_last_error() */
+#define CGTP_ERR_UNSUPPORTED (-5) /* valid request this build does not support */
+
+/* dtypes */
+#define CGTP_F32 0
+#define CGTP_F64 1
+
+/* plan flags */
+#define CGTP_VALIDATE_CSR 1u   /* copy the CSR to the host and check it before launching */
+#define CGTP_EDGE_SEPARATED 2u /* edge field by separated Legendre+Fourier synthesis
+                                  (Eqs. msgpass-FE, msgpass-AE) instead of the zonal
+                                  addition-theorem form; same values, more work */
+
+/* operations for cgtp_workspace_bytes */
+#define CGTP_OP_ONSITE 0
+#define CGTP_OP_MESSAGE_PASS 1
+
+typedef struct cgtp_plan_s *cgtp_plan;
+
+typedef struct {
+    int lmax;       /* band limit, 0 <= lmax <= CGTP_MAX_LMAX */
+    int channels;   /* C >= 1 radial channels (input = output, as in the paper's benchmark) */
+    int rank;       /* R >= 1 CP rank */
+    int n_theta;    /* Gauss-Legendre nodes; 0 => ceil((3 lmax + 2)/2); otherwise must be
+                       >= ceil((3 lmax + 1)/2), the exactness bound of Sec. "Representation
+                       using Structured Tensor-Product Grids" */
+    int n_phi;      /* equispaced phi nodes phi_v = 2 pi v / n_phi; 0 => 3 lmax + 1; otherwise
+                       must be >= 3 lmax + 1 */
+    int dtype;      /* CGTP_F32 or CGTP_F64 */
+    unsigned flags; /* CGTP_VALIDATE_CSR | CGTP_EDGE_SEPARATED */
+} cgtp_desc;
+
+/* Create a plan: validates the descriptor, builds the grid tables on the host in
+ * fp64 (Gauss-Legendre nodes/weights, Pt_l^m and dPt_l^m/dx at the nodes, real
+ * Fourier factors q_vm of Eq. realq) and uploads them in the plan's dtype to the
+ * current HIP device. The plan owns these tables (and any workspace it grows
+ * itself) until cgtp_destroy. Errors: CGTP_ERR_ARG (bad descriptor or NULL out),
+ * CGTP_ERR_UNSUPPORTED (a size whose on-chip staging exceeds the kernel limits),
+ * CGTP_ERR_HIP (allocation/copy failure). *plan is NULL on failure. */
+int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan);
+
+/* Grid actually used by the plan (after defaults). Any pointer may be NULL. */
+int cgtp_plan_grid(cgtp_plan plan, int *n_theta, int *n_phi);
+
+/* Bytes of device workspace an operation needs for n_nodes nodes and n_edges
+ * edges (n_edges ignored for CGTP_OP_ONSITE). */
+int cgtp_workspace_bytes(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edges,
+                         size_t *bytes);
+
+/* On-site contraction, Eq. phi-cg with Eq. cp-decomp, by the structured
+ * pipeline (Eqs. struct-H, struct-F, struct-tildeA, struct-S, struct-Tmu,
+ * struct-Tlm, struct-phi) plus the surface-curl channel (Eq. cat-beta-curl with
+ * the neighbour sum dropped, as in the on-site paragraph of the same section).
+ *   A, B                  [N][C][K] natural-parity coefficients; B may equal A.
+ *   U_A, U_B              [L][C][R] first-operand and second-operand CP factors.
+ *   U_out_even, U_out_odd [L][C][R] output projections (lambda); may alias.
+ *   out_even, out_odd     [N][C][K]; either may be NULL to skip that channel (not both).
+ *   workspace, ws_bytes   device scratch of at least cgtp_workspace_bytes(ONSITE);
+ *                         workspace == NULL => the plan allocates and keeps one.
+ * n_nodes == 0 is a no-op (pointers may then be NULL).
+ * Errors: CGTP_ERR_ARG, CGTP_ERR_WORKSPACE, CGTP_ERR_HIP. */
+int cgtp_onsite(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B,
+                const void *U_A, const void *U_B, const void *U_out_even,
+                const void *U_out_odd, void *out_even, void *out_odd, void *workspace,
+                size_t ws_bytes, void *stream);
+
+/* Message passing, Eq. msgpass-parity-start, by the parity-aware pipeline
+ * (Eqs. msgpass-tildeR, msgpass-HI, msgpass-FI, msgpass-AI, msgpass-S,
+ * cat-beta-curl, msgpass-Tmu, msgpass-Tlm, cat-alpha-phi, cat-beta-phi) for a
+ * single natural-parity node slot, where Case A feeds out_even and Case B
+ * feeds out_odd (Table 1).
+ *   row_ptr [N+1], col [E]  int32 CSR by receiver i: edges e in [row_ptr[i],
+ *                           row_ptr[i+1]) carry messages from sender j = col[e] to i.
+ *   edge_unit   [E][3]      direction of r_ji = r_j - r_i (renormalised; must be non-zero).
+ *   edge_radial [E][C][L]   radial features R_{n l1}(|r_ji|).
+ *   node_feat   [N][C][K]   sender features I_j (natural parity).
+ *   U_E, U_I                [L][C][R] CP factors of the edge and node operands.
+ *   U_out_even, U_out_odd   [L][C][R] output projections; may alias.
+ *   out_even, out_odd       [N][C][K]; either may be NULL (not both). Receivers
+ *                           with no edges get zeros.
+ * n_nodes == 0 (with n_edges == 0) is a no-op; with n_edges == 0 the edge pointers
+ * may be NULL. Preconditions (checked only with CGTP_VALIDATE_CSR): row_ptr[0] = 0,
+ * non-decreasing, row_ptr[N] = E, 0 <= col[e] < N; E < 2^31.
+ * Errors: CGTP_ERR_ARG, CGTP_ERR_WORKSPACE, CGTP_ERR_CSR, CGTP_ERR_HIP. */
+int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
+                      const int32_t *row_ptr, const int32_t *col, const void *edge_unit,
+                      const void *edge_radial, const void *node_feat, const void *U_E,
+                      const void *U_I, const void *U_out_even, const void *U_out_odd,
+                      void *out_even, void *out_odd, void *workspace, size_t ws_bytes,
+                      void *stream);
+
+/* Release the plan and everything it owns. Synchronises the device first.
+ * cgtp_destroy(NULL) is a no-op. */
+int cgtp_destroy(cgtp_plan plan);
+
+/* Static description of a status code. */
+const char *cgtp_status_string(int status);
+
+/* Detail message of the last failing call on this host thread ("" if none). */
+const char *cgtp_last_error(void);
+
+/* Host-only (no GPU needed): the fp64 grid tables a plan would upload, for
+ * testing. Sizes with U = n_theta, V = n_phi, P = (lmax+1)(lmax+2)/2:
+ *   x[U], w[U]         Gauss-Legendre nodes cos(theta_u) and weights (sum 2)
+ *   p[U][P], dp[U][P]  Pt_l^m(x_u) and dPt_l^m/dx(x_u), index l(l+1)/2 + m, m >= 0
+ *   q[V][2 lmax + 1]   real Fourier factors q_vm of Eq. realq, column m + lmax
+ * Any output pointer may be NULL. n_theta / n_phi follow the cgtp_desc rules. */
+int cgtp_host_tables(int lmax, int n_theta, int n_phi, double *x, double *w, double *p,
+                     double *dp, double *q);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CGTP_H */

@@ -175,7 +175,35 @@ def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I
 
     row_ptr [N+1], col [E] (int32 CSR by receiver), edge_unit [E,3],
     edge_radial [E,C,L], node_feat [N,C,L^2], U_*: [L,C,R].
-    Returns (out_even, out_odd), each [len(receivers), C, L^2]."""
+    Returns (out_even, out_odd), each [len(receivers), C, L^2] (all receivers
+    when receivers is None)."""
+    if receivers is None:
+        n = np.asarray(node_feat).shape[0]
+        return _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
+                        U_out_even, U_out_odd, np.arange(n), nthreads)
+    # Marshalling only: cut out the rows of the requested receivers and the
+    # features of their senders, so large inputs are not converted to fp64 whole.
+    row_ptr = np.asarray(row_ptr)
+    rec = np.asarray(receivers, dtype=np.int64)
+    starts, ends = row_ptr[rec].astype(np.int64), row_ptr[rec + 1].astype(np.int64)
+    parts = [np.arange(a, b, dtype=np.int64) for a, b in zip(starts, ends)]
+    eidx = np.concatenate(parts) if parts else np.zeros(0, np.int64)
+    senders, local_col = np.unique(np.asarray(col)[eidx], return_inverse=True)
+    # compact graph: node q < len(rec) is receiver rec[q]; node table rows are the senders
+    n_compact = max(len(rec), len(senders), 1)
+    nf_full = np.asarray(node_feat)
+    nf = np.zeros((n_compact,) + nf_full.shape[1:], dtype=np.float64)
+    nf[:len(senders)] = nf_full[senders]
+    rp = np.zeros(n_compact + 1, np.int32)
+    rp[1:len(rec) + 1] = np.cumsum(ends - starts)
+    rp[len(rec) + 1:] = rp[len(rec)]
+    return _mp_rows(lmax, rp, local_col.astype(np.int32), np.asarray(edge_unit)[eidx],
+                    np.asarray(edge_radial)[eidx], nf, U_E, U_I, U_out_even, U_out_odd,
+                    np.arange(len(rec)), nthreads)
+
+
+def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I, U_out_even,
+             U_out_odd, receivers, nthreads):
     lib = _load()
     row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
     col = np.ascontiguousarray(col, dtype=np.int32)
@@ -186,8 +214,6 @@ def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I
     R = U_E.shape[2]
     assert L2 == (lmax + 1) ** 2 and row_ptr.shape[0] == N + 1
     assert er.shape == (E, C, lmax + 1) and eu.shape == (E, 3)
-    if receivers is None:
-        receivers = np.arange(N)
     rec = np.ascontiguousarray(receivers, dtype=np.int64)
     oe = np.zeros((rec.shape[0], C, L2))
     oo = np.zeros((rec.shape[0], C, L2))

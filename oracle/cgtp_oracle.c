@@ -224,41 +224,72 @@ double cgo_real_entry(int kind, int l1, int m1, int l2, int m2, int l3, int m3, 
     return (double)v;
 }
 
+/* Entries of one l1 block, appended at arrays + n (count only when val is NULL). */
+static long real_table_block(int kind, int l1, int lmax_in, int lmax_out, int32_t *k1,
+                             int32_t *k2, int32_t *k3, double *val, long n, long double *worst_im)
+{
+    for (int m1 = -l1; m1 <= l1; ++m1)
+        for (int l2 = 0; l2 <= lmax_in; ++l2)
+            for (int m2 = -l2; m2 <= l2; ++m2)
+                for (int l3 = abs(l1 - l2); l3 <= imin(l1 + l2, lmax_out); ++l3)
+                    for (int m3 = -l3; m3 <= l3; ++m3) {
+                        int am = abs(m3);
+                        /* only |m3| = |m1|+|m2| or ||m1|-|m2|| can pair with mu1+mu2+mu3=0 */
+                        if (am != abs(m1) + abs(m2) && am != abs(abs(m1) - abs(m2))) continue;
+                        long double im = 0.0L;
+                        long double v = real_entry(kind, l1, m1, l2, m2, l3, m3, &im);
+                        if (fabsl(im) > *worst_im) *worst_im = fabsl(im);
+                        if (fabsl(v) <= 1e-12L) continue;
+                        if (val) {
+                            k1[n] = l1 * l1 + l1 + m1;
+                            k2[n] = l2 * l2 + l2 + m2;
+                            k3[n] = l3 * l3 + l3 + m3;
+                            val[n] = (double)v;
+                        }
+                        ++n;
+                    }
+    return n;
+}
+
 /* Sparse real table over all k1, k2 <= lmax_in and k3 <= lmax_out:
  * entries (k1, k2, k3, value) with |value| > 1e-12. Entries that vanish exactly
  * (e.g. an odd number of sine factors under the phi integral) come out of the
  * unitary sum as cancellation residue of at most ~1e-15, while every genuine
  * entry up to lmax = 20 is above 9e-7, so the cut only removes residue. When
- * arrays are NULL only the count is returned. max_imag receives the largest
+ * arrays are NULL (or cap is short) only the count is returned. max_imag receives the largest
  * |Im| seen (must be ~0: the real-basis tables are real). */
 long cgo_real_table(int kind, int lmax_in, int lmax_out, int32_t *k1, int32_t *k2, int32_t *k3,
                     double *val, long cap, double *max_imag)
 {
-    long n = 0;
+    init_fact();
+    long counts[ORC_MAXJ + 1];
+    long double worst[ORC_MAXJ + 1];
+    if (lmax_in > ORC_MAXJ) return -1;
+    /* pass 1: entries per l1 block (blocks are independent) */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int l1 = 0; l1 <= lmax_in; ++l1) {
+        worst[l1] = 0.0L;
+        counts[l1] = real_table_block(kind, l1, lmax_in, lmax_out, NULL, NULL, NULL, NULL, 0,
+                                      &worst[l1]);
+    }
+    long total = 0;
+    long start[ORC_MAXJ + 1];
     long double worst_im = 0.0L;
-    for (int l1 = 0; l1 <= lmax_in; ++l1)
-        for (int m1 = -l1; m1 <= l1; ++m1)
-            for (int l2 = 0; l2 <= lmax_in; ++l2)
-                for (int m2 = -l2; m2 <= l2; ++m2)
-                    for (int l3 = abs(l1 - l2); l3 <= imin(l1 + l2, lmax_out); ++l3)
-                        for (int m3 = -l3; m3 <= l3; ++m3) {
-                            int am = abs(m3);
-                            /* only |m3| = |m1|+|m2| or ||m1|-|m2|| can pair with mu1+mu2+mu3=0 */
-                            if (am != abs(m1) + abs(m2) && am != abs(abs(m1) - abs(m2))) continue;
-                            long double im = 0.0L;
-                            long double v = real_entry(kind, l1, m1, l2, m2, l3, m3, &im);
-                            if (fabsl(im) > worst_im) worst_im = fabsl(im);
-                            if (fabsl(v) <= 1e-12L) continue;
-                            if (val && n < cap) {
-                                k1[n] = l1 * l1 + l1 + m1;
-                                k2[n] = l2 * l2 + l2 + m2;
-                                k3[n] = l3 * l3 + l3 + m3;
-                                val[n] = (double)v;
-                            }
-                            ++n;
-                        }
+    for (int l1 = 0; l1 <= lmax_in; ++l1) {
+        start[l1] = total;
+        total += counts[l1];
+        if (worst[l1] > worst_im) worst_im = worst[l1];
+    }
+    /* pass 2: fill each block at its offset, in the same (l1, m1, l2, m2, l3, m3) order */
+    if (val && cap >= total) {
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int l1 = 0; l1 <= lmax_in; ++l1) {
+            long double w = 0.0L;
+            real_table_block(kind, l1, lmax_in, lmax_out, k1, k2, k3, val, start[l1], &w);
+        }
+    }
     if (max_imag) *max_imag = (double)worst_im;
-    return n;
+    return total;
 }
 
 /* Real spherical harmonics of App. C, Eq. realY, in the direction of (x, y, z):
@@ -333,17 +364,17 @@ static int degree_of(int k)
     return l;
 }
 
-/* H[r][k] = sum_n U[l(k)][n][r] X[n][k]  (structured pipeline, Eq. struct-H), X is [C][L^2]. */
-static void channel_contract(int lmax, int C, int R, const double *U, const double *X, double *H)
+/* One CP rank r of Eq. struct-H: H[k] = sum_n U[l(k)][n][r] X[n][k], X is [C][L^2]. */
+static void channel_contract_r(int lmax, int C, int R, int r, const double *U, const double *X,
+                               double *H)
 {
     int L2 = (lmax + 1) * (lmax + 1);
-    for (int r = 0; r < R; ++r)
-        for (int k = 0; k < L2; ++k) {
-            int l = degree_of(k);
-            double s = 0.0;
-            for (int n = 0; n < C; ++n) s += U[((size_t)l * C + n) * R + r] * X[(size_t)n * L2 + k];
-            H[(size_t)r * L2 + k] = s;
-        }
+    for (int k = 0; k < L2; ++k) {
+        int l = degree_of(k);
+        double s = 0.0;
+        for (int n = 0; n < C; ++n) s += U[((size_t)l * C + n) * R + r] * X[(size_t)n * L2 + k];
+        H[k] = s;
+    }
 }
 
 /* out[n][k] = sum_r U[l(k)][n][r] T[r][k]  (structured pipeline, Eq. struct-phi). */
@@ -359,16 +390,10 @@ static void project_out(int lmax, int C, int R, const double *U, const double *T
         }
 }
 
-/* T[r][k3] += sum_entries v * X1[r][k1] * X2[r][k2]  (the explicit sparse sum). */
-static void sparse_couple(const sparse_tab *t, int R, int L2, const double *X1, const double *X2,
-                          double *T)
+/* T[k3] += sum_entries v * X1[k1] * X2[k2]  (the explicit sparse sum, one rank). */
+static void sparse_couple(const sparse_tab *t, const double *X1, const double *X2, double *T)
 {
-    for (int r = 0; r < R; ++r) {
-        const double *a = X1 + (size_t)r * L2;
-        const double *b = X2 + (size_t)r * L2;
-        double *o = T + (size_t)r * L2;
-        for (long e = 0; e < t->n; ++e) o[t->k3[e]] += t->v[e] * a[t->k1[e]] * b[t->k2[e]];
-    }
+    for (long e = 0; e < t->n; ++e) T[t->k3[e]] += t->v[e] * X1[t->k1[e]] * X2[t->k2[e]];
 }
 
 static int set_threads(int nthreads)
@@ -382,9 +407,24 @@ static int set_threads(int nthreads)
 #endif
 }
 
+/* Projection of Ta/Tb [n][R][L^2] to out_even/out_odd [n][C][L^2]. */
+static void project_all(int lmax, int C, int R, long n, const double *U_oe, const double *U_oo,
+                        const double *Ta, const double *Tb, double *out_even, double *out_odd)
+{
+    int L2 = (lmax + 1) * (lmax + 1);
+#pragma omp parallel for schedule(static)
+    for (long i = 0; i < n; ++i) {
+        if (out_even)
+            project_out(lmax, C, R, U_oe, Ta + (size_t)i * R * L2, out_even + (size_t)i * C * L2);
+        if (out_odd)
+            project_out(lmax, C, R, U_oo, Tb + (size_t)i * R * L2, out_odd + (size_t)i * C * L2);
+    }
+}
+
 /* On-site contraction for nodes [0, n_nodes). Arrays (fp64, row-major):
  *   A, B: [N][C][L^2]; U_A, U_B, U_oe, U_oo: [L][C][R];
- *   out_even, out_odd: [N][C][L^2] (either may be NULL to skip that slot). */
+ *   out_even, out_odd: [N][C][L^2] (either may be NULL to skip that slot).
+ * Every (node, rank) pair is independent; they are spread over the threads. */
 int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const double *B,
                const double *U_A, const double *U_B, const double *U_oe, const double *U_oo,
                double *out_even, double *out_odd, int nthreads)
@@ -394,31 +434,32 @@ int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const doub
     int L2 = (lmax + 1) * (lmax + 1);
     sparse_tab G, Q;
     if (build_tab(0, lmax, &G) || build_tab(1, lmax, &Q)) return -2;
+    double *Ta = (double *)calloc((size_t)n_nodes * R * L2 + 1, sizeof(double));
+    double *Tb = (double *)calloc((size_t)n_nodes * R * L2 + 1, sizeof(double));
+    if (!Ta || !Tb) return -2;
     int err = 0;
 #pragma omp parallel
     {
-        double *H1 = (double *)malloc(sizeof(double) * R * L2);
-        double *H2 = (double *)malloc(sizeof(double) * R * L2);
-        double *Ta = (double *)malloc(sizeof(double) * R * L2);
-        double *Tb = (double *)malloc(sizeof(double) * R * L2);
-        if (!H1 || !H2 || !Ta || !Tb) {
+        double *H1 = (double *)malloc(sizeof(double) * L2);
+        double *H2 = (double *)malloc(sizeof(double) * L2);
+        if (!H1 || !H2) {
 #pragma omp atomic write
             err = -2;
         } else {
-#pragma omp for schedule(dynamic, 1)
-            for (long i = 0; i < n_nodes; ++i) {
-                channel_contract(lmax, C, R, U_A, A + (size_t)i * C * L2, H1);
-                channel_contract(lmax, C, R, U_B, B + (size_t)i * C * L2, H2);
-                memset(Ta, 0, sizeof(double) * R * L2);
-                memset(Tb, 0, sizeof(double) * R * L2);
-                if (out_even) sparse_couple(&G, R, L2, H1, H2, Ta);
-                if (out_odd) sparse_couple(&Q, R, L2, H1, H2, Tb);
-                if (out_even) project_out(lmax, C, R, U_oe, Ta, out_even + (size_t)i * C * L2);
-                if (out_odd) project_out(lmax, C, R, U_oo, Tb, out_odd + (size_t)i * C * L2);
+#pragma omp for schedule(dynamic, 4)
+            for (long ir = 0; ir < n_nodes * R; ++ir) {
+                long i = ir / R;
+                int r = (int)(ir % R);
+                channel_contract_r(lmax, C, R, r, U_A, A + (size_t)i * C * L2, H1);
+                channel_contract_r(lmax, C, R, r, U_B, B + (size_t)i * C * L2, H2);
+                if (out_even) sparse_couple(&G, H1, H2, Ta + (size_t)ir * L2);
+                if (out_odd) sparse_couple(&Q, H1, H2, Tb + (size_t)ir * L2);
             }
         }
-        free(H1); free(H2); free(Ta); free(Tb);
+        free(H1); free(H2);
     }
+    if (!err) project_all(lmax, C, R, n_nodes, U_oe, U_oo, Ta, Tb, out_even, out_odd);
+    free(Ta); free(Tb);
     free_tab(&G); free_tab(&Q);
     return err;
 }
@@ -427,7 +468,8 @@ int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const doub
  *   row_ptr: [N+1], col: [E] (sender of edge e), edge_unit: [E][3],
  *   edge_radial: [E][C][L] (R_{n l1}(r_ji)), node_feat: [N][C][L^2],
  *   U_E, U_I, U_oe, U_oo: [L][C][R];
- *   out_even, out_odd: [n_recv][C][L^2] (row q is receiver recv[q]). */
+ *   out_even, out_odd: [n_recv][C][L^2] (row q is receiver recv[q]).
+ * Every (receiver, rank) pair is independent; they are spread over the threads. */
 int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const int32_t *row_ptr,
                      const int32_t *col, const double *edge_unit, const double *edge_radial,
                      const double *node_feat, const double *U_E, const double *U_I,
@@ -435,57 +477,53 @@ int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const i
                      double *out_even, double *out_odd, int nthreads)
 {
     if (lmax < 0 || C < 1 || R < 1 || n_nodes < 0 || n_edges < 0 || n_recv < 0) return -1;
+    for (long q = 0; q < n_recv; ++q)
+        if (recv[q] < 0 || recv[q] >= n_nodes) return -1;
     set_threads(nthreads);
     int L = lmax + 1, L2 = L * L;
     sparse_tab G, Q;
     if (build_tab(0, lmax, &G) || build_tab(1, lmax, &Q)) return -2;
+    double *Ta = (double *)calloc((size_t)n_recv * R * L2 + 1, sizeof(double));
+    double *Tb = (double *)calloc((size_t)n_recv * R * L2 + 1, sizeof(double));
+    if (!Ta || !Tb) return -2;
     int err = 0;
 #pragma omp parallel
     {
-        double *E = (double *)malloc(sizeof(double) * R * L2);
-        double *H = (double *)malloc(sizeof(double) * R * L2);
-        double *Ta = (double *)malloc(sizeof(double) * R * L2);
-        double *Tb = (double *)malloc(sizeof(double) * R * L2);
+        double *E = (double *)malloc(sizeof(double) * L2);
+        double *H = (double *)malloc(sizeof(double) * L2);
         double *Y = (double *)malloc(sizeof(double) * L2);
-        if (!E || !H || !Ta || !Tb || !Y) {
+        if (!E || !H || !Y) {
 #pragma omp atomic write
             err = -2;
         } else {
 #pragma omp for schedule(dynamic, 1)
-            for (long q = 0; q < n_recv; ++q) {
-                long i = (long)recv[q];
-                memset(Ta, 0, sizeof(double) * R * L2);
-                memset(Tb, 0, sizeof(double) * R * L2);
-                if (i < 0 || i >= n_nodes) {
-#pragma omp atomic write
-                    err = -1;
-                    continue;
-                }
+            for (long qr = 0; qr < n_recv * R; ++qr) {
+                long i = (long)recv[qr / R];
+                int r = (int)(qr % R);
                 for (long e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
                     long j = col[e];
                     const double *u = edge_unit + 3 * (size_t)e;
                     cgo_real_sh(lmax, u[0], u[1], u[2], Y);
                     const double *rad = edge_radial + (size_t)e * C * L;
                     /* Eq. msgpass-tildeR, then multiply by Y_{l1 m1}(rhat) */
-                    for (int r = 0; r < R; ++r)
-                        for (int l1 = 0; l1 < L; ++l1) {
-                            double s = 0.0;
-                            for (int n = 0; n < C; ++n)
-                                s += U_E[((size_t)l1 * C + n) * R + r] * rad[(size_t)n * L + l1];
-                            for (int m1 = -l1; m1 <= l1; ++m1)
-                                E[(size_t)r * L2 + l1 * l1 + l1 + m1] = s * Y[l1 * l1 + l1 + m1];
-                        }
+                    for (int l1 = 0; l1 < L; ++l1) {
+                        double s = 0.0;
+                        for (int n = 0; n < C; ++n)
+                            s += U_E[((size_t)l1 * C + n) * R + r] * rad[(size_t)n * L + l1];
+                        for (int m1 = -l1; m1 <= l1; ++m1)
+                            E[l1 * l1 + l1 + m1] = s * Y[l1 * l1 + l1 + m1];
+                    }
                     /* Eq. msgpass-HI */
-                    channel_contract(lmax, C, R, U_I, node_feat + (size_t)j * C * L2, H);
-                    if (out_even) sparse_couple(&G, R, L2, E, H, Ta);
-                    if (out_odd) sparse_couple(&Q, R, L2, E, H, Tb);
+                    channel_contract_r(lmax, C, R, r, U_I, node_feat + (size_t)j * C * L2, H);
+                    if (out_even) sparse_couple(&G, E, H, Ta + (size_t)qr * L2);
+                    if (out_odd) sparse_couple(&Q, E, H, Tb + (size_t)qr * L2);
                 }
-                if (out_even) project_out(lmax, C, R, U_oe, Ta, out_even + (size_t)q * C * L2);
-                if (out_odd) project_out(lmax, C, R, U_oo, Tb, out_odd + (size_t)q * C * L2);
             }
         }
-        free(E); free(H); free(Ta); free(Tb); free(Y);
+        free(E); free(H); free(Y);
     }
+    if (!err) project_all(lmax, C, R, n_recv, U_oe, U_oo, Ta, Tb, out_even, out_odd);
+    free(Ta); free(Tb);
     free_tab(&G); free_tab(&Q);
     return err;
 }

@@ -1,0 +1,239 @@
+"""Python binding of libcgtp (contracted Clebsch-Gordan products on MI355X).
+
+Thin ctypes marshalling over the C ABI declared in ``include/cgtp.h``: every
+step of the computation runs in the HIP kernels of ``libcgtp.so``. Tensors are
+torch device tensors (torch provides device memory and streams only). If the
+shared library is missing this module raises on first use; there is no CPU
+fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcgtp.so")
+
+CGTP_OK = 0
+CGTP_ERR_ARG = -1
+CGTP_ERR_WORKSPACE = -2
+CGTP_ERR_CSR = -3
+CGTP_ERR_HIP = -4
+CGTP_ERR_UNSUPPORTED = -5
+CGTP_F32 = 0
+CGTP_F64 = 1
+CGTP_VALIDATE_CSR = 1
+CGTP_EDGE_SEPARATED = 2
+CGTP_OP_ONSITE = 0
+CGTP_OP_MESSAGE_PASS = 1
+CGTP_MAX_LMAX = 24
+
+EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
+            "cgtp_message_pass", "cgtp_destroy", "cgtp_status_string", "cgtp_last_error",
+            "cgtp_host_tables")
+
+
+class CgtpError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [("lmax", ctypes.c_int), ("channels", ctypes.c_int), ("rank", ctypes.c_int),
+                ("n_theta", ctypes.c_int), ("n_phi", ctypes.c_int), ("dtype", ctypes.c_int),
+                ("flags", ctypes.c_uint)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libcgtp.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libcgtp.so not found at {path}: build it with "
+                           "`python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+    lib.cgtp_plan_create.argtypes = [ctypes.POINTER(_Desc), ctypes.POINTER(vp)]
+    lib.cgtp_plan_grid.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.cgtp_workspace_bytes.argtypes = [vp, i32, i64, i64, ctypes.POINTER(sz)]
+    lib.cgtp_onsite.argtypes = [vp, i64] + [vp] * 8 + [vp, sz, vp]
+    lib.cgtp_message_pass.argtypes = [vp, i64, i64] + [vp] * 11 + [vp, sz, vp]
+    lib.cgtp_destroy.argtypes = [vp]
+    lib.cgtp_status_string.argtypes = [i32]
+    lib.cgtp_status_string.restype = ctypes.c_char_p
+    lib.cgtp_last_error.argtypes = []
+    lib.cgtp_last_error.restype = ctypes.c_char_p
+    lib.cgtp_host_tables.argtypes = [i32, i32, i32] + [vp] * 5
+    for name in ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
+                 "cgtp_message_pass", "cgtp_destroy", "cgtp_host_tables"):
+        getattr(lib, name).restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != CGTP_OK:
+        lib = load_library()
+        detail = lib.cgtp_last_error().decode() or lib.cgtp_status_string(status).decode()
+        raise CgtpError(status, where, detail)
+
+
+class Plan:
+    """Owns a cgtp_plan handle (grid tables on the current device)."""
+
+    def __init__(self, lmax: int, channels: int, rank: int, n_theta: int = 0, n_phi: int = 0,
+                 dtype: str = "f32", flags: int = 0):
+        lib = load_library()
+        self.lmax, self.channels, self.rank = lmax, channels, rank
+        self.dtype = dtype
+        desc = _Desc(lmax, channels, rank, n_theta, n_phi,
+                     CGTP_F64 if dtype == "f64" else CGTP_F32, flags)
+        h = ctypes.c_void_p()
+        _check(lib.cgtp_plan_create(ctypes.byref(desc), ctypes.byref(h)), "cgtp_plan_create")
+        self.handle = h
+        u, v = ctypes.c_int(), ctypes.c_int()
+        _check(lib.cgtp_plan_grid(h, ctypes.byref(u), ctypes.byref(v)), "cgtp_plan_grid")
+        self.n_theta, self.n_phi = u.value, v.value
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _check(load_library().cgtp_destroy(self.handle), "cgtp_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def plan_create(lmax: int, channels: int, rank: int, n_theta: int = 0, n_phi: int = 0,
+                dtype: str = "f32", flags: int = 0) -> Plan:
+    return Plan(lmax, channels, rank, n_theta, n_phi, dtype, flags)
+
+
+def destroy(plan: Plan) -> None:
+    plan.close()
+
+
+def workspace_bytes(plan: Plan, op: int, n_nodes: int, n_edges: int = 0) -> int:
+    out = ctypes.c_size_t()
+    _check(load_library().cgtp_workspace_bytes(plan.handle, op, n_nodes, n_edges,
+                                               ctypes.byref(out)), "cgtp_workspace_bytes")
+    return out.value
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _want(plan: Plan, name: str, t, shape, dtype=None):
+    torch = _torch()
+    dt = dtype or (torch.float64 if plan.dtype == "f64" else torch.float32)
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda or t.dtype != dt or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected contiguous {dt} device tensor of shape {tuple(shape)}, "
+                         f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def onsite(plan: Plan, A, B, U_A, U_B, U_out_even, U_out_odd, out_even=None, out_odd=None,
+           workspace=None, stream=None):
+    """cgtp_onsite. A, B [N, C, K]; U_* [L, C, R]; outputs [N, C, K] (allocated if not given
+    and not explicitly skipped with out_even=False / out_odd=False)."""
+    torch = _torch()
+    N, C, K = A.shape
+    L = plan.lmax + 1
+    _want(plan, "A", A, (N, plan.channels, L * L))
+    _want(plan, "B", B, A.shape)
+    for nm, U in (("U_A", U_A), ("U_B", U_B)):
+        _want(plan, nm, U, (L, plan.channels, plan.rank))
+    outs = []
+    for nm, o, U in (("out_even", out_even, U_out_even), ("out_odd", out_odd, U_out_odd)):
+        if o is False:
+            outs.append(None)
+            continue
+        _want(plan, nm.replace("out", "U_out"), U, (L, plan.channels, plan.rank))
+        if o is None:
+            o = torch.empty_like(A)
+        _want(plan, nm, o, A.shape)
+        outs.append(o)
+    ws_ptr, ws_len = None, 0
+    if workspace is not None:
+        ws_ptr, ws_len = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(load_library().cgtp_onsite(plan.handle, N, _ptr(A), _ptr(B), _ptr(U_A), _ptr(U_B),
+                                      _ptr(U_out_even), _ptr(U_out_odd), _ptr(outs[0]),
+                                      _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)),
+           "cgtp_onsite")
+    return outs[0], outs[1]
+
+
+def message_pass(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
+                 U_out_even, U_out_odd, out_even=None, out_odd=None, workspace=None,
+                 stream=None):
+    """cgtp_message_pass. row_ptr [N+1], col [E] int32; edge_unit [E, 3];
+    edge_radial [E, C, L]; node_feat [N, C, K]; U_* [L, C, R]; outputs [N, C, K]."""
+    torch = _torch()
+    N = node_feat.shape[0]
+    E = col.shape[0]
+    L = plan.lmax + 1
+    _want(plan, "row_ptr", row_ptr, (N + 1,), torch.int32)
+    _want(plan, "col", col, (E,), torch.int32)
+    _want(plan, "edge_unit", edge_unit, (E, 3))
+    _want(plan, "edge_radial", edge_radial, (E, plan.channels, L))
+    _want(plan, "node_feat", node_feat, (N, plan.channels, L * L))
+    for nm, U in (("U_E", U_E), ("U_I", U_I)):
+        _want(plan, nm, U, (L, plan.channels, plan.rank))
+    outs = []
+    for nm, o, U in (("out_even", out_even, U_out_even), ("out_odd", out_odd, U_out_odd)):
+        if o is False:
+            outs.append(None)
+            continue
+        _want(plan, nm.replace("out", "U_out"), U, (L, plan.channels, plan.rank))
+        if o is None:
+            o = torch.empty_like(node_feat)
+        _want(plan, nm, o, node_feat.shape)
+        outs.append(o)
+    ws_ptr, ws_len = None, 0
+    if workspace is not None:
+        ws_ptr, ws_len = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(load_library().cgtp_message_pass(
+        plan.handle, N, E, _ptr(row_ptr), _ptr(col), _ptr(edge_unit), _ptr(edge_radial),
+        _ptr(node_feat), _ptr(U_E), _ptr(U_I), _ptr(U_out_even), _ptr(U_out_odd), _ptr(outs[0]),
+        _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)), "cgtp_message_pass")
+    return outs[0], outs[1]
+
+
+def host_tables(lmax: int, n_theta: int = 0, n_phi: int = 0):
+    """fp64 grid tables (x, w, p, dp, q) as the plan builds them; host only."""
+    import numpy as np
+
+    lib = load_library()
+    u, v = n_theta, n_phi
+    if u == 0:
+        u = (3 * lmax + 3) // 2
+    if v == 0:
+        v = 3 * lmax + 1
+    P = (lmax + 1) * (lmax + 2) // 2
+    x, w = np.zeros(u), np.zeros(u)
+    p, dp = np.zeros((u, P)), np.zeros((u, P))
+    q = np.zeros((v, 2 * lmax + 1))
+    args = [ctypes.c_void_p(a.ctypes.data) for a in (x, w, p, dp, q)]
+    _check(lib.cgtp_host_tables(lmax, n_theta, n_phi, *args), "cgtp_host_tables")
+    return x, w, p, dp, q

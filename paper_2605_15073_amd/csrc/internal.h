@@ -1,0 +1,87 @@
+// Internal declarations shared by the host plan code and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "cgtp.h"
+
+namespace cgtp {
+
+// Grid sizes derived from lmax and the (possibly overridden) grid.
+struct Dims {
+    int lmax;  // band limit
+    int L;     // lmax + 1
+    int K;     // (lmax + 1)^2 flattened SH coefficients
+    int M;     // 2 lmax + 1 azimuthal orders
+    int P;     // (lmax + 1)(lmax + 2)/2 Legendre (l, m >= 0) pairs
+    int U;     // Gauss-Legendre nodes in x = cos(theta)
+    int V;     // equispaced phi nodes
+    int UV;    // U * V grid points
+};
+
+bool resolve_grid(int lmax, int n_theta, int n_phi, int *U, int *V);
+Dims make_dims(int lmax, int U, int V);
+
+// fp64 host tables (see cgtp_host_tables in cgtp.h for the layouts).
+void gauss_legendre(int n, double *x, double *w);
+void legendre_tables(int lmax, int U, const double *x, double *p, double *dp);
+void fourier_table(int lmax, int V, double *q);
+
+// Device tables, all in the plan's scalar type T, one allocation per plan.
+template <typename T>
+struct Tabs {
+    const T *x;     // [U] cos(theta_u)
+    const T *sx;    // [U] sin(theta_u)
+    const T *xsx;   // [U] cos/sin, for d(rhat.Omega)/dx
+    const T *wq;    // [U] w_u * 2 pi / V (quadrature weight of a grid point)
+    const T *p;     // [U][P] Pt_l^m(x_u)
+    const T *dp;    // [U][P] dPt_l^m/dx(x_u)
+    const T *q;     // [V][M] real Fourier factor q_vm, column m + lmax
+    const T *cphi;  // [V] cos(phi_v)
+    const T *sphi;  // [V] sin(phi_v)
+    const T *cl;    // [L] (2l+1)/(4 pi): addition theorem weight
+    const T *rc1;   // [L] (2l-1)/l  Legendre recurrence, l >= 1
+    const T *rc2;   // [L] (l-1)/l
+    const T *ya;    // [P] normalised-Legendre recurrence factor a_lm (edge SH)
+    const T *yb;    // [P] normalised-Legendre recurrence factor b_lm (edge SH)
+    const T *ymm;   // [L] sqrt((2m+1)/(2m)) diagonal step (edge SH), ymm[0] = 1/sqrt(4 pi)
+    Dims d;
+};
+
+// Number of T elements of each table region, in the order of Tabs.
+size_t table_elems(const Dims &d);
+void fill_tables(const Dims &d, double *host);  // host fp64 image, table_elems(d) long
+template <typename T>
+Tabs<T> bind_tables(const Dims &d, const void *dev);
+
+// Generic per-degree channel contraction (Eq. struct-H / struct-phi / msgpass-tildeR):
+//   Y[b][o][k] = scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so] * X[b][i][k]
+// l(k) = k when kdeg, else the degree of the flattened index k. scale may be null.
+template <typename T>
+hipError_t launch_contract(int64_t B, int Cin, int Cout, int K, bool kdeg, const T *W,
+                           int64_t w_sl, int64_t w_si, int64_t w_so, const T *X, T *Y,
+                           const T *scale, hipStream_t s);
+
+// Node-side synthesis of the three grid fields (A, dA/dx, dA/dphi) of H[b][r][K]:
+// SF[b][r][3][UV] (Eqs. struct-F, struct-tildeA plus the derivative passes).
+template <typename T>
+hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H, T *SF,
+                                hipStream_t s);
+
+// On-site grid product and surface curl followed by the inverse transforms:
+// Ta/Tb[b][r][K] from HA/HB[b][r][K].
+template <typename T>
+hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, const T *HB,
+                              T *Ta, T *Tb, hipStream_t s);
+
+// Message-passing receiver pass: per receiver, synthesise the edge fields, multiply
+// with the streamed sender fields, sum over the CSR row, then the inverse transforms.
+template <typename T>
+hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
+                           const int32_t *row_ptr, const int32_t *col, const T *unit,
+                           const T *Rt, const T *SF, T *Ta, T *Tb, hipStream_t s);
+
+}  // namespace cgtp

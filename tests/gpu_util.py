@@ -1,0 +1,41 @@
+"""Helpers for the GPU parity tests: move seeded inputs to the device, call the
+library through its binding, compare with the oracle per output slot."""
+from __future__ import annotations
+
+import numpy as np
+
+ONSITE_KEYS = ("A", "B", "U_A", "U_B", "U_out_even", "U_out_odd")
+MP_KEYS = ("row_ptr", "col", "edge_unit", "edge_radial", "node_feat", "U_E", "U_I",
+           "U_out_even", "U_out_odd")
+
+TOL_F32 = 2e-5      # max|gpu - ref| / max|ref| per output slot (fp32 path)
+TOL_F64 = 1e-11     # fp64 path of the same kernels
+
+
+def to_dev(d, keys, dtype="f32"):
+    import torch
+
+    out = {}
+    for k in keys:
+        a = d[k]
+        if a.dtype == np.int32:
+            out[k] = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+        else:
+            out[k] = torch.from_numpy(np.ascontiguousarray(
+                a.astype(np.float64 if dtype == "f64" else np.float32))).cuda()
+    return out
+
+
+def rel_err(gpu, ref, scale=None):
+    g = gpu.detach().cpu().numpy() if hasattr(gpu, "detach") else np.asarray(gpu)
+    s = np.abs(ref).max() if scale is None else scale
+    return float(np.abs(g.astype(np.float64) - ref).max() / max(s, 1e-300))
+
+
+def run_onsite(cg, plan, t, **kw):
+    return cg.onsite(plan, t["A"], t["B"], t["U_A"], t["U_B"], t["U_out_even"], t["U_out_odd"],
+                     **kw)
+
+
+def run_mp(cg, plan, t, **kw):
+    return cg.message_pass(plan, *(t[k] for k in MP_KEYS), **kw)
