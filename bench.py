@@ -1,0 +1,276 @@
+#!/usr/bin/env python
+"""Benchmark of the contracted Clebsch-Gordan products on one MI355X.
+
+A step is one call of the library on one batch of synthetic input. The default
+workload is message passing on 10,000 atoms (periodic box at 0.1 atoms/A^3,
+5 A cutoff, about 525k directed edges), lmax = 6, C = R = 128, fp32. One
+cgtp_message_pass call runs every stage of the method: node-side channel
+contraction and grid synthesis (A, dA/dx, dA/dphi), edge-radial contraction,
+the receiver pass (edge-field synthesis, grid product and surface curl summed
+over neighbours, quadrature analysis) and both output projections.
+
+Prints ONE JSON line: throughput in nodes*channels/s (receivers x C per second),
+the per-stage GPU times measured with HIP events on the library's stream over
+the timed steps, the roofline of the dominant kernel, and the fp64 CPU oracle
+timed on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+  python bench.py --sweep-out FILE     # lmax sweeps, one JSON line per point in FILE
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector (and matrix) peak
+CSRC = os.path.join(ROOT, "paper_2605_15073_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_sha() -> str:
+    """Hash of the library sources: traffic counters are only valid for this version."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def grid_dims(lmax: int):
+    U = (3 * lmax + 3) // 2
+    V = 3 * lmax + 1
+    return U, V
+
+
+# ---------------------------------------------------------------- algorithmic work
+
+def receiver_bytes(lmax: int, R: int, N: int, E: int) -> int:
+    """HBM bytes the receiver pass must move (fp32): per edge the three sender grid
+    fields (3 R UV), the edge radial coefficients (R L), the unit vector and the
+    sender index; per receiver the row pointer and the two analysed fields (2 R K)."""
+    U, V = grid_dims(lmax)
+    L, K = lmax + 1, (lmax + 1) ** 2
+    per_edge = 4 * (3 * R * U * V + R * L + 3 + 1)
+    per_recv = 4 * (1 + 2 * R * K)
+    return E * per_edge + N * per_recv
+
+
+def onsite_grid_flops(lmax: int, R: int, N: int) -> int:
+    """fp32 flops of the on-site grid stage with the paper's dense transforms, per
+    (node, rank): Legendre synthesis of F and dF/dx for both operands (8 U L^2),
+    Fourier synthesis of 3 fields per operand (12 U V M), product and curl (4 U V),
+    Fourier analysis of 2 fields (4 U V M), Gauss-Legendre analysis (4 U L^2)."""
+    U, V = grid_dims(lmax)
+    L, M = lmax + 1, 2 * lmax + 1
+    per = 12 * U * L * L + 16 * U * V * M + 4 * U * V
+    return N * R * per
+
+
+# ---------------------------------------------------------------- helpers
+
+def to_dev(d, keys):
+    import numpy as np
+    import torch
+
+    out = {}
+    for k in keys:
+        a = d[k]
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        out[k] = t.cuda()
+    return out
+
+
+MP_KEYS = ("row_ptr", "col", "edge_unit", "edge_radial", "node_feat", "U_E", "U_I",
+           "U_out_even", "U_out_odd")
+ONSITE_KEYS = ("A", "B", "U_A", "U_B", "U_out_even", "U_out_odd")
+
+
+def load_traffic(workload: str):
+    path = os.path.join(PROFILES, f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_sha") != kernel_sha():
+        return None                      # counters were taken on another kernel version
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(w, d, budget_s: float = 15.0):
+    """Time the fp64 oracle on a bounded sample of the same workload."""
+    import numpy as np
+
+    import oracle
+
+    cores = oracle.max_threads()
+    if w.kind == "mp":
+        def run(n):
+            return oracle.message_pass(w.lmax, *(d[k] for k in MP_KEYS),
+                                       receivers=np.arange(n))
+        unit_name = "receivers"
+    else:
+        def run(n):
+            return oracle.onsite(w.lmax, d["A"][:n], d["B"][:n], d["U_A"], d["U_B"],
+                                 d["U_out_even"], d["U_out_odd"])
+        unit_name = "nodes"
+    probe = min(w.n, 16)
+    t0 = time.perf_counter()
+    run(probe)
+    tp = time.perf_counter() - t0
+    n = int(min(w.n, max(probe, probe * budget_s / max(tp, 1e-6))))
+    t0 = time.perf_counter()
+    run(n)
+    t = time.perf_counter() - t0
+    return {"value": n * w.C / t, "unit": "nodes*channels/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n} {unit_name} (of {w.n}) of the same workload, fp64, "
+                      f"{t:.1f} s on {cores} OpenMP threads"}
+
+
+# ---------------------------------------------------------------- one workload
+
+def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=False):
+    import torch
+
+    import paper_2605_15073_amd as cg
+
+    if d is None:
+        d = w.make()
+    plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
+    if w.kind == "mp":
+        t = to_dev(d, MP_KEYS)
+        E = int(d["n_edges"])
+        op = cg.CGTP_OP_MESSAGE_PASS
+        ws = torch.empty(cg.workspace_bytes(plan, op, w.n, E), dtype=torch.uint8, device="cuda")
+        oe = torch.empty_like(t["node_feat"])
+        oo = torch.empty_like(t["node_feat"])
+
+        def step():
+            cg.message_pass(plan, *(t[k] for k in MP_KEYS), out_even=oe, out_odd=oo, workspace=ws)
+    else:
+        t = to_dev(d, ONSITE_KEYS)
+        if w.self_coupled:
+            t["B"] = t["A"]
+        E = 0
+        op = cg.CGTP_OP_ONSITE
+        ws = torch.empty(cg.workspace_bytes(plan, op, w.n), dtype=torch.uint8, device="cuda")
+        oe = torch.empty_like(t["A"])
+        oo = torch.empty_like(t["A"])
+
+        def step():
+            cg.onsite(plan, t["A"], t["B"], t["U_A"], t["U_B"], t["U_out_even"], t["U_out_odd"],
+                      out_even=oe, out_odd=oo, workspace=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    cg.stage_times(plan, op)                     # drop the warm-up events
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    stages, calls = cg.stage_times(plan, op)
+    assert calls == steps, (calls, steps)
+    ms_step = 1e3 * wall / steps
+    stage_avg = {k: v / steps for k, v in stages.items()}
+    dom = max(stage_avg, key=stage_avg.get)
+    U, V = grid_dims(w.lmax)
+    rec = {
+        "metric": "contracted CG products/sec (nodes*channels/s)",
+        "value": w.n * w.C / (ms_step / 1e3),
+        "unit": "nodes*channels/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "kind": "message_passing" if w.kind == "mp" else "onsite",
+                   "nodes": w.n, "edges": E, "lmax": w.lmax, "channels": w.C, "rank": w.R,
+                   "grid": f"{U}x{V}", "seed": w.seed},
+        "stages_ms": {k: round(v, 4) for k, v in stage_avg.items()},
+        "dominant_kernel": dom,
+    }
+    t_dom = stage_avg[dom] / 1e3
+    if w.kind == "mp" and dom == "receiver":
+        alg = receiver_bytes(w.lmax, w.R, w.n, E)
+        traffic = load_traffic(w.name)
+        rec["roofline"] = {"bound": "hbm", "achieved": alg / t_dom / 1e9, "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "frac": alg / t_dom / 1e9 / HBM_PEAK_GBS,
+                           "traffic": traffic, "algorithmic_bytes": alg}
+    elif w.kind == "onsite" and dom == "grid_product_curl_analysis":
+        fl = onsite_grid_flops(w.lmax, w.R, w.n)
+        rec["roofline"] = {"bound": "alu", "achieved": fl / t_dom / 1e12,
+                           "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                           "frac": fl / t_dom / 1e12 / FP32_PEAK_TFLOPS,
+                           "traffic": load_traffic(w.name), "algorithmic_flops": fl}
+    else:
+        rec["roofline"] = None
+    rec["cpu_baseline"] = cpu_baseline(w, d) if with_cpu else None
+    plan.close()
+    return rec
+
+
+def sweep(path: str, steps: int, warmup: int):
+    from paper_2605_15073_amd.inputs import Workload
+
+    pts = []
+    for lmax in range(2, 21, 2):
+        pts.append(Workload(f"onsite_n4096_l{lmax}_c128", "onsite", 4096, lmax, 128, 128,
+                            seed=3, per_degree=True))
+        pts.append(Workload(f"onsite_n1000_l{lmax}_c64", "onsite", 1000, lmax, 64, 64, seed=3,
+                            per_degree=True))
+    for lmax in range(2, 21, 2):
+        pts.append(Workload(f"mp_1000_l{lmax}_c64", "mp", 1000, lmax, 64, 64, seed=4))
+        pts.append(Workload(f"mp_5k_l{lmax}_c64", "mp", 5000, lmax, 64, 64, seed=4))
+    with open(path, "w") as f:
+        for w in pts:
+            rec = bench_workload(w, steps, warmup, with_cpu=False)
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            print(f"sweep {w.name}: {rec['ms_per_step']:.3f} ms/step "
+                  f"dominant {rec['dominant_kernel']}", flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mp_10k_l6_c128")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep-out", default=None)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the method is "
+                                   "measured on one MI355X (--gpus 1)"}), flush=True)
+        sys.exit(2)
+    import torch
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}), flush=True)
+        sys.exit(1)
+    from paper_2605_15073_amd.inputs import WORKLOADS
+
+    if args.sweep_out:
+        sweep(args.sweep_out, max(3, args.steps // 4), args.warmup)
+        return
+    w = WORKLOADS[args.workload]
+    rec = bench_workload(w, args.steps, args.warmup, with_cpu=not args.no_cpu_baseline)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -74,6 +74,8 @@ extern "C" {
 #define CGTP_EDGE_SEPARATED 2u /* edge field by separated Legendre+Fourier synthesis
                                   (Eqs. msgpass-FE, msgpass-AE) instead of the zonal
                                   addition-theorem form; same values, more work */
+#define CGTP_TIME_STAGES 4u    /* record HIP events between the kernel stages of every call
+                                  (read with cgtp_stage_times) */
 
 /* operations for cgtp_workspace_bytes */
 #define CGTP_OP_ONSITE 0
@@ -91,7 +93,7 @@ typedef struct {
     int n_phi;      /* equispaced phi nodes phi_v = 2 pi v / n_phi; 0 => 3 lmax + 1; otherwise
                        must be >= 3 lmax + 1 */
     int dtype;      /* CGTP_F32 or CGTP_F64 */
-    unsigned flags; /* CGTP_VALIDATE_CSR | CGTP_EDGE_SEPARATED */
+    unsigned flags; /* CGTP_VALIDATE_CSR | CGTP_EDGE_SEPARATED | CGTP_TIME_STAGES */
 } cgtp_desc;
 
 /* Create a plan: validates the descriptor, builds the grid tables on the host in
@@ -152,6 +154,19 @@ int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                       const void *U_I, const void *U_out_even, const void *U_out_odd,
                       void *out_even, void *out_odd, void *workspace, size_t ws_bytes,
                       void *stream);
+
+/* Per-stage GPU time of the calls made since the previous cgtp_stage_times on
+ * this plan (plan created with CGTP_TIME_STAGES), in the spirit of the paper's
+ * per-step breakdown (App. D, Table 4). Waits for the recorded events, writes the
+ * summed milliseconds of each stage of `op` to ms[0 .. *n_stages) (at most cap
+ * entries) and the number of calls to *n_calls, then resets the accumulation.
+ * Stages of CGTP_OP_ONSITE: 0 contract A, 1 contract B, 2 grid product+curl and
+ * analysis, 3 project even, 4 project odd. Stages of CGTP_OP_MESSAGE_PASS:
+ * 0 contract node features, 1 sender grid fields, 2 contract edge radial,
+ * 3 receiver pass (edge synthesis, products, neighbour sum, analysis),
+ * 4 project even, 5 project odd. A skipped stage counts as 0.
+ * Errors: CGTP_ERR_ARG (NULL, flag not set, unknown op), CGTP_ERR_HIP. */
+int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages, int *n_calls);
 
 /* Release the plan and everything it owns. Synchronises the device first.
  * cgtp_destroy(NULL) is a no-op. */

@@ -24,13 +24,18 @@ CGTP_F32 = 0
 CGTP_F64 = 1
 CGTP_VALIDATE_CSR = 1
 CGTP_EDGE_SEPARATED = 2
+CGTP_TIME_STAGES = 4
 CGTP_OP_ONSITE = 0
 CGTP_OP_MESSAGE_PASS = 1
 CGTP_MAX_LMAX = 24
 
 EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
-            "cgtp_message_pass", "cgtp_destroy", "cgtp_status_string", "cgtp_last_error",
-            "cgtp_host_tables")
+            "cgtp_message_pass", "cgtp_stage_times", "cgtp_destroy", "cgtp_status_string",
+            "cgtp_last_error", "cgtp_host_tables")
+ONSITE_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis", "project_even",
+                 "project_odd")
+MP_STAGES = ("contract_node", "sender_fields", "contract_edge_radial", "receiver",
+             "project_even", "project_odd")
 
 
 class CgtpError(RuntimeError):
@@ -63,6 +68,8 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_workspace_bytes.argtypes = [vp, i32, i64, i64, ctypes.POINTER(sz)]
     lib.cgtp_onsite.argtypes = [vp, i64] + [vp] * 8 + [vp, sz, vp]
     lib.cgtp_message_pass.argtypes = [vp, i64, i64] + [vp] * 11 + [vp, sz, vp]
+    lib.cgtp_stage_times.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double), i32,
+                                     ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.cgtp_destroy.argtypes = [vp]
     lib.cgtp_status_string.argtypes = [i32]
     lib.cgtp_status_string.restype = ctypes.c_char_p
@@ -70,7 +77,7 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_last_error.restype = ctypes.c_char_p
     lib.cgtp_host_tables.argtypes = [i32, i32, i32] + [vp] * 5
     for name in ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
-                 "cgtp_message_pass", "cgtp_destroy", "cgtp_host_tables"):
+                 "cgtp_message_pass", "cgtp_stage_times", "cgtp_destroy", "cgtp_host_tables"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib
@@ -126,6 +133,16 @@ def workspace_bytes(plan: Plan, op: int, n_nodes: int, n_edges: int = 0) -> int:
     _check(load_library().cgtp_workspace_bytes(plan.handle, op, n_nodes, n_edges,
                                                ctypes.byref(out)), "cgtp_workspace_bytes")
     return out.value
+
+
+def stage_times(plan: Plan, op: int):
+    """cgtp_stage_times: ({stage name: summed ms}, number of calls) since the last query."""
+    ms = (ctypes.c_double * 8)()
+    ns, nc = ctypes.c_int(), ctypes.c_int()
+    _check(load_library().cgtp_stage_times(plan.handle, op, ms, 8, ctypes.byref(ns),
+                                           ctypes.byref(nc)), "cgtp_stage_times")
+    names = ONSITE_STAGES if op == CGTP_OP_ONSITE else MP_STAGES
+    return {names[i]: ms[i] for i in range(ns.value)}, nc.value
 
 
 def _torch():

@@ -1,0 +1,189 @@
+// Per-degree channel contraction (Eqs. struct-H, msgpass-HI, msgpass-tildeR and
+// the lambda projection struct-phi / cat-alpha-phi / cat-beta-phi):
+//
+//   Y[b][o][k] = scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so] * X[b][i][k]
+//
+// For a fixed degree l this is a GEMM Y_l[o][c] = sum_i W_l[i][o] X_l[i][c] over
+// the columns c = (b, m), m = 0..2l (or c = b when k is the degree itself).
+//
+// fp32 path: MFMA tiles (v_mfma_f32_16x16x4f32). A block owns 64 output rows
+// and 64 columns of one degree of a group of 64 nodes; the blocks of a group run
+// back to back over all degrees, so the group's input lines are reused from L2.
+// A group of 64 nodes has 64(2l+1) columns of degree l, a whole number of 64-wide
+// tiles, so no tile straddles two degrees and only the last group has a ragged edge.
+// fp64 path: one thread per output (verification build).
+#include "internal.h"
+
+namespace cgtp {
+
+namespace {
+
+constexpr int kTile = 64;      // output rows (o) and columns (c) per block
+constexpr int kChunk = 16;     // reduction (i) slice staged in LDS per step
+constexpr int kThreadsC = 256; // 4 waves, each a 32 x 32 sub-tile (2 x 2 MFMA 16 x 16)
+
+__device__ __forceinline__ int isqrt_small(int t)
+{
+    int l = (int)sqrtf((float)t);
+    while (l * l > t) --l;
+    while ((l + 1) * (l + 1) <= t) ++l;
+    return l;
+}
+
+typedef float float4_t __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
+    int64_t B, int Cin, int Cout, int K, int kdeg, int tiles_per_group, int otiles,
+    const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
+    const float *__restrict__ X, float *__restrict__ Y, const float *__restrict__ scale)
+{
+    __shared__ float As[kChunk][kTile + 4];  // As[i][o] = W_l[i0 + i][o0 + o]
+    __shared__ float Bs[kChunk][kTile + 4];  // Bs[i][c] = X_l[i0 + i][c0 + c]
+
+    const int64_t bid = blockIdx.x;
+    const int ot = (int)(bid % otiles);
+    const int64_t rest = bid / otiles;
+    const int t = (int)(rest % tiles_per_group);
+    const int64_t g = rest / tiles_per_group;
+    int l, sub, width, kofs;
+    if (kdeg) {
+        l = t;
+        sub = 0;
+        width = 1;
+        kofs = t;
+    } else {
+        l = isqrt_small(t);
+        sub = t - l * l;
+        width = 2 * l + 1;
+        kofs = l * l;
+    }
+    const int64_t b0 = g * kTile;                      // first node of the group
+    const int64_t nb = (B - b0 < kTile) ? (B - b0) : kTile;
+    const int ncols = (int)nb * width;                 // columns of degree l in this group
+    const int c0 = sub * kTile;
+    const int o0 = ot * kTile;
+    const float *Wl = W + l * w_sl;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int osub = (wave >> 1) * 32;
+    const int csub = (wave & 1) * 32;
+
+    float4_t acc[2][2];
+    for (int a = 0; a < 2; ++a)
+        for (int b = 0; b < 2; ++b) acc[a][b] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+    // this thread's column for the B-tile loads (fixed over the reduction)
+    const int lc = tid & (kTile - 1);
+    const int li = tid >> 6;  // 0..3, rows li, li+4, li+8, li+12 of the chunk
+    const int cg = c0 + lc;
+    const bool c_ok = cg < ncols;
+    const int bl = c_ok ? cg / width : 0;
+    const int mm = c_ok ? cg - bl * width : 0;
+    const float *xcol = X + (b0 + bl) * (int64_t)Cin * K + kofs + mm;
+
+    for (int i0 = 0; i0 < Cin; i0 += kChunk) {
+        // stage W_l[i0 .. i0+16)[o0 .. o0+64) and X_l[i0 .. i0+16)[c0 .. c0+64)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            int i = li + 4 * r;
+            int ig = i0 + i;
+            int og = o0 + lc;
+            As[i][lc] = (ig < Cin && og < Cout) ? Wl[ig * w_si + og * w_so] : 0.f;
+            Bs[i][lc] = (ig < Cin && c_ok) ? xcol[(int64_t)ig * K] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < kChunk; kk += 4) {
+            const int ki = kk + (lane >> 4);
+            float a0 = As[ki][osub + (lane & 15)];
+            float a1 = As[ki][osub + 16 + (lane & 15)];
+            float b0v = Bs[ki][csub + (lane & 15)];
+            float b1v = Bs[ki][csub + 16 + (lane & 15)];
+            acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0v, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1v, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0v, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1v, acc[1][1], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+
+    const float s = scale ? scale[l] : 1.f;
+    // D[row][col] of a 16 x 16 tile: lane holds rows 4*(lane/16) + j, column lane % 16
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb) {
+            int c = c0 + csub + 16 * bb + (lane & 15);
+            if (c >= ncols) continue;
+            int bcol = c / width;
+            int m = c - bcol * width;
+            float *ycol = Y + (b0 + bcol) * (int64_t)Cout * K + kofs + m;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                int o = o0 + osub + 16 * a + 4 * (lane >> 4) + j;
+                if (o < Cout) ycol[(int64_t)o * K] = acc[a][bb][j] * s;
+            }
+        }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int Cout, int K,
+                                                         int kdeg, const T *__restrict__ W,
+                                                         int64_t w_sl, int64_t w_si, int64_t w_so,
+                                                         const T *__restrict__ X,
+                                                         T *__restrict__ Y,
+                                                         const T *__restrict__ scale)
+{
+    const int64_t total = B * (int64_t)Cout * K;
+    for (int64_t idx = blockIdx.x * (int64_t)256 + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * 256) {
+        int k = (int)(idx % K);
+        int64_t rest = idx / K;
+        int o = (int)(rest % Cout);
+        int64_t b = rest / Cout;
+        int l = kdeg ? k : isqrt_small(k);
+        const T *w = W + l * w_sl + o * w_so;
+        const T *x = X + b * (int64_t)Cin * K + k;
+        T acc = 0;
+        for (int i = 0; i < Cin; ++i) acc += w[i * w_si] * x[(int64_t)i * K];
+        if (scale) acc *= scale[l];
+        Y[idx] = acc;
+    }
+}
+
+}  // namespace
+
+template <>
+hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg, const float *W,
+                                  int64_t w_sl, int64_t w_si, int64_t w_so, const float *X,
+                                  float *Y, const float *scale, hipStream_t s)
+{
+    if (B == 0 || Cout == 0 || K == 0) return hipSuccess;
+    const int64_t groups = (B + kTile - 1) / kTile;
+    const int tiles_per_group = K;  // sum over degrees of (2l+1), or L tiles when kdeg
+    const int otiles = (Cout + kTile - 1) / kTile;
+    const int64_t blocks = groups * tiles_per_group * otiles;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_contract_mfma, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B, Cin,
+                       Cout, K, kdeg ? 1 : 0, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, Y,
+                       scale);
+    return hipGetLastError();
+}
+
+template <>
+hipError_t launch_contract<double>(int64_t B, int Cin, int Cout, int K, bool kdeg,
+                                   const double *W, int64_t w_sl, int64_t w_si, int64_t w_so,
+                                   const double *X, double *Y, const double *scale, hipStream_t s)
+{
+    int64_t total = B * (int64_t)Cout * K;
+    if (total == 0) return hipSuccess;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > (1 << 20)) blocks = 1 << 20;
+    hipLaunchKernelGGL(k_contract_simple<double>, dim3((unsigned)blocks), dim3(256), 0, s, B, Cin,
+                       Cout, K, kdeg ? 1 : 0, W, w_sl, w_si, w_so, X, Y, scale);
+    return hipGetLastError();
+}
+
+}  // namespace cgtp

@@ -1,6 +1,6 @@
-// HIP kernels for gfx950 (wave64): channel contractions, grid synthesis, the
-// on-site grid product / surface curl, the message-passing receiver pass and
-// the quadrature analysis. Templated on the scalar type (fp32, fp64).
+// HIP kernels for gfx950 (wave64): grid synthesis, the on-site grid product /
+// surface curl, the message-passing receiver pass and the quadrature analysis.
+// Templated on the scalar type (fp32, fp64).
 //
 // Layouts (row-major): coefficients [b][c][K]; grid fields [b][r][f][UV] with
 // UV = u * V + v; azimuthal index mi = m + lmax.
@@ -16,48 +16,6 @@ __device__ __forceinline__ int degree_of(int k)
     while (l * l > k) --l;
     while ((l + 1) * (l + 1) <= k) ++l;
     return l;
-}
-
-// ---------------------------------------------------------------------------
-// Per-degree channel contraction (Eqs. struct-H, msgpass-HI, msgpass-tildeR,
-// struct-phi): Y[b][o][k] = scale[l] * sum_i W[l*w_sl + i*w_si + o*w_so] X[b][i][k].
-// ---------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(kThreads) void k_contract(int64_t B, int Cin, int Cout, int K,
-                                                       int kdeg, const T *__restrict__ W,
-                                                       int64_t w_sl, int64_t w_si, int64_t w_so,
-                                                       const T *__restrict__ X, T *__restrict__ Y,
-                                                       const T *__restrict__ scale)
-{
-    const int64_t total = B * (int64_t)Cout * K;
-    for (int64_t idx = blockIdx.x * (int64_t)kThreads + threadIdx.x; idx < total;
-         idx += (int64_t)gridDim.x * kThreads) {
-        int k = (int)(idx % K);
-        int64_t rest = idx / K;
-        int o = (int)(rest % Cout);
-        int64_t b = rest / Cout;
-        int l = kdeg ? k : degree_of(k);
-        const T *w = W + l * w_sl + o * w_so;
-        const T *x = X + b * (int64_t)Cin * K + k;
-        T acc = 0;
-        for (int i = 0; i < Cin; ++i) acc += w[i * w_si] * x[(int64_t)i * K];
-        if (scale) acc *= scale[l];
-        Y[idx] = acc;
-    }
-}
-
-template <typename T>
-hipError_t launch_contract(int64_t B, int Cin, int Cout, int K, bool kdeg, const T *W,
-                           int64_t w_sl, int64_t w_si, int64_t w_so, const T *X, T *Y,
-                           const T *scale, hipStream_t s)
-{
-    int64_t total = B * (int64_t)Cout * K;
-    if (total == 0) return hipSuccess;
-    int64_t blocks = (total + kThreads - 1) / kThreads;
-    if (blocks > (1 << 20)) blocks = 1 << 20;
-    hipLaunchKernelGGL(k_contract<T>, dim3((unsigned)blocks), dim3(kThreads), 0, s, B, Cin, Cout,
-                       K, kdeg ? 1 : 0, W, w_sl, w_si, w_so, X, Y, scale);
-    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -259,76 +217,128 @@ __device__ __forceinline__ void load_unit(const T *unit, int64_t e, T &ux, T &uy
     uz *= inv;
 }
 
-template <typename T, int NPT>
-__global__ __launch_bounds__(kThreads) void k_receiver_zonal(Tabs<T> tb, int R,
-                                                             const int32_t *__restrict__ row_ptr,
-                                                             const int32_t *__restrict__ col,
-                                                             const T *__restrict__ unit,
-                                                             const T *__restrict__ Rt,
-                                                             const T *__restrict__ SF,
-                                                             T *__restrict__ Ta,
-                                                             T *__restrict__ Tb)
+// Block = (receiver i, RB consecutive ranks); thread = NPT fixed grid points.
+// Per edge, the Legendre recurrence in t = rhat . Omega runs once per point and
+// serves all RB ranks; the 3 RB sender values of a point are loaded before the
+// arithmetic so that their latency overlaps it.
+constexpr int kRecvMaxThreads = 1024;
+
+template <typename T, int RB, int NPT>
+__global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
+    Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ SF,
+    T *__restrict__ Ta, T *__restrict__ Tb)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
     const Dims &d = tb.d;
-    const int64_t br = blockIdx.x;
-    const int64_t i = br / R;
-    const int r = (int)(br - i * R);
-    T sa[NPT], sb[NPT];
+    const int UV = d.UV, L = d.L, lmax = d.lmax;
+    const int nrb = (R + RB - 1) / RB;
+    const int64_t i = blockIdx.x / nrb;
+    const int r0 = (int)(blockIdx.x - i * nrb) * RB;
+    const int nr = (R - r0 < RB) ? (R - r0) : RB;
+
+    int uvs[NPT];
+    T px[NPT], psx[NPT], pxsx[NPT], pcp[NPT], psp[NPT];
 #pragma unroll
-    for (int s = 0; s < NPT; ++s) sa[s] = sb[s] = 0;
+    for (int s = 0; s < NPT; ++s) {
+        int uv = threadIdx.x + s * blockDim.x;
+        uvs[s] = uv;
+        int uvc = uv < UV ? uv : 0;
+        int u = uvc / d.V, v = uvc - u * d.V;
+        px[s] = tb.x[u];
+        psx[s] = tb.sx[u];
+        pxsx[s] = tb.xsx[u];
+        pcp[s] = tb.cphi[v];
+        psp[s] = tb.sphi[v];
+    }
+    T sa[NPT][RB], sb[NPT][RB];
+#pragma unroll
+    for (int s = 0; s < NPT; ++s)
+#pragma unroll
+        for (int q = 0; q < RB; ++q) sa[s][q] = sb[s][q] = 0;
+
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     for (int e = e0; e < e1; ++e) {
         const int64_t j = col[e];
         T ux, uy, uz;
         load_unit(unit, e, ux, uy, uz);
-        const T *rt = Rt + ((int64_t)e * R + r) * d.L;
-        const T *sf = SF + (j * R + r) * 3 * (int64_t)d.UV;
+        const T *rt = Rt + ((int64_t)e * R + r0) * L;
+        const T *sf = SF + (j * R + r0) * 3 * (int64_t)UV;
 #pragma unroll
         for (int s = 0; s < NPT; ++s) {
-            int uv = threadIdx.x + s * kThreads;
-            if (uv < d.UV) {
-                int u = uv / d.V, v = uv - u * d.V;
-                T x = tb.x[u], sx = tb.sx[u], cp = tb.cphi[v], sp = tb.sphi[v];
-                T h = ux * cp + uy * sp;
-                T t = uz * x + sx * h;
-                T p0 = 1, p1 = t, d1 = 1;
-                T a = rt[0], g = 0;
-                if (d.lmax >= 1) {
-                    a += rt[1] * t;
-                    g = rt[1];
+            const int uv = uvs[s];
+            if (uv >= UV) continue;
+            T fI[RB], fX[RB], fP[RB];
+#pragma unroll
+            for (int q = 0; q < RB; ++q) {
+                if (q < nr) {
+                    const T *f = sf + (int64_t)q * 3 * UV + uv;
+                    fI[q] = f[0];
+                    fX[q] = f[UV];
+                    fP[q] = f[2 * UV];
+                } else {
+                    fI[q] = fX[q] = fP[q] = 0;
                 }
-                for (int l = 2; l <= d.lmax; ++l) {
-                    T p2 = tb.rc1[l] * t * p1 - tb.rc2[l] * p0;
-                    T d2 = (T)l * p1 + t * d1;
-                    a += rt[l] * p2;
-                    g += rt[l] * d2;
-                    p0 = p1;
-                    p1 = p2;
-                    d1 = d2;
+            }
+            const T h = ux * pcp[s] + uy * psp[s];
+            const T t = uz * px[s] + psx[s] * h;
+            T a[RB], g[RB];
+#pragma unroll
+            for (int q = 0; q < RB; ++q) {
+                a[q] = q < nr ? rt[q * L] : (T)0;
+                g[q] = 0;
+            }
+            if (lmax >= 1) {
+#pragma unroll
+                for (int q = 0; q < RB; ++q) {
+                    T c = q < nr ? rt[q * L + 1] : (T)0;
+                    a[q] += c * t;
+                    g[q] = c;
                 }
-                T dxt = uz - tb.xsx[u] * h;
-                T dpt = sx * (uy * cp - ux * sp);
-                T fI = sf[uv], fX = sf[d.UV + uv], fP = sf[2 * d.UV + uv];
-                sa[s] += a * fI;
-                sb[s] += g * (dpt * fX - dxt * fP);
+            }
+            T p0 = 1, p1 = t, d1 = 1;
+            for (int l = 2; l <= lmax; ++l) {
+                const T p2 = tb.rc1[l] * t * p1 - tb.rc2[l] * p0;
+                const T d2 = (T)l * p1 + t * d1;
+#pragma unroll
+                for (int q = 0; q < RB; ++q) {
+                    T c = q < nr ? rt[q * L + l] : (T)0;
+                    a[q] += c * p2;
+                    g[q] += c * d2;
+                }
+                p0 = p1;
+                p1 = p2;
+                d1 = d2;
+            }
+            const T dxt = uz - pxsx[s] * h;
+            const T dpt = psx[s] * (uy * pcp[s] - ux * psp[s]);
+#pragma unroll
+            for (int q = 0; q < RB; ++q) {
+                sa[s][q] += a[q] * fI[q];
+                sb[s][q] += g[q] * (dpt * fX[q] - dxt * fP[q]);
             }
         }
     }
+    // inverse transforms, one rank at a time through LDS
     T *Sa = smem;
-    T *Sb = Sa + d.UV;
-    T *Tm = Sb + d.UV;
+    T *Sb = Sa + UV;
+    T *Tm = Sb + UV;
 #pragma unroll
-    for (int s = 0; s < NPT; ++s) {
-        int uv = threadIdx.x + s * kThreads;
-        if (uv < d.UV) {
-            Sa[uv] = sa[s];
-            Sb[uv] = sb[s];
+    for (int q = 0; q < RB; ++q) {
+        if (q >= nr) break;
+#pragma unroll
+        for (int s = 0; s < NPT; ++s) {
+            if (uvs[s] < UV) {
+                Sa[uvs[s]] = sa[s][q];
+                Sb[uvs[s]] = sb[s][q];
+            }
         }
+        __syncthreads();
+        const int64_t br = i * R + r0 + q;
+        analysis2(tb, Sa, Sb, Tm, Ta + br * d.K, Tb + br * d.K);
+        __syncthreads();
     }
-    __syncthreads();
-    analysis2(tb, Sa, Sb, Tm, Ta + br * d.K, Tb + br * d.K);
 }
 
 // Separated edge synthesis (Eqs. msgpass-FE, msgpass-AE and the derivative
@@ -432,23 +442,26 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
         return hipGetLastError();
     }
     size_t sh = sizeof(T) * (2 * d.UV + 2 * d.M * d.U);
-    int npt = (d.UV + kThreads - 1) / kThreads;
-#define CGTP_RECV(NP)                                                                         \
-    hipLaunchKernelGGL((k_receiver_zonal<T, NP>), dim3((unsigned)blocks), dim3(kThreads), sh, s, \
-                       tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb)
-    if (npt <= 1) CGTP_RECV(1);
-    else if (npt <= 2) CGTP_RECV(2);
-    else if (npt <= 4) CGTP_RECV(4);
-    else if (npt <= 8) CGTP_RECV(8);
-    else CGTP_RECV(11);
+    const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
+    const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
+#define CGTP_RECV(RBV, NP)                                                                     \
+    do {                                                                                       \
+        int64_t nb = N * ((R + RBV - 1) / RBV);                                                \
+        hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP>), dim3((unsigned)nb), dim3(threads), sh, \
+                           s, tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb);                       \
+    } while (0)
+    // ranks per block: sized so the per-thread accumulators and in-flight loads fit in
+    // registers without spilling (fp64 values take two registers)
+    constexpr int rb1 = sizeof(T) == 4 ? 8 : 4;
+    constexpr int rb2 = sizeof(T) == 4 ? 4 : 2;
+    if (npt <= 1) CGTP_RECV(rb1, 1);
+    else if (npt <= 2) CGTP_RECV(rb2, 2);
+    else CGTP_RECV(2, 3);
 #undef CGTP_RECV
     return hipGetLastError();
 }
 
 #define CGTP_INSTANTIATE(T)                                                                      \
-    template hipError_t launch_contract<T>(int64_t, int, int, int, bool, const T *, int64_t,     \
-                                           int64_t, int64_t, const T *, T *, const T *,          \
-                                           hipStream_t);                                         \
     template hipError_t launch_sender_fields<T>(const Tabs<T> &, int64_t, int, const T *, T *,   \
                                                 hipStream_t);                                    \
     template hipError_t launch_onsite_grid<T>(const Tabs<T> &, int64_t, int, const T *,          \

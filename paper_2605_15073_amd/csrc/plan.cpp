@@ -8,6 +8,17 @@
 
 #include "internal.h"
 
+namespace {
+constexpr int kMaxStages = 6;
+// HIP events bracketing the kernel stages of one call (CGTP_TIME_STAGES).
+struct EventSet {
+    hipEvent_t ev[kMaxStages + 1];
+    int op;
+    int n_stages;
+    bool complete;
+};
+}  // namespace
+
 struct cgtp_plan_s {
     cgtp::Dims d;
     int C, R, dtype;
@@ -16,6 +27,10 @@ struct cgtp_plan_s {
     void *tables;        // device table image (plan dtype)
     void *own_ws;        // workspace grown by the plan when the caller passes none
     size_t own_ws_bytes;
+    std::vector<EventSet> timers;  // reused across calls; timers_used are pending
+    size_t timers_used;
+    double stage_acc[2][kMaxStages];  // drained sums per op (onsite, message pass)
+    int stage_calls[2];
 };
 
 namespace {
@@ -119,6 +134,75 @@ int get_workspace(cgtp_plan_s *p, size_t need, void *ws, size_t ws_bytes, void *
     return CGTP_OK;
 }
 
+// Fold the pending event sets into the plan's running sums.
+int drain_timers(cgtp_plan_s *p)
+{
+    int status = CGTP_OK;
+    for (size_t i = 0; i < p->timers_used; ++i) {
+        EventSet &es = p->timers[i];
+        if (!es.complete) continue;
+        hipError_t e = hipEventSynchronize(es.ev[es.n_stages]);
+        double t_stage[kMaxStages] = {0};
+        for (int k = 0; e == hipSuccess && k < es.n_stages; ++k) {
+            float t = 0.f;
+            e = hipEventElapsedTime(&t, es.ev[k], es.ev[k + 1]);
+            t_stage[k] = t;
+        }
+        if (e != hipSuccess) {
+            status = hip_fail(e, "stage events");
+            continue;
+        }
+        for (int k = 0; k < es.n_stages; ++k) p->stage_acc[es.op][k] += t_stage[k];
+        p->stage_calls[es.op] += 1;
+    }
+    p->timers_used = 0;
+    return status;
+}
+
+constexpr size_t kMaxPendingTimers = 1024;
+
+// Records the stage boundaries of one call when the plan times its stages.
+struct StageRec {
+    EventSet *set = nullptr;
+    hipStream_t s = nullptr;
+    int next = 0;
+
+    int begin(cgtp_plan_s *p, int op, int n_stages, hipStream_t stream)
+    {
+        if (!(p->flags & CGTP_TIME_STAGES)) return CGTP_OK;
+        if (p->timers_used == kMaxPendingTimers) {
+            int st = drain_timers(p);
+            if (st) return st;
+        }
+        if (p->timers_used == p->timers.size()) {
+            EventSet es{};
+            for (int i = 0; i <= kMaxStages; ++i) {
+                hipError_t e = hipEventCreate(&es.ev[i]);
+                if (e != hipSuccess) {
+                    for (int j = 0; j < i; ++j) (void)hipEventDestroy(es.ev[j]);
+                    return hip_fail(e, "hipEventCreate");
+                }
+            }
+            p->timers.push_back(es);
+        }
+        set = &p->timers[p->timers_used++];
+        set->op = op;
+        set->n_stages = n_stages;
+        set->complete = false;
+        s = stream;
+        next = 0;
+        hipError_t e = hipEventRecord(set->ev[0], s);
+        return e == hipSuccess ? CGTP_OK : hip_fail(e, "hipEventRecord");
+    }
+    // stage `next` has been enqueued (or skipped)
+    void mark()
+    {
+        if (!set) return;
+        (void)hipEventRecord(set->ev[++next], s);
+        if (next == set->n_stages) set->complete = true;
+    }
+};
+
 template <typename T>
 int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const void *UA,
                const void *UB, const void *Uoe, const void *Uoo, void *oe, void *oo, char *ws,
@@ -133,11 +217,15 @@ int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const vo
     T *Ta = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[3]);
     const int64_t sl = (int64_t)C * R;
+    StageRec rec;
+    int st = rec.begin(p, CGTP_OP_ONSITE, 5, s);
+    if (st) return st;
     hipError_t e;
     // Eq. struct-H for both operands (shared when the operands coincide)
     e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UA, sl, R, 1, (const T *)A, HA,
                                  nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "contract A");
+    rec.mark();
     const T *HBp = HA;
     if (!(A == B && UA == UB)) {
         e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UB, sl, R, 1, (const T *)B,
@@ -145,19 +233,23 @@ int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const vo
         if (e != hipSuccess) return hip_fail(e, "contract B");
         HBp = HB;
     }
+    rec.mark();
     e = cgtp::launch_onsite_grid<T>(tb, N, R, HA, HBp, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "onsite grid");
+    rec.mark();
     // Eq. struct-phi: out[b][n][k] = sum_r Uout[l][n][r] T[b][r][k]
     if (oe) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoe, sl, 1, R, Ta, (T *)oe,
                                      nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project even");
     }
+    rec.mark();
     if (oo) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoo, sl, 1, R, Tb, (T *)oo,
                                      nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project odd");
     }
+    rec.mark();
     return CGTP_OK;
 }
 
@@ -177,30 +269,39 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
     T *Ta = reinterpret_cast<T *>(ws + lay.off[3]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
     const int64_t sl = (int64_t)C * R;
+    StageRec rec;
+    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS, 6, s);
+    if (st) return st;
     hipError_t e;
     // Eq. msgpass-HI, then the node-side forward transforms (Eqs. msgpass-FI, msgpass-AI)
     e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UI, sl, R, 1, (const T *)I, HI,
                                  nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "contract node features");
+    rec.mark();
     e = cgtp::launch_sender_fields<T>(tb, N, R, HI, SF, s);
     if (e != hipSuccess) return hip_fail(e, "sender fields");
+    rec.mark();
     // Eq. msgpass-tildeR (zonal form folds in the addition-theorem weight (2l+1)/(4 pi))
     e = cgtp::launch_contract<T>(E, C, R, d.L, true, (const T *)UE, sl, R, 1, (const T *)rad, Rt,
                                  separated ? nullptr : tb.cl, s);
     if (e != hipSuccess) return hip_fail(e, "contract edge radial");
+    rec.mark();
     e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, SF, Ta,
                                  Tb, s);
     if (e != hipSuccess) return hip_fail(e, "receiver");
+    rec.mark();
     if (oe) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoe, sl, 1, R, Ta, (T *)oe,
                                      nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project even");
     }
+    rec.mark();
     if (oo) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoo, sl, 1, R, Tb, (T *)oo,
                                      nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project odd");
     }
+    rec.mark();
     return CGTP_OK;
 }
 
@@ -242,7 +343,7 @@ int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan)
                     desc->rank);
     if (desc->dtype != CGTP_F32 && desc->dtype != CGTP_F64)
         return fail(CGTP_ERR_ARG, "unknown dtype %d", desc->dtype);
-    if (desc->flags & ~(CGTP_VALIDATE_CSR | CGTP_EDGE_SEPARATED))
+    if (desc->flags & ~(CGTP_VALIDATE_CSR | CGTP_EDGE_SEPARATED | CGTP_TIME_STAGES))
         return fail(CGTP_ERR_ARG, "unknown flags 0x%x", desc->flags);
     int U, V;
     if (desc->n_theta < 0 || desc->n_phi < 0 ||
@@ -277,7 +378,7 @@ int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan)
         (void)hipFree(dt);
         return hip_fail(e, "hipMemcpy(tables)");
     }
-    cgtp_plan_s *p = new (std::nothrow) cgtp_plan_s;
+    cgtp_plan_s *p = new (std::nothrow) cgtp_plan_s();
     if (!p) {
         (void)hipFree(dt);
         return fail(CGTP_ERR_ARG, "out of host memory");
@@ -291,6 +392,7 @@ int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan)
     p->tables = dt;
     p->own_ws = nullptr;
     p->own_ws_bytes = 0;
+    p->timers_used = 0;
     *plan = p;
     return CGTP_OK;
 }
@@ -387,9 +489,29 @@ int cgtp_destroy(cgtp_plan plan)
     hipError_t e = hipDeviceSynchronize();
     if (plan->own_ws) (void)hipFree(plan->own_ws);
     if (plan->tables) (void)hipFree(plan->tables);
+    for (EventSet &es : plan->timers)
+        for (int i = 0; i <= kMaxStages; ++i) (void)hipEventDestroy(es.ev[i]);
     delete plan;
     if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
     return CGTP_OK;
+}
+
+int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages, int *n_calls)
+{
+    if (!plan || !ms || !n_stages || !n_calls) return fail(CGTP_ERR_ARG, "NULL argument");
+    if (!(plan->flags & CGTP_TIME_STAGES))
+        return fail(CGTP_ERR_ARG, "plan was created without CGTP_TIME_STAGES");
+    int ns;
+    if (op == CGTP_OP_ONSITE) ns = 5;
+    else if (op == CGTP_OP_MESSAGE_PASS) ns = 6;
+    else return fail(CGTP_ERR_ARG, "unknown op %d", op);
+    int status = drain_timers(plan);
+    for (int k = 0; k < ns && k < cap; ++k) ms[k] = plan->stage_acc[op][k];
+    *n_stages = ns;
+    *n_calls = plan->stage_calls[op];
+    for (int k = 0; k < kMaxStages; ++k) plan->stage_acc[op][k] = 0.0;
+    plan->stage_calls[op] = 0;
+    return status;
 }
 
 const char *cgtp_status_string(int status)
