@@ -252,6 +252,9 @@ def main():
     ap.add_argument("--workload", default="mp_10k_l6_c128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep-out", default=None)
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="run only a plain device-to-device copy of this many bytes (3 times), "
+                         "the calibration kernel for the HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the method is "
@@ -264,6 +267,15 @@ def main():
         sys.exit(1)
     from paper_2605_15073_amd.inputs import WORKLOADS
 
+    if args.copy_bytes:
+        n = args.copy_bytes // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n * 4, "copies": 3}), flush=True)
+        return
     if args.sweep_out:
         sweep(args.sweep_out, max(3, args.steps // 4), args.warmup)
         return

@@ -1,7 +1,7 @@
 // Per-degree channel contraction (Eqs. struct-H, msgpass-HI, msgpass-tildeR and
 // the lambda projection struct-phi / cat-alpha-phi / cat-beta-phi):
 //
-//   Y[b][o][k] = scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so] * X[b][i][k]
+//   Y[b*y_sb + o*y_so + k*y_sk] = scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so] * X[b][i][k]
 //
 // For a fixed degree l this is a GEMM Y_l[o][c] = sum_i W_l[i][o] X_l[i][c] over
 // the columns c = (b, m), m = 0..2l (or c = b when k is the degree itself).
@@ -35,12 +35,19 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     int64_t B, int Cin, int Cout, int K, int kdeg, int tiles_per_group, int otiles,
     const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
-    const float *__restrict__ X, float *__restrict__ Y, const float *__restrict__ scale)
+    const float *__restrict__ X, float *__restrict__ Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
+    const float *__restrict__ scale)
 {
     __shared__ float As[kChunk][kTile + 4];  // As[i][o] = W_l[i0 + i][o0 + o]
     __shared__ float Bs[kChunk][kTile + 4];  // Bs[i][c] = X_l[i0 + i][c0 + c]
 
-    const int64_t bid = blockIdx.x;
+    // Blocks are dealt round-robin to the 8 XCDs (block b runs on XCD b % 8), each with
+    // its own L2. Remap so that each XCD gets a contiguous range of tiles: the tiles of a
+    // node group, which read the same input lines, then share one L2.
+    const int64_t nblk = gridDim.x;
+    const int64_t per = nblk / 8, rem = nblk % 8;
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t bid = (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
     const int ot = (int)(bid % otiles);
     const int64_t rest = bid / otiles;
     const int t = (int)(rest % tiles_per_group);
@@ -119,11 +126,11 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
             if (c >= ncols) continue;
             int bcol = c / width;
             int m = c - bcol * width;
-            float *ycol = Y + (b0 + bcol) * (int64_t)Cout * K + kofs + m;
+            float *ycol = Y + (b0 + bcol) * y_sb + (int64_t)(kofs + m) * y_sk;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 int o = o0 + osub + 16 * a + 4 * (lane >> 4) + j;
-                if (o < Cout) ycol[(int64_t)o * K] = acc[a][bb][j] * s;
+                if (o < Cout) ycol[(int64_t)o * y_so] = acc[a][bb][j] * s;
             }
         }
 }
@@ -133,7 +140,8 @@ __global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int
                                                          int kdeg, const T *__restrict__ W,
                                                          int64_t w_sl, int64_t w_si, int64_t w_so,
                                                          const T *__restrict__ X,
-                                                         T *__restrict__ Y,
+                                                         T *__restrict__ Y, int64_t y_sb,
+                                                         int64_t y_so, int64_t y_sk,
                                                          const T *__restrict__ scale)
 {
     const int64_t total = B * (int64_t)Cout * K;
@@ -149,7 +157,7 @@ __global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int
         T acc = 0;
         for (int i = 0; i < Cin; ++i) acc += w[i * w_si] * x[(int64_t)i * K];
         if (scale) acc *= scale[l];
-        Y[idx] = acc;
+        Y[b * y_sb + o * y_so + (int64_t)k * y_sk] = acc;
     }
 }
 
@@ -158,7 +166,8 @@ __global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int
 template <>
 hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg, const float *W,
                                   int64_t w_sl, int64_t w_si, int64_t w_so, const float *X,
-                                  float *Y, const float *scale, hipStream_t s)
+                                  float *Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
+                                  const float *scale, hipStream_t s)
 {
     if (B == 0 || Cout == 0 || K == 0) return hipSuccess;
     const int64_t groups = (B + kTile - 1) / kTile;
@@ -168,21 +177,22 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_contract_mfma, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B, Cin,
                        Cout, K, kdeg ? 1 : 0, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, Y,
-                       scale);
+                       y_sb, y_so, y_sk, scale);
     return hipGetLastError();
 }
 
 template <>
 hipError_t launch_contract<double>(int64_t B, int Cin, int Cout, int K, bool kdeg,
                                    const double *W, int64_t w_sl, int64_t w_si, int64_t w_so,
-                                   const double *X, double *Y, const double *scale, hipStream_t s)
+                                   const double *X, double *Y, int64_t y_sb, int64_t y_so,
+                                   int64_t y_sk, const double *scale, hipStream_t s)
 {
     int64_t total = B * (int64_t)Cout * K;
     if (total == 0) return hipSuccess;
     int64_t blocks = (total + 255) / 256;
     if (blocks > (1 << 20)) blocks = 1 << 20;
     hipLaunchKernelGGL(k_contract_simple<double>, dim3((unsigned)blocks), dim3(256), 0, s, B, Cin,
-                       Cout, K, kdeg ? 1 : 0, W, w_sl, w_si, w_so, X, Y, scale);
+                       Cout, K, kdeg ? 1 : 0, W, w_sl, w_si, w_so, X, Y, y_sb, y_so, y_sk, scale);
     return hipGetLastError();
 }
 

@@ -48,12 +48,13 @@ __device__ void legendre_synth(const Tabs<T> &tb, const T *H, T *F, T *Fx)
 // Fourier synthesis at one grid point (Eq. struct-tildeA) of the field, its
 // x-derivative, and its phi-derivative. In the real basis d/dphi maps the cosine
 // slot +k to -k * (sine slot) and the sine slot -k to +k * (cosine slot).
+// q points at the [V][M] Fourier table (staged in LDS by the callers).
 template <typename T>
-__device__ __forceinline__ void fourier_point(const Tabs<T> &tb, const T *F, const T *Fx, int u,
-                                              int v, T &a, T &ax, T &ap)
+__device__ __forceinline__ void fourier_point(const Tabs<T> &tb, const T *q, const T *F,
+                                              const T *Fx, int u, int v, T &a, T &ax, T &ap)
 {
     const Dims &d = tb.d;
-    const T *qv = tb.q + (size_t)v * d.M;
+    const T *qv = q + v * d.M;
     const int lm = d.lmax, U = d.U;
     a = qv[lm] * F[lm * U + u];
     ax = qv[lm] * Fx[lm * U + u];
@@ -70,7 +71,8 @@ __device__ __forceinline__ void fourier_point(const Tabs<T> &tb, const T *F, con
 // Quadrature analysis (Eqs. struct-Tmu, struct-Tlm) of two grid fields S1, S2
 // [UV] held on chip, through Tm scratch [2][M][U]; writes out1/out2 [K].
 template <typename T>
-__device__ void analysis2(const Tabs<T> &tb, const T *S1, const T *S2, T *Tm, T *out1, T *out2)
+__device__ void analysis2(const Tabs<T> &tb, const T *q, const T *S1, const T *S2, T *Tm, T *out1,
+                          T *out2)
 {
     const Dims &d = tb.d;
     const int MU = d.M * d.U;
@@ -80,7 +82,7 @@ __device__ void analysis2(const Tabs<T> &tb, const T *S1, const T *S2, T *Tm, T 
         int mi = rem / d.U, u = rem - mi * d.U;
         const T *S = (which ? S2 : S1) + u * d.V;
         T s = 0;
-        for (int v = 0; v < d.V; ++v) s += tb.q[(size_t)v * d.M + mi] * S[v];
+        for (int v = 0; v < d.V; ++v) s += q[v * d.M + mi] * S[v];
         Tm[idx] = s;
     }
     __syncthreads();
@@ -96,34 +98,52 @@ __device__ void analysis2(const Tabs<T> &tb, const T *S1, const T *S2, T *Tm, T 
     }
 }
 
+// Copy the [V][M] Fourier table into LDS (callers synchronise afterwards).
+template <typename T>
+__device__ __forceinline__ void stage_q(const Tabs<T> &tb, T *qs)
+{
+    for (int k = threadIdx.x; k < tb.d.V * tb.d.M; k += blockDim.x) qs[k] = tb.q[k];
+}
+
 // ---------------------------------------------------------------------------
 // Sender (node-side) grid fields: SF[b][r][0..2][UV] = (A, dA/dx, dA/dphi).
-// One block per (node, rank).
+// One block per (node, rb consecutive ranks): the Legendre pass of all rb ranks,
+// then every thread writes the three fields of its grid points for each rank.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_sender_fields(Tabs<T> tb, int R,
+__global__ __launch_bounds__(kThreads) void k_sender_fields(Tabs<T> tb, int R, int rb,
                                                             const T *__restrict__ H,
                                                             T *__restrict__ SF)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
     const Dims &d = tb.d;
-    const int64_t br = blockIdx.x;  // b * R + r
-    T *Hs = smem;
-    T *F = Hs + d.K;
-    T *Fx = F + d.M * d.U;
-    for (int k = threadIdx.x; k < d.K; k += blockDim.x) Hs[k] = H[br * d.K + k];
+    const int MU = d.M * d.U;
+    const int nrb = (R + rb - 1) / rb;
+    const int64_t b = blockIdx.x / nrb;
+    const int r0 = (int)(blockIdx.x - b * nrb) * rb;
+    const int nr = (R - r0 < rb) ? (R - r0) : rb;
+    T *qs = smem;               // [V][M]
+    T *Hs = qs + d.V * d.M;     // [rb][K]
+    T *F = Hs + rb * d.K;       // [rb][M][U]
+    T *Fx = F + rb * MU;        // [rb][M][U]
+    stage_q(tb, qs);
+    const T *hsrc = H + (b * R + r0) * (int64_t)d.K;
+    for (int k = threadIdx.x; k < nr * d.K; k += blockDim.x) Hs[k] = hsrc[k];
     __syncthreads();
-    legendre_synth(tb, Hs, F, Fx);
+    for (int q = 0; q < nr; ++q) legendre_synth(tb, Hs + q * d.K, F + q * MU, Fx + q * MU);
     __syncthreads();
-    T *out = SF + br * 3 * (int64_t)d.UV;
+    T *out = SF + (b * R + r0) * 3 * (int64_t)d.UV;
     for (int uv = threadIdx.x; uv < d.UV; uv += blockDim.x) {
-        int u = uv / d.V, v = uv - u * d.V;
-        T a, ax, ap;
-        fourier_point(tb, F, Fx, u, v, a, ax, ap);
-        out[uv] = a;
-        out[d.UV + uv] = ax;
-        out[2 * d.UV + uv] = ap;
+        const int u = uv / d.V, v = uv - u * d.V;
+        for (int q = 0; q < nr; ++q) {
+            T a, ax, ap;
+            fourier_point(tb, qs, F + q * MU, Fx + q * MU, u, v, a, ax, ap);
+            T *o = out + (int64_t)q * 3 * d.UV + uv;
+            o[0] = a;
+            o[d.UV] = ax;
+            o[2 * d.UV] = ap;
+        }
     }
 }
 
@@ -131,11 +151,17 @@ template <typename T>
 hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H, T *SF,
                                 hipStream_t s)
 {
-    int64_t blocks = B * R;
-    if (blocks == 0) return hipSuccess;
-    size_t sh = sizeof(T) * (tb.d.K + 2 * tb.d.M * tb.d.U);
+    if (B == 0) return hipSuccess;
+    const size_t per_rank = tb.d.K + 2 * (size_t)tb.d.M * tb.d.U;
+    const size_t fixed = (size_t)tb.d.V * tb.d.M;
+    int rb = (int)((48 * 1024 / sizeof(T) - fixed) / per_rank);
+    if (rb > 8) rb = 8;
+    if (rb < 1) rb = 1;
+    if (rb > R) rb = R;
+    const int64_t blocks = B * ((R + rb - 1) / rb);
+    const size_t sh = sizeof(T) * (fixed + rb * per_rank);
     hipLaunchKernelGGL(k_sender_fields<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R,
-                       H, SF);
+                       rb, H, SF);
     return hipGetLastError();
 }
 
@@ -146,7 +172,7 @@ hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H,
 // then analyse both back to (l, m).
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(kThreads) void k_onsite_grid(Tabs<T> tb, int R,
+__global__ __launch_bounds__(kThreads) void k_onsite_grid(Tabs<T> tb, int R, int q_in_lds,
                                                           const T *__restrict__ HA,
                                                           const T *__restrict__ HB,
                                                           T *__restrict__ Ta, T *__restrict__ Tb)
@@ -156,7 +182,9 @@ __global__ __launch_bounds__(kThreads) void k_onsite_grid(Tabs<T> tb, int R,
     const Dims &d = tb.d;
     const int64_t br = blockIdx.x;
     const int MU = d.M * d.U;
-    T *H1 = smem;
+    // the Fourier table is staged in LDS unless that would exceed the 64 KiB budget
+    T *qs = smem;
+    T *H1 = qs + (q_in_lds ? d.V * d.M : 0);
     T *H2 = H1 + d.K;
     T *F1 = H2 + d.K;
     T *F1x = F1 + MU;
@@ -164,6 +192,8 @@ __global__ __launch_bounds__(kThreads) void k_onsite_grid(Tabs<T> tb, int R,
     T *F2x = F2 + MU;
     T *Sa = F2x + MU;
     T *Sb = Sa + d.UV;
+    if (q_in_lds) stage_q(tb, qs);
+    const T *q = q_in_lds ? qs : tb.q;
     for (int k = threadIdx.x; k < d.K; k += blockDim.x) {
         H1[k] = HA[br * d.K + k];
         H2[k] = HB[br * d.K + k];
@@ -175,13 +205,14 @@ __global__ __launch_bounds__(kThreads) void k_onsite_grid(Tabs<T> tb, int R,
     for (int uv = threadIdx.x; uv < d.UV; uv += blockDim.x) {
         int u = uv / d.V, v = uv - u * d.V;
         T a1, a1x, a1p, a2, a2x, a2p;
-        fourier_point(tb, F1, F1x, u, v, a1, a1x, a1p);
-        fourier_point(tb, F2, F2x, u, v, a2, a2x, a2p);
+        fourier_point(tb, q, F1, F1x, u, v, a1, a1x, a1p);
+        fourier_point(tb, q, F2, F2x, u, v, a2, a2x, a2p);
         Sa[uv] = a1 * a2;
         Sb[uv] = a1p * a2x - a1x * a2p;
     }
     __syncthreads();
-    analysis2(tb, Sa, Sb, F1 /* reused as Tm scratch [2][M][U] */, Ta + br * d.K, Tb + br * d.K);
+    analysis2(tb, q, Sa, Sb, F1 /* reused as Tm scratch [2][M][U] */, Ta + br * d.K,
+              Tb + br * d.K);
 }
 
 template <typename T>
@@ -190,9 +221,12 @@ hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, 
 {
     int64_t blocks = B * R;
     if (blocks == 0) return hipSuccess;
-    size_t sh = sizeof(T) * (2 * tb.d.K + 4 * tb.d.M * tb.d.U + 2 * tb.d.UV);
-    hipLaunchKernelGGL(k_onsite_grid<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R, HA,
-                       HB, Ta, Tb);
+    const size_t base = 2 * tb.d.K + 4 * tb.d.M * tb.d.U + 2 * tb.d.UV;
+    const size_t with_q = base + tb.d.V * tb.d.M;
+    const int q_in_lds = sizeof(T) * with_q <= 65536 ? 1 : 0;
+    const size_t sh = sizeof(T) * (q_in_lds ? with_q : base);
+    hipLaunchKernelGGL(k_onsite_grid<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R,
+                       q_in_lds, HA, HB, Ta, Tb);
     return hipGetLastError();
 }
 
@@ -223,7 +257,33 @@ __device__ __forceinline__ void load_unit(const T *unit, int64_t e, T &ux, T &uy
 // arithmetic so that their latency overlaps it.
 constexpr int kRecvMaxThreads = 1024;
 
-template <typename T, int RB, int NPT>
+// Raw buffer loads: one descriptor per edge over the sender's rank block; every
+// load of a grid point shares its VGPR byte offset and differs only in a scalar
+// offset. Out-of-range offsets read 0 (num_records bounds the block).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, unsigned bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+template <typename T>
+__device__ __forceinline__ T buf_load(__amdgpu_buffer_rsrc_t rs, unsigned voff, unsigned soff);
+
+template <>
+__device__ __forceinline__ float buf_load<float>(__amdgpu_buffer_rsrc_t rs, unsigned voff,
+                                                 unsigned soff)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0));
+}
+
+template <>
+__device__ __forceinline__ double buf_load<double>(__amdgpu_buffer_rsrc_t rs, unsigned voff,
+                                                   unsigned soff)
+{
+    return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0));
+}
+
+template <typename T, int RB, int NPT, bool FULL>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
     const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ SF,
@@ -234,9 +294,15 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     const Dims &d = tb.d;
     const int UV = d.UV, L = d.L, lmax = d.lmax;
     const int nrb = (R + RB - 1) / RB;
-    const int64_t i = blockIdx.x / nrb;
-    const int r0 = (int)(blockIdx.x - i * nrb) * RB;
-    const int nr = (R - r0 < RB) ? (R - r0) : RB;
+    // The rank blocks of one receiver read the same edge coefficient lines: keep them on
+    // one XCD (block b runs on XCD b % 8) by giving each XCD a contiguous range.
+    const int64_t nblk = gridDim.x, per = nblk / 8, rem = nblk % 8;
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t lb = (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+    const int64_t i = lb / nrb;
+    const int r0 = (int)(lb - i * nrb) * RB;
+    // FULL: R is a multiple of RB, so every rank of the block exists (no guards)
+    const int nr = FULL ? RB : ((R - r0 < RB) ? (R - r0) : RB);
 
     int uvs[NPT];
     T px[NPT], psx[NPT], pxsx[NPT], pcp[NPT], psp[NPT];
@@ -259,40 +325,51 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
         for (int q = 0; q < RB; ++q) sa[s][q] = sb[s][q] = 0;
 
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
+    // the next edge's sender index and direction are fetched one iteration ahead
+    // (the sender index is the same for the whole block: readfirstlane keeps it, and the
+    // per-edge base address, in scalar registers)
+    int jn = 0;
+    T uxn = 0, uyn = 0, uzn = 1;
+    if (e0 < e1) {
+        jn = __builtin_amdgcn_readfirstlane(col[e0]);
+        load_unit(unit, e0, uxn, uyn, uzn);
+    }
     for (int e = e0; e < e1; ++e) {
-        const int64_t j = col[e];
-        T ux, uy, uz;
-        load_unit(unit, e, ux, uy, uz);
-        const T *rt = Rt + ((int64_t)e * R + r0) * L;
-        const T *sf = SF + (j * R + r0) * 3 * (int64_t)UV;
+        const int64_t j = jn;
+        const T ux = uxn, uy = uyn, uz = uzn;
+        if (e + 1 < e1) {
+            jn = __builtin_amdgcn_readfirstlane(col[e + 1]);
+            load_unit(unit, e + 1, uxn, uyn, uzn);
+        }
+        const T *rt = Rt + (int64_t)e * L * R + r0;   // Rt[e][l][r0 + q] = rt[l * R + q]
+        const __amdgpu_buffer_rsrc_t sfr =
+            make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UV, (unsigned)(nr * 3 * UV * sizeof(T)));
+        const unsigned fstride = (unsigned)(UV * sizeof(T));
 #pragma unroll
         for (int s = 0; s < NPT; ++s) {
             const int uv = uvs[s];
             if (uv >= UV) continue;
+            const unsigned voff = (unsigned)(uv * sizeof(T));
             T fI[RB], fX[RB], fP[RB];
 #pragma unroll
             for (int q = 0; q < RB; ++q) {
-                if (q < nr) {
-                    const T *f = sf + (int64_t)q * 3 * UV + uv;
-                    fI[q] = f[0];
-                    fX[q] = f[UV];
-                    fP[q] = f[2 * UV];
-                } else {
-                    fI[q] = fX[q] = fP[q] = 0;
-                }
+                // ranks past nr fall outside the descriptor's range and read 0
+                fI[q] = buf_load<T>(sfr, voff, (3 * q) * fstride);
+                fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
+                fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
             }
-            const T h = ux * pcp[s] + uy * psp[s];
+    const T h = ux * pcp[s] + uy * psp[s];
             const T t = uz * px[s] + psx[s] * h;
             T a[RB], g[RB];
 #pragma unroll
             for (int q = 0; q < RB; ++q) {
-                a[q] = q < nr ? rt[q * L] : (T)0;
+                a[q] = (FULL || q < nr) ? rt[q] : (T)0;
                 g[q] = 0;
             }
             if (lmax >= 1) {
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
-                    T c = q < nr ? rt[q * L + 1] : (T)0;
+                    T c = (FULL || q < nr) ? rt[R + q] : (T)0;
                     a[q] += c * t;
                     g[q] = c;
                 }
@@ -303,7 +380,7 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
                 const T d2 = (T)l * p1 + t * d1;
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
-                    T c = q < nr ? rt[q * L + l] : (T)0;
+                    T c = (FULL || q < nr) ? rt[l * R + q] : (T)0;
                     a[q] += c * p2;
                     g[q] += c * d2;
                 }
@@ -321,9 +398,11 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
         }
     }
     // inverse transforms, one rank at a time through LDS
-    T *Sa = smem;
+    T *qs = smem;
+    T *Sa = qs + d.V * d.M;
     T *Sb = Sa + UV;
     T *Tm = Sb + UV;
+    stage_q(tb, qs);
 #pragma unroll
     for (int q = 0; q < RB; ++q) {
         if (q >= nr) break;
@@ -336,7 +415,7 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
         }
         __syncthreads();
         const int64_t br = i * R + r0 + q;
-        analysis2(tb, Sa, Sb, Tm, Ta + br * d.K, Tb + br * d.K);
+        analysis2(tb, qs, Sa, Sb, Tm, Ta + br * d.K, Tb + br * d.K);
         __syncthreads();
     }
 }
@@ -395,11 +474,13 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
     const int64_t i = br / R;
     const int r = (int)(br - i * R);
     const int MU = d.M * d.U;
-    T *Sa = smem;
+    T *qs = smem;
+    T *Sa = qs + d.V * d.M;
     T *Sb = Sa + d.UV;
     T *Y = Sb + d.UV;
     T *F = Y + d.K;
     T *Fx = F + MU;
+    stage_q(tb, qs);
     for (int uv = threadIdx.x; uv < d.UV; uv += blockDim.x) Sa[uv] = Sb[uv] = 0;
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     for (int e = e0; e < e1; ++e) {
@@ -409,8 +490,8 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
         __syncthreads();  // previous edge done with Y / F
         edge_sh(tb, ux, uy, uz, Y);
         __syncthreads();
-        const T *rt = Rt + ((int64_t)e * R + r) * d.L;
-        for (int k = threadIdx.x; k < d.K; k += blockDim.x) Y[k] *= rt[degree_of(k)];
+        const T *rt = Rt + (int64_t)e * d.L * R + r;   // Rt[e][l][r] = rt[l * R]
+        for (int k = threadIdx.x; k < d.K; k += blockDim.x) Y[k] *= rt[degree_of(k) * R];
         __syncthreads();
         legendre_synth(tb, Y, F, Fx);
         __syncthreads();
@@ -418,13 +499,13 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
         for (int uv = threadIdx.x; uv < d.UV; uv += blockDim.x) {
             int u = uv / d.V, v = uv - u * d.V;
             T a, ax, ap;
-            fourier_point(tb, F, Fx, u, v, a, ax, ap);
+            fourier_point(tb, qs, F, Fx, u, v, a, ax, ap);
             Sa[uv] += a * sf[uv];
             Sb[uv] += ap * sf[d.UV + uv] - ax * sf[2 * d.UV + uv];
         }
     }
     __syncthreads();
-    analysis2(tb, Sa, Sb, F /* Tm scratch, 2 MU */, Ta + br * d.K, Tb + br * d.K);
+    analysis2(tb, qs, Sa, Sb, F /* Tm scratch, 2 MU */, Ta + br * d.K, Tb + br * d.K);
 }
 
 template <typename T>
@@ -436,19 +517,23 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     if (blocks == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (separated) {
-        size_t sh = sizeof(T) * (2 * d.UV + d.K + 2 * d.M * d.U);
+        size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + d.K + 2 * d.M * d.U);
         hipLaunchKernelGGL(k_receiver_separated<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s,
                            tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb);
         return hipGetLastError();
     }
-    size_t sh = sizeof(T) * (2 * d.UV + 2 * d.M * d.U);
+    size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + 2 * d.M * d.U);
     const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
     const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
 #define CGTP_RECV(RBV, NP)                                                                     \
     do {                                                                                       \
         int64_t nb = N * ((R + RBV - 1) / RBV);                                                \
-        hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP>), dim3((unsigned)nb), dim3(threads), sh, \
-                           s, tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb);                       \
+        if (R % RBV == 0)                                                                      \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true>), dim3((unsigned)nb),       \
+                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb); \
+        else                                                                                   \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false>), dim3((unsigned)nb),      \
+                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb); \
     } while (0)
     // ranks per block: sized so the per-thread accumulators and in-flight loads fit in
     // registers without spilling (fp64 values take two registers)

@@ -56,8 +56,11 @@ size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 // Largest dynamic LDS any kernel of the plan asks for, in bytes.
 size_t max_lds_bytes(const cgtp::Dims &d, size_t es)
 {
-    size_t onsite = es * (2 * d.K + 4 * (size_t)d.M * d.U + 2 * (size_t)d.UV);
-    size_t recv_sep = es * (2 * (size_t)d.UV + d.K + 2 * (size_t)d.M * d.U);
+    size_t qtab = (size_t)d.V * d.M;
+    size_t onsite = es * (2 * d.K + 4 * (size_t)d.M * d.U + 2 * (size_t)d.UV);  // q may stay global
+    size_t recv_sep = es * (qtab + 2 * (size_t)d.UV + d.K + 2 * (size_t)d.M * d.U);
+    size_t sender = es * (qtab + d.K + 2 * (size_t)d.M * d.U);
+    if (sender > recv_sep) recv_sep = sender;
     size_t m = onsite > recv_sep ? onsite : recv_sep;
     return m;
 }
@@ -223,13 +226,13 @@ int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const vo
     hipError_t e;
     // Eq. struct-H for both operands (shared when the operands coincide)
     e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UA, sl, R, 1, (const T *)A, HA,
-                                 nullptr, s);
+                                 (int64_t)R * d.K, d.K, 1, nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "contract A");
     rec.mark();
     const T *HBp = HA;
     if (!(A == B && UA == UB)) {
         e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UB, sl, R, 1, (const T *)B,
-                                     HB, nullptr, s);
+                                     HB, (int64_t)R * d.K, d.K, 1, nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "contract B");
         HBp = HB;
     }
@@ -240,13 +243,13 @@ int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const vo
     // Eq. struct-phi: out[b][n][k] = sum_r Uout[l][n][r] T[b][r][k]
     if (oe) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoe, sl, 1, R, Ta, (T *)oe,
-                                     nullptr, s);
+                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project even");
     }
     rec.mark();
     if (oo) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoo, sl, 1, R, Tb, (T *)oo,
-                                     nullptr, s);
+                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project odd");
     }
     rec.mark();
@@ -275,15 +278,16 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
     hipError_t e;
     // Eq. msgpass-HI, then the node-side forward transforms (Eqs. msgpass-FI, msgpass-AI)
     e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UI, sl, R, 1, (const T *)I, HI,
-                                 nullptr, s);
+                                 (int64_t)R * d.K, d.K, 1, nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "contract node features");
     rec.mark();
     e = cgtp::launch_sender_fields<T>(tb, N, R, HI, SF, s);
     if (e != hipSuccess) return hip_fail(e, "sender fields");
     rec.mark();
-    // Eq. msgpass-tildeR (zonal form folds in the addition-theorem weight (2l+1)/(4 pi))
+    // Eq. msgpass-tildeR into Rt [E][L][R] (the zonal form folds in the addition-theorem
+    // weight (2l+1)/(4 pi))
     e = cgtp::launch_contract<T>(E, C, R, d.L, true, (const T *)UE, sl, R, 1, (const T *)rad, Rt,
-                                 separated ? nullptr : tb.cl, s);
+                                 (int64_t)d.L * R, 1, R, separated ? nullptr : tb.cl, s);
     if (e != hipSuccess) return hip_fail(e, "contract edge radial");
     rec.mark();
     e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, SF, Ta,
@@ -292,13 +296,13 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
     rec.mark();
     if (oe) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoe, sl, 1, R, Ta, (T *)oe,
-                                     nullptr, s);
+                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project even");
     }
     rec.mark();
     if (oo) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoo, sl, 1, R, Tb, (T *)oo,
-                                     nullptr, s);
+                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
         if (e != hipSuccess) return hip_fail(e, "project odd");
     }
     rec.mark();
