@@ -20,6 +20,8 @@ struct Dims {
     int U;     // Gauss-Legendre nodes in x = cos(theta)
     int V;     // equispaced phi nodes
     int UV;    // U * V grid points
+    int UVs;   // row stride of stored grid fields: UV rounded up to 32 elements, so every
+               // row starts on a 128-byte line
 };
 
 bool resolve_grid(int lmax, int n_theta, int n_phi, int *U, int *V);
@@ -77,7 +79,7 @@ hipError_t launch_contract<double>(int64_t, int, int, int, bool, const double *,
                                    const double *, hipStream_t);
 
 // Node-side synthesis of the three grid fields (A, dA/dx, dA/dphi) of H[b][r][K]:
-// SF[b][r][3][UV] (Eqs. struct-F, struct-tildeA plus the derivative passes).
+// SF[b][r][3][UVs] (Eqs. struct-F, struct-tildeA plus the derivative passes).
 template <typename T>
 hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H, T *SF,
                                 hipStream_t s);

@@ -2,8 +2,9 @@
 // surface curl, the message-passing receiver pass and the quadrature analysis.
 // Templated on the scalar type (fp32, fp64).
 //
-// Layouts (row-major): coefficients [b][c][K]; grid fields [b][r][f][UV] with
-// UV = u * V + v; azimuthal index mi = m + lmax.
+// Layouts (row-major): coefficients [b][c][K]; stored grid fields [b][r][f][UVs]
+// with point index u * V + v and rows padded to UVs (a multiple of 32 elements);
+// azimuthal index mi = m + lmax.
 #include "internal.h"
 
 namespace cgtp {
@@ -133,16 +134,16 @@ __global__ __launch_bounds__(kThreads) void k_sender_fields(Tabs<T> tb, int R, i
     __syncthreads();
     for (int q = 0; q < nr; ++q) legendre_synth(tb, Hs + q * d.K, F + q * MU, Fx + q * MU);
     __syncthreads();
-    T *out = SF + (b * R + r0) * 3 * (int64_t)d.UV;
+    T *out = SF + (b * R + r0) * 3 * (int64_t)d.UVs;
     for (int uv = threadIdx.x; uv < d.UV; uv += blockDim.x) {
         const int u = uv / d.V, v = uv - u * d.V;
         for (int q = 0; q < nr; ++q) {
             T a, ax, ap;
             fourier_point(tb, qs, F + q * MU, Fx + q * MU, u, v, a, ax, ap);
-            T *o = out + (int64_t)q * 3 * d.UV + uv;
+            T *o = out + (int64_t)q * 3 * d.UVs + uv;
             o[0] = a;
-            o[d.UV] = ax;
-            o[2 * d.UV] = ap;
+            o[d.UVs] = ax;
+            o[2 * d.UVs] = ap;
         }
     }
 }
@@ -342,9 +343,10 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
             load_unit(unit, e + 1, uxn, uyn, uzn);
         }
         const T *rt = Rt + (int64_t)e * L * R + r0;   // Rt[e][l][r0 + q] = rt[l * R + q]
+        const int UVs = d.UVs;
         const __amdgpu_buffer_rsrc_t sfr =
-            make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UV, (unsigned)(nr * 3 * UV * sizeof(T)));
-        const unsigned fstride = (unsigned)(UV * sizeof(T));
+            make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs, (unsigned)(nr * 3 * UVs * sizeof(T)));
+        const unsigned fstride = (unsigned)(UVs * sizeof(T));
 #pragma unroll
         for (int s = 0; s < NPT; ++s) {
             const int uv = uvs[s];
@@ -495,13 +497,13 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
         __syncthreads();
         legendre_synth(tb, Y, F, Fx);
         __syncthreads();
-        const T *sf = SF + (j * R + r) * 3 * (int64_t)d.UV;
+        const T *sf = SF + (j * R + r) * 3 * (int64_t)d.UVs;
         for (int uv = threadIdx.x; uv < d.UV; uv += blockDim.x) {
             int u = uv / d.V, v = uv - u * d.V;
             T a, ax, ap;
             fourier_point(tb, qs, F, Fx, u, v, a, ax, ap);
             Sa[uv] += a * sf[uv];
-            Sb[uv] += ap * sf[d.UV + uv] - ax * sf[2 * d.UV + uv];
+            Sb[uv] += ap * sf[d.UVs + uv] - ax * sf[2 * d.UVs + uv];
         }
     }
     __syncthreads();

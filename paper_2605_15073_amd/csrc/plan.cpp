@@ -81,12 +81,12 @@ Layout onsite_layout(const cgtp_plan_s *p, int64_t N)
     return l;
 }
 
-// Message-passing workspace: HI [N][R][K], SF [N][R][3][UV], Rt [E][R][L], Ta, Tb [N][R][K].
+// Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K].
 Layout mp_layout(const cgtp_plan_s *p, int64_t N, int64_t E)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
     size_t h = align256(es * (size_t)N * p->R * p->d.K);
-    size_t sf = align256(es * (size_t)N * p->R * 3 * p->d.UV);
+    size_t sf = align256(es * (size_t)N * p->R * 3 * p->d.UVs);
     size_t rt = align256(es * (size_t)E * p->R * p->d.L);
     Layout l{};
     l.off[0] = 0;

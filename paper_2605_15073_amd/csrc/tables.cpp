@@ -44,6 +44,7 @@ Dims make_dims(int lmax, int U, int V)
     d.U = U;
     d.V = V;
     d.UV = U * V;
+    d.UVs = (d.UV + 31) / 32 * 32;
     return d;
 }
 
