@@ -90,6 +90,12 @@ template <typename T>
 hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, const T *HB,
                               T *Ta, T *Tb, hipStream_t s);
 
+// fp32 on-site grid stage for lmax <= kOnsiteFoldedMaxL (onsite.hip); returns
+// hipErrorNotSupported above that.
+constexpr int kOnsiteFoldedMaxL = 14;
+hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
+                                const float *HB, float *Ta, float *Tb, hipStream_t s);
+
 // Message-passing receiver pass: per receiver, synthesise the edge fields, multiply
 // with the streamed sender fields, sum over the CSR row, then the inverse transforms.
 // Rt is the edge-radial contraction in the layout [E][L][R].

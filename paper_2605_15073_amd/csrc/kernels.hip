@@ -222,6 +222,12 @@ hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, 
 {
     int64_t blocks = B * R;
     if (blocks == 0) return hipSuccess;
+    if constexpr (sizeof(T) == 4) {
+        if (tb.d.lmax <= kOnsiteFoldedMaxL) {
+            hipError_t e = launch_onsite_folded(tb, B, R, HA, HB, Ta, Tb, s);
+            if (e != hipErrorNotSupported && e != hipErrorInvalidValue) return e;
+        }
+    }
     const size_t base = 2 * tb.d.K + 4 * tb.d.M * tb.d.U + 2 * tb.d.UV;
     const size_t with_q = base + tb.d.V * tb.d.M;
     const int q_in_lds = sizeof(T) * with_q <= 65536 ? 1 : 0;

@@ -1,0 +1,182 @@
+// On-site grid stage, fp32, lmax <= kOnsiteFoldedMaxL: one workgroup per
+// (node, block of rb ranks), one thread per (rank, Gauss-Legendre node u).
+//
+// A thread keeps the Legendre coefficients F[m] and dF/dx[m] of both operands in
+// registers (Eq. struct-F and its x-derivative pass), then sweeps the azimuth in
+// pairs (v, V - v): cos(m phi) is the same at both points and sin(m phi) changes
+// sign, so the cosine part C and the sine part S of each synthesised field
+// (Eq. struct-tildeA) give A(v) = C + S and A(V - v) = C - S. At both points it
+// forms the product (Eq. struct-S) and the surface curl (Eq. poisson-S2-x), and
+// accumulates the Fourier analysis (Eq. struct-Tmu) in registers with the same
+// pairing. The Gauss-Legendre analysis across u (Eq. struct-Tlm) goes through LDS.
+#include "internal.h"
+
+namespace cgtp {
+
+namespace {
+
+template <int LM>
+__global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, int rb,
+                                                       const float *__restrict__ HA,
+                                                       const float *__restrict__ HB,
+                                                       float *__restrict__ Ta,
+                                                       float *__restrict__ Tb)
+{
+    constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
+    extern __shared__ float smem[];
+    const int U = tb.d.U, V = tb.d.V;
+    float *qs = smem;              // [V][M]
+    float *ps = qs + V * M;        // [U][P]
+    float *dps = ps + U * P;       // [U][P]
+    float *Hs = dps + U * P;       // [2][rb][K]
+    float *Tm = Hs + 2 * rb * K;   // [rb][2][M][U]
+
+    const int nrb = (R + rb - 1) / rb;
+    const int64_t b = blockIdx.x / nrb;
+    const int r0 = (int)(blockIdx.x - b * nrb) * rb;
+    const int nr = (R - r0 < rb) ? (R - r0) : rb;
+    for (int k = threadIdx.x; k < V * M; k += blockDim.x) qs[k] = tb.q[k];
+    for (int k = threadIdx.x; k < U * P; k += blockDim.x) {
+        ps[k] = tb.p[k];
+        dps[k] = tb.dp[k];
+    }
+    const float *ha = HA + (b * R + r0) * (int64_t)K;
+    const float *hb = HB + (b * R + r0) * (int64_t)K;
+    for (int k = threadIdx.x; k < nr * K; k += blockDim.x) {
+        Hs[k] = ha[k];
+        Hs[rb * K + k] = hb[k];
+    }
+    __syncthreads();
+
+    const int q = threadIdx.x / U, u = threadIdx.x - q * U;
+    const bool active = q < nr;
+    if (active) {
+        float FA[M], FxA[M], FB[M], FxB[M];
+        const float *h1 = Hs + q * K, *h2 = Hs + (rb + q) * K;
+        const float *pu = ps + u * P, *dpu = dps + u * P;
+#pragma unroll
+        for (int mi = 0; mi < M; ++mi) {
+            const int m = mi - LM, am = m < 0 ? -m : m;
+            float f1 = 0.f, g1 = 0.f, f2 = 0.f, g2 = 0.f;
+#pragma unroll
+            for (int l = am; l <= LM; ++l) {
+                const float p = pu[l * (l + 1) / 2 + am], dp = dpu[l * (l + 1) / 2 + am];
+                const float c1 = h1[l * l + l + m], c2 = h2[l * l + l + m];
+                f1 += p * c1;
+                g1 += dp * c1;
+                f2 += p * c2;
+                g2 += dp * c2;
+            }
+            FA[mi] = f1;
+            FxA[mi] = g1;
+            FB[mi] = f2;
+            FxB[mi] = g2;
+        }
+        float TA[M], TB[M];
+#pragma unroll
+        for (int mi = 0; mi < M; ++mi) TA[mi] = TB[mi] = 0.f;
+        for (int v = 0; 2 * v <= V; ++v) {
+            const int pv = v == 0 ? 0 : V - v;
+            const bool paired = v != 0 && pv != v;
+            const float *qr = qs + v * M;
+            // cosine (C) and sine (S) parts of A, dA/dx, dA/dphi for both operands
+            float aC = FA[LM], aS = 0.f, axC = FxA[LM], axS = 0.f, apC = 0.f, apS = 0.f;
+            float bC = FB[LM], bS = 0.f, bxC = FxB[LM], bxS = 0.f, bpC = 0.f, bpS = 0.f;
+#pragma unroll
+            for (int k = 1; k <= LM; ++k) {
+                const float c = qr[LM + k], s = qr[LM - k];
+                const float kc = (float)k * c, ks = (float)k * s;
+                aC += c * FA[LM + k];
+                aS += s * FA[LM - k];
+                axC += c * FxA[LM + k];
+                axS += s * FxA[LM - k];
+                apC += kc * FA[LM - k];
+                apS -= ks * FA[LM + k];
+                bC += c * FB[LM + k];
+                bS += s * FB[LM - k];
+                bxC += c * FxB[LM + k];
+                bxS += s * FxB[LM - k];
+                bpC += kc * FB[LM - k];
+                bpS -= ks * FB[LM + k];
+            }
+            float sa0 = (aC + aS) * (bC + bS);
+            float sb0 = (apC + apS) * (bxC + bxS) - (axC + axS) * (bpC + bpS);
+            float sa1 = 0.f, sb1 = 0.f;
+            if (paired) {
+                sa1 = (aC - aS) * (bC - bS);
+                sb1 = (apC - apS) * (bxC - bxS) - (axC - axS) * (bpC - bpS);
+            }
+            const float saP = sa0 + sa1, saM = sa0 - sa1, sbP = sb0 + sb1, sbM = sb0 - sb1;
+            TA[LM] += saP;
+            TB[LM] += sbP;
+#pragma unroll
+            for (int k = 1; k <= LM; ++k) {
+                const float c = qr[LM + k], s = qr[LM - k];
+                TA[LM + k] += c * saP;
+                TA[LM - k] += s * saM;
+                TB[LM + k] += c * sbP;
+                TB[LM - k] += s * sbM;
+            }
+        }
+        float *tm = Tm + q * 2 * M * U;
+#pragma unroll
+        for (int mi = 0; mi < M; ++mi) {
+            tm[mi * U + u] = TA[mi];
+            tm[(M + mi) * U + u] = TB[mi];
+        }
+    }
+    __syncthreads();
+    // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
+    for (int idx = threadIdx.x; idx < 2 * nr * K; idx += blockDim.x) {
+        const int which = idx / (nr * K);
+        const int rem = idx - which * nr * K;
+        const int qq = rem / K, k = rem - qq * K;
+        int l = (int)sqrtf((float)k);
+        while (l * l > k) --l;
+        while ((l + 1) * (l + 1) <= k) ++l;
+        const int m = k - l * l - l, am = m < 0 ? -m : m;
+        const float *tm = Tm + (qq * 2 + which) * M * U + (m + LM) * U;
+        const int pi = l * (l + 1) / 2 + am;
+        float s = 0.f;
+        for (int uu = 0; uu < U; ++uu) s += tb.wq[uu] * ps[uu * P + pi] * tm[uu];
+        (which ? Tb : Ta)[(b * R + r0 + qq) * (int64_t)K + k] = s;
+    }
+}
+
+template <int LM>
+hipError_t launch_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
+                         const float *HB, float *Ta, float *Tb, hipStream_t s)
+{
+    constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
+    const int U = tb.d.U, V = tb.d.V;
+    int rb = 256 / U;
+    if (rb > R) rb = R;
+    if (rb < 1) return hipErrorInvalidValue;
+    auto lds = [&](int r) { return sizeof(float) * (V * M + 2 * U * P + 2 * r * K + r * 2 * M * U); };
+    while (rb > 1 && lds(rb) > 65536) --rb;
+    if (lds(rb) > 65536) return hipErrorInvalidValue;
+    const int threads = (rb * U + 63) / 64 * 64;
+    const int64_t blocks = B * ((R + rb - 1) / rb);
+    hipLaunchKernelGGL((k_onsite_folded<LM>), dim3((unsigned)blocks), dim3(threads), lds(rb), s,
+                       tb, R, rb, HA, HB, Ta, Tb);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
+                                const float *HB, float *Ta, float *Tb, hipStream_t s)
+{
+    if (B == 0) return hipSuccess;
+    switch (tb.d.lmax) {
+#define CGTP_CASE(LMV) \
+    case LMV: return launch_folded<LMV>(tb, B, R, HA, HB, Ta, Tb, s);
+        CGTP_CASE(0) CGTP_CASE(1) CGTP_CASE(2) CGTP_CASE(3) CGTP_CASE(4) CGTP_CASE(5)
+        CGTP_CASE(6) CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11)
+        CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
+#undef CGTP_CASE
+    default: return hipErrorNotSupported;
+    }
+}
+
+}  // namespace cgtp
