@@ -66,9 +66,17 @@ size_t max_lds_bytes(const cgtp::Dims &d, size_t es)
 }
 
 struct Layout {
-    size_t off[5];
+    size_t off[6];
     size_t total;
 };
+
+// Receiver on MFMA: fp32, zonal edge field, R a multiple of 16, lmax high enough that the
+// per-thread recurrence sums would make the SIMT receiver compute-bound.
+bool use_mfma_receiver(const cgtp_plan_s *p)
+{
+    return p->dtype == CGTP_F32 && !(p->flags & CGTP_EDGE_SEPARATED) &&
+           p->d.lmax >= cgtp::kMfmaRecvMinL && cgtp::receiver_mfma_supported(p->d, p->R);
+}
 
 // On-site workspace: HA, HB, Ta, Tb, each [N][R][K].
 Layout onsite_layout(const cgtp_plan_s *p, int64_t N)
@@ -81,20 +89,23 @@ Layout onsite_layout(const cgtp_plan_s *p, int64_t N)
     return l;
 }
 
-// Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K].
+// Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],
+// and, for the MFMA receiver, the summed grid fields S [N][R][2][UVs].
 Layout mp_layout(const cgtp_plan_s *p, int64_t N, int64_t E)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
     size_t h = align256(es * (size_t)N * p->R * p->d.K);
     size_t sf = align256(es * (size_t)N * p->R * 3 * p->d.UVs);
     size_t rt = align256(es * (size_t)E * p->R * p->d.L);
+    size_t sg = use_mfma_receiver(p) ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, p->R)) : 0;
     Layout l{};
     l.off[0] = 0;
     l.off[1] = h;
     l.off[2] = h + sf;
     l.off[3] = h + sf + rt;
     l.off[4] = 2 * h + sf + rt;
-    l.total = 3 * h + sf + rt;
+    l.off[5] = 3 * h + sf + rt;
+    l.total = 3 * h + sf + rt + sg;
     return l;
 }
 
@@ -290,10 +301,21 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
                                  (int64_t)d.L * R, 1, R, separated ? nullptr : tb.cl, s);
     if (e != hipSuccess) return hip_fail(e, "contract edge radial");
     rec.mark();
+    if constexpr (sizeof(T) == 4) {
+        if (use_mfma_receiver(p)) {
+            float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
+            e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt, SF, Sg,
+                                           Ta, Tb, s);
+            if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
+            rec.mark();
+            goto projections;
+        }
+    }
     e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, SF, Ta,
                                  Tb, s);
     if (e != hipSuccess) return hip_fail(e, "receiver");
     rec.mark();
+projections:
     if (oe) {
         e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoe, sl, 1, R, Ta, (T *)oe,
                                      (int64_t)C * d.K, d.K, 1, nullptr, s);
