@@ -104,6 +104,11 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
                            const T *Rt, const T *SF, T *Ta, T *Tb, hipStream_t s);
 
+// fp32 folded inverse transforms (folded.hip), lmax <= 24; hipErrorNotSupported when
+// the LDS staging does not fit.
+hipError_t launch_analysis_folded(const Tabs<float> &tb, int64_t B, int R, const float *S,
+                                  float *Ta, float *Tb, hipStream_t s);
+
 // fp32 receiver pass with the edge synthesis on MFMA (receiver_mfma.hip): writes the
 // summed grid fields to S [N][R][2][UVs] and then runs the inverse transforms into
 // Ta, Tb. Requires R % 16 == 0.

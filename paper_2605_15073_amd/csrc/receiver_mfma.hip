@@ -5,11 +5,13 @@
 // t_p = rhat_e . Omega_p (addition theorem; the (2l+1)/(4 pi) weights are folded
 // into Rt). Both are [16 ranks x L] x [L x 16 points] products, one
 // v_mfma_f32_16x16x4f32 per 4 degrees. A workgroup owns one receiver, 16 ranks
-// and 64 * TPW grid points (4 waves, TPW 16-point tiles per wave). Per edge every
-// thread runs the Legendre recurrence for one point into LDS (the B operand),
+// and 64 * TPW grid points (4 waves, TPW 16-point tiles per wave). Per edge the
+// first 64 * TPW threads run the Legendre recurrence, one point each, into LDS (the
+// B operand),
 // the wave multiplies, and each lane combines its 4 ranks x 1 point of a and g
 // with the streamed sender fields (Eqs. msgpass-S and cat-beta-curl), all in
-// registers. The summed grid fields go to S [N][R][2][UVs]; k_analysis_rows
+// registers. The summed grid fields go to S [N][R][2][UVs]; the folded analysis
+// (k_analysis_rows when it does not fit)
 // then runs the inverse transforms (Eqs. msgpass-Tmu, msgpass-Tlm).
 #include "internal.h"
 
@@ -68,7 +70,7 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
         Pl[k] = 0.f;
         Dl[k] = 0.f;
     }
-    // this thread's recurrence point
+    // this thread's recurrence point (threads tid < PC)
     const int pr = p0 + tid;
     const int prc = pr < UV ? pr : 0;
     const int ur = prc / d.V, vr = prc - ur * d.V;
@@ -114,7 +116,7 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
             A[kk] = (kk < KS && l <= lmax) ? rte[l * R] : 0.f;
         }
         __syncthreads();  // previous edge done with Pl / Dl
-        {
+        if (tid < PC) {
             const float h = ux * rcp + uy * rsp;
             const float t = uz * rx + rsx * h;
             float p0v = 1.f, p1v = t, d1 = 1.f;
@@ -245,7 +247,7 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
-    constexpr int TPW = 4, PC = 64 * TPW;
+    constexpr int TPW = 2, PC = 64 * TPW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
     const int64_t blocks = N * (R / kRT) * nchunks;
@@ -255,6 +257,8 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
                        nchunks, row_ptr, col, unit, Rt, SF, S);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    e = launch_analysis_folded(tb, N, R, S, Ta, Tb, s);
+    if (e != hipErrorNotSupported) return e;
     int rb = 8;
     if (rb > R) rb = R;
     const size_t sh2 = sizeof(float) * (d.V * d.M + 2 * d.UV + 2 * d.M * d.U);
