@@ -3,12 +3,12 @@
 // For an edge e the zonal edge field and its t-derivative at grid point p are
 //   a[r][p] = sum_l Rt[e][l][r] P_l(t_p),   g[r][p] = sum_l Rt[e][l][r] P_l'(t_p),
 // t_p = rhat_e . Omega_p (addition theorem; the (2l+1)/(4 pi) weights are folded
-// into Rt). Both are [16 ranks x L] x [L x 16 points] products, one
+// into Rt). Both are [16 points x L] x [L x 16 ranks] products, one
 // v_mfma_f32_16x16x4f32 per 4 degrees. A workgroup owns one receiver, 16 ranks
-// and 64 * TPW grid points (4 waves, TPW 16-point tiles per wave). Per edge the
-// first 64 * TPW threads run the Legendre recurrence, one point each, into LDS (the
-// B operand),
-// the wave multiplies, and each lane combines its 4 ranks x 1 point of a and g
+// and 64 * TPW grid points (4 waves, TPW 16-point tiles per wave). Each wave is
+// self-contained: per edge it runs the Legendre recurrence for its own 16 * TPW
+// points into wave-private LDS (the B operand; lanes split P and P'), multiplies,
+// and each lane combines its 4 points x 1 rank of a and g
 // with the streamed sender fields (Eqs. msgpass-S and cat-beta-curl), all in
 // registers. The summed grid fields go to S [N][R][2][UVs]; the folded analysis
 // (k_analysis_rows when it does not fit)
@@ -32,9 +32,25 @@ __device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t rs, unsigned voff,
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0));
 }
 
-constexpr int kRT = 16;  // ranks per workgroup (MFMA rows)
+__device__ __forceinline__ float4_t bload4(__amdgpu_buffer_rsrc_t rs, unsigned voff, unsigned soff)
+{
+    return __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
+}
 
-template <int TPW>
+constexpr int kRT = 16;  // ranks per workgroup (MFMA columns)
+
+// Wave-scope ordering of LDS writes before reads by other lanes of the same wave
+// (LDS operations of a wave complete in order; the fences keep the compiler from
+// moving accesses across).
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// LM is lmax: the recurrence is unrolled with compile-time coefficients.
+template <int TPW, int LM>
 __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
                                                        const int32_t *__restrict__ row_ptr,
                                                        const int32_t *__restrict__ col,
@@ -43,15 +59,23 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
                                                        const float *__restrict__ SF,
                                                        float *__restrict__ S)
 {
-    constexpr int PC = 64 * TPW;  // grid points per workgroup
+    constexpr int PW = 16 * TPW;  // grid points per wave
+    constexpr int PC = 4 * PW;    // grid points per workgroup
+    constexpr int L = LM + 1;
+    constexpr int KS = (L + 3) / 4;  // K steps of 4 degrees
+    // LDS row stride: rows of the 4 lane groups land in different bank halves
+    constexpr int RS = PW + 16;
     const Dims &d = tb.d;
-    const int UV = d.UV, UVs = d.UVs, L = d.L, lmax = d.lmax;
-    const int KS = (L + 3) / 4;  // K steps of 4 degrees
+    const int UV = d.UV, UVs = d.UVs;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, n = lane & 15;
+    // wave-private LDS: P_l and P_l' at the wave's points, then dt/dx and dt/dphi
     extern __shared__ float smem[];
-    float *Pl = smem;                 // [4 KS][PC]  P_l(t_p)
-    float *Dl = Pl + 4 * KS * PC;     // [4 KS][PC]  P_l'(t_p)
-    float *dxs = Dl + 4 * KS * PC;    // [PC] dt/dx
-    float *dps = dxs + PC;            // [PC] dt/dphi
+    constexpr int wstride = 2 * 4 * KS * RS + 2 * PW;
+    float *Pl = smem + wave * wstride;  // [4 KS][RS]
+    float *Dl = Pl + 4 * KS * RS;       // [4 KS][RS]
+    float *dxs = Dl + 4 * KS * RS;      // [PW]
+    float *dps = dxs + PW;              // [PW]
 
     // XCD-aware order: the blocks of one receiver share an XCD (block b runs on XCD b % 8)
     const int64_t nblk = gridDim.x, per = nblk / 8, rem = nblk % 8;
@@ -61,115 +85,117 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
     const int64_t i = lb / ((int64_t)nrt * nchunks);
     const int rest = (int)(lb - i * (int64_t)nrt * nchunks);
     const int r0 = (rest / nchunks) * kRT;
-    const int p0 = (rest % nchunks) * PC;
+    const int pw0 = (rest % nchunks) * PC + wave * PW;  // first point of this wave
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int g = lane >> 4, n = lane & 15;
-    // degrees beyond lmax stay zero in the B operand
-    for (int k = tid; k < 4 * KS * PC; k += 256) {
-        Pl[k] = 0.f;
-        Dl[k] = 0.f;
-    }
-    // this thread's recurrence point (threads tid < PC)
-    const int pr = p0 + tid;
+    // degrees beyond lmax stay zero in the A operand
+    for (int k = lane; k < 2 * 4 * KS * RS; k += 64) Pl[k] = 0.f;
+    // recurrence point of this lane: lanes 0..PW-1 write P, lanes PW..2PW-1 write P'
+    const int rl = lane % PW;
+    const bool wr_p = lane < PW, wr_d = lane >= PW && lane < 2 * PW;
+    const int pr = pw0 + rl;
     const int prc = pr < UV ? pr : 0;
     const int ur = prc / d.V, vr = prc - ur * d.V;
     const float rx = tb.x[ur], rsx = tb.sx[ur], rxsx = tb.xsx[ur], rcp = tb.cphi[vr],
                 rsp = tb.sphi[vr];
 
+    // D[row = point 4 g + j][col = rank n]: a lane holds 4 consecutive points of one
+    // rank, so its sender values are 16-byte loads and its S values 16-byte stores.
     float4_t sa[TPW], sb[TPW];
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
         sa[t] = float4_t{0.f, 0.f, 0.f, 0.f};
         sb[t] = float4_t{0.f, 0.f, 0.f, 0.f};
     }
-    // lane's points: p0 + (wave * TPW + t) * 16 + n; lane's ranks: r0 + 4 g + jj
-    const int pl0 = (wave * TPW) * 16 + n;  // local index of tile 0
-    const unsigned voff = (unsigned)((12 * g * UVs + p0 + pl0) * 4);
+    // lane's points: pw0 + 16 t + 4 g + (0..3); lane's rank: r0 + n
+    const unsigned voff = (unsigned)((n * 3 * UVs + pw0 + 4 * g) * 4);
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     for (int e = e0; e < e1; ++e) {
         const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
-        // sender rank block [16][3][UVs], read with one VGPR offset per lane
+        // sender rank block [16][3][UVs]
         const __amdgpu_buffer_rsrc_t sfr =
             rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs, (unsigned)(kRT * 3 * UVs * 4));
-        float fI[TPW][4], fX[TPW][4], fP[TPW][4];
+        float4_t fI[TPW], fX[TPW], fP[TPW];
 #pragma unroll
-        for (int t = 0; t < TPW; ++t)
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const unsigned so = (unsigned)(((jj * 3) * UVs + t * 16) * 4);
-                fI[t][jj] = bload(sfr, voff, so);
-                fX[t][jj] = bload(sfr, voff, so + UVs * 4);
-                fP[t][jj] = bload(sfr, voff, so + 2 * UVs * 4);
-            }
+        for (int t = 0; t < TPW; ++t) {
+            const unsigned so = (unsigned)(t * 16 * 4);
+            fI[t] = bload4(sfr, voff, so);
+            fX[t] = bload4(sfr, voff, so + UVs * 4);
+            fP[t] = bload4(sfr, voff, so + 2 * UVs * 4);
+        }
         float ux = unit[3 * (int64_t)e], uy = unit[3 * (int64_t)e + 1], uz = unit[3 * (int64_t)e + 2];
         const float inv = 1.f / sqrtf(ux * ux + uy * uy + uz * uz);
         ux *= inv;
         uy *= inv;
         uz *= inv;
-        // A operand: Rt[e][4 kk + g][r0 + n]
+        // B operand: Rt[e][4 kk + g][r0 + n]
         const float *rte = Rt + (int64_t)e * L * R + r0 + n;
-        float A[8];
+        float Bv[KS];
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
+        for (int kk = 0; kk < KS; ++kk) {
             const int l = 4 * kk + g;
-            A[kk] = (kk < KS && l <= lmax) ? rte[l * R] : 0.f;
+            Bv[kk] = l <= LM ? rte[l * R] : 0.f;
         }
-        __syncthreads();  // previous edge done with Pl / Dl
-        if (tid < PC) {
+        wave_sync();  // this wave is done reading the previous edge's P, P'
+        {
             const float h = ux * rcp + uy * rsp;
             const float t = uz * rx + rsx * h;
             float p0v = 1.f, p1v = t, d1 = 1.f;
-            Pl[tid] = 1.f;
-            Dl[tid] = 0.f;
-            if (lmax >= 1) {
-                Pl[PC + tid] = t;
-                Dl[PC + tid] = 1.f;
+            if (wr_p) Pl[rl] = 1.f;
+            if (wr_d) Dl[rl] = 0.f;
+            if (LM >= 1) {
+                if (wr_p) Pl[RS + rl] = t;
+                if (wr_d) Dl[RS + rl] = 1.f;
             }
-            for (int l = 2; l <= lmax; ++l) {
-                const float p2 = tb.rc1[l] * t * p1v - tb.rc2[l] * p0v;
+#pragma unroll
+            for (int l = 2; l <= LM; ++l) {
+                const float c1 = (float)(2 * l - 1) / (float)l, c2 = (float)(l - 1) / (float)l;
+                const float p2 = c1 * t * p1v - c2 * p0v;
                 const float d2 = (float)l * p1v + t * d1;
-                Pl[l * PC + tid] = p2;
-                Dl[l * PC + tid] = d2;
+                if (wr_p) Pl[l * RS + rl] = p2;
+                if (wr_d) Dl[l * RS + rl] = d2;
                 p0v = p1v;
                 p1v = p2;
                 d1 = d2;
             }
-            dxs[tid] = uz - rxsx * h;
-            dps[tid] = rsx * (uy * rcp - ux * rsp);
+            if (wr_p) dxs[rl] = uz - rxsx * h;
+            if (wr_d) dps[rl] = rsx * (uy * rcp - ux * rsp);
         }
-        __syncthreads();
+        wave_sync();
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
-            const int pl = pl0 + 16 * t;
+            // A operand: P_{4 kk + g}(t_p) at point p = 16 t + n (rows are points)
             float4_t a = float4_t{0.f, 0.f, 0.f, 0.f}, gg = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kk = 0; kk < 8; ++kk) {
-                if (kk < KS) {
-                    const float bp = Pl[(4 * kk + g) * PC + pl];
-                    const float bd = Dl[(4 * kk + g) * PC + pl];
-                    a = __builtin_amdgcn_mfma_f32_16x16x4f32(A[kk], bp, a, 0, 0, 0);
-                    gg = __builtin_amdgcn_mfma_f32_16x16x4f32(A[kk], bd, gg, 0, 0, 0);
-                }
+            for (int kk = 0; kk < KS; ++kk) {
+                const float ap = Pl[(4 * kk + g) * RS + 16 * t + n];
+                const float ad = Dl[(4 * kk + g) * RS + 16 * t + n];
+                a = __builtin_amdgcn_mfma_f32_16x16x4f32(ap, Bv[kk], a, 0, 0, 0);
+                gg = __builtin_amdgcn_mfma_f32_16x16x4f32(ad, Bv[kk], gg, 0, 0, 0);
             }
-            const float dxt = dxs[pl], dpt = dps[pl];
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
+                const int pl = 16 * t + 4 * g + jj;
+                const float dxt = dxs[pl], dpt = dps[pl];
                 sa[t][jj] += a[jj] * fI[t][jj];
                 sb[t][jj] += gg[jj] * (dpt * fX[t][jj] - dxt * fP[t][jj]);
             }
         }
     }
-    // S[i][r0 + 4 g + jj][0 / 1][p]
+    // S[i][r0 + n][0 / 1][p .. p + 3]
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
-        const int p = p0 + pl0 + 16 * t;
-        if (p >= UV) continue;
+        const int p = pw0 + 16 * t + 4 * g;
+        float *o = S + ((i * R + r0 + n) * 2) * (int64_t)UVs + p;
+        if (p + 3 < UV) {
+            *reinterpret_cast<float4_t *>(o) = sa[t];
+            *reinterpret_cast<float4_t *>(o + UVs) = sb[t];
+        } else {
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            float *o = S + ((i * R + r0 + 4 * g + jj) * 2) * (int64_t)UVs + p;
-            o[0] = sa[t][jj];
-            o[UVs] = sb[t][jj];
+            for (int jj = 0; jj < 4; ++jj)
+                if (p + jj < UV) {
+                    o[jj] = sa[t][jj];
+                    o[UVs + jj] = sb[t][jj];
+                }
         }
     }
 }
@@ -247,14 +273,24 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
-    constexpr int TPW = 2, PC = 64 * TPW;
+    constexpr int TPW = 2, PW = 16 * TPW, PC = 4 * PW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
     const int64_t blocks = N * (R / kRT) * nchunks;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    const size_t sh = sizeof(float) * (2 * 4 * KS * PC + 2 * PC);
-    hipLaunchKernelGGL(k_receiver_mfma<TPW>, dim3((unsigned)blocks), dim3(256), sh, s, tb, R,
-                       nchunks, row_ptr, col, unit, Rt, SF, S);
+    const size_t sh = sizeof(float) * 4 * (2 * 4 * KS * (PW + 16) + 2 * PW);
+    switch (d.lmax) {
+#define CGTP_CASE(LMV)                                                                          \
+    case LMV:                                                                                   \
+        hipLaunchKernelGGL((k_receiver_mfma<TPW, LMV>), dim3((unsigned)blocks), dim3(256), sh, s, \
+                           tb, R, nchunks, row_ptr, col, unit, Rt, SF, S);                      \
+        break;
+        CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11) CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
+        CGTP_CASE(15) CGTP_CASE(16) CGTP_CASE(17) CGTP_CASE(18) CGTP_CASE(19) CGTP_CASE(20)
+        CGTP_CASE(21) CGTP_CASE(22) CGTP_CASE(23) CGTP_CASE(24)
+#undef CGTP_CASE
+    default: return hipErrorNotSupported;
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = launch_analysis_folded(tb, N, R, S, Ta, Tb, s);
