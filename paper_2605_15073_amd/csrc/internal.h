@@ -50,6 +50,9 @@ struct Tabs {
     const T *ya;    // [P] normalised-Legendre recurrence factor a_lm (edge SH)
     const T *yb;    // [P] normalised-Legendre recurrence factor b_lm (edge SH)
     const T *ymm;   // [L] sqrt((2m+1)/(2m)) diagonal step (edge SH), ymm[0] = 1/sqrt(4 pi)
+    const T *pt;    // [P][Ut] p transposed, Ut = U rounded up to 4, zero padded
+    const T *dpt;   // [P][Ut] dp transposed
+    const T *wpt;   // [P][Ut] wq[u] * p transposed (Gauss-Legendre analysis weights)
     Dims d;
 };
 
@@ -108,6 +111,15 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
 // the LDS staging does not fit.
 hipError_t launch_analysis_folded(const Tabs<float> &tb, int64_t B, int R, const float *S,
                                   float *Ta, float *Tb, hipStream_t s);
+
+// fp32 azimuthal transforms on MFMA (fourier_mfma.hip): the sender-field synthesis
+// (same output as launch_sender_fields) and the inverse transforms of S [N][R][2][UVs]
+// into Ta, Tb. hipErrorNotSupported when the grid is wider than their tiling
+// (V > 80) or the LDS staging does not fit.
+hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
+                              hipStream_t s);
+hipError_t launch_analysis_mfma(const Tabs<float> &tb, int64_t B, int R, const float *S,
+                                float *Ta, float *Tb, hipStream_t s);
 
 // fp32 receiver pass with the edge synthesis on MFMA (receiver_mfma.hip): writes the
 // summed grid fields to S [N][R][2][UVs] and then runs the inverse transforms into

@@ -153,6 +153,10 @@ hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H,
                                 hipStream_t s)
 {
     if (B == 0) return hipSuccess;
+    if constexpr (sizeof(T) == 4) {
+        hipError_t e = launch_sender_mfma(tb, B, R, H, SF, s);
+        if (e != hipErrorNotSupported) return e;
+    }
     const size_t per_rank = tb.d.K + 2 * (size_t)tb.d.M * tb.d.U;
     const size_t fixed = (size_t)tb.d.V * tb.d.M;
     int rb = (int)((48 * 1024 / sizeof(T) - fixed) / per_rank);
@@ -301,13 +305,13 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     const Dims &d = tb.d;
     const int UV = d.UV, L = d.L, lmax = d.lmax;
     const int nrb = (R + RB - 1) / RB;
-    // The rank blocks of one receiver read the same edge coefficient lines: keep them on
-    // one XCD (block b runs on XCD b % 8) by giving each XCD a contiguous range.
-    const int64_t nblk = gridDim.x, per = nblk / 8, rem = nblk % 8;
-    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-    const int64_t lb = (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-    const int64_t i = lb / nrb;
-    const int r0 = (int)(lb - i * nrb) * RB;
+    // Block order: rank blocks in turn, and inside one, all receivers. Blocks in flight then
+    // read the same rank slice of the sender fields, which the memory-side cache keeps
+    // across receivers.
+    const int64_t NN = (int64_t)gridDim.x / nrb;
+    const int64_t c = blockIdx.x / NN;
+    const int64_t i = blockIdx.x - c * NN;
+    const int r0 = (int)c * RB;
     // FULL: R is a multiple of RB, so every rank of the block exists (no guards)
     const int nr = FULL ? RB : ((R - r0 < RB) ? (R - r0) : RB);
 

@@ -27,11 +27,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, unsigne
                                              0x00020000);
 }
 
-__device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t rs, unsigned voff, unsigned soff)
-{
-    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0));
-}
-
 __device__ __forceinline__ float4_t bload4(__amdgpu_buffer_rsrc_t rs, unsigned voff, unsigned soff)
 {
     return __builtin_bit_cast(float4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
@@ -77,13 +72,12 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
     float *dxs = Dl + 4 * KS * RS;      // [PW]
     float *dps = dxs + PW;              // [PW]
 
-    // XCD-aware order: the blocks of one receiver share an XCD (block b runs on XCD b % 8)
-    const int64_t nblk = gridDim.x, per = nblk / 8, rem = nblk % 8;
-    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-    const int64_t lb = (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-    const int nrt = R / kRT;
-    const int64_t i = lb / ((int64_t)nrt * nchunks);
-    const int rest = (int)(lb - i * (int64_t)nrt * nchunks);
+    // Block order: (rank tile, point chunk) slices run one after another, and inside a slice
+    // all receivers. Blocks in flight then read one slice of the sender fields, which the
+    // memory-side cache keeps across receivers.
+    const int64_t NN = (int64_t)gridDim.x / ((int64_t)(R / kRT) * nchunks);
+    const int rest = (int)(blockIdx.x / NN);
+    const int64_t i = blockIdx.x - (int64_t)rest * NN;
     const int r0 = (rest / nchunks) * kRT;
     const int pw0 = (rest % nchunks) * PC + wave * PW;  // first point of this wave
 
@@ -276,9 +270,9 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     constexpr int TPW = 2, PW = 16 * TPW, PC = 4 * PW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
+    const size_t sh = sizeof(float) * 4 * (2 * 4 * KS * (PW + 16) + 2 * PW);
     const int64_t blocks = N * (R / kRT) * nchunks;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    const size_t sh = sizeof(float) * 4 * (2 * 4 * KS * (PW + 16) + 2 * PW);
     switch (d.lmax) {
 #define CGTP_CASE(LMV)                                                                          \
     case LMV:                                                                                   \
@@ -293,6 +287,8 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    e = launch_analysis_mfma(tb, N, R, S, Ta, Tb, s);
+    if (e != hipErrorNotSupported) return e;
     e = launch_analysis_folded(tb, N, R, S, Ta, Tb, s);
     if (e != hipErrorNotSupported) return e;
     int rb = 8;

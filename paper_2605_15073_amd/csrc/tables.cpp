@@ -160,9 +160,13 @@ static void region_sizes(const Dims &d, size_t *n)
     n[12] = d.P;                // ya
     n[13] = d.P;                // yb
     n[14] = d.L;                // ymm
+    const size_t ut = (size_t)(d.U + 3) / 4 * 4;
+    n[15] = (size_t)d.P * ut;   // pt
+    n[16] = (size_t)d.P * ut;   // dpt
+    n[17] = (size_t)d.P * ut;   // wpt
 }
 
-static const int kRegions = 15;
+static const int kRegions = 18;
 
 static size_t round_up(size_t n) { return (n + 63) & ~(size_t)63; }  // 512 B for fp64
 
@@ -204,6 +208,15 @@ void fill_tables(const Dims &d, double *h)
         h[off[11] + l] = l > 0 ? (l - 1.0) / l : 0.0;
         h[off[14] + l] = l == 0 ? 1.0 / std::sqrt(4.0 * kPi) : std::sqrt((2.0 * l + 1.0) / (2.0 * l));
     }
+    // transposed copies [P][Ut] (u fastest, rows zero padded to a multiple of 4)
+    const int ut = (d.U + 3) / 4 * 4;
+    for (int u = 0; u < d.U; ++u)
+        for (int i = 0; i < d.P; ++i) {
+            const double pv = h[off[4] + (size_t)u * d.P + i];
+            h[off[15] + (size_t)i * ut + u] = pv;
+            h[off[16] + (size_t)i * ut + u] = h[off[5] + (size_t)u * d.P + i];
+            h[off[17] + (size_t)i * ut + u] = h[off[3] + u] * pv;
+        }
     for (int l = 0; l <= d.lmax; ++l)
         for (int m = 0; m <= l; ++m) {
             int idx = l * (l + 1) / 2 + m;
@@ -246,6 +259,9 @@ Tabs<T> bind_tables(const Dims &d, const void *dev)
     tb.ya = ptr[12];
     tb.yb = ptr[13];
     tb.ymm = ptr[14];
+    tb.pt = ptr[15];
+    tb.dpt = ptr[16];
+    tb.wpt = ptr[17];
     tb.d = d;
     return tb;
 }
