@@ -18,6 +18,15 @@
 //   runs on MFMA and the Gauss-Legendre sum over u reads the weighted transposed
 //   Legendre table with 16-byte loads.
 //
+// k_onsite_mfma: the whole on-site grid stage for a node and rb ranks (Eqs. struct-F,
+//   struct-tildeA, struct-S, poisson-S2-x, struct-Tmu, struct-Tlm). The synthesis runs
+//   with the operands swapped, D[v][(q,u)] = sum_m q_vm F[(q,u)][m], so a lane ends up
+//   holding, for its row (q,u), the field values at v = 16 t + 4 g + j. Those are exactly
+//   the A operands the analysis product Tm[(q,u)][m] = sum_v S[(q,u)][v] q_vm needs when
+//   its reduction over v is visited in the order (t, j): the pointwise product and the
+//   surface curl are formed in registers and never leave the wave. Only Tm goes through
+//   LDS, for the Gauss-Legendre sum.
+//
 // MFMA 16x16x4 operand layout (wave64): lane = 16 g + n supplies A[row n][k g] and
 // B[k g][col n]; the result lane holds D[rows 4 g + j][col n], j = 0..3.
 #include "internal.h"
@@ -34,13 +43,25 @@ struct Grid {
     static constexpr int U = (3 * LM + 3) / 2 < 1 ? 1 : (3 * LM + 3) / 2;
     static constexpr int V = 3 * LM + 1;
     static constexpr int UV = U * V, UVs = (UV + 31) / 32 * 32;
-    static constexpr int Ut = (U + 3) / 4 * 4;        // row length of pt, dpt, wpt
-    static constexpr int KM = (M + 3) / 4;            // synthesis reduction steps over m
-    static constexpr int VT = (V + 15) / 16;          // synthesis column tiles over v
-    static constexpr int QW = VT * 16;
+    static constexpr int Ut = (U + 3) / 4 * 4;           // row length of pt, wpt
+    static constexpr int KM = (M + 3) / 4;               // synthesis reduction steps over m
+    static constexpr int VT = (V + 15) / 16;             // synthesis tiles over v
     static constexpr int KV = (V + 3) / 4, VP = 4 * KV;  // analysis reduction steps over v
-    static constexpr int VS = (VP + 31) / 32 * 32 + 2;  // LDS row stride: <= 2-way conflicts
-    static constexpr int MT = (M + 15) / 16, MW = MT * 16;  // analysis column tiles over m
+    static constexpr int MT = (M + 15) / 16, MW = MT * 16;  // analysis tiles over m
+    // coefficient rows with margins: orders of the padded reduction run over
+    // m = -lmax .. lmax + 3, so l^2 + l +- m stays in [-(lmax + 3), K + 2]
+    static constexpr int HL = LM + 3, HR = HL + K + 3;
+    // LDS row strides of the staged Fourier tables. A 64-lane LDS read is served in two
+    // halves of 32 lanes (n = 0..15, two lane groups g); each stride puts the two groups
+    // of a half on disjoint banks.
+    static constexpr int QB = (VT * 16 + 31) / 32 * 32 + 16;  // [m][v], read at g QB + n
+    static constexpr int QS = (MW + 31) / 32 * 32 + 2;        // [v][m], read at n QS + g
+                                                              // (and at 4 g QS + n: 2-way)
+    static constexpr int QM = (MW + 31) / 32 * 32 + 16;       // [v][m], read at g QM + n
+    static constexpr int VS = (VP + 31) / 32 * 32 + 2;        // staged S rows, read at n VS + g
+    // Tm rows [m][TS]: written at 16 mt + n (stride TS: 2-way), read as 16-byte words by
+    // consecutive m (stride TS / 4 words, odd: conflict-free)
+    static constexpr int TS = Ut + (Ut % 8 == 0 ? 4 : 0);
 };
 
 constexpr size_t kLdsTarget = 40 * 1024;  // keeps several workgroups resident per CU
@@ -54,6 +75,132 @@ int pick_rb(int R, size_t fixed, size_t per_rank)
     return rb;
 }
 
+// Workgroup size: one wave per 16-row tile, at most four.
+int waves_for(int rows)
+{
+    const int t = (rows + 15) / 16;
+    return t < 4 ? t : 4;
+}
+
+// Stages q_vm (zero padded) as table[i][j] with row stride ld, where (v, m) = (i, j) when
+// v_major, else (j, i).
+template <int LM>
+__device__ __forceinline__ void stage_q(const Tabs<float> &tb, float *table, int rows, int ld,
+                                        bool v_major)
+{
+    using G = Grid<LM>;
+    for (int k = threadIdx.x; k < rows * ld; k += blockDim.x) {
+        const int i = k / ld, j = k - i * ld;
+        const int v = v_major ? i : j, m = v_major ? j : i;
+        table[k] = (m < G::M && v < G::V) ? tb.q[v * G::M + m] : 0.f;
+    }
+}
+
+// Legendre recurrence coefficients per (l, m >= 0) pair, staged in LDS as
+// {a_lm, b_lm, c_lm, 0}: Pt_l = a (x Pt_{l-1} - b Pt_{l-2}) and
+// (1 - x^2) dPt_l/dx = c Pt_{l-1} - l x Pt_l.
+template <int LM>
+__device__ __forceinline__ void stage_coefs(const Tabs<float> &tb, float4_t *cf)
+{
+    constexpr int P = (LM + 1) * (LM + 2) / 2;
+    for (int k = threadIdx.x; k < P; k += blockDim.x)
+        cf[k] = float4_t{tb.ya[k], tb.yb[k], tb.yc[k], 0.f};
+}
+
+// Copies nr coefficient rows src[q][K] into margin-padded rows dst[q][HR] (margins zero).
+template <int LM>
+__device__ __forceinline__ void stage_rows(const float *src, float *dst, int nr)
+{
+    using G = Grid<LM>;
+    for (int k = threadIdx.x; k < nr * G::HR; k += blockDim.x) {
+        const int q = k / G::HR, i = k - q * G::HR - G::HL;
+        dst[k] = (i >= 0 && i < G::K) ? src[q * G::K + i] : 0.f;
+    }
+}
+
+// Legendre pass of one lane at reduction step KK (order m = 4 KK + g - lmax), for NOP
+// operands whose margin-padded coefficient rows start at h[o] (index 0 = (l, m) = (0, 0)):
+// fa = sum_l Pt_l^|m|(x) h[l, m], fx = the same with dPt/dx, fn = sum_l Pt_l^|m|(x) h[l, -m]
+// (Eq. msgpass-FI and its x-derivative). The functions come from the three-term recurrence
+// in l, started by adding seed = Pt_|m|^|m|(x) at l = |m| (seed 0 for the padding orders
+// |m| > lmax). Below l = |m| a lane carries zeros. The loop is unrolled from the lowest
+// |m| of the step, so every table offset is a constant.
+template <int LM, int KK, int NOP>
+__device__ __forceinline__ void legendre_step(const float4_t *cf, const float *const *h, float seed,
+                                              float x, float r, int m, float *fa, float *fx,
+                                              float *fn)
+{
+    constexpr int lo = 4 * KK - LM, hi = lo + 3;
+    constexpr int A0 = (lo <= 0 && hi >= 0) ? 0 : (lo > 0 ? lo : -hi);
+    const int am = m < 0 ? (-m < LM ? -m : LM) : (m < LM ? m : LM);
+    const float4_t *ca = cf + am;
+    float p1 = 0.f, p2 = 0.f;
+#pragma unroll
+    for (int l = A0; l <= LM; ++l) {
+        const float4_t c = ca[l * (l + 1) / 2];
+        const float inj = (l == am) ? seed : 0.f;
+        const float pv = c[0] * (x * p1 - c[1] * p2) + inj;
+        const float dv = (c[2] * p1 - (float)l * x * pv) * r;
+#pragma unroll
+        for (int o = 0; o < NOP; ++o) {
+            const float cp = h[o][l * l + l + m];
+            fa[o] += pv * cp;
+            fx[o] += dv * cp;
+            fn[o] += pv * h[o][l * l + l - m];
+        }
+        p2 = p1;
+        p1 = pv;
+    }
+}
+
+// Seeds Pt_|m|^|m|(x_u) of the KM reduction steps of one lane.
+template <int LM>
+__device__ __forceinline__ void load_seeds(const Tabs<float> &tb, int g4, int ua, float *seed)
+{
+    using G = Grid<LM>;
+#pragma unroll
+    for (int kk = 0; kk < G::KM; ++kk) {
+        const int m = 4 * kk + g4 - LM, am = m < 0 ? -m : m;
+        seed[kk] = am <= LM ? tb.pt[(am * (am + 1) / 2 + am) * G::Ut + ua] : 0.f;
+    }
+}
+
+// ---------------------------------------------------------------- sender fields
+
+// Legendre pass of all reduction steps of one lane for NOP operands: bf[kk][o][f] holds
+// F, dF/dx and m F[-m] (the d/dphi slot swap) of operand o at order m = 4 kk + g - lmax.
+template <int LM, int NOP>
+struct LaneRows {
+    const float4_t *cf;
+    const float *h[NOP];
+    const float *seed;
+    float x, r;
+    int g4;
+};
+
+template <int LM, int NOP, int KK>
+__device__ __forceinline__ void legendre_all(const LaneRows<LM, NOP> &c,
+                                             float (&bf)[Grid<LM>::KM][NOP][3])
+{
+    if constexpr (KK < Grid<LM>::KM) {
+        const int m = 4 * KK + c.g4 - LM;
+        float fa[NOP], fx[NOP], fn[NOP];
+#pragma unroll
+        for (int o = 0; o < NOP; ++o) fa[o] = fx[o] = fn[o] = 0.f;
+        legendre_step<LM, KK, NOP>(c.cf, c.h, c.seed[KK], c.x, c.r, m, fa, fx, fn);
+#pragma unroll
+        for (int o = 0; o < NOP; ++o) {
+            bf[KK][o][0] = fa[o];
+            bf[KK][o][1] = fx[o];
+            bf[KK][o][2] = (float)m * fn[o];
+        }
+        // keep the scheduler from hoisting the next step's loads over this one: the straight
+        // line code would otherwise hold every step's operands in registers at once
+        __builtin_amdgcn_sched_barrier(0);
+        legendre_all<LM, NOP, KK + 1>(c, bf);
+    }
+}
+
 template <int LM>
 __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int rb,
                                                      const float *__restrict__ H,
@@ -61,63 +208,54 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
 {
     using G = Grid<LM>;
     extern __shared__ float smem[];
-    float *qs = smem;                    // [4 KM][QW]: q_vm as [m][v], zero padded
-    float *Hs = qs + 4 * G::KM * G::QW;  // [rb][K]
+    float4_t *cf = reinterpret_cast<float4_t *>(smem);  // [P] recurrence coefficients
+    float *qs = smem + 4 * G::P;                         // [4 KM][QB]: q_vm as [m][v]
+    float *Hs = qs + 4 * G::KM * G::QB;                  // [rb][HR]
     const int nrb = (R + rb - 1) / rb;
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
-    const int tid = threadIdx.x;
-    for (int k = tid; k < 4 * G::KM * G::QW; k += 256) {
-        const int m = k / G::QW, v = k - m * G::QW;
-        qs[k] = (m < G::M && v < G::V) ? tb.q[v * G::M + m] : 0.f;
-    }
-    const float *h = H + (b * R + r0) * (int64_t)G::K;
-    for (int k = tid; k < nr * G::K; k += 256) Hs[k] = h[k];
+    stage_q<LM>(tb, qs, 4 * G::KM, G::QB, false);
+    stage_rows<LM>(H + (b * R + r0) * (int64_t)G::K, Hs, nr);
+    stage_coefs<LM>(tb, cf);
     __syncthreads();
 
-    const int lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, n = lane & 15;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int g4 = lane >> 4, n = lane & 15;
     const int rows = nr * G::U;
     const int rtiles = (rows + 15) / 16;
-    for (int rt = wave; rt < rtiles; rt += 4) {
-        const int ra = rt * 16 + n;  // this lane's A-operand row (q, u)
-        const bool ok = ra < rows;
-        const int qa = ok ? ra / G::U : 0, ua = ok ? ra - qa * G::U : 0;
-        const float *hq = Hs + qa * G::K;
-        const float *ptu = tb.pt + ua, *dptu = tb.dpt + ua;
+    for (int rt = wave; rt < rtiles; rt += nw) {
+        // this lane's A-operand row (q, u); rows past the end compute on row 0 and are
+        // never stored (a result row depends on its own A row only)
+        const int ra = rt * 16 + n;
+        const int qa = ra < rows ? ra / G::U : 0, ua = ra < rows ? ra - qa * G::U : 0;
+        float seed[G::KM];
+        load_seeds<LM>(tb, g4, ua, seed);
+        LaneRows<LM, 1> c;
+        c.cf = cf;
+        c.h[0] = Hs + qa * G::HR + G::HL;
+        c.seed = seed;
+        const float sxu = tb.sx[ua];
+        c.x = tb.x[ua];
+        c.r = 1.f / (sxu * sxu);
+        c.g4 = g4;
+        float bf[G::KM][1][3];
+        legendre_all<LM, 1, 0>(c, bf);
+        // Fourier pass: D[(q,u)][v] = sum_m F[(q,u)][m] q_vm, one v tile at a time
         float4_t acc[3][G::VT];
 #pragma unroll
-        for (int t = 0; t < G::VT; ++t)
+        for (int t = 0; t < G::VT; ++t) {
             acc[0][t] = acc[1][t] = acc[2][t] = float4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 1
-        for (int kk = 0; kk < G::KM; ++kk) {
-            const int m = 4 * kk + g4 - LM, am = m < 0 ? -m : m;
-            // lowest |m| over the four lane groups: the loop bound is wave-uniform
-            const int lo = 4 * kk - LM, hi = lo + 3;
-            const int am0 = (lo <= 0 && hi >= 0) ? 0 : (lo > 0 ? lo : -hi);
-            float fa = 0.f, fx = 0.f, fn = 0.f;
-#pragma unroll 4
-            for (int l = am0; l <= LM; ++l) {
-                if (l >= am) {  // also false for the padding orders |m| > lmax
-                    const int pi = l * (l + 1) / 2 + am;
-                    const float pv = ptu[pi * G::Ut], dv = dptu[pi * G::Ut];
-                    const float cp = hq[l * l + l + m], cn = hq[l * l + l - m];
-                    fa += pv * cp;
-                    fx += dv * cp;
-                    fn += pv * cn;
-                }
-            }
-            const float fp = ok ? (float)m * fn : 0.f;
-            if (!ok) fa = fx = 0.f;
-            const float *qr = qs + (4 * kk + g4) * G::QW + n;
 #pragma unroll
-            for (int t = 0; t < G::VT; ++t) {
-                const float bq = qr[t * 16];
-                acc[0][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa, bq, acc[0][t], 0, 0, 0);
-                acc[1][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fx, bq, acc[1][t], 0, 0, 0);
-                acc[2][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(fp, bq, acc[2][t], 0, 0, 0);
+            for (int kk = 0; kk < G::KM; ++kk) {
+                const float bq = qs[(4 * kk + g4) * G::QB + t * 16 + n];
+#pragma unroll
+                for (int f = 0; f < 3; ++f)
+                    acc[f][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[kk][0][f], bq, acc[f][t],
+                                                                     0, 0, 0);
             }
         }
+        // D[(q,u) = 16 rt + 4 g + j][v = 16 t + n]
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int ro = rt * 16 + 4 * g4 + j;
@@ -137,6 +275,8 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
     }
 }
 
+// ------------------------------------------------------ inverse transforms (MP)
+
 template <int LM>
 __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, int rb,
                                                        const float *__restrict__ S,
@@ -145,36 +285,34 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
 {
     using G = Grid<LM>;
     extern __shared__ float smem[];
-    float *qs = smem;                       // [VP][MW]: q_vm as [v][m], zero padded
-    float *Ss = qs + G::VP * G::MW;         // [rb U][VS]
-    float *Tm = Ss + (rb * G::U * G::VS + 3) / 4 * 4;  // [rb][M][Ut], 16-byte aligned
+    float *qs = smem;                                   // [VP][QM]: q_vm as [v][m]
+    float *Ss = qs + G::VP * G::QM;                     // [rb U][VS]
+    float *Tm = Ss + (rb * G::U * G::VS + 3) / 4 * 4;   // [rb][M][TS], 16-byte aligned
     const int nrb = (R + rb - 1) / rb;
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g4 = lane >> 4, n = lane & 15;
-    for (int k = tid; k < G::VP * G::MW; k += 256) {
-        const int v = k / G::MW, m = k - v * G::MW;
-        qs[k] = (m < G::M && v < G::V) ? tb.q[v * G::M + m] : 0.f;
-    }
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int lane = tid & 63, wave = tid >> 6, nw = nt >> 6, g4 = lane >> 4, n = lane & 15;
+    stage_q<LM>(tb, qs, G::VP, G::QM, true);
     const int rows = nr * G::U;
     const int rtiles = (rows + 15) / 16;
     constexpr int pad = G::VP - G::V;
     if (pad > 0)
-        for (int k = tid; k < rows * pad; k += 256) {
+        for (int k = tid; k < rows * pad; k += nt) {
             const int ro = k / pad;
             Ss[ro * G::VS + G::V + (k - ro * pad)] = 0.f;
         }
     constexpr int tpad = G::Ut - G::U;
     if (tpad > 0)
-        for (int k = tid; k < nr * G::M * tpad; k += 256) {
+        for (int k = tid; k < nr * G::M * tpad; k += nt) {
             const int ro = k / tpad;
-            Tm[ro * G::Ut + G::U + (k - ro * tpad)] = 0.f;
+            Tm[ro * G::TS + G::U + (k - ro * tpad)] = 0.f;
         }
     constexpr int R4 = G::UVs / 4;  // 16-byte words per stored row
     for (int which = 0; which < 2; ++which) {
         // stage rows (q, u) of S as Ss[q U + u][v]
-        for (int k = tid; k < nr * R4; k += 256) {
+        for (int k = tid; k < nr * R4; k += nt) {
             const int q = k / R4, r = 4 * (k - q * R4);
             if (r < G::UV) {
                 const float4_t x = *reinterpret_cast<const float4_t *>(
@@ -191,21 +329,20 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
             }
         }
         __syncthreads();
-        for (int rt = wave; rt < rtiles; rt += 4) {
+        for (int rt = wave; rt < rtiles; rt += nw) {
             const int ra = rt * 16 + n;
-            const bool ok = ra < rows;
-            const float *sa = Ss + (ok ? ra : 0) * G::VS + g4;
-            const float *qc = qs + g4 * G::MW + n;
+            const float *sa = Ss + (ra < rows ? ra : 0) * G::VS + g4;
+            const float *qc = qs + g4 * G::QM + n;
             float4_t acc[G::MT];
 #pragma unroll
             for (int t = 0; t < G::MT; ++t) acc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
+#pragma unroll
             for (int kk = 0; kk < G::KV; ++kk) {
-                const float av = ok ? sa[4 * kk] : 0.f;
+                const float av = sa[4 * kk];
 #pragma unroll
                 for (int t = 0; t < G::MT; ++t)
                     acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                        av, qc[4 * kk * G::MW + t * 16], acc[t], 0, 0, 0);
+                        av, qc[4 * kk * G::QM + t * 16], acc[t], 0, 0, 0);
             }
 #pragma unroll
             for (int t = 0; t < G::MT; ++t) {
@@ -216,7 +353,7 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
                         const int ro = rt * 16 + 4 * g4 + j;
                         if (ro < rows) {
                             const int qo = ro / G::U, uo = ro - qo * G::U;
-                            Tm[(qo * G::M + mi) * G::Ut + uo] = acc[t][j];
+                            Tm[(qo * G::M + mi) * G::TS + uo] = acc[t][j];
                         }
                     }
                 }
@@ -225,16 +362,14 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
         __syncthreads();
         // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
         float *out = which ? Tb : Ta;
-        for (int idx = tid; idx < nr * G::K; idx += 256) {
+        for (int idx = tid; idx < nr * G::K; idx += nt) {
             const int qq = idx / G::K, k = idx - qq * G::K;
-            int l = (int)sqrtf((float)k);
-            while (l * l > k) --l;
-            while ((l + 1) * (l + 1) <= k) ++l;
+            const int l = (int)sqrtf((float)k + 0.5f);  // exact for k < 2^20
             const int m = k - l * l - l, am = m < 0 ? -m : m;
             const float4_t *w4 =
                 reinterpret_cast<const float4_t *>(tb.wpt + (l * (l + 1) / 2 + am) * G::Ut);
             const float4_t *t4 =
-                reinterpret_cast<const float4_t *>(Tm + (qq * G::M + m + LM) * G::Ut);
+                reinterpret_cast<const float4_t *>(Tm + (qq * G::M + m + LM) * G::TS);
             float s = 0.f;
 #pragma unroll
             for (int c = 0; c < G::Ut / 4; ++c) {
@@ -247,18 +382,159 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
     }
 }
 
+// ------------------------------------------------------------- on-site grid stage
+
+template <int LM>
+__global__ __launch_bounds__(256) void k_onsite_mfma(Tabs<float> tb, int R, int rb,
+                                                     const float *__restrict__ HA,
+                                                     const float *__restrict__ HB,
+                                                     float *__restrict__ Ta,
+                                                     float *__restrict__ Tb)
+{
+    using G = Grid<LM>;
+    constexpr int QR = G::VT * 16;     // rows (v) of the staged Fourier tables
+    extern __shared__ float smem[];
+    float4_t *cf = reinterpret_cast<float4_t *>(smem);  // [P] recurrence coefficients
+    float *qs = smem + 4 * G::P;                         // [QR][QS]: q_vm as [v][m]
+    float *Hs = qs + QR * G::QS;                         // [2][rb][HR]
+    float *Tm = Hs + (2 * rb * G::HR + 3) / 4 * 4;       // [rb][2][M][TS], 16-byte aligned
+    const int nrb = (R + rb - 1) / rb;
+    const int64_t b = blockIdx.x / nrb;
+    const int r0 = (int)(blockIdx.x - b * nrb) * rb;
+    const int nr = (R - r0 < rb) ? (R - r0) : rb;
+    const int tid = threadIdx.x, nt = blockDim.x;
+    stage_q<LM>(tb, qs, QR, G::QS, true);
+    stage_rows<LM>(HA + (b * R + r0) * (int64_t)G::K, Hs, nr);
+    stage_rows<LM>(HB + (b * R + r0) * (int64_t)G::K, Hs + rb * G::HR, nr);
+    stage_coefs<LM>(tb, cf);
+    constexpr int tpad = G::Ut - G::U;
+    if (tpad > 0)
+        for (int k = tid; k < nr * 2 * G::M * tpad; k += nt) {
+            const int ro = k / tpad;
+            Tm[ro * G::TS + G::U + (k - ro * tpad)] = 0.f;
+        }
+    __syncthreads();
+
+    const int lane = tid & 63, wave = tid >> 6, nw = nt >> 6, g4 = lane >> 4, n = lane & 15;
+    const int rows = nr * G::U;
+    const int rtiles = (rows + 15) / 16;
+    for (int rt = wave; rt < rtiles; rt += nw) {
+        // this lane's row (q, u); rows past the end compute on row 0 and are never stored
+        const int ra = rt * 16 + n;
+        const int qa = ra < rows ? ra / G::U : 0, ua = ra < rows ? ra - qa * G::U : 0;
+        float seed[G::KM];
+        load_seeds<LM>(tb, g4, ua, seed);
+        LaneRows<LM, 2> c;
+        c.cf = cf;
+        c.h[0] = Hs + qa * G::HR + G::HL;
+        c.h[1] = Hs + (rb + qa) * G::HR + G::HL;
+        c.seed = seed;
+        const float sxu = tb.sx[ua];
+        c.x = tb.x[ua];
+        c.r = 1.f / (sxu * sxu);
+        c.g4 = g4;
+        float bf[G::KM][2][3];
+        legendre_all<LM, 2, 0>(c, bf);
+        // per v tile: synthesis with the operands swapped, D[v = 16 t + 4 g + j][(q,u) = n]
+        // for both operands and the three fields; the products S_alpha = A1 A2
+        // (Eq. struct-S) and S_beta = dA1/dphi dA2/dx - dA1/dx dA2/dphi (Eq. poisson-S2-x) at
+        // this lane's row; and their share of the analysis Tm[(q,u)][m] = sum_v S q_vm,
+        // whose reduction over v is visited as (t, j)
+        float4_t ta[G::MT], tbv[G::MT];
+#pragma unroll
+        for (int mt = 0; mt < G::MT; ++mt) ta[mt] = tbv[mt] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < G::VT; ++t) {
+            float4_t a[2][3];
+#pragma unroll
+            for (int f = 0; f < 3; ++f) a[0][f] = a[1][f] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kk = 0; kk < G::KM; ++kk) {
+                const float aq = qs[(t * 16 + n) * G::QS + 4 * kk + g4];
+#pragma unroll
+                for (int f = 0; f < 3; ++f) {
+                    a[0][f] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq, bf[kk][0][f], a[0][f], 0, 0, 0);
+                    a[1][f] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq, bf[kk][1][f], a[1][f], 0, 0, 0);
+                }
+            }
+            const float4_t sal = a[0][0] * a[1][0];
+            const float4_t sbe = a[0][2] * a[1][1] - a[0][1] * a[1][2];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float *qb = qs + (t * 16 + 4 * g4 + j) * G::QS + n;
+#pragma unroll
+                for (int mt = 0; mt < G::MT; ++mt) {
+                    const float bq = qb[mt * 16];
+                    ta[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(sal[j], bq, ta[mt], 0, 0, 0);
+                    tbv[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(sbe[j], bq, tbv[mt], 0, 0, 0);
+                }
+            }
+        }
+        // D[(q,u) = 16 rt + 4 g + j][m = 16 mt + n]
+#pragma unroll
+        for (int mt = 0; mt < G::MT; ++mt) {
+            const int mi = mt * 16 + n;
+            if (mi < G::M) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int ro = rt * 16 + 4 * g4 + j;
+                    if (ro < rows) {
+                        const int qo = ro / G::U, uo = ro - qo * G::U;
+                        Tm[((qo * 2) * G::M + mi) * G::TS + uo] = ta[mt][j];
+                        Tm[((qo * 2 + 1) * G::M + mi) * G::TS + uo] = tbv[mt][j];
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+    // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
+    for (int idx = tid; idx < 2 * nr * G::K; idx += nt) {
+        const int qf = idx / G::K, k = idx - qf * G::K;  // qf = 2 q + field
+        const int l = (int)sqrtf((float)k + 0.5f);        // exact for k < 2^20
+        const int m = k - l * l - l, am = m < 0 ? -m : m;
+        const float4_t *w4 =
+            reinterpret_cast<const float4_t *>(tb.wpt + (l * (l + 1) / 2 + am) * G::Ut);
+        const float4_t *t4 = reinterpret_cast<const float4_t *>(Tm + (qf * G::M + m + LM) * G::TS);
+        float sum = 0.f;
+#pragma unroll
+        for (int c = 0; c < G::Ut / 4; ++c) {
+            const float4_t w = w4[c], tv = t4[c];
+            sum += w[0] * tv[0] + w[1] * tv[1] + w[2] * tv[2] + w[3] * tv[3];
+        }
+        const int q = qf >> 1;
+        ((qf & 1) ? Tb : Ta)[(b * R + r0 + q) * (int64_t)G::K + k] = sum;
+    }
+}
+
+template <int LM>
+hipError_t onsite_lm(const Tabs<float> &tb, int64_t B, int R, const float *HA, const float *HB,
+                     float *Ta, float *Tb, hipStream_t s)
+{
+    using G = Grid<LM>;
+    const size_t fixed = 4 * (size_t)G::P + (size_t)G::VT * 16 * G::QS + 4;
+    const size_t per_rank = 2 * (size_t)G::HR + 2 * (size_t)G::M * G::TS;
+    const int rb = pick_rb(R, fixed, per_rank);
+    if (rb < 1) return hipErrorNotSupported;
+    const int64_t blocks = B * ((R + rb - 1) / rb);
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_onsite_mfma<LM>), dim3((unsigned)blocks), dim3(64 * waves_for(rb * G::U)),
+                       sizeof(float) * (fixed + rb * per_rank), s, tb, R, rb, HA, HB, Ta, Tb);
+    return hipGetLastError();
+}
+
 template <int LM>
 hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
                      hipStream_t s)
 {
     using G = Grid<LM>;
-    const size_t fixed = (size_t)4 * G::KM * G::QW;
-    const int rb = pick_rb(R, fixed, G::K);
+    const size_t fixed = 4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB;
+    const int rb = pick_rb(R, fixed, G::HR);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_sender_mfma<LM>), dim3((unsigned)blocks), dim3(256),
-                       sizeof(float) * (fixed + rb * (size_t)G::K), s, tb, R, rb, H, SF);
+    hipLaunchKernelGGL((k_sender_mfma<LM>), dim3((unsigned)blocks), dim3(64 * waves_for(rb * G::U)),
+                       sizeof(float) * (fixed + rb * (size_t)G::HR), s, tb, R, rb, H, SF);
     return hipGetLastError();
 }
 
@@ -267,14 +543,15 @@ hipError_t analysis_lm(const Tabs<float> &tb, int64_t B, int R, const float *S, 
                        float *Tb, hipStream_t s)
 {
     using G = Grid<LM>;
-    const size_t fixed = (size_t)G::VP * G::MW + 3;  // + alignment of the Tm region
-    const size_t per_rank = (size_t)G::U * G::VS + (size_t)G::M * G::Ut;
+    const size_t fixed = (size_t)G::VP * G::QM + 3;  // + alignment of the Tm region
+    const size_t per_rank = (size_t)G::U * G::VS + (size_t)G::M * G::TS;
     const int rb = pick_rb(R, fixed, per_rank);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_analysis_mfma<LM>), dim3((unsigned)blocks), dim3(256),
-                       sizeof(float) * (fixed + rb * per_rank), s, tb, R, rb, S, Ta, Tb);
+    hipLaunchKernelGGL((k_analysis_mfma<LM>), dim3((unsigned)blocks),
+                       dim3(64 * waves_for(rb * G::U)), sizeof(float) * (fixed + rb * per_rank), s,
+                       tb, R, rb, S, Ta, Tb);
     return hipGetLastError();
 }
 
@@ -298,6 +575,20 @@ hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
     switch (tb.d.lmax) {
 #define CGTP_CASE(LMV) \
     case LMV: return sender_lm<LMV>(tb, B, R, H, SF, s);
+        CGTP_LMAX_CASES(CGTP_CASE)
+#undef CGTP_CASE
+    default: return hipErrorNotSupported;
+    }
+}
+
+hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const float *HA,
+                              const float *HB, float *Ta, float *Tb, hipStream_t s)
+{
+    if (B == 0) return hipSuccess;
+    if (!default_grid(tb.d)) return hipErrorNotSupported;
+    switch (tb.d.lmax) {
+#define CGTP_CASE(LMV) \
+    case LMV: return onsite_lm<LMV>(tb, B, R, HA, HB, Ta, Tb, s);
         CGTP_LMAX_CASES(CGTP_CASE)
 #undef CGTP_CASE
     default: return hipErrorNotSupported;

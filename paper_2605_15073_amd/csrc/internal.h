@@ -53,6 +53,9 @@ struct Tabs {
     const T *pt;    // [P][Ut] p transposed, Ut = U rounded up to 4, zero padded
     const T *dpt;   // [P][Ut] dp transposed
     const T *wpt;   // [P][Ut] wq[u] * p transposed (Gauss-Legendre analysis weights)
+    const T *yc;    // [P] sqrt((2l+1)(l^2-m^2)/(2l-1)): (1-x^2) dPt_l^m/dx
+                    //     = yc Pt_{l-1}^m - l x Pt_l^m
+
     Dims d;
 };
 
@@ -120,6 +123,12 @@ hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
                               hipStream_t s);
 hipError_t launch_analysis_mfma(const Tabs<float> &tb, int64_t B, int R, const float *S,
                                 float *Ta, float *Tb, hipStream_t s);
+// fp32 on-site grid stage on MFMA (fourier_mfma.hip), default grid only: the same
+// contract as launch_onsite_grid. Used from kOnsiteMfmaMinL up; below it the
+// register-resident folded kernel is faster.
+constexpr int kOnsiteMfmaMinL = 13;
+hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const float *HA,
+                              const float *HB, float *Ta, float *Tb, hipStream_t s);
 
 // fp32 receiver pass with the edge synthesis on MFMA (receiver_mfma.hip): writes the
 // summed grid fields to S [N][R][2][UVs] and then runs the inverse transforms into

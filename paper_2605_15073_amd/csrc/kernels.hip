@@ -227,6 +227,10 @@ hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, 
     int64_t blocks = B * R;
     if (blocks == 0) return hipSuccess;
     if constexpr (sizeof(T) == 4) {
+        if (tb.d.lmax >= kOnsiteMfmaMinL) {
+            hipError_t e = launch_onsite_mfma(tb, B, R, HA, HB, Ta, Tb, s);
+            if (e != hipErrorNotSupported) return e;
+        }
         if (tb.d.lmax <= kOnsiteFoldedMaxL) {
             hipError_t e = launch_onsite_folded(tb, B, R, HA, HB, Ta, Tb, s);
             if (e != hipErrorNotSupported && e != hipErrorInvalidValue) return e;

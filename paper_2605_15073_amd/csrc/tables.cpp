@@ -164,9 +164,10 @@ static void region_sizes(const Dims &d, size_t *n)
     n[15] = (size_t)d.P * ut;   // pt
     n[16] = (size_t)d.P * ut;   // dpt
     n[17] = (size_t)d.P * ut;   // wpt
+    n[18] = d.P;                // yc
 }
 
-static const int kRegions = 18;
+static const int kRegions = 19;
 
 static size_t round_up(size_t n) { return (n + 63) & ~(size_t)63; }  // 512 B for fp64
 
@@ -220,6 +221,9 @@ void fill_tables(const Dims &d, double *h)
     for (int l = 0; l <= d.lmax; ++l)
         for (int m = 0; m <= l; ++m) {
             int idx = l * (l + 1) / 2 + m;
+            if (l > m)
+                h[off[18] + idx] = std::sqrt((2.0 * l + 1.0) * ((double)l * l - (double)m * m)
+                                             / (2.0 * l - 1.0));
             if (l >= m + 2) {
                 h[off[12] + idx] = std::sqrt((4.0 * l * l - 1.0) / ((double)l * l - (double)m * m));
                 h[off[13] + idx] = std::sqrt(((l - 1.0) * (l - 1.0) - (double)m * m)
@@ -262,6 +266,7 @@ Tabs<T> bind_tables(const Dims &d, const void *dev)
     tb.pt = ptr[15];
     tb.dpt = ptr[16];
     tb.wpt = ptr[17];
+    tb.yc = ptr[18];
     tb.d = d;
     return tb;
 }

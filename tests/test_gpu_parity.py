@@ -66,6 +66,16 @@ def test_onsite_lmax_sweep_ragged(cg, lmax, n, C, R):
     _check_pair(run_onsite(cg, plan, to_dev(d, ONSITE_KEYS)), _oracle_onsite(lmax, d), TOL_F32)
 
 
+@pytest.mark.parametrize("lmax,n,C,R", [(2, 9, 5, 17), (6, 7, 8, 33), (12, 5, 6, 19),
+                                        (15, 3, 4, 7), (16, 4, 5, 18), (20, 3, 4, 18),
+                                        (24, 2, 3, 5)])
+def test_onsite_rank_blocks_and_high_lmax(cg, lmax, n, C, R):
+    # rank counts that leave a partial rank block; lmax >= 15 runs the MFMA grid stage
+    d = inputs.onsite_inputs(n, lmax, C, R, seed=300 + lmax, distinct_out=True)
+    plan = cg.plan_create(lmax, C, R)
+    _check_pair(run_onsite(cg, plan, to_dev(d, ONSITE_KEYS)), _oracle_onsite(lmax, d), TOL_F32)
+
+
 def test_onsite_ace_n2048_l4_self_coupled(cg):
     w = inputs.WORKLOADS["onsite_ace_n2048_l4_c64"]
     d = w.make()
