@@ -32,6 +32,20 @@ __device__ __forceinline__ int isqrt_small(int t)
 
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
+// Raw buffer resource over [base, base + bytes): loads past the end return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, unsigned bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t rs, unsigned voff)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0));
+}
+
+constexpr unsigned kOutside = 0xfffffff0u;  // a buffer offset past every resource: reads 0
+
 __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     int64_t B, int Cin, int Cout, int K, int kdeg, int tiles_per_group, int otiles,
     const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
@@ -135,6 +149,125 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
         }
 }
 
+// kdeg contraction (the edge side, Eq. msgpass-tildeR): Y[b][o][l] over the L degree
+// slots of X [B][Cin][L]. A workgroup owns 64 rows b and 64 outputs o for a group of LG
+// degrees, so a row's input block is read once for all of those degrees. The reduction
+// runs in slices of kCk inputs: each thread prefetches its share of the next slice into
+// registers while the matrix cores work on the current one from LDS. X rows keep their
+// natural (i, l) order in LDS (row stride kSB = 2 mod 32, so the A-operand reads of a
+// half-wave hit distinct banks); W is staged as Ws[l][i][o]. Wave (wb, wo) accumulates
+// its 32 x 32 sub-tile of D[b][o] for every degree of the group (A = X rows, B = W
+// columns, so 16 lanes write 64 contiguous bytes of a row of Y).
+constexpr int kCk = 8;           // reduction slice per LDS stage
+constexpr int kLG = 7;           // degrees per workgroup
+constexpr int kSB = 66;          // LDS row stride of a staged X row (kCk * kLG = 56 used)
+constexpr int kSW = kTile + 16;  // LDS row stride of Ws: lane groups of a half-wave apart
+constexpr int kNX = kTile * kCk * kLG / kThreadsC;  // staged elements per thread and slice
+
+__global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
+    int64_t B, int Cin, int Cout, int L, int otiles, int lgroups, const float *__restrict__ W,
+    unsigned w_bytes, int w_sl, int w_si, int w_so, const float *__restrict__ X,
+    float *__restrict__ Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
+    const float *__restrict__ scale)
+{
+    __shared__ float Xs[kTile * kSB];
+    __shared__ float Ws[kLG][kCk][kSW];
+    // XCD-aware order (block b runs on XCD b % 8): the output tiles and degree groups of a
+    // row group, which read the same input lines, get consecutive ids on one XCD.
+    const int64_t nblk = gridDim.x, per = nblk / 8, rem = nblk % 8;
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int64_t bid = (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+    const int ot = (int)(bid % otiles);
+    const int64_t rest = bid / otiles;
+    const int lg = (int)(rest % lgroups);
+    const int64_t grp = rest / lgroups;
+    const int64_t b0 = grp * kTile;
+    const int o0 = ot * kTile;
+    const int l0 = lg * kLG;
+    const int nl = (L - l0 < kLG) ? (L - l0) : kLG;
+    const int nb = (B - b0 < kTile) ? (int)(B - b0) : kTile;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, n = lane & 15;
+    const int wb = (wave >> 1) * 32, wo = (wave & 1) * 32;
+    float4_t acc[kLG][2][2];
+#pragma unroll
+    for (int l = 0; l < kLG; ++l)
+#pragma unroll
+        for (int a = 0; a < 2; ++a) acc[l][a][0] = acc[l][a][1] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+    // the row group's inputs (reads past its last row return 0) and the weights
+    const __amdgpu_buffer_rsrc_t xs =
+        rsrc(X + b0 * (int64_t)Cin * L, (unsigned)((int64_t)nb * Cin * L * 4));
+    const __amdgpu_buffer_rsrc_t ws = rsrc(W, w_bytes);
+    // this thread's staged elements: X (b, i, l) and W (l, i, o) at k = tid + 256 s
+    float xr[kNX], wr[kNX];
+    auto fetch = [&](int i0) {
+#pragma unroll
+        for (int s2 = 0; s2 < kNX; ++s2) {
+            const int k = tid + kThreadsC * s2;
+            const int b = k / (kCk * kLG), r = k - b * (kCk * kLG);
+            const int i = r / kLG, l = r - i * kLG;
+            const unsigned xo = (i0 + i < Cin && l < nl)
+                                    ? (unsigned)((b * Cin + i0 + i) * L + l0 + l) * 4u : kOutside;
+            xr[s2] = bload(xs, xo);
+            const int lw = k / (kCk * kTile), rw = k - lw * (kCk * kTile);
+            const int iw = rw / kTile, o = rw - iw * kTile;
+            const unsigned wo4 = (lw < nl && i0 + iw < Cin && o0 + o < Cout)
+                                     ? (unsigned)((l0 + lw) * w_sl + (i0 + iw) * w_si + (o0 + o) * w_so) * 4u
+                                     : kOutside;
+            wr[s2] = bload(ws, wo4);
+        }
+    };
+    fetch(0);
+    for (int i0 = 0; i0 < Cin; i0 += kCk) {
+        __syncthreads();  // the previous slice is consumed
+#pragma unroll
+        for (int s2 = 0; s2 < kNX; ++s2) {
+            const int k = tid + kThreadsC * s2;
+            const int b = k / (kCk * kLG), r = k - b * (kCk * kLG);
+            Xs[b * kSB + r] = xr[s2];
+            const int lw = k / (kCk * kTile), rw = k - lw * (kCk * kTile);
+            const int iw = rw / kTile, o = rw - iw * kTile;
+            Ws[lw][iw][o] = wr[s2];
+        }
+        __syncthreads();
+        if (i0 + kCk < Cin) fetch(i0 + kCk);
+#pragma unroll
+        for (int l = 0; l < kLG; ++l)
+#pragma unroll
+            for (int kk = 0; kk < kCk; kk += 4) {
+                const int xo = (kk + g) * kLG + l;
+                const float a0 = Xs[(wb + n) * kSB + xo], a1 = Xs[(wb + 16 + n) * kSB + xo];
+                const float b0v = Ws[l][kk + g][wo + n], b1v = Ws[l][kk + g][wo + 16 + n];
+                acc[l][0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0v, acc[l][0][0], 0, 0, 0);
+                acc[l][0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1v, acc[l][0][1], 0, 0, 0);
+                acc[l][1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0v, acc[l][1][0], 0, 0, 0);
+                acc[l][1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1v, acc[l][1][1], 0, 0, 0);
+            }
+    }
+    // D[b = 4 g + j][o = n] of each 16 x 16 tile
+#pragma unroll
+    for (int l = 0; l < kLG; ++l) {
+        if (l >= nl) break;
+        const float sc = scale ? scale[l0 + l] : 1.f;
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int o = o0 + wo + 16 * c + n;
+                if (o >= Cout) continue;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int b = wb + 16 * a + 4 * g + j;
+                    if (b < nb)
+                        Y[(b0 + b) * y_sb + (int64_t)o * y_so + (int64_t)(l0 + l) * y_sk] =
+                            acc[l][a][c][j] * sc;
+                }
+            }
+    }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int Cout, int K,
                                                          int kdeg, const T *__restrict__ W,
@@ -170,6 +303,23 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
                                   const float *scale, hipStream_t s)
 {
     if (B == 0 || Cout == 0 || K == 0) return hipSuccess;
+    if (kdeg) {
+        const int64_t groups = (B + kTile - 1) / kTile;
+        const int otiles = (Cout + kTile - 1) / kTile;
+        const int lgroups = (K + kLG - 1) / kLG;
+        const int64_t blocks = groups * otiles * lgroups;
+        if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+        // 32-bit buffer offsets: the row group's inputs and every weight index must fit
+        const int64_t w_span = 4 * ((K - 1) * w_sl + (int64_t)(Cin - 1) * w_si +
+                                    (int64_t)(Cout - 1) * w_so + 1);
+        if (w_span >= (int64_t)kOutside || 4 * (int64_t)kTile * Cin * K >= (int64_t)kOutside ||
+            w_sl < 0 || w_si < 0 || w_so < 0)
+            return hipErrorNotSupported;
+        hipLaunchKernelGGL(k_contract_kdeg, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B,
+                           Cin, Cout, K, otiles, lgroups, W, (unsigned)w_span, (int)w_sl,
+                           (int)w_si, (int)w_so, X, Y, y_sb, y_so, y_sk, scale);
+        return hipGetLastError();
+    }
     const int64_t groups = (B + kTile - 1) / kTile;
     const int tiles_per_group = K;  // sum over degrees of (2l+1), or L tiles when kdeg
     const int otiles = (Cout + kTile - 1) / kTile;

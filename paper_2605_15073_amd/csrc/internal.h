@@ -133,7 +133,7 @@ hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
 // fp32 receiver pass with the edge synthesis on MFMA (receiver_mfma.hip): writes the
 // summed grid fields to S [N][R][2][UVs] and then runs the inverse transforms into
 // Ta, Tb. Requires R % 16 == 0.
-constexpr int kMfmaRecvMinL = 9;  // below this the per-thread SIMT receiver is used
+constexpr int kMfmaRecvMinL = 7;  // below this the per-thread SIMT receiver is used
 bool receiver_mfma_supported(const Dims &d, int R);
 size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R);
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,

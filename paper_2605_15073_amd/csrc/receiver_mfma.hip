@@ -279,7 +279,7 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
         hipLaunchKernelGGL((k_receiver_mfma<TPW, LMV>), dim3((unsigned)blocks), dim3(256), sh, s, \
                            tb, R, nchunks, row_ptr, col, unit, Rt, SF, S);                      \
         break;
-        CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11) CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
+        CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11) CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
         CGTP_CASE(15) CGTP_CASE(16) CGTP_CASE(17) CGTP_CASE(18) CGTP_CASE(19) CGTP_CASE(20)
         CGTP_CASE(21) CGTP_CASE(22) CGTP_CASE(23) CGTP_CASE(24)
 #undef CGTP_CASE

@@ -307,9 +307,9 @@ def test_mp_5k_l20_sampled(cg):
     _check_pair(gpu, _oracle_mp(w.lmax, d, rec), TOL_F32, nodes=rec)
 
 
-@pytest.mark.parametrize("lmax,R", [(9, 16), (10, 32), (13, 16), (24, 16)])
+@pytest.mark.parametrize("lmax,R", [(7, 16), (8, 48), (9, 16), (10, 32), (13, 16), (24, 16)])
 def test_mp_mfma_receiver(cg, lmax, R):
-    """Ranks in multiples of 16 at lmax >= 9 take the MFMA receiver pass."""
+    """Ranks in multiples of 16 at lmax >= 7 take the MFMA receiver pass."""
     d = _tiny_mp(lmax, n=48, C=4, R=R, seed=70 + lmax, r_cut=3.5)
     plan = cg.plan_create(lmax, 4, R)
     _check_pair(run_mp(cg, plan, to_dev(d, MP_KEYS)), _oracle_mp(lmax, d), TOL_F32)
