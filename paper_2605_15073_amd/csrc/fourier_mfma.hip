@@ -202,7 +202,7 @@ __device__ __forceinline__ void legendre_all(const LaneRows<LM, NOP> &c,
 }
 
 template <int LM>
-__global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int rb,
+__global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int rb, int nc,
                                                      const float *__restrict__ H,
                                                      float *__restrict__ SF)
 {
@@ -261,13 +261,30 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
             const int ro = rt * 16 + 4 * g4 + j;
             if (ro < rows) {
                 const int qo = ro / G::U, uo = ro - qo * G::U;
-                float *o = SF + (b * R + r0 + qo) * 3 * (int64_t)G::UVs + uo * G::V + n;
+                if (nc == 0) {  // SF [B][R][3][UVs]
+                    float *o = SF + (b * R + r0 + qo) * 3 * (int64_t)G::UVs + uo * G::V + n;
 #pragma unroll
-                for (int t = 0; t < G::VT; ++t) {
-                    if (t * 16 + n < G::V) {
-                        o[t * 16] = acc[0][t][j];
-                        o[G::UVs + t * 16] = acc[1][t][j];
-                        o[2 * G::UVs + t * 16] = acc[2][t][j];
+                    for (int t = 0; t < G::VT; ++t) {
+                        if (t * 16 + n < G::V) {
+                            o[t * 16] = acc[0][t][j];
+                            o[G::UVs + t * 16] = acc[1][t][j];
+                            o[2 * G::UVs + t * 16] = acc[2][t][j];
+                        }
+                    }
+                } else {  // SF [R/16][nc][B][16][3][64]
+                    const int r = r0 + qo;
+                    const int64_t nb = gridDim.x / nrb;  // B
+#pragma unroll
+                    for (int t = 0; t < G::VT; ++t) {
+                        const int p = uo * G::V + t * 16 + n;
+                        if (t * 16 + n < G::V) {
+                            const int c = p / kSfChunk, pp = p - c * kSfChunk;
+                            float *o = SF + ((((int64_t)(r >> 4) * nc + c) * nb + b) * 16 + (r & 15)) *
+                                                3 * kSfChunk + pp;
+                            o[0] = acc[0][t][j];
+                            o[kSfChunk] = acc[1][t][j];
+                            o[2 * kSfChunk] = acc[2][t][j];
+                        }
                     }
                 }
             }
@@ -525,7 +542,7 @@ hipError_t onsite_lm(const Tabs<float> &tb, int64_t B, int R, const float *HA, c
 
 template <int LM>
 hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
-                     hipStream_t s)
+                     bool chunked, hipStream_t s)
 {
     using G = Grid<LM>;
     const size_t fixed = 4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB;
@@ -533,8 +550,10 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    if (chunked && R % 16 != 0) return hipErrorInvalidValue;
+    const int nc = chunked ? sf_chunks(tb.d) : 0;
     hipLaunchKernelGGL((k_sender_mfma<LM>), dim3((unsigned)blocks), dim3(64 * waves_for(rb * G::U)),
-                       sizeof(float) * (fixed + rb * (size_t)G::HR), s, tb, R, rb, H, SF);
+                       sizeof(float) * (fixed + rb * (size_t)G::HR), s, tb, R, rb, nc, H, SF);
     return hipGetLastError();
 }
 
@@ -567,14 +586,16 @@ bool default_grid(const Dims &d)
     X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15)     \
     X(16) X(17) X(18) X(19) X(20) X(21) X(22) X(23) X(24)
 
+bool sender_mfma_supported(const Dims &d) { return default_grid(d) && d.lmax <= 24; }
+
 hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
-                              hipStream_t s)
+                              bool chunked, hipStream_t s)
 {
     if (B == 0) return hipSuccess;
-    if (!default_grid(tb.d)) return hipErrorNotSupported;
+    if (!sender_mfma_supported(tb.d)) return hipErrorNotSupported;
     switch (tb.d.lmax) {
 #define CGTP_CASE(LMV) \
-    case LMV: return sender_lm<LMV>(tb, B, R, H, SF, s);
+    case LMV: return sender_lm<LMV>(tb, B, R, H, SF, chunked, s);
         CGTP_LMAX_CASES(CGTP_CASE)
 #undef CGTP_CASE
     default: return hipErrorNotSupported;

@@ -119,8 +119,15 @@ hipError_t launch_analysis_folded(const Tabs<float> &tb, int64_t B, int R, const
 // (same output as launch_sender_fields) and the inverse transforms of S [N][R][2][UVs]
 // into Ta, Tb. hipErrorNotSupported when the grid is wider than their tiling
 // (V > 80) or the LDS staging does not fit.
+// With chunked set, SF is written in the layout the MFMA receiver reads:
+// [R/16][NC][B][16][3][64], NC = ceil(UV / 64) chunks of 64 grid points, so the fields a
+// receiver wave needs from one sender (16 ranks x 3 fields x 64 points) are one
+// contiguous 12 KiB run. Requires R % 16 == 0.
+constexpr int kSfChunk = 64;
+inline int sf_chunks(const Dims &d) { return (d.UV + kSfChunk - 1) / kSfChunk; }
+bool sender_mfma_supported(const Dims &d);
 hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
-                              hipStream_t s);
+                              bool chunked, hipStream_t s);
 hipError_t launch_analysis_mfma(const Tabs<float> &tb, int64_t B, int R, const float *S,
                                 float *Ta, float *Tb, hipStream_t s);
 // fp32 on-site grid stage on MFMA (fourier_mfma.hip), default grid only: the same
@@ -138,6 +145,7 @@ bool receiver_mfma_supported(const Dims &d, int R);
 size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R);
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
-                                const float *SF, float *S, float *Ta, float *Tb, hipStream_t s);
+                                const float *SF, bool sf_chunked, float *S, float *Ta, float *Tb,
+                                hipStream_t s);
 
 }  // namespace cgtp

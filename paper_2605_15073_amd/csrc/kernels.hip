@@ -154,7 +154,7 @@ hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H,
 {
     if (B == 0) return hipSuccess;
     if constexpr (sizeof(T) == 4) {
-        hipError_t e = launch_sender_mfma(tb, B, R, H, SF, s);
+        hipError_t e = launch_sender_mfma(tb, B, R, H, SF, false, s);
         if (e != hipErrorNotSupported) return e;
     }
     const size_t per_rank = tb.d.K + 2 * (size_t)tb.d.M * tb.d.U;

@@ -78,6 +78,13 @@ bool use_mfma_receiver(const cgtp_plan_s *p)
            p->d.lmax >= cgtp::kMfmaRecvMinL && cgtp::receiver_mfma_supported(p->d, p->R);
 }
 
+// The MFMA receiver reads the sender fields in 64-point chunks when the MFMA sender writes
+// them (fp32, default grid).
+bool sf_chunked(const cgtp_plan_s *p)
+{
+    return use_mfma_receiver(p) && cgtp::sender_mfma_supported(p->d);
+}
+
 // On-site workspace: HA, HB, Ta, Tb, each [N][R][K].
 Layout onsite_layout(const cgtp_plan_s *p, int64_t N)
 {
@@ -95,7 +102,8 @@ Layout mp_layout(const cgtp_plan_s *p, int64_t N, int64_t E)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
     size_t h = align256(es * (size_t)N * p->R * p->d.K);
-    size_t sf = align256(es * (size_t)N * p->R * 3 * p->d.UVs);
+    const size_t sf_pts = sf_chunked(p) ? (size_t)cgtp::sf_chunks(p->d) * cgtp::kSfChunk : p->d.UVs;
+    size_t sf = align256(es * (size_t)N * p->R * 3 * sf_pts);
     size_t rt = align256(es * (size_t)E * p->R * p->d.L);
     size_t sg = use_mfma_receiver(p) ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, p->R)) : 0;
     Layout l{};
@@ -292,7 +300,14 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
                                  (int64_t)R * d.K, d.K, 1, nullptr, s);
     if (e != hipSuccess) return hip_fail(e, "contract node features");
     rec.mark();
-    e = cgtp::launch_sender_fields<T>(tb, N, R, HI, SF, s);
+    if constexpr (sizeof(T) == 4) {
+        if (sf_chunked(p))
+            e = cgtp::launch_sender_mfma(tb, N, R, HI, SF, true, s);
+        else
+            e = cgtp::launch_sender_fields<T>(tb, N, R, HI, SF, s);
+    } else {
+        e = cgtp::launch_sender_fields<T>(tb, N, R, HI, SF, s);
+    }
     if (e != hipSuccess) return hip_fail(e, "sender fields");
     rec.mark();
     // Eq. msgpass-tildeR into Rt [E][L][R] (the zonal form folds in the addition-theorem
@@ -304,8 +319,8 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
     if constexpr (sizeof(T) == 4) {
         if (use_mfma_receiver(p)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
-            e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt, SF, Sg,
-                                           Ta, Tb, s);
+            e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt, SF,
+                                           sf_chunked(p), Sg, Ta, Tb, s);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
             goto projections;

@@ -44,21 +44,26 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// LM is lmax: the recurrence is unrolled with compile-time coefficients.
-template <int TPW, int LM>
-__global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
-                                                       const int32_t *__restrict__ row_ptr,
-                                                       const int32_t *__restrict__ col,
-                                                       const float *__restrict__ unit,
-                                                       const float *__restrict__ Rt,
-                                                       const float *__restrict__ SF,
-                                                       float *__restrict__ S)
+// LM is lmax: the recurrence is unrolled with compile-time coefficients. A workgroup
+// is WPB waves; each wave owns PW = 64 grid points, one per lane: per edge a lane runs
+// the Legendre recurrence for P_l and P_l' at its own point (both in the same lane) into
+// wave-private LDS, then the wave multiplies those [64 points x L] values with the
+// [L x 16 ranks] edge coefficients on the matrix cores.
+template <int WPB, int LM>
+__global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
+                                                            const int32_t *__restrict__ row_ptr,
+                                                            const int32_t *__restrict__ col,
+                                                            const float *__restrict__ unit,
+                                                            const float *__restrict__ Rt,
+                                                            const float *__restrict__ SF,
+                                                            int sf_nc, float *__restrict__ S)
 {
-    constexpr int PW = 16 * TPW;  // grid points per wave
-    constexpr int PC = 4 * PW;    // grid points per workgroup
+    constexpr int TPW = 4;           // 16-point tiles per wave
+    constexpr int PW = 16 * TPW;     // grid points per wave: one per lane
+    constexpr int PC = WPB * PW;     // grid points per workgroup
     constexpr int L = LM + 1;
     constexpr int KS = (L + 3) / 4;  // K steps of 4 degrees
-    // LDS row stride: rows of the 4 lane groups land in different bank halves
+    // LDS row stride: the rows read by lane groups g and g + 1 land in different bank halves
     constexpr int RS = PW + 16;
     const Dims &d = tb.d;
     const int UV = d.UV, UVs = d.UVs;
@@ -83,10 +88,8 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
 
     // degrees beyond lmax stay zero in the A operand
     for (int k = lane; k < 2 * 4 * KS * RS; k += 64) Pl[k] = 0.f;
-    // recurrence point of this lane: lanes 0..PW-1 write P, lanes PW..2PW-1 write P'
-    const int rl = lane % PW;
-    const bool wr_p = lane < PW, wr_d = lane >= PW && lane < 2 * PW;
-    const int pr = pw0 + rl;
+    // this lane's recurrence point (points past the grid compute on point 0, never stored)
+    const int pr = pw0 + lane;
     const int prc = pr < UV ? pr : 0;
     const int ur = prc / d.V, vr = prc - ur * d.V;
     const float rx = tb.x[ur], rsx = tb.sx[ur], rxsx = tb.xsx[ur], rcp = tb.cphi[vr],
@@ -100,22 +103,42 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
         sa[t] = float4_t{0.f, 0.f, 0.f, 0.f};
         sb[t] = float4_t{0.f, 0.f, 0.f, 0.f};
     }
-    // lane's points: pw0 + 16 t + 4 g + (0..3); lane's rank: r0 + n
-    const unsigned voff = (unsigned)((n * 3 * UVs + pw0 + 4 * g) * 4);
+    // lane's points: pw0 + 16 t + 4 g + (0..3); lane's rank: r0 + n. The sender fields are
+    // either SF [N][R][3][UVs] (a sender's 16-rank block is [16][3][UVs]) or, with sf_nc
+    // chunks, SF [R/16][sf_nc][N][16][3][64] (this wave's 64 points of a sender are one
+    // contiguous [16][3][64] run).
+    const int fstride = sf_nc ? kSfChunk : UVs;  // field stride, elements
+    const unsigned voff = sf_nc ? (unsigned)((n * 3 * kSfChunk + 4 * g) * 4)
+                                : (unsigned)((n * 3 * UVs + pw0 + 4 * g) * 4);
+    const float *sfb = sf_nc ? SF + ((int64_t)(r0 / kRT) * sf_nc + pw0 / kSfChunk) * NN * (kRT * 3 * kSfChunk)
+                             : SF + (int64_t)r0 * 3 * UVs;
+    const int64_t jstride = sf_nc ? (int64_t)kRT * 3 * kSfChunk : (int64_t)R * 3 * UVs;
+    const unsigned sfbytes = (unsigned)(kRT * 3 * fstride * 4);
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
-    for (int e = e0; e < e1; ++e) {
+    // sender fields of edge e (cur) and e + 1 (nxt): the next edge's loads are in flight
+    // while this one is computed
+    float4_t cI[TPW], cX[TPW], cP[TPW];
+    auto load_fields = [&](int e, float4_t *fI, float4_t *fX, float4_t *fP) {
         const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
-        // sender rank block [16][3][UVs]
-        const __amdgpu_buffer_rsrc_t sfr =
-            rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs, (unsigned)(kRT * 3 * UVs * 4));
-        float4_t fI[TPW], fX[TPW], fP[TPW];
+        const __amdgpu_buffer_rsrc_t sfr = rsrc(sfb + j * jstride, sfbytes);
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
             const unsigned so = (unsigned)(t * 16 * 4);
             fI[t] = bload4(sfr, voff, so);
-            fX[t] = bload4(sfr, voff, so + UVs * 4);
-            fP[t] = bload4(sfr, voff, so + 2 * UVs * 4);
+            fX[t] = bload4(sfr, voff, so + fstride * 4);
+            fP[t] = bload4(sfr, voff, so + 2 * fstride * 4);
         }
+    };
+    if (e0 < e1) load_fields(e0, cI, cX, cP);
+    for (int e = e0; e < e1; ++e) {
+        float4_t fI[TPW], fX[TPW], fP[TPW];
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+            fI[t] = cI[t];
+            fX[t] = cX[t];
+            fP[t] = cP[t];
+        }
+        if (e + 1 < e1) load_fields(e + 1, cI, cX, cP);
         float ux = unit[3 * (int64_t)e], uy = unit[3 * (int64_t)e + 1], uz = unit[3 * (int64_t)e + 2];
         const float inv = 1.f / sqrtf(ux * ux + uy * uy + uz * uz);
         ux *= inv;
@@ -131,28 +154,30 @@ __global__ __launch_bounds__(256) void k_receiver_mfma(Tabs<float> tb, int R, in
         }
         wave_sync();  // this wave is done reading the previous edge's P, P'
         {
+            // t = rhat . Omega at this lane's point; P_l(t) and P_l'(t) by the Legendre and
+            // derivative recurrences
             const float h = ux * rcp + uy * rsp;
             const float t = uz * rx + rsx * h;
             float p0v = 1.f, p1v = t, d1 = 1.f;
-            if (wr_p) Pl[rl] = 1.f;
-            if (wr_d) Dl[rl] = 0.f;
+            Pl[lane] = 1.f;
+            Dl[lane] = 0.f;
             if (LM >= 1) {
-                if (wr_p) Pl[RS + rl] = t;
-                if (wr_d) Dl[RS + rl] = 1.f;
+                Pl[RS + lane] = t;
+                Dl[RS + lane] = 1.f;
             }
 #pragma unroll
             for (int l = 2; l <= LM; ++l) {
                 const float c1 = (float)(2 * l - 1) / (float)l, c2 = (float)(l - 1) / (float)l;
                 const float p2 = c1 * t * p1v - c2 * p0v;
                 const float d2 = (float)l * p1v + t * d1;
-                if (wr_p) Pl[l * RS + rl] = p2;
-                if (wr_d) Dl[l * RS + rl] = d2;
+                Pl[l * RS + lane] = p2;
+                Dl[l * RS + lane] = d2;
                 p0v = p1v;
                 p1v = p2;
                 d1 = d2;
             }
-            if (wr_p) dxs[rl] = uz - rxsx * h;
-            if (wr_d) dps[rl] = rsx * (uy * rcp - ux * rsp);
+            dxs[lane] = uz - rxsx * h;
+            dps[lane] = rsx * (uy * rcp - ux * rsp);
         }
         wave_sync();
 #pragma unroll
@@ -262,22 +287,25 @@ size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R)
 
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
-                                const float *SF, float *S, float *Ta, float *Tb, hipStream_t s)
+                                const float *SF, bool sf_chunked, float *S, float *Ta, float *Tb,
+                                hipStream_t s)
 {
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
-    constexpr int TPW = 2, PW = 16 * TPW, PC = 4 * PW;
+    constexpr int WPB = 2, PW = 64, PC = WPB * PW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
-    const size_t sh = sizeof(float) * 4 * (2 * 4 * KS * (PW + 16) + 2 * PW);
+    const size_t sh = sizeof(float) * WPB * (2 * 4 * KS * (PW + 16) + 2 * PW);
     const int64_t blocks = N * (R / kRT) * nchunks;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    static_assert(PW == kSfChunk, "a receiver wave reads one chunk of the chunked layout");
+    const int sf_nc = sf_chunked ? sf_chunks(d) : 0;
     switch (d.lmax) {
 #define CGTP_CASE(LMV)                                                                          \
     case LMV:                                                                                   \
-        hipLaunchKernelGGL((k_receiver_mfma<TPW, LMV>), dim3((unsigned)blocks), dim3(256), sh, s, \
-                           tb, R, nchunks, row_ptr, col, unit, Rt, SF, S);                      \
+        hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV>), dim3((unsigned)blocks), dim3(64 * WPB), sh, s, \
+                           tb, R, nchunks, row_ptr, col, unit, Rt, SF, sf_nc, S);               \
         break;
         CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11) CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
         CGTP_CASE(15) CGTP_CASE(16) CGTP_CASE(17) CGTP_CASE(18) CGTP_CASE(19) CGTP_CASE(20)
