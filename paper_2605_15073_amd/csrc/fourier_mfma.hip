@@ -57,7 +57,6 @@ struct Grid {
     static constexpr int QB = (VT * 16 + 31) / 32 * 32 + 16;  // [m][v], read at g QB + n
     static constexpr int QS = (MW + 31) / 32 * 32 + 2;        // [v][m], read at n QS + g
                                                               // (and at 4 g QS + n: 2-way)
-    static constexpr int QM = (MW + 31) / 32 * 32 + 16;       // [v][m], read at g QM + n
     static constexpr int VS = (VP + 31) / 32 * 32 + 2;        // staged S rows, read at n VS + g
     // Tm rows [m][TS]: written at 16 mt + n (stride TS: 2-way), read as 16-byte words by
     // consecutive m (stride TS / 4 words, odd: conflict-free)
@@ -302,100 +301,110 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
 {
     using G = Grid<LM>;
     extern __shared__ float smem[];
-    float *qs = smem;                                   // [VP][QM]: q_vm as [v][m]
-    float *Ss = qs + G::VP * G::QM;                     // [rb U][VS]
-    float *Tm = Ss + (rb * G::U * G::VS + 3) / 4 * 4;   // [rb][M][TS], 16-byte aligned
+    float *Ss = smem;                                      // [2][rb U][VS]
+    float *Tm = Ss + (2 * rb * G::U * G::VS + 3) / 4 * 4;  // [rb][2][M][TS], 16-byte aligned
     const int nrb = (R + rb - 1) / rb;
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
     const int tid = threadIdx.x, nt = blockDim.x;
     const int lane = tid & 63, wave = tid >> 6, nw = nt >> 6, g4 = lane >> 4, n = lane & 15;
-    stage_q<LM>(tb, qs, G::VP, G::QM, true);
     const int rows = nr * G::U;
     const int rtiles = (rows + 15) / 16;
+    // stage rows (q, u) of both fields as Ss[f][q U + u][v] (16-byte loads of the stored rows;
+    // columns V .. VP - 1 zero)
+    constexpr int R4 = G::UVs / 4;  // 16-byte words per stored row
+    for (int k = tid; k < 2 * nr * R4; k += nt) {
+        const int qf = k / R4, r = 4 * (k - qf * R4);  // qf = 2 q + f
+        if (r < G::UV) {
+            const float4_t x = *reinterpret_cast<const float4_t *>(
+                S + ((b * R + r0) * 2 + qf) * (int64_t)G::UVs + r);
+            const int q = qf >> 1, f = qf & 1;
+            float *dst = Ss + (f * rb + q) * G::U * G::VS;
+            int u = r / G::V, v = r - u * G::V;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (r + e < G::UV) dst[u * G::VS + v] = x[e];
+                if (++v == G::V) {
+                    v = 0;
+                    ++u;
+                }
+            }
+        }
+    }
     constexpr int pad = G::VP - G::V;
     if (pad > 0)
-        for (int k = tid; k < rows * pad; k += nt) {
+        for (int k = tid; k < 2 * rb * G::U * pad; k += nt) {
             const int ro = k / pad;
             Ss[ro * G::VS + G::V + (k - ro * pad)] = 0.f;
         }
     constexpr int tpad = G::Ut - G::U;
     if (tpad > 0)
-        for (int k = tid; k < nr * G::M * tpad; k += nt) {
+        for (int k = tid; k < nr * 2 * G::M * tpad; k += nt) {
             const int ro = k / tpad;
             Tm[ro * G::TS + G::U + (k - ro * tpad)] = 0.f;
         }
-    constexpr int R4 = G::UVs / 4;  // 16-byte words per stored row
-    for (int which = 0; which < 2; ++which) {
-        // stage rows (q, u) of S as Ss[q U + u][v]
-        for (int k = tid; k < nr * R4; k += nt) {
-            const int q = k / R4, r = 4 * (k - q * R4);
-            if (r < G::UV) {
-                const float4_t x = *reinterpret_cast<const float4_t *>(
-                    S + ((b * R + r0 + q) * 2 + which) * (int64_t)G::UVs + r);
-                int u = r / G::V, v = r - u * G::V;
+    // B operand q[v = 4 kk + g][m = 16 t + n], the same for every tile: held in registers
+    float qb[G::KV][G::MT];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    if (r + e < G::UV) Ss[(q * G::U + u) * G::VS + v] = x[e];
-                    if (++v == G::V) {
-                        v = 0;
-                        ++u;
+    for (int kk = 0; kk < G::KV; ++kk)
+#pragma unroll
+        for (int t = 0; t < G::MT; ++t) {
+            const int v = 4 * kk + g4, m = 16 * t + n;
+            qb[kk][t] = (v < G::V && m < G::M) ? tb.q[v * G::M + m] : 0.f;
+        }
+    __syncthreads();
+    // Tm[(q,u)][m] = sum_v S[(q,u)][v] q_vm for both fields (Eq. msgpass-Tmu)
+    for (int job = wave; job < 2 * rtiles; job += nw) {
+        const int f = job & 1, rt = job >> 1;
+        const int ra = rt * 16 + n;
+        const float *sa = Ss + (f * rb * G::U + (ra < rows ? ra : 0)) * G::VS + g4;
+        float4_t acc[G::MT];
+#pragma unroll
+        for (int t = 0; t < G::MT; ++t) acc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < G::KV; ++kk) {
+            const float av = sa[4 * kk];
+#pragma unroll
+            for (int t = 0; t < G::MT; ++t)
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, qb[kk][t], acc[t], 0, 0, 0);
+        }
+#pragma unroll
+        for (int t = 0; t < G::MT; ++t) {
+            const int mi = t * 16 + n;
+            if (mi < G::M) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int ro = rt * 16 + 4 * g4 + j;
+                    if (ro < rows) {
+                        const int qo = ro / G::U, uo = ro - qo * G::U;
+                        Tm[((qo * 2 + f) * G::M + mi) * G::TS + uo] = acc[t][j];
                     }
                 }
             }
         }
-        __syncthreads();
-        for (int rt = wave; rt < rtiles; rt += nw) {
-            const int ra = rt * 16 + n;
-            const float *sa = Ss + (ra < rows ? ra : 0) * G::VS + g4;
-            const float *qc = qs + g4 * G::QM + n;
-            float4_t acc[G::MT];
+    }
+    __syncthreads();
+    // Gauss-Legendre analysis of both fields: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
+    // (Eq. msgpass-Tlm); one weight row serves both fields
+    for (int idx = tid; idx < nr * G::K; idx += nt) {
+        const int q = idx / G::K, k = idx - q * G::K;
+        const int l = (int)sqrtf((float)k + 0.5f);  // exact for k < 2^20
+        const int m = k - l * l - l, am = m < 0 ? -m : m;
+        const float4_t *w4 =
+            reinterpret_cast<const float4_t *>(tb.wpt + (l * (l + 1) / 2 + am) * G::Ut);
+        const float4_t *ta4 = reinterpret_cast<const float4_t *>(Tm + ((q * 2) * G::M + m + LM) * G::TS);
+        const float4_t *tb4 =
+            reinterpret_cast<const float4_t *>(Tm + ((q * 2 + 1) * G::M + m + LM) * G::TS);
+        float s0 = 0.f, s1 = 0.f;
 #pragma unroll
-            for (int t = 0; t < G::MT; ++t) acc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kk = 0; kk < G::KV; ++kk) {
-                const float av = sa[4 * kk];
-#pragma unroll
-                for (int t = 0; t < G::MT; ++t)
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                        av, qc[4 * kk * G::QM + t * 16], acc[t], 0, 0, 0);
-            }
-#pragma unroll
-            for (int t = 0; t < G::MT; ++t) {
-                const int mi = t * 16 + n;
-                if (mi < G::M) {
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int ro = rt * 16 + 4 * g4 + j;
-                        if (ro < rows) {
-                            const int qo = ro / G::U, uo = ro - qo * G::U;
-                            Tm[(qo * G::M + mi) * G::TS + uo] = acc[t][j];
-                        }
-                    }
-                }
-            }
+        for (int c = 0; c < G::Ut / 4; ++c) {
+            const float4_t w = w4[c], x0 = ta4[c], x1 = tb4[c];
+            s0 += w[0] * x0[0] + w[1] * x0[1] + w[2] * x0[2] + w[3] * x0[3];
+            s1 += w[0] * x1[0] + w[1] * x1[1] + w[2] * x1[2] + w[3] * x1[3];
         }
-        __syncthreads();
-        // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
-        float *out = which ? Tb : Ta;
-        for (int idx = tid; idx < nr * G::K; idx += nt) {
-            const int qq = idx / G::K, k = idx - qq * G::K;
-            const int l = (int)sqrtf((float)k + 0.5f);  // exact for k < 2^20
-            const int m = k - l * l - l, am = m < 0 ? -m : m;
-            const float4_t *w4 =
-                reinterpret_cast<const float4_t *>(tb.wpt + (l * (l + 1) / 2 + am) * G::Ut);
-            const float4_t *t4 =
-                reinterpret_cast<const float4_t *>(Tm + (qq * G::M + m + LM) * G::TS);
-            float s = 0.f;
-#pragma unroll
-            for (int c = 0; c < G::Ut / 4; ++c) {
-                const float4_t w = w4[c], t = t4[c];
-                s += w[0] * t[0] + w[1] * t[1] + w[2] * t[2] + w[3] * t[3];
-            }
-            out[(b * R + r0 + qq) * (int64_t)G::K + k] = s;
-        }
-        __syncthreads();
+        Ta[(b * R + r0 + q) * (int64_t)G::K + k] = s0;
+        Tb[(b * R + r0 + q) * (int64_t)G::K + k] = s1;
     }
 }
 
@@ -562,8 +571,8 @@ hipError_t analysis_lm(const Tabs<float> &tb, int64_t B, int R, const float *S, 
                        float *Tb, hipStream_t s)
 {
     using G = Grid<LM>;
-    const size_t fixed = (size_t)G::VP * G::QM + 3;  // + alignment of the Tm region
-    const size_t per_rank = (size_t)G::U * G::VS + (size_t)G::M * G::TS;
+    const size_t fixed = 3;  // alignment of the Tm region
+    const size_t per_rank = 2 * (size_t)G::U * G::VS + 2 * (size_t)G::M * G::TS;
     const int rb = pick_rb(R, fixed, per_rank);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
