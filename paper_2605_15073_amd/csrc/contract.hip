@@ -6,11 +6,12 @@
 // For a fixed degree l this is a GEMM Y_l[o][c] = sum_i W_l[i][o] X_l[i][c] over
 // the columns c = (b, m), m = 0..2l (or c = b when k is the degree itself).
 //
-// fp32 path: MFMA tiles (v_mfma_f32_16x16x4f32). A block owns 64 output rows
-// and 64 columns of one degree of a group of 64 nodes; the blocks of a group run
-// back to back over all degrees, so the group's input lines are reused from L2.
-// A group of 64 nodes has 64(2l+1) columns of degree l, a whole number of 64-wide
-// tiles, so no tile straddles two degrees and only the last group has a ragged edge.
+// fp32 path: MFMA tiles (v_mfma_f32_16x16x4f32). k_contract_mfma: a block owns 64
+// output rows and 64 columns of one degree of a group of 64 nodes; the blocks of a group
+// run back to back over all degrees, so the group's input lines are reused from L2. A
+// group of 64 nodes has 64(2l+1) columns of degree l, a whole number of 64-wide tiles,
+// so no tile straddles two degrees and only the last group has a ragged edge.
+// k_contract_kdeg: the case where k is the degree itself (the edge side).
 // fp64 path: one thread per output (verification build).
 #include "internal.h"
 
@@ -19,7 +20,6 @@ namespace cgtp {
 namespace {
 
 constexpr int kTile = 64;      // output rows (o) and columns (c) per block
-constexpr int kChunk = 16;     // reduction (i) slice staged in LDS per step
 constexpr int kThreadsC = 256; // 4 waves, each a 32 x 32 sub-tile (2 x 2 MFMA 16 x 16)
 
 __device__ __forceinline__ int isqrt_small(int t)
@@ -46,14 +46,26 @@ __device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t rs, unsigned voff)
 
 constexpr unsigned kOutside = 0xfffffff0u;  // a buffer offset past every resource: reads 0
 
+// One reduction slice of kCs inputs per LDS stage; each thread prefetches its share of
+// the next slice into registers while the matrix cores work on the current one. WT: the
+// weights are contiguous along the input index i (w_si == 1) and are staged as
+// Ws[o][i] (row stride kSWt = 2 mod 32); otherwise as Ws[i][o] (row stride kSWo = 16 mod
+// 32). Either way the global reads are coalesced and the A-operand reads of a half-wave
+// hit distinct banks. X is staged as Xs[i][c] (row stride kSWo).
+constexpr int kCs = 32;
+constexpr int kSWo = kTile + 16;
+constexpr int kSWt = kCs + 2;
+constexpr int kNS = kTile * kCs / kThreadsC;  // staged elements per thread, per operand
+
+template <bool WT>
 __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
-    int64_t B, int Cin, int Cout, int K, int kdeg, int tiles_per_group, int otiles,
+    int64_t B, int Cin, int Cout, int K, int tiles_per_group, int otiles,
     const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
     const float *__restrict__ X, float *__restrict__ Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
     const float *__restrict__ scale)
 {
-    __shared__ float As[kChunk][kTile + 4];  // As[i][o] = W_l[i0 + i][o0 + o]
-    __shared__ float Bs[kChunk][kTile + 4];  // Bs[i][c] = X_l[i0 + i][c0 + c]
+    __shared__ float Ws[WT ? kTile * kSWt : kCs * kSWo];
+    __shared__ float Xs[kCs * kSWo];
 
     // Blocks are dealt round-robin to the 8 XCDs (block b runs on XCD b % 8), each with
     // its own L2. Remap so that each XCD gets a contiguous range of tiles: the tiles of a
@@ -66,18 +78,8 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     const int64_t rest = bid / otiles;
     const int t = (int)(rest % tiles_per_group);
     const int64_t g = rest / tiles_per_group;
-    int l, sub, width, kofs;
-    if (kdeg) {
-        l = t;
-        sub = 0;
-        width = 1;
-        kofs = t;
-    } else {
-        l = isqrt_small(t);
-        sub = t - l * l;
-        width = 2 * l + 1;
-        kofs = l * l;
-    }
+    const int l = isqrt_small(t);
+    const int sub = t - l * l, width = 2 * l + 1, kofs = l * l;
     const int64_t b0 = g * kTile;                      // first node of the group
     const int64_t nb = (B - b0 < kTile) ? (B - b0) : kTile;
     const int ncols = (int)nb * width;                 // columns of degree l in this group
@@ -90,61 +92,84 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     const int wave = tid >> 6;
     const int osub = (wave >> 1) * 32;
     const int csub = (wave & 1) * 32;
+    const int gg = lane >> 4, n = lane & 15;
 
     float4_t acc[2][2];
     for (int a = 0; a < 2; ++a)
-        for (int b = 0; b < 2; ++b) acc[a][b] = float4_t{0.f, 0.f, 0.f, 0.f};
+        for (int bb = 0; bb < 2; ++bb) acc[a][bb] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-    // this thread's column for the B-tile loads (fixed over the reduction)
-    const int lc = tid & (kTile - 1);
-    const int li = tid >> 6;  // 0..3, rows li, li+4, li+8, li+12 of the chunk
+    // this thread's column of X (fixed over the reduction): c = tid % 64, rows i = tid / 64 + 4 s
+    const int lc = tid & (kTile - 1), li = tid >> 6;
     const int cg = c0 + lc;
     const bool c_ok = cg < ncols;
     const int bl = c_ok ? cg / width : 0;
     const int mm = c_ok ? cg - bl * width : 0;
     const float *xcol = X + (b0 + bl) * (int64_t)Cin * K + kofs + mm;
-
-    for (int i0 = 0; i0 < Cin; i0 += kChunk) {
-        // stage W_l[i0 .. i0+16)[o0 .. o0+64) and X_l[i0 .. i0+16)[c0 .. c0+64)
+    float wr[kNS], xr[kNS];
+    auto fetch = [&](int i0) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            int i = li + 4 * r;
-            int ig = i0 + i;
-            int og = o0 + lc;
-            As[i][lc] = (ig < Cin && og < Cout) ? Wl[ig * w_si + og * w_so] : 0.f;
-            Bs[i][lc] = (ig < Cin && c_ok) ? xcol[(int64_t)ig * K] : 0.f;
+        for (int s2 = 0; s2 < kNS; ++s2) {
+            const int ig = i0 + li + 4 * s2;
+            xr[s2] = (ig < Cin && c_ok) ? xcol[(int64_t)ig * K] : 0.f;
+            if (WT) {  // k = tid + 256 s -> (o, i), i fastest
+                const int k = tid + kThreadsC * s2, o = k / kCs, i = k - o * kCs;
+                wr[s2] = (i0 + i < Cin && o0 + o < Cout) ? Wl[(i0 + i) + (int64_t)(o0 + o) * w_so] : 0.f;
+            } else {   // (i, o), o fastest
+                wr[s2] = (ig < Cin && o0 + lc < Cout) ? Wl[(int64_t)ig * w_si + (o0 + lc) * w_so] : 0.f;
+            }
+        }
+    };
+    fetch(0);
+    for (int i0 = 0; i0 < Cin; i0 += kCs) {
+        __syncthreads();  // the previous slice is consumed
+#pragma unroll
+        for (int s2 = 0; s2 < kNS; ++s2) {
+            const int i = li + 4 * s2;
+            Xs[i * kSWo + lc] = xr[s2];
+            if (WT) {
+                const int k = tid + kThreadsC * s2, o = k / kCs, ii = k - o * kCs;
+                Ws[o * kSWt + ii] = wr[s2];
+            } else {
+                Ws[i * kSWo + lc] = wr[s2];
+            }
         }
         __syncthreads();
+        if (i0 + kCs < Cin) fetch(i0 + kCs);
 #pragma unroll
-        for (int kk = 0; kk < kChunk; kk += 4) {
-            const int ki = kk + (lane >> 4);
-            float a0 = As[ki][osub + (lane & 15)];
-            float a1 = As[ki][osub + 16 + (lane & 15)];
-            float b0v = Bs[ki][csub + (lane & 15)];
-            float b1v = Bs[ki][csub + 16 + (lane & 15)];
+        for (int kk = 0; kk < kCs; kk += 4) {
+            const int ki = kk + gg;
+            float a0, a1;
+            if (WT) {
+                a0 = Ws[(osub + n) * kSWt + ki];
+                a1 = Ws[(osub + 16 + n) * kSWt + ki];
+            } else {
+                a0 = Ws[ki * kSWo + osub + n];
+                a1 = Ws[ki * kSWo + osub + 16 + n];
+            }
+            const float b0v = Xs[ki * kSWo + csub + n];
+            const float b1v = Xs[ki * kSWo + csub + 16 + n];
             acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0v, acc[0][0], 0, 0, 0);
             acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1v, acc[0][1], 0, 0, 0);
             acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0v, acc[1][0], 0, 0, 0);
             acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1v, acc[1][1], 0, 0, 0);
         }
-        __syncthreads();
     }
 
-    const float s = scale ? scale[l] : 1.f;
+    const float sc = scale ? scale[l] : 1.f;
     // D[row][col] of a 16 x 16 tile: lane holds rows 4*(lane/16) + j, column lane % 16
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb) {
-            int c = c0 + csub + 16 * bb + (lane & 15);
+            int c = c0 + csub + 16 * bb + n;
             if (c >= ncols) continue;
             int bcol = c / width;
             int m = c - bcol * width;
             float *ycol = Y + (b0 + bcol) * y_sb + (int64_t)(kofs + m) * y_sk;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                int o = o0 + osub + 16 * a + 4 * (lane >> 4) + j;
-                if (o < Cout) ycol[(int64_t)o * y_so] = acc[a][bb][j] * s;
+                int o = o0 + osub + 16 * a + 4 * gg + j;
+                if (o < Cout) ycol[(int64_t)o * y_so] = acc[a][bb][j] * sc;
             }
         }
 }
@@ -321,13 +346,18 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
         return hipGetLastError();
     }
     const int64_t groups = (B + kTile - 1) / kTile;
-    const int tiles_per_group = K;  // sum over degrees of (2l+1), or L tiles when kdeg
+    const int tiles_per_group = K;  // sum over degrees of the (2l+1) tiles of 64 columns
     const int otiles = (Cout + kTile - 1) / kTile;
     const int64_t blocks = groups * tiles_per_group * otiles;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_contract_mfma, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B, Cin,
-                       Cout, K, kdeg ? 1 : 0, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, Y,
-                       y_sb, y_so, y_sk, scale);
+    if (w_si == 1)
+        hipLaunchKernelGGL(k_contract_mfma<true>, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B,
+                           Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, Y, y_sb,
+                           y_so, y_sk, scale);
+    else
+        hipLaunchKernelGGL(k_contract_mfma<false>, dim3((unsigned)blocks), dim3(kThreadsC), 0, s,
+                           B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, Y,
+                           y_sb, y_so, y_sk, scale);
     return hipGetLastError();
 }
 
