@@ -225,21 +225,39 @@ __global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
     const __amdgpu_buffer_rsrc_t xs =
         rsrc(X + b0 * (int64_t)Cin * L, (unsigned)((int64_t)nb * Cin * L * 4));
     const __amdgpu_buffer_rsrc_t ws = rsrc(W, w_bytes);
-    // this thread's staged elements: X (b, i, l) and W (l, i, o) at k = tid + 256 s
+    // Staged elements of this thread, k = tid + 256 s. X: row b = k / (kCk kLG), slot
+    // r = k % (kCk kLG) = i kLG + l of the row's slice (consecutive threads read consecutive
+    // slots of a row); their offsets at i0 = 0 and LDS positions are fixed over the
+    // reduction. W: output o = tid % 64 for the wave-uniform (l, i) pairs p = wave + 4 s,
+    // l = p / kCk, i = p % kCk.
+    unsigned xoff[kNX];
+    int xlds[kNX];
+#pragma unroll
+    for (int s2 = 0; s2 < kNX; ++s2) {
+        const int k = tid + kThreadsC * s2;
+        const int b = k / (kCk * kLG), r = k - b * (kCk * kLG);
+        const int i = r / kLG, l = r - i * kLG;
+        xoff[s2] = l < nl ? (unsigned)((b * Cin + i) * L + l0 + l) * 4u : kOutside;
+        xlds[s2] = b * kSB + r;
+    }
+    const bool full_i = Cin % kCk == 0;  // every slice has kCk inputs
+    const bool o_ok = o0 + (tid & 63) < Cout;
+    const unsigned wcol = (unsigned)((o0 + (tid & 63)) * w_so) * 4u;
     float xr[kNX], wr[kNX];
     auto fetch = [&](int i0) {
+        const unsigned di = (unsigned)(i0 * L) * 4u;
 #pragma unroll
         for (int s2 = 0; s2 < kNX; ++s2) {
-            const int k = tid + kThreadsC * s2;
-            const int b = k / (kCk * kLG), r = k - b * (kCk * kLG);
-            const int i = r / kLG, l = r - i * kLG;
-            const unsigned xo = (i0 + i < Cin && l < nl)
-                                    ? (unsigned)((b * Cin + i0 + i) * L + l0 + l) * 4u : kOutside;
+            unsigned xo = xoff[s2] == kOutside ? kOutside : xoff[s2] + di;
+            if (!full_i) {
+                const int k = tid + kThreadsC * s2;
+                const int i = (k % (kCk * kLG)) / kLG;
+                if (i0 + i >= Cin) xo = kOutside;
+            }
             xr[s2] = bload(xs, xo);
-            const int lw = k / (kCk * kTile), rw = k - lw * (kCk * kTile);
-            const int iw = rw / kTile, o = rw - iw * kTile;
-            const unsigned wo4 = (lw < nl && i0 + iw < Cin && o0 + o < Cout)
-                                     ? (unsigned)((l0 + lw) * w_sl + (i0 + iw) * w_si + (o0 + o) * w_so) * 4u
+            const int p = wave + 4 * s2, lw = p / kCk, iw = p % kCk;  // wave-uniform
+            const unsigned wo4 = (o_ok && lw < nl && i0 + iw < Cin)
+                                     ? wcol + (unsigned)((l0 + lw) * w_sl + (i0 + iw) * w_si) * 4u
                                      : kOutside;
             wr[s2] = bload(ws, wo4);
         }
@@ -249,12 +267,9 @@ __global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
         __syncthreads();  // the previous slice is consumed
 #pragma unroll
         for (int s2 = 0; s2 < kNX; ++s2) {
-            const int k = tid + kThreadsC * s2;
-            const int b = k / (kCk * kLG), r = k - b * (kCk * kLG);
-            Xs[b * kSB + r] = xr[s2];
-            const int lw = k / (kCk * kTile), rw = k - lw * (kCk * kTile);
-            const int iw = rw / kTile, o = rw - iw * kTile;
-            Ws[lw][iw][o] = wr[s2];
+            Xs[xlds[s2]] = xr[s2];
+            const int p = wave + 4 * s2;
+            Ws[p / kCk][p % kCk][tid & 63] = wr[s2];
         }
         __syncthreads();
         if (i0 + kCk < Cin) fetch(i0 + kCk);
