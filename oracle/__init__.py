@@ -58,7 +58,7 @@ def _load():
     lib.cgo_onsite.restype = i32
     lib.cgo_onsite.argtypes = [i32, i32, i32, i64, p, p, p, p, p, p, p, p, i32]
     lib.cgo_message_pass.restype = i32
-    lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64, p, p, p, p, p, p, p, p, p,
+    lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64, p, p, p, p, p, p, p, p, p, p,
                                      p, i64, p, p, i32]
     lib.cgo_max_threads.restype = i32
     lib.cgo_max_threads.argtypes = []
@@ -170,17 +170,20 @@ def onsite(lmax, A, B, U_A, U_B, U_out_even, U_out_odd, nthreads: int = 0):
 
 
 def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
-                 U_out_even, U_out_odd, receivers=None, nthreads: int = 0):
+                 U_out_even, U_out_odd, receivers=None, nthreads: int = 0, node_flip=None):
     """Message-passing contracted product, fp64, for a receiver subset.
 
     row_ptr [N+1], col [E] (int32 CSR by receiver), edge_unit [E,3],
-    edge_radial [E,C,L], node_feat [N,C,L^2], U_*: [L,C,R].
+    edge_radial [E,C,L], node_feat [N,C,L^2] (natural-parity slot), U_*: [L,C,R].
+    node_flip: None, or the parity-flipped node slot [N,C,L^2] (Table 1, Cases C and D:
+    out_even, the natural-parity output, gains the curl coupling with it and out_odd, the
+    opposite-parity output, its Gaunt coupling).
     Returns (out_even, out_odd), each [len(receivers), C, L^2] (all receivers
     when receivers is None)."""
     if receivers is None:
         n = np.asarray(node_feat).shape[0]
-        return _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
-                        U_out_even, U_out_odd, np.arange(n), nthreads)
+        return _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U_E,
+                        U_I, U_out_even, U_out_odd, np.arange(n), nthreads)
     # Marshalling only: cut out the rows of the requested receivers and the
     # features of their senders, so large inputs are not converted to fp64 whole.
     row_ptr = np.asarray(row_ptr)
@@ -191,23 +194,31 @@ def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I
     senders, local_col = np.unique(np.asarray(col)[eidx], return_inverse=True)
     # compact graph: node q < len(rec) is receiver rec[q]; node table rows are the senders
     n_compact = max(len(rec), len(senders), 1)
-    nf_full = np.asarray(node_feat)
-    nf = np.zeros((n_compact,) + nf_full.shape[1:], dtype=np.float64)
-    nf[:len(senders)] = nf_full[senders]
+    def compact(a):
+        full = np.asarray(a)
+        out = np.zeros((n_compact,) + full.shape[1:], dtype=np.float64)
+        out[:len(senders)] = full[senders]
+        return out
+
+    nf = compact(node_feat)
+    nfl = None if node_flip is None else compact(node_flip)
     rp = np.zeros(n_compact + 1, np.int32)
     rp[1:len(rec) + 1] = np.cumsum(ends - starts)
     rp[len(rec) + 1:] = rp[len(rec)]
     return _mp_rows(lmax, rp, local_col.astype(np.int32), np.asarray(edge_unit)[eidx],
-                    np.asarray(edge_radial)[eidx], nf, U_E, U_I, U_out_even, U_out_odd,
+                    np.asarray(edge_radial)[eidx], nf, nfl, U_E, U_I, U_out_even, U_out_odd,
                     np.arange(len(rec)), nthreads)
 
 
-def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I, U_out_even,
-             U_out_odd, receivers, nthreads):
+def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U_E, U_I,
+             U_out_even, U_out_odd, receivers, nthreads):
     lib = _load()
     row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
     col = np.ascontiguousarray(col, dtype=np.int32)
     eu, er, nf = _f64(edge_unit), _f64(edge_radial), _f64(node_feat)
+    nfl = None if node_flip is None else _f64(node_flip)
+    if nfl is not None:
+        assert nfl.shape == nf.shape
     U_E, U_I, U_oe, U_oo = _f64(U_E), _f64(U_I), _f64(U_out_even), _f64(U_out_odd)
     N, C, L2 = nf.shape
     E = col.shape[0]
@@ -218,8 +229,9 @@ def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I, U_
     oe = np.zeros((rec.shape[0], C, L2))
     oo = np.zeros((rec.shape[0], C, L2))
     rc = lib.cgo_message_pass(lmax, C, R, N, E, _ptr(row_ptr), _ptr(col), _ptr(eu), _ptr(er),
-                              _ptr(nf), _ptr(U_E), _ptr(U_I), _ptr(U_oe), _ptr(U_oo), _ptr(rec),
-                              rec.shape[0], _ptr(oe), _ptr(oo), int(nthreads))
+                              _ptr(nf), _ptr(nfl), _ptr(U_E), _ptr(U_I),
+                              _ptr(U_oe), _ptr(U_oo), _ptr(rec), rec.shape[0], _ptr(oe), _ptr(oo),
+                              int(nthreads))
     if rc != 0:
         raise RuntimeError(f"cgo_message_pass failed ({rc})")
     return oe, oo

@@ -467,14 +467,21 @@ int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const doub
 /* Message passing for the receivers listed in recv[0..n_recv) (CSR by receiver):
  *   row_ptr: [N+1], col: [E] (sender of edge e), edge_unit: [E][3],
  *   edge_radial: [E][C][L] (R_{n l1}(r_ji)), node_feat: [N][C][L^2],
+ *   node_flip: NULL, or the parity-flipped node slot [N][C][L^2],
  *   U_E, U_I, U_oe, U_oo: [L][C][R];
  *   out_even, out_odd: [n_recv][C][L^2] (row q is receiver recv[q]).
+ * The edge feature R Y has natural parity, so by Table 1 (Cases A-D) the natural-parity
+ * output of degree l collects the Gaunt coupling with the natural node slot and the
+ * surface-curl coupling with the flipped slot; the opposite-parity output collects the
+ * curl coupling with the natural slot and the Gaunt coupling with the flipped slot.
+ * Both slots share the factors U_I.
  * Every (receiver, rank) pair is independent; they are spread over the threads. */
 int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const int32_t *row_ptr,
                      const int32_t *col, const double *edge_unit, const double *edge_radial,
-                     const double *node_feat, const double *U_E, const double *U_I,
-                     const double *U_oe, const double *U_oo, const int64_t *recv, long n_recv,
-                     double *out_even, double *out_odd, int nthreads)
+                     const double *node_feat, const double *node_flip, const double *U_E,
+                     const double *U_I, const double *U_oe, const double *U_oo,
+                     const int64_t *recv, long n_recv, double *out_even, double *out_odd,
+                     int nthreads)
 {
     if (lmax < 0 || C < 1 || R < 1 || n_nodes < 0 || n_edges < 0 || n_recv < 0) return -1;
     for (long q = 0; q < n_recv; ++q)
@@ -491,8 +498,9 @@ int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const i
     {
         double *E = (double *)malloc(sizeof(double) * L2);
         double *H = (double *)malloc(sizeof(double) * L2);
+        double *Hf = (double *)malloc(sizeof(double) * L2);
         double *Y = (double *)malloc(sizeof(double) * L2);
-        if (!E || !H || !Y) {
+        if (!E || !H || !Hf || !Y) {
 #pragma omp atomic write
             err = -2;
         } else {
@@ -517,10 +525,15 @@ int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const i
                     channel_contract_r(lmax, C, R, r, U_I, node_feat + (size_t)j * C * L2, H);
                     if (out_even) sparse_couple(&G, E, H, Ta + (size_t)qr * L2);
                     if (out_odd) sparse_couple(&Q, E, H, Tb + (size_t)qr * L2);
+                    if (node_flip) { /* Cases C and D: the parity-flipped slot */
+                        channel_contract_r(lmax, C, R, r, U_I, node_flip + (size_t)j * C * L2, Hf);
+                        if (out_even) sparse_couple(&Q, E, Hf, Ta + (size_t)qr * L2);
+                        if (out_odd) sparse_couple(&G, E, Hf, Tb + (size_t)qr * L2);
+                    }
                 }
             }
         }
-        free(E); free(H); free(Y);
+        free(E); free(H); free(Hf); free(Y);
     }
     if (!err) project_all(lmax, C, R, n_recv, U_oe, U_oo, Ta, Tb, out_even, out_odd);
     free(Ta); free(Tb);

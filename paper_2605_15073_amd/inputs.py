@@ -91,8 +91,12 @@ def gaussian_radial(dist: np.ndarray, r_cut: float, n_basis: int = 8) -> np.ndar
 
 
 def mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, density: float = 0.1,
-              r_cut: float = 5.0, n_basis: int = 8, distinct_out: bool = False):
-    """Draw order: positions, W_rad, I, U_E, U_I, U_out (, U_out_odd)."""
+              r_cut: float = 5.0, n_basis: int = 8, distinct_out: bool = False,
+              two_slot: bool = False):
+    """Draw order: positions, W_rad, I, U_E, U_I, U_out (, U_out_odd) (, I_flip).
+
+    two_slot adds node_flip, the parity-flipped node slot [N, C, L^2], drawn last so the
+    other arrays are the same as without it."""
     rng = np.random.default_rng(seed)
     box = (n_atoms / density) ** (1.0 / 3.0)
     pos = rng.uniform(0.0, box, size=(n_atoms, 3))
@@ -108,9 +112,12 @@ def mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, density: float
     edge_radial = np.empty((g.shape[0], C, lmax + 1), dtype=np.float32)  # [E, C, L]
     for l in range(lmax + 1):
         edge_radial[:, :, l] = g @ W_rad[l].T
-    return dict(row_ptr=row_ptr, col=col, edge_unit=edge_unit, edge_radial=edge_radial,
-                node_feat=node_feat, U_E=U_E, U_I=U_I, U_out_even=U_out, U_out_odd=U_out_odd,
-                box=box, n_edges=int(col.shape[0]))
+    out = dict(row_ptr=row_ptr, col=col, edge_unit=edge_unit, edge_radial=edge_radial,
+               node_feat=node_feat, U_E=U_E, U_I=U_I, U_out_even=U_out, U_out_odd=U_out_odd,
+               box=box, n_edges=int(col.shape[0]))
+    if two_slot:
+        out["node_flip"] = coefficients(rng, n_atoms, C, lmax, per_degree=False)
+    return out
 
 
 @dataclass(frozen=True)
@@ -125,12 +132,14 @@ class Workload:
     per_degree: bool = False
     self_coupled: bool = False
     r_cut: float = 5.0
+    two_slot: bool = False   # message passing with both node parity slots (Cases A-D)
 
     def make(self, **kw):
         if self.kind == "onsite":
             return onsite_inputs(self.n, self.lmax, self.C, self.R, self.seed,
                                  per_degree=self.per_degree, self_coupled=self.self_coupled, **kw)
-        return mp_inputs(self.n, self.lmax, self.C, self.R, self.seed, r_cut=self.r_cut, **kw)
+        return mp_inputs(self.n, self.lmax, self.C, self.R, self.seed, r_cut=self.r_cut,
+                         two_slot=self.two_slot, **kw)
 
 
 # The five workloads of the benchmark plan, named by what they are.
@@ -142,4 +151,8 @@ WORKLOADS = {
     "onsite_n4096_l12_c128": Workload("onsite_n4096_l12_c128", "onsite", 4096, 12, 128, 128,
                                       seed=3, per_degree=True),
     "mp_5k_l20_c64": Workload("mp_5k_l20_c64", "mp", 5000, 20, 64, 64, seed=4),
+    # both node parity slots populated (natural and parity-flipped), Cases A-D of Table 1
+    "mp2_10k_l6_c128": Workload("mp2_10k_l6_c128", "mp", 10000, 6, 128, 128, seed=2,
+                                two_slot=True),
+    "mp2_5k_l20_c64": Workload("mp2_5k_l20_c64", "mp", 5000, 20, 64, 64, seed=4, two_slot=True),
 }
