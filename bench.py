@@ -53,13 +53,14 @@ def grid_dims(lmax: int):
 
 # ---------------------------------------------------------------- algorithmic work
 
-def receiver_bytes(lmax: int, R: int, N: int, E: int) -> int:
+def receiver_bytes(lmax: int, R: int, N: int, E: int, slots: int = 1) -> int:
     """HBM bytes the receiver pass must move (fp32): per edge the three sender grid
-    fields (3 R UV), the edge radial coefficients (R L), the unit vector and the
-    sender index; per receiver the row pointer and the two analysed fields (2 R K)."""
+    fields (3 R UV) of every node slot, the edge radial coefficients (R L), the unit
+    vector and the sender index; per receiver the row pointer and the two analysed
+    fields (2 R K)."""
     U, V = grid_dims(lmax)
     L, K = lmax + 1, (lmax + 1) ** 2
-    per_edge = 4 * (3 * R * U * V + R * L + 3 + 1)
+    per_edge = 4 * (3 * slots * R * U * V + R * L + 3 + 1)
     per_recv = 4 * (1 + 2 * R * K)
     return E * per_edge + N * per_recv
 
@@ -115,7 +116,7 @@ def cpu_baseline(w, d, budget_s: float = 15.0):
     if w.kind == "mp":
         def run(n):
             return oracle.message_pass(w.lmax, *(d[k] for k in MP_KEYS),
-                                       receivers=np.arange(n))
+                                       receivers=np.arange(n), node_flip=d.get("node_flip"))
         unit_name = "receivers"
     else:
         def run(n):
@@ -146,15 +147,17 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
     if w.kind == "mp":
-        t = to_dev(d, MP_KEYS)
+        two = w.two_slot
+        t = to_dev(d, MP_KEYS + (("node_flip",) if two else ()))
         E = int(d["n_edges"])
-        op = cg.CGTP_OP_MESSAGE_PASS
+        op = cg.CGTP_OP_MESSAGE_PASS_TWO_SLOT if two else cg.CGTP_OP_MESSAGE_PASS
         ws = torch.empty(cg.workspace_bytes(plan, op, w.n, E), dtype=torch.uint8, device="cuda")
         oe = torch.empty_like(t["node_feat"])
         oo = torch.empty_like(t["node_feat"])
 
         def step():
-            cg.message_pass(plan, *(t[k] for k in MP_KEYS), out_even=oe, out_odd=oo, workspace=ws)
+            cg.message_pass(plan, *(t[k] for k in MP_KEYS), out_even=oe, out_odd=oo, workspace=ws,
+                            node_flip=t.get("node_flip"))
     else:
         t = to_dev(d, ONSITE_KEYS)
         if w.self_coupled:
@@ -197,7 +200,9 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "kind": "message_passing" if w.kind == "mp" else "onsite",
+        "config": {"workload": w.name,
+                   "kind": ("message_passing_two_slot" if w.two_slot else "message_passing")
+                   if w.kind == "mp" else "onsite",
                    "nodes": w.n, "edges": E, "lmax": w.lmax, "channels": w.C, "rank": w.R,
                    "grid": f"{U}x{V}", "seed": w.seed},
         "stages_ms": {k: round(v, 4) for k, v in stage_avg.items()},
@@ -205,7 +210,7 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
     }
     t_dom = stage_avg[dom] / 1e3
     if w.kind == "mp" and dom == "receiver":
-        alg = receiver_bytes(w.lmax, w.R, w.n, E)
+        alg = receiver_bytes(w.lmax, w.R, w.n, E, 2 if w.two_slot else 1)
         traffic = load_traffic(w.name)
         rec["roofline"] = {"bound": "hbm", "achieved": alg / t_dom / 1e9, "peak": HBM_PEAK_GBS,
                            "unit": "GB/s", "frac": alg / t_dom / 1e9 / HBM_PEAK_GBS,

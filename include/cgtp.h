@@ -77,9 +77,10 @@ extern "C" {
 #define CGTP_TIME_STAGES 4u    /* record HIP events between the kernel stages of every call
                                   (read with cgtp_stage_times) */
 
-/* operations for cgtp_workspace_bytes */
+/* operations for cgtp_workspace_bytes and cgtp_stage_times */
 #define CGTP_OP_ONSITE 0
 #define CGTP_OP_MESSAGE_PASS 1
+#define CGTP_OP_MESSAGE_PASS_TWO_SLOT 2
 
 typedef struct cgtp_plan_s *cgtp_plan;
 
@@ -155,6 +156,27 @@ int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                       void *out_even, void *out_odd, void *workspace, size_t ws_bytes,
                       void *stream);
 
+/* Message passing with both node parity slots (Table 1, Cases A-D; Eqs.
+ * cat-alpha-slot and cat-beta-slot): each sender carries a natural-parity slot
+ * node_feat (parity (-1)^l2) and a parity-flipped slot node_flip (parity -(-1)^l2),
+ * contracted with the same factors U_I. The edge feature R Y has natural parity,
+ * so by the parity rule p = p1 p2 the outputs of degree l are
+ *   out_even (parity (-1)^l)  = Gaunt(edge, node_feat) + curl(edge, node_flip)
+ *   out_odd  (parity -(-1)^l) = curl(edge, node_feat)  + Gaunt(edge, node_flip)
+ * (Cases A and D feed out_even, Cases B and C out_odd), each projected with its own
+ * factors U_out_even / U_out_odd. Arguments are those of cgtp_message_pass plus
+ *   node_flip [N][C][K]      sender features in the parity-flipped slot.
+ * The workspace is cgtp_workspace_bytes(CGTP_OP_MESSAGE_PASS_TWO_SLOT). With
+ * node_flip all zero the result equals cgtp_message_pass on node_feat.
+ * Errors: those of cgtp_message_pass; CGTP_ERR_UNSUPPORTED for a plan created
+ * with CGTP_EDGE_SEPARATED. */
+int cgtp_message_pass_two_slot(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
+                               const int32_t *row_ptr, const int32_t *col, const void *edge_unit,
+                               const void *edge_radial, const void *node_feat,
+                               const void *node_flip, const void *U_E, const void *U_I,
+                               const void *U_out_even, const void *U_out_odd, void *out_even,
+                               void *out_odd, void *workspace, size_t ws_bytes, void *stream);
+
 /* Per-stage GPU time of the calls made since the previous cgtp_stage_times on
  * this plan (plan created with CGTP_TIME_STAGES), in the spirit of the paper's
  * per-step breakdown (App. D, Table 4). Waits for the recorded events, writes the
@@ -164,7 +186,8 @@ int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
  * analysis, 3 project even, 4 project odd. Stages of CGTP_OP_MESSAGE_PASS:
  * 0 contract node features, 1 sender grid fields, 2 contract edge radial,
  * 3 receiver pass (edge synthesis, products, neighbour sum, analysis),
- * 4 project even, 5 project odd. A skipped stage counts as 0.
+ * 4 project even, 5 project odd. CGTP_OP_MESSAGE_PASS_TWO_SLOT has the same six
+ * stages, each covering both node slots. A skipped stage counts as 0.
  * Errors: CGTP_ERR_ARG (NULL, flag not set, unknown op), CGTP_ERR_HIP. */
 int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages, int *n_calls);
 

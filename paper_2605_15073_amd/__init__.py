@@ -27,11 +27,12 @@ CGTP_EDGE_SEPARATED = 2
 CGTP_TIME_STAGES = 4
 CGTP_OP_ONSITE = 0
 CGTP_OP_MESSAGE_PASS = 1
+CGTP_OP_MESSAGE_PASS_TWO_SLOT = 2
 CGTP_MAX_LMAX = 24
 
 EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
-            "cgtp_message_pass", "cgtp_stage_times", "cgtp_destroy", "cgtp_status_string",
-            "cgtp_last_error", "cgtp_host_tables")
+            "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_stage_times",
+            "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables")
 ONSITE_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis", "project_even",
                  "project_odd")
 MP_STAGES = ("contract_node", "sender_fields", "contract_edge_radial", "receiver",
@@ -68,6 +69,7 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_workspace_bytes.argtypes = [vp, i32, i64, i64, ctypes.POINTER(sz)]
     lib.cgtp_onsite.argtypes = [vp, i64] + [vp] * 8 + [vp, sz, vp]
     lib.cgtp_message_pass.argtypes = [vp, i64, i64] + [vp] * 11 + [vp, sz, vp]
+    lib.cgtp_message_pass_two_slot.argtypes = [vp, i64, i64] + [vp] * 12 + [vp, sz, vp]
     lib.cgtp_stage_times.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double), i32,
                                      ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.cgtp_destroy.argtypes = [vp]
@@ -77,7 +79,8 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_last_error.restype = ctypes.c_char_p
     lib.cgtp_host_tables.argtypes = [i32, i32, i32] + [vp] * 5
     for name in ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
-                 "cgtp_message_pass", "cgtp_stage_times", "cgtp_destroy", "cgtp_host_tables"):
+                 "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_stage_times",
+                 "cgtp_destroy", "cgtp_host_tables"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib
@@ -203,9 +206,11 @@ def onsite(plan: Plan, A, B, U_A, U_B, U_out_even, U_out_odd, out_even=None, out
 
 def message_pass(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
                  U_out_even, U_out_odd, out_even=None, out_odd=None, workspace=None,
-                 stream=None):
-    """cgtp_message_pass. row_ptr [N+1], col [E] int32; edge_unit [E, 3];
-    edge_radial [E, C, L]; node_feat [N, C, K]; U_* [L, C, R]; outputs [N, C, K]."""
+                 stream=None, node_flip=None):
+    """cgtp_message_pass (or cgtp_message_pass_two_slot when node_flip is given).
+    row_ptr [N+1], col [E] int32; edge_unit [E, 3]; edge_radial [E, C, L];
+    node_feat [N, C, K] (natural-parity slot); node_flip [N, C, K] (parity-flipped slot);
+    U_* [L, C, R]; outputs [N, C, K]."""
     torch = _torch()
     N = node_feat.shape[0]
     E = col.shape[0]
@@ -215,6 +220,8 @@ def message_pass(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_feat, U_
     _want(plan, "edge_unit", edge_unit, (E, 3))
     _want(plan, "edge_radial", edge_radial, (E, plan.channels, L))
     _want(plan, "node_feat", node_feat, (N, plan.channels, L * L))
+    if node_flip is not None:
+        _want(plan, "node_flip", node_flip, (N, plan.channels, L * L))
     for nm, U in (("U_E", U_E), ("U_I", U_I)):
         _want(plan, nm, U, (L, plan.channels, plan.rank))
     outs = []
@@ -230,10 +237,16 @@ def message_pass(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_feat, U_
     ws_ptr, ws_len = None, 0
     if workspace is not None:
         ws_ptr, ws_len = _ptr(workspace), workspace.numel() * workspace.element_size()
-    _check(load_library().cgtp_message_pass(
-        plan.handle, N, E, _ptr(row_ptr), _ptr(col), _ptr(edge_unit), _ptr(edge_radial),
-        _ptr(node_feat), _ptr(U_E), _ptr(U_I), _ptr(U_out_even), _ptr(U_out_odd), _ptr(outs[0]),
-        _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)), "cgtp_message_pass")
+    lib = load_library()
+    head = (plan.handle, N, E, _ptr(row_ptr), _ptr(col), _ptr(edge_unit), _ptr(edge_radial),
+            _ptr(node_feat))
+    tail = (_ptr(U_E), _ptr(U_I), _ptr(U_out_even), _ptr(U_out_odd), _ptr(outs[0]),
+            _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream))
+    if node_flip is None:
+        _check(lib.cgtp_message_pass(*head, *tail), "cgtp_message_pass")
+    else:
+        _check(lib.cgtp_message_pass_two_slot(*head, _ptr(node_flip), *tail),
+               "cgtp_message_pass_two_slot")
     return outs[0], outs[1]
 
 

@@ -105,10 +105,12 @@ hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const f
 // Message-passing receiver pass: per receiver, synthesise the edge fields, multiply
 // with the streamed sender fields, sum over the CSR row, then the inverse transforms.
 // Rt is the edge-radial contraction in the layout [E][L][R].
+// SFf: NULL, or the sender fields of the parity-flipped node slot (two-slot message
+// passing; not with the separated edge field).
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
-                           const T *Rt, const T *SF, T *Ta, T *Tb, hipStream_t s);
+                           const T *Rt, const T *SF, const T *SFf, T *Ta, T *Tb, hipStream_t s);
 
 // fp32 folded inverse transforms (folded.hip), lmax <= 24; hipErrorNotSupported when
 // the LDS staging does not fit.
@@ -145,7 +147,7 @@ bool receiver_mfma_supported(const Dims &d, int R);
 size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R);
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
-                                const float *SF, bool sf_chunked, float *S, float *Ta, float *Tb,
-                                hipStream_t s);
+                                const float *SF, const float *SFf, bool sf_chunked, float *S,
+                                float *Ta, float *Tb, hipStream_t s);
 
 }  // namespace cgtp

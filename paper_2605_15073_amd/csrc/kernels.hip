@@ -298,11 +298,13 @@ __device__ __forceinline__ double buf_load<double>(__amdgpu_buffer_rsrc_t rs, un
     return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0));
 }
 
-template <typename T, int RB, int NPT, bool FULL>
+// TWO: the senders carry a second, parity-flipped node slot SFf (same layout as SF). By
+// Table 1 its Gaunt product then feeds Tb and its curl product Ta.
+template <typename T, int RB, int NPT, bool FULL, bool TWO>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
     const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ SF,
-    T *__restrict__ Ta, T *__restrict__ Tb)
+    const T *__restrict__ SFf, T *__restrict__ Ta, T *__restrict__ Tb)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
@@ -360,19 +362,27 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
         const int UVs = d.UVs;
         const __amdgpu_buffer_rsrc_t sfr =
             make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs, (unsigned)(nr * 3 * UVs * sizeof(T)));
+        const __amdgpu_buffer_rsrc_t sff =
+            make_rsrc((TWO ? SFf : SF) + (j * R + r0) * 3 * (int64_t)UVs,
+                      (unsigned)(nr * 3 * UVs * sizeof(T)));
         const unsigned fstride = (unsigned)(UVs * sizeof(T));
 #pragma unroll
         for (int s = 0; s < NPT; ++s) {
             const int uv = uvs[s];
             if (uv >= UV) continue;
             const unsigned voff = (unsigned)(uv * sizeof(T));
-            T fI[RB], fX[RB], fP[RB];
+            T fI[RB], fX[RB], fP[RB], gI[RB], gX[RB], gP[RB];
 #pragma unroll
             for (int q = 0; q < RB; ++q) {
                 // ranks past nr fall outside the descriptor's range and read 0
                 fI[q] = buf_load<T>(sfr, voff, (3 * q) * fstride);
                 fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
                 fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
+                if (TWO) {
+                    gI[q] = buf_load<T>(sff, voff, (3 * q) * fstride);
+                    gX[q] = buf_load<T>(sff, voff, (3 * q + 1) * fstride);
+                    gP[q] = buf_load<T>(sff, voff, (3 * q + 2) * fstride);
+                }
             }
     const T h = ux * pcp[s] + uy * psp[s];
             const T t = uz * px[s] + psx[s] * h;
@@ -410,6 +420,10 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
             for (int q = 0; q < RB; ++q) {
                 sa[s][q] += a[q] * fI[q];
                 sb[s][q] += g[q] * (dpt * fX[q] - dxt * fP[q]);
+                if (TWO) {
+                    sa[s][q] += g[q] * (dpt * gX[q] - dxt * gP[q]);
+                    sb[s][q] += a[q] * gI[q];
+                }
             }
         }
     }
@@ -527,12 +541,13 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
-                           const T *Rt, const T *SF, T *Ta, T *Tb, hipStream_t s)
+                           const T *Rt, const T *SF, const T *SFf, T *Ta, T *Tb, hipStream_t s)
 {
     int64_t blocks = N * R;
     if (blocks == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (separated) {
+        if (SFf) return hipErrorNotSupported;
         size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + d.K + 2 * d.M * d.U);
         hipLaunchKernelGGL(k_receiver_separated<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s,
                            tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb);
@@ -541,15 +556,22 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + 2 * d.M * d.U);
     const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
     const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
-#define CGTP_RECV(RBV, NP)                                                                     \
+#define CGTP_RECV_TW(RBV, NP, TW)                                                              \
     do {                                                                                       \
         int64_t nb = N * ((R + RBV - 1) / RBV);                                                \
         if (R % RBV == 0)                                                                      \
-            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true>), dim3((unsigned)nb),       \
-                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb); \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true, TW>), dim3((unsigned)nb),   \
+                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, SFf,   \
+                               Ta, Tb);                                                        \
         else                                                                                   \
-            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false>), dim3((unsigned)nb),      \
-                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb); \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false, TW>), dim3((unsigned)nb),  \
+                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, SFf,   \
+                               Ta, Tb);                                                        \
+    } while (0)
+#define CGTP_RECV(RBV, NP)                 \
+    do {                                   \
+        if (SFf) CGTP_RECV_TW(RBV, NP, true);  \
+        else CGTP_RECV_TW(RBV, NP, false); \
     } while (0)
     // ranks per block: sized so the per-thread accumulators and in-flight loads fit in
     // registers without spilling (fp64 values take two registers)
@@ -559,6 +581,7 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     else if (npt <= 2) CGTP_RECV(rb2, 2);
     else CGTP_RECV(2, 3);
 #undef CGTP_RECV
+#undef CGTP_RECV_TW
     return hipGetLastError();
 }
 
@@ -569,7 +592,7 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                                               const T *, T *, T *, hipStream_t);                 \
     template hipError_t launch_receiver<T>(const Tabs<T> &, bool, int64_t, int, const int32_t *, \
                                            const int32_t *, const T *, const T *, const T *,     \
-                                           T *, T *, hipStream_t);
+                                           const T *, T *, T *, hipStream_t);
 
 CGTP_INSTANTIATE(float)
 CGTP_INSTANTIATE(double)

@@ -29,8 +29,8 @@ struct cgtp_plan_s {
     size_t own_ws_bytes;
     std::vector<EventSet> timers;  // reused across calls; timers_used are pending
     size_t timers_used;
-    double stage_acc[2][kMaxStages];  // drained sums per op (onsite, message pass)
-    int stage_calls[2];
+    double stage_acc[3][kMaxStages];  // drained sums per op (onsite, message pass, two-slot)
+    int stage_calls[3];
 };
 
 namespace {
@@ -68,6 +68,7 @@ size_t max_lds_bytes(const cgtp::Dims &d, size_t es)
 struct Layout {
     size_t off[6];
     size_t total;
+    size_t hf = 0, sff = 0;  // offsets of the flipped slot from HI and from SF (two slots)
 };
 
 // Receiver on MFMA: fp32, zonal edge field, R a multiple of 16, lmax high enough that the
@@ -97,10 +98,12 @@ Layout onsite_layout(const cgtp_plan_s *p, int64_t N)
 }
 
 // Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],
-// and, for the MFMA receiver, the summed grid fields S [N][R][2][UVs].
-Layout mp_layout(const cgtp_plan_s *p, int64_t N, int64_t E)
+// and, for the MFMA receiver, the summed grid fields S [N][R][2][UVs]. With two node slots,
+// HI and SF hold the natural slot followed by the flipped one.
+Layout mp_layout(const cgtp_plan_s *p, int64_t N, int64_t E, bool two = false)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
+    const size_t slots = two ? 2 : 1;
     size_t h = align256(es * (size_t)N * p->R * p->d.K);
     const size_t sf_pts = sf_chunked(p) ? (size_t)cgtp::sf_chunks(p->d) * cgtp::kSfChunk : p->d.UVs;
     size_t sf = align256(es * (size_t)N * p->R * 3 * sf_pts);
@@ -108,12 +111,14 @@ Layout mp_layout(const cgtp_plan_s *p, int64_t N, int64_t E)
     size_t sg = use_mfma_receiver(p) ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, p->R)) : 0;
     Layout l{};
     l.off[0] = 0;
-    l.off[1] = h;
-    l.off[2] = h + sf;
-    l.off[3] = h + sf + rt;
-    l.off[4] = 2 * h + sf + rt;
-    l.off[5] = 3 * h + sf + rt;
-    l.total = 3 * h + sf + rt + sg;
+    l.off[1] = slots * h;
+    l.off[2] = slots * (h + sf);
+    l.off[3] = slots * (h + sf) + rt;
+    l.off[4] = slots * (h + sf) + rt + h;
+    l.off[5] = slots * (h + sf) + rt + 2 * h;
+    l.total = slots * (h + sf) + rt + 2 * h + sg;
+    l.hf = h;
+    l.sff = sf;
     return l;
 }
 
@@ -277,38 +282,49 @@ int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const vo
 
 template <typename T>
 int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const int32_t *col,
-           const void *unit, const void *rad, const void *I, const void *UE, const void *UI,
-           const void *Uoe, const void *Uoo, void *oe, void *oo, char *ws, hipStream_t s)
+           const void *unit, const void *rad, const void *I, const void *If, const void *UE,
+           const void *UI, const void *Uoe, const void *Uoo, void *oe, void *oo, char *ws,
+           hipStream_t s)
 {
     const cgtp::Dims &d = p->d;
     const int C = p->C, R = p->R;
     const bool separated = (p->flags & CGTP_EDGE_SEPARATED) != 0;
+    const bool two = If != nullptr;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
-    Layout lay = mp_layout(p, N, E);
+    Layout lay = mp_layout(p, N, E, two);
     T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
     T *SF = reinterpret_cast<T *>(ws + lay.off[1]);
     T *Rt = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Ta = reinterpret_cast<T *>(ws + lay.off[3]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
+    T *HIf = two ? reinterpret_cast<T *>(ws + lay.off[0] + lay.hf) : nullptr;
+    T *SFf = two ? reinterpret_cast<T *>(ws + lay.off[1] + lay.sff) : nullptr;
     const int64_t sl = (int64_t)C * R;
     StageRec rec;
-    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS, 6, s);
+    int st = rec.begin(p, two ? CGTP_OP_MESSAGE_PASS_TWO_SLOT : CGTP_OP_MESSAGE_PASS, 6, s);
     if (st) return st;
     hipError_t e;
-    // Eq. msgpass-HI, then the node-side forward transforms (Eqs. msgpass-FI, msgpass-AI)
-    e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UI, sl, R, 1, (const T *)I, HI,
-                                 (int64_t)R * d.K, d.K, 1, nullptr, s);
-    if (e != hipSuccess) return hip_fail(e, "contract node features");
-    rec.mark();
-    if constexpr (sizeof(T) == 4) {
-        if (sf_chunked(p))
-            e = cgtp::launch_sender_mfma(tb, N, R, HI, SF, true, s);
-        else
-            e = cgtp::launch_sender_fields<T>(tb, N, R, HI, SF, s);
-    } else {
-        e = cgtp::launch_sender_fields<T>(tb, N, R, HI, SF, s);
+    // Eq. msgpass-HI, then the node-side forward transforms (Eqs. msgpass-FI, msgpass-AI),
+    // for each node slot
+    for (int slot = 0; slot < (two ? 2 : 1); ++slot) {
+        e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UI, sl, R, 1,
+                                     (const T *)(slot ? If : I), slot ? HIf : HI,
+                                     (int64_t)R * d.K, d.K, 1, nullptr, s);
+        if (e != hipSuccess) return hip_fail(e, "contract node features");
     }
-    if (e != hipSuccess) return hip_fail(e, "sender fields");
+    rec.mark();
+    for (int slot = 0; slot < (two ? 2 : 1); ++slot) {
+        T *h = slot ? HIf : HI, *sf = slot ? SFf : SF;
+        if constexpr (sizeof(T) == 4) {
+            if (sf_chunked(p))
+                e = cgtp::launch_sender_mfma(tb, N, R, h, sf, true, s);
+            else
+                e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s);
+        } else {
+            e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s);
+        }
+        if (e != hipSuccess) return hip_fail(e, "sender fields");
+    }
     rec.mark();
     // Eq. msgpass-tildeR into Rt [E][L][R] (the zonal form folds in the addition-theorem
     // weight (2l+1)/(4 pi))
@@ -320,14 +336,14 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
         if (use_mfma_receiver(p)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
             e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt, SF,
-                                           sf_chunked(p), Sg, Ta, Tb, s);
+                                           SFf, sf_chunked(p), Sg, Ta, Tb, s);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
             goto projections;
         }
     }
-    e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, SF, Ta,
-                                 Tb, s);
+    e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, SF, SFf,
+                                 Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "receiver");
     rec.mark();
 projections:
@@ -452,6 +468,8 @@ int cgtp_workspace_bytes(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edge
     if (n_nodes < 0 || n_edges < 0) return fail(CGTP_ERR_ARG, "negative size");
     if (op == CGTP_OP_ONSITE) *bytes = onsite_layout(plan, n_nodes).total;
     else if (op == CGTP_OP_MESSAGE_PASS) *bytes = mp_layout(plan, n_nodes, n_edges).total;
+    else if (op == CGTP_OP_MESSAGE_PASS_TWO_SLOT)
+        *bytes = mp_layout(plan, n_nodes, n_edges, true).total;
     else return fail(CGTP_ERR_ARG, "unknown op %d", op);
     return CGTP_OK;
 }
@@ -483,11 +501,15 @@ int cgtp_onsite(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B, c
                              out_odd, static_cast<char *>(ws), s);
 }
 
-int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,
+namespace {
+
+// Shared by the one- and two-slot entry points (node_flip NULL for one slot).
+int message_pass_impl(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,
                       const int32_t *col, const void *edge_unit, const void *edge_radial,
-                      const void *node_feat, const void *U_E, const void *U_I,
-                      const void *U_out_even, const void *U_out_odd, void *out_even, void *out_odd,
-                      void *workspace, size_t ws_bytes, void *stream)
+                      const void *node_feat, const void *node_flip, const void *U_E,
+                      const void *U_I, const void *U_out_even, const void *U_out_odd,
+                      void *out_even, void *out_odd, void *workspace, size_t ws_bytes,
+                      void *stream)
 {
     g_err[0] = 0;
     if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
@@ -505,6 +527,10 @@ int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
         return fail(CGTP_ERR_ARG, "NULL output projection");
     if (n_nodes * (int64_t)plan->R > 0x7fffffffLL)
         return fail(CGTP_ERR_UNSUPPORTED, "n_nodes * rank exceeds 2^31 - 1");
+    const bool two = node_flip != nullptr;
+    if (two && (plan->flags & CGTP_EDGE_SEPARATED))
+        return fail(CGTP_ERR_UNSUPPORTED,
+                    "two node slots are built for the zonal edge field, not CGTP_EDGE_SEPARATED");
     int st = check_device(plan);
     if (st) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -513,15 +539,45 @@ int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
         if (st) return st;
     }
     void *ws = nullptr;
-    st = get_workspace(plan, mp_layout(plan, n_nodes, n_edges).total, workspace, ws_bytes, &ws);
+    st = get_workspace(plan, mp_layout(plan, n_nodes, n_edges, two).total, workspace, ws_bytes,
+                       &ws);
     if (st) return st;
     if (plan->dtype == CGTP_F64)
         return run_mp<double>(plan, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial,
-                              node_feat, U_E, U_I, U_out_even, U_out_odd, out_even, out_odd,
-                              static_cast<char *>(ws), s);
+                              node_feat, node_flip, U_E, U_I, U_out_even, U_out_odd, out_even,
+                              out_odd, static_cast<char *>(ws), s);
     return run_mp<float>(plan, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial, node_feat,
-                         U_E, U_I, U_out_even, U_out_odd, out_even, out_odd,
+                         node_flip, U_E, U_I, U_out_even, U_out_odd, out_even, out_odd,
                          static_cast<char *>(ws), s);
+}
+
+}  // namespace
+
+int cgtp_message_pass(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,
+                      const int32_t *col, const void *edge_unit, const void *edge_radial,
+                      const void *node_feat, const void *U_E, const void *U_I,
+                      const void *U_out_even, const void *U_out_odd, void *out_even, void *out_odd,
+                      void *workspace, size_t ws_bytes, void *stream)
+{
+    return message_pass_impl(plan, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial,
+                             node_feat, nullptr, U_E, U_I, U_out_even, U_out_odd, out_even,
+                             out_odd, workspace, ws_bytes, stream);
+}
+
+int cgtp_message_pass_two_slot(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
+                               const int32_t *row_ptr, const int32_t *col, const void *edge_unit,
+                               const void *edge_radial, const void *node_feat,
+                               const void *node_flip, const void *U_E, const void *U_I,
+                               const void *U_out_even, const void *U_out_odd, void *out_even,
+                               void *out_odd, void *workspace, size_t ws_bytes, void *stream)
+{
+    if (n_nodes > 0 && !node_flip) {
+        g_err[0] = 0;
+        return fail(CGTP_ERR_ARG, "NULL input (node_flip)");
+    }
+    return message_pass_impl(plan, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial,
+                             node_feat, node_flip, U_E, U_I, U_out_even, U_out_odd, out_even,
+                             out_odd, workspace, ws_bytes, stream);
 }
 
 int cgtp_destroy(cgtp_plan plan)
@@ -544,7 +600,7 @@ int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages,
         return fail(CGTP_ERR_ARG, "plan was created without CGTP_TIME_STAGES");
     int ns;
     if (op == CGTP_OP_ONSITE) ns = 5;
-    else if (op == CGTP_OP_MESSAGE_PASS) ns = 6;
+    else if (op == CGTP_OP_MESSAGE_PASS || op == CGTP_OP_MESSAGE_PASS_TWO_SLOT) ns = 6;
     else return fail(CGTP_ERR_ARG, "unknown op %d", op);
     int status = drain_timers(plan);
     for (int k = 0; k < ns && k < cap; ++k) ms[k] = plan->stage_acc[op][k];

@@ -49,13 +49,17 @@ __device__ __forceinline__ void wave_sync()
 // the Legendre recurrence for P_l and P_l' at its own point (both in the same lane) into
 // wave-private LDS, then the wave multiplies those [64 points x L] values with the
 // [L x 16 ranks] edge coefficients on the matrix cores.
-template <int WPB, int LM>
+// TWO: the senders carry a second, parity-flipped node slot SFf (same layout as SF); by
+// Table 1 its curl product then feeds S_alpha's slot (natural parity) and its Gaunt
+// product S_beta's. The next edge is prefetched only with one slot (registers).
+template <int WPB, int LM, bool TWO>
 __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
                                                             const int32_t *__restrict__ row_ptr,
                                                             const int32_t *__restrict__ col,
                                                             const float *__restrict__ unit,
                                                             const float *__restrict__ Rt,
                                                             const float *__restrict__ SF,
+                                                            const float *__restrict__ SFf,
                                                             int sf_nc, float *__restrict__ S)
 {
     constexpr int TPW = 4;           // 16-point tiles per wave
@@ -110,17 +114,19 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     const int fstride = sf_nc ? kSfChunk : UVs;  // field stride, elements
     const unsigned voff = sf_nc ? (unsigned)((n * 3 * kSfChunk + 4 * g) * 4)
                                 : (unsigned)((n * 3 * UVs + pw0 + 4 * g) * 4);
-    const float *sfb = sf_nc ? SF + ((int64_t)(r0 / kRT) * sf_nc + pw0 / kSfChunk) * NN * (kRT * 3 * kSfChunk)
-                             : SF + (int64_t)r0 * 3 * UVs;
+    const int64_t sfo = sf_nc ? ((int64_t)(r0 / kRT) * sf_nc + pw0 / kSfChunk) * NN * (kRT * 3 * kSfChunk)
+                              : (int64_t)r0 * 3 * UVs;
+    const float *sfb = SF + sfo;
+    const float *sfbf = (TWO ? SFf : SF) + sfo;
     const int64_t jstride = sf_nc ? (int64_t)kRT * 3 * kSfChunk : (int64_t)R * 3 * UVs;
     const unsigned sfbytes = (unsigned)(kRT * 3 * fstride * 4);
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     // sender fields of edge e (cur) and e + 1 (nxt): the next edge's loads are in flight
     // while this one is computed
     float4_t cI[TPW], cX[TPW], cP[TPW];
-    auto load_fields = [&](int e, float4_t *fI, float4_t *fX, float4_t *fP) {
+    auto load_fields = [&](const float *base, int e, float4_t *fI, float4_t *fX, float4_t *fP) {
         const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
-        const __amdgpu_buffer_rsrc_t sfr = rsrc(sfb + j * jstride, sfbytes);
+        const __amdgpu_buffer_rsrc_t sfr = rsrc(base + j * jstride, sfbytes);
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
             const unsigned so = (unsigned)(t * 16 * 4);
@@ -129,16 +135,21 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
             fP[t] = bload4(sfr, voff, so + 2 * fstride * 4);
         }
     };
-    if (e0 < e1) load_fields(e0, cI, cX, cP);
+    if (!TWO && e0 < e1) load_fields(sfb, e0, cI, cX, cP);
     for (int e = e0; e < e1; ++e) {
-        float4_t fI[TPW], fX[TPW], fP[TPW];
+        float4_t fI[TPW], fX[TPW], fP[TPW], hI[TPW], hX[TPW], hP[TPW];
+        if (TWO) {
+            load_fields(sfb, e, fI, fX, fP);
+            load_fields(sfbf, e, hI, hX, hP);
+        } else {
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) {
-            fI[t] = cI[t];
-            fX[t] = cX[t];
-            fP[t] = cP[t];
+            for (int t = 0; t < TPW; ++t) {
+                fI[t] = cI[t];
+                fX[t] = cX[t];
+                fP[t] = cP[t];
+            }
+            if (e + 1 < e1) load_fields(sfb, e + 1, cI, cX, cP);
         }
-        if (e + 1 < e1) load_fields(e + 1, cI, cX, cP);
         float ux = unit[3 * (int64_t)e], uy = unit[3 * (int64_t)e + 1], uz = unit[3 * (int64_t)e + 2];
         const float inv = 1.f / sqrtf(ux * ux + uy * uy + uz * uz);
         ux *= inv;
@@ -197,6 +208,10 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
                 const float dxt = dxs[pl], dpt = dps[pl];
                 sa[t][jj] += a[jj] * fI[t][jj];
                 sb[t][jj] += gg[jj] * (dpt * fX[t][jj] - dxt * fP[t][jj]);
+                if (TWO) {
+                    sa[t][jj] += gg[jj] * (dpt * hX[t][jj] - dxt * hP[t][jj]);
+                    sb[t][jj] += a[jj] * hI[t][jj];
+                }
             }
         }
     }
@@ -287,8 +302,8 @@ size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R)
 
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
-                                const float *SF, bool sf_chunked, float *S, float *Ta, float *Tb,
-                                hipStream_t s)
+                                const float *SF, const float *SFf, bool sf_chunked, float *S,
+                                float *Ta, float *Tb, hipStream_t s)
 {
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
@@ -304,8 +319,14 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     switch (d.lmax) {
 #define CGTP_CASE(LMV)                                                                          \
     case LMV:                                                                                   \
-        hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV>), dim3((unsigned)blocks), dim3(64 * WPB), sh, s, \
-                           tb, R, nchunks, row_ptr, col, unit, Rt, SF, sf_nc, S);               \
+        if (SFf)                                                                                \
+            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, true>), dim3((unsigned)blocks),       \
+                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt, SF, \
+                               SFf, sf_nc, S);                                                  \
+        else                                                                                    \
+            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, false>), dim3((unsigned)blocks),      \
+                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt, SF, \
+                               SFf, sf_nc, S);                                                  \
         break;
         CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11) CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
         CGTP_CASE(15) CGTP_CASE(16) CGTP_CASE(17) CGTP_CASE(18) CGTP_CASE(19) CGTP_CASE(20)
