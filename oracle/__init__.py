@@ -56,10 +56,9 @@ def _load():
     lib.cgo_real_sh.restype = None
     lib.cgo_real_sh.argtypes = [i32, dbl, dbl, dbl, p]
     lib.cgo_onsite.restype = i32
-    lib.cgo_onsite.argtypes = [i32, i32, i32, i64, p, p, p, p, p, p, p, p, i32]
+    lib.cgo_onsite.argtypes = [i32, i32, i32, i64] + [p] * 12 + [i32]
     lib.cgo_message_pass.restype = i32
-    lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64, p, p, p, p, p, p, p, p, p, p,
-                                     p, i64, p, p, i32]
+    lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64] + [p] * 13 + [i64, p, p, i32]
     lib.cgo_max_threads.restype = i32
     lib.cgo_max_threads.argtypes = []
     _lib = lib
@@ -148,29 +147,42 @@ def real_sh(lmax: int, unit) -> np.ndarray:
     return out.reshape(tuple(np.shape(unit)[:-1]) + ((lmax + 1) ** 2,))
 
 
-def onsite(lmax, A, B, U_A, U_B, U_out_even, U_out_odd, nthreads: int = 0):
+def onsite(lmax, A, B, U_A, U_B, U_out_even, U_out_odd, nthreads: int = 0, A_flip=None,
+           B_flip=None, U_A_curl=None, U_B_curl=None):
     """On-site contracted product, fp64. A, B: [N, C, L^2]; U_*: [L, C, R].
 
+    A_flip, B_flip: parity-flipped slots of the two operands (None: absent). Slot pairs of
+    equal relative parity send their Gaunt coupling to out_even (natural parity) and their
+    curl coupling to out_odd; mixed pairs the other way round (p = p1 p2).
+    U_A, U_B factor the Gaunt couplings; U_A_curl, U_B_curl (None: the same) the curl ones.
     Returns (out_even, out_odd), each [N, C, L^2] float64."""
     lib = _load()
     A, B = _f64(A), _f64(B)
+    Af = None if A_flip is None else _f64(A_flip)
+    Bf = None if B_flip is None else _f64(B_flip)
     U_A, U_B, U_oe, U_oo = _f64(U_A), _f64(U_B), _f64(U_out_even), _f64(U_out_odd)
+    UAc = None if U_A_curl is None else _f64(U_A_curl)
+    UBc = None if U_B_curl is None else _f64(U_B_curl)
     N, C, L2 = A.shape
     R = U_A.shape[2]
     assert L2 == (lmax + 1) ** 2 and B.shape == A.shape
-    for U in (U_A, U_B, U_oe, U_oo):
-        assert U.shape == (lmax + 1, C, R)
+    for X in (Af, Bf):
+        assert X is None or X.shape == A.shape
+    for U in (U_A, U_B, U_oe, U_oo, UAc, UBc):
+        assert U is None or U.shape == (lmax + 1, C, R)
     oe = np.zeros((N, C, L2))
     oo = np.zeros((N, C, L2))
-    rc = lib.cgo_onsite(lmax, C, R, N, _ptr(A), _ptr(B), _ptr(U_A), _ptr(U_B), _ptr(U_oe),
-                        _ptr(U_oo), _ptr(oe), _ptr(oo), int(nthreads))
+    rc = lib.cgo_onsite(lmax, C, R, N, _ptr(A), _ptr(Af), _ptr(B), _ptr(Bf), _ptr(U_A),
+                        _ptr(U_B), _ptr(UAc), _ptr(UBc), _ptr(U_oe), _ptr(U_oo), _ptr(oe),
+                        _ptr(oo), int(nthreads))
     if rc != 0:
         raise RuntimeError(f"cgo_onsite failed ({rc})")
     return oe, oo
 
 
 def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
-                 U_out_even, U_out_odd, receivers=None, nthreads: int = 0, node_flip=None):
+                 U_out_even, U_out_odd, receivers=None, nthreads: int = 0, node_flip=None,
+                 U_E_curl=None, U_I_curl=None):
     """Message-passing contracted product, fp64, for a receiver subset.
 
     row_ptr [N+1], col [E] (int32 CSR by receiver), edge_unit [E,3],
@@ -178,12 +190,13 @@ def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I
     node_flip: None, or the parity-flipped node slot [N,C,L^2] (Table 1, Cases C and D:
     out_even, the natural-parity output, gains the curl coupling with it and out_odd, the
     opposite-parity output, its Gaunt coupling).
+    U_E, U_I factor the Gaunt couplings; U_E_curl, U_I_curl (None: the same) the curl ones.
     Returns (out_even, out_odd), each [len(receivers), C, L^2] (all receivers
     when receivers is None)."""
     if receivers is None:
         n = np.asarray(node_feat).shape[0]
         return _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U_E,
-                        U_I, U_out_even, U_out_odd, np.arange(n), nthreads)
+                        U_I, U_E_curl, U_I_curl, U_out_even, U_out_odd, np.arange(n), nthreads)
     # Marshalling only: cut out the rows of the requested receivers and the
     # features of their senders, so large inputs are not converted to fp64 whole.
     row_ptr = np.asarray(row_ptr)
@@ -206,12 +219,12 @@ def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I
     rp[1:len(rec) + 1] = np.cumsum(ends - starts)
     rp[len(rec) + 1:] = rp[len(rec)]
     return _mp_rows(lmax, rp, local_col.astype(np.int32), np.asarray(edge_unit)[eidx],
-                    np.asarray(edge_radial)[eidx], nf, nfl, U_E, U_I, U_out_even, U_out_odd,
-                    np.arange(len(rec)), nthreads)
+                    np.asarray(edge_radial)[eidx], nf, nfl, U_E, U_I, U_E_curl, U_I_curl,
+                    U_out_even, U_out_odd, np.arange(len(rec)), nthreads)
 
 
 def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U_E, U_I,
-             U_out_even, U_out_odd, receivers, nthreads):
+             U_E_curl, U_I_curl, U_out_even, U_out_odd, receivers, nthreads):
     lib = _load()
     row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
     col = np.ascontiguousarray(col, dtype=np.int32)
@@ -220,6 +233,8 @@ def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U
     if nfl is not None:
         assert nfl.shape == nf.shape
     U_E, U_I, U_oe, U_oo = _f64(U_E), _f64(U_I), _f64(U_out_even), _f64(U_out_odd)
+    UEc = None if U_E_curl is None else _f64(U_E_curl)
+    UIc = None if U_I_curl is None else _f64(U_I_curl)
     N, C, L2 = nf.shape
     E = col.shape[0]
     R = U_E.shape[2]
@@ -229,7 +244,7 @@ def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U
     oe = np.zeros((rec.shape[0], C, L2))
     oo = np.zeros((rec.shape[0], C, L2))
     rc = lib.cgo_message_pass(lmax, C, R, N, E, _ptr(row_ptr), _ptr(col), _ptr(eu), _ptr(er),
-                              _ptr(nf), _ptr(nfl), _ptr(U_E), _ptr(U_I),
+                              _ptr(nf), _ptr(nfl), _ptr(U_E), _ptr(U_I), _ptr(UEc), _ptr(UIc),
                               _ptr(U_oe), _ptr(U_oo), _ptr(rec), rec.shape[0], _ptr(oe), _ptr(oo),
                               int(nthreads))
     if rc != 0:

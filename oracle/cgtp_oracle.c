@@ -17,10 +17,18 @@
  *     out_even[n][k] = sum_r U_oe[l][n][r] Ta[r][k],  out_odd likewise with Tb
  *
  *   message passing (Eq. msgpass-parity-start; edge factor R*Y as in
- *   Eq. msgpass-tildeR), single natural-parity node slot:
+ *   Eq. msgpass-tildeR), natural-parity node slot:
  *     E_e[r][k1] = (sum_n U_E[l1][n][r] Rad_e[n][l1]) * Y_k1(rhat_e)
  *     H_j[r][k2] = sum_n U_I[l2][n][r] I_j[n][k2]
  *     Ta_i[r][k] = sum_{e=(j->i)} sum GR E_e H_j,  Tb_i likewise with QR
+ *
+ *   General parity (Eqs. msgpass-cp-alpha / msgpass-cp-beta, Table 1, Cases A-D):
+ *   the Gaunt and curl couplings may carry their own input factors (U_*_curl
+ *   for the curl one; NULL means the Gaunt factor), and an operand may carry a
+ *   parity-flipped slot (parity -(-1)^l) beside its natural one. Parity is
+ *   multiplicative: a pair of slots of equal relative parity sends its Gaunt
+ *   coupling to out_even (parity (-1)^l) and its curl coupling to out_odd, a
+ *   mixed pair the other way round. The edge factor has natural parity.
  *
  * GR and QR are the real-basis triple integrals
  *     GR[k1][k2][k] = int Y_k1 Y_k2 Y_k dOmega                 (Eq. gaunt)
@@ -422,27 +430,38 @@ static void project_all(int lmax, int C, int R, long n, const double *U_oe, cons
 }
 
 /* On-site contraction for nodes [0, n_nodes). Arrays (fp64, row-major):
- *   A, B: [N][C][L^2]; U_A, U_B, U_oe, U_oo: [L][C][R];
- *   out_even, out_odd: [N][C][L^2] (either may be NULL to skip that slot).
+ *   A, B: [N][C][L^2] natural-parity slots of the two operands;
+ *   A_flip, B_flip: NULL, or the parity-flipped slots [N][C][L^2];
+ *   U_A, U_B: [L][C][R] factors of the Gaunt couplings;
+ *   U_A_curl, U_B_curl: NULL (then U_A, U_B), or the factors of the curl couplings;
+ *   U_oe, U_oo: [L][C][R]; out_even, out_odd: [N][C][L^2] (either may be NULL).
+ * By the parity rule p = p1 p2 (Table 1 and the two-parity-bearing-factor cases): slot
+ * pairs of equal relative parity (natural x natural, flipped x flipped) send their Gaunt
+ * coupling to the natural-parity output out_even and their curl coupling to out_odd;
+ * mixed pairs the other way round.
  * Every (node, rank) pair is independent; they are spread over the threads. */
-int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const double *B,
-               const double *U_A, const double *U_B, const double *U_oe, const double *U_oo,
-               double *out_even, double *out_odd, int nthreads)
+int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const double *A_flip,
+               const double *B, const double *B_flip, const double *U_A, const double *U_B,
+               const double *U_A_curl, const double *U_B_curl, const double *U_oe,
+               const double *U_oo, double *out_even, double *out_odd, int nthreads)
 {
     if (lmax < 0 || C < 1 || R < 1 || n_nodes < 0) return -1;
     set_threads(nthreads);
     int L2 = (lmax + 1) * (lmax + 1);
+    if (!U_A_curl) U_A_curl = U_A;
+    if (!U_B_curl) U_B_curl = U_B;
     sparse_tab G, Q;
     if (build_tab(0, lmax, &G) || build_tab(1, lmax, &Q)) return -2;
     double *Ta = (double *)calloc((size_t)n_nodes * R * L2 + 1, sizeof(double));
     double *Tb = (double *)calloc((size_t)n_nodes * R * L2 + 1, sizeof(double));
     if (!Ta || !Tb) return -2;
+    const double *X1[2] = {A, A_flip}, *X2[2] = {B, B_flip};
     int err = 0;
 #pragma omp parallel
     {
-        double *H1 = (double *)malloc(sizeof(double) * L2);
-        double *H2 = (double *)malloc(sizeof(double) * L2);
-        if (!H1 || !H2) {
+        /* H[slot][g/c]: the slot's coefficients contracted with the Gaunt / curl factors */
+        double *H = (double *)malloc(sizeof(double) * 8 * L2);
+        if (!H) {
 #pragma omp atomic write
             err = -2;
         } else {
@@ -450,13 +469,31 @@ int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const doub
             for (long ir = 0; ir < n_nodes * R; ++ir) {
                 long i = ir / R;
                 int r = (int)(ir % R);
-                channel_contract_r(lmax, C, R, r, U_A, A + (size_t)i * C * L2, H1);
-                channel_contract_r(lmax, C, R, r, U_B, B + (size_t)i * C * L2, H2);
-                if (out_even) sparse_couple(&G, H1, H2, Ta + (size_t)ir * L2);
-                if (out_odd) sparse_couple(&Q, H1, H2, Tb + (size_t)ir * L2);
+                for (int s = 0; s < 2; ++s) {
+                    if (X1[s]) {
+                        channel_contract_r(lmax, C, R, r, U_A, X1[s] + (size_t)i * C * L2, H + (0 + 2 * s) * L2);
+                        channel_contract_r(lmax, C, R, r, U_A_curl, X1[s] + (size_t)i * C * L2, H + (1 + 2 * s) * L2);
+                    }
+                    if (X2[s]) {
+                        channel_contract_r(lmax, C, R, r, U_B, X2[s] + (size_t)i * C * L2, H + (4 + 2 * s) * L2);
+                        channel_contract_r(lmax, C, R, r, U_B_curl, X2[s] + (size_t)i * C * L2, H + (5 + 2 * s) * L2);
+                    }
+                }
+                for (int s1 = 0; s1 < 2; ++s1)
+                    for (int s2 = 0; s2 < 2; ++s2) {
+                        if (!X1[s1] || !X2[s2]) continue;
+                        const double *h1g = H + (0 + 2 * s1) * L2, *h1c = H + (1 + 2 * s1) * L2;
+                        const double *h2g = H + (4 + 2 * s2) * L2, *h2c = H + (5 + 2 * s2) * L2;
+                        double *to_g = (s1 == s2) ? Ta : Tb;  /* Gaunt: equal slots -> natural */
+                        double *to_c = (s1 == s2) ? Tb : Ta;
+                        const int want_g = (s1 == s2) ? (out_even != NULL) : (out_odd != NULL);
+                        const int want_c = (s1 == s2) ? (out_odd != NULL) : (out_even != NULL);
+                        if (want_g) sparse_couple(&G, h1g, h2g, to_g + (size_t)ir * L2);
+                        if (want_c) sparse_couple(&Q, h1c, h2c, to_c + (size_t)ir * L2);
+                    }
             }
         }
-        free(H1); free(H2);
+        free(H);
     }
     if (!err) project_all(lmax, C, R, n_nodes, U_oe, U_oo, Ta, Tb, out_even, out_odd);
     free(Ta); free(Tb);
@@ -468,7 +505,9 @@ int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const doub
  *   row_ptr: [N+1], col: [E] (sender of edge e), edge_unit: [E][3],
  *   edge_radial: [E][C][L] (R_{n l1}(r_ji)), node_feat: [N][C][L^2],
  *   node_flip: NULL, or the parity-flipped node slot [N][C][L^2],
- *   U_E, U_I, U_oe, U_oo: [L][C][R];
+ *   U_E, U_I: [L][C][R] factors of the Gaunt couplings;
+ *   U_E_curl, U_I_curl: NULL (then U_E, U_I), or the factors of the curl couplings;
+ *   U_oe, U_oo: [L][C][R];
  *   out_even, out_odd: [n_recv][C][L^2] (row q is receiver recv[q]).
  * The edge feature R Y has natural parity, so by Table 1 (Cases A-D) the natural-parity
  * output of degree l collects the Gaunt coupling with the natural node slot and the
@@ -479,10 +518,12 @@ int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const doub
 int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const int32_t *row_ptr,
                      const int32_t *col, const double *edge_unit, const double *edge_radial,
                      const double *node_feat, const double *node_flip, const double *U_E,
-                     const double *U_I, const double *U_oe, const double *U_oo,
-                     const int64_t *recv, long n_recv, double *out_even, double *out_odd,
-                     int nthreads)
+                     const double *U_I, const double *U_E_curl, const double *U_I_curl,
+                     const double *U_oe, const double *U_oo, const int64_t *recv, long n_recv,
+                     double *out_even, double *out_odd, int nthreads)
 {
+    if (!U_E_curl) U_E_curl = U_E;
+    if (!U_I_curl) U_I_curl = U_I;
     if (lmax < 0 || C < 1 || R < 1 || n_nodes < 0 || n_edges < 0 || n_recv < 0) return -1;
     for (long q = 0; q < n_recv; ++q)
         if (recv[q] < 0 || recv[q] >= n_nodes) return -1;
@@ -496,11 +537,10 @@ int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const i
     int err = 0;
 #pragma omp parallel
     {
-        double *E = (double *)malloc(sizeof(double) * L2);
-        double *H = (double *)malloc(sizeof(double) * L2);
-        double *Hf = (double *)malloc(sizeof(double) * L2);
+        double *E = (double *)malloc(sizeof(double) * 2 * L2);   /* Gaunt, curl factors */
+        double *H = (double *)malloc(sizeof(double) * 4 * L2);   /* [slot][Gaunt/curl] */
         double *Y = (double *)malloc(sizeof(double) * L2);
-        if (!E || !H || !Hf || !Y) {
+        if (!E || !H || !Y) {
 #pragma omp atomic write
             err = -2;
         } else {
@@ -514,26 +554,32 @@ int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const i
                     cgo_real_sh(lmax, u[0], u[1], u[2], Y);
                     const double *rad = edge_radial + (size_t)e * C * L;
                     /* Eq. msgpass-tildeR, then multiply by Y_{l1 m1}(rhat) */
-                    for (int l1 = 0; l1 < L; ++l1) {
-                        double s = 0.0;
-                        for (int n = 0; n < C; ++n)
-                            s += U_E[((size_t)l1 * C + n) * R + r] * rad[(size_t)n * L + l1];
-                        for (int m1 = -l1; m1 <= l1; ++m1)
-                            E[l1 * l1 + l1 + m1] = s * Y[l1 * l1 + l1 + m1];
+                    for (int f = 0; f < 2; ++f) {
+                        const double *UE = f ? U_E_curl : U_E;
+                        for (int l1 = 0; l1 < L; ++l1) {
+                            double s = 0.0;
+                            for (int n = 0; n < C; ++n)
+                                s += UE[((size_t)l1 * C + n) * R + r] * rad[(size_t)n * L + l1];
+                            for (int m1 = -l1; m1 <= l1; ++m1)
+                                E[f * L2 + l1 * l1 + l1 + m1] = s * Y[l1 * l1 + l1 + m1];
+                        }
                     }
-                    /* Eq. msgpass-HI */
+                    /* Eq. msgpass-HI, natural slot */
                     channel_contract_r(lmax, C, R, r, U_I, node_feat + (size_t)j * C * L2, H);
+                    channel_contract_r(lmax, C, R, r, U_I_curl, node_feat + (size_t)j * C * L2, H + L2);
                     if (out_even) sparse_couple(&G, E, H, Ta + (size_t)qr * L2);
-                    if (out_odd) sparse_couple(&Q, E, H, Tb + (size_t)qr * L2);
+                    if (out_odd) sparse_couple(&Q, E + L2, H + L2, Tb + (size_t)qr * L2);
                     if (node_flip) { /* Cases C and D: the parity-flipped slot */
-                        channel_contract_r(lmax, C, R, r, U_I, node_flip + (size_t)j * C * L2, Hf);
-                        if (out_even) sparse_couple(&Q, E, Hf, Ta + (size_t)qr * L2);
-                        if (out_odd) sparse_couple(&G, E, Hf, Tb + (size_t)qr * L2);
+                        const double *xf = node_flip + (size_t)j * C * L2;
+                        channel_contract_r(lmax, C, R, r, U_I, xf, H + 2 * L2);
+                        channel_contract_r(lmax, C, R, r, U_I_curl, xf, H + 3 * L2);
+                        if (out_even) sparse_couple(&Q, E + L2, H + 3 * L2, Ta + (size_t)qr * L2);
+                        if (out_odd) sparse_couple(&G, E, H + 2 * L2, Tb + (size_t)qr * L2);
                     }
                 }
             }
         }
-        free(E); free(H); free(Hf); free(Y);
+        free(E); free(H); free(Y);
     }
     if (!err) project_all(lmax, C, R, n_recv, U_oe, U_oo, Ta, Tb, out_even, out_odd);
     free(Ta); free(Tb);
