@@ -56,9 +56,9 @@ def _load():
     lib.cgo_real_sh.restype = None
     lib.cgo_real_sh.argtypes = [i32, dbl, dbl, dbl, p]
     lib.cgo_onsite.restype = i32
-    lib.cgo_onsite.argtypes = [i32, i32, i32, i64] + [p] * 12 + [i32]
+    lib.cgo_onsite.argtypes = [i32, i32, i32, i64] + [p] * 9 + [i32]
     lib.cgo_message_pass.restype = i32
-    lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64] + [p] * 13 + [i64, p, p, i32]
+    lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64] + [p] * 9 + [p, i64, p, p, i32]
     lib.cgo_max_threads.restype = i32
     lib.cgo_max_threads.argtypes = []
     _lib = lib
@@ -147,42 +147,78 @@ def real_sh(lmax: int, unit) -> np.ndarray:
     return out.reshape(tuple(np.shape(unit)[:-1]) + ((lmax + 1) ** 2,))
 
 
+def _in_blocks(U, lmax, C):
+    """Input factors of the four blocks b = 2 * category + sector (category 0: Gaunt,
+    1: curl; sector 0: out_even, 1: out_odd). U: [L, C, R] (all blocks share it),
+    [2, L, C, R] (per category) or [4, L, C, R] (per block)."""
+    U = _f64(U)
+    if U.ndim == 3:
+        blocks = [U] * 4
+    elif U.shape[0] == 2:
+        blocks = [U[0], U[0], U[1], U[1]]
+    else:
+        assert U.shape[0] == 4, "factor blocks: [L,C,R], [2,L,C,R] or [4,L,C,R]"
+        blocks = [U[b] for b in range(4)]
+    blocks = [np.ascontiguousarray(x) for x in blocks]
+    for x in blocks:
+        assert x.shape[:2] == (lmax + 1, C)
+    return blocks
+
+
+def _out_blocks(U_out_even, U_out_odd, lmax, C):
+    """Output weights per block from the per-sector arrays: [L, C, R] (both categories share
+    it) or [2, L, C, R] (Gaunt, curl)."""
+    per = []
+    for U in (U_out_even, U_out_odd):
+        U = _f64(U)
+        per.append([U, U] if U.ndim == 3 else [U[0], U[1]])
+    blocks = [np.ascontiguousarray(per[b & 1][b >> 1]) for b in range(4)]
+    for x in blocks:
+        assert x.shape[:2] == (lmax + 1, C)
+    return blocks
+
+
+def _ptr_array(arrays):
+    arr = (ctypes.c_void_p * len(arrays))(*[a.ctypes.data for a in arrays])
+    return arr, ctypes.cast(arr, ctypes.c_void_p)
+
+
 def onsite(lmax, A, B, U_A, U_B, U_out_even, U_out_odd, nthreads: int = 0, A_flip=None,
-           B_flip=None, U_A_curl=None, U_B_curl=None):
-    """On-site contracted product, fp64. A, B: [N, C, L^2]; U_*: [L, C, R].
+           B_flip=None):
+    """On-site contracted product, fp64. A, B: [N, C, L^2].
 
     A_flip, B_flip: parity-flipped slots of the two operands (None: absent). Slot pairs of
     equal relative parity send their Gaunt coupling to out_even (natural parity) and their
     curl coupling to out_odd; mixed pairs the other way round (p = p1 p2).
-    U_A, U_B factor the Gaunt couplings; U_A_curl, U_B_curl (None: the same) the curl ones.
+    U_A, U_B: input factors, [L, C, R] shared by all couplings, [2, L, C, R] per category
+    (Gaunt, curl) or [4, L, C, R] per block 2 * category + sector (Eqs. msgpass-cp-alpha,
+    msgpass-cp-beta). U_out_even, U_out_odd: [L, C, R], or [2, L, C, R] per category.
     Returns (out_even, out_odd), each [N, C, L^2] float64."""
     lib = _load()
     A, B = _f64(A), _f64(B)
     Af = None if A_flip is None else _f64(A_flip)
     Bf = None if B_flip is None else _f64(B_flip)
-    U_A, U_B, U_oe, U_oo = _f64(U_A), _f64(U_B), _f64(U_out_even), _f64(U_out_odd)
-    UAc = None if U_A_curl is None else _f64(U_A_curl)
-    UBc = None if U_B_curl is None else _f64(U_B_curl)
     N, C, L2 = A.shape
-    R = U_A.shape[2]
     assert L2 == (lmax + 1) ** 2 and B.shape == A.shape
     for X in (Af, Bf):
         assert X is None or X.shape == A.shape
-    for U in (U_A, U_B, U_oe, U_oo, UAc, UBc):
-        assert U is None or U.shape == (lmax + 1, C, R)
+    UA, UB = _in_blocks(U_A, lmax, C), _in_blocks(U_B, lmax, C)
+    Uo = _out_blocks(U_out_even, U_out_odd, lmax, C)
+    R = UA[0].shape[2]
+    for x in UA + UB + Uo:
+        assert x.shape == (lmax + 1, C, R)
+    keep = [_ptr_array(x) for x in (UA, UB, Uo)]
     oe = np.zeros((N, C, L2))
     oo = np.zeros((N, C, L2))
-    rc = lib.cgo_onsite(lmax, C, R, N, _ptr(A), _ptr(Af), _ptr(B), _ptr(Bf), _ptr(U_A),
-                        _ptr(U_B), _ptr(UAc), _ptr(UBc), _ptr(U_oe), _ptr(U_oo), _ptr(oe),
-                        _ptr(oo), int(nthreads))
+    rc = lib.cgo_onsite(lmax, C, R, N, _ptr(A), _ptr(Af), _ptr(B), _ptr(Bf), keep[0][1],
+                        keep[1][1], keep[2][1], _ptr(oe), _ptr(oo), int(nthreads))
     if rc != 0:
         raise RuntimeError(f"cgo_onsite failed ({rc})")
     return oe, oo
 
 
 def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
-                 U_out_even, U_out_odd, receivers=None, nthreads: int = 0, node_flip=None,
-                 U_E_curl=None, U_I_curl=None):
+                 U_out_even, U_out_odd, receivers=None, nthreads: int = 0, node_flip=None):
     """Message-passing contracted product, fp64, for a receiver subset.
 
     row_ptr [N+1], col [E] (int32 CSR by receiver), edge_unit [E,3],
@@ -190,13 +226,15 @@ def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I
     node_flip: None, or the parity-flipped node slot [N,C,L^2] (Table 1, Cases C and D:
     out_even, the natural-parity output, gains the curl coupling with it and out_odd, the
     opposite-parity output, its Gaunt coupling).
-    U_E, U_I factor the Gaunt couplings; U_E_curl, U_I_curl (None: the same) the curl ones.
+    U_E, U_I: edge / node input factors, [L, C, R] shared by all couplings, [2, L, C, R]
+    per category (Gaunt, curl) or [4, L, C, R] per block 2 * category + sector.
+    U_out_even, U_out_odd: [L, C, R], or [2, L, C, R] per category.
     Returns (out_even, out_odd), each [len(receivers), C, L^2] (all receivers
     when receivers is None)."""
     if receivers is None:
         n = np.asarray(node_feat).shape[0]
         return _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U_E,
-                        U_I, U_E_curl, U_I_curl, U_out_even, U_out_odd, np.arange(n), nthreads)
+                        U_I, U_out_even, U_out_odd, np.arange(n), nthreads)
     # Marshalling only: cut out the rows of the requested receivers and the
     # features of their senders, so large inputs are not converted to fp64 whole.
     row_ptr = np.asarray(row_ptr)
@@ -219,12 +257,12 @@ def message_pass(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I
     rp[1:len(rec) + 1] = np.cumsum(ends - starts)
     rp[len(rec) + 1:] = rp[len(rec)]
     return _mp_rows(lmax, rp, local_col.astype(np.int32), np.asarray(edge_unit)[eidx],
-                    np.asarray(edge_radial)[eidx], nf, nfl, U_E, U_I, U_E_curl, U_I_curl,
+                    np.asarray(edge_radial)[eidx], nf, nfl, U_E, U_I,
                     U_out_even, U_out_odd, np.arange(len(rec)), nthreads)
 
 
 def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U_E, U_I,
-             U_E_curl, U_I_curl, U_out_even, U_out_odd, receivers, nthreads):
+             U_out_even, U_out_odd, receivers, nthreads):
     lib = _load()
     row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
     col = np.ascontiguousarray(col, dtype=np.int32)
@@ -232,21 +270,22 @@ def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U
     nfl = None if node_flip is None else _f64(node_flip)
     if nfl is not None:
         assert nfl.shape == nf.shape
-    U_E, U_I, U_oe, U_oo = _f64(U_E), _f64(U_I), _f64(U_out_even), _f64(U_out_odd)
-    UEc = None if U_E_curl is None else _f64(U_E_curl)
-    UIc = None if U_I_curl is None else _f64(U_I_curl)
     N, C, L2 = nf.shape
+    UE, UI = _in_blocks(U_E, lmax, C), _in_blocks(U_I, lmax, C)
+    Uo = _out_blocks(U_out_even, U_out_odd, lmax, C)
+    R = UE[0].shape[2]
+    for x in UE + UI + Uo:
+        assert x.shape == (lmax + 1, C, R)
     E = col.shape[0]
-    R = U_E.shape[2]
     assert L2 == (lmax + 1) ** 2 and row_ptr.shape[0] == N + 1
     assert er.shape == (E, C, lmax + 1) and eu.shape == (E, 3)
     rec = np.ascontiguousarray(receivers, dtype=np.int64)
+    keep = [_ptr_array(x) for x in (UE, UI, Uo)]
     oe = np.zeros((rec.shape[0], C, L2))
     oo = np.zeros((rec.shape[0], C, L2))
     rc = lib.cgo_message_pass(lmax, C, R, N, E, _ptr(row_ptr), _ptr(col), _ptr(eu), _ptr(er),
-                              _ptr(nf), _ptr(nfl), _ptr(U_E), _ptr(U_I), _ptr(UEc), _ptr(UIc),
-                              _ptr(U_oe), _ptr(U_oo), _ptr(rec), rec.shape[0], _ptr(oe), _ptr(oo),
-                              int(nthreads))
+                              _ptr(nf), _ptr(nfl), keep[0][1], keep[1][1], keep[2][1], _ptr(rec),
+                              rec.shape[0], _ptr(oe), _ptr(oo), int(nthreads))
     if rc != 0:
         raise RuntimeError(f"cgo_message_pass failed ({rc})")
     return oe, oo

@@ -416,87 +416,113 @@ static int set_threads(int nthreads)
 }
 
 /* Projection of Ta/Tb [n][R][L^2] to out_even/out_odd [n][C][L^2]. */
-static void project_all(int lmax, int C, int R, long n, const double *U_oe, const double *U_oo,
-                        const double *Ta, const double *Tb, double *out_even, double *out_odd)
+/* Factor blocks (Eqs. msgpass-cp-alpha and msgpass-cp-beta): the model parameterizes the
+ * couplings of each category (0: Gaunt, Category alpha; 1: surface curl, Category beta) and
+ * each output parity sector (0: out_even, parity (-1)^l; 1: out_odd, parity -(-1)^l) with
+ * their own input factors and output weights. Block b = 2 * category + sector. */
+#define CGO_NB 4
+
+/* out_s[n][k] = sum_{cat} sum_r Uo[2 cat + s][l(k)][n][r] T[2 cat + s][r][k]; a block with
+ * no coupling routed to it (live[b] == 0) holds zeros and is skipped. */
+static void project_blocks(int lmax, int C, int R, long n, const double *const *Uo,
+                           double *const *T, const int *live, double *out_even, double *out_odd)
 {
     int L2 = (lmax + 1) * (lmax + 1);
-#pragma omp parallel for schedule(static)
-    for (long i = 0; i < n; ++i) {
-        if (out_even)
-            project_out(lmax, C, R, U_oe, Ta + (size_t)i * R * L2, out_even + (size_t)i * C * L2);
-        if (out_odd)
-            project_out(lmax, C, R, U_oo, Tb + (size_t)i * R * L2, out_odd + (size_t)i * C * L2);
+    double *outs[2] = {out_even, out_odd};
+#pragma omp parallel
+    {
+        double *tmp = (double *)malloc(sizeof(double) * (size_t)C * L2);
+#pragma omp for schedule(static)
+        for (long i = 0; i < n; ++i)
+            for (int sec = 0; sec < 2; ++sec) {
+                if (!outs[sec]) continue;
+                double *o = outs[sec] + (size_t)i * C * L2;
+                memset(o, 0, sizeof(double) * (size_t)C * L2);
+                for (int cat = 0; cat < 2; ++cat) {
+                    int b = 2 * cat + sec;
+                    if (!live[b] || !tmp) continue;
+                    project_out(lmax, C, R, Uo[b], T[b] + (size_t)i * R * L2, tmp);
+                    for (size_t q = 0; q < (size_t)C * L2; ++q) o[q] += tmp[q];
+                }
+            }
+        free(tmp);
     }
+}
+
+/* Block receiving the coupling of category cat for a slot pair of relative parity rel
+ * (0: equal slots, 1: mixed): by p = p1 p2 with the Gaunt coupling keeping the
+ * parity-of-degree rule and the curl coupling reversing it (Table 1), Gaunt sends equal
+ * pairs to the natural sector and mixed pairs to the opposite one; curl the other way. */
+static int block_of(int cat, int rel)
+{
+    int sec = cat ? !rel : rel;
+    return 2 * cat + sec;
 }
 
 /* On-site contraction for nodes [0, n_nodes). Arrays (fp64, row-major):
  *   A, B: [N][C][L^2] natural-parity slots of the two operands;
  *   A_flip, B_flip: NULL, or the parity-flipped slots [N][C][L^2];
- *   U_A, U_B: [L][C][R] factors of the Gaunt couplings;
- *   U_A_curl, U_B_curl: NULL (then U_A, U_B), or the factors of the curl couplings;
- *   U_oe, U_oo: [L][C][R]; out_even, out_odd: [N][C][L^2] (either may be NULL).
- * By the parity rule p = p1 p2 (Table 1 and the two-parity-bearing-factor cases): slot
- * pairs of equal relative parity (natural x natural, flipped x flipped) send their Gaunt
- * coupling to the natural-parity output out_even and their curl coupling to out_odd;
- * mixed pairs the other way round.
+ *   U_A[b], U_B[b]: [L][C][R] input factors of block b (the four may alias);
+ *   U_out[b]: [L][C][R] output weights of block b;
+ *   out_even, out_odd: [N][C][L^2] (either may be NULL).
+ * Every slot pair (s1, s2) of the operands contributes its Gaunt and its curl coupling, each
+ * computed with the factors of the block it is routed to (block_of).
  * Every (node, rank) pair is independent; they are spread over the threads. */
 int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const double *A_flip,
-               const double *B, const double *B_flip, const double *U_A, const double *U_B,
-               const double *U_A_curl, const double *U_B_curl, const double *U_oe,
-               const double *U_oo, double *out_even, double *out_odd, int nthreads)
+               const double *B, const double *B_flip, const double *const *U_A,
+               const double *const *U_B, const double *const *U_out, double *out_even,
+               double *out_odd, int nthreads)
 {
     if (lmax < 0 || C < 1 || R < 1 || n_nodes < 0) return -1;
     set_threads(nthreads);
     int L2 = (lmax + 1) * (lmax + 1);
-    if (!U_A_curl) U_A_curl = U_A;
-    if (!U_B_curl) U_B_curl = U_B;
+    const double *X1[2] = {A, A_flip}, *X2[2] = {B, B_flip};
+    int live[CGO_NB] = {0, 0, 0, 0};
+    for (int s1 = 0; s1 < 2; ++s1)
+        for (int s2 = 0; s2 < 2; ++s2)
+            if (X1[s1] && X2[s2])
+                for (int cat = 0; cat < 2; ++cat) {
+                    int b = block_of(cat, s1 != s2);
+                    if ((b & 1) ? out_odd != NULL : out_even != NULL) live[b] = 1;
+                }
     sparse_tab G, Q;
     if (build_tab(0, lmax, &G) || build_tab(1, lmax, &Q)) return -2;
-    double *Ta = (double *)calloc((size_t)n_nodes * R * L2 + 1, sizeof(double));
-    double *Tb = (double *)calloc((size_t)n_nodes * R * L2 + 1, sizeof(double));
-    if (!Ta || !Tb) return -2;
-    const double *X1[2] = {A, A_flip}, *X2[2] = {B, B_flip};
+    double *T[CGO_NB];
     int err = 0;
-#pragma omp parallel
-    {
-        /* H[slot][g/c]: the slot's coefficients contracted with the Gaunt / curl factors */
-        double *H = (double *)malloc(sizeof(double) * 8 * L2);
-        if (!H) {
-#pragma omp atomic write
-            err = -2;
-        } else {
-#pragma omp for schedule(dynamic, 4)
-            for (long ir = 0; ir < n_nodes * R; ++ir) {
-                long i = ir / R;
-                int r = (int)(ir % R);
-                for (int s = 0; s < 2; ++s) {
-                    if (X1[s]) {
-                        channel_contract_r(lmax, C, R, r, U_A, X1[s] + (size_t)i * C * L2, H + (0 + 2 * s) * L2);
-                        channel_contract_r(lmax, C, R, r, U_A_curl, X1[s] + (size_t)i * C * L2, H + (1 + 2 * s) * L2);
-                    }
-                    if (X2[s]) {
-                        channel_contract_r(lmax, C, R, r, U_B, X2[s] + (size_t)i * C * L2, H + (4 + 2 * s) * L2);
-                        channel_contract_r(lmax, C, R, r, U_B_curl, X2[s] + (size_t)i * C * L2, H + (5 + 2 * s) * L2);
-                    }
-                }
-                for (int s1 = 0; s1 < 2; ++s1)
-                    for (int s2 = 0; s2 < 2; ++s2) {
-                        if (!X1[s1] || !X2[s2]) continue;
-                        const double *h1g = H + (0 + 2 * s1) * L2, *h1c = H + (1 + 2 * s1) * L2;
-                        const double *h2g = H + (4 + 2 * s2) * L2, *h2c = H + (5 + 2 * s2) * L2;
-                        double *to_g = (s1 == s2) ? Ta : Tb;  /* Gaunt: equal slots -> natural */
-                        double *to_c = (s1 == s2) ? Tb : Ta;
-                        const int want_g = (s1 == s2) ? (out_even != NULL) : (out_odd != NULL);
-                        const int want_c = (s1 == s2) ? (out_odd != NULL) : (out_even != NULL);
-                        if (want_g) sparse_couple(&G, h1g, h2g, to_g + (size_t)ir * L2);
-                        if (want_c) sparse_couple(&Q, h1c, h2c, to_c + (size_t)ir * L2);
-                    }
-            }
-        }
-        free(H);
+    for (int b = 0; b < CGO_NB; ++b) {
+        T[b] = (double *)calloc(live[b] ? (size_t)n_nodes * R * L2 + 1 : 1, sizeof(double));
+        if (!T[b]) err = -2;
     }
-    if (!err) project_all(lmax, C, R, n_nodes, U_oe, U_oo, Ta, Tb, out_even, out_odd);
-    free(Ta); free(Tb);
+    if (!err) {
+#pragma omp parallel
+        {
+            double *h1 = (double *)malloc(sizeof(double) * 2 * L2), *h2 = h1 ? h1 + L2 : NULL;
+            if (!h1) {
+#pragma omp atomic write
+                err = -2;
+            } else {
+#pragma omp for schedule(dynamic, 4)
+                for (long ir = 0; ir < n_nodes * R; ++ir) {
+                    long i = ir / R;
+                    int r = (int)(ir % R);
+                    for (int s1 = 0; s1 < 2; ++s1)
+                        for (int s2 = 0; s2 < 2; ++s2) {
+                            if (!X1[s1] || !X2[s2]) continue;
+                            for (int cat = 0; cat < 2; ++cat) {
+                                int b = block_of(cat, s1 != s2);
+                                if (!live[b]) continue;
+                                channel_contract_r(lmax, C, R, r, U_A[b], X1[s1] + (size_t)i * C * L2, h1);
+                                channel_contract_r(lmax, C, R, r, U_B[b], X2[s2] + (size_t)i * C * L2, h2);
+                                sparse_couple(cat ? &Q : &G, h1, h2, T[b] + (size_t)ir * L2);
+                            }
+                        }
+                }
+            }
+            free(h1);
+        }
+    }
+    if (!err) project_blocks(lmax, C, R, n_nodes, U_out, T, live, out_even, out_odd);
+    for (int b = 0; b < CGO_NB; ++b) free(T[b]);
     free_tab(&G); free_tab(&Q);
     return err;
 }
@@ -505,84 +531,86 @@ int cgo_onsite(int lmax, int C, int R, long n_nodes, const double *A, const doub
  *   row_ptr: [N+1], col: [E] (sender of edge e), edge_unit: [E][3],
  *   edge_radial: [E][C][L] (R_{n l1}(r_ji)), node_feat: [N][C][L^2],
  *   node_flip: NULL, or the parity-flipped node slot [N][C][L^2],
- *   U_E, U_I: [L][C][R] factors of the Gaunt couplings;
- *   U_E_curl, U_I_curl: NULL (then U_E, U_I), or the factors of the curl couplings;
- *   U_oe, U_oo: [L][C][R];
+ *   U_E[b], U_I[b]: [L][C][R] edge / node input factors of block b (the four may alias);
+ *   U_out[b]: [L][C][R] output weights of block b;
  *   out_even, out_odd: [n_recv][C][L^2] (row q is receiver recv[q]).
- * The edge feature R Y has natural parity, so by Table 1 (Cases A-D) the natural-parity
- * output of degree l collects the Gaunt coupling with the natural node slot and the
- * surface-curl coupling with the flipped slot; the opposite-parity output collects the
- * curl coupling with the natural slot and the Gaunt coupling with the flipped slot.
- * Both slots share the factors U_I.
+ * The edge feature R Y has natural parity, so the natural node slot pairs with it as an
+ * equal pair and the flipped slot as a mixed one: by Table 1 (Cases A-D) out_even collects
+ * the Gaunt coupling with the natural slot and the curl coupling with the flipped slot,
+ * out_odd the curl coupling with the natural slot and the Gaunt coupling with the flipped.
  * Every (receiver, rank) pair is independent; they are spread over the threads. */
 int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const int32_t *row_ptr,
                      const int32_t *col, const double *edge_unit, const double *edge_radial,
-                     const double *node_feat, const double *node_flip, const double *U_E,
-                     const double *U_I, const double *U_E_curl, const double *U_I_curl,
-                     const double *U_oe, const double *U_oo, const int64_t *recv, long n_recv,
+                     const double *node_feat, const double *node_flip,
+                     const double *const *U_E, const double *const *U_I,
+                     const double *const *U_out, const int64_t *recv, long n_recv,
                      double *out_even, double *out_odd, int nthreads)
 {
-    if (!U_E_curl) U_E_curl = U_E;
-    if (!U_I_curl) U_I_curl = U_I;
     if (lmax < 0 || C < 1 || R < 1 || n_nodes < 0 || n_edges < 0 || n_recv < 0) return -1;
     for (long q = 0; q < n_recv; ++q)
         if (recv[q] < 0 || recv[q] >= n_nodes) return -1;
     set_threads(nthreads);
     int L = lmax + 1, L2 = L * L;
+    const double *X2[2] = {node_feat, node_flip};
+    int live[CGO_NB] = {0, 0, 0, 0};
+    for (int s2 = 0; s2 < 2; ++s2)
+        if (X2[s2])
+            for (int cat = 0; cat < 2; ++cat) {
+                int b = block_of(cat, s2);
+                if ((b & 1) ? out_odd != NULL : out_even != NULL) live[b] = 1;
+            }
     sparse_tab G, Q;
     if (build_tab(0, lmax, &G) || build_tab(1, lmax, &Q)) return -2;
-    double *Ta = (double *)calloc((size_t)n_recv * R * L2 + 1, sizeof(double));
-    double *Tb = (double *)calloc((size_t)n_recv * R * L2 + 1, sizeof(double));
-    if (!Ta || !Tb) return -2;
+    double *T[CGO_NB];
     int err = 0;
+    for (int b = 0; b < CGO_NB; ++b) {
+        T[b] = (double *)calloc(live[b] ? (size_t)n_recv * R * L2 + 1 : 1, sizeof(double));
+        if (!T[b]) err = -2;
+    }
+    if (!err) {
 #pragma omp parallel
-    {
-        double *E = (double *)malloc(sizeof(double) * 2 * L2);   /* Gaunt, curl factors */
-        double *H = (double *)malloc(sizeof(double) * 4 * L2);   /* [slot][Gaunt/curl] */
-        double *Y = (double *)malloc(sizeof(double) * L2);
-        if (!E || !H || !Y) {
+        {
+            double *E = (double *)malloc(sizeof(double) * 3 * L2), *H = E ? E + L2 : NULL;
+            double *Y = H ? H + L2 : NULL;
+            if (!E) {
 #pragma omp atomic write
-            err = -2;
-        } else {
+                err = -2;
+            } else {
 #pragma omp for schedule(dynamic, 1)
-            for (long qr = 0; qr < n_recv * R; ++qr) {
-                long i = (long)recv[qr / R];
-                int r = (int)(qr % R);
-                for (long e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
-                    long j = col[e];
-                    const double *u = edge_unit + 3 * (size_t)e;
-                    cgo_real_sh(lmax, u[0], u[1], u[2], Y);
-                    const double *rad = edge_radial + (size_t)e * C * L;
-                    /* Eq. msgpass-tildeR, then multiply by Y_{l1 m1}(rhat) */
-                    for (int f = 0; f < 2; ++f) {
-                        const double *UE = f ? U_E_curl : U_E;
-                        for (int l1 = 0; l1 < L; ++l1) {
-                            double s = 0.0;
-                            for (int n = 0; n < C; ++n)
-                                s += UE[((size_t)l1 * C + n) * R + r] * rad[(size_t)n * L + l1];
-                            for (int m1 = -l1; m1 <= l1; ++m1)
-                                E[f * L2 + l1 * l1 + l1 + m1] = s * Y[l1 * l1 + l1 + m1];
+                for (long qr = 0; qr < n_recv * R; ++qr) {
+                    long i = (long)recv[qr / R];
+                    int r = (int)(qr % R);
+                    for (long e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+                        long j = col[e];
+                        const double *u = edge_unit + 3 * (size_t)e;
+                        cgo_real_sh(lmax, u[0], u[1], u[2], Y);
+                        const double *rad = edge_radial + (size_t)e * C * L;
+                        for (int s2 = 0; s2 < 2; ++s2) {
+                            if (!X2[s2]) continue;
+                            for (int cat = 0; cat < 2; ++cat) {
+                                int b = block_of(cat, s2);
+                                if (!live[b]) continue;
+                                /* Eq. msgpass-tildeR, then multiply by Y_{l1 m1}(rhat) */
+                                for (int l1 = 0; l1 < L; ++l1) {
+                                    double s = 0.0;
+                                    for (int n = 0; n < C; ++n)
+                                        s += U_E[b][((size_t)l1 * C + n) * R + r] * rad[(size_t)n * L + l1];
+                                    for (int m1 = -l1; m1 <= l1; ++m1)
+                                        E[l1 * l1 + l1 + m1] = s * Y[l1 * l1 + l1 + m1];
+                                }
+                                /* Eq. msgpass-HI */
+                                channel_contract_r(lmax, C, R, r, U_I[b], X2[s2] + (size_t)j * C * L2, H);
+                                sparse_couple(cat ? &Q : &G, E, H, T[b] + (size_t)qr * L2);
+                            }
                         }
-                    }
-                    /* Eq. msgpass-HI, natural slot */
-                    channel_contract_r(lmax, C, R, r, U_I, node_feat + (size_t)j * C * L2, H);
-                    channel_contract_r(lmax, C, R, r, U_I_curl, node_feat + (size_t)j * C * L2, H + L2);
-                    if (out_even) sparse_couple(&G, E, H, Ta + (size_t)qr * L2);
-                    if (out_odd) sparse_couple(&Q, E + L2, H + L2, Tb + (size_t)qr * L2);
-                    if (node_flip) { /* Cases C and D: the parity-flipped slot */
-                        const double *xf = node_flip + (size_t)j * C * L2;
-                        channel_contract_r(lmax, C, R, r, U_I, xf, H + 2 * L2);
-                        channel_contract_r(lmax, C, R, r, U_I_curl, xf, H + 3 * L2);
-                        if (out_even) sparse_couple(&Q, E + L2, H + 3 * L2, Ta + (size_t)qr * L2);
-                        if (out_odd) sparse_couple(&G, E, H + 2 * L2, Tb + (size_t)qr * L2);
                     }
                 }
             }
+            free(E);
         }
-        free(E); free(H); free(Y);
     }
-    if (!err) project_all(lmax, C, R, n_recv, U_oe, U_oo, Ta, Tb, out_even, out_odd);
-    free(Ta); free(Tb);
+    if (!err) project_blocks(lmax, C, R, n_recv, U_out, T, live, out_even, out_odd);
+    for (int b = 0; b < CGO_NB; ++b) free(T[b]);
     free_tab(&G); free_tab(&Q);
     return err;
 }

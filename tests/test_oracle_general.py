@@ -1,15 +1,18 @@
-"""Pins of the oracle's general parity parameterization: independent factors for the Gaunt
-(Category alpha) and curl (Category beta) couplings (Eqs. msgpass-cp-alpha, msgpass-cp-beta),
-and on-site operands that each carry a natural- and a parity-flipped slot (the two
-parity-bearing factors case, Eq. twoparity-phi with the on-site specialization).
+"""Pins of the oracle's general parameterization (Eqs. msgpass-cp-alpha, msgpass-cp-beta,
+Table 1, and the on-site contraction with parity-labelled inputs).
 
-* Without the optional inputs, and with the curl factors equal to the Gaunt ones, the
-  results are the single-slot shared-factor ones, exactly.
-* With one slot each, out_even does not depend on the curl factors and out_odd equals the
-  shared-factor result computed with the curl factors.
+Each coupling category (Gaunt, Category alpha; surface curl, Category beta) and each output
+parity sector (out_even, parity (-1)^l; out_odd, parity -(-1)^l) has its own input factors
+and output weights: four blocks b = 2 * category + sector. On-site operands may each carry
+a natural and a parity-flipped slot; the message-passing node feature too.
+
+* Stacked factor forms reduce to one another exactly: [L,C,R] is four equal blocks, the
+  per-category form [2,L,C,R] is blocks (g, g, c, c), per-sector output weights are equal
+  Gaunt and curl weights.
+* Routing: with one slot per operand only blocks 0 (Gaunt -> out_even) and 3 (curl ->
+  out_odd) are read; the other two blocks may hold anything.
 * Dense-grid brute force (scipy harmonics, finite-difference surface gradients, numpy
-  quadrature) of the on-site sum over the four slot pairs and of message passing with
-  independent factors.
+  quadrature) of the four blocks with distinct factors, on-site and message passing.
 * Inversion with each slot multiplied by its own parity; rotation equivariance.
 * On-site dispatch check in the manner of App. B: operand 1 restricted to one degree l1 in
   its natural slot, operand 2 only in the slot of absolute parity +1: only output sectors of
@@ -26,72 +29,108 @@ from tests import bruteforce as bf
 from tests.test_oracle_contractions import _grid_fields, _parity_diag, _per_k, _rel
 
 
+def _factors(rng, nb, lmax, C, R):
+    return (rng.standard_normal((nb, lmax + 1, C, R)) / np.sqrt(C)).astype(np.float32)
+
+
 def _onsite_d(lmax, n=3, C=3, R=4, seed=11):
     d = inputs.onsite_inputs(n, lmax, C, R, seed=seed, distinct_out=True)
     rng = np.random.default_rng(seed + 1000)
     K = (lmax + 1) ** 2
     d["A_flip"] = rng.standard_normal((n, C, K)).astype(np.float32)
     d["B_flip"] = rng.standard_normal((n, C, K)).astype(np.float32)
-    d["U_A_curl"] = (rng.standard_normal((lmax + 1, C, R)) / np.sqrt(C)).astype(np.float32)
-    d["U_B_curl"] = (rng.standard_normal((lmax + 1, C, R)) / np.sqrt(C)).astype(np.float32)
+    d["UA4"] = _factors(rng, 4, lmax, C, R)
+    d["UB4"] = _factors(rng, 4, lmax, C, R)
+    d["Uoe2"] = _factors(rng, 2, lmax, C, R)
+    d["Uoo2"] = _factors(rng, 2, lmax, C, R)
     return d
 
 
 def _on(lmax, d, **over):
-    a = dict(A=d["A"], B=d["B"], U_A=d["U_A"], U_B=d["U_B"], U_out_even=d["U_out_even"],
-             U_out_odd=d["U_out_odd"], A_flip=d["A_flip"], B_flip=d["B_flip"],
-             U_A_curl=d["U_A_curl"], U_B_curl=d["U_B_curl"])
+    a = dict(A=d["A"], B=d["B"], U_A=d["UA4"], U_B=d["UB4"], U_out_even=d["Uoe2"],
+             U_out_odd=d["Uoo2"], A_flip=d["A_flip"], B_flip=d["B_flip"])
     a.update(over)
     return oracle.onsite(lmax, **a)
 
 
+def _block(cat, rel):
+    """Block of the coupling of category cat (0 Gaunt, 1 curl) for a slot pair of relative
+    parity rel (0 equal, 1 mixed), by p = p1 p2 (Table 1)."""
+    return 2 * cat + (rel if cat == 0 else 1 - rel)
+
+
+def _sum_blocks(lmax, S, Uo, W, Y):
+    """out_sec = sum over categories of the projection of the analysed block field."""
+    outs = []
+    for sec in range(2):
+        o = 0.0
+        for cat in range(2):
+            b = 2 * cat + sec
+            if S[b] is None:
+                continue
+            T = np.einsum("p,...rp,pk->...rk", W, S[b], Y)
+            o = o + np.einsum("knr,...rk->...nk", Uo[b], T)
+        outs.append(o)
+    return outs
+
+
 def _brute_onsite_general(lmax, d):
     Y, Dt, Dp, W = bf.sh_and_derivs(lmax)
-    f64 = lambda k: d[k].astype(np.float64)
-    U = {k: _per_k(f64(k), lmax) for k in ("U_A", "U_B", "U_A_curl", "U_B_curl",
-                                           "U_out_even", "U_out_odd")}
-    H = lambda Uk, X: np.einsum("knr,ink->irk", U[Uk], f64(X))
-    slots1 = {"n": "A", "f": "A_flip"}
-    slots2 = {"n": "B", "f": "B_flip"}
-    Sn = So = 0.0
-    for s1, x1 in slots1.items():
-        for s2, x2 in slots2.items():
-            a1 = _grid_fields(H("U_A", x1), Y, Dt, Dp)[0]
-            a2 = _grid_fields(H("U_B", x2), Y, Dt, Dp)[0]
-            _, t1, p1 = _grid_fields(H("U_A_curl", x1), Y, Dt, Dp)
-            _, t2, p2 = _grid_fields(H("U_B_curl", x2), Y, Dt, Dp)
-            g, c = a1 * a2, bf.bracket(t1, p1, t2, p2)
-            if s1 == s2:
-                Sn, So = Sn + g, So + c
-            else:
-                Sn, So = Sn + c, So + g
-    Tn = np.einsum("p,irp,pk->irk", W, Sn, Y)
-    To = np.einsum("p,irp,pk->irk", W, So, Y)
-    return (np.einsum("knr,irk->ink", U["U_out_even"], Tn),
-            np.einsum("knr,irk->ink", U["U_out_odd"], To))
+    UA = [_per_k(d["UA4"][b].astype(np.float64), lmax) for b in range(4)]
+    UB = [_per_k(d["UB4"][b].astype(np.float64), lmax) for b in range(4)]
+    Uo = [_per_k(d["Uoe2" if b % 2 == 0 else "Uoo2"][b // 2].astype(np.float64), lmax)
+          for b in range(4)]
+    X1 = [d["A"].astype(np.float64), d["A_flip"].astype(np.float64)]
+    X2 = [d["B"].astype(np.float64), d["B_flip"].astype(np.float64)]
+    S = [None] * 4
+    for s1 in range(2):
+        for s2 in range(2):
+            for cat in range(2):
+                b = _block(cat, s1 != s2)
+                h1 = np.einsum("knr,ink->irk", UA[b], X1[s1])
+                h2 = np.einsum("knr,ink->irk", UB[b], X2[s2])
+                a1, t1, p1 = _grid_fields(h1, Y, Dt, Dp)
+                a2, t2, p2 = _grid_fields(h2, Y, Dt, Dp)
+                v = a1 * a2 if cat == 0 else bf.bracket(t1, p1, t2, p2)
+                S[b] = v if S[b] is None else S[b] + v
+    return _sum_blocks(lmax, S, Uo, W, Y)
 
 
-def test_onsite_optional_inputs_reduce_to_base():
+def test_onsite_factor_forms_reduce_exactly():
     lmax = 3
     d = _onsite_d(lmax)
-    base = oracle.onsite(lmax, d["A"], d["B"], d["U_A"], d["U_B"], d["U_out_even"],
-                         d["U_out_odd"])
-    none = _on(lmax, d, A_flip=None, B_flip=None, U_A_curl=None, U_B_curl=None)
-    same = _on(lmax, d, A_flip=None, B_flip=None, U_A_curl=d["U_A"], U_B_curl=d["U_B"])
-    for o in (none, same):
-        assert np.array_equal(o[0], base[0]) and np.array_equal(o[1], base[1])
+    U, V = d["U_A"], d["U_B"]
+    shared = _on(lmax, d, U_A=U, U_B=V, U_out_even=d["U_out_even"], U_out_odd=d["U_out_odd"])
+    four = _on(lmax, d, U_A=np.stack([U] * 4), U_B=np.stack([V] * 4),
+               U_out_even=np.stack([d["U_out_even"]] * 2), U_out_odd=np.stack([d["U_out_odd"]] * 2))
+    g, c = d["UA4"][0], d["UA4"][3]
+    two = _on(lmax, d, U_A=np.stack([g, c]))
+    twof = _on(lmax, d, U_A=np.stack([g, g, c, c]))
+    for x, y in ((shared, four), (two, twof)):
+        assert np.array_equal(x[0], y[0]) and np.array_equal(x[1], y[1])
+    base = oracle.onsite(lmax, d["A"], d["B"], U, V, d["U_out_even"], d["U_out_odd"])
+    one = _on(lmax, d, U_A=U, U_B=V, U_out_even=d["U_out_even"], U_out_odd=d["U_out_odd"],
+              A_flip=None, B_flip=None)
+    assert np.array_equal(base[0], one[0]) and np.array_equal(base[1], one[1])
 
 
-def test_onsite_independent_factors_route_by_category():
+def test_onsite_single_slot_reads_blocks_0_and_3_only():
     lmax = 4
     d = _onsite_d(lmax, seed=12)
-    ind = _on(lmax, d, A_flip=None, B_flip=None)
-    base_g = oracle.onsite(lmax, d["A"], d["B"], d["U_A"], d["U_B"], d["U_out_even"],
-                           d["U_out_odd"])
-    base_c = oracle.onsite(lmax, d["A"], d["B"], d["U_A_curl"], d["U_B_curl"],
-                           d["U_out_even"], d["U_out_odd"])
-    assert _rel(ind[0], base_g[0]) < 1e-14
-    assert _rel(ind[1], base_c[1]) < 1e-14
+    ref = _on(lmax, d, A_flip=None, B_flip=None)
+    junk = {k: d[k].copy() for k in ("UA4", "UB4")}
+    for k in junk:
+        junk[k][1:3] = 7.0
+    Uoe, Uoo = d["Uoe2"].copy(), d["Uoo2"].copy()
+    Uoe[1] = -3.0     # curl weights of out_even: no curl coupling reaches it
+    Uoo[0] = 5.0      # Gaunt weights of out_odd
+    got = _on(lmax, d, A_flip=None, B_flip=None, U_A=junk["UA4"], U_B=junk["UB4"],
+              U_out_even=Uoe, U_out_odd=Uoo)
+    assert np.array_equal(got[0], ref[0]) and np.array_equal(got[1], ref[1])
+    # block 0 alone is the shared-factor Gaunt output, block 3 the curl output
+    g = oracle.onsite(lmax, d["A"], d["B"], d["UA4"][0], d["UB4"][0], d["Uoe2"][0], d["Uoo2"][1])
+    c = oracle.onsite(lmax, d["A"], d["B"], d["UA4"][3], d["UB4"][3], d["Uoe2"][0], d["Uoo2"][1])
+    assert _rel(ref[0], g[0]) < 1e-14 and _rel(ref[1], c[1]) < 1e-14
 
 
 @pytest.mark.parametrize("lmax", [1, 2, 3])
@@ -142,37 +181,44 @@ def test_onsite_dispatch_rule_single_degree(l1):
 
 # ------------------------------------------------------------------ message passing ---
 
-def _mp_d(lmax, seed=5):
-    d = inputs.mp_inputs(14, lmax, 3, 2, seed, density=0.1, r_cut=2.5, distinct_out=True,
+def _mp_d(lmax, seed=5, C=3, R=2):
+    d = inputs.mp_inputs(14, lmax, C, R, seed, density=0.1, r_cut=2.5, distinct_out=True,
                          two_slot=True)
     rng = np.random.default_rng(seed + 2000)
-    d["U_E_curl"] = (rng.standard_normal((lmax + 1, 3, 2)) / np.sqrt(3)).astype(np.float32)
-    d["U_I_curl"] = (rng.standard_normal((lmax + 1, 3, 2)) / np.sqrt(3)).astype(np.float32)
+    d["UE4"] = _factors(rng, 4, lmax, C, R)
+    d["UI4"] = _factors(rng, 4, lmax, C, R)
+    d["Uoe2"] = _factors(rng, 2, lmax, C, R)
+    d["Uoo2"] = _factors(rng, 2, lmax, C, R)
     return d
 
 
 def _mp(lmax, d, rec, **over):
     a = dict(row_ptr=d["row_ptr"], col=d["col"], edge_unit=d["edge_unit"],
-             edge_radial=d["edge_radial"], node_feat=d["node_feat"], U_E=d["U_E"], U_I=d["U_I"],
-             U_out_even=d["U_out_even"], U_out_odd=d["U_out_odd"], receivers=rec,
-             node_flip=d["node_flip"], U_E_curl=d["U_E_curl"], U_I_curl=d["U_I_curl"])
+             edge_radial=d["edge_radial"], node_feat=d["node_feat"], U_E=d["UE4"], U_I=d["UI4"],
+             U_out_even=d["Uoe2"], U_out_odd=d["Uoo2"], receivers=rec, node_flip=d["node_flip"])
     a.update(over)
     return oracle.message_pass(lmax, **a)
 
 
-def test_mp_independent_factors_route_by_category():
+def test_mp_factor_forms_and_routing():
     lmax = 3
     d = _mp_d(lmax)
     rec = np.arange(d["row_ptr"].shape[0] - 1)
-    ind = _mp(lmax, d, rec, node_flip=None)
-    base_g = _mp(lmax, d, rec, node_flip=None, U_E_curl=None, U_I_curl=None)
-    base_c = _mp(lmax, d, rec, node_flip=None, U_E_curl=None, U_I_curl=None,
-                 U_E=d["U_E_curl"], U_I=d["U_I_curl"])
-    assert _rel(ind[0], base_g[0]) < 1e-14
-    assert _rel(ind[1], base_c[1]) < 1e-14
-    same = _mp(lmax, d, rec, U_E_curl=d["U_E"], U_I_curl=d["U_I"])
-    shared = _mp(lmax, d, rec, U_E_curl=None, U_I_curl=None)
-    assert np.array_equal(same[0], shared[0]) and np.array_equal(same[1], shared[1])
+    shared = _mp(lmax, d, rec, U_E=d["U_E"], U_I=d["U_I"], U_out_even=d["U_out_even"],
+                 U_out_odd=d["U_out_odd"])
+    four = _mp(lmax, d, rec, U_E=np.stack([d["U_E"]] * 4), U_I=np.stack([d["U_I"]] * 4),
+               U_out_even=np.stack([d["U_out_even"]] * 2),
+               U_out_odd=np.stack([d["U_out_odd"]] * 2))
+    assert np.array_equal(shared[0], four[0]) and np.array_equal(shared[1], four[1])
+    ref = _mp(lmax, d, rec, node_flip=None)
+    junk = {k: d[k].copy() for k in ("UE4", "UI4")}
+    for k in junk:
+        junk[k][1:3] = 7.0
+    Uoe, Uoo = d["Uoe2"].copy(), d["Uoo2"].copy()
+    Uoe[1], Uoo[0] = -3.0, 5.0
+    got = _mp(lmax, d, rec, node_flip=None, U_E=junk["UE4"], U_I=junk["UI4"], U_out_even=Uoe,
+              U_out_odd=Uoo)
+    assert np.array_equal(got[0], ref[0]) and np.array_equal(got[1], ref[1])
 
 
 @pytest.mark.parametrize("lmax", [1, 2, 3])
@@ -181,31 +227,40 @@ def test_mp_general_matches_dense_bruteforce(lmax):
     rec = np.arange(d["row_ptr"].shape[0] - 1)
     on, oo = _mp(lmax, d, rec)
     Y, Dt, Dp, W = bf.sh_and_derivs(lmax)
-    f64 = lambda k: d[k].astype(np.float64)
-    U = {k: _per_k(f64(k), lmax) for k in ("U_E", "U_I", "U_E_curl", "U_I_curl",
-                                           "U_out_even", "U_out_odd")}
-    Ye = bf.real_sh_xyz(lmax, f64("edge_unit"))
-    rad = f64("edge_radial")
+    UE = [_per_k(d["UE4"][b].astype(np.float64), lmax) for b in range(4)]
+    UI = [_per_k(d["UI4"][b].astype(np.float64), lmax) for b in range(4)]
+    Uo = [_per_k(d["Uoe2" if b % 2 == 0 else "Uoo2"][b // 2].astype(np.float64), lmax)
+          for b in range(4)]
+    Ye = bf.real_sh_xyz(lmax, d["edge_unit"].astype(np.float64))
+    rad = d["edge_radial"].astype(np.float64)
     lk = np.array([l for l in range(lmax + 1) for _ in range(2 * l + 1)])
-    HEg = np.einsum("knr,enk->erk", U["U_E"], rad[:, :, lk]) * Ye[:, None, :]
-    HEc = np.einsum("knr,enk->erk", U["U_E_curl"], rad[:, :, lk]) * Ye[:, None, :]
-    HI = {(s, c): np.einsum("knr,ink->irk", U[c], f64(s)) for s in ("node_feat", "node_flip")
-          for c in ("U_I", "U_I_curl")}
+    X2 = [d["node_feat"].astype(np.float64), d["node_flip"].astype(np.float64)]
     rp, col = d["row_ptr"], d["col"]
-    bn, bo = [], []
-    for i in rec:
-        Sn = So = 0.0
+    S = [np.zeros((len(rec), UE[0].shape[2], Y.shape[0])) for _ in range(4)]
+    for q, i in enumerate(rec):
         for e in range(rp[i], rp[i + 1]):
             j = col[e]
-            ag = _grid_fields(HEg[e], Y, Dt, Dp)[0]
-            _, tc, pc = _grid_fields(HEc[e], Y, Dt, Dp)
-            an = _grid_fields(HI[("node_feat", "U_I")][j], Y, Dt, Dp)[0]
-            af = _grid_fields(HI[("node_flip", "U_I")][j], Y, Dt, Dp)[0]
-            _, tn, pn = _grid_fields(HI[("node_feat", "U_I_curl")][j], Y, Dt, Dp)
-            _, tf, pf = _grid_fields(HI[("node_flip", "U_I_curl")][j], Y, Dt, Dp)
-            Sn = Sn + ag * an + bf.bracket(tc, pc, tf, pf)
-            So = So + bf.bracket(tc, pc, tn, pn) + ag * af
-        bn.append(np.einsum("knr,rk->nk", U["U_out_even"], np.einsum("p,rp,pk->rk", W, Sn, Y)))
-        bo.append(np.einsum("knr,rk->nk", U["U_out_odd"], np.einsum("p,rp,pk->rk", W, So, Y)))
-    assert _rel(on, np.array(bn)) < 1e-8
-    assert _rel(oo, np.array(bo)) < 1e-8
+            for s2 in range(2):
+                for cat in range(2):
+                    b = _block(cat, s2)
+                    he = np.einsum("knr,nk->rk", UE[b], rad[e][:, lk]) * Ye[e][None, :]
+                    hi = np.einsum("knr,nk->rk", UI[b], X2[s2][j])
+                    ae, te, pe = _grid_fields(he, Y, Dt, Dp)
+                    ai, ti, pi = _grid_fields(hi, Y, Dt, Dp)
+                    S[b][q] += ae * ai if cat == 0 else bf.bracket(te, pe, ti, pi)
+    bn, bo = _sum_blocks(lmax, S, Uo, W, Y)
+    assert _rel(on, bn) < 1e-8
+    assert _rel(oo, bo) < 1e-8
+    assert np.abs(on).max() > 1e-2 and np.abs(oo).max() > 1e-2
+
+
+def test_mp_general_inversion():
+    lmax = 4
+    d = _mp_d(lmax, seed=9)
+    rec = np.arange(d["row_ptr"].shape[0] - 1)
+    on, oo = _mp(lmax, d, rec)
+    P = _parity_diag(lmax)
+    inn, ino = _mp(lmax, d, rec, edge_unit=-d["edge_unit"].astype(np.float64),
+                   node_feat=d["node_feat"] * P, node_flip=-d["node_flip"] * P)
+    assert _rel(inn, on * P) < 1e-13
+    assert _rel(ino, -oo * P) < 1e-13
