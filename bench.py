@@ -53,27 +53,68 @@ def grid_dims(lmax: int):
 
 # ---------------------------------------------------------------- algorithmic work
 
-def receiver_bytes(lmax: int, R: int, N: int, E: int, slots: int = 1) -> int:
-    """HBM bytes the receiver pass must move (fp32): per edge the three sender grid
-    fields (3 R UV) of every node slot, the edge radial coefficients (R L), the unit
-    vector and the sender index; per receiver the row pointer and the two analysed
-    fields (2 R K)."""
+def receiver_bytes(lmax: int, R: int, N: int, E: int, slots: int = 1, planes: int = 0,
+                   rt_blocks: int = 1, t_fields: int = 2) -> int:
+    """HBM bytes the receiver pass must move (fp32): per edge the sender grid fields the
+    couplings read (value A for a Gaunt coupling, dA/dx and dA/dphi for a curl coupling:
+    3 R UV per node slot when both categories share the factors), the edge radial
+    coefficients (R L per distinct edge factor block), the unit vector and the sender
+    index; per receiver the row pointer and the analysed fields (R K each)."""
     U, V = grid_dims(lmax)
     L, K = lmax + 1, (lmax + 1) ** 2
-    per_edge = 4 * (3 * slots * R * U * V + R * L + 3 + 1)
-    per_recv = 4 * (1 + 2 * R * K)
+    planes = planes or 3 * slots
+    per_edge = 4 * (planes * R * U * V + rt_blocks * R * L + 3 + 1)
+    per_recv = 4 * (1 + t_fields * R * K)
     return E * per_edge + N * per_recv
 
 
-def onsite_grid_flops(lmax: int, R: int, N: int) -> int:
+def live_blocks(flip1: bool, flip2: bool):
+    """Blocks b = 2 category + sector that receive a coupling: Gaunt sends equal slot pairs
+    to the even sector and mixed ones to the odd sector, curl the other way round."""
+    live = set()
+    for s1 in (0, 1) if flip1 else (0,):
+        for s2 in (0, 1) if flip2 else (0,):
+            rel = int(s1 != s2)
+            live.update({rel, 2 + (1 - rel)})
+    return sorted(live)
+
+
+def general_receiver_bytes(w, N: int, E: int) -> int:
+    """Algorithmic receiver bytes of general message passing: one grid field per Gaunt
+    block, two per curl block; one edge factor per block (one when shared); one analysed
+    field per block with per-category weights (two otherwise)."""
+    live = live_blocks(False, w.two_slot)
+    planes = sum(1 if b < 2 else 2 for b in live)
+    rt = 1 if w.in_blocks == 1 else len(live)
+    tf = len(live) if w.out_blocks == 2 else 2
+    return receiver_bytes(w.lmax, w.R, N, E, planes=planes, rt_blocks=rt, t_fields=tf)
+
+
+def onsite_grid_flops(lmax: int, R: int, N: int, kind: str = "both") -> int:
     """fp32 flops of the on-site grid stage with the paper's dense transforms, per
-    (node, rank): Legendre synthesis of F and dF/dx for both operands (8 U L^2),
-    Fourier synthesis of 3 fields per operand (12 U V M), product and curl (4 U V),
-    Fourier analysis of 2 fields (4 U V M), Gauss-Legendre analysis (4 U L^2)."""
+    (node, rank). Both products: Legendre synthesis of F and dF/dx for both operands
+    (8 U L^2), Fourier synthesis of 3 fields per operand (12 U V M), product and curl
+    (4 U V), Fourier analysis of 2 fields (4 U V M), Gauss-Legendre analysis (4 U L^2).
+    Gaunt only: F of both operands, one field each, one product, one analysis. Curl
+    only: F and dF/dx of both operands, two fields each, the bracket, one analysis."""
     U, V = grid_dims(lmax)
     L, M = lmax + 1, 2 * lmax + 1
-    per = 12 * U * L * L + 16 * U * V * M + 4 * U * V
+    per = {"both": 12 * U * L * L + 16 * U * V * M + 4 * U * V,
+           "gaunt": 6 * U * L * L + 6 * U * V * M + U * V,
+           "curl": 10 * U * L * L + 10 * U * V * M + 3 * U * V}[kind]
     return N * R * per
+
+
+def general_onsite_flops(w) -> int:
+    """Algorithmic grid flops of the general on-site call: with shared factors every slot
+    pair needs both products; with per-block factors every (slot pair, block) needs the
+    product of its category only."""
+    pairs = [(s1, s2) for s1 in ((0, 1) if w.flip1 else (0,))
+             for s2 in ((0, 1) if w.two_slot else (0,))]
+    if w.in_blocks == 1:
+        return len(pairs) * onsite_grid_flops(w.lmax, w.R, w.n)
+    return len(pairs) * (onsite_grid_flops(w.lmax, w.R, w.n, "gaunt")
+                         + onsite_grid_flops(w.lmax, w.R, w.n, "curl"))
 
 
 # ---------------------------------------------------------------- helpers
@@ -84,9 +125,8 @@ def to_dev(d, keys):
 
     out = {}
     for k in keys:
-        a = d[k]
-        t = torch.from_numpy(np.ascontiguousarray(a))
-        out[k] = t.cuda()
+        a = d.get(k)
+        out[k] = None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
     return out
 
 
@@ -120,8 +160,10 @@ def cpu_baseline(w, d, budget_s: float = 15.0):
         unit_name = "receivers"
     else:
         def run(n):
+            cut = lambda k: None if d.get(k) is None else d[k][:n]
             return oracle.onsite(w.lmax, d["A"][:n], d["B"][:n], d["U_A"], d["U_B"],
-                                 d["U_out_even"], d["U_out_odd"])
+                                 d["U_out_even"], d["U_out_odd"], A_flip=cut("A_flip"),
+                                 B_flip=cut("B_flip"))
         unit_name = "nodes"
     probe = min(w.n, 16)
     t0 = time.perf_counter()
@@ -146,7 +188,35 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
     if d is None:
         d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
-    if w.kind == "mp":
+    if w.general and w.kind == "mp":
+        t = to_dev(d, MP_KEYS + ("node_flip",))
+        E = int(d["n_edges"])
+        op = cg.CGTP_OP_MESSAGE_PASS_GENERAL
+        ws = torch.empty(cg.workspace_bytes_general(plan, op, w.n, E, 2 if w.two_slot else 0,
+                                                    w.in_blocks, w.out_blocks),
+                         dtype=torch.uint8, device="cuda")
+        oe = torch.empty_like(t["node_feat"])
+        oo = torch.empty_like(t["node_feat"])
+
+        def step():
+            cg.message_pass_general(plan, *(t[k] for k in MP_KEYS), node_flip=t["node_flip"],
+                                    out_even=oe, out_odd=oo, workspace=ws)
+    elif w.general:
+        t = to_dev(d, ONSITE_KEYS + ("A_flip", "B_flip"))
+        E = 0
+        op = cg.CGTP_OP_ONSITE_GENERAL
+        flips = (1 if w.flip1 else 0) | (2 if w.two_slot else 0)
+        ws = torch.empty(cg.workspace_bytes_general(plan, op, w.n, 0, flips, w.in_blocks,
+                                                    w.out_blocks),
+                         dtype=torch.uint8, device="cuda")
+        oe = torch.empty_like(t["A"])
+        oo = torch.empty_like(t["A"])
+
+        def step():
+            cg.onsite_general(plan, t["A"], t["B"], t["U_A"], t["U_B"], t["U_out_even"],
+                              t["U_out_odd"], A_flip=t["A_flip"], B_flip=t["B_flip"],
+                              out_even=oe, out_odd=oo, workspace=ws)
+    elif w.kind == "mp":
         two = w.two_slot
         t = to_dev(d, MP_KEYS + (("node_flip",) if two else ()))
         E = int(d["n_edges"])
@@ -201,22 +271,26 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name,
-                   "kind": ("message_passing_two_slot" if w.two_slot else "message_passing")
-                   if w.kind == "mp" else "onsite",
+                   "kind": ("message_passing" if w.kind == "mp" else "onsite")
+                   + ("_general" if w.general else "_two_slot" if w.two_slot else ""),
                    "nodes": w.n, "edges": E, "lmax": w.lmax, "channels": w.C, "rank": w.R,
                    "grid": f"{U}x{V}", "seed": w.seed},
         "stages_ms": {k: round(v, 4) for k, v in stage_avg.items()},
         "dominant_kernel": dom,
     }
     t_dom = stage_avg[dom] / 1e3
+    if w.general:
+        rec["config"].update(in_blocks=w.in_blocks, out_blocks=w.out_blocks,
+                             flips=[bool(w.flip1), bool(w.two_slot)])
     if w.kind == "mp" and dom == "receiver":
-        alg = receiver_bytes(w.lmax, w.R, w.n, E, 2 if w.two_slot else 1)
+        alg = (general_receiver_bytes(w, w.n, E) if w.general
+               else receiver_bytes(w.lmax, w.R, w.n, E, 2 if w.two_slot else 1))
         traffic = load_traffic(w.name)
         rec["roofline"] = {"bound": "hbm", "achieved": alg / t_dom / 1e9, "peak": HBM_PEAK_GBS,
                            "unit": "GB/s", "frac": alg / t_dom / 1e9 / HBM_PEAK_GBS,
                            "traffic": traffic, "algorithmic_bytes": alg}
     elif w.kind == "onsite" and dom == "grid_product_curl_analysis":
-        fl = onsite_grid_flops(w.lmax, w.R, w.n)
+        fl = general_onsite_flops(w) if w.general else onsite_grid_flops(w.lmax, w.R, w.n)
         rec["roofline"] = {"bound": "alu", "achieved": fl / t_dom / 1e12,
                            "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                            "frac": fl / t_dom / 1e12 / FP32_PEAK_TFLOPS,

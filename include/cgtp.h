@@ -81,6 +81,8 @@ extern "C" {
 #define CGTP_OP_ONSITE 0
 #define CGTP_OP_MESSAGE_PASS 1
 #define CGTP_OP_MESSAGE_PASS_TWO_SLOT 2
+#define CGTP_OP_ONSITE_GENERAL 3        /* cgtp_workspace_bytes_general / cgtp_stage_times */
+#define CGTP_OP_MESSAGE_PASS_GENERAL 4
 
 typedef struct cgtp_plan_s *cgtp_plan;
 
@@ -177,6 +179,59 @@ int cgtp_message_pass_two_slot(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                                const void *U_out_even, const void *U_out_odd, void *out_even,
                                void *out_odd, void *workspace, size_t ws_bytes, void *stream);
 
+/* General parameterization (Eqs. msgpass-cp-alpha and msgpass-cp-beta; Table 1; the
+ * on-site contraction with parity-labelled inputs). Each coupling category (Gaunt,
+ * Category alpha; surface curl, Category beta) and each output parity sector (out_even,
+ * parity (-1)^l; out_odd, parity -(-1)^l) has its own CP input factors and output weights:
+ * block b = 2 * category + sector (0 Gaunt->even, 1 Gaunt->odd, 2 curl->even,
+ * 3 curl->odd). An operand may carry, besides its natural-parity slot (parity (-1)^l), a
+ * parity-flipped slot (parity -(-1)^l). By p = p1 p2 a slot pair of equal relative parity
+ * sends its Gaunt coupling to out_even and its curl coupling to out_odd; a mixed pair the
+ * other way round. Every pair is contracted with the factors of the block it feeds:
+ *   out_s = sum_{cat} sum_r Uout[cat, s][l][n][r] T_{2 cat + s}[r][k],
+ *   T_b   = sum over the slot pairs (s1, s2) routed to b of the block-b coupling of
+ *           U1[b]^T X1[s1] and U2[b]^T X2[s2] (Gaunt table G or curl table Q).
+ * Factor layouts: in_blocks = 1: U [L][C][R] shared by every block; 2: U [2][L][C][R]
+ * (Gaunt, curl); 4: U [4][L][C][R] indexed by b. out_blocks = 1: U_out_even and U_out_odd
+ * [L][C][R] serve both categories; 2: each is [2][L][C][R] (Gaunt, curl).
+ * With in_blocks = 1, out_blocks = 1 and no flipped slots these are cgtp_onsite /
+ * cgtp_message_pass. Other cases stack one rank group per (slot pair, factor block) and
+ * run the same kernels at a multiple of the plan's rank (at most 8x on-site, 4x for
+ * message passing), so the workspace grows accordingly: query it with
+ * cgtp_workspace_bytes_general. Preconditions, ownership, streams and errors are those of
+ * cgtp_onsite / cgtp_message_pass; CGTP_ERR_UNSUPPORTED also when n_nodes times the
+ * stacked rank exceeds 2^31 - 1. */
+
+/* Workspace of a general call. op: CGTP_OP_ONSITE_GENERAL or CGTP_OP_MESSAGE_PASS_GENERAL;
+ * flips: bit 0 set when the first on-site operand has a flipped slot, bit 1 when the second
+ * operand (on-site) or the node feature (message passing) has one; in_blocks, out_blocks
+ * as in the calls. */
+int cgtp_workspace_bytes_general(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edges,
+                                 int flips, int in_blocks, int out_blocks, size_t *bytes);
+
+/* On-site contraction with general parity.
+ *   A, B            [N][C][K] natural-parity slots; A_flip, B_flip [N][C][K] or NULL.
+ *   U_A, U_B        input factors, in_blocks blocks of [L][C][R].
+ *   U_out_even, U_out_odd  output weights, out_blocks blocks of [L][C][R] each.
+ *   out_even, out_odd      [N][C][K]; either may be NULL (not both). */
+int cgtp_onsite_general(cgtp_plan plan, int64_t n_nodes, const void *A, const void *A_flip,
+                        const void *B, const void *B_flip, int in_blocks, const void *U_A,
+                        const void *U_B, int out_blocks, const void *U_out_even,
+                        const void *U_out_odd, void *out_even, void *out_odd, void *workspace,
+                        size_t ws_bytes, void *stream);
+
+/* Message passing with general parity: the edge feature R Y is the first operand (natural
+ * parity only), the node feature the second (node_flip: its flipped slot, or NULL).
+ *   U_E, U_I        input factors of the edge radial and node operands, in_blocks blocks.
+ * Other arguments as in cgtp_message_pass; U_out_* as in cgtp_onsite_general. */
+int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
+                              const int32_t *row_ptr, const int32_t *col, const void *edge_unit,
+                              const void *edge_radial, const void *node_feat,
+                              const void *node_flip, int in_blocks, const void *U_E,
+                              const void *U_I, int out_blocks, const void *U_out_even,
+                              const void *U_out_odd, void *out_even, void *out_odd,
+                              void *workspace, size_t ws_bytes, void *stream);
+
 /* Per-stage GPU time of the calls made since the previous cgtp_stage_times on
  * this plan (plan created with CGTP_TIME_STAGES), in the spirit of the paper's
  * per-step breakdown (App. D, Table 4). Waits for the recorded events, writes the
@@ -187,7 +242,9 @@ int cgtp_message_pass_two_slot(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
  * 0 contract node features, 1 sender grid fields, 2 contract edge radial,
  * 3 receiver pass (edge synthesis, products, neighbour sum, analysis),
  * 4 project even, 5 project odd. CGTP_OP_MESSAGE_PASS_TWO_SLOT has the same six
- * stages, each covering both node slots. A skipped stage counts as 0.
+ * stages, each covering both node slots; CGTP_OP_ONSITE_GENERAL and
+ * CGTP_OP_MESSAGE_PASS_GENERAL those of CGTP_OP_ONSITE / CGTP_OP_MESSAGE_PASS, covering
+ * every rank group. A skipped stage counts as 0.
  * Errors: CGTP_ERR_ARG (NULL, flag not set, unknown op), CGTP_ERR_HIP. */
 int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages, int *n_calls);
 

@@ -28,10 +28,13 @@ CGTP_TIME_STAGES = 4
 CGTP_OP_ONSITE = 0
 CGTP_OP_MESSAGE_PASS = 1
 CGTP_OP_MESSAGE_PASS_TWO_SLOT = 2
+CGTP_OP_ONSITE_GENERAL = 3
+CGTP_OP_MESSAGE_PASS_GENERAL = 4
 CGTP_MAX_LMAX = 24
 
 EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
-            "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_stage_times",
+            "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_workspace_bytes_general",
+            "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_stage_times",
             "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables")
 ONSITE_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis", "project_even",
                  "project_odd")
@@ -70,6 +73,12 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_onsite.argtypes = [vp, i64] + [vp] * 8 + [vp, sz, vp]
     lib.cgtp_message_pass.argtypes = [vp, i64, i64] + [vp] * 11 + [vp, sz, vp]
     lib.cgtp_message_pass_two_slot.argtypes = [vp, i64, i64] + [vp] * 12 + [vp, sz, vp]
+    lib.cgtp_workspace_bytes_general.argtypes = [vp, i32, i64, i64, i32, i32, i32,
+                                                 ctypes.POINTER(sz)]
+    lib.cgtp_onsite_general.argtypes = ([vp, i64] + [vp] * 4 + [i32, vp, vp, i32] + [vp] * 4
+                                        + [vp, sz, vp])
+    lib.cgtp_message_pass_general.argtypes = ([vp, i64, i64] + [vp] * 6 + [i32, vp, vp, i32]
+                                              + [vp] * 4 + [vp, sz, vp])
     lib.cgtp_stage_times.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double), i32,
                                      ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.cgtp_destroy.argtypes = [vp]
@@ -144,7 +153,7 @@ def stage_times(plan: Plan, op: int):
     ns, nc = ctypes.c_int(), ctypes.c_int()
     _check(load_library().cgtp_stage_times(plan.handle, op, ms, 8, ctypes.byref(ns),
                                            ctypes.byref(nc)), "cgtp_stage_times")
-    names = ONSITE_STAGES if op == CGTP_OP_ONSITE else MP_STAGES
+    names = ONSITE_STAGES if op in (CGTP_OP_ONSITE, CGTP_OP_ONSITE_GENERAL) else MP_STAGES
     return {names[i]: ms[i] for i in range(ns.value)}, nc.value
 
 
@@ -247,6 +256,101 @@ def message_pass(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_feat, U_
     else:
         _check(lib.cgtp_message_pass_two_slot(*head, _ptr(node_flip), *tail),
                "cgtp_message_pass_two_slot")
+    return outs[0], outs[1]
+
+
+def workspace_bytes_general(plan: Plan, op: int, n_nodes: int, n_edges: int = 0, flips: int = 0,
+                            in_blocks: int = 1, out_blocks: int = 1) -> int:
+    """cgtp_workspace_bytes_general (flips: bit 0 first on-site operand, bit 1 second operand
+    or node feature)."""
+    out = ctypes.c_size_t()
+    _check(load_library().cgtp_workspace_bytes_general(plan.handle, op, n_nodes, n_edges, flips,
+                                                       in_blocks, out_blocks, ctypes.byref(out)),
+           "cgtp_workspace_bytes_general")
+    return out.value
+
+
+def _blocks(plan: Plan, name: str, U, allowed):
+    """Number of factor blocks of a stacked factor tensor: [L, C, R] is 1, [n, L, C, R] is n."""
+    L = plan.lmax + 1
+    base = (L, plan.channels, plan.rank)
+    n = 1 if U is not None and U.dim() == 3 else (U.shape[0] if U is not None else 0)
+    if n not in allowed:
+        raise ValueError(f"{name}: expected {allowed} stacked blocks of {base}")
+    _want(plan, name, U, base if n == 1 else (n,) + base)
+    return n
+
+
+def _outputs(plan: Plan, like, out_even, out_odd, U_out_even, U_out_odd):
+    torch = _torch()
+    outs, nout = [], set()
+    for nm, o, U in (("out_even", out_even, U_out_even), ("out_odd", out_odd, U_out_odd)):
+        if o is False:
+            outs.append(None)
+            continue
+        nout.add(_blocks(plan, nm.replace("out", "U_out"), U, (1, 2)))
+        if o is None:
+            o = torch.empty_like(like)
+        _want(plan, nm, o, like.shape)
+        outs.append(o)
+    if len(nout) != 1:
+        raise ValueError("U_out_even and U_out_odd must have the same number of blocks")
+    return outs, nout.pop()
+
+
+def onsite_general(plan: Plan, A, B, U_A, U_B, U_out_even, U_out_odd, A_flip=None, B_flip=None,
+                   out_even=None, out_odd=None, workspace=None, stream=None):
+    """cgtp_onsite_general. A, B (and the flipped slots A_flip, B_flip) [N, C, K].
+    U_A, U_B: [L, C, R], or stacked [2, L, C, R] (Gaunt, curl) or [4, L, C, R] (block
+    2 * category + sector). U_out_even, U_out_odd: [L, C, R] or [2, L, C, R] (Gaunt, curl)."""
+    N = A.shape[0]
+    L = plan.lmax + 1
+    _want(plan, "A", A, (N, plan.channels, L * L))
+    for nm, X in (("B", B), ("A_flip", A_flip), ("B_flip", B_flip)):
+        if X is not None or nm == "B":
+            _want(plan, nm, X, A.shape)
+    nin = _blocks(plan, "U_A", U_A, (1, 2, 4))
+    if _blocks(plan, "U_B", U_B, (1, 2, 4)) != nin:
+        raise ValueError("U_A and U_B must have the same number of blocks")
+    outs, nout = _outputs(plan, A, out_even, out_odd, U_out_even, U_out_odd)
+    ws_ptr, ws_len = None, 0
+    if workspace is not None:
+        ws_ptr, ws_len = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(load_library().cgtp_onsite_general(
+        plan.handle, N, _ptr(A), _ptr(A_flip), _ptr(B), _ptr(B_flip), nin, _ptr(U_A), _ptr(U_B),
+        nout, _ptr(U_out_even), _ptr(U_out_odd), _ptr(outs[0]), _ptr(outs[1]), ws_ptr, ws_len,
+        _stream_handle(stream)), "cgtp_onsite_general")
+    return outs[0], outs[1]
+
+
+def message_pass_general(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,
+                         U_out_even, U_out_odd, node_flip=None, out_even=None, out_odd=None,
+                         workspace=None, stream=None):
+    """cgtp_message_pass_general. Arguments as in message_pass; U_E, U_I and U_out_* stacked
+    as in onsite_general."""
+    torch = _torch()
+    N = node_feat.shape[0]
+    E = col.shape[0]
+    L = plan.lmax + 1
+    _want(plan, "row_ptr", row_ptr, (N + 1,), torch.int32)
+    _want(plan, "col", col, (E,), torch.int32)
+    _want(plan, "edge_unit", edge_unit, (E, 3))
+    _want(plan, "edge_radial", edge_radial, (E, plan.channels, L))
+    _want(plan, "node_feat", node_feat, (N, plan.channels, L * L))
+    if node_flip is not None:
+        _want(plan, "node_flip", node_flip, node_feat.shape)
+    nin = _blocks(plan, "U_E", U_E, (1, 2, 4))
+    if _blocks(plan, "U_I", U_I, (1, 2, 4)) != nin:
+        raise ValueError("U_E and U_I must have the same number of blocks")
+    outs, nout = _outputs(plan, node_feat, out_even, out_odd, U_out_even, U_out_odd)
+    ws_ptr, ws_len = None, 0
+    if workspace is not None:
+        ws_ptr, ws_len = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(load_library().cgtp_message_pass_general(
+        plan.handle, N, E, _ptr(row_ptr), _ptr(col), _ptr(edge_unit), _ptr(edge_radial),
+        _ptr(node_feat), _ptr(node_flip), nin, _ptr(U_E), _ptr(U_I), nout, _ptr(U_out_even),
+        _ptr(U_out_odd), _ptr(outs[0]), _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)),
+        "cgtp_message_pass_general")
     return outs[0], outs[1]
 
 

@@ -1,10 +1,12 @@
 // Per-degree channel contraction (Eqs. struct-H, msgpass-HI, msgpass-tildeR and
 // the lambda projection struct-phi / cat-alpha-phi / cat-beta-phi):
 //
-//   Y[b*y_sb + o*y_so + k*y_sk] = scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so] * X[b][i][k]
+//   Y[b*y_sb + o*y_so + k*y_sk] (+)= scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so]
+//                                                   * X[b*x_sb + i*K + k]
 //
-// For a fixed degree l this is a GEMM Y_l[o][c] = sum_i W_l[i][o] X_l[i][c] over
-// the columns c = (b, m), m = 0..2l (or c = b when k is the degree itself).
+// (with accumulate the result is added to Y). For a fixed degree l this is a GEMM
+// Y_l[o][c] = sum_i W_l[i][o] X_l[i][c] over the columns c = (b, m), m = 0..2l (or c = b
+// when k is the degree itself).
 //
 // fp32 path: MFMA tiles (v_mfma_f32_16x16x4f32). k_contract_mfma: a block owns 64
 // output rows and 64 columns of one degree of a group of 64 nodes; the blocks of a group
@@ -61,8 +63,8 @@ template <bool WT>
 __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     int64_t B, int Cin, int Cout, int K, int tiles_per_group, int otiles,
     const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
-    const float *__restrict__ X, float *__restrict__ Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
-    const float *__restrict__ scale)
+    const float *__restrict__ X, int64_t x_sb, float *__restrict__ Y, int64_t y_sb, int64_t y_so,
+    int64_t y_sk, const float *__restrict__ scale, bool accumulate)
 {
     __shared__ float Ws[WT ? kTile * kSWt : kCs * kSWo];
     __shared__ float Xs[kCs * kSWo];
@@ -104,7 +106,7 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     const bool c_ok = cg < ncols;
     const int bl = c_ok ? cg / width : 0;
     const int mm = c_ok ? cg - bl * width : 0;
-    const float *xcol = X + (b0 + bl) * (int64_t)Cin * K + kofs + mm;
+    const float *xcol = X + (b0 + bl) * x_sb + kofs + mm;
     float wr[kNS], xr[kNS];
     auto fetch = [&](int i0) {
 #pragma unroll
@@ -169,7 +171,11 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 int o = o0 + osub + 16 * a + 4 * gg + j;
-                if (o < Cout) ycol[(int64_t)o * y_so] = acc[a][bb][j] * sc;
+                if (o < Cout) {
+                    float v = acc[a][bb][j] * sc;
+                    if (accumulate) v += ycol[(int64_t)o * y_so];
+                    ycol[(int64_t)o * y_so] = v;
+                }
             }
         }
 }
@@ -191,9 +197,9 @@ constexpr int kNX = kTile * kCk * kLG / kThreadsC;  // staged elements per threa
 
 __global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
     int64_t B, int Cin, int Cout, int L, int otiles, int lgroups, const float *__restrict__ W,
-    unsigned w_bytes, int w_sl, int w_si, int w_so, const float *__restrict__ X,
+    unsigned w_bytes, int w_sl, int w_si, int w_so, const float *__restrict__ X, int x_sb,
     float *__restrict__ Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
-    const float *__restrict__ scale)
+    const float *__restrict__ scale, bool accumulate)
 {
     __shared__ float Xs[kTile * kSB];
     __shared__ float Ws[kLG][kCk][kSW];
@@ -223,7 +229,7 @@ __global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
 
     // the row group's inputs (reads past its last row return 0) and the weights
     const __amdgpu_buffer_rsrc_t xs =
-        rsrc(X + b0 * (int64_t)Cin * L, (unsigned)((int64_t)nb * Cin * L * 4));
+        rsrc(X + b0 * (int64_t)x_sb, (unsigned)(((int64_t)(nb - 1) * x_sb + (int64_t)Cin * L) * 4));
     const __amdgpu_buffer_rsrc_t ws = rsrc(W, w_bytes);
     // Staged elements of this thread, k = tid + 256 s. X: row b = k / (kCk kLG), slot
     // r = k % (kCk kLG) = i kLG + l of the row's slice (consecutive threads read consecutive
@@ -237,7 +243,7 @@ __global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
         const int k = tid + kThreadsC * s2;
         const int b = k / (kCk * kLG), r = k - b * (kCk * kLG);
         const int i = r / kLG, l = r - i * kLG;
-        xoff[s2] = l < nl ? (unsigned)((b * Cin + i) * L + l0 + l) * 4u : kOutside;
+        xoff[s2] = l < nl && b < nb ? (unsigned)(b * x_sb + i * L + l0 + l) * 4u : kOutside;
         xlds[s2] = b * kSB + r;
     }
     const bool full_i = Cin % kCk == 0;  // every slice has kCk inputs
@@ -300,9 +306,12 @@ __global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int b = wb + 16 * a + 4 * g + j;
-                    if (b < nb)
-                        Y[(b0 + b) * y_sb + (int64_t)o * y_so + (int64_t)(l0 + l) * y_sk] =
-                            acc[l][a][c][j] * sc;
+                    if (b < nb) {
+                        float *y = Y + (b0 + b) * y_sb + (int64_t)o * y_so + (int64_t)(l0 + l) * y_sk;
+                        float v = acc[l][a][c][j] * sc;
+                        if (accumulate) v += *y;
+                        *y = v;
+                    }
                 }
             }
     }
@@ -312,10 +321,11 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int Cout, int K,
                                                          int kdeg, const T *__restrict__ W,
                                                          int64_t w_sl, int64_t w_si, int64_t w_so,
-                                                         const T *__restrict__ X,
+                                                         const T *__restrict__ X, int64_t x_sb,
                                                          T *__restrict__ Y, int64_t y_sb,
                                                          int64_t y_so, int64_t y_sk,
-                                                         const T *__restrict__ scale)
+                                                         const T *__restrict__ scale,
+                                                         bool accumulate)
 {
     const int64_t total = B * (int64_t)Cout * K;
     for (int64_t idx = blockIdx.x * (int64_t)256 + threadIdx.x; idx < total;
@@ -326,11 +336,12 @@ __global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int
         int64_t b = rest / Cout;
         int l = kdeg ? k : isqrt_small(k);
         const T *w = W + l * w_sl + o * w_so;
-        const T *x = X + b * (int64_t)Cin * K + k;
+        const T *x = X + b * x_sb + k;
         T acc = 0;
         for (int i = 0; i < Cin; ++i) acc += w[i * w_si] * x[(int64_t)i * K];
         if (scale) acc *= scale[l];
-        Y[b * y_sb + o * y_so + (int64_t)k * y_sk] = acc;
+        T *y = Y + b * y_sb + o * y_so + (int64_t)k * y_sk;
+        *y = accumulate ? *y + acc : acc;
     }
 }
 
@@ -339,10 +350,11 @@ __global__ __launch_bounds__(256) void k_contract_simple(int64_t B, int Cin, int
 template <>
 hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg, const float *W,
                                   int64_t w_sl, int64_t w_si, int64_t w_so, const float *X,
-                                  float *Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
-                                  const float *scale, hipStream_t s)
+                                  int64_t x_sb, float *Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
+                                  const float *scale, bool accumulate, hipStream_t s)
 {
     if (B == 0 || Cout == 0 || K == 0) return hipSuccess;
+    if (x_sb < (int64_t)Cin * K) return hipErrorInvalidValue;
     if (kdeg) {
         const int64_t groups = (B + kTile - 1) / kTile;
         const int otiles = (Cout + kTile - 1) / kTile;
@@ -352,12 +364,14 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
         // 32-bit buffer offsets: the row group's inputs and every weight index must fit
         const int64_t w_span = 4 * ((K - 1) * w_sl + (int64_t)(Cin - 1) * w_si +
                                     (int64_t)(Cout - 1) * w_so + 1);
-        if (w_span >= (int64_t)kOutside || 4 * (int64_t)kTile * Cin * K >= (int64_t)kOutside ||
+        if (w_span >= (int64_t)kOutside ||
+            4 * ((int64_t)(kTile - 1) * x_sb + (int64_t)Cin * K) >= (int64_t)kOutside ||
             w_sl < 0 || w_si < 0 || w_so < 0)
             return hipErrorNotSupported;
         hipLaunchKernelGGL(k_contract_kdeg, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B,
                            Cin, Cout, K, otiles, lgroups, W, (unsigned)w_span, (int)w_sl,
-                           (int)w_si, (int)w_so, X, Y, y_sb, y_so, y_sk, scale);
+                           (int)w_si, (int)w_so, X, (int)x_sb, Y, y_sb, y_so, y_sk, scale,
+                           accumulate);
         return hipGetLastError();
     }
     const int64_t groups = (B + kTile - 1) / kTile;
@@ -367,27 +381,30 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     if (w_si == 1)
         hipLaunchKernelGGL(k_contract_mfma<true>, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B,
-                           Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, Y, y_sb,
-                           y_so, y_sk, scale);
+                           Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, x_sb, Y,
+                           y_sb, y_so, y_sk, scale, accumulate);
     else
         hipLaunchKernelGGL(k_contract_mfma<false>, dim3((unsigned)blocks), dim3(kThreadsC), 0, s,
-                           B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, Y,
-                           y_sb, y_so, y_sk, scale);
+                           B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, x_sb,
+                           Y, y_sb, y_so, y_sk, scale, accumulate);
     return hipGetLastError();
 }
 
 template <>
 hipError_t launch_contract<double>(int64_t B, int Cin, int Cout, int K, bool kdeg,
                                    const double *W, int64_t w_sl, int64_t w_si, int64_t w_so,
-                                   const double *X, double *Y, int64_t y_sb, int64_t y_so,
-                                   int64_t y_sk, const double *scale, hipStream_t s)
+                                   const double *X, int64_t x_sb, double *Y, int64_t y_sb,
+                                   int64_t y_so, int64_t y_sk, const double *scale,
+                                   bool accumulate, hipStream_t s)
 {
     int64_t total = B * (int64_t)Cout * K;
     if (total == 0) return hipSuccess;
+    if (x_sb < (int64_t)Cin * K) return hipErrorInvalidValue;
     int64_t blocks = (total + 255) / 256;
     if (blocks > (1 << 20)) blocks = 1 << 20;
     hipLaunchKernelGGL(k_contract_simple<double>, dim3((unsigned)blocks), dim3(256), 0, s, B, Cin,
-                       Cout, K, kdeg ? 1 : 0, W, w_sl, w_si, w_so, X, Y, y_sb, y_so, y_sk, scale);
+                       Cout, K, kdeg ? 1 : 0, W, w_sl, w_si, w_so, X, x_sb, Y, y_sb, y_so, y_sk,
+                       scale, accumulate);
     return hipGetLastError();
 }
 

@@ -66,23 +66,25 @@ template <typename T>
 Tabs<T> bind_tables(const Dims &d, const void *dev);
 
 // Generic per-degree channel contraction (Eq. struct-H / struct-phi / msgpass-tildeR):
-//   Y[b*y_sb + o*y_so + k*y_sk] = scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so] * X[b][i][k]
-// with X [B][Cin][K]; l(k) = k when kdeg, else the degree of the flattened index
-// k. scale may be null. fp32: MFMA tiles; fp64: one thread per output (both
-// specialised in contract.hip).
+//   Y[b*y_sb + o*y_so + k*y_sk] (+)= scale[l(k)] * sum_i W[l(k)*w_sl + i*w_si + o*w_so]
+//                                                   * X[b*x_sb + i*K + k]
+// for rows b < B, inputs i < Cin, outputs o < Cout; x_sb >= Cin*K (Cin*K when X is a packed
+// [B][Cin][K]); l(k) = k when kdeg, else the degree of the flattened index k. scale may be
+// null. With accumulate the result is added to Y instead of overwriting it. fp32: MFMA
+// tiles; fp64: one thread per output (both specialised in contract.hip).
 template <typename T>
 hipError_t launch_contract(int64_t B, int Cin, int Cout, int K, bool kdeg, const T *W,
-                           int64_t w_sl, int64_t w_si, int64_t w_so, const T *X, T *Y,
-                           int64_t y_sb, int64_t y_so, int64_t y_sk, const T *scale,
-                           hipStream_t s);
+                           int64_t w_sl, int64_t w_si, int64_t w_so, const T *X, int64_t x_sb,
+                           T *Y, int64_t y_sb, int64_t y_so, int64_t y_sk, const T *scale,
+                           bool accumulate, hipStream_t s);
 template <>
 hipError_t launch_contract<float>(int64_t, int, int, int, bool, const float *, int64_t, int64_t,
-                                  int64_t, const float *, float *, int64_t, int64_t, int64_t,
-                                  const float *, hipStream_t);
+                                  int64_t, const float *, int64_t, float *, int64_t, int64_t,
+                                  int64_t, const float *, bool, hipStream_t);
 template <>
 hipError_t launch_contract<double>(int64_t, int, int, int, bool, const double *, int64_t, int64_t,
-                                   int64_t, const double *, double *, int64_t, int64_t, int64_t,
-                                   const double *, hipStream_t);
+                                   int64_t, const double *, int64_t, double *, int64_t, int64_t,
+                                   int64_t, const double *, bool, hipStream_t);
 
 // Node-side synthesis of the three grid fields (A, dA/dx, dA/dphi) of H[b][r][K]:
 // SF[b][r][3][UVs] (Eqs. struct-F, struct-tildeA plus the derivative passes).

@@ -10,6 +10,7 @@
 
 namespace {
 constexpr int kMaxStages = 6;
+constexpr int kNumOps = 5;  // CGTP_OP_ONSITE .. CGTP_OP_MESSAGE_PASS_GENERAL
 // HIP events bracketing the kernel stages of one call (CGTP_TIME_STAGES).
 struct EventSet {
     hipEvent_t ev[kMaxStages + 1];
@@ -29,8 +30,8 @@ struct cgtp_plan_s {
     size_t own_ws_bytes;
     std::vector<EventSet> timers;  // reused across calls; timers_used are pending
     size_t timers_used;
-    double stage_acc[3][kMaxStages];  // drained sums per op (onsite, message pass, two-slot)
-    int stage_calls[3];
+    double stage_acc[kNumOps][kMaxStages];  // drained sums per op (CGTP_OP_*)
+    int stage_calls[kNumOps];
 };
 
 namespace {
@@ -73,24 +74,25 @@ struct Layout {
 
 // Receiver on MFMA: fp32, zonal edge field, R a multiple of 16, lmax high enough that the
 // per-thread recurrence sums would make the SIMT receiver compute-bound.
-bool use_mfma_receiver(const cgtp_plan_s *p)
+bool use_mfma_receiver(const cgtp_plan_s *p, int R)
 {
     return p->dtype == CGTP_F32 && !(p->flags & CGTP_EDGE_SEPARATED) &&
-           p->d.lmax >= cgtp::kMfmaRecvMinL && cgtp::receiver_mfma_supported(p->d, p->R);
+           p->d.lmax >= cgtp::kMfmaRecvMinL && cgtp::receiver_mfma_supported(p->d, R);
 }
 
 // The MFMA receiver reads the sender fields in 64-point chunks when the MFMA sender writes
 // them (fp32, default grid).
-bool sf_chunked(const cgtp_plan_s *p)
+bool sf_chunked(const cgtp_plan_s *p, int R)
 {
-    return use_mfma_receiver(p) && cgtp::sender_mfma_supported(p->d);
+    return use_mfma_receiver(p, R) && cgtp::sender_mfma_supported(p->d);
 }
 
-// On-site workspace: HA, HB, Ta, Tb, each [N][R][K].
-Layout onsite_layout(const cgtp_plan_s *p, int64_t N)
+// On-site workspace: HA, HB, Ta, Tb, each [N][R][K] (R: the plan's rank, or the total
+// rank of the groups of the general path).
+Layout onsite_layout(const cgtp_plan_s *p, int R, int64_t N)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
-    size_t blk = align256(es * (size_t)N * p->R * p->d.K);
+    size_t blk = align256(es * (size_t)N * R * p->d.K);
     Layout l{};
     for (int i = 0; i < 4; ++i) l.off[i] = i * blk;
     l.total = 4 * blk;
@@ -100,15 +102,15 @@ Layout onsite_layout(const cgtp_plan_s *p, int64_t N)
 // Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],
 // and, for the MFMA receiver, the summed grid fields S [N][R][2][UVs]. With two node slots,
 // HI and SF hold the natural slot followed by the flipped one.
-Layout mp_layout(const cgtp_plan_s *p, int64_t N, int64_t E, bool two = false)
+Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = false)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
     const size_t slots = two ? 2 : 1;
-    size_t h = align256(es * (size_t)N * p->R * p->d.K);
-    const size_t sf_pts = sf_chunked(p) ? (size_t)cgtp::sf_chunks(p->d) * cgtp::kSfChunk : p->d.UVs;
-    size_t sf = align256(es * (size_t)N * p->R * 3 * sf_pts);
-    size_t rt = align256(es * (size_t)E * p->R * p->d.L);
-    size_t sg = use_mfma_receiver(p) ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, p->R)) : 0;
+    size_t h = align256(es * (size_t)N * R * p->d.K);
+    const size_t sf_pts = sf_chunked(p, R) ? (size_t)cgtp::sf_chunks(p->d) * cgtp::kSfChunk : p->d.UVs;
+    size_t sf = align256(es * (size_t)N * R * 3 * sf_pts);
+    size_t rt = align256(es * (size_t)E * R * p->d.L);
+    size_t sg = use_mfma_receiver(p, R) ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, R)) : 0;
     Layout l{};
     l.off[0] = 0;
     l.off[1] = slots * h;
@@ -230,33 +232,51 @@ struct StageRec {
     }
 };
 
+// Eq. struct-phi / cat-alpha-phi / cat-beta-phi: out[n][k] (+)= sum_r Uout[l][n][r] T[r][k]
+// over R ranks of T, whose rows are x_sb elements apart.
 template <typename T>
-int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const void *UA,
+hipError_t project(int64_t N, int C, int R, int K, const void *Uout, const T *Tsrc, int64_t x_sb,
+                   void *out, bool accumulate, hipStream_t s)
+{
+    return cgtp::launch_contract<T>(N, R, C, K, false, (const T *)Uout, (int64_t)C * R, 1, R, Tsrc,
+                                    x_sb, (T *)out, (int64_t)C * K, K, 1, nullptr, accumulate, s);
+}
+
+// Eq. struct-H / msgpass-HI: H[b][r][k] = sum_n U[l][n][r] X[b][n][k] into rows of H that are
+// h_sb elements apart.
+template <typename T>
+hipError_t contract_in(int64_t N, int C, int R, int K, const void *U, const void *X, T *H,
+                       int64_t h_sb, hipStream_t s)
+{
+    return cgtp::launch_contract<T>(N, C, R, K, false, (const T *)U, (int64_t)C * R, R, 1,
+                                    (const T *)X, (int64_t)C * K, H, h_sb, K, 1, nullptr, false, s);
+}
+
+template <typename T>
+int run_onsite(cgtp_plan_s *p, int op, int64_t N, const void *A, const void *B, const void *UA,
                const void *UB, const void *Uoe, const void *Uoo, void *oe, void *oo, char *ws,
                hipStream_t s)
 {
     const cgtp::Dims &d = p->d;
     const int C = p->C, R = p->R;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
-    Layout lay = onsite_layout(p, N);
+    Layout lay = onsite_layout(p, R, N);
     T *HA = reinterpret_cast<T *>(ws + lay.off[0]);
     T *HB = reinterpret_cast<T *>(ws + lay.off[1]);
     T *Ta = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[3]);
-    const int64_t sl = (int64_t)C * R;
+    const int64_t hs = (int64_t)R * d.K;
     StageRec rec;
-    int st = rec.begin(p, CGTP_OP_ONSITE, 5, s);
+    int st = rec.begin(p, op, 5, s);
     if (st) return st;
     hipError_t e;
     // Eq. struct-H for both operands (shared when the operands coincide)
-    e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UA, sl, R, 1, (const T *)A, HA,
-                                 (int64_t)R * d.K, d.K, 1, nullptr, s);
+    e = contract_in<T>(N, C, R, d.K, UA, A, HA, hs, s);
     if (e != hipSuccess) return hip_fail(e, "contract A");
     rec.mark();
     const T *HBp = HA;
     if (!(A == B && UA == UB)) {
-        e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UB, sl, R, 1, (const T *)B,
-                                     HB, (int64_t)R * d.K, d.K, 1, nullptr, s);
+        e = contract_in<T>(N, C, R, d.K, UB, B, HB, hs, s);
         if (e != hipSuccess) return hip_fail(e, "contract B");
         HBp = HB;
     }
@@ -264,16 +284,13 @@ int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const vo
     e = cgtp::launch_onsite_grid<T>(tb, N, R, HA, HBp, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "onsite grid");
     rec.mark();
-    // Eq. struct-phi: out[b][n][k] = sum_r Uout[l][n][r] T[b][r][k]
     if (oe) {
-        e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoe, sl, 1, R, Ta, (T *)oe,
-                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
+        e = project<T>(N, C, R, d.K, Uoe, Ta, hs, oe, false, s);
         if (e != hipSuccess) return hip_fail(e, "project even");
     }
     rec.mark();
     if (oo) {
-        e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoo, sl, 1, R, Tb, (T *)oo,
-                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
+        e = project<T>(N, C, R, d.K, Uoo, Tb, hs, oo, false, s);
         if (e != hipSuccess) return hip_fail(e, "project odd");
     }
     rec.mark();
@@ -281,17 +298,17 @@ int run_onsite(cgtp_plan_s *p, int64_t N, const void *A, const void *B, const vo
 }
 
 template <typename T>
-int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const int32_t *col,
-           const void *unit, const void *rad, const void *I, const void *If, const void *UE,
-           const void *UI, const void *Uoe, const void *Uoo, void *oe, void *oo, char *ws,
-           hipStream_t s)
+int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
+           const int32_t *col, const void *unit, const void *rad, const void *I, const void *If,
+           const void *UE, const void *UI, const void *Uoe, const void *Uoo, void *oe, void *oo,
+           char *ws, hipStream_t s)
 {
     const cgtp::Dims &d = p->d;
     const int C = p->C, R = p->R;
     const bool separated = (p->flags & CGTP_EDGE_SEPARATED) != 0;
     const bool two = If != nullptr;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
-    Layout lay = mp_layout(p, N, E, two);
+    Layout lay = mp_layout(p, R, N, E, two);
     T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
     T *SF = reinterpret_cast<T *>(ws + lay.off[1]);
     T *Rt = reinterpret_cast<T *>(ws + lay.off[2]);
@@ -299,24 +316,22 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
     T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
     T *HIf = two ? reinterpret_cast<T *>(ws + lay.off[0] + lay.hf) : nullptr;
     T *SFf = two ? reinterpret_cast<T *>(ws + lay.off[1] + lay.sff) : nullptr;
-    const int64_t sl = (int64_t)C * R;
+    const int64_t hs = (int64_t)R * d.K;
     StageRec rec;
-    int st = rec.begin(p, two ? CGTP_OP_MESSAGE_PASS_TWO_SLOT : CGTP_OP_MESSAGE_PASS, 6, s);
+    int st = rec.begin(p, op, 6, s);
     if (st) return st;
     hipError_t e;
     // Eq. msgpass-HI, then the node-side forward transforms (Eqs. msgpass-FI, msgpass-AI),
     // for each node slot
     for (int slot = 0; slot < (two ? 2 : 1); ++slot) {
-        e = cgtp::launch_contract<T>(N, C, R, d.K, false, (const T *)UI, sl, R, 1,
-                                     (const T *)(slot ? If : I), slot ? HIf : HI,
-                                     (int64_t)R * d.K, d.K, 1, nullptr, s);
+        e = contract_in<T>(N, C, R, d.K, UI, slot ? If : I, slot ? HIf : HI, hs, s);
         if (e != hipSuccess) return hip_fail(e, "contract node features");
     }
     rec.mark();
     for (int slot = 0; slot < (two ? 2 : 1); ++slot) {
         T *h = slot ? HIf : HI, *sf = slot ? SFf : SF;
         if constexpr (sizeof(T) == 4) {
-            if (sf_chunked(p))
+            if (sf_chunked(p, R))
                 e = cgtp::launch_sender_mfma(tb, N, R, h, sf, true, s);
             else
                 e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s);
@@ -328,15 +343,16 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
     rec.mark();
     // Eq. msgpass-tildeR into Rt [E][L][R] (the zonal form folds in the addition-theorem
     // weight (2l+1)/(4 pi))
-    e = cgtp::launch_contract<T>(E, C, R, d.L, true, (const T *)UE, sl, R, 1, (const T *)rad, Rt,
-                                 (int64_t)d.L * R, 1, R, separated ? nullptr : tb.cl, s);
+    e = cgtp::launch_contract<T>(E, C, R, d.L, true, (const T *)UE, (int64_t)C * R, R, 1,
+                                 (const T *)rad, (int64_t)C * d.L, Rt, (int64_t)d.L * R, 1, R,
+                                 separated ? nullptr : tb.cl, false, s);
     if (e != hipSuccess) return hip_fail(e, "contract edge radial");
     rec.mark();
     if constexpr (sizeof(T) == 4) {
-        if (use_mfma_receiver(p)) {
+        if (use_mfma_receiver(p, R)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
             e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt, SF,
-                                           SFf, sf_chunked(p), Sg, Ta, Tb, s);
+                                           SFf, sf_chunked(p, R), Sg, Ta, Tb, s);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
             goto projections;
@@ -348,18 +364,272 @@ int run_mp(cgtp_plan_s *p, int64_t N, int64_t E, const int32_t *row_ptr, const i
     rec.mark();
 projections:
     if (oe) {
-        e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoe, sl, 1, R, Ta, (T *)oe,
-                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
+        e = project<T>(N, C, R, d.K, Uoe, Ta, hs, oe, false, s);
         if (e != hipSuccess) return hip_fail(e, "project even");
     }
     rec.mark();
     if (oo) {
-        e = cgtp::launch_contract<T>(N, R, C, d.K, false, (const T *)Uoo, sl, 1, R, Tb, (T *)oo,
-                                     (int64_t)C * d.K, d.K, 1, nullptr, s);
+        e = project<T>(N, C, R, d.K, Uoo, Tb, hs, oo, false, s);
         if (e != hipSuccess) return hip_fail(e, "project odd");
     }
     rec.mark();
     return CGTP_OK;
+}
+
+// ---------------------------------------------------------------------------------------
+// General parameterization (Eqs. msgpass-cp-alpha, msgpass-cp-beta; Table 1): every
+// coupling category (0 Gaunt, 1 curl) and output sector (0 out_even, 1 out_odd) may carry
+// its own input factors and output weights: block b = 2 category + sector. Operands may
+// carry a parity-flipped slot. A slot pair of relative parity rel (0 equal, 1 mixed)
+// sends its Gaunt coupling to sector rel and its curl coupling to sector 1 - rel.
+//
+// The general call is lowered onto the fused kernels by stacking rank groups: group g
+// holds the ranks [g R, (g+1) R) of one slot pair contracted with one factor block, so
+// one launch of the grid stage at rank G R computes every group's Gaunt product (into
+// Ta) and curl (into Tb). Each block then projects the groups that feed it, through Ta
+// for a Gaunt block and Tb for a curl block, accumulating into its sector's output.
+// With shared input factors a group feeds one Gaunt and one curl block and nothing is
+// discarded; with per-block factors a group feeds one block and its other product is
+// not used.
+
+constexpr int kMaxGroups = 8;
+
+struct Group {
+    int s1, s2;  // slots of the first and second operand (0 natural, 1 flipped)
+    int blk;     // factor block, or -1 when every block shares the factors
+};
+
+struct Groups {
+    int n = 0;
+    Group g[kMaxGroups];
+    int lo[4] = {0, 0, 0, 0}, hi[4] = {0, 0, 0, 0};  // groups [lo, hi) feed block b
+};
+
+int block_of(int cat, int rel) { return 2 * cat + (cat ? 1 - rel : rel); }
+
+// f1 / f2: the first / second operand has a flipped slot (message passing: f1 = false, the
+// edge field); in_blocks: 1 (shared factors), 2 (per category) or 4 (per block).
+Groups make_groups(bool f1, bool f2, int in_blocks)
+{
+    Groups G;
+    auto present = [&](int s1, int s2) { return (s1 == 0 || f1) && (s2 == 0 || f2); };
+    if (in_blocks == 1) {
+        const int pairs[4][2] = {{0, 0}, {1, 1}, {0, 1}, {1, 0}};
+        for (const auto &pr : pairs)
+            if (present(pr[0], pr[1])) G.g[G.n++] = Group{pr[0], pr[1], -1};
+    } else {
+        for (int b = 0; b < 4; ++b) {
+            const int cat = b >> 1, sec = b & 1, rel = cat ? 1 - sec : sec;
+            const int pairs[2][2] = {{0, rel}, {1, 1 - rel}};
+            for (const auto &pr : pairs)
+                if (present(pr[0], pr[1])) G.g[G.n++] = Group{pr[0], pr[1], b};
+        }
+    }
+    // each block's groups are consecutive by construction
+    for (int b = 0; b < 4; ++b) {
+        int lo = -1, hi = -1;
+        for (int i = 0; i < G.n; ++i) {
+            const Group &g = G.g[i];
+            const bool feeds = block_of(b >> 1, g.s1 != g.s2) == b && (g.blk < 0 || g.blk == b);
+            if (!feeds) continue;
+            if (lo < 0) lo = i;
+            hi = i + 1;
+        }
+        G.lo[b] = lo < 0 ? 0 : lo;
+        G.hi[b] = hi < 0 ? 0 : hi;
+    }
+    return G;
+}
+
+// Factor pointers of the general entry points, resolved per block.
+struct Factors {
+    const void *in1[4], *in2[4];  // input factors of the first / second operand per block
+    const void *out[4];           // output weights per block
+};
+
+Factors resolve_factors(const cgtp_plan_s *p, int in_blocks, const void *U1, const void *U2,
+                        int out_blocks, const void *Uoe, const void *Uoo)
+{
+    const size_t es = p->dtype == CGTP_F64 ? 8 : 4;
+    const size_t blk = es * (size_t)p->d.L * p->C * p->R;
+    Factors f{};
+    for (int b = 0; b < 4; ++b) {
+        const int cat = b >> 1, sec = b & 1;
+        const int ib = in_blocks == 1 ? 0 : (in_blocks == 2 ? cat : b);
+        f.in1[b] = static_cast<const char *>(U1) + ib * blk;
+        f.in2[b] = static_cast<const char *>(U2) + ib * blk;
+        const void *base = sec ? Uoo : Uoe;
+        f.out[b] = base ? static_cast<const char *>(base) + (out_blocks == 2 ? cat : 0) * blk
+                        : nullptr;
+    }
+    return f;
+}
+
+template <typename T>
+int project_blocks(const cgtp_plan_s *p, const Groups &G, int64_t N, const Factors &f,
+                   const T *Ta, const T *Tb, void *oe, void *oo, hipStream_t s, StageRec &rec)
+{
+    const int64_t rs = (int64_t)G.n * p->R * p->d.K;  // row stride of Ta / Tb
+    void *outs[2] = {oe, oo};
+    for (int sec = 0; sec < 2; ++sec) {
+        bool first = true;
+        for (int cat = 0; cat < 2 && outs[sec]; ++cat) {
+            const int b = 2 * cat + sec;
+            for (int gi = G.lo[b]; gi < G.hi[b]; ++gi) {
+                const T *src = (cat ? Tb : Ta) + (int64_t)gi * p->R * p->d.K;
+                hipError_t e = project<T>(N, p->C, p->R, p->d.K, f.out[b], src, rs, outs[sec],
+                                          !first, s);
+                if (e != hipSuccess) return hip_fail(e, sec ? "project odd" : "project even");
+                first = false;
+            }
+        }
+        rec.mark();
+    }
+    return CGTP_OK;
+}
+
+template <typename T>
+int run_onsite_groups(cgtp_plan_s *p, const Groups &G, int64_t N, const void *const X1[2],
+                      const void *const X2[2], const Factors &f, void *oe, void *oo, char *ws,
+                      hipStream_t s)
+{
+    const cgtp::Dims &d = p->d;
+    const int C = p->C, R = p->R, Rg = G.n * R;
+    cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
+    Layout lay = onsite_layout(p, Rg, N);
+    T *HA = reinterpret_cast<T *>(ws + lay.off[0]);
+    T *HB = reinterpret_cast<T *>(ws + lay.off[1]);
+    T *Ta = reinterpret_cast<T *>(ws + lay.off[2]);
+    T *Tb = reinterpret_cast<T *>(ws + lay.off[3]);
+    const int64_t hs = (int64_t)Rg * d.K;
+    StageRec rec;
+    int st = rec.begin(p, CGTP_OP_ONSITE_GENERAL, 5, s);
+    if (st) return st;
+    hipError_t e;
+    for (int gi = 0; gi < G.n; ++gi) {
+        const Group &g = G.g[gi];
+        e = contract_in<T>(N, C, R, d.K, f.in1[g.blk < 0 ? 0 : g.blk], X1[g.s1],
+                           HA + (int64_t)gi * R * d.K, hs, s);
+        if (e != hipSuccess) return hip_fail(e, "contract first operand");
+    }
+    rec.mark();
+    for (int gi = 0; gi < G.n; ++gi) {
+        const Group &g = G.g[gi];
+        e = contract_in<T>(N, C, R, d.K, f.in2[g.blk < 0 ? 0 : g.blk], X2[g.s2],
+                           HB + (int64_t)gi * R * d.K, hs, s);
+        if (e != hipSuccess) return hip_fail(e, "contract second operand");
+    }
+    rec.mark();
+    e = cgtp::launch_onsite_grid<T>(tb, N, Rg, HA, HB, Ta, Tb, s);
+    if (e != hipSuccess) return hip_fail(e, "onsite grid");
+    rec.mark();
+    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+}
+
+template <typename T>
+int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const int32_t *row_ptr,
+                  const int32_t *col, const void *unit, const void *rad, const void *const X2[2],
+                  const Factors &f, void *oe, void *oo, char *ws, hipStream_t s)
+{
+    const cgtp::Dims &d = p->d;
+    const int C = p->C, R = p->R, Rg = G.n * R;
+    const bool separated = (p->flags & CGTP_EDGE_SEPARATED) != 0;
+    cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
+    Layout lay = mp_layout(p, Rg, N, E);
+    T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
+    T *SF = reinterpret_cast<T *>(ws + lay.off[1]);
+    T *Rt = reinterpret_cast<T *>(ws + lay.off[2]);
+    T *Ta = reinterpret_cast<T *>(ws + lay.off[3]);
+    T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
+    StageRec rec;
+    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_GENERAL, 6, s);
+    if (st) return st;
+    hipError_t e;
+    for (int gi = 0; gi < G.n; ++gi) {
+        const Group &g = G.g[gi];
+        e = contract_in<T>(N, C, R, d.K, f.in2[g.blk < 0 ? 0 : g.blk], X2[g.s2],
+                           HI + (int64_t)gi * R * d.K, (int64_t)Rg * d.K, s);
+        if (e != hipSuccess) return hip_fail(e, "contract node features");
+    }
+    rec.mark();
+    if constexpr (sizeof(T) == 4) {
+        if (sf_chunked(p, Rg))
+            e = cgtp::launch_sender_mfma(tb, N, Rg, HI, SF, true, s);
+        else
+            e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s);
+    } else {
+        e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sender fields");
+    rec.mark();
+    for (int gi = 0; gi < G.n; ++gi) {
+        const Group &g = G.g[gi];
+        e = cgtp::launch_contract<T>(E, C, R, d.L, true, (const T *)f.in1[g.blk < 0 ? 0 : g.blk],
+                                     (int64_t)C * R, R, 1, (const T *)rad, (int64_t)C * d.L,
+                                     Rt + (int64_t)gi * R, (int64_t)d.L * Rg, 1, Rg,
+                                     separated ? nullptr : tb.cl, false, s);
+        if (e != hipSuccess) return hip_fail(e, "contract edge radial");
+    }
+    rec.mark();
+    e = hipSuccess;
+    if constexpr (sizeof(T) == 4) {
+        if (use_mfma_receiver(p, Rg)) {
+            float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
+            e = cgtp::launch_receiver_mfma(tb, N, Rg, row_ptr, col, (const float *)unit, Rt, SF,
+                                           nullptr, sf_chunked(p, Rg), Sg, Ta, Tb, s);
+            if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
+            rec.mark();
+            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+        }
+    }
+    e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, SF,
+                                 nullptr, Ta, Tb, s);
+    if (e != hipSuccess) return hip_fail(e, "receiver");
+    rec.mark();
+    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+}
+
+// How a general call runs: on the fused single-group kernels when the factors are shared
+// and each output sector reads one set of weights, else through rank groups.
+struct GeneralRoute {
+    bool fused;   // run_onsite / run_mp with the plan's rank
+    Groups G;     // otherwise: the rank groups
+    size_t ws;    // workspace bytes
+};
+
+GeneralRoute route_onsite(const cgtp_plan_s *p, int64_t N, bool f1, bool f2, int in_blocks)
+{
+    GeneralRoute r{};
+    r.fused = in_blocks == 1 && !f1 && !f2;
+    if (r.fused) {
+        r.ws = onsite_layout(p, p->R, N).total;
+    } else {
+        r.G = make_groups(f1, f2, in_blocks);
+        r.ws = onsite_layout(p, r.G.n * p->R, N).total;
+    }
+    return r;
+}
+
+GeneralRoute route_mp(const cgtp_plan_s *p, int64_t N, int64_t E, bool flip, int in_blocks,
+                      int out_blocks)
+{
+    GeneralRoute r{};
+    // one slot: each sector holds one coupling, so per-category weights change nothing
+    r.fused = in_blocks == 1 && (!flip || out_blocks == 1) &&
+              !(flip && (p->flags & CGTP_EDGE_SEPARATED));
+    if (r.fused) {
+        r.ws = mp_layout(p, p->R, N, E, flip).total;
+    } else {
+        r.G = make_groups(false, flip, in_blocks);
+        r.ws = mp_layout(p, r.G.n * p->R, N, E).total;
+    }
+    return r;
+}
+
+bool valid_blocks(int in_blocks, int out_blocks)
+{
+    return (in_blocks == 1 || in_blocks == 2 || in_blocks == 4) &&
+           (out_blocks == 1 || out_blocks == 2);
 }
 
 int validate_csr(int64_t N, int64_t E, const int32_t *row_ptr, const int32_t *col, hipStream_t s)
@@ -466,11 +736,11 @@ int cgtp_workspace_bytes(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edge
 {
     if (!plan || !bytes) return fail(CGTP_ERR_ARG, "NULL argument");
     if (n_nodes < 0 || n_edges < 0) return fail(CGTP_ERR_ARG, "negative size");
-    if (op == CGTP_OP_ONSITE) *bytes = onsite_layout(plan, n_nodes).total;
-    else if (op == CGTP_OP_MESSAGE_PASS) *bytes = mp_layout(plan, n_nodes, n_edges).total;
+    if (op == CGTP_OP_ONSITE) *bytes = onsite_layout(plan, plan->R, n_nodes).total;
+    else if (op == CGTP_OP_MESSAGE_PASS) *bytes = mp_layout(plan, plan->R, n_nodes, n_edges).total;
     else if (op == CGTP_OP_MESSAGE_PASS_TWO_SLOT)
-        *bytes = mp_layout(plan, n_nodes, n_edges, true).total;
-    else return fail(CGTP_ERR_ARG, "unknown op %d", op);
+        *bytes = mp_layout(plan, plan->R, n_nodes, n_edges, true).total;
+    else return fail(CGTP_ERR_ARG, "unknown op %d (general ops: cgtp_workspace_bytes_general)", op);
     return CGTP_OK;
 }
 
@@ -491,14 +761,14 @@ int cgtp_onsite(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B, c
     int st = check_device(plan);
     if (st) return st;
     void *ws = nullptr;
-    st = get_workspace(plan, onsite_layout(plan, n_nodes).total, workspace, ws_bytes, &ws);
+    st = get_workspace(plan, onsite_layout(plan, plan->R, n_nodes).total, workspace, ws_bytes, &ws);
     if (st) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (plan->dtype == CGTP_F64)
-        return run_onsite<double>(plan, n_nodes, A, B, U_A, U_B, U_out_even, U_out_odd, out_even,
-                                  out_odd, static_cast<char *>(ws), s);
-    return run_onsite<float>(plan, n_nodes, A, B, U_A, U_B, U_out_even, U_out_odd, out_even,
-                             out_odd, static_cast<char *>(ws), s);
+        return run_onsite<double>(plan, CGTP_OP_ONSITE, n_nodes, A, B, U_A, U_B, U_out_even,
+                                  U_out_odd, out_even, out_odd, static_cast<char *>(ws), s);
+    return run_onsite<float>(plan, CGTP_OP_ONSITE, n_nodes, A, B, U_A, U_B, U_out_even, U_out_odd,
+                             out_even, out_odd, static_cast<char *>(ws), s);
 }
 
 namespace {
@@ -539,15 +809,16 @@ int message_pass_impl(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
         if (st) return st;
     }
     void *ws = nullptr;
-    st = get_workspace(plan, mp_layout(plan, n_nodes, n_edges, two).total, workspace, ws_bytes,
-                       &ws);
+    st = get_workspace(plan, mp_layout(plan, plan->R, n_nodes, n_edges, two).total, workspace,
+                       ws_bytes, &ws);
     if (st) return st;
+    const int op = two ? CGTP_OP_MESSAGE_PASS_TWO_SLOT : CGTP_OP_MESSAGE_PASS;
     if (plan->dtype == CGTP_F64)
-        return run_mp<double>(plan, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial,
+        return run_mp<double>(plan, op, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial,
                               node_feat, node_flip, U_E, U_I, U_out_even, U_out_odd, out_even,
                               out_odd, static_cast<char *>(ws), s);
-    return run_mp<float>(plan, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial, node_feat,
-                         node_flip, U_E, U_I, U_out_even, U_out_odd, out_even, out_odd,
+    return run_mp<float>(plan, op, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial,
+                         node_feat, node_flip, U_E, U_I, U_out_even, U_out_odd, out_even, out_odd,
                          static_cast<char *>(ws), s);
 }
 
@@ -580,6 +851,121 @@ int cgtp_message_pass_two_slot(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                              out_odd, workspace, ws_bytes, stream);
 }
 
+int cgtp_workspace_bytes_general(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edges,
+                                 int flips, int in_blocks, int out_blocks, size_t *bytes)
+{
+    if (!plan || !bytes) return fail(CGTP_ERR_ARG, "NULL argument");
+    if (n_nodes < 0 || n_edges < 0) return fail(CGTP_ERR_ARG, "negative size");
+    if (!valid_blocks(in_blocks, out_blocks) || (flips & ~3))
+        return fail(CGTP_ERR_ARG, "in_blocks %d / out_blocks %d / flips %d invalid", in_blocks,
+                    out_blocks, flips);
+    if (op == CGTP_OP_ONSITE_GENERAL)
+        *bytes = route_onsite(plan, n_nodes, flips & 1, flips & 2, in_blocks).ws;
+    else if (op == CGTP_OP_MESSAGE_PASS_GENERAL)
+        *bytes = route_mp(plan, n_nodes, n_edges, flips & 2, in_blocks, out_blocks).ws;
+    else return fail(CGTP_ERR_ARG, "unknown general op %d", op);
+    return CGTP_OK;
+}
+
+int cgtp_onsite_general(cgtp_plan plan, int64_t n_nodes, const void *A, const void *A_flip,
+                        const void *B, const void *B_flip, int in_blocks, const void *U_A,
+                        const void *U_B, int out_blocks, const void *U_out_even,
+                        const void *U_out_odd, void *out_even, void *out_odd, void *workspace,
+                        size_t ws_bytes, void *stream)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
+    if (n_nodes < 0) return fail(CGTP_ERR_ARG, "n_nodes < 0");
+    if (!valid_blocks(in_blocks, out_blocks))
+        return fail(CGTP_ERR_ARG, "in_blocks %d / out_blocks %d invalid", in_blocks, out_blocks);
+    if (n_nodes == 0) return CGTP_OK;
+    if (!out_even && !out_odd) return fail(CGTP_ERR_ARG, "both outputs are NULL");
+    if (!A || !B || !U_A || !U_B) return fail(CGTP_ERR_ARG, "NULL input");
+    if ((out_even && !U_out_even) || (out_odd && !U_out_odd))
+        return fail(CGTP_ERR_ARG, "NULL output projection");
+    GeneralRoute r = route_onsite(plan, n_nodes, A_flip != nullptr, B_flip != nullptr, in_blocks);
+    const int Rg = r.fused ? plan->R : r.G.n * plan->R;
+    if (n_nodes * (int64_t)Rg > 0x7fffffffLL)
+        return fail(CGTP_ERR_UNSUPPORTED, "n_nodes * total rank exceeds 2^31 - 1");
+    int st = check_device(plan);
+    if (st) return st;
+    void *ws = nullptr;
+    st = get_workspace(plan, r.ws, workspace, ws_bytes, &ws);
+    if (st) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    Factors f = resolve_factors(plan, in_blocks, U_A, U_B, out_blocks, U_out_even, U_out_odd);
+    char *w = static_cast<char *>(ws);
+    if (r.fused) {  // one slot each: out_even holds block 0 (Gaunt), out_odd block 3 (curl)
+        if (plan->dtype == CGTP_F64)
+            return run_onsite<double>(plan, CGTP_OP_ONSITE_GENERAL, n_nodes, A, B, U_A, U_B,
+                                      f.out[0], f.out[3], out_even, out_odd, w, s);
+        return run_onsite<float>(plan, CGTP_OP_ONSITE_GENERAL, n_nodes, A, B, U_A, U_B, f.out[0],
+                                 f.out[3], out_even, out_odd, w, s);
+    }
+    const void *X1[2] = {A, A_flip}, *X2[2] = {B, B_flip};
+    if (plan->dtype == CGTP_F64)
+        return run_onsite_groups<double>(plan, r.G, n_nodes, X1, X2, f, out_even, out_odd, w, s);
+    return run_onsite_groups<float>(plan, r.G, n_nodes, X1, X2, f, out_even, out_odd, w, s);
+}
+
+int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
+                              const int32_t *row_ptr, const int32_t *col, const void *edge_unit,
+                              const void *edge_radial, const void *node_feat,
+                              const void *node_flip, int in_blocks, const void *U_E,
+                              const void *U_I, int out_blocks, const void *U_out_even,
+                              const void *U_out_odd, void *out_even, void *out_odd,
+                              void *workspace, size_t ws_bytes, void *stream)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
+    if (n_nodes < 0 || n_edges < 0) return fail(CGTP_ERR_ARG, "negative size");
+    if (n_edges >= 0x7fffffffLL) return fail(CGTP_ERR_ARG, "n_edges must be below 2^31 - 1");
+    if (!valid_blocks(in_blocks, out_blocks))
+        return fail(CGTP_ERR_ARG, "in_blocks %d / out_blocks %d invalid", in_blocks, out_blocks);
+    if (n_nodes == 0) {
+        if (n_edges != 0) return fail(CGTP_ERR_ARG, "edges without nodes");
+        return CGTP_OK;
+    }
+    if (!out_even && !out_odd) return fail(CGTP_ERR_ARG, "both outputs are NULL");
+    if (!row_ptr || !node_feat || !U_E || !U_I) return fail(CGTP_ERR_ARG, "NULL input");
+    if (n_edges > 0 && (!col || !edge_unit || !edge_radial))
+        return fail(CGTP_ERR_ARG, "NULL edge input");
+    if ((out_even && !U_out_even) || (out_odd && !U_out_odd))
+        return fail(CGTP_ERR_ARG, "NULL output projection");
+    const bool flip = node_flip != nullptr;
+    GeneralRoute r = route_mp(plan, n_nodes, n_edges, flip, in_blocks, out_blocks);
+    const int Rg = r.fused ? plan->R : r.G.n * plan->R;
+    if (n_nodes * (int64_t)Rg > 0x7fffffffLL)
+        return fail(CGTP_ERR_UNSUPPORTED, "n_nodes * total rank exceeds 2^31 - 1");
+    int st = check_device(plan);
+    if (st) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (plan->flags & CGTP_VALIDATE_CSR) {
+        st = validate_csr(n_nodes, n_edges, row_ptr, col, s);
+        if (st) return st;
+    }
+    void *ws = nullptr;
+    st = get_workspace(plan, r.ws, workspace, ws_bytes, &ws);
+    if (st) return st;
+    Factors f = resolve_factors(plan, in_blocks, U_E, U_I, out_blocks, U_out_even, U_out_odd);
+    char *w = static_cast<char *>(ws);
+    if (r.fused) {  // out_even: blocks 0 (+ 2), out_odd: blocks 3 (+ 1), one weight set each
+        if (plan->dtype == CGTP_F64)
+            return run_mp<double>(plan, CGTP_OP_MESSAGE_PASS_GENERAL, n_nodes, n_edges, row_ptr,
+                                  col, edge_unit, edge_radial, node_feat, node_flip, U_E, U_I,
+                                  f.out[0], f.out[3], out_even, out_odd, w, s);
+        return run_mp<float>(plan, CGTP_OP_MESSAGE_PASS_GENERAL, n_nodes, n_edges, row_ptr, col,
+                             edge_unit, edge_radial, node_feat, node_flip, U_E, U_I, f.out[0],
+                             f.out[3], out_even, out_odd, w, s);
+    }
+    const void *X2[2] = {node_feat, node_flip};
+    if (plan->dtype == CGTP_F64)
+        return run_mp_groups<double>(plan, r.G, n_nodes, n_edges, row_ptr, col, edge_unit,
+                                     edge_radial, X2, f, out_even, out_odd, w, s);
+    return run_mp_groups<float>(plan, r.G, n_nodes, n_edges, row_ptr, col, edge_unit, edge_radial,
+                                X2, f, out_even, out_odd, w, s);
+}
+
 int cgtp_destroy(cgtp_plan plan)
 {
     if (!plan) return CGTP_OK;
@@ -599,8 +985,10 @@ int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages,
     if (!(plan->flags & CGTP_TIME_STAGES))
         return fail(CGTP_ERR_ARG, "plan was created without CGTP_TIME_STAGES");
     int ns;
-    if (op == CGTP_OP_ONSITE) ns = 5;
-    else if (op == CGTP_OP_MESSAGE_PASS || op == CGTP_OP_MESSAGE_PASS_TWO_SLOT) ns = 6;
+    if (op == CGTP_OP_ONSITE || op == CGTP_OP_ONSITE_GENERAL) ns = 5;
+    else if (op == CGTP_OP_MESSAGE_PASS || op == CGTP_OP_MESSAGE_PASS_TWO_SLOT ||
+             op == CGTP_OP_MESSAGE_PASS_GENERAL)
+        ns = 6;
     else return fail(CGTP_ERR_ARG, "unknown op %d", op);
     int status = drain_timers(plan);
     for (int k = 0; k < ns && k < cap; ++k) ms[k] = plan->stage_acc[op][k];

@@ -17,6 +17,10 @@ performance"; no public dataset is involved):
   ``edge_unit`` = (r_j - r_i)/|r_j - r_i|. Radial features
   R_{n l}(r) = sum_k W[l][n][k] g_k(r) with 8 Gaussians
   g_k(r) = exp(-(r - k r_cut/7)^2 / (2 (r_cut/7)^2)), W ~ N(0, 1/8).
+* General parameterization: parity-flipped slots N(0, 1) like the natural ones; input
+  factors stacked [n_blocks][L][C][R] and output weights [2][L][C][R] (Gaunt, curl), each
+  block N(0, 1/C), drawn from a second generator seeded seed + 7919 so the graph and the
+  natural slots are those of the plain workload of the same seed.
 """
 from __future__ import annotations
 
@@ -120,6 +124,47 @@ def mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, density: float
     return out
 
 
+def _stacked(rng, n_blocks: int, lmax: int, C: int, R: int) -> np.ndarray:
+    if n_blocks == 1:
+        return cp_factors(rng, lmax, C, R)
+    return np.stack([cp_factors(rng, lmax, C, R) for _ in range(n_blocks)])
+
+
+def _general_factors(rng, names, lmax, C, R, in_blocks, out_blocks):
+    out = {nm: _stacked(rng, in_blocks, lmax, C, R) for nm in names}
+    for nm in ("U_out_even", "U_out_odd"):
+        out[nm] = _stacked(rng, out_blocks, lmax, C, R)
+    return out
+
+
+def general_onsite_inputs(n: int, lmax: int, C: int, R: int, seed: int, flip1: bool = True,
+                          flip2: bool = True, in_blocks: int = 4, out_blocks: int = 2,
+                          per_degree: bool = False):
+    """On-site operands with optional parity-flipped slots and stacked factor blocks.
+    Draw order (second generator): A_flip, B_flip (each if present), U_A, U_B, U_out_even,
+    U_out_odd."""
+    d = onsite_inputs(n, lmax, C, R, seed, per_degree=per_degree)
+    rng = np.random.default_rng(seed + 7919)
+    d["A_flip"] = coefficients(rng, n, C, lmax, per_degree) if flip1 else None
+    d["B_flip"] = coefficients(rng, n, C, lmax, per_degree) if flip2 else None
+    d.update(_general_factors(rng, ("U_A", "U_B"), lmax, C, R, in_blocks, out_blocks))
+    return d
+
+
+def general_mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, flip: bool = True,
+                      in_blocks: int = 4, out_blocks: int = 2, density: float = 0.1,
+                      r_cut: float = 5.0):
+    """Message passing with an optional flipped node slot and stacked factor blocks (the
+    graph, radial features and node slots of mp_inputs with the same seed). Draw order
+    (second generator): U_E, U_I, U_out_even, U_out_odd."""
+    d = mp_inputs(n_atoms, lmax, C, R, seed, density=density, r_cut=r_cut, two_slot=flip)
+    if not flip:
+        d["node_flip"] = None
+    rng = np.random.default_rng(seed + 7919)
+    d.update(_general_factors(rng, ("U_E", "U_I"), lmax, C, R, in_blocks, out_blocks))
+    return d
+
+
 @dataclass(frozen=True)
 class Workload:
     name: str
@@ -133,8 +178,25 @@ class Workload:
     self_coupled: bool = False
     r_cut: float = 5.0
     two_slot: bool = False   # message passing with both node parity slots (Cases A-D)
+    # general parameterization (0: the plain calls): input factor blocks 1, 2 or 4 ...
+    in_blocks: int = 0
+    out_blocks: int = 1      # ... output weight blocks per sector (1 or 2)
+    flip1: bool = False      # first on-site operand carries a flipped slot
+
+    @property
+    def general(self) -> bool:
+        return self.in_blocks > 0
 
     def make(self, **kw):
+        if self.general and self.kind == "onsite":
+            return general_onsite_inputs(self.n, self.lmax, self.C, self.R, self.seed,
+                                         flip1=self.flip1, flip2=self.two_slot,
+                                         in_blocks=self.in_blocks, out_blocks=self.out_blocks,
+                                         per_degree=self.per_degree, **kw)
+        if self.general:
+            return general_mp_inputs(self.n, self.lmax, self.C, self.R, self.seed,
+                                     flip=self.two_slot, in_blocks=self.in_blocks,
+                                     out_blocks=self.out_blocks, r_cut=self.r_cut, **kw)
         if self.kind == "onsite":
             return onsite_inputs(self.n, self.lmax, self.C, self.R, self.seed,
                                  per_degree=self.per_degree, self_coupled=self.self_coupled, **kw)
@@ -155,4 +217,11 @@ WORKLOADS = {
     "mp2_10k_l6_c128": Workload("mp2_10k_l6_c128", "mp", 10000, 6, 128, 128, seed=2,
                                 two_slot=True),
     "mp2_5k_l20_c64": Workload("mp2_5k_l20_c64", "mp", 5000, 20, 64, 64, seed=4, two_slot=True),
+    # the general parameterization: both parity slots, input factors and output weights per
+    # (category, sector) block (Eqs. msgpass-cp-alpha, msgpass-cp-beta)
+    "mpg_10k_l6_c128": Workload("mpg_10k_l6_c128", "mp", 10000, 6, 128, 128, seed=2,
+                                two_slot=True, in_blocks=4, out_blocks=2),
+    "onsiteg_n4096_l12_c128": Workload("onsiteg_n4096_l12_c128", "onsite", 4096, 12, 128, 128,
+                                       seed=3, per_degree=True, two_slot=True, flip1=True,
+                                       in_blocks=4, out_blocks=2),
 }
