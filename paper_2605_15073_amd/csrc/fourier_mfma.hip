@@ -203,7 +203,7 @@ __device__ __forceinline__ void legendre_all(const LaneRows<LM, NOP> &c,
 template <int LM>
 __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int rb, int nc,
                                                      const float *__restrict__ H,
-                                                     float *__restrict__ SF)
+                                                     float *__restrict__ SF, int planes)
 {
     using G = Grid<LM>;
     extern __shared__ float smem[];
@@ -265,9 +265,9 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
 #pragma unroll
                     for (int t = 0; t < G::VT; ++t) {
                         if (t * 16 + n < G::V) {
-                            o[t * 16] = acc[0][t][j];
-                            o[G::UVs + t * 16] = acc[1][t][j];
-                            o[2 * G::UVs + t * 16] = acc[2][t][j];
+                            if (planes & 1) o[t * 16] = acc[0][t][j];
+                            if (planes & 2) o[G::UVs + t * 16] = acc[1][t][j];
+                            if (planes & 4) o[2 * G::UVs + t * 16] = acc[2][t][j];
                         }
                     }
                 } else {  // SF [R/16][nc][B][16][3][64]
@@ -280,9 +280,9 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
                             const int c = p / kSfChunk, pp = p - c * kSfChunk;
                             float *o = SF + ((((int64_t)(r >> 4) * nc + c) * nb + b) * 16 + (r & 15)) *
                                                 3 * kSfChunk + pp;
-                            o[0] = acc[0][t][j];
-                            o[kSfChunk] = acc[1][t][j];
-                            o[2 * kSfChunk] = acc[2][t][j];
+                            if (planes & 1) o[0] = acc[0][t][j];
+                            if (planes & 2) o[kSfChunk] = acc[1][t][j];
+                            if (planes & 4) o[2 * kSfChunk] = acc[2][t][j];
                         }
                     }
                 }
@@ -551,7 +551,7 @@ hipError_t onsite_lm(const Tabs<float> &tb, int64_t B, int R, const float *HA, c
 
 template <int LM>
 hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
-                     bool chunked, hipStream_t s)
+                     bool chunked, hipStream_t s, int planes)
 {
     using G = Grid<LM>;
     const size_t fixed = 4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB;
@@ -562,7 +562,8 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
     if (chunked && R % 16 != 0) return hipErrorInvalidValue;
     const int nc = chunked ? sf_chunks(tb.d) : 0;
     hipLaunchKernelGGL((k_sender_mfma<LM>), dim3((unsigned)blocks), dim3(64 * waves_for(rb * G::U)),
-                       sizeof(float) * (fixed + rb * (size_t)G::HR), s, tb, R, rb, nc, H, SF);
+                       sizeof(float) * (fixed + rb * (size_t)G::HR), s, tb, R, rb, nc, H, SF,
+                       planes);
     return hipGetLastError();
 }
 
@@ -598,13 +599,13 @@ bool default_grid(const Dims &d)
 bool sender_mfma_supported(const Dims &d) { return default_grid(d) && d.lmax <= 24; }
 
 hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
-                              bool chunked, hipStream_t s)
+                              bool chunked, hipStream_t s, int planes)
 {
     if (B == 0) return hipSuccess;
     if (!sender_mfma_supported(tb.d)) return hipErrorNotSupported;
     switch (tb.d.lmax) {
 #define CGTP_CASE(LMV) \
-    case LMV: return sender_lm<LMV>(tb, B, R, H, SF, chunked, s);
+    case LMV: return sender_lm<LMV>(tb, B, R, H, SF, chunked, s, planes);
         CGTP_LMAX_CASES(CGTP_CASE)
 #undef CGTP_CASE
     default: return hipErrorNotSupported;

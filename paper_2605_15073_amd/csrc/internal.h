@@ -87,10 +87,11 @@ hipError_t launch_contract<double>(int64_t, int, int, int, bool, const double *,
                                    int64_t, const double *, bool, hipStream_t);
 
 // Node-side synthesis of the three grid fields (A, dA/dx, dA/dphi) of H[b][r][K]:
-// SF[b][r][3][UVs] (Eqs. struct-F, struct-tildeA plus the derivative passes).
+// SF[b][r][3][UVs] (Eqs. struct-F, struct-tildeA plus the derivative passes). Only the
+// fields whose bit is set in planes (1: A, 2: dA/dx, 4: dA/dphi) are written.
 template <typename T>
 hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H, T *SF,
-                                hipStream_t s);
+                                hipStream_t s, int planes = 7);
 
 // On-site grid product and surface curl followed by the inverse transforms:
 // Ta/Tb[b][r][K] from HA/HB[b][r][K].
@@ -107,12 +108,15 @@ hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const f
 // Message-passing receiver pass: per receiver, synthesise the edge fields, multiply
 // with the streamed sender fields, sum over the CSR row, then the inverse transforms.
 // Rt is the edge-radial contraction in the layout [E][L][R].
+// Rtg: NULL, or separate edge coefficients of the curl product (same layout; zonal edge
+// field, one node slot).
 // SFf: NULL, or the sender fields of the parity-flipped node slot (two-slot message
 // passing; not with the separated edge field).
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
-                           const T *Rt, const T *SF, const T *SFf, T *Ta, T *Tb, hipStream_t s);
+                           const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
+                           hipStream_t s);
 
 // fp32 folded inverse transforms (folded.hip), lmax <= 24; hipErrorNotSupported when
 // the LDS staging does not fit.
@@ -131,7 +135,7 @@ constexpr int kSfChunk = 64;
 inline int sf_chunks(const Dims &d) { return (d.UV + kSfChunk - 1) / kSfChunk; }
 bool sender_mfma_supported(const Dims &d);
 hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
-                              bool chunked, hipStream_t s);
+                              bool chunked, hipStream_t s, int planes = 7);
 hipError_t launch_analysis_mfma(const Tabs<float> &tb, int64_t B, int R, const float *S,
                                 float *Ta, float *Tb, hipStream_t s);
 // fp32 on-site grid stage on MFMA (fourier_mfma.hip), default grid only: the same
@@ -149,7 +153,7 @@ bool receiver_mfma_supported(const Dims &d, int R);
 size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R);
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
-                                const float *SF, const float *SFf, bool sf_chunked, float *S,
-                                float *Ta, float *Tb, hipStream_t s);
+                                const float *Rtg, const float *SF, const float *SFf,
+                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s);
 
 }  // namespace cgtp

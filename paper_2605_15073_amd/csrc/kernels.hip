@@ -107,14 +107,15 @@ __device__ __forceinline__ void stage_q(const Tabs<T> &tb, T *qs)
 }
 
 // ---------------------------------------------------------------------------
-// Sender (node-side) grid fields: SF[b][r][0..2][UV] = (A, dA/dx, dA/dphi).
+// Sender (node-side) grid fields: SF[b][r][0..2][UV] = (A, dA/dx, dA/dphi); only the fields
+// whose bit is set in `planes` are stored.
 // One block per (node, rb consecutive ranks): the Legendre pass of all rb ranks,
 // then every thread writes the three fields of its grid points for each rank.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_sender_fields(Tabs<T> tb, int R, int rb,
                                                             const T *__restrict__ H,
-                                                            T *__restrict__ SF)
+                                                            T *__restrict__ SF, int planes)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
@@ -141,20 +142,20 @@ __global__ __launch_bounds__(kThreads) void k_sender_fields(Tabs<T> tb, int R, i
             T a, ax, ap;
             fourier_point(tb, qs, F + q * MU, Fx + q * MU, u, v, a, ax, ap);
             T *o = out + (int64_t)q * 3 * d.UVs + uv;
-            o[0] = a;
-            o[d.UVs] = ax;
-            o[2 * d.UVs] = ap;
+            if (planes & 1) o[0] = a;
+            if (planes & 2) o[d.UVs] = ax;
+            if (planes & 4) o[2 * d.UVs] = ap;
         }
     }
 }
 
 template <typename T>
 hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H, T *SF,
-                                hipStream_t s)
+                                hipStream_t s, int planes)
 {
     if (B == 0) return hipSuccess;
     if constexpr (sizeof(T) == 4) {
-        hipError_t e = launch_sender_mfma(tb, B, R, H, SF, false, s);
+        hipError_t e = launch_sender_mfma(tb, B, R, H, SF, false, s, planes);
         if (e != hipErrorNotSupported) return e;
     }
     const size_t per_rank = tb.d.K + 2 * (size_t)tb.d.M * tb.d.U;
@@ -166,7 +167,7 @@ hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H,
     const int64_t blocks = B * ((R + rb - 1) / rb);
     const size_t sh = sizeof(T) * (fixed + rb * per_rank);
     hipLaunchKernelGGL(k_sender_fields<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R,
-                       rb, H, SF);
+                       rb, H, SF, planes);
     return hipGetLastError();
 }
 
@@ -300,11 +301,13 @@ __device__ __forceinline__ double buf_load<double>(__amdgpu_buffer_rsrc_t rs, un
 
 // TWO: the senders carry a second, parity-flipped node slot SFf (same layout as SF). By
 // Table 1 its Gaunt product then feeds Tb and its curl product Ta.
-template <typename T, int RB, int NPT, bool FULL, bool TWO>
+// SPLIT: the curl product takes the edge coefficients Rtg (its own CP factors) for the
+// derivative sum g, the Gaunt product Rt for the value sum a.
+template <typename T, int RB, int NPT, bool FULL, bool TWO, bool SPLIT>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
-    const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ SF,
-    const T *__restrict__ SFf, T *__restrict__ Ta, T *__restrict__ Tb)
+    const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ Rtg,
+    const T *__restrict__ SF, const T *__restrict__ SFf, T *__restrict__ Ta, T *__restrict__ Tb)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
@@ -359,6 +362,7 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
             load_unit(unit, e + 1, uxn, uyn, uzn);
         }
         const T *rt = Rt + (int64_t)e * L * R + r0;   // Rt[e][l][r0 + q] = rt[l * R + q]
+        const T *rtg = SPLIT ? Rtg + (int64_t)e * L * R + r0 : rt;
         const int UVs = d.UVs;
         const __amdgpu_buffer_rsrc_t sfr =
             make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs, (unsigned)(nr * 3 * UVs * sizeof(T)));
@@ -397,7 +401,7 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
                 for (int q = 0; q < RB; ++q) {
                     T c = (FULL || q < nr) ? rt[R + q] : (T)0;
                     a[q] += c * t;
-                    g[q] = c;
+                    g[q] = SPLIT ? ((FULL || q < nr) ? rtg[R + q] : (T)0) : c;
                 }
             }
             T p0 = 1, p1 = t, d1 = 1;
@@ -407,8 +411,9 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
                     T c = (FULL || q < nr) ? rt[l * R + q] : (T)0;
+                    T cg = SPLIT ? ((FULL || q < nr) ? rtg[l * R + q] : (T)0) : c;
                     a[q] += c * p2;
-                    g[q] += c * d2;
+                    g[q] += cg * d2;
                 }
                 p0 = p1;
                 p1 = p2;
@@ -541,13 +546,15 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
-                           const T *Rt, const T *SF, const T *SFf, T *Ta, T *Tb, hipStream_t s)
+                           const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
+                           hipStream_t s)
 {
     int64_t blocks = N * R;
     if (blocks == 0) return hipSuccess;
     const Dims &d = tb.d;
+    if (SFf && Rtg) return hipErrorNotSupported;
     if (separated) {
-        if (SFf) return hipErrorNotSupported;
+        if (SFf || Rtg) return hipErrorNotSupported;
         size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + d.K + 2 * d.M * d.U);
         hipLaunchKernelGGL(k_receiver_separated<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s,
                            tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb);
@@ -556,22 +563,23 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + 2 * d.M * d.U);
     const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
     const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
-#define CGTP_RECV_TW(RBV, NP, TW)                                                              \
+#define CGTP_RECV_TW(RBV, NP, TW, SP)                                                          \
     do {                                                                                       \
         int64_t nb = N * ((R + RBV - 1) / RBV);                                                \
         if (R % RBV == 0)                                                                      \
-            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true, TW>), dim3((unsigned)nb),   \
-                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, SFf,   \
-                               Ta, Tb);                                                        \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true, TW, SP>),                   \
+                               dim3((unsigned)nb), dim3(threads), sh, s, tb, R, row_ptr, col,  \
+                               unit, Rt, Rtg, SF, SFf, Ta, Tb);                                \
         else                                                                                   \
-            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false, TW>), dim3((unsigned)nb),  \
-                               dim3(threads), sh, s, tb, R, row_ptr, col, unit, Rt, SF, SFf,   \
-                               Ta, Tb);                                                        \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false, TW, SP>),                  \
+                               dim3((unsigned)nb), dim3(threads), sh, s, tb, R, row_ptr, col,  \
+                               unit, Rt, Rtg, SF, SFf, Ta, Tb);                                \
     } while (0)
-#define CGTP_RECV(RBV, NP)                 \
-    do {                                   \
-        if (SFf) CGTP_RECV_TW(RBV, NP, true);  \
-        else CGTP_RECV_TW(RBV, NP, false); \
+#define CGTP_RECV(RBV, NP)                              \
+    do {                                                \
+        if (SFf) CGTP_RECV_TW(RBV, NP, true, false);    \
+        else if (Rtg) CGTP_RECV_TW(RBV, NP, false, true); \
+        else CGTP_RECV_TW(RBV, NP, false, false);       \
     } while (0)
     // ranks per block: sized so the per-thread accumulators and in-flight loads fit in
     // registers without spilling (fp64 values take two registers)
@@ -587,12 +595,12 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
 
 #define CGTP_INSTANTIATE(T)                                                                      \
     template hipError_t launch_sender_fields<T>(const Tabs<T> &, int64_t, int, const T *, T *,   \
-                                                hipStream_t);                                    \
+                                                hipStream_t, int);                               \
     template hipError_t launch_onsite_grid<T>(const Tabs<T> &, int64_t, int, const T *,          \
                                               const T *, T *, T *, hipStream_t);                 \
     template hipError_t launch_receiver<T>(const Tabs<T> &, bool, int64_t, int, const int32_t *, \
                                            const int32_t *, const T *, const T *, const T *,     \
-                                           const T *, T *, T *, hipStream_t);
+                                           const T *, const T *, T *, T *, hipStream_t);
 
 CGTP_INSTANTIATE(float)
 CGTP_INSTANTIATE(double)

@@ -69,7 +69,8 @@ size_t max_lds_bytes(const cgtp::Dims &d, size_t es)
 struct Layout {
     size_t off[6];
     size_t total;
-    size_t hf = 0, sff = 0;  // offsets of the flipped slot from HI and from SF (two slots)
+    size_t hf = 0, sff = 0;  // offsets of the second HI / SF (flipped slot or curl factors)
+    size_t rtf = 0;          // offset of the second Rt (curl factors)
 };
 
 // Receiver on MFMA: fp32, zonal edge field, R a multiple of 16, lmax high enough that the
@@ -101,11 +102,13 @@ Layout onsite_layout(const cgtp_plan_s *p, int R, int64_t N)
 
 // Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],
 // and, for the MFMA receiver, the summed grid fields S [N][R][2][UVs]. With two node slots,
-// HI and SF hold the natural slot followed by the flipped one.
-Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = false)
+// HI and SF hold the natural slot followed by the flipped one. With split factors (general
+// path), HI and Rt hold the Gaunt factors' contraction followed by the curl factors'.
+Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = false,
+                 bool split = false)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
-    const size_t slots = two ? 2 : 1;
+    const size_t nh = (two || split) ? 2 : 1, nsf = two ? 2 : 1, nrt = split ? 2 : 1;
     size_t h = align256(es * (size_t)N * R * p->d.K);
     const size_t sf_pts = sf_chunked(p, R) ? (size_t)cgtp::sf_chunks(p->d) * cgtp::kSfChunk : p->d.UVs;
     size_t sf = align256(es * (size_t)N * R * 3 * sf_pts);
@@ -113,14 +116,15 @@ Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = f
     size_t sg = use_mfma_receiver(p, R) ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, R)) : 0;
     Layout l{};
     l.off[0] = 0;
-    l.off[1] = slots * h;
-    l.off[2] = slots * (h + sf);
-    l.off[3] = slots * (h + sf) + rt;
-    l.off[4] = slots * (h + sf) + rt + h;
-    l.off[5] = slots * (h + sf) + rt + 2 * h;
-    l.total = slots * (h + sf) + rt + 2 * h + sg;
+    l.off[1] = nh * h;
+    l.off[2] = nh * h + nsf * sf;
+    l.off[3] = l.off[2] + nrt * rt;
+    l.off[4] = l.off[3] + h;
+    l.off[5] = l.off[4] + h;
+    l.total = l.off[5] + sg;
     l.hf = h;
     l.sff = sf;
+    l.rtf = rt;
     return l;
 }
 
@@ -351,15 +355,15 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
     if constexpr (sizeof(T) == 4) {
         if (use_mfma_receiver(p, R)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
-            e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt, SF,
-                                           SFf, sf_chunked(p, R), Sg, Ta, Tb, s);
+            e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt,
+                                           nullptr, SF, SFf, sf_chunked(p, R), Sg, Ta, Tb, s);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
             goto projections;
         }
     }
-    e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, SF, SFf,
-                                 Ta, Tb, s);
+    e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, nullptr,
+                                 SF, SFf, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "receiver");
     rec.mark();
 projections:
@@ -384,23 +388,29 @@ projections:
 // sends its Gaunt coupling to sector rel and its curl coupling to sector 1 - rel.
 //
 // The general call is lowered onto the fused kernels by stacking rank groups: group g
-// holds the ranks [g R, (g+1) R) of one slot pair contracted with one factor block, so
-// one launch of the grid stage at rank G R computes every group's Gaunt product (into
-// Ta) and curl (into Tb). Each block then projects the groups that feed it, through Ta
-// for a Gaunt block and Tb for a curl block, accumulating into its sector's output.
-// With shared input factors a group feeds one Gaunt and one curl block and nothing is
-// discarded; with per-block factors a group feeds one block and its other product is
-// not used.
+// holds the ranks [g R, (g+1) R) of one slot pair, contracted with the factors of the
+// blocks it feeds, so one launch of the grid stage at rank G R computes every group's
+// Gaunt product (into Ta) and curl (into Tb). Each block then projects the groups that
+// feed it, through Ta for a Gaunt block and Tb for a curl block, accumulating into its
+// sector's output. With shared input factors a group feeds one Gaunt and one curl block.
+// Message passing with per-block factors splits each group: the Gaunt product reads the
+// sender value and the edge value sum contracted with its block's factors, the curl
+// product the sender derivatives and edge derivative sum contracted with its own; so a
+// slot is one group and nothing is computed twice. On-site (both grid operands from one
+// contraction per group) and the separated edge field use one group per (slot pair,
+// block) instead, and each group's product of the other category is not used.
 
 constexpr int kMaxGroups = 8;
 
 struct Group {
     int s1, s2;  // slots of the first and second operand (0 natural, 1 flipped)
-    int blk;     // factor block, or -1 when every block shares the factors
+    int bg, bc;  // blocks fed by the group's Gaunt / curl product (-1: none); their input
+                 // factors contract the operands
 };
 
 struct Groups {
     int n = 0;
+    bool split = false;  // groups take different factors for their Gaunt and curl products
     Group g[kMaxGroups];
     int lo[4] = {0, 0, 0, 0}, hi[4] = {0, 0, 0, 0};  // groups [lo, hi) feed block b
 };
@@ -408,30 +418,33 @@ struct Groups {
 int block_of(int cat, int rel) { return 2 * cat + (cat ? 1 - rel : rel); }
 
 // f1 / f2: the first / second operand has a flipped slot (message passing: f1 = false, the
-// edge field); in_blocks: 1 (shared factors), 2 (per category) or 4 (per block).
-Groups make_groups(bool f1, bool f2, int in_blocks)
+// edge field); in_blocks: 1 (shared factors), 2 (per category) or 4 (per block); split:
+// per-block factors may differ between a group's two products.
+Groups make_groups(bool f1, bool f2, int in_blocks, bool split)
 {
     Groups G;
     auto present = [&](int s1, int s2) { return (s1 == 0 || f1) && (s2 == 0 || f2); };
-    if (in_blocks == 1) {
-        const int pairs[4][2] = {{0, 0}, {1, 1}, {0, 1}, {1, 0}};
-        for (const auto &pr : pairs)
-            if (present(pr[0], pr[1])) G.g[G.n++] = Group{pr[0], pr[1], -1};
+    const int pairs[4][2] = {{0, 0}, {1, 1}, {0, 1}, {1, 0}};
+    if (in_blocks == 1 || split) {
+        G.split = in_blocks > 1;
+        for (const auto &pr : pairs) {
+            const int rel = pr[0] != pr[1];
+            if (present(pr[0], pr[1]))
+                G.g[G.n++] = Group{pr[0], pr[1], block_of(0, rel), block_of(1, rel)};
+        }
     } else {
         for (int b = 0; b < 4; ++b) {
             const int cat = b >> 1, sec = b & 1, rel = cat ? 1 - sec : sec;
-            const int pairs[2][2] = {{0, rel}, {1, 1 - rel}};
             for (const auto &pr : pairs)
-                if (present(pr[0], pr[1])) G.g[G.n++] = Group{pr[0], pr[1], b};
+                if ((pr[0] != pr[1]) == rel && present(pr[0], pr[1]))
+                    G.g[G.n++] = Group{pr[0], pr[1], cat ? -1 : b, cat ? b : -1};
         }
     }
     // each block's groups are consecutive by construction
     for (int b = 0; b < 4; ++b) {
         int lo = -1, hi = -1;
         for (int i = 0; i < G.n; ++i) {
-            const Group &g = G.g[i];
-            const bool feeds = block_of(b >> 1, g.s1 != g.s2) == b && (g.blk < 0 || g.blk == b);
-            if (!feeds) continue;
+            if ((b >> 1 ? G.g[i].bc : G.g[i].bg) != b) continue;
             if (lo < 0) lo = i;
             hi = i + 1;
         }
@@ -440,6 +453,9 @@ Groups make_groups(bool f1, bool f2, int in_blocks)
     }
     return G;
 }
+
+// The block whose input factors contract a group's operands when it has one contraction.
+int group_block(const Group &g) { return g.bg >= 0 ? g.bg : g.bc; }
 
 // Factor pointers of the general entry points, resolved per block.
 struct Factors {
@@ -508,14 +524,14 @@ int run_onsite_groups(cgtp_plan_s *p, const Groups &G, int64_t N, const void *co
     hipError_t e;
     for (int gi = 0; gi < G.n; ++gi) {
         const Group &g = G.g[gi];
-        e = contract_in<T>(N, C, R, d.K, f.in1[g.blk < 0 ? 0 : g.blk], X1[g.s1],
+        e = contract_in<T>(N, C, R, d.K, f.in1[group_block(g)], X1[g.s1],
                            HA + (int64_t)gi * R * d.K, hs, s);
         if (e != hipSuccess) return hip_fail(e, "contract first operand");
     }
     rec.mark();
     for (int gi = 0; gi < G.n; ++gi) {
         const Group &g = G.g[gi];
-        e = contract_in<T>(N, C, R, d.K, f.in2[g.blk < 0 ? 0 : g.blk], X2[g.s2],
+        e = contract_in<T>(N, C, R, d.K, f.in2[group_block(g)], X2[g.s2],
                            HB + (int64_t)gi * R * d.K, hs, s);
         if (e != hipSuccess) return hip_fail(e, "contract second operand");
     }
@@ -535,54 +551,68 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     const int C = p->C, R = p->R, Rg = G.n * R;
     const bool separated = (p->flags & CGTP_EDGE_SEPARATED) != 0;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
-    Layout lay = mp_layout(p, Rg, N, E);
+    Layout lay = mp_layout(p, Rg, N, E, false, G.split);
     T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
     T *SF = reinterpret_cast<T *>(ws + lay.off[1]);
     T *Rt = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Ta = reinterpret_cast<T *>(ws + lay.off[3]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
+    // split: the curl products' node contraction and edge coefficients
+    T *HIc = G.split ? reinterpret_cast<T *>(ws + lay.off[0] + lay.hf) : nullptr;
+    T *Rtc = G.split ? reinterpret_cast<T *>(ws + lay.off[2] + lay.rtf) : nullptr;
     StageRec rec;
     int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_GENERAL, 6, s);
     if (st) return st;
     hipError_t e;
     for (int gi = 0; gi < G.n; ++gi) {
         const Group &g = G.g[gi];
-        e = contract_in<T>(N, C, R, d.K, f.in2[g.blk < 0 ? 0 : g.blk], X2[g.s2],
-                           HI + (int64_t)gi * R * d.K, (int64_t)Rg * d.K, s);
+        const int64_t off = (int64_t)gi * R * d.K, hs = (int64_t)Rg * d.K;
+        e = contract_in<T>(N, C, R, d.K, f.in2[G.split ? g.bg : group_block(g)], X2[g.s2],
+                           HI + off, hs, s);
+        if (e == hipSuccess && G.split)
+            e = contract_in<T>(N, C, R, d.K, f.in2[g.bc], X2[g.s2], HIc + off, hs, s);
         if (e != hipSuccess) return hip_fail(e, "contract node features");
     }
     rec.mark();
-    if constexpr (sizeof(T) == 4) {
-        if (sf_chunked(p, Rg))
-            e = cgtp::launch_sender_mfma(tb, N, Rg, HI, SF, true, s);
-        else
-            e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s);
-    } else {
-        e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s);
+    // split: the Gaunt factors' contraction gives the sender values, the curl factors' the
+    // two derivative fields, into the same field slots
+    for (int pass = 0; pass < (G.split ? 2 : 1); ++pass) {
+        const T *h = pass ? HIc : HI;
+        const int planes = G.split ? (pass ? 6 : 1) : 7;
+        if constexpr (sizeof(T) == 4) {
+            if (sf_chunked(p, Rg))
+                e = cgtp::launch_sender_mfma(tb, N, Rg, h, SF, true, s, planes);
+            else
+                e = cgtp::launch_sender_fields<T>(tb, N, Rg, h, SF, s, planes);
+        } else {
+            e = cgtp::launch_sender_fields<T>(tb, N, Rg, h, SF, s, planes);
+        }
+        if (e != hipSuccess) return hip_fail(e, "sender fields");
     }
-    if (e != hipSuccess) return hip_fail(e, "sender fields");
     rec.mark();
     for (int gi = 0; gi < G.n; ++gi) {
         const Group &g = G.g[gi];
-        e = cgtp::launch_contract<T>(E, C, R, d.L, true, (const T *)f.in1[g.blk < 0 ? 0 : g.blk],
-                                     (int64_t)C * R, R, 1, (const T *)rad, (int64_t)C * d.L,
-                                     Rt + (int64_t)gi * R, (int64_t)d.L * Rg, 1, Rg,
-                                     separated ? nullptr : tb.cl, false, s);
-        if (e != hipSuccess) return hip_fail(e, "contract edge radial");
+        for (int pass = 0; pass < (G.split ? 2 : 1); ++pass) {
+            const int blk = G.split ? (pass ? g.bc : g.bg) : group_block(g);
+            e = cgtp::launch_contract<T>(E, C, R, d.L, true, (const T *)f.in1[blk],
+                                         (int64_t)C * R, R, 1, (const T *)rad, (int64_t)C * d.L,
+                                         (pass ? Rtc : Rt) + (int64_t)gi * R, (int64_t)d.L * Rg,
+                                         1, Rg, separated ? nullptr : tb.cl, false, s);
+            if (e != hipSuccess) return hip_fail(e, "contract edge radial");
+        }
     }
     rec.mark();
-    e = hipSuccess;
     if constexpr (sizeof(T) == 4) {
         if (use_mfma_receiver(p, Rg)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
-            e = cgtp::launch_receiver_mfma(tb, N, Rg, row_ptr, col, (const float *)unit, Rt, SF,
-                                           nullptr, sf_chunked(p, Rg), Sg, Ta, Tb, s);
+            e = cgtp::launch_receiver_mfma(tb, N, Rg, row_ptr, col, (const float *)unit, Rt, Rtc,
+                                           SF, nullptr, sf_chunked(p, Rg), Sg, Ta, Tb, s);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
             return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
         }
     }
-    e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, SF,
+    e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, Rtc, SF,
                                  nullptr, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "receiver");
     rec.mark();
@@ -604,7 +634,7 @@ GeneralRoute route_onsite(const cgtp_plan_s *p, int64_t N, bool f1, bool f2, int
     if (r.fused) {
         r.ws = onsite_layout(p, p->R, N).total;
     } else {
-        r.G = make_groups(f1, f2, in_blocks);
+        r.G = make_groups(f1, f2, in_blocks, false);
         r.ws = onsite_layout(p, r.G.n * p->R, N).total;
     }
     return r;
@@ -620,8 +650,8 @@ GeneralRoute route_mp(const cgtp_plan_s *p, int64_t N, int64_t E, bool flip, int
     if (r.fused) {
         r.ws = mp_layout(p, p->R, N, E, flip).total;
     } else {
-        r.G = make_groups(false, flip, in_blocks);
-        r.ws = mp_layout(p, r.G.n * p->R, N, E).total;
+        r.G = make_groups(false, flip, in_blocks, !(p->flags & CGTP_EDGE_SEPARATED));
+        r.ws = mp_layout(p, r.G.n * p->R, N, E, false, r.G.split).total;
     }
     return r;
 }

@@ -52,12 +52,15 @@ __device__ __forceinline__ void wave_sync()
 // TWO: the senders carry a second, parity-flipped node slot SFf (same layout as SF); by
 // Table 1 its curl product then feeds S_alpha's slot (natural parity) and its Gaunt
 // product S_beta's. The next edge is prefetched only with one slot (registers).
-template <int WPB, int LM, bool TWO>
+// SPLIT: the curl product's edge coefficients are Rtg (its own CP factors): the derivative
+// sum g multiplies P' with those, the value sum a P with Rt.
+template <int WPB, int LM, bool TWO, bool SPLIT>
 __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
                                                             const int32_t *__restrict__ row_ptr,
                                                             const int32_t *__restrict__ col,
                                                             const float *__restrict__ unit,
                                                             const float *__restrict__ Rt,
+                                                            const float *__restrict__ Rtg,
                                                             const float *__restrict__ SF,
                                                             const float *__restrict__ SFf,
                                                             int sf_nc, float *__restrict__ S)
@@ -157,11 +160,13 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
         uz *= inv;
         // B operand: Rt[e][4 kk + g][r0 + n]
         const float *rte = Rt + (int64_t)e * L * R + r0 + n;
-        float Bv[KS];
+        const float *rtg = SPLIT ? Rtg + (int64_t)e * L * R + r0 + n : rte;
+        float Bv[KS], Bg[KS];
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
             const int l = 4 * kk + g;
             Bv[kk] = l <= LM ? rte[l * R] : 0.f;
+            Bg[kk] = SPLIT ? (l <= LM ? rtg[l * R] : 0.f) : Bv[kk];
         }
         wave_sync();  // this wave is done reading the previous edge's P, P'
         {
@@ -200,7 +205,7 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
                 const float ap = Pl[(4 * kk + g) * RS + 16 * t + n];
                 const float ad = Dl[(4 * kk + g) * RS + 16 * t + n];
                 a = __builtin_amdgcn_mfma_f32_16x16x4f32(ap, Bv[kk], a, 0, 0, 0);
-                gg = __builtin_amdgcn_mfma_f32_16x16x4f32(ad, Bv[kk], gg, 0, 0, 0);
+                gg = __builtin_amdgcn_mfma_f32_16x16x4f32(ad, Bg[kk], gg, 0, 0, 0);
             }
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
@@ -302,12 +307,13 @@ size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R)
 
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
-                                const float *SF, const float *SFf, bool sf_chunked, float *S,
-                                float *Ta, float *Tb, hipStream_t s)
+                                const float *Rtg, const float *SF, const float *SFf,
+                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s)
 {
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
+    if (SFf && Rtg) return hipErrorNotSupported;
     constexpr int WPB = 2, PW = 64, PC = WPB * PW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
@@ -320,13 +326,17 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
 #define CGTP_CASE(LMV)                                                                          \
     case LMV:                                                                                   \
         if (SFf)                                                                                \
-            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, true>), dim3((unsigned)blocks),       \
-                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt, SF, \
-                               SFf, sf_nc, S);                                                  \
+            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, true, false>), dim3((unsigned)blocks), \
+                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt,   \
+                               Rtg, SF, SFf, sf_nc, S);                                         \
+        else if (Rtg)                                                                           \
+            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, false, true>), dim3((unsigned)blocks), \
+                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt,   \
+                               Rtg, SF, SFf, sf_nc, S);                                         \
         else                                                                                    \
-            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, false>), dim3((unsigned)blocks),      \
-                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt, SF, \
-                               SFf, sf_nc, S);                                                  \
+            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, false, false>),                       \
+                               dim3((unsigned)blocks), dim3(64 * WPB), sh, s, tb, R, nchunks,   \
+                               row_ptr, col, unit, Rt, Rtg, SF, SFf, sf_nc, S);                 \
         break;
         CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11) CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
         CGTP_CASE(15) CGTP_CASE(16) CGTP_CASE(17) CGTP_CASE(18) CGTP_CASE(19) CGTP_CASE(20)
