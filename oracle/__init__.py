@@ -59,6 +59,9 @@ def _load():
     lib.cgo_onsite.argtypes = [i32, i32, i32, i64] + [p] * 9 + [i32]
     lib.cgo_message_pass.restype = i32
     lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64] + [p] * 9 + [p, i64, p, p, i32]
+    lib.cgo_message_pass_fields.restype = i32
+    lib.cgo_message_pass_fields.argtypes = ([i32, i32, i32, i64, i64] + [p] * 9
+                                            + [p, i64, p, p, i32])
     lib.cgo_max_threads.restype = i32
     lib.cgo_max_threads.argtypes = []
     _lib = lib
@@ -288,4 +291,76 @@ def _mp_rows(lmax, row_ptr, col, edge_unit, edge_radial, node_feat, node_flip, U
                               rec.shape[0], _ptr(oe), _ptr(oo), int(nthreads))
     if rc != 0:
         raise RuntimeError(f"cgo_message_pass failed ({rc})")
+    return oe, oo
+
+
+def message_pass_fields(lmax, row_ptr, col, edge_feat, node_feat, U_E, U_I, U_out_even,
+                        U_out_odd, receivers=None, nthreads: int = 0, edge_flip=None,
+                        node_flip=None):
+    """Message passing with two parity-bearing fields (Eq. twoparity-phi), fp64.
+
+    row_ptr [N+1], col [E] (int32 CSR by receiver); edge_feat [E, C, L^2] (natural-parity
+    slot of the per-edge field) and edge_flip (its parity-flipped slot, or None);
+    node_feat, node_flip [N, C, L^2]; factor arrays stacked as in onsite().
+    Returns (out_even, out_odd), each [len(receivers), C, L^2] (all receivers when
+    receivers is None)."""
+    if receivers is None:
+        n = np.asarray(node_feat).shape[0]
+        return _mpf_rows(lmax, row_ptr, col, edge_feat, edge_flip, node_feat, node_flip, U_E,
+                         U_I, U_out_even, U_out_odd, np.arange(n), nthreads)
+    # Marshalling only: the rows of the requested receivers, their edges and the features
+    # of their senders, so large inputs are not converted to fp64 whole.
+    row_ptr = np.asarray(row_ptr)
+    rec = np.asarray(receivers, dtype=np.int64)
+    starts, ends = row_ptr[rec].astype(np.int64), row_ptr[rec + 1].astype(np.int64)
+    parts = [np.arange(a, b, dtype=np.int64) for a, b in zip(starts, ends)]
+    eidx = np.concatenate(parts) if parts else np.zeros(0, np.int64)
+    senders, local_col = np.unique(np.asarray(col)[eidx], return_inverse=True)
+    n_compact = max(len(rec), len(senders), 1)
+
+    def compact(a):
+        if a is None:
+            return None
+        full = np.asarray(a)
+        out = np.zeros((n_compact,) + full.shape[1:], dtype=np.float64)
+        out[:len(senders)] = full[senders]
+        return out
+
+    rp = np.zeros(n_compact + 1, np.int32)
+    rp[1:len(rec) + 1] = np.cumsum(ends - starts)
+    rp[len(rec) + 1:] = rp[len(rec)]
+    cut = lambda a: None if a is None else np.asarray(a)[eidx]
+    return _mpf_rows(lmax, rp, local_col.astype(np.int32), cut(edge_feat), cut(edge_flip),
+                     compact(node_feat), compact(node_flip), U_E, U_I, U_out_even, U_out_odd,
+                     np.arange(len(rec)), nthreads)
+
+
+def _mpf_rows(lmax, row_ptr, col, edge_feat, edge_flip, node_feat, node_flip, U_E, U_I,
+              U_out_even, U_out_odd, receivers, nthreads):
+    lib = _load()
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    col = np.ascontiguousarray(col, dtype=np.int32)
+    ef, nf = _f64(edge_feat), _f64(node_feat)
+    efl = None if edge_flip is None else _f64(edge_flip)
+    nfl = None if node_flip is None else _f64(node_flip)
+    N, C, L2 = nf.shape
+    E = col.shape[0]
+    assert L2 == (lmax + 1) ** 2 and row_ptr.shape[0] == N + 1 and ef.shape == (E, C, L2)
+    assert efl is None or efl.shape == ef.shape
+    assert nfl is None or nfl.shape == nf.shape
+    UE, UI = _in_blocks(U_E, lmax, C), _in_blocks(U_I, lmax, C)
+    Uo = _out_blocks(U_out_even, U_out_odd, lmax, C)
+    R = UE[0].shape[2]
+    for x in UE + UI + Uo:
+        assert x.shape == (lmax + 1, C, R)
+    rec = np.ascontiguousarray(receivers, dtype=np.int64)
+    keep = [_ptr_array(x) for x in (UE, UI, Uo)]
+    oe = np.zeros((rec.shape[0], C, L2))
+    oo = np.zeros((rec.shape[0], C, L2))
+    rc = lib.cgo_message_pass_fields(lmax, C, R, N, E, _ptr(row_ptr), _ptr(col), _ptr(ef),
+                                     _ptr(efl), _ptr(nf), _ptr(nfl), keep[0][1], keep[1][1],
+                                     keep[2][1], _ptr(rec), rec.shape[0], _ptr(oe), _ptr(oo),
+                                     int(nthreads))
+    if rc != 0:
+        raise RuntimeError(f"cgo_message_pass_fields failed ({rc})")
     return oe, oo

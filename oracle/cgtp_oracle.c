@@ -615,6 +615,85 @@ int cgo_message_pass(int lmax, int C, int R, long n_nodes, long n_edges, const i
     return err;
 }
 
+/* Message passing with two parity-bearing fields (Eq. twoparity-phi): the edge operand is a
+ * general per-edge feature with its own parity slots instead of R Y, so its channel
+ * contraction runs per edge like the node side (Eq. msgpass-HI applied to the edge field).
+ *   edge_feat: [E][C][L^2] natural-parity slot of the edge field I^(E);
+ *   edge_flip: NULL, or its parity-flipped slot [E][C][L^2];
+ *   node_feat, node_flip: the node field I^(N) as in cgo_message_pass;
+ *   U_E[b], U_I[b], U_out[b]: per-block factors as in cgo_onsite;
+ *   out_even, out_odd: [n_recv][C][L^2] (row q is receiver recv[q]).
+ * For every edge e = (j -> i) every slot pair (s1 of the edge field, s2 of the node field of
+ * sender j) contributes its Gaunt and curl couplings, routed to blocks by p = p1 p2 exactly as
+ * the on-site pairs; the sum over the edges of a receiver replaces the on-site product.
+ * Every (receiver, rank) pair is independent; they are spread over the threads. */
+int cgo_message_pass_fields(int lmax, int C, int R, long n_nodes, long n_edges,
+                            const int32_t *row_ptr, const int32_t *col, const double *edge_feat,
+                            const double *edge_flip, const double *node_feat,
+                            const double *node_flip, const double *const *U_E,
+                            const double *const *U_I, const double *const *U_out,
+                            const int64_t *recv, long n_recv, double *out_even, double *out_odd,
+                            int nthreads)
+{
+    if (lmax < 0 || C < 1 || R < 1 || n_nodes < 0 || n_edges < 0 || n_recv < 0) return -1;
+    for (long q = 0; q < n_recv; ++q)
+        if (recv[q] < 0 || recv[q] >= n_nodes) return -1;
+    set_threads(nthreads);
+    int L2 = (lmax + 1) * (lmax + 1);
+    const double *X1[2] = {edge_feat, edge_flip}, *X2[2] = {node_feat, node_flip};
+    int live[CGO_NB] = {0, 0, 0, 0};
+    for (int s1 = 0; s1 < 2; ++s1)
+        for (int s2 = 0; s2 < 2; ++s2)
+            if (X1[s1] && X2[s2])
+                for (int cat = 0; cat < 2; ++cat) {
+                    int b = block_of(cat, s1 != s2);
+                    if ((b & 1) ? out_odd != NULL : out_even != NULL) live[b] = 1;
+                }
+    sparse_tab G, Q;
+    if (build_tab(0, lmax, &G) || build_tab(1, lmax, &Q)) return -2;
+    double *T[CGO_NB];
+    int err = 0;
+    for (int b = 0; b < CGO_NB; ++b) {
+        T[b] = (double *)calloc(live[b] ? (size_t)n_recv * R * L2 + 1 : 1, sizeof(double));
+        if (!T[b]) err = -2;
+    }
+    if (!err) {
+#pragma omp parallel
+        {
+            double *h1 = (double *)malloc(sizeof(double) * 2 * L2), *h2 = h1 ? h1 + L2 : NULL;
+            if (!h1) {
+#pragma omp atomic write
+                err = -2;
+            } else {
+#pragma omp for schedule(dynamic, 1)
+                for (long qr = 0; qr < n_recv * R; ++qr) {
+                    long i = (long)recv[qr / R];
+                    int r = (int)(qr % R);
+                    for (long e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+                        long j = col[e];
+                        for (int s1 = 0; s1 < 2; ++s1)
+                            for (int s2 = 0; s2 < 2; ++s2) {
+                                if (!X1[s1] || !X2[s2]) continue;
+                                for (int cat = 0; cat < 2; ++cat) {
+                                    int b = block_of(cat, s1 != s2);
+                                    if (!live[b]) continue;
+                                    channel_contract_r(lmax, C, R, r, U_E[b], X1[s1] + (size_t)e * C * L2, h1);
+                                    channel_contract_r(lmax, C, R, r, U_I[b], X2[s2] + (size_t)j * C * L2, h2);
+                                    sparse_couple(cat ? &Q : &G, h1, h2, T[b] + (size_t)qr * L2);
+                                }
+                            }
+                    }
+                }
+            }
+            free(h1);
+        }
+    }
+    if (!err) project_blocks(lmax, C, R, n_recv, U_out, T, live, out_even, out_odd);
+    for (int b = 0; b < CGO_NB; ++b) free(T[b]);
+    free_tab(&G); free_tab(&Q);
+    return err;
+}
+
 int cgo_max_threads(void)
 {
     return set_threads(0);

@@ -21,6 +21,8 @@ performance"; no public dataset is involved):
   factors stacked [n_blocks][L][C][R] and output weights [2][L][C][R] (Gaunt, curl), each
   block N(0, 1/C), drawn from a second generator seeded seed + 7919 so the graph and the
   natural slots are those of the plain workload of the same seed.
+* Two parity-bearing fields: per-edge field coefficients [E][C][L^2] (and their flipped
+  slot) N(0, 1), with the factor blocks, from a third generator seeded seed + 104729.
 """
 from __future__ import annotations
 
@@ -165,10 +167,28 @@ def general_mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, flip: 
     return d
 
 
+def fields_mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, edge_flip: bool = True,
+                     node_flip: bool = True, in_blocks: int = 4, out_blocks: int = 2,
+                     density: float = 0.1, r_cut: float = 5.0):
+    """Message passing with two parity-bearing fields: the graph and node slots of mp_inputs
+    with the same seed, and a per-edge field [E][C][L^2] (and its flipped slot) of N(0, 1)
+    coefficients in place of R Y. Draw order (a third generator, seed + 104729): edge_feat,
+    edge_flip (if present), U_E, U_I, U_out_even, U_out_odd."""
+    d = mp_inputs(n_atoms, lmax, C, R, seed, density=density, r_cut=r_cut, two_slot=node_flip)
+    if not node_flip:
+        d["node_flip"] = None
+    rng = np.random.default_rng(seed + 104729)
+    E = d["n_edges"]
+    d["edge_feat"] = coefficients(rng, E, C, lmax, per_degree=False)
+    d["edge_flip"] = coefficients(rng, E, C, lmax, per_degree=False) if edge_flip else None
+    d.update(_general_factors(rng, ("U_E", "U_I"), lmax, C, R, in_blocks, out_blocks))
+    return d
+
+
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str          # "onsite" or "mp"
+    kind: str          # "onsite", "mp" or "mp_fields" (two parity-bearing fields)
     n: int             # nodes (on-site) or atoms (message passing)
     lmax: int
     C: int
@@ -181,13 +201,18 @@ class Workload:
     # general parameterization (0: the plain calls): input factor blocks 1, 2 or 4 ...
     in_blocks: int = 0
     out_blocks: int = 1      # ... output weight blocks per sector (1 or 2)
-    flip1: bool = False      # first on-site operand carries a flipped slot
+    flip1: bool = False      # first operand (on-site A, or the edge field) has a flipped slot
 
     @property
     def general(self) -> bool:
         return self.in_blocks > 0
 
     def make(self, **kw):
+        if self.kind == "mp_fields":
+            return fields_mp_inputs(self.n, self.lmax, self.C, self.R, self.seed,
+                                    edge_flip=self.flip1, node_flip=self.two_slot,
+                                    in_blocks=self.in_blocks, out_blocks=self.out_blocks,
+                                    r_cut=self.r_cut, **kw)
         if self.general and self.kind == "onsite":
             return general_onsite_inputs(self.n, self.lmax, self.C, self.R, self.seed,
                                          flip1=self.flip1, flip2=self.two_slot,
