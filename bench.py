@@ -105,6 +105,25 @@ def onsite_grid_flops(lmax: int, R: int, N: int, kind: str = "both") -> int:
     return N * R * per
 
 
+def fields_receiver_flops(w, N: int, E: int) -> int:
+    """Algorithmic flops of the edge-field receiver (two parity-bearing fields), dense
+    transforms as in onsite_grid_flops. Per (edge, rank) of a slot pair: the edge field's
+    Legendre and Fourier syntheses and the product; per (receiver, rank): the analysis. With
+    shared factors a pair needs both products (F and dF/dx, three fields, product and
+    bracket, two analysed fields); with per-block factors each (pair, category) needs its own
+    (Gaunt: F, one field, one product, one analysed field; curl: F and dF/dx, two fields, the
+    bracket, one analysed field)."""
+    U, V = grid_dims(w.lmax)
+    L, M = w.lmax + 1, 2 * w.lmax + 1
+    pairs = (2 if w.flip1 else 1) * (2 if w.two_slot else 1)
+    both_e, both_r = 4 * U * L * L + 6 * U * V * M + 4 * U * V, 4 * U * V * M + 4 * U * L * L
+    g_e, g_r = 2 * U * L * L + 2 * U * V * M + U * V, 2 * U * V * M + 2 * U * L * L
+    c_e, c_r = 4 * U * L * L + 4 * U * V * M + 3 * U * V, 2 * U * V * M + 2 * U * L * L
+    if w.in_blocks == 1:
+        return pairs * w.R * (E * both_e + N * both_r)
+    return pairs * w.R * (E * (g_e + c_e) + N * (g_r + c_r))
+
+
 def general_onsite_flops(w) -> int:
     """Algorithmic grid flops of the general on-site call: with shared factors every slot
     pair needs both products; with per-block factors every (slot pair, block) needs the
@@ -132,6 +151,8 @@ def to_dev(d, keys):
 
 MP_KEYS = ("row_ptr", "col", "edge_unit", "edge_radial", "node_feat", "U_E", "U_I",
            "U_out_even", "U_out_odd")
+MPF_KEYS = ("row_ptr", "col", "edge_feat", "node_feat", "U_E", "U_I", "U_out_even",
+            "U_out_odd")
 ONSITE_KEYS = ("A", "B", "U_A", "U_B", "U_out_even", "U_out_odd")
 
 
@@ -153,7 +174,13 @@ def cpu_baseline(w, d, budget_s: float = 15.0):
     import oracle
 
     cores = oracle.max_threads()
-    if w.kind == "mp":
+    if w.kind == "mp_fields":
+        def run(n):
+            return oracle.message_pass_fields(w.lmax, *(d[k] for k in MPF_KEYS),
+                                              receivers=np.arange(n), edge_flip=d["edge_flip"],
+                                              node_flip=d["node_flip"])
+        unit_name = "receivers"
+    elif w.kind == "mp":
         def run(n):
             return oracle.message_pass(w.lmax, *(d[k] for k in MP_KEYS),
                                        receivers=np.arange(n), node_flip=d.get("node_flip"))
@@ -188,7 +215,22 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
     if d is None:
         d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
-    if w.general and w.kind == "mp":
+    if w.kind == "mp_fields":
+        t = to_dev(d, MPF_KEYS + ("edge_flip", "node_flip"))
+        E = int(d["n_edges"])
+        op = cg.CGTP_OP_MESSAGE_PASS_FIELDS
+        flips = (1 if w.flip1 else 0) | (2 if w.two_slot else 0)
+        ws = torch.empty(cg.workspace_bytes_general(plan, op, w.n, E, flips, w.in_blocks,
+                                                    w.out_blocks),
+                         dtype=torch.uint8, device="cuda")
+        oe = torch.empty_like(t["node_feat"])
+        oo = torch.empty_like(t["node_feat"])
+
+        def step():
+            cg.message_pass_fields(plan, *(t[k] for k in MPF_KEYS), edge_flip=t["edge_flip"],
+                                   node_flip=t["node_flip"], out_even=oe, out_odd=oo,
+                                   workspace=ws)
+    elif w.general and w.kind == "mp":
         t = to_dev(d, MP_KEYS + ("node_flip",))
         E = int(d["n_edges"])
         op = cg.CGTP_OP_MESSAGE_PASS_GENERAL
@@ -271,7 +313,8 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name,
-                   "kind": ("message_passing" if w.kind == "mp" else "onsite")
+                   "kind": "message_passing_two_fields" if w.kind == "mp_fields" else
+                   ("message_passing" if w.kind == "mp" else "onsite")
                    + ("_general" if w.general else "_two_slot" if w.two_slot else ""),
                    "nodes": w.n, "edges": E, "lmax": w.lmax, "channels": w.C, "rank": w.R,
                    "grid": f"{U}x{V}", "seed": w.seed},
@@ -282,7 +325,13 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
     if w.general:
         rec["config"].update(in_blocks=w.in_blocks, out_blocks=w.out_blocks,
                              flips=[bool(w.flip1), bool(w.two_slot)])
-    if w.kind == "mp" and dom == "receiver":
+    if w.kind == "mp_fields" and dom == "receiver":
+        fl = fields_receiver_flops(w, w.n, E)
+        rec["roofline"] = {"bound": "alu", "achieved": fl / t_dom / 1e12,
+                           "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                           "frac": fl / t_dom / 1e12 / FP32_PEAK_TFLOPS,
+                           "traffic": load_traffic(w.name), "algorithmic_flops": fl}
+    elif w.kind == "mp" and dom == "receiver":
         alg = (general_receiver_bytes(w, w.n, E) if w.general
                else receiver_bytes(w.lmax, w.R, w.n, E, 2 if w.two_slot else 1))
         traffic = load_traffic(w.name)

@@ -83,6 +83,7 @@ extern "C" {
 #define CGTP_OP_MESSAGE_PASS_TWO_SLOT 2
 #define CGTP_OP_ONSITE_GENERAL 3        /* cgtp_workspace_bytes_general / cgtp_stage_times */
 #define CGTP_OP_MESSAGE_PASS_GENERAL 4
+#define CGTP_OP_MESSAGE_PASS_FIELDS 5
 
 typedef struct cgtp_plan_s *cgtp_plan;
 
@@ -202,10 +203,10 @@ int cgtp_message_pass_two_slot(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
  * cgtp_onsite / cgtp_message_pass; CGTP_ERR_UNSUPPORTED also when n_nodes times the
  * stacked rank exceeds 2^31 - 1. */
 
-/* Workspace of a general call. op: CGTP_OP_ONSITE_GENERAL or CGTP_OP_MESSAGE_PASS_GENERAL;
- * flips: bit 0 set when the first on-site operand has a flipped slot, bit 1 when the second
- * operand (on-site) or the node feature (message passing) has one; in_blocks, out_blocks
- * as in the calls. */
+/* Workspace of a general call. op: CGTP_OP_ONSITE_GENERAL, CGTP_OP_MESSAGE_PASS_GENERAL or
+ * CGTP_OP_MESSAGE_PASS_FIELDS; flips: bit 0 set when the first operand (on-site A, or the
+ * edge field of cgtp_message_pass_fields) has a flipped slot, bit 1 when the second operand
+ * (on-site B, or the node feature) has one; in_blocks, out_blocks as in the calls. */
 int cgtp_workspace_bytes_general(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edges,
                                  int flips, int in_blocks, int out_blocks, size_t *bytes);
 
@@ -232,6 +233,31 @@ int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                               const void *U_out_odd, void *out_even, void *out_odd,
                               void *workspace, size_t ws_bytes, void *stream);
 
+/* Message passing with two parity-bearing fields (Eq. twoparity-phi): the edge operand is a
+ * general per-edge feature with its own parity slots (a message that has gathered parity
+ * content in earlier layers) instead of R Y. Its channel contraction runs per edge (the
+ * analogue of Eq. msgpass-HI) and its grid fields come from the full Legendre and Fourier
+ * syntheses, so the zonal form does not apply. Every (edge slot, node slot) pair is routed
+ * to the factor blocks exactly as the on-site slot pairs of cgtp_onsite_general:
+ *   out_s = sum_{cat} sum_r Uout[cat, s] T_{2 cat + s},  T_b = sum over the edges
+ *           (j -> i) and the slot pairs routed to b of the block-b coupling of
+ *           U_E[b]^T I^(E)_e[s1] and U_I[b]^T I^(N)_j[s2].
+ *   edge_feat [E][C][K]   natural-parity slot of the edge field (edge e in CSR order);
+ *   edge_flip [E][C][K]   its parity-flipped slot, or NULL;
+ *   node_feat, node_flip  [N][C][K] node field slots (node_flip may be NULL);
+ *   U_E, U_I              input factors of the edge and node fields, in_blocks blocks;
+ *   U_out_even, U_out_odd output weights, out_blocks blocks each (cgtp_onsite_general).
+ * Rank groups are stacked as in cgtp_onsite_general (up to 8x the plan's rank); query the
+ * workspace with cgtp_workspace_bytes_general(CGTP_OP_MESSAGE_PASS_FIELDS). Other
+ * arguments, preconditions and errors as in cgtp_message_pass; CGTP_ERR_UNSUPPORTED also
+ * when the receiver's LDS staging does not fit (fp64 at the highest degrees). */
+int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
+                             const int32_t *row_ptr, const int32_t *col, const void *edge_feat,
+                             const void *edge_flip, const void *node_feat, const void *node_flip,
+                             int in_blocks, const void *U_E, const void *U_I, int out_blocks,
+                             const void *U_out_even, const void *U_out_odd, void *out_even,
+                             void *out_odd, void *workspace, size_t ws_bytes, void *stream);
+
 /* Per-stage GPU time of the calls made since the previous cgtp_stage_times on
  * this plan (plan created with CGTP_TIME_STAGES), in the spirit of the paper's
  * per-step breakdown (App. D, Table 4). Waits for the recorded events, writes the
@@ -244,7 +270,9 @@ int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
  * 4 project even, 5 project odd. CGTP_OP_MESSAGE_PASS_TWO_SLOT has the same six
  * stages, each covering both node slots; CGTP_OP_ONSITE_GENERAL and
  * CGTP_OP_MESSAGE_PASS_GENERAL those of CGTP_OP_ONSITE / CGTP_OP_MESSAGE_PASS, covering
- * every rank group. A skipped stage counts as 0.
+ * every rank group; CGTP_OP_MESSAGE_PASS_FIELDS: 0 contract node features, 1 sender grid
+ * fields, 2 contract edge field, 3 receiver pass, 4 project even, 5 project odd. A
+ * skipped stage counts as 0.
  * Errors: CGTP_ERR_ARG (NULL, flag not set, unknown op), CGTP_ERR_HIP. */
 int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages, int *n_calls);
 

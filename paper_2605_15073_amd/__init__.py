@@ -30,11 +30,13 @@ CGTP_OP_MESSAGE_PASS = 1
 CGTP_OP_MESSAGE_PASS_TWO_SLOT = 2
 CGTP_OP_ONSITE_GENERAL = 3
 CGTP_OP_MESSAGE_PASS_GENERAL = 4
+CGTP_OP_MESSAGE_PASS_FIELDS = 5
 CGTP_MAX_LMAX = 24
 
 EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
             "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_workspace_bytes_general",
-            "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_stage_times",
+            "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_message_pass_fields",
+            "cgtp_stage_times",
             "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables")
 ONSITE_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis", "project_even",
                  "project_odd")
@@ -79,6 +81,7 @@ def load_library(path: str = LIB_PATH):
                                         + [vp, sz, vp])
     lib.cgtp_message_pass_general.argtypes = ([vp, i64, i64] + [vp] * 6 + [i32, vp, vp, i32]
                                               + [vp] * 4 + [vp, sz, vp])
+    lib.cgtp_message_pass_fields.argtypes = lib.cgtp_message_pass_general.argtypes
     lib.cgtp_stage_times.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double), i32,
                                      ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.cgtp_destroy.argtypes = [vp]
@@ -351,6 +354,39 @@ def message_pass_general(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_
         _ptr(node_feat), _ptr(node_flip), nin, _ptr(U_E), _ptr(U_I), nout, _ptr(U_out_even),
         _ptr(U_out_odd), _ptr(outs[0]), _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)),
         "cgtp_message_pass_general")
+    return outs[0], outs[1]
+
+
+def message_pass_fields(plan: Plan, row_ptr, col, edge_feat, node_feat, U_E, U_I, U_out_even,
+                        U_out_odd, edge_flip=None, node_flip=None, out_even=None, out_odd=None,
+                        workspace=None, stream=None):
+    """cgtp_message_pass_fields (two parity-bearing fields). row_ptr [N+1], col [E] int32;
+    edge_feat, edge_flip [E, C, K]; node_feat, node_flip [N, C, K]; factors stacked as in
+    onsite_general."""
+    torch = _torch()
+    N = node_feat.shape[0]
+    E = col.shape[0]
+    L = plan.lmax + 1
+    _want(plan, "row_ptr", row_ptr, (N + 1,), torch.int32)
+    _want(plan, "col", col, (E,), torch.int32)
+    _want(plan, "edge_feat", edge_feat, (E, plan.channels, L * L))
+    if edge_flip is not None:
+        _want(plan, "edge_flip", edge_flip, edge_feat.shape)
+    _want(plan, "node_feat", node_feat, (N, plan.channels, L * L))
+    if node_flip is not None:
+        _want(plan, "node_flip", node_flip, node_feat.shape)
+    nin = _blocks(plan, "U_E", U_E, (1, 2, 4))
+    if _blocks(plan, "U_I", U_I, (1, 2, 4)) != nin:
+        raise ValueError("U_E and U_I must have the same number of blocks")
+    outs, nout = _outputs(plan, node_feat, out_even, out_odd, U_out_even, U_out_odd)
+    ws_ptr, ws_len = None, 0
+    if workspace is not None:
+        ws_ptr, ws_len = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(load_library().cgtp_message_pass_fields(
+        plan.handle, N, E, _ptr(row_ptr), _ptr(col), _ptr(edge_feat), _ptr(edge_flip),
+        _ptr(node_feat), _ptr(node_flip), nin, _ptr(U_E), _ptr(U_I), nout, _ptr(U_out_even),
+        _ptr(U_out_odd), _ptr(outs[0]), _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)),
+        "cgtp_message_pass_fields")
     return outs[0], outs[1]
 
 

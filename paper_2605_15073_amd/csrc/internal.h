@@ -118,6 +118,16 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
                            hipStream_t s);
 
+// Receiver pass for a general per-edge field (two parity-bearing fields): HE [E][R][K] are
+// the edge field's channel-contracted coefficients (edge e = row_ptr order), SF the sender
+// fields [N][R][3][UVs]; per receiver, the edge syntheses, products with the sender fields,
+// the sum over the CSR row and the inverse transforms into Ta, Tb [N][R][K].
+// hipErrorNotSupported when the LDS staging does not fit (fp64 at the highest degrees).
+template <typename T>
+hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int32_t *row_ptr,
+                                  const int32_t *col, const T *HE, const T *SF, T *Ta, T *Tb,
+                                  hipStream_t s);
+
 // fp32 folded inverse transforms (folded.hip), lmax <= 24; hipErrorNotSupported when
 // the LDS staging does not fit.
 hipError_t launch_analysis_folded(const Tabs<float> &tb, int64_t B, int R, const float *S,

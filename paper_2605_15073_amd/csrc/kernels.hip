@@ -543,6 +543,167 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
     analysis2(tb, qs, Sa, Sb, F /* Tm scratch, 2 MU */, Ta + br * d.K, Tb + br * d.K);
 }
 
+// Receiver for a general per-edge field (two parity-bearing fields, Eq. twoparity-phi):
+// the edge field no longer factors as R Y, so its channel-contracted coefficients
+// HE[e][r][K] go through the Legendre and Fourier syntheses (Eqs. msgpass-FI, msgpass-AI
+// and their derivative passes, applied on the edge side) and multiply the streamed sender
+// fields (Eqs. msgpass-S, cat-beta-curl). One workgroup per (receiver, RB ranks), one
+// thread per grid point (NPT points per thread). Per edge the RB ranks' coefficients are
+// staged in LDS and the Legendre stage F, dF/dx is shared through LDS; each thread then
+// forms the Fourier sums at its points and accumulates in registers. Blocks run rank
+// block by rank block, all receivers inside one, as in k_receiver_zonal.
+template <typename T, int RB, int NPT, bool FULL>
+__global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_fields(
+    Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    const T *__restrict__ HE, const T *__restrict__ SF, T *__restrict__ Ta, T *__restrict__ Tb)
+{
+    extern __shared__ unsigned char smem_raw[];
+    T *smem = reinterpret_cast<T *>(smem_raw);
+    const Dims &d = tb.d;
+    const int UV = d.UV, UVs = d.UVs, K = d.K, MU = d.M * d.U, lmax = d.lmax;
+    const int nrb = (R + RB - 1) / RB;
+    const int64_t NN = (int64_t)gridDim.x / nrb;
+    const int64_t c = blockIdx.x / NN;
+    const int64_t i = blockIdx.x - c * NN;
+    const int r0 = (int)c * RB;
+    const int nr = FULL ? RB : ((R - r0 < RB) ? (R - r0) : RB);
+    T *qs = smem;            // [V][M]
+    T *Hs = qs + d.V * d.M;  // [RB][K] this edge's coefficients
+    T *F = Hs + RB * K;      // [RB][M][U]
+    T *Fx = F + RB * MU;     // [RB][M][U]
+    stage_q(tb, qs);
+
+    int uvs[NPT], us[NPT], vs[NPT];
+#pragma unroll
+    for (int s = 0; s < NPT; ++s) {
+        const int uv = threadIdx.x + s * blockDim.x;
+        const int uvc = uv < UV ? uv : 0;
+        uvs[s] = uv;
+        us[s] = uvc / d.V;
+        vs[s] = uvc - us[s] * d.V;
+    }
+    T sa[NPT][RB], sb[NPT][RB];
+#pragma unroll
+    for (int s = 0; s < NPT; ++s)
+#pragma unroll
+        for (int q = 0; q < RB; ++q) sa[s][q] = sb[s][q] = 0;
+
+    const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
+    for (int e = e0; e < e1; ++e) {
+        const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
+        __syncthreads();  // the previous edge's F, Fx are consumed (and qs is staged)
+        const T *he = HE + ((int64_t)e * R + r0) * K;
+        for (int k = threadIdx.x; k < RB * K; k += blockDim.x) Hs[k] = k < nr * K ? he[k] : (T)0;
+        __syncthreads();
+        // Legendre stage of the RB ranks: F[q][mi][u] = sum_l Pt_l^|m|(x_u) HE[q][l, m]
+        for (int idx = threadIdx.x; idx < RB * MU; idx += blockDim.x) {
+            const int q = idx / MU, rem = idx - q * MU;
+            const int mi = rem / d.U, u = rem - mi * d.U;
+            const int m = mi - lmax, am = m < 0 ? -m : m;
+            const T *pu = tb.p + (size_t)u * d.P;
+            const T *dpu = tb.dp + (size_t)u * d.P;
+            const T *h = Hs + q * K;
+            T f = 0, fx = 0;
+            for (int l = am; l <= lmax; ++l) {
+                const T hv = h[l * l + l + m];
+                const int pi = l * (l + 1) / 2 + am;
+                f += pu[pi] * hv;
+                fx += dpu[pi] * hv;
+            }
+            F[idx] = f;
+            Fx[idx] = fx;
+        }
+        __syncthreads();
+        const T *sf = SF + (j * R + r0) * 3 * (int64_t)UVs;
+#pragma unroll
+        for (int s = 0; s < NPT; ++s) {
+            const int uv = uvs[s];
+            if (uv >= UV) continue;
+#pragma unroll
+            for (int q = 0; q < RB; ++q) {
+                if (!FULL && q >= nr) break;
+                T a, ax, ap;
+                fourier_point(tb, qs, F + q * MU, Fx + q * MU, us[s], vs[s], a, ax, ap);
+                const T *f = sf + (int64_t)q * 3 * UVs + uv;
+                sa[s][q] += a * f[0];
+                sb[s][q] += ap * f[UVs] - ax * f[2 * UVs];
+            }
+        }
+    }
+    // inverse transforms, one rank at a time through LDS (reusing the edge staging)
+    T *Sa = Hs;
+    T *Sb = Sa + UV;
+    T *Tm = Sb + UV;
+#pragma unroll
+    for (int q = 0; q < RB; ++q) {
+        if (q >= nr) break;
+        __syncthreads();
+#pragma unroll
+        for (int s = 0; s < NPT; ++s) {
+            if (uvs[s] < UV) {
+                Sa[uvs[s]] = sa[s][q];
+                Sb[uvs[s]] = sb[s][q];
+            }
+        }
+        __syncthreads();
+        const int64_t br = i * R + r0 + q;
+        analysis2(tb, qs, Sa, Sb, Tm, Ta + br * K, Tb + br * K);
+    }
+}
+
+template <typename T>
+hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int32_t *row_ptr,
+                                  const int32_t *col, const T *HE, const T *SF, T *Ta, T *Tb,
+                                  hipStream_t s)
+{
+    if (N == 0 || R == 0) return hipSuccess;
+    const Dims &d = tb.d;
+    const size_t MU = (size_t)d.M * d.U;
+    // ranks per block: the largest that keeps the LDS staging within 64 KiB (the analysis
+    // reuses the edge staging, 2 UV + 2 MU elements)
+    int rb = 0;
+    size_t sh = 0;
+    for (int cand : {8, 4, 2, 1}) {
+        const size_t stage = cand * ((size_t)d.K + 2 * MU);
+        const size_t need = sizeof(T) * ((size_t)d.V * d.M +
+                                         (stage > 2 * (size_t)d.UV + 2 * MU ? stage
+                                                                           : 2 * (size_t)d.UV + 2 * MU));
+        if (need <= 65536) {
+            rb = cand;
+            sh = need;
+            break;
+        }
+    }
+    if (rb == 0) return hipErrorNotSupported;
+    const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
+    if (npt > 3) return hipErrorNotSupported;
+    const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
+    const int64_t blocks = N * ((R + rb - 1) / rb);
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+#define CGTP_FIELDS(RBV, NP)                                                                   \
+    do {                                                                                       \
+        if (R % RBV == 0)                                                                      \
+            hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, true>), dim3((unsigned)blocks),  \
+                               dim3(threads), sh, s, tb, R, row_ptr, col, HE, SF, Ta, Tb);     \
+        else                                                                                   \
+            hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, false>), dim3((unsigned)blocks), \
+                               dim3(threads), sh, s, tb, R, row_ptr, col, HE, SF, Ta, Tb);     \
+    } while (0)
+#define CGTP_FIELDS_NP(RBV)                 \
+    do {                                    \
+        if (npt == 1) CGTP_FIELDS(RBV, 1);  \
+        else if (npt == 2) CGTP_FIELDS(RBV, 2); \
+        else CGTP_FIELDS(RBV, 3);           \
+    } while (0)
+    if (rb == 8) CGTP_FIELDS_NP(8);
+    else if (rb == 4) CGTP_FIELDS_NP(4);
+    else if (rb == 2) CGTP_FIELDS_NP(2);
+    else CGTP_FIELDS_NP(1);
+#undef CGTP_FIELDS_NP
+#undef CGTP_FIELDS
+    return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
@@ -600,7 +761,10 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                                               const T *, T *, T *, hipStream_t);                 \
     template hipError_t launch_receiver<T>(const Tabs<T> &, bool, int64_t, int, const int32_t *, \
                                            const int32_t *, const T *, const T *, const T *,     \
-                                           const T *, const T *, T *, T *, hipStream_t);
+                                           const T *, const T *, T *, T *, hipStream_t);         \
+    template hipError_t launch_receiver_fields<T>(const Tabs<T> &, int64_t, int, const int32_t *, \
+                                                  const int32_t *, const T *, const T *, T *, T *, \
+                                                  hipStream_t);
 
 CGTP_INSTANTIATE(float)
 CGTP_INSTANTIATE(double)

@@ -10,7 +10,7 @@
 
 namespace {
 constexpr int kMaxStages = 6;
-constexpr int kNumOps = 5;  // CGTP_OP_ONSITE .. CGTP_OP_MESSAGE_PASS_GENERAL
+constexpr int kNumOps = 6;  // CGTP_OP_ONSITE .. CGTP_OP_MESSAGE_PASS_FIELDS
 // HIP events bracketing the kernel stages of one call (CGTP_TIME_STAGES).
 struct EventSet {
     hipEvent_t ev[kMaxStages + 1];
@@ -125,6 +125,25 @@ Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = f
     l.hf = h;
     l.sff = sf;
     l.rtf = rt;
+    return l;
+}
+
+// Workspace of message passing with a general edge field: HI [N][R][K], SF [N][R][3][UVs],
+// HE [E][R][K], Ta, Tb [N][R][K].
+Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E)
+{
+    size_t es = p->dtype == CGTP_F64 ? 8 : 4;
+    size_t h = align256(es * (size_t)N * R * p->d.K);
+    size_t sf = align256(es * (size_t)N * R * 3 * p->d.UVs);
+    size_t he = align256(es * (size_t)E * R * p->d.K);
+    Layout l{};
+    l.off[0] = 0;
+    l.off[1] = h;
+    l.off[2] = h + sf;
+    l.off[3] = h + sf + he;
+    l.off[4] = l.off[3] + h;
+    l.off[5] = l.off[4] + h;
+    l.total = l.off[5];
     return l;
 }
 
@@ -619,6 +638,54 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
 }
 
+// Message passing with two parity-bearing fields (Eq. twoparity-phi): rank groups as for
+// the on-site contraction (slot pairs of the edge and node fields); the edge field's
+// coefficients are contracted per edge (the analogue of Eq. msgpass-HI on the edge side)
+// and synthesised on the grid inside the receiver.
+template <typename T>
+int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const int32_t *row_ptr,
+                  const int32_t *col, const void *const X1[2], const void *const X2[2],
+                  const Factors &f, void *oe, void *oo, char *ws, hipStream_t s)
+{
+    const cgtp::Dims &d = p->d;
+    const int C = p->C, R = p->R, Rg = G.n * R;
+    cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
+    Layout lay = mpf_layout(p, Rg, N, E);
+    T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
+    T *SF = reinterpret_cast<T *>(ws + lay.off[1]);
+    T *HE = reinterpret_cast<T *>(ws + lay.off[2]);
+    T *Ta = reinterpret_cast<T *>(ws + lay.off[3]);
+    T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
+    const int64_t hs = (int64_t)Rg * d.K;
+    StageRec rec;
+    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_FIELDS, 6, s);
+    if (st) return st;
+    hipError_t e;
+    for (int gi = 0; gi < G.n; ++gi) {
+        const Group &g = G.g[gi];
+        e = contract_in<T>(N, C, R, d.K, f.in2[group_block(g)], X2[g.s2],
+                           HI + (int64_t)gi * R * d.K, hs, s);
+        if (e != hipSuccess) return hip_fail(e, "contract node features");
+    }
+    rec.mark();
+    e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s);
+    if (e != hipSuccess) return hip_fail(e, "sender fields");
+    rec.mark();
+    for (int gi = 0; gi < G.n; ++gi) {
+        const Group &g = G.g[gi];
+        e = contract_in<T>(E, C, R, d.K, f.in1[group_block(g)], X1[g.s1],
+                           HE + (int64_t)gi * R * d.K, hs, s);
+        if (e != hipSuccess) return hip_fail(e, "contract edge field");
+    }
+    rec.mark();
+    e = cgtp::launch_receiver_fields<T>(tb, N, Rg, row_ptr, col, HE, SF, Ta, Tb, s);
+    if (e == hipErrorNotSupported)
+        return fail(CGTP_ERR_UNSUPPORTED, "edge-field receiver staging exceeds 64 KiB of LDS");
+    if (e != hipSuccess) return hip_fail(e, "receiver (edge field)");
+    rec.mark();
+    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+}
+
 // How a general call runs: on the fused single-group kernels when the factors are shared
 // and each output sector reads one set of weights, else through rank groups.
 struct GeneralRoute {
@@ -893,6 +960,9 @@ int cgtp_workspace_bytes_general(cgtp_plan plan, int op, int64_t n_nodes, int64_
         *bytes = route_onsite(plan, n_nodes, flips & 1, flips & 2, in_blocks).ws;
     else if (op == CGTP_OP_MESSAGE_PASS_GENERAL)
         *bytes = route_mp(plan, n_nodes, n_edges, flips & 2, in_blocks, out_blocks).ws;
+    else if (op == CGTP_OP_MESSAGE_PASS_FIELDS)
+        *bytes = mpf_layout(plan, make_groups(flips & 1, flips & 2, in_blocks, false).n * plan->R,
+                            n_nodes, n_edges).total;
     else return fail(CGTP_ERR_ARG, "unknown general op %d", op);
     return CGTP_OK;
 }
@@ -996,6 +1066,53 @@ int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                                 X2, f, out_even, out_odd, w, s);
 }
 
+int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
+                             const int32_t *row_ptr, const int32_t *col, const void *edge_feat,
+                             const void *edge_flip, const void *node_feat, const void *node_flip,
+                             int in_blocks, const void *U_E, const void *U_I, int out_blocks,
+                             const void *U_out_even, const void *U_out_odd, void *out_even,
+                             void *out_odd, void *workspace, size_t ws_bytes, void *stream)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
+    if (n_nodes < 0 || n_edges < 0) return fail(CGTP_ERR_ARG, "negative size");
+    if (n_edges >= 0x7fffffffLL) return fail(CGTP_ERR_ARG, "n_edges must be below 2^31 - 1");
+    if (!valid_blocks(in_blocks, out_blocks))
+        return fail(CGTP_ERR_ARG, "in_blocks %d / out_blocks %d invalid", in_blocks, out_blocks);
+    if (n_nodes == 0) {
+        if (n_edges != 0) return fail(CGTP_ERR_ARG, "edges without nodes");
+        return CGTP_OK;
+    }
+    if (!out_even && !out_odd) return fail(CGTP_ERR_ARG, "both outputs are NULL");
+    if (!row_ptr || !node_feat || !U_E || !U_I) return fail(CGTP_ERR_ARG, "NULL input");
+    if (n_edges > 0 && (!col || !edge_feat)) return fail(CGTP_ERR_ARG, "NULL edge input");
+    if ((out_even && !U_out_even) || (out_odd && !U_out_odd))
+        return fail(CGTP_ERR_ARG, "NULL output projection");
+    Groups G = make_groups(edge_flip != nullptr, node_flip != nullptr, in_blocks, false);
+    const int Rg = G.n * plan->R;
+    if ((n_nodes > n_edges ? n_nodes : n_edges) * (int64_t)Rg > 0x7fffffffLL)
+        return fail(CGTP_ERR_UNSUPPORTED, "rows * total rank exceeds 2^31 - 1");
+    int st = check_device(plan);
+    if (st) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (plan->flags & CGTP_VALIDATE_CSR) {
+        st = validate_csr(n_nodes, n_edges, row_ptr, col, s);
+        if (st) return st;
+    }
+    void *ws = nullptr;
+    st = get_workspace(plan, mpf_layout(plan, Rg, n_nodes, n_edges).total, workspace, ws_bytes,
+                       &ws);
+    if (st) return st;
+    Factors f = resolve_factors(plan, in_blocks, U_E, U_I, out_blocks, U_out_even, U_out_odd);
+    const void *X1[2] = {edge_feat, edge_flip}, *X2[2] = {node_feat, node_flip};
+    char *w = static_cast<char *>(ws);
+    if (plan->dtype == CGTP_F64)
+        return run_mp_fields<double>(plan, G, n_nodes, n_edges, row_ptr, col, X1, X2, f, out_even,
+                                     out_odd, w, s);
+    return run_mp_fields<float>(plan, G, n_nodes, n_edges, row_ptr, col, X1, X2, f, out_even,
+                                out_odd, w, s);
+}
+
 int cgtp_destroy(cgtp_plan plan)
 {
     if (!plan) return CGTP_OK;
@@ -1017,7 +1134,7 @@ int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages,
     int ns;
     if (op == CGTP_OP_ONSITE || op == CGTP_OP_ONSITE_GENERAL) ns = 5;
     else if (op == CGTP_OP_MESSAGE_PASS || op == CGTP_OP_MESSAGE_PASS_TWO_SLOT ||
-             op == CGTP_OP_MESSAGE_PASS_GENERAL)
+             op == CGTP_OP_MESSAGE_PASS_GENERAL || op == CGTP_OP_MESSAGE_PASS_FIELDS)
         ns = 6;
     else return fail(CGTP_ERR_ARG, "unknown op %d", op);
     int status = drain_timers(plan);

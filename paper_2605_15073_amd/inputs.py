@@ -22,7 +22,9 @@ performance"; no public dataset is involved):
   block N(0, 1/C), drawn from a second generator seeded seed + 7919 so the graph and the
   natural slots are those of the plain workload of the same seed.
 * Two parity-bearing fields: per-edge field coefficients [E][C][L^2] (and their flipped
-  slot) N(0, 1), with the factor blocks, from a third generator seeded seed + 104729.
+  slot) N(0, 1) drawn directly in fp32 from 64 PCG64 streams spawned from
+  SeedSequence(seed + 104729) (flipped slot: seed + 104730), each filling a fixed slice;
+  factor blocks from a generator seeded seed + 104731.
 """
 from __future__ import annotations
 
@@ -167,20 +169,44 @@ def general_mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, flip: 
     return d
 
 
+def normal_f32_streams(seed: int, shape, streams: int = 64) -> np.ndarray:
+    """N(0, 1) fp32 array filled from `streams` PCG64 generators spawned from
+    SeedSequence(seed), stream c filling the c-th of `streams` equal slices of the flattened
+    array. The values depend on seed, shape and streams only; the slices are filled by
+    parallel threads (numpy releases the GIL while it draws)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+
+    out = np.empty(shape, dtype=np.float32)
+    flat = out.reshape(-1)
+    kids = np.random.SeedSequence(seed).spawn(streams)
+    cuts = np.linspace(0, flat.size, streams + 1).astype(np.int64)
+
+    def fill(c):
+        np.random.default_rng(kids[c]).standard_normal(out=flat[cuts[c]:cuts[c + 1]],
+                                                       dtype=np.float32)
+
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(fill, range(streams)))
+    return out
+
+
 def fields_mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, edge_flip: bool = True,
                      node_flip: bool = True, in_blocks: int = 4, out_blocks: int = 2,
                      density: float = 0.1, r_cut: float = 5.0):
     """Message passing with two parity-bearing fields: the graph and node slots of mp_inputs
     with the same seed, and a per-edge field [E][C][L^2] (and its flipped slot) of N(0, 1)
-    coefficients in place of R Y. Draw order (a third generator, seed + 104729): edge_feat,
-    edge_flip (if present), U_E, U_I, U_out_even, U_out_odd."""
+    coefficients in place of R Y, drawn in fp32 by normal_f32_streams (seeds seed + 104729
+    and seed + 104730). The factor blocks come from a generator seeded seed + 104731, in the
+    order U_E, U_I, U_out_even, U_out_odd."""
     d = mp_inputs(n_atoms, lmax, C, R, seed, density=density, r_cut=r_cut, two_slot=node_flip)
     if not node_flip:
         d["node_flip"] = None
-    rng = np.random.default_rng(seed + 104729)
     E = d["n_edges"]
-    d["edge_feat"] = coefficients(rng, E, C, lmax, per_degree=False)
-    d["edge_flip"] = coefficients(rng, E, C, lmax, per_degree=False) if edge_flip else None
+    K = (lmax + 1) ** 2
+    d["edge_feat"] = normal_f32_streams(seed + 104729, (E, C, K))
+    d["edge_flip"] = normal_f32_streams(seed + 104730, (E, C, K)) if edge_flip else None
+    rng = np.random.default_rng(seed + 104731)
     d.update(_general_factors(rng, ("U_E", "U_I"), lmax, C, R, in_blocks, out_blocks))
     return d
 
@@ -249,4 +275,8 @@ WORKLOADS = {
     "onsiteg_n4096_l12_c128": Workload("onsiteg_n4096_l12_c128", "onsite", 4096, 12, 128, 128,
                                        seed=3, per_degree=True, two_slot=True, flip1=True,
                                        in_blocks=4, out_blocks=2),
+    # two parity-bearing fields (Eq. twoparity-phi): a per-edge field with both slots in place
+    # of R Y, both node slots, per-block factors
+    "mpf_5k_l6_c64": Workload("mpf_5k_l6_c64", "mp_fields", 5000, 6, 64, 64, seed=4,
+                              two_slot=True, flip1=True, in_blocks=4, out_blocks=2),
 }
