@@ -291,6 +291,166 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
     }
 }
 
+// ------------------------------------------------------ edge-field receiver (MP)
+
+// Ranks per workgroup of k_receiver_fields_mfma: one wave per 16-row tile of (rank, node u)
+// rows, at most 8 waves (so a lane may hold up to 256 registers).
+template <int LM>
+struct FieldsTiles {
+    using G = Grid<LM>;
+    static constexpr int RB = (128 / G::U) < 16 ? (128 / G::U) : 16;
+    static constexpr int KPT = 8;  // prefetched coefficients per thread and edge, at most
+};
+
+// Receiver for a general per-edge field (two parity-bearing fields, Eq. twoparity-phi):
+// a workgroup owns one receiver and rb ranks, one wave per 16-row tile of rows (rank q,
+// node u). Per edge each wave synthesises its rows of the edge field's grid fields exactly
+// as k_sender_mfma does for a node (the Legendre sums formed in the A-operand registers, the
+// Fourier product on MFMA; columns v) and each lane multiplies its D values, rows
+// 16 rt + 4 g + j at v = 16 t + n, with the sender fields at the same (q, u, v) (Eqs.
+// msgpass-S and cat-beta-curl; 16 lanes read 64 contiguous bytes of a row). A lane requests
+// its sender fields and its share of the next edge's coefficient rows when the edge starts,
+// so both arrive while it computes; the rows are double-buffered in LDS (one barrier per
+// edge). The products accumulate in registers over the CSR row; the sums go to
+// S [N][R][2][UVs] for k_analysis_mfma. Blocks run rank block by rank block, all receivers
+// inside one, so the memory-side cache serves a rank slice of the sender fields.
+template <int LM>
+__global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, int R, int rb,
+                                                               const int32_t *__restrict__ row_ptr,
+                                                               const int32_t *__restrict__ col,
+                                                               const float *__restrict__ HE,
+                                                               const float *__restrict__ SF,
+                                                               float *__restrict__ S)
+{
+    using G = Grid<LM>;
+    constexpr int KPT = FieldsTiles<LM>::KPT;
+    extern __shared__ float smem[];
+    float4_t *cf = reinterpret_cast<float4_t *>(smem);  // [P] recurrence coefficients
+    float *qs = smem + 4 * G::P;                         // [4 KM][QB]: q_vm as [m][v]
+    float *Hs = qs + 4 * G::KM * G::QB;                  // [2][rb][HR] this / the next edge
+    const int nrb = (R + rb - 1) / rb;
+    const int64_t NN = (int64_t)gridDim.x / nrb;
+    const int cb = (int)(blockIdx.x / NN);
+    const int64_t i = blockIdx.x - (int64_t)cb * NN;
+    const int r0 = cb * rb;
+    const int nr = (R - r0 < rb) ? (R - r0) : rb;
+    const int nh = nr * G::HR;  // staged elements of one edge
+    stage_q<LM>(tb, qs, 4 * G::KM, G::QB, false);
+    stage_coefs<LM>(tb, cf);
+
+    const int lane = threadIdx.x & 63, rt = threadIdx.x >> 6;  // this wave's row tile
+    const int g4 = lane >> 4, n = lane & 15;
+    const int rows = nr * G::U;
+    // this lane's A row (qa, ua) and its Legendre seeds; its four D rows 16 rt + 4 g + j
+    const int ra = rt * 16 + n;
+    const int qa = ra < rows ? ra / G::U : 0, ua = ra < rows ? ra - qa * G::U : 0;
+    float seed[G::KM];
+    load_seeds<LM>(tb, g4, ua, seed);
+    const float sxu = tb.sx[ua];
+    LaneRows<LM, 1> c;
+    c.cf = cf;
+    c.seed = seed;
+    c.x = tb.x[ua];
+    c.r = 1.f / (sxu * sxu);
+    c.g4 = g4;
+    int off[4];  // offset of D row j in a sender's rank block [rb][3][UVs], -1 if none
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int ro = rt * 16 + 4 * g4 + j;
+        const int qo = ro / G::U, uo = ro - qo * G::U;
+        off[j] = ro < rows ? qo * 3 * G::UVs + uo * G::V : -1;
+    }
+    float4_t sa[G::VT], sb[G::VT];
+#pragma unroll
+    for (int t = 0; t < G::VT; ++t) sa[t] = sb[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+    // staging of a margin-padded coefficient row element k = q HR + HL + i of an edge
+    auto coef = [&](const float *he, int k) -> float {
+        const int q = k / G::HR, ii = k - q * G::HR - G::HL;
+        return (k < nh && ii >= 0 && ii < G::K) ? he[q * G::K + ii] : 0.f;
+    };
+    const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
+    if (e0 < e1) {
+        const float *he = HE + ((int64_t)e0 * R + r0) * G::K;
+        for (int k = threadIdx.x; k < nh; k += blockDim.x) Hs[k] = coef(he, k);
+    }
+    __syncthreads();
+    for (int e = e0; e < e1; ++e) {
+        const int cur = (e - e0) & 1;
+        const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
+        // this edge's sender fields at the lane's D rows and columns
+        const float *sfj = SF + (j * R + r0) * 3 * (int64_t)G::UVs;
+        float fI[G::VT][4], fX[G::VT][4], fP[G::VT][4];
+#pragma unroll
+        for (int t = 0; t < G::VT; ++t) {
+            const int v = t * 16 + n;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const bool ok = off[jj] >= 0 && v < G::V;
+                const float *f = sfj + (ok ? off[jj] + v : 0);
+                fI[t][jj] = ok ? f[0] : 0.f;
+                fX[t][jj] = ok ? f[G::UVs] : 0.f;
+                fP[t][jj] = ok ? f[2 * G::UVs] : 0.f;
+            }
+        }
+        // the next edge's coefficient rows, stored after this edge's Legendre pass
+        float hn[KPT];
+        const bool more = e + 1 < e1;
+        if (more) {
+            const float *he = HE + ((int64_t)(e + 1) * R + r0) * G::K;
+#pragma unroll
+            for (int t = 0; t < KPT; ++t) hn[t] = coef(he, threadIdx.x + t * blockDim.x);
+        }
+        if (rt * 16 < rows) {  // wave-uniform: waves past the last tile only help stage rows
+            c.h[0] = Hs + cur * rb * G::HR + qa * G::HR + G::HL;
+            float bf[G::KM][1][3];
+            legendre_all<LM, 1, 0>(c, bf);
+#pragma unroll
+            for (int t = 0; t < G::VT; ++t) {
+                float4_t acc[3] = {float4_t{0.f, 0.f, 0.f, 0.f}, float4_t{0.f, 0.f, 0.f, 0.f},
+                                   float4_t{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+                for (int kk = 0; kk < G::KM; ++kk) {
+                    const float bq = qs[(4 * kk + g4) * G::QB + t * 16 + n];
+#pragma unroll
+                    for (int f = 0; f < 3; ++f)
+                        acc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[kk][0][f], bq, acc[f], 0,
+                                                                      0, 0);
+                }
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    sa[t][jj] += acc[0][jj] * fI[t][jj];
+                    sb[t][jj] += acc[2][jj] * fX[t][jj] - acc[1][jj] * fP[t][jj];
+                }
+            }
+        }
+        if (more) {
+            float *hnext = Hs + (cur ^ 1) * rb * G::HR;
+#pragma unroll
+            for (int t = 0; t < KPT; ++t) {
+                const int k = threadIdx.x + t * blockDim.x;
+                if (k < nh) hnext[k] = hn[t];
+            }
+        }
+        __syncthreads();  // the next rows are staged; this edge's rows are consumed
+    }
+    float *Sr = S + (i * R + r0) * 2 * (int64_t)G::UVs;
+#pragma unroll
+    for (int t = 0; t < G::VT; ++t) {
+        const int v = t * 16 + n;
+        if (v >= G::V) continue;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            if (off[jj] < 0) continue;
+            const int ro = rt * 16 + 4 * g4 + jj;
+            const int qo = ro / G::U, uo = ro - qo * G::U;
+            float *o = Sr + qo * 2 * G::UVs + uo * G::V + v;
+            o[0] = sa[t][jj];
+            o[G::UVs] = sb[t][jj];
+        }
+    }
+}
+
 // ------------------------------------------------------ inverse transforms (MP)
 
 template <int LM>
@@ -610,6 +770,49 @@ hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
 #undef CGTP_CASE
     default: return hipErrorNotSupported;
     }
+}
+
+template <int LM>
+hipError_t receiver_fields_lm(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
+                              const int32_t *col, const float *HE, const float *SF, float *S,
+                              hipStream_t s)
+{
+    using G = Grid<LM>;
+    int rb = FieldsTiles<LM>::RB;
+    if (rb > R) rb = R;
+    if (rb < 1) return hipErrorNotSupported;
+    const int waves = (rb * G::U + 15) / 16;
+    // every staged row element is fetched by some thread's prefetch
+    if ((size_t)rb * G::HR > (size_t)FieldsTiles<LM>::KPT * 64 * waves) return hipErrorNotSupported;
+    const size_t sh = sizeof(float) * (4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB +
+                                       2 * (size_t)rb * G::HR);
+    if (sh > 65536) return hipErrorNotSupported;
+    const int64_t blocks = N * ((R + rb - 1) / rb);
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_receiver_fields_mfma<LM>), dim3((unsigned)blocks), dim3(64 * waves), sh,
+                       s, tb, R, rb, row_ptr, col, HE, SF, S);
+    return hipGetLastError();
+}
+
+hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
+                                       const int32_t *row_ptr, const int32_t *col,
+                                       const float *HE, const float *SF, float *S, float *Ta,
+                                       float *Tb, hipStream_t s)
+{
+    if (N == 0) return hipSuccess;
+    if (!sender_mfma_supported(tb.d)) return hipErrorNotSupported;
+    hipError_t e = hipErrorNotSupported;
+    switch (tb.d.lmax) {
+#define CGTP_CASE(LMV) \
+    case LMV: e = receiver_fields_lm<LMV>(tb, N, R, row_ptr, col, HE, SF, S, s); break;
+        CGTP_LMAX_CASES(CGTP_CASE)
+#undef CGTP_CASE
+    default: return hipErrorNotSupported;
+    }
+    if (e != hipSuccess) return e;
+    e = launch_analysis_mfma(tb, N, R, S, Ta, Tb, s);
+    if (e != hipErrorNotSupported) return e;
+    return launch_analysis_folded(tb, N, R, S, Ta, Tb, s);
 }
 
 hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const float *HA,

@@ -128,6 +128,14 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
                                   const int32_t *col, const T *HE, const T *SF, T *Ta, T *Tb,
                                   hipStream_t s);
 
+// fp32 edge-field receiver on MFMA (fourier_mfma.hip), default grid: the summed grid fields
+// go to S [N][R][2][UVs] and the inverse transforms into Ta, Tb follow. SF in the layout
+// [N][R][3][UVs]. hipErrorNotSupported off the default grid.
+hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
+                                       const int32_t *row_ptr, const int32_t *col,
+                                       const float *HE, const float *SF, float *S, float *Ta,
+                                       float *Tb, hipStream_t s);
+
 // fp32 folded inverse transforms (folded.hip), lmax <= 24; hipErrorNotSupported when
 // the LDS staging does not fit.
 hipError_t launch_analysis_folded(const Tabs<float> &tb, int64_t B, int R, const float *S,

@@ -548,11 +548,16 @@ __global__ __launch_bounds__(kThreads) void k_receiver_separated(
 // HE[e][r][K] go through the Legendre and Fourier syntheses (Eqs. msgpass-FI, msgpass-AI
 // and their derivative passes, applied on the edge side) and multiply the streamed sender
 // fields (Eqs. msgpass-S, cat-beta-curl). One workgroup per (receiver, RB ranks), one
-// thread per grid point (NPT points per thread). Per edge the RB ranks' coefficients are
-// staged in LDS and the Legendre stage F, dF/dx is shared through LDS; each thread then
-// forms the Fourier sums at its points and accumulates in registers. Blocks run rank
-// block by rank block, all receivers inside one, as in k_receiver_zonal.
-template <typename T, int RB, int NPT, bool FULL>
+// thread per grid point (NPT points per thread). Per edge the RB ranks' coefficients sit in
+// LDS (double-buffered: the next edge's are loaded while this one is transformed), the
+// Legendre stage F, dF/dx is shared through LDS (with the Legendre tables in LDS when LT),
+// and each thread forms the Fourier sums at its points and accumulates in registers. The
+// sender fields of an edge are requested before its Legendre stage, so their latency is
+// hidden behind it. Blocks run rank block by rank block, all receivers inside one, as in
+// k_receiver_zonal.
+constexpr int kFieldsKpt = 8;  // staged coefficients per thread and edge, at most
+
+template <typename T, int RB, int NPT, bool FULL, bool LT>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_fields(
     Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
     const T *__restrict__ HE, const T *__restrict__ SF, T *__restrict__ Ta, T *__restrict__ Tb)
@@ -560,18 +565,29 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_fields(
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
     const Dims &d = tb.d;
-    const int UV = d.UV, UVs = d.UVs, K = d.K, MU = d.M * d.U, lmax = d.lmax;
+    const int UV = d.UV, UVs = d.UVs, K = d.K, MU = d.M * d.U, lmax = d.lmax, P = d.P;
     const int nrb = (R + RB - 1) / RB;
     const int64_t NN = (int64_t)gridDim.x / nrb;
     const int64_t c = blockIdx.x / NN;
     const int64_t i = blockIdx.x - c * NN;
     const int r0 = (int)c * RB;
     const int nr = FULL ? RB : ((R - r0 < RB) ? (R - r0) : RB);
-    T *qs = smem;            // [V][M]
-    T *Hs = qs + d.V * d.M;  // [RB][K] this edge's coefficients
-    T *F = Hs + RB * K;      // [RB][M][U]
-    T *Fx = F + RB * MU;     // [RB][M][U]
+    const int nk = nr * K;  // staged coefficients of one edge
+    T *qs = smem;                        // [V][M]
+    T *Pt = qs + d.V * d.M;              // LT: [U][P] Pt_l^m(x_u), then [U][P] dPt/dx
+    T *Dt = Pt + (LT ? d.U * P : 0);
+    T *Hs = Dt + (LT ? d.U * P : 0);     // [2][RB][K] coefficients of this / the next edge
+    T *F = Hs + 2 * RB * K;              // [RB][M][U]
+    T *Fx = F + RB * MU;                 // [RB][M][U]
     stage_q(tb, qs);
+    if (LT) {
+        for (int k = threadIdx.x; k < d.U * P; k += blockDim.x) {
+            Pt[k] = tb.p[k];
+            Dt[k] = tb.dp[k];
+        }
+    }
+    const T *ptab = LT ? Pt : tb.p;
+    const T *dtab = LT ? Dt : tb.dp;
 
     int uvs[NPT], us[NPT], vs[NPT];
 #pragma unroll
@@ -589,44 +605,80 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_fields(
         for (int q = 0; q < RB; ++q) sa[s][q] = sb[s][q] = 0;
 
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
+    if (e0 < e1) {
+        const T *he = HE + ((int64_t)e0 * R + r0) * K;
+        for (int k = threadIdx.x; k < nk; k += blockDim.x) Hs[k] = he[k];
+    }
     for (int e = e0; e < e1; ++e) {
+        const int cur = (e - e0) & 1;
+        __syncthreads();  // this edge's coefficients are staged; the previous F is consumed
         const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
-        __syncthreads();  // the previous edge's F, Fx are consumed (and qs is staged)
-        const T *he = HE + ((int64_t)e * R + r0) * K;
-        for (int k = threadIdx.x; k < RB * K; k += blockDim.x) Hs[k] = k < nr * K ? he[k] : (T)0;
-        __syncthreads();
+        // this edge's sender fields, consumed after the Legendre stage
+        T fI[NPT][RB], fX[NPT][RB], fP[NPT][RB];
+        const T *sf = SF + (j * R + r0) * 3 * (int64_t)UVs;
+#pragma unroll
+        for (int s = 0; s < NPT; ++s) {
+            const int uvc = uvs[s] < UV ? uvs[s] : 0;
+#pragma unroll
+            for (int q = 0; q < RB; ++q) {
+                const bool ok = FULL || q < nr;
+                const T *f = sf + (int64_t)(ok ? q : 0) * 3 * UVs + uvc;
+                fI[s][q] = ok ? f[0] : (T)0;
+                fX[s][q] = ok ? f[UVs] : (T)0;
+                fP[s][q] = ok ? f[2 * UVs] : (T)0;
+            }
+        }
+        // the next edge's coefficients, stored after the Legendre stage
+        T hn[kFieldsKpt];
+        const bool more = e + 1 < e1;
+        if (more) {
+            const T *he = HE + ((int64_t)(e + 1) * R + r0) * K;
+#pragma unroll
+            for (int t = 0; t < kFieldsKpt; ++t) {
+                const int k = threadIdx.x + t * blockDim.x;
+                hn[t] = k < nk ? he[k] : (T)0;
+            }
+        }
         // Legendre stage of the RB ranks: F[q][mi][u] = sum_l Pt_l^|m|(x_u) HE[q][l, m]
+        const T *hc = Hs + cur * RB * K;
         for (int idx = threadIdx.x; idx < RB * MU; idx += blockDim.x) {
             const int q = idx / MU, rem = idx - q * MU;
             const int mi = rem / d.U, u = rem - mi * d.U;
             const int m = mi - lmax, am = m < 0 ? -m : m;
-            const T *pu = tb.p + (size_t)u * d.P;
-            const T *dpu = tb.dp + (size_t)u * d.P;
-            const T *h = Hs + q * K;
+            const T *pu = ptab + u * P;
+            const T *dpu = dtab + u * P;
+            const T *h = hc + q * K;
             T f = 0, fx = 0;
-            for (int l = am; l <= lmax; ++l) {
-                const T hv = h[l * l + l + m];
-                const int pi = l * (l + 1) / 2 + am;
-                f += pu[pi] * hv;
-                fx += dpu[pi] * hv;
+            if (FULL || q < nr) {
+                for (int l = am; l <= lmax; ++l) {
+                    const T hv = h[l * l + l + m];
+                    const int pi = l * (l + 1) / 2 + am;
+                    f += pu[pi] * hv;
+                    fx += dpu[pi] * hv;
+                }
             }
             F[idx] = f;
             Fx[idx] = fx;
         }
+        if (more) {
+            T *hnext = Hs + (cur ^ 1) * RB * K;
+#pragma unroll
+            for (int t = 0; t < kFieldsKpt; ++t) {
+                const int k = threadIdx.x + t * blockDim.x;
+                if (k < nk) hnext[k] = hn[t];
+            }
+        }
         __syncthreads();
-        const T *sf = SF + (j * R + r0) * 3 * (int64_t)UVs;
 #pragma unroll
         for (int s = 0; s < NPT; ++s) {
-            const int uv = uvs[s];
-            if (uv >= UV) continue;
+            if (uvs[s] >= UV) continue;
 #pragma unroll
             for (int q = 0; q < RB; ++q) {
                 if (!FULL && q >= nr) break;
                 T a, ax, ap;
                 fourier_point(tb, qs, F + q * MU, Fx + q * MU, us[s], vs[s], a, ax, ap);
-                const T *f = sf + (int64_t)q * 3 * UVs + uv;
-                sa[s][q] += a * f[0];
-                sb[s][q] += ap * f[UVs] - ax * f[2 * UVs];
+                sa[s][q] += a * fI[s][q];
+                sb[s][q] += ap * fX[s][q] - ax * fP[s][q];
             }
         }
     }
@@ -659,47 +711,60 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
     if (N == 0 || R == 0) return hipSuccess;
     const Dims &d = tb.d;
     const size_t MU = (size_t)d.M * d.U;
-    // ranks per block: the largest that keeps the LDS staging within 64 KiB (the analysis
-    // reuses the edge staging, 2 UV + 2 MU elements)
+    const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
+    if (npt > 3) return hipErrorNotSupported;
+    const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
+    // ranks per block and table staging: the largest RB whose registers (five values per
+    // rank and point) and LDS (at most 64 KiB; the analysis reuses the edge staging, 2 UV +
+    // 2 MU elements) fit, with the Legendre tables in LDS when they fit too
+    const size_t analysis = 2 * (size_t)d.UV + 2 * MU;
     int rb = 0;
+    bool lt = false;
     size_t sh = 0;
-    for (int cand : {8, 4, 2, 1}) {
-        const size_t stage = cand * ((size_t)d.K + 2 * MU);
-        const size_t need = sizeof(T) * ((size_t)d.V * d.M +
-                                         (stage > 2 * (size_t)d.UV + 2 * MU ? stage
-                                                                           : 2 * (size_t)d.UV + 2 * MU));
-        if (need <= 65536) {
-            rb = cand;
-            sh = need;
+    // (at most two ranks per thread: the per-point Fourier sums keep about 60 registers live
+    // per rank and the 1024-thread bound leaves 128)
+    for (int cand : {2, 1}) {
+        if (cand * npt > 2 || (size_t)cand * d.K > (size_t)kFieldsKpt * threads) continue;
+        const size_t stage = cand * (2 * (size_t)d.K + 2 * MU);
+        const size_t base = (size_t)d.V * d.M + (stage > analysis ? stage : analysis);
+        const size_t tabs = 2 * (size_t)d.U * d.P;
+        if (sizeof(T) * (base + tabs) <= 65536) {
+            rb = cand, lt = true, sh = sizeof(T) * (base + tabs);
+            break;
+        }
+        if (sizeof(T) * base <= 65536) {
+            rb = cand, lt = false, sh = sizeof(T) * base;
             break;
         }
     }
     if (rb == 0) return hipErrorNotSupported;
-    const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
-    if (npt > 3) return hipErrorNotSupported;
-    const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
     const int64_t blocks = N * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-#define CGTP_FIELDS(RBV, NP)                                                                   \
+#define CGTP_FIELDS(RBV, NP, LTV)                                                              \
     do {                                                                                       \
         if (R % RBV == 0)                                                                      \
-            hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, true>), dim3((unsigned)blocks),  \
-                               dim3(threads), sh, s, tb, R, row_ptr, col, HE, SF, Ta, Tb);     \
+            hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, true, LTV>),                     \
+                               dim3((unsigned)blocks), dim3(threads), sh, s, tb, R, row_ptr,   \
+                               col, HE, SF, Ta, Tb);                                           \
         else                                                                                   \
-            hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, false>), dim3((unsigned)blocks), \
-                               dim3(threads), sh, s, tb, R, row_ptr, col, HE, SF, Ta, Tb);     \
+            hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, false, LTV>),                    \
+                               dim3((unsigned)blocks), dim3(threads), sh, s, tb, R, row_ptr,   \
+                               col, HE, SF, Ta, Tb);                                           \
     } while (0)
-#define CGTP_FIELDS_NP(RBV)                 \
-    do {                                    \
-        if (npt == 1) CGTP_FIELDS(RBV, 1);  \
-        else if (npt == 2) CGTP_FIELDS(RBV, 2); \
-        else CGTP_FIELDS(RBV, 3);           \
+#define CGTP_FIELDS_LT(RBV, NP)                          \
+    do {                                                 \
+        if (lt) CGTP_FIELDS(RBV, NP, true);              \
+        else CGTP_FIELDS(RBV, NP, false);                \
     } while (0)
-    if (rb == 8) CGTP_FIELDS_NP(8);
-    else if (rb == 4) CGTP_FIELDS_NP(4);
-    else if (rb == 2) CGTP_FIELDS_NP(2);
-    else CGTP_FIELDS_NP(1);
-#undef CGTP_FIELDS_NP
+    if (npt == 1) {
+        if (rb == 2) CGTP_FIELDS_LT(2, 1);
+        else CGTP_FIELDS_LT(1, 1);
+    } else if (npt == 2) {
+        CGTP_FIELDS_LT(1, 2);
+    } else {
+        CGTP_FIELDS_LT(1, 3);
+    }
+#undef CGTP_FIELDS_LT
 #undef CGTP_FIELDS
     return hipGetLastError();
 }

@@ -128,14 +128,22 @@ Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = f
     return l;
 }
 
+// The edge-field receiver on MFMA (fp32, default grid) writes the summed grid fields
+// S [N][R][2][UVs] before the inverse transforms.
+bool use_mfma_fields(const cgtp_plan_s *p)
+{
+    return p->dtype == CGTP_F32 && cgtp::sender_mfma_supported(p->d);
+}
+
 // Workspace of message passing with a general edge field: HI [N][R][K], SF [N][R][3][UVs],
-// HE [E][R][K], Ta, Tb [N][R][K].
+// HE [E][R][K], Ta, Tb [N][R][K], and S [N][R][2][UVs] for the MFMA receiver.
 Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
     size_t h = align256(es * (size_t)N * R * p->d.K);
     size_t sf = align256(es * (size_t)N * R * 3 * p->d.UVs);
     size_t he = align256(es * (size_t)E * R * p->d.K);
+    size_t sg = use_mfma_fields(p) ? align256(es * (size_t)N * R * 2 * p->d.UVs) : 0;
     Layout l{};
     l.off[0] = 0;
     l.off[1] = h;
@@ -143,7 +151,7 @@ Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E)
     l.off[3] = h + sf + he;
     l.off[4] = l.off[3] + h;
     l.off[5] = l.off[4] + h;
-    l.total = l.off[5];
+    l.total = l.off[5] + sg;
     return l;
 }
 
@@ -678,6 +686,15 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
         if (e != hipSuccess) return hip_fail(e, "contract edge field");
     }
     rec.mark();
+    if constexpr (sizeof(T) == 4) {
+        if (use_mfma_fields(p)) {
+            float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
+            e = cgtp::launch_receiver_fields_mfma(tb, N, Rg, row_ptr, col, HE, SF, Sg, Ta, Tb, s);
+            if (e != hipSuccess) return hip_fail(e, "receiver (edge field, mfma)");
+            rec.mark();
+            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+        }
+    }
     e = cgtp::launch_receiver_fields<T>(tb, N, Rg, row_ptr, col, HE, SF, Ta, Tb, s);
     if (e == hipErrorNotSupported)
         return fail(CGTP_ERR_UNSUPPORTED, "edge-field receiver staging exceeds 64 KiB of LDS");
