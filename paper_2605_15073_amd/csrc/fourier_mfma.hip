@@ -294,11 +294,12 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
 // ------------------------------------------------------ edge-field receiver (MP)
 
 // Ranks per workgroup of k_receiver_fields_mfma: one wave per 16-row tile of (rank, node u)
-// rows, at most 8 waves (so a lane may hold up to 256 registers).
+// rows, at most 4 waves, so that several workgroups share a CU and one waiting at its
+// per-edge barrier leaves the others running.
 template <int LM>
 struct FieldsTiles {
     using G = Grid<LM>;
-    static constexpr int RB = (128 / G::U) < 16 ? (128 / G::U) : 16;
+    static constexpr int RB = (64 / G::U) < 1 ? 1 : ((64 / G::U) < 16 ? (64 / G::U) : 16);
     static constexpr int KPT = 8;  // prefetched coefficients per thread and edge, at most
 };
 
