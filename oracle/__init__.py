@@ -59,6 +59,8 @@ def _load():
     lib.cgo_onsite.argtypes = [i32, i32, i32, i64] + [p] * 9 + [i32]
     lib.cgo_message_pass.restype = i32
     lib.cgo_message_pass.argtypes = [i32, i32, i32, i64, i64] + [p] * 9 + [p, i64, p, p, i32]
+    lib.cgo_nbody.restype = i32
+    lib.cgo_nbody.argtypes = [i32, i32, i32, i32, i64, p, p, p, p, i32]
     lib.cgo_message_pass_fields.restype = i32
     lib.cgo_message_pass_fields.argtypes = ([i32, i32, i32, i64, i64] + [p] * 9
                                             + [p, i64, p, p, i32])
@@ -364,3 +366,27 @@ def _mpf_rows(lmax, row_ptr, col, edge_feat, edge_flip, node_feat, node_flip, U_
     if rc != 0:
         raise RuntimeError(f"cgo_message_pass_fields failed ({rc})")
     return oe, oo
+
+
+def nbody(lmax, X, U, U_out, nthreads: int = 0):
+    """nu-body on-site product, fp64: X, U lists of nu arrays [N, C, L^2] and [L, C, R];
+    U_out [L, C, R]. Returns out [N, C, L^2] (natural parity)."""
+    lib = _load()
+    nu = len(X)
+    assert nu == len(U) and nu >= 1
+    Xs = [_f64(x) for x in X]
+    Us = [_f64(u) for u in U]
+    Uo = _f64(U_out)
+    N, C, L2 = Xs[0].shape
+    R = Us[0].shape[2]
+    assert L2 == (lmax + 1) ** 2
+    for x in Xs:
+        assert x.shape == (N, C, L2)
+    for u in Us + [Uo]:
+        assert u.shape == (lmax + 1, C, R)
+    kx, ku = _ptr_array(Xs), _ptr_array(Us)
+    out = np.zeros((N, C, L2))
+    rc = lib.cgo_nbody(lmax, C, R, nu, N, kx[1], ku[1], _ptr(Uo), _ptr(out), int(nthreads))
+    if rc != 0:
+        raise RuntimeError(f"cgo_nbody failed ({rc})")
+    return out

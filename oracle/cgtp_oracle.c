@@ -233,11 +233,11 @@ double cgo_real_entry(int kind, int l1, int m1, int l2, int m2, int l3, int m3, 
 }
 
 /* Entries of one l1 block, appended at arrays + n (count only when val is NULL). */
-static long real_table_block(int kind, int l1, int lmax_in, int lmax_out, int32_t *k1,
+static long real_table_block(int kind, int l1, int l2max, int lmax_out, int32_t *k1,
                              int32_t *k2, int32_t *k3, double *val, long n, long double *worst_im)
 {
     for (int m1 = -l1; m1 <= l1; ++m1)
-        for (int l2 = 0; l2 <= lmax_in; ++l2)
+        for (int l2 = 0; l2 <= l2max; ++l2)
             for (int m2 = -l2; m2 <= l2; ++m2)
                 for (int l3 = abs(l1 - l2); l3 <= imin(l1 + l2, lmax_out); ++l3)
                     for (int m3 = -l3; m3 <= l3; ++m3) {
@@ -266,24 +266,25 @@ static long real_table_block(int kind, int l1, int lmax_in, int lmax_out, int32_
  * entry up to lmax = 20 is above 9e-7, so the cut only removes residue. When
  * arrays are NULL (or cap is short) only the count is returned. max_imag receives the largest
  * |Im| seen (must be ~0: the real-basis tables are real). */
-long cgo_real_table(int kind, int lmax_in, int lmax_out, int32_t *k1, int32_t *k2, int32_t *k3,
-                    double *val, long cap, double *max_imag)
+/* Entries with l1 <= l1max, l2 <= l2max and l3 <= lmax_out (see cgo_real_table). */
+static long real_table(int kind, int l1max, int l2max, int lmax_out, int32_t *k1, int32_t *k2,
+                       int32_t *k3, double *val, long cap, double *max_imag)
 {
     init_fact();
     long counts[ORC_MAXJ + 1];
     long double worst[ORC_MAXJ + 1];
-    if (lmax_in > ORC_MAXJ) return -1;
+    if (l1max > ORC_MAXJ || l2max > ORC_MAXJ || lmax_out > ORC_MAXJ) return -1;
     /* pass 1: entries per l1 block (blocks are independent) */
 #pragma omp parallel for schedule(dynamic, 1)
-    for (int l1 = 0; l1 <= lmax_in; ++l1) {
+    for (int l1 = 0; l1 <= l1max; ++l1) {
         worst[l1] = 0.0L;
-        counts[l1] = real_table_block(kind, l1, lmax_in, lmax_out, NULL, NULL, NULL, NULL, 0,
+        counts[l1] = real_table_block(kind, l1, l2max, lmax_out, NULL, NULL, NULL, NULL, 0,
                                       &worst[l1]);
     }
     long total = 0;
     long start[ORC_MAXJ + 1];
     long double worst_im = 0.0L;
-    for (int l1 = 0; l1 <= lmax_in; ++l1) {
+    for (int l1 = 0; l1 <= l1max; ++l1) {
         start[l1] = total;
         total += counts[l1];
         if (worst[l1] > worst_im) worst_im = worst[l1];
@@ -291,13 +292,26 @@ long cgo_real_table(int kind, int lmax_in, int lmax_out, int32_t *k1, int32_t *k
     /* pass 2: fill each block at its offset, in the same (l1, m1, l2, m2, l3, m3) order */
     if (val && cap >= total) {
 #pragma omp parallel for schedule(dynamic, 1)
-        for (int l1 = 0; l1 <= lmax_in; ++l1) {
+        for (int l1 = 0; l1 <= l1max; ++l1) {
             long double w = 0.0L;
-            real_table_block(kind, l1, lmax_in, lmax_out, k1, k2, k3, val, start[l1], &w);
+            real_table_block(kind, l1, l2max, lmax_out, k1, k2, k3, val, start[l1], &w);
         }
     }
     if (max_imag) *max_imag = (double)worst_im;
     return total;
+}
+
+/* Sparse real table over all k1, k2 <= lmax_in and k3 <= lmax_out:
+ * entries (k1, k2, k3, value) with |value| > 1e-12. Entries that vanish exactly
+ * (e.g. an odd number of sine factors under the phi integral) come out of the
+ * unitary sum as cancellation residue of at most ~1e-15, while every genuine
+ * entry up to lmax = 20 is above 9e-7, so the cut only removes residue. When
+ * arrays are NULL (or cap is short) only the count is returned. max_imag receives the largest
+ * |Im| seen (must be ~0: the real-basis tables are real). */
+long cgo_real_table(int kind, int lmax_in, int lmax_out, int32_t *k1, int32_t *k2, int32_t *k3,
+                    double *val, long cap, double *max_imag)
+{
+    return real_table(kind, lmax_in, lmax_in, lmax_out, k1, k2, k3, val, cap, max_imag);
 }
 
 /* Real spherical harmonics of App. C, Eq. realY, in the direction of (x, y, z):
@@ -347,17 +361,23 @@ typedef struct {
     double *v;
 } sparse_tab;
 
-static int build_tab(int kind, int lmax, sparse_tab *t)
+static int build_tab3(int kind, int l1max, int l2max, int lomax, sparse_tab *t)
 {
-    t->n = cgo_real_table(kind, lmax, lmax, NULL, NULL, NULL, NULL, 0, NULL);
+    t->n = real_table(kind, l1max, l2max, lomax, NULL, NULL, NULL, NULL, 0, NULL);
+    if (t->n < 0) return -1;
     long n = t->n > 0 ? t->n : 1;
     t->k1 = (int32_t *)malloc(sizeof(int32_t) * n);
     t->k2 = (int32_t *)malloc(sizeof(int32_t) * n);
     t->k3 = (int32_t *)malloc(sizeof(int32_t) * n);
     t->v = (double *)malloc(sizeof(double) * n);
     if (!t->k1 || !t->k2 || !t->k3 || !t->v) return -1;
-    cgo_real_table(kind, lmax, lmax, t->k1, t->k2, t->k3, t->v, t->n, NULL);
+    real_table(kind, l1max, l2max, lomax, t->k1, t->k2, t->k3, t->v, t->n, NULL);
     return 0;
+}
+
+static int build_tab(int kind, int lmax, sparse_tab *t)
+{
+    return build_tab3(kind, lmax, lmax, lmax, t);
 }
 
 static void free_tab(sparse_tab *t)
@@ -691,6 +711,70 @@ int cgo_message_pass_fields(int lmax, int C, int R, long n_nodes, long n_edges,
     if (!err) project_blocks(lmax, C, R, n_recv, U_out, T, live, out_even, out_odd);
     for (int b = 0; b < CGO_NB; ++b) free(T[b]);
     free_tab(&G); free_tab(&Q);
+    return err;
+}
+
+/* nu-body on-site product: the grid pointwise product extended to nu operands (the
+ * ACE-style extension in the discussion of other algorithms; Eq. phi-cg is nu = 2):
+ *   H_t[r][k] = sum_n U_t[l][n][r] X_t[n][k],                    t = 1 .. nu
+ *   T[r][k]   = int Y_k prod_t (sum_{k'} H_t[r][k'] Y_{k'}) dOmega,
+ *   out[n][k] = sum_r U_out[l][n][r] T[r][k].
+ * The integral is written out as the exact chain of real Gaunt couplings: P_1 = H_1 and
+ * P_t[k] = sum GR[k1][k2][k] P_{t-1}[k1] H_t[k2], where P_t keeps every degree up to t lmax
+ * (a product of fields of degrees a and b has degree a + b) and the last step only the
+ * output degrees up to lmax. Only Gaunt couplings enter: with natural-parity inputs the
+ * product has natural parity. Arrays: X[t] [N][C][L^2], U[t] [L][C][R], U_out [L][C][R],
+ * out [N][C][L^2]; operands may alias. */
+int cgo_nbody(int lmax, int C, int R, int nu, long n_nodes, const double *const *X,
+              const double *const *U, const double *U_out, double *out, int nthreads)
+{
+    if (lmax < 0 || C < 1 || R < 1 || nu < 1 || n_nodes < 0) return -1;
+    if ((long)nu * lmax > ORC_MAXJ) return -1;
+    set_threads(nthreads);
+    const int L2 = (lmax + 1) * (lmax + 1);
+    /* intermediate products: degrees up to (nu - 1) lmax, and at least the input's */
+    const int Lp = (nu > 1 ? nu - 1 : 1) * lmax + 1, P2 = Lp * Lp;
+    sparse_tab *G = (sparse_tab *)calloc((size_t)nu + 1, sizeof(sparse_tab));
+    if (!G) return -2;
+    for (int t = 2; t <= nu; ++t)
+        if (build_tab3(0, (t - 1) * lmax, lmax, t == nu ? lmax : t * lmax, &G[t])) return -2;
+    double *T = (double *)calloc((size_t)n_nodes * R * L2 + 1, sizeof(double));
+    if (!T) return -2;
+    int err = 0;
+#pragma omp parallel
+    {
+        double *buf = (double *)malloc(sizeof(double) * ((size_t)L2 + 2 * (size_t)P2));
+        if (!buf) {
+#pragma omp atomic write
+            err = -2;
+        } else {
+            double *h = buf, *p = buf + L2, *q = p + P2;
+#pragma omp for schedule(dynamic, 4)
+            for (long ir = 0; ir < n_nodes * R; ++ir) {
+                long i = ir / R;
+                int r = (int)(ir % R);
+                channel_contract_r(lmax, C, R, r, U[0], X[0] + (size_t)i * C * L2, h);
+                memset(p, 0, sizeof(double) * P2);
+                memcpy(p, h, sizeof(double) * L2);
+                for (int t = 2; t <= nu; ++t) {
+                    channel_contract_r(lmax, C, R, r, U[t - 1], X[t - 1] + (size_t)i * C * L2, h);
+                    memset(q, 0, sizeof(double) * P2);
+                    sparse_couple(&G[t], p, h, q);
+                    double *sw = p; p = q; q = sw;
+                }
+                memcpy(T + (size_t)ir * L2, p, sizeof(double) * L2);
+            }
+        }
+        free(buf);
+    }
+    if (!err) {
+#pragma omp parallel for schedule(static)
+        for (long i = 0; i < n_nodes; ++i)
+            project_out(lmax, C, R, U_out, T + (size_t)i * R * L2, out + (size_t)i * C * L2);
+    }
+    free(T);
+    for (int t = 2; t <= nu; ++t) free_tab(&G[t]);
+    free(G);
     return err;
 }
 
