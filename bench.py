@@ -124,6 +124,18 @@ def fields_receiver_flops(w, N: int, E: int) -> int:
     return pairs * w.R * (E * (g_e + c_e) + N * (g_r + c_r))
 
 
+def nbody_grid_flops(w) -> int:
+    """Algorithmic flops of the nu-body grid stage on its grid (U, V) = the exact grid for
+    nu operands, dense transforms, per (node, rank): value-only Legendre synthesis of nu
+    operands (2 U L^2 each), one Fourier synthesis each (2 U V M), nu - 1 products per point,
+    one Fourier analysis (2 U V M) and one Gauss-Legendre analysis (2 U L^2)."""
+    deg = (w.nu + 1) * w.lmax
+    U, V = max(1, (deg + 2) // 2), deg + 1
+    L, M = w.lmax + 1, 2 * w.lmax + 1
+    per = (w.nu + 1) * (2 * U * L * L + 2 * U * V * M) + (w.nu - 1) * U * V
+    return w.n * w.R * per
+
+
 def general_onsite_flops(w) -> int:
     """Algorithmic grid flops of the general on-site call: with shared factors every slot
     pair needs both products; with per-block factors every (slot pair, block) needs the
@@ -174,7 +186,11 @@ def cpu_baseline(w, d, budget_s: float = 15.0):
     import oracle
 
     cores = oracle.max_threads()
-    if w.kind == "mp_fields":
+    if w.kind == "nbody":
+        def run(n):
+            return oracle.nbody(w.lmax, [x[:n] for x in d["X"]], d["U"], d["U_out"])
+        unit_name = "nodes"
+    elif w.kind == "mp_fields":
         def run(n):
             return oracle.message_pass_fields(w.lmax, *(d[k] for k in MPF_KEYS),
                                               receivers=np.arange(n), edge_flip=d["edge_flip"],
@@ -214,8 +230,30 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
 
     if d is None:
         d = w.make()
-    plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
-    if w.kind == "mp_fields":
+    if w.kind == "nbody":
+        nt, nph = cg.nbody_grid(w.lmax, w.nu)
+        plan = cg.plan_create(w.lmax, w.C, w.R, n_theta=nt, n_phi=nph,
+                              flags=cg.CGTP_TIME_STAGES)
+    else:
+        plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
+    if w.kind == "nbody":
+        import numpy as np
+
+        uniq = {}
+        X = [uniq.setdefault(id(x), torch.from_numpy(np.ascontiguousarray(x)).cuda())
+             for x in d["X"]]
+        Ut = [torch.from_numpy(np.ascontiguousarray(u)).cuda() for u in d["U"]]
+        Uo = torch.from_numpy(np.ascontiguousarray(d["U_out"])).cuda()
+        E = 0
+        op = cg.CGTP_OP_ONSITE_NBODY
+        ws = torch.empty(cg.workspace_bytes_nbody(plan, w.n, w.nu), dtype=torch.uint8,
+                         device="cuda")
+        oe = torch.empty_like(X[0])
+        oo = None
+
+        def step():
+            cg.onsite_nbody(plan, X, Ut, Uo, out=oe, workspace=ws)
+    elif w.kind == "mp_fields":
         t = to_dev(d, MPF_KEYS + ("edge_flip", "node_flip"))
         E = int(d["n_edges"])
         op = cg.CGTP_OP_MESSAGE_PASS_FIELDS
@@ -313,7 +351,8 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name,
-                   "kind": "message_passing_two_fields" if w.kind == "mp_fields" else
+                   "kind": "onsite_nbody" if w.kind == "nbody" else
+                   "message_passing_two_fields" if w.kind == "mp_fields" else
                    ("message_passing" if w.kind == "mp" else "onsite")
                    + ("_general" if w.general else "_two_slot" if w.two_slot else ""),
                    "nodes": w.n, "edges": E, "lmax": w.lmax, "channels": w.C, "rank": w.R,
@@ -322,10 +361,19 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         "dominant_kernel": dom,
     }
     t_dom = stage_avg[dom] / 1e3
+    if w.kind == "nbody":
+        nt, nph = cg.nbody_grid(w.lmax, w.nu)
+        rec["config"].update(nu=w.nu, grid=f"{nt}x{nph}", self_coupled=bool(w.self_coupled))
     if w.general:
         rec["config"].update(in_blocks=w.in_blocks, out_blocks=w.out_blocks,
                              flips=[bool(w.flip1), bool(w.two_slot)])
-    if w.kind == "mp_fields" and dom == "receiver":
+    if w.kind == "nbody" and dom == "grid_product_analysis":
+        fl = nbody_grid_flops(w)
+        rec["roofline"] = {"bound": "alu", "achieved": fl / t_dom / 1e12,
+                           "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                           "frac": fl / t_dom / 1e12 / FP32_PEAK_TFLOPS,
+                           "traffic": load_traffic(w.name), "algorithmic_flops": fl}
+    elif w.kind == "mp_fields" and dom == "receiver":
         fl = fields_receiver_flops(w, w.n, E)
         rec["roofline"] = {"bound": "alu", "achieved": fl / t_dom / 1e12,
                            "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -84,6 +84,9 @@ extern "C" {
 #define CGTP_OP_ONSITE_GENERAL 3        /* cgtp_workspace_bytes_general / cgtp_stage_times */
 #define CGTP_OP_MESSAGE_PASS_GENERAL 4
 #define CGTP_OP_MESSAGE_PASS_FIELDS 5
+#define CGTP_OP_ONSITE_NBODY 6
+
+#define CGTP_MAX_NU 8   /* largest body order of cgtp_onsite_nbody */
 
 typedef struct cgtp_plan_s *cgtp_plan;
 
@@ -257,6 +260,28 @@ int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                              int in_blocks, const void *U_E, const void *U_I, int out_blocks,
                              const void *U_out_even, const void *U_out_odd, void *out_even,
                              void *out_odd, void *workspace, size_t ws_bytes, void *stream);
+
+/* nu-body on-site product: the grid pointwise product extended to nu operands, followed by
+ * a single inverse transform (the ACE-style higher-body-order extension the paper sketches
+ * after its comparison with other algorithms; nu = 2 is the Gaunt part of Eq. phi-cg):
+ *   H_t[r][k] = sum_n U[t][l][n][r] X[t][n][k],   t = 0 .. nu-1   (Eq. struct-H)
+ *   out[n][k] = sum_r U_out[l][n][r] int Y_k prod_t (sum_k' H_t[r][k'] Y_k') dOmega.
+ * With natural-parity inputs the output has natural parity (only Gaunt couplings).
+ *   nu         1 .. CGTP_MAX_NU;
+ *   X, U       host arrays of nu device pointers: X[t] [N][C][K], U[t] [L][C][R]; entries may
+ *              repeat (an operand with the same pointer and factors is contracted once);
+ *   U_out      [L][C][R]; out [N][C][K] (overwritten).
+ * Exactness needs a finer grid than the bilinear product: the plan must have been created
+ * with n_theta >= ((nu + 1) lmax + 2) / 2 (integer division) and n_phi >= (nu + 1) lmax + 1
+ * (CGTP_ERR_ARG otherwise, with the sizes in cgtp_last_error). The workspace is
+ * cgtp_workspace_bytes_nbody. n_nodes == 0 is a no-op. Errors: CGTP_ERR_ARG,
+ * CGTP_ERR_WORKSPACE, CGTP_ERR_UNSUPPORTED (LDS staging over 64 KiB), CGTP_ERR_HIP.
+ * Stages for cgtp_stage_times (CGTP_OP_ONSITE_NBODY): 0 contract operands, 1 grid product
+ * and analysis, 2 project. */
+int cgtp_workspace_bytes_nbody(cgtp_plan plan, int64_t n_nodes, int nu, size_t *bytes);
+int cgtp_onsite_nbody(cgtp_plan plan, int64_t n_nodes, int nu, const void *const *X,
+                      const void *const *U, const void *U_out, void *out, void *workspace,
+                      size_t ws_bytes, void *stream);
 
 /* Per-stage GPU time of the calls made since the previous cgtp_stage_times on
  * this plan (plan created with CGTP_TIME_STAGES), in the spirit of the paper's

@@ -31,17 +31,20 @@ CGTP_OP_MESSAGE_PASS_TWO_SLOT = 2
 CGTP_OP_ONSITE_GENERAL = 3
 CGTP_OP_MESSAGE_PASS_GENERAL = 4
 CGTP_OP_MESSAGE_PASS_FIELDS = 5
+CGTP_OP_ONSITE_NBODY = 6
+CGTP_MAX_NU = 8
 CGTP_MAX_LMAX = 24
 
 EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
             "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_workspace_bytes_general",
             "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_message_pass_fields",
-            "cgtp_stage_times",
+            "cgtp_workspace_bytes_nbody", "cgtp_onsite_nbody", "cgtp_stage_times",
             "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables")
 ONSITE_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis", "project_even",
                  "project_odd")
 MP_STAGES = ("contract_node", "sender_fields", "contract_edge_radial", "receiver",
              "project_even", "project_odd")
+NBODY_STAGES = ("contract_operands", "grid_product_analysis", "project")
 
 
 class CgtpError(RuntimeError):
@@ -82,6 +85,8 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_message_pass_general.argtypes = ([vp, i64, i64] + [vp] * 6 + [i32, vp, vp, i32]
                                               + [vp] * 4 + [vp, sz, vp])
     lib.cgtp_message_pass_fields.argtypes = lib.cgtp_message_pass_general.argtypes
+    lib.cgtp_workspace_bytes_nbody.argtypes = [vp, i64, i32, ctypes.POINTER(sz)]
+    lib.cgtp_onsite_nbody.argtypes = [vp, i64, i32, vp, vp, vp, vp, vp, sz, vp]
     lib.cgtp_stage_times.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double), i32,
                                      ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.cgtp_destroy.argtypes = [vp]
@@ -156,7 +161,8 @@ def stage_times(plan: Plan, op: int):
     ns, nc = ctypes.c_int(), ctypes.c_int()
     _check(load_library().cgtp_stage_times(plan.handle, op, ms, 8, ctypes.byref(ns),
                                            ctypes.byref(nc)), "cgtp_stage_times")
-    names = ONSITE_STAGES if op in (CGTP_OP_ONSITE, CGTP_OP_ONSITE_GENERAL) else MP_STAGES
+    names = (NBODY_STAGES if op == CGTP_OP_ONSITE_NBODY else
+             ONSITE_STAGES if op in (CGTP_OP_ONSITE, CGTP_OP_ONSITE_GENERAL) else MP_STAGES)
     return {names[i]: ms[i] for i in range(ns.value)}, nc.value
 
 
@@ -388,6 +394,48 @@ def message_pass_fields(plan: Plan, row_ptr, col, edge_feat, node_feat, U_E, U_I
         _ptr(U_out_odd), _ptr(outs[0]), _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)),
         "cgtp_message_pass_fields")
     return outs[0], outs[1]
+
+
+def nbody_grid(lmax: int, nu: int):
+    """Smallest (n_theta, n_phi) on which cgtp_onsite_nbody is exact for nu operands."""
+    deg = (nu + 1) * lmax
+    return max(1, (deg + 2) // 2), deg + 1
+
+
+def workspace_bytes_nbody(plan: Plan, n_nodes: int, nu: int) -> int:
+    out = ctypes.c_size_t()
+    _check(load_library().cgtp_workspace_bytes_nbody(plan.handle, n_nodes, nu,
+                                                     ctypes.byref(out)),
+           "cgtp_workspace_bytes_nbody")
+    return out.value
+
+
+def onsite_nbody(plan: Plan, X, U, U_out, out=None, workspace=None, stream=None):
+    """cgtp_onsite_nbody. X: sequence of nu device tensors [N, C, K]; U: nu factor tensors
+    [L, C, R]; U_out [L, C, R]. The plan's grid must be at least nbody_grid(lmax, nu)."""
+    torch = _torch()
+    nu = len(X)
+    if nu != len(U) or nu < 1:
+        raise ValueError("X and U must hold the same number (>= 1) of operands")
+    L = plan.lmax + 1
+    N = X[0].shape[0]
+    for t in range(nu):
+        _want(plan, f"X[{t}]", X[t], (N, plan.channels, L * L))
+        _want(plan, f"U[{t}]", U[t], (L, plan.channels, plan.rank))
+    _want(plan, "U_out", U_out, (L, plan.channels, plan.rank))
+    if out is None:
+        out = torch.empty_like(X[0])
+    _want(plan, "out", out, X[0].shape)
+    xs = (ctypes.c_void_p * nu)(*[x.data_ptr() for x in X])
+    us = (ctypes.c_void_p * nu)(*[u.data_ptr() for u in U])
+    ws_ptr, ws_len = None, 0
+    if workspace is not None:
+        ws_ptr, ws_len = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(load_library().cgtp_onsite_nbody(plan.handle, N, nu, ctypes.cast(xs, ctypes.c_void_p),
+                                            ctypes.cast(us, ctypes.c_void_p), _ptr(U_out),
+                                            _ptr(out), ws_ptr, ws_len, _stream_handle(stream)),
+           "cgtp_onsite_nbody")
+    return out
 
 
 def host_tables(lmax: int, n_theta: int = 0, n_phi: int = 0):

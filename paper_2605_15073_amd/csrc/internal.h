@@ -136,6 +136,18 @@ hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const float *HE, const float *SF, float *S, float *Ta,
                                        float *Tb, hipStream_t s);
 
+// nu-body on-site grid product (kernels.hip): Tout[b][r][K] = the analysis of the pointwise
+// product of the nu fields synthesised from H.h[t][b][r][K]. The grid of tb must be fine
+// enough for the (nu + 1) lmax integrand (checked by the caller).
+constexpr int kMaxNu = 8;
+template <typename T>
+struct NbodyOperands {
+    const T *h[kMaxNu];
+};
+template <typename T>
+hipError_t launch_nbody_grid(const Tabs<T> &tb, int64_t B, int R, int nu,
+                             const NbodyOperands<T> &H, T *Tout, hipStream_t s);
+
 // fp32 folded inverse transforms (folded.hip), lmax <= 24; hipErrorNotSupported when
 // the LDS staging does not fit.
 hipError_t launch_analysis_folded(const Tabs<float> &tb, int64_t B, int R, const float *S,

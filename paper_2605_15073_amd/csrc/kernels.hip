@@ -69,6 +69,56 @@ __device__ __forceinline__ void fourier_point(const Tabs<T> &tb, const T *q, con
     }
 }
 
+// Value-only Legendre synthesis (Eq. struct-F): F[mi][u] = sum_{l>=|m|} Pt_l^|m|(x_u) H[l,m].
+template <typename T>
+__device__ void legendre_value(const Tabs<T> &tb, const T *H, T *F)
+{
+    const Dims &d = tb.d;
+    for (int idx = threadIdx.x; idx < d.M * d.U; idx += blockDim.x) {
+        int mi = idx / d.U, u = idx - mi * d.U;
+        int m = mi - d.lmax, am = m < 0 ? -m : m;
+        const T *pu = tb.p + (size_t)u * d.P;
+        T f = 0;
+        for (int l = am; l <= d.lmax; ++l) f += pu[l * (l + 1) / 2 + am] * H[l * l + l + m];
+        F[idx] = f;
+    }
+}
+
+// Value-only Fourier synthesis at one grid point (Eq. struct-tildeA).
+template <typename T>
+__device__ __forceinline__ T fourier_value(const Tabs<T> &tb, const T *q, const T *F, int u, int v)
+{
+    const Dims &d = tb.d;
+    const T *qv = q + v * d.M;
+    T a = 0;
+    for (int mi = 0; mi < d.M; ++mi) a += qv[mi] * F[mi * d.U + u];
+    return a;
+}
+
+// Quadrature analysis (Eqs. struct-Tmu, struct-Tlm) of one grid field S [UV] held on chip,
+// through Tm scratch [M][U]; writes out [K].
+template <typename T>
+__device__ void analysis1(const Tabs<T> &tb, const T *q, const T *S, T *Tm, T *out)
+{
+    const Dims &d = tb.d;
+    for (int idx = threadIdx.x; idx < d.M * d.U; idx += blockDim.x) {
+        int mi = idx / d.U, u = idx - mi * d.U;
+        const T *row = S + u * d.V;
+        T s = 0;
+        for (int v = 0; v < d.V; ++v) s += q[v * d.M + mi] * row[v];
+        Tm[idx] = s;
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < d.K; k += blockDim.x) {
+        int l = degree_of(k), m = k - l * l - l, am = m < 0 ? -m : m;
+        const T *tm = Tm + (m + d.lmax) * d.U;
+        int pi = l * (l + 1) / 2 + am;
+        T s = 0;
+        for (int u = 0; u < d.U; ++u) s += tb.wq[u] * tb.p[(size_t)u * d.P + pi] * tm[u];
+        out[k] = s;
+    }
+}
+
 // Quadrature analysis (Eqs. struct-Tmu, struct-Tlm) of two grid fields S1, S2
 // [UV] held on chip, through Tm scratch [2][M][U]; writes out1/out2 [K].
 template <typename T>
@@ -243,6 +293,62 @@ hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, 
     const size_t sh = sizeof(T) * (q_in_lds ? with_q : base);
     hipLaunchKernelGGL(k_onsite_grid<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R,
                        q_in_lds, HA, HB, Ta, Tb);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// nu-body on-site product: per (node, rank) synthesise the values of the nu operands'
+// fields, multiply them pointwise on the grid and analyse the product back to (l, m) (the
+// grid product extended to nu operands, one inverse transform). The plan's grid must be fine
+// enough for the (nu + 1) lmax integrand.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_nbody_grid(Tabs<T> tb, int R, int nu, int q_in_lds,
+                                                         NbodyOperands<T> H, T *__restrict__ Tout)
+{
+    extern __shared__ unsigned char smem_raw[];
+    T *smem = reinterpret_cast<T *>(smem_raw);
+    const Dims &d = tb.d;
+    const int64_t br = blockIdx.x;
+    const int MU = d.M * d.U;
+    T *qs = smem;
+    T *Hs = qs + (q_in_lds ? d.V * d.M : 0);  // [nu][K]
+    T *F = Hs + nu * d.K;                       // [nu][M][U]
+    T *S = F + nu * MU;                         // [UV]
+    T *Tm = S + d.UV;                           // [M][U]
+    if (q_in_lds) stage_q(tb, qs);
+    const T *q = q_in_lds ? qs : tb.q;
+    for (int t = 0; t < nu; ++t)
+        for (int k = threadIdx.x; k < d.K; k += blockDim.x) Hs[t * d.K + k] = H.h[t][br * d.K + k];
+    __syncthreads();
+    for (int t = 0; t < nu; ++t) legendre_value(tb, Hs + t * d.K, F + t * MU);
+    __syncthreads();
+    for (int uv = threadIdx.x; uv < d.UV; uv += blockDim.x) {
+        const int u = uv / d.V, v = uv - u * d.V;
+        T prod = fourier_value(tb, q, F, u, v);
+        for (int t = 1; t < nu; ++t) prod *= fourier_value(tb, q, F + t * MU, u, v);
+        S[uv] = prod;
+    }
+    __syncthreads();
+    analysis1(tb, q, S, Tm, Tout + br * d.K);
+}
+
+template <typename T>
+hipError_t launch_nbody_grid(const Tabs<T> &tb, int64_t B, int R, int nu,
+                             const NbodyOperands<T> &H, T *Tout, hipStream_t s)
+{
+    const int64_t blocks = B * R;
+    if (blocks == 0) return hipSuccess;
+    if (nu < 1 || nu > kMaxNu) return hipErrorInvalidValue;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    const size_t MU = (size_t)tb.d.M * tb.d.U;
+    const size_t base = nu * (tb.d.K + MU) + tb.d.UV + MU;
+    const size_t with_q = base + (size_t)tb.d.V * tb.d.M;
+    const int q_in_lds = sizeof(T) * with_q <= 65536 ? 1 : 0;
+    const size_t sh = sizeof(T) * (q_in_lds ? with_q : base);
+    if (sh > 65536) return hipErrorNotSupported;
+    hipLaunchKernelGGL(k_nbody_grid<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R, nu,
+                       q_in_lds, H, Tout);
     return hipGetLastError();
 }
 
@@ -829,7 +935,9 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                                            const T *, const T *, T *, T *, hipStream_t);         \
     template hipError_t launch_receiver_fields<T>(const Tabs<T> &, int64_t, int, const int32_t *, \
                                                   const int32_t *, const T *, const T *, T *, T *, \
-                                                  hipStream_t);
+                                                  hipStream_t);                                   \
+    template hipError_t launch_nbody_grid<T>(const Tabs<T> &, int64_t, int, int,                  \
+                                             const NbodyOperands<T> &, T *, hipStream_t);
 
 CGTP_INSTANTIATE(float)
 CGTP_INSTANTIATE(double)

@@ -10,7 +10,7 @@
 
 namespace {
 constexpr int kMaxStages = 6;
-constexpr int kNumOps = 6;  // CGTP_OP_ONSITE .. CGTP_OP_MESSAGE_PASS_FIELDS
+constexpr int kNumOps = 7;  // CGTP_OP_ONSITE .. CGTP_OP_ONSITE_NBODY
 // HIP events bracketing the kernel stages of one call (CGTP_TIME_STAGES).
 struct EventSet {
     hipEvent_t ev[kMaxStages + 1];
@@ -153,6 +153,30 @@ Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E)
     l.off[5] = l.off[4] + h;
     l.total = l.off[5] + sg;
     return l;
+}
+
+// Workspace of the nu-body product: the nu operand contractions H [N][R][K] each, then
+// T [N][R][K].
+Layout nbody_layout(const cgtp_plan_s *p, int64_t N, int nu)
+{
+    size_t es = p->dtype == CGTP_F64 ? 8 : 4;
+    size_t h = align256(es * (size_t)N * p->R * p->d.K);
+    Layout l{};
+    l.off[0] = 0;
+    l.off[1] = (size_t)nu * h;
+    l.total = (size_t)(nu + 1) * h;
+    l.hf = h;
+    return l;
+}
+
+// Smallest grid on which the product of nu fields of degree lmax, projected onto degree
+// lmax, is integrated exactly: Gauss-Legendre with 2 U - 1 >= (nu + 1) lmax, V > (nu + 1) lmax.
+void nbody_min_grid(int lmax, int nu, int *U, int *V)
+{
+    const int deg = (nu + 1) * lmax;
+    *U = (deg + 2) / 2;
+    if (*U < 1) *U = 1;
+    *V = deg + 1;
 }
 
 int check_device(const cgtp_plan_s *p)
@@ -703,6 +727,47 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
 }
 
+// nu-body on-site product: one channel contraction per distinct (operand, factor) pair,
+// then the fused grid product and analysis, then the projection.
+template <typename T>
+int run_nbody(cgtp_plan_s *p, int64_t N, int nu, const void *const *X, const void *const *U,
+              const void *Uout, void *out, char *ws, hipStream_t s)
+{
+    const cgtp::Dims &d = p->d;
+    const int C = p->C, R = p->R;
+    cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
+    Layout lay = nbody_layout(p, N, nu);
+    T *Tn = reinterpret_cast<T *>(ws + lay.off[1]);
+    const int64_t hs = (int64_t)R * d.K;
+    StageRec rec;
+    int st = rec.begin(p, CGTP_OP_ONSITE_NBODY, 3, s);
+    if (st) return st;
+    cgtp::NbodyOperands<T> H{};
+    for (int t = 0; t < nu; ++t) {
+        int same = -1;  // identical operand and factors: share the contraction
+        for (int u = 0; u < t && same < 0; ++u)
+            if (X[u] == X[t] && U[u] == U[t]) same = u;
+        if (same >= 0) {
+            H.h[t] = H.h[same];
+            continue;
+        }
+        T *h = reinterpret_cast<T *>(ws + lay.off[0] + (size_t)t * lay.hf);
+        hipError_t e = contract_in<T>(N, C, R, d.K, U[t], X[t], h, hs, s);
+        if (e != hipSuccess) return hip_fail(e, "contract operand");
+        H.h[t] = h;
+    }
+    rec.mark();
+    hipError_t e = cgtp::launch_nbody_grid<T>(tb, N, R, nu, H, Tn, s);
+    if (e == hipErrorNotSupported)
+        return fail(CGTP_ERR_UNSUPPORTED, "nu-body grid staging exceeds 64 KiB of LDS");
+    if (e != hipSuccess) return hip_fail(e, "nu-body grid product");
+    rec.mark();
+    e = project<T>(N, C, R, d.K, Uout, Tn, hs, out, false, s);
+    if (e != hipSuccess) return hip_fail(e, "project");
+    rec.mark();
+    return CGTP_OK;
+}
+
 // How a general call runs: on the fused single-group kernels when the factors are shared
 // and each output sector reads one set of weights, else through rank groups.
 struct GeneralRoute {
@@ -1130,6 +1195,47 @@ int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                                 out_odd, w, s);
 }
 
+int cgtp_workspace_bytes_nbody(cgtp_plan plan, int64_t n_nodes, int nu, size_t *bytes)
+{
+    if (!plan || !bytes) return fail(CGTP_ERR_ARG, "NULL argument");
+    if (n_nodes < 0) return fail(CGTP_ERR_ARG, "negative size");
+    if (nu < 1 || nu > CGTP_MAX_NU) return fail(CGTP_ERR_ARG, "nu %d outside [1, %d]", nu, CGTP_MAX_NU);
+    *bytes = nbody_layout(plan, n_nodes, nu).total;
+    return CGTP_OK;
+}
+
+int cgtp_onsite_nbody(cgtp_plan plan, int64_t n_nodes, int nu, const void *const *X,
+                      const void *const *U, const void *U_out, void *out, void *workspace,
+                      size_t ws_bytes, void *stream)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
+    if (n_nodes < 0) return fail(CGTP_ERR_ARG, "n_nodes < 0");
+    if (nu < 1 || nu > CGTP_MAX_NU) return fail(CGTP_ERR_ARG, "nu %d outside [1, %d]", nu, CGTP_MAX_NU);
+    int Umin, Vmin;
+    nbody_min_grid(plan->d.lmax, nu, &Umin, &Vmin);
+    if (plan->d.U < Umin || plan->d.V < Vmin)
+        return fail(CGTP_ERR_ARG,
+                    "grid %d x %d too coarse for a %d-fold product at lmax %d: create the plan "
+                    "with n_theta >= %d and n_phi >= %d",
+                    plan->d.U, plan->d.V, nu, plan->d.lmax, Umin, Vmin);
+    if (n_nodes == 0) return CGTP_OK;
+    if (!X || !U || !U_out || !out) return fail(CGTP_ERR_ARG, "NULL argument");
+    for (int t = 0; t < nu; ++t)
+        if (!X[t] || !U[t]) return fail(CGTP_ERR_ARG, "NULL operand %d", t);
+    if (n_nodes * (int64_t)plan->R > 0x7fffffffLL)
+        return fail(CGTP_ERR_UNSUPPORTED, "n_nodes * rank exceeds 2^31 - 1");
+    int st = check_device(plan);
+    if (st) return st;
+    void *ws = nullptr;
+    st = get_workspace(plan, nbody_layout(plan, n_nodes, nu).total, workspace, ws_bytes, &ws);
+    if (st) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char *w = static_cast<char *>(ws);
+    if (plan->dtype == CGTP_F64) return run_nbody<double>(plan, n_nodes, nu, X, U, U_out, out, w, s);
+    return run_nbody<float>(plan, n_nodes, nu, X, U, U_out, out, w, s);
+}
+
 int cgtp_destroy(cgtp_plan plan)
 {
     if (!plan) return CGTP_OK;
@@ -1149,7 +1255,8 @@ int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages,
     if (!(plan->flags & CGTP_TIME_STAGES))
         return fail(CGTP_ERR_ARG, "plan was created without CGTP_TIME_STAGES");
     int ns;
-    if (op == CGTP_OP_ONSITE || op == CGTP_OP_ONSITE_GENERAL) ns = 5;
+    if (op == CGTP_OP_ONSITE_NBODY) ns = 3;
+    else if (op == CGTP_OP_ONSITE || op == CGTP_OP_ONSITE_GENERAL) ns = 5;
     else if (op == CGTP_OP_MESSAGE_PASS || op == CGTP_OP_MESSAGE_PASS_TWO_SLOT ||
              op == CGTP_OP_MESSAGE_PASS_GENERAL || op == CGTP_OP_MESSAGE_PASS_FIELDS)
         ns = 6;

@@ -211,10 +211,25 @@ def fields_mp_inputs(n_atoms: int, lmax: int, C: int, R: int, seed: int, edge_fl
     return d
 
 
+def nbody_inputs(n: int, lmax: int, C: int, R: int, seed: int, nu: int,
+                 self_coupled: bool = True, per_degree: bool = True):
+    """nu-body on-site operands: X (a list of nu [N][C][L^2] arrays; with self_coupled one
+    array repeated, the ACE density raised to the nu-th power), U (nu factor matrices),
+    U_out. Draw order: X (once, or nu times), U[0 .. nu-1], U_out."""
+    rng = np.random.default_rng(seed)
+    if self_coupled:
+        A = coefficients(rng, n, C, lmax, per_degree)
+        X = [A] * nu
+    else:
+        X = [coefficients(rng, n, C, lmax, per_degree) for _ in range(nu)]
+    U = [cp_factors(rng, lmax, C, R) for _ in range(nu)]
+    return dict(X=X, U=U, U_out=cp_factors(rng, lmax, C, R))
+
+
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str          # "onsite", "mp" or "mp_fields" (two parity-bearing fields)
+    kind: str          # "onsite", "mp", "mp_fields" (two parity-bearing fields) or "nbody"
     n: int             # nodes (on-site) or atoms (message passing)
     lmax: int
     C: int
@@ -228,12 +243,16 @@ class Workload:
     in_blocks: int = 0
     out_blocks: int = 1      # ... output weight blocks per sector (1 or 2)
     flip1: bool = False      # first operand (on-site A, or the edge field) has a flipped slot
+    nu: int = 0              # body order of a "nbody" workload
 
     @property
     def general(self) -> bool:
         return self.in_blocks > 0
 
     def make(self, **kw):
+        if self.kind == "nbody":
+            return nbody_inputs(self.n, self.lmax, self.C, self.R, self.seed, self.nu,
+                                self_coupled=self.self_coupled, per_degree=self.per_degree, **kw)
         if self.kind == "mp_fields":
             return fields_mp_inputs(self.n, self.lmax, self.C, self.R, self.seed,
                                     edge_flip=self.flip1, node_flip=self.two_slot,
@@ -279,4 +298,10 @@ WORKLOADS = {
     # of R Y, both node slots, per-block factors
     "mpf_5k_l6_c64": Workload("mpf_5k_l6_c64", "mp_fields", 5000, 6, 64, 64, seed=4,
                               two_slot=True, flip1=True, in_blocks=4, out_blocks=2),
+    # nu-body grid products (ACE-style: the density A to the nu-th power, one factor matrix per
+    # power, one inverse transform), on the grid exact for the (nu + 1) lmax integrand
+    "nbody_n2048_l4_c64_nu3": Workload("nbody_n2048_l4_c64_nu3", "nbody", 2048, 4, 64, 64,
+                                       seed=5, per_degree=True, self_coupled=True, nu=3),
+    "nbody_n2048_l8_c64_nu4": Workload("nbody_n2048_l8_c64_nu4", "nbody", 2048, 8, 64, 64,
+                                       seed=6, per_degree=True, self_coupled=True, nu=4),
 }
