@@ -367,7 +367,14 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
     if w.general:
         rec["config"].update(in_blocks=w.in_blocks, out_blocks=w.out_blocks,
                              flips=[bool(w.flip1), bool(w.two_slot)])
-    if w.kind == "nbody" and dom == "grid_product_analysis":
+    if w.kind == "nbody" and dom == "contract_operands":
+        # one per-degree channel contraction per power: 2 C R flops per (node, k)
+        fl = w.nu * 2 * w.n * w.C * w.R * (w.lmax + 1) ** 2
+        rec["roofline"] = {"bound": "mfma", "achieved": fl / t_dom / 1e12,
+                           "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                           "frac": fl / t_dom / 1e12 / FP32_PEAK_TFLOPS,
+                           "traffic": load_traffic(w.name), "algorithmic_flops": fl}
+    elif w.kind == "nbody" and dom == "grid_product_analysis":
         fl = nbody_grid_flops(w)
         rec["roofline"] = {"bound": "alu", "achieved": fl / t_dom / 1e12,
                            "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -147,6 +147,10 @@ struct NbodyOperands {
 template <typename T>
 hipError_t launch_nbody_grid(const Tabs<T> &tb, int64_t B, int R, int nu,
                              const NbodyOperands<T> &H, T *Tout, hipStream_t s);
+// fp32 folded form of the same (onsite.hip) for lmax <= 10 and nu = 2 .. 4;
+// hipErrorNotSupported otherwise.
+hipError_t launch_nbody_folded(const Tabs<float> &tb, int64_t B, int R, int nu,
+                               const NbodyOperands<float> &H, float *Tout, hipStream_t s);
 
 // fp32 folded inverse transforms (folded.hip), lmax <= 24; hipErrorNotSupported when
 // the LDS staging does not fit.

@@ -341,6 +341,10 @@ hipError_t launch_nbody_grid(const Tabs<T> &tb, int64_t B, int R, int nu,
     if (blocks == 0) return hipSuccess;
     if (nu < 1 || nu > kMaxNu) return hipErrorInvalidValue;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    if constexpr (sizeof(T) == 4) {
+        hipError_t e = launch_nbody_folded(tb, B, R, nu, H, Tout, s);
+        if (e != hipErrorNotSupported) return e;
+    }
     const size_t MU = (size_t)tb.d.M * tb.d.U;
     const size_t base = nu * (tb.d.K + MU) + tb.d.UV + MU;
     const size_t with_q = base + (size_t)tb.d.V * tb.d.M;

@@ -162,6 +162,135 @@ hipError_t launch_folded(const Tabs<float> &tb, int64_t B, int R, const float *H
     return hipGetLastError();
 }
 
+// nu-body product in the folded form (fp32, lmax <= kNbodyFoldedMaxL, NU operands): one
+// thread per (rank, Gauss-Legendre node u) keeps the Legendre coefficients F_t[m] of every
+// operand in registers (Eq. struct-F), sweeps the azimuth in pairs (v, V - v) forming each
+// field's value at both points from its cosine and sine parts, multiplies the NU values at
+// each point and accumulates the Fourier analysis (Eq. struct-Tmu) of the product in
+// registers with the same pairing. The Gauss-Legendre analysis across u (Eq. struct-Tlm)
+// goes through LDS. The grid (U, V) is the plan's, exact for the (NU + 1) lmax integrand.
+template <int LM, int NU>
+__global__ __launch_bounds__(256) void k_nbody_folded(Tabs<float> tb, int R, int rb,
+                                                      NbodyOperands<float> H,
+                                                      float *__restrict__ Tout)
+{
+    constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
+    extern __shared__ float smem[];
+    const int U = tb.d.U, V = tb.d.V;
+    float *qs = smem;              // [V][M]
+    float *ps = qs + V * M;        // [U][P]
+    float *Hs = ps + U * P;        // [NU][rb][K]
+    float *Tm = Hs + NU * rb * K;  // [rb][M][U]
+
+    const int nrb = (R + rb - 1) / rb;
+    const int64_t b = blockIdx.x / nrb;
+    const int r0 = (int)(blockIdx.x - b * nrb) * rb;
+    const int nr = (R - r0 < rb) ? (R - r0) : rb;
+    for (int k = threadIdx.x; k < V * M; k += blockDim.x) qs[k] = tb.q[k];
+    for (int k = threadIdx.x; k < U * P; k += blockDim.x) ps[k] = tb.p[k];
+#pragma unroll
+    for (int t = 0; t < NU; ++t) {
+        const float *h = H.h[t] + (b * R + r0) * (int64_t)K;
+        for (int k = threadIdx.x; k < nr * K; k += blockDim.x) Hs[t * rb * K + k] = h[k];
+    }
+    __syncthreads();
+
+    const int q = threadIdx.x / U, u = threadIdx.x - q * U;
+    if (q < nr) {
+        float F[NU][M];
+        const float *pu = ps + u * P;
+#pragma unroll
+        for (int t = 0; t < NU; ++t) {
+            const float *h = Hs + (t * rb + q) * K;
+#pragma unroll
+            for (int mi = 0; mi < M; ++mi) {
+                const int m = mi - LM, am = m < 0 ? -m : m;
+                float f = 0.f;
+#pragma unroll
+                for (int l = am; l <= LM; ++l) f += pu[l * (l + 1) / 2 + am] * h[l * l + l + m];
+                F[t][mi] = f;
+            }
+        }
+        float T[M];
+#pragma unroll
+        for (int mi = 0; mi < M; ++mi) T[mi] = 0.f;
+        for (int v = 0; 2 * v <= V; ++v) {
+            const int pv = v == 0 ? 0 : V - v;
+            const bool paired = v != 0 && pv != v;
+            const float *qr = qs + v * M;
+            float p0 = 1.f, p1 = 1.f;  // the product at v and at V - v
+#pragma unroll
+            for (int t = 0; t < NU; ++t) {
+                float c0 = F[t][LM], s0 = 0.f;
+#pragma unroll
+                for (int k = 1; k <= LM; ++k) {
+                    c0 += qr[LM + k] * F[t][LM + k];
+                    s0 += qr[LM - k] * F[t][LM - k];
+                }
+                p0 *= c0 + s0;
+                p1 *= c0 - s0;
+            }
+            if (!paired) p1 = 0.f;
+            const float sP = p0 + p1, sM = p0 - p1;
+            T[LM] += sP;
+#pragma unroll
+            for (int k = 1; k <= LM; ++k) {
+                T[LM + k] += qr[LM + k] * sP;
+                T[LM - k] += qr[LM - k] * sM;
+            }
+        }
+        float *tm = Tm + q * M * U;
+#pragma unroll
+        for (int mi = 0; mi < M; ++mi) tm[mi * U + u] = T[mi];
+    }
+    __syncthreads();
+    // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
+    for (int idx = threadIdx.x; idx < nr * K; idx += blockDim.x) {
+        const int qq = idx / K, k = idx - qq * K;
+        int l = (int)sqrtf((float)k);
+        while (l * l > k) --l;
+        while ((l + 1) * (l + 1) <= k) ++l;
+        const int m = k - l * l - l, am = m < 0 ? -m : m;
+        const float *tm = Tm + qq * M * U + (m + LM) * U;
+        const int pi = l * (l + 1) / 2 + am;
+        float s = 0.f;
+        for (int uu = 0; uu < U; ++uu) s += tb.wq[uu] * ps[uu * P + pi] * tm[uu];
+        Tout[(b * R + r0 + qq) * (int64_t)K + k] = s;
+    }
+}
+
+template <int LM, int NU>
+hipError_t launch_nbody_folded_lm(const Tabs<float> &tb, int64_t B, int R,
+                                  const NbodyOperands<float> &H, float *Tout, hipStream_t s)
+{
+    constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
+    const int U = tb.d.U, V = tb.d.V;
+    int rb = 256 / U;
+    if (rb > R) rb = R;
+    if (rb < 1) return hipErrorNotSupported;
+    auto lds = [&](int r) { return sizeof(float) * (V * M + U * P + NU * r * K + r * M * U); };
+    while (rb > 1 && lds(rb) > 65536) --rb;
+    if (lds(rb) > 65536) return hipErrorNotSupported;
+    const int threads = (rb * U + 63) / 64 * 64;
+    const int64_t blocks = B * ((R + rb - 1) / rb);
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_nbody_folded<LM, NU>), dim3((unsigned)blocks), dim3(threads), lds(rb),
+                       s, tb, R, rb, H, Tout);
+    return hipGetLastError();
+}
+
+template <int LM>
+hipError_t launch_nbody_folded_nu(const Tabs<float> &tb, int64_t B, int R, int nu,
+                                  const NbodyOperands<float> &H, float *Tout, hipStream_t s)
+{
+    switch (nu) {
+    case 2: return launch_nbody_folded_lm<LM, 2>(tb, B, R, H, Tout, s);
+    case 3: return launch_nbody_folded_lm<LM, 3>(tb, B, R, H, Tout, s);
+    case 4: return launch_nbody_folded_lm<LM, 4>(tb, B, R, H, Tout, s);
+    default: return hipErrorNotSupported;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
@@ -174,6 +303,20 @@ hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const f
         CGTP_CASE(0) CGTP_CASE(1) CGTP_CASE(2) CGTP_CASE(3) CGTP_CASE(4) CGTP_CASE(5)
         CGTP_CASE(6) CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11)
         CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
+#undef CGTP_CASE
+    default: return hipErrorNotSupported;
+    }
+}
+
+hipError_t launch_nbody_folded(const Tabs<float> &tb, int64_t B, int R, int nu,
+                               const NbodyOperands<float> &H, float *Tout, hipStream_t s)
+{
+    if (B == 0) return hipSuccess;
+    switch (tb.d.lmax) {
+#define CGTP_CASE(LMV) \
+    case LMV: return launch_nbody_folded_nu<LMV>(tb, B, R, nu, H, Tout, s);
+        CGTP_CASE(0) CGTP_CASE(1) CGTP_CASE(2) CGTP_CASE(3) CGTP_CASE(4) CGTP_CASE(5)
+        CGTP_CASE(6) CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10)
 #undef CGTP_CASE
     default: return hipErrorNotSupported;
     }
