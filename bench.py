@@ -36,10 +36,11 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_sha() -> str:
-    """Hash of the library sources: traffic counters are only valid for this version."""
+    """Hash of the library's device code (the .hip sources and their headers): traffic
+    counters are only valid for this version of the kernels."""
     h = hashlib.sha256()
     for name in sorted(os.listdir(CSRC)):
-        if name.endswith((".hip", ".h", ".cpp")):
+        if name.endswith((".hip", ".h")):
             with open(os.path.join(CSRC, name), "rb") as f:
                 h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
