@@ -71,6 +71,7 @@ struct Layout {
     size_t total;
     size_t hf = 0, sff = 0;  // offsets of the second HI / SF (flipped slot or curl factors)
     size_t rtf = 0;          // offset of the second Rt (curl factors)
+    size_t wc = 0;           // concatenated factor blocks of a run of rank groups [L][C][R]
 };
 
 // Receiver on MFMA: fp32, zonal edge field, R a multiple of 16, lmax high enough that the
@@ -96,7 +97,8 @@ Layout onsite_layout(const cgtp_plan_s *p, int R, int64_t N)
     size_t blk = align256(es * (size_t)N * R * p->d.K);
     Layout l{};
     for (int i = 0; i < 4; ++i) l.off[i] = i * blk;
-    l.total = 4 * blk;
+    l.wc = 4 * blk;
+    l.total = 4 * blk + align256(es * (size_t)p->d.L * p->C * R);
     return l;
 }
 
@@ -151,7 +153,8 @@ Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E)
     l.off[3] = h + sf + he;
     l.off[4] = l.off[3] + h;
     l.off[5] = l.off[4] + h;
-    l.total = l.off[5] + sg;
+    l.wc = l.off[5] + sg;
+    l.total = l.wc + align256(es * (size_t)p->d.L * p->C * R);
     return l;
 }
 
@@ -463,44 +466,32 @@ struct Groups {
     int n = 0;
     bool split = false;  // groups take different factors for their Gaunt and curl products
     Group g[kMaxGroups];
-    int lo[4] = {0, 0, 0, 0}, hi[4] = {0, 0, 0, 0};  // groups [lo, hi) feed block b
 };
 
 int block_of(int cat, int rel) { return 2 * cat + (cat ? 1 - rel : rel); }
 
+// Whether group g's product of block b's category feeds block b.
+bool feeds(const Group &g, int b) { return (b >> 1 ? g.bc : g.bg) == b; }
+
 // f1 / f2: the first / second operand has a flipped slot (message passing: f1 = false, the
 // edge field); in_blocks: 1 (shared factors), 2 (per category) or 4 (per block); split:
-// per-block factors may differ between a group's two products.
+// per-block factors may differ between a group's two products. Groups are ordered by slot
+// pair, so the groups that contract the same operand slot are runs of consecutive groups.
 Groups make_groups(bool f1, bool f2, int in_blocks, bool split)
 {
     Groups G;
     auto present = [&](int s1, int s2) { return (s1 == 0 || f1) && (s2 == 0 || f2); };
-    const int pairs[4][2] = {{0, 0}, {1, 1}, {0, 1}, {1, 0}};
-    if (in_blocks == 1 || split) {
-        G.split = in_blocks > 1;
-        for (const auto &pr : pairs) {
-            const int rel = pr[0] != pr[1];
-            if (present(pr[0], pr[1]))
-                G.g[G.n++] = Group{pr[0], pr[1], block_of(0, rel), block_of(1, rel)};
+    const int pairs[4][2] = {{0, 0}, {0, 1}, {1, 0}, {1, 1}};
+    G.split = split && in_blocks > 1;
+    for (const auto &pr : pairs) {
+        if (!present(pr[0], pr[1])) continue;
+        const int rel = pr[0] != pr[1];
+        if (in_blocks == 1 || G.split) {
+            G.g[G.n++] = Group{pr[0], pr[1], block_of(0, rel), block_of(1, rel)};
+        } else {
+            G.g[G.n++] = Group{pr[0], pr[1], block_of(0, rel), -1};
+            G.g[G.n++] = Group{pr[0], pr[1], -1, block_of(1, rel)};
         }
-    } else {
-        for (int b = 0; b < 4; ++b) {
-            const int cat = b >> 1, sec = b & 1, rel = cat ? 1 - sec : sec;
-            for (const auto &pr : pairs)
-                if ((pr[0] != pr[1]) == rel && present(pr[0], pr[1]))
-                    G.g[G.n++] = Group{pr[0], pr[1], cat ? -1 : b, cat ? b : -1};
-        }
-    }
-    // each block's groups are consecutive by construction
-    for (int b = 0; b < 4; ++b) {
-        int lo = -1, hi = -1;
-        for (int i = 0; i < G.n; ++i) {
-            if ((b >> 1 ? G.g[i].bc : G.g[i].bg) != b) continue;
-            if (lo < 0) lo = i;
-            hi = i + 1;
-        }
-        G.lo[b] = lo < 0 ? 0 : lo;
-        G.hi[b] = hi < 0 ? 0 : hi;
     }
     return G;
 }
@@ -542,7 +533,8 @@ int project_blocks(const cgtp_plan_s *p, const Groups &G, int64_t N, const Facto
         bool first = true;
         for (int cat = 0; cat < 2 && outs[sec]; ++cat) {
             const int b = 2 * cat + sec;
-            for (int gi = G.lo[b]; gi < G.hi[b]; ++gi) {
+            for (int gi = 0; gi < G.n; ++gi) {
+                if (!feeds(G.g[gi], b)) continue;
                 const T *src = (cat ? Tb : Ta) + (int64_t)gi * p->R * p->d.K;
                 hipError_t e = project<T>(N, p->C, p->R, p->d.K, f.out[b], src, rs, outs[sec],
                                           !first, s);
@@ -555,37 +547,66 @@ int project_blocks(const cgtp_plan_s *p, const Groups &G, int64_t N, const Facto
     return CGTP_OK;
 }
 
+// Channel contraction of every group's operand (first when first, else second) into
+// H [rows][G R][K]: one launch per run of consecutive groups that read the same operand slot,
+// with the runs' factor blocks concatenated along the rank into wcat [L][C][n R].
+template <typename T>
+hipError_t contract_runs(const cgtp_plan_s *p, const Groups &G, int64_t rows, bool first,
+                         const void *const X[2], const void *const fac[4], T *H, T *wcat,
+                         hipStream_t s)
+{
+    const cgtp::Dims &d = p->d;
+    const int C = p->C, R = p->R, Rg = G.n * R;
+    const size_t es = sizeof(T);
+    int g0 = 0;
+    while (g0 < G.n) {
+        const int slot = first ? G.g[g0].s1 : G.g[g0].s2;
+        int g1 = g0 + 1;
+        while (g1 < G.n && (first ? G.g[g1].s1 : G.g[g1].s2) == slot) ++g1;
+        const int n = g1 - g0;
+        const T *W = static_cast<const T *>(fac[group_block(G.g[g0])]);
+        if (n > 1) {
+            for (int gi = g0; gi < g1; ++gi) {
+                hipError_t e = hipMemcpy2DAsync(wcat + (size_t)(gi - g0) * R, es * n * R,
+                                                fac[group_block(G.g[gi])], es * R, es * R,
+                                                (size_t)d.L * C, hipMemcpyDeviceToDevice, s);
+                if (e != hipSuccess) return e;
+            }
+            W = wcat;
+        }
+        hipError_t e = cgtp::launch_contract<T>(rows, C, n * R, d.K, false, W, (int64_t)C * n * R,
+                                                n * R, 1, static_cast<const T *>(X[slot]),
+                                                (int64_t)C * d.K, H + (int64_t)g0 * R * d.K,
+                                                (int64_t)Rg * d.K, d.K, 1, nullptr, false, s);
+        if (e != hipSuccess) return e;
+        g0 = g1;
+    }
+    return hipSuccess;
+}
+
 template <typename T>
 int run_onsite_groups(cgtp_plan_s *p, const Groups &G, int64_t N, const void *const X1[2],
                       const void *const X2[2], const Factors &f, void *oe, void *oo, char *ws,
                       hipStream_t s)
 {
     const cgtp::Dims &d = p->d;
-    const int C = p->C, R = p->R, Rg = G.n * R;
+    const int Rg = G.n * p->R;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
     Layout lay = onsite_layout(p, Rg, N);
     T *HA = reinterpret_cast<T *>(ws + lay.off[0]);
     T *HB = reinterpret_cast<T *>(ws + lay.off[1]);
     T *Ta = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[3]);
-    const int64_t hs = (int64_t)Rg * d.K;
     StageRec rec;
     int st = rec.begin(p, CGTP_OP_ONSITE_GENERAL, 5, s);
     if (st) return st;
     hipError_t e;
-    for (int gi = 0; gi < G.n; ++gi) {
-        const Group &g = G.g[gi];
-        e = contract_in<T>(N, C, R, d.K, f.in1[group_block(g)], X1[g.s1],
-                           HA + (int64_t)gi * R * d.K, hs, s);
-        if (e != hipSuccess) return hip_fail(e, "contract first operand");
-    }
+    T *wc = reinterpret_cast<T *>(ws + lay.wc);
+    e = contract_runs<T>(p, G, N, true, X1, f.in1, HA, wc, s);
+    if (e != hipSuccess) return hip_fail(e, "contract first operand");
     rec.mark();
-    for (int gi = 0; gi < G.n; ++gi) {
-        const Group &g = G.g[gi];
-        e = contract_in<T>(N, C, R, d.K, f.in2[group_block(g)], X2[g.s2],
-                           HB + (int64_t)gi * R * d.K, hs, s);
-        if (e != hipSuccess) return hip_fail(e, "contract second operand");
-    }
+    e = contract_runs<T>(p, G, N, false, X2, f.in2, HB, wc, s);
+    if (e != hipSuccess) return hip_fail(e, "contract second operand");
     rec.mark();
     e = cgtp::launch_onsite_grid<T>(tb, N, Rg, HA, HB, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "onsite grid");
@@ -680,7 +701,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
                   const Factors &f, void *oe, void *oo, char *ws, hipStream_t s)
 {
     const cgtp::Dims &d = p->d;
-    const int C = p->C, R = p->R, Rg = G.n * R;
+    const int Rg = G.n * p->R;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
     Layout lay = mpf_layout(p, Rg, N, E);
     T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
@@ -688,27 +709,19 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     T *HE = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Ta = reinterpret_cast<T *>(ws + lay.off[3]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
-    const int64_t hs = (int64_t)Rg * d.K;
     StageRec rec;
     int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_FIELDS, 6, s);
     if (st) return st;
     hipError_t e;
-    for (int gi = 0; gi < G.n; ++gi) {
-        const Group &g = G.g[gi];
-        e = contract_in<T>(N, C, R, d.K, f.in2[group_block(g)], X2[g.s2],
-                           HI + (int64_t)gi * R * d.K, hs, s);
-        if (e != hipSuccess) return hip_fail(e, "contract node features");
-    }
+    T *wc = reinterpret_cast<T *>(ws + lay.wc);
+    e = contract_runs<T>(p, G, N, false, X2, f.in2, HI, wc, s);
+    if (e != hipSuccess) return hip_fail(e, "contract node features");
     rec.mark();
     e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s);
     if (e != hipSuccess) return hip_fail(e, "sender fields");
     rec.mark();
-    for (int gi = 0; gi < G.n; ++gi) {
-        const Group &g = G.g[gi];
-        e = contract_in<T>(E, C, R, d.K, f.in1[group_block(g)], X1[g.s1],
-                           HE + (int64_t)gi * R * d.K, hs, s);
-        if (e != hipSuccess) return hip_fail(e, "contract edge field");
-    }
+    e = contract_runs<T>(p, G, E, true, X1, f.in1, HE, wc, s);
+    if (e != hipSuccess) return hip_fail(e, "contract edge field");
     rec.mark();
     if constexpr (sizeof(T) == 4) {
         if (use_mfma_fields(p)) {
