@@ -59,14 +59,19 @@ constexpr int kSWo = kTile + 16;
 constexpr int kSWt = kCs + 2;
 constexpr int kNS = kTile * kCs / kThreadsC;  // staged elements per thread, per operand
 
-template <bool WT>
+// OT output rows per block (64 or 128): wave (wo, wc) owns OT / 2 rows x 32 columns, i.e.
+// OT / 32 x 2 MFMA tiles, so a block with OT = 128 stages each X slice once for 128 outputs.
+template <bool WT, int OT>
 __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     int64_t B, int Cin, int Cout, int K, int tiles_per_group, int otiles,
     const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
     const float *__restrict__ X, int64_t x_sb, float *__restrict__ Y, int64_t y_sb, int64_t y_so,
     int64_t y_sk, const float *__restrict__ scale, bool accumulate)
 {
-    __shared__ float Ws[WT ? kTile * kSWt : kCs * kSWo];
+    constexpr int SWo = OT + 16;                 // LDS row stride of Ws[i][o]: 16 mod 32
+    constexpr int NW = OT * kCs / kThreadsC;     // staged W elements per thread
+    constexpr int OTW = OT / 32;                 // 16-row MFMA tiles per wave
+    __shared__ float Ws[WT ? OT * kSWt : kCs * SWo];
     __shared__ float Xs[kCs * kSWo];
 
     // Blocks are dealt round-robin to the 8 XCDs (block b runs on XCD b % 8), each with
@@ -86,18 +91,19 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     const int64_t nb = (B - b0 < kTile) ? (B - b0) : kTile;
     const int ncols = (int)nb * width;                 // columns of degree l in this group
     const int c0 = sub * kTile;
-    const int o0 = ot * kTile;
+    const int o0 = ot * OT;
     const float *Wl = W + l * w_sl;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int osub = (wave >> 1) * 32;
+    const int osub = (wave >> 1) * (OT / 2);
     const int csub = (wave & 1) * 32;
     const int gg = lane >> 4, n = lane & 15;
 
-    float4_t acc[2][2];
-    for (int a = 0; a < 2; ++a)
+    float4_t acc[OTW][2];
+#pragma unroll
+    for (int a = 0; a < OTW; ++a)
         for (int bb = 0; bb < 2; ++bb) acc[a][bb] = float4_t{0.f, 0.f, 0.f, 0.f};
 
     // this thread's column of X (fixed over the reduction): c = tid % 64, rows i = tid / 64 + 4 s
@@ -107,17 +113,21 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     const int bl = c_ok ? cg / width : 0;
     const int mm = c_ok ? cg - bl * width : 0;
     const float *xcol = X + (b0 + bl) * x_sb + kofs + mm;
-    float wr[kNS], xr[kNS];
+    float wr[NW], xr[kNS];
     auto fetch = [&](int i0) {
 #pragma unroll
         for (int s2 = 0; s2 < kNS; ++s2) {
             const int ig = i0 + li + 4 * s2;
             xr[s2] = (ig < Cin && c_ok) ? xcol[(int64_t)ig * K] : 0.f;
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < NW; ++s2) {
             if (WT) {  // k = tid + 256 s -> (o, i), i fastest
                 const int k = tid + kThreadsC * s2, o = k / kCs, i = k - o * kCs;
                 wr[s2] = (i0 + i < Cin && o0 + o < Cout) ? Wl[(i0 + i) + (int64_t)(o0 + o) * w_so] : 0.f;
-            } else {   // (i, o), o fastest
-                wr[s2] = (ig < Cin && o0 + lc < Cout) ? Wl[(int64_t)ig * w_si + (o0 + lc) * w_so] : 0.f;
+            } else {   // (i, o), o fastest: rows li + 4 (s % kNS), outputs lc + 64 (s / kNS)
+                const int ig = i0 + li + 4 * (s2 % kNS), oo = lc + 64 * (s2 / kNS);
+                wr[s2] = (ig < Cin && o0 + oo < Cout) ? Wl[(int64_t)ig * w_si + (o0 + oo) * w_so] : 0.f;
             }
         }
     };
@@ -125,14 +135,14 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     for (int i0 = 0; i0 < Cin; i0 += kCs) {
         __syncthreads();  // the previous slice is consumed
 #pragma unroll
-        for (int s2 = 0; s2 < kNS; ++s2) {
-            const int i = li + 4 * s2;
-            Xs[i * kSWo + lc] = xr[s2];
+        for (int s2 = 0; s2 < kNS; ++s2) Xs[(li + 4 * s2) * kSWo + lc] = xr[s2];
+#pragma unroll
+        for (int s2 = 0; s2 < NW; ++s2) {
             if (WT) {
                 const int k = tid + kThreadsC * s2, o = k / kCs, ii = k - o * kCs;
                 Ws[o * kSWt + ii] = wr[s2];
             } else {
-                Ws[i * kSWo + lc] = wr[s2];
+                Ws[(li + 4 * (s2 % kNS)) * SWo + lc + 64 * (s2 / kNS)] = wr[s2];
             }
         }
         __syncthreads();
@@ -140,27 +150,24 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
 #pragma unroll
         for (int kk = 0; kk < kCs; kk += 4) {
             const int ki = kk + gg;
-            float a0, a1;
-            if (WT) {
-                a0 = Ws[(osub + n) * kSWt + ki];
-                a1 = Ws[(osub + 16 + n) * kSWt + ki];
-            } else {
-                a0 = Ws[ki * kSWo + osub + n];
-                a1 = Ws[ki * kSWo + osub + 16 + n];
-            }
+            float av[OTW];
+#pragma unroll
+            for (int a = 0; a < OTW; ++a)
+                av[a] = WT ? Ws[(osub + 16 * a + n) * kSWt + ki] : Ws[ki * SWo + osub + 16 * a + n];
             const float b0v = Xs[ki * kSWo + csub + n];
             const float b1v = Xs[ki * kSWo + csub + 16 + n];
-            acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0v, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1v, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0v, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1v, acc[1][1], 0, 0, 0);
+#pragma unroll
+            for (int a = 0; a < OTW; ++a) {
+                acc[a][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], b0v, acc[a][0], 0, 0, 0);
+                acc[a][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], b1v, acc[a][1], 0, 0, 0);
+            }
         }
     }
 
     const float sc = scale ? scale[l] : 1.f;
     // D[row][col] of a 16 x 16 tile: lane holds rows 4*(lane/16) + j, column lane % 16
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < OTW; ++a)
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb) {
             int c = c0 + csub + 16 * bb + n;
@@ -376,17 +383,24 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
     }
     const int64_t groups = (B + kTile - 1) / kTile;
     const int tiles_per_group = K;  // sum over degrees of the (2l+1) tiles of 64 columns
-    const int otiles = (Cout + kTile - 1) / kTile;
+    // 128 outputs per block once there are that many: each X slice is staged once for them
+    const bool wide = Cout >= 128;
+    const int ot_rows = wide ? 128 : kTile;
+    const int otiles = (Cout + ot_rows - 1) / ot_rows;
     const int64_t blocks = groups * tiles_per_group * otiles;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    if (w_si == 1)
-        hipLaunchKernelGGL(k_contract_mfma<true>, dim3((unsigned)blocks), dim3(kThreadsC), 0, s, B,
-                           Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, x_sb, Y,
-                           y_sb, y_so, y_sk, scale, accumulate);
-    else
-        hipLaunchKernelGGL(k_contract_mfma<false>, dim3((unsigned)blocks), dim3(kThreadsC), 0, s,
-                           B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X, x_sb,
-                           Y, y_sb, y_so, y_sk, scale, accumulate);
+#define CGTP_CONTRACT(WTV, OTV)                                                                 \
+    hipLaunchKernelGGL((k_contract_mfma<WTV, OTV>), dim3((unsigned)blocks), dim3(kThreadsC), 0, \
+                       s, B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X,     \
+                       x_sb, Y, y_sb, y_so, y_sk, scale, accumulate)
+    if (w_si == 1) {
+        if (wide) CGTP_CONTRACT(true, 128);
+        else CGTP_CONTRACT(true, 64);
+    } else {
+        if (wide) CGTP_CONTRACT(false, 128);
+        else CGTP_CONTRACT(false, 64);
+    }
+#undef CGTP_CONTRACT
     return hipGetLastError();
 }
 
