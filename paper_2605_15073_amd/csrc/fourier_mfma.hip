@@ -315,27 +315,33 @@ struct FieldsTiles {
 // edge). The products accumulate in registers over the CSR row; the sums go to
 // S [N][R][2][UVs] for k_analysis_mfma. Blocks run rank block by rank block, all receivers
 // inside one, so the memory-side cache serves a rank slice of the sender fields.
-template <int LM>
+// SPLIT: the value field comes from the rows HE (Gaunt factors) and the two derivative
+// fields from the rows HEc (curl factors); both row sets are staged and the Legendre pass
+// runs over both.
+template <int LM, bool SPLIT>
 __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, int R, int rb,
-                                                               const int32_t *__restrict__ row_ptr,
-                                                               const int32_t *__restrict__ col,
-                                                               const float *__restrict__ HE,
-                                                               const float *__restrict__ SF,
-                                                               float *__restrict__ S)
+                                                              const int32_t *__restrict__ row_ptr,
+                                                              const int32_t *__restrict__ col,
+                                                              const float *__restrict__ HE,
+                                                              const float *__restrict__ HEc,
+                                                              const float *__restrict__ SF,
+                                                              float *__restrict__ S)
 {
     using G = Grid<LM>;
     constexpr int KPT = FieldsTiles<LM>::KPT;
+    constexpr int NS = SPLIT ? 2 : 1;  // coefficient row sets per edge
     extern __shared__ float smem[];
     float4_t *cf = reinterpret_cast<float4_t *>(smem);  // [P] recurrence coefficients
     float *qs = smem + 4 * G::P;                         // [4 KM][QB]: q_vm as [m][v]
-    float *Hs = qs + 4 * G::KM * G::QB;                  // [2][rb][HR] this / the next edge
+    float *Hs = qs + 4 * G::KM * G::QB;                  // [2][NS][rb][HR] this / the next edge
     const int nrb = (R + rb - 1) / rb;
     const int64_t NN = (int64_t)gridDim.x / nrb;
     const int cb = (int)(blockIdx.x / NN);
     const int64_t i = blockIdx.x - (int64_t)cb * NN;
     const int r0 = cb * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
-    const int nh = nr * G::HR;  // staged elements of one edge
+    const int nh = nr * G::HR;          // staged elements of one row set
+    const int hset = rb * G::HR;        // LDS stride of a row set
     stage_q<LM>(tb, qs, 4 * G::KM, G::QB, false);
     stage_coefs<LM>(tb, cf);
 
@@ -348,7 +354,7 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
     float seed[G::KM];
     load_seeds<LM>(tb, g4, ua, seed);
     const float sxu = tb.sx[ua];
-    LaneRows<LM, 1> c;
+    LaneRows<LM, NS> c;
     c.cf = cf;
     c.seed = seed;
     c.x = tb.x[ua];
@@ -365,15 +371,19 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
 #pragma unroll
     for (int t = 0; t < G::VT; ++t) sa[t] = sb[t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-    // staging of a margin-padded coefficient row element k = q HR + HL + i of an edge
-    auto coef = [&](const float *he, int k) -> float {
-        const int q = k / G::HR, ii = k - q * G::HR - G::HL;
-        return (k < nh && ii >= 0 && ii < G::K) ? he[q * G::K + ii] : 0.f;
+    // staged element k of an edge: row set k / nh, then the margin-padded row element
+    // q HR + HL + i of that set
+    auto coef = [&](int64_t e, int k) -> float {
+        const int set = (SPLIT && k >= nh) ? 1 : 0;
+        const int kk = k - set * nh;
+        const int q = kk / G::HR, ii = kk - q * G::HR - G::HL;
+        const float *he = (set ? HEc : HE) + (e * R + r0) * G::K;
+        return (k < NS * nh && ii >= 0 && ii < G::K) ? he[q * G::K + ii] : 0.f;
     };
+    auto slot_of = [&](int k) { return (SPLIT && k >= nh) ? hset + (k - nh) : k; };
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     if (e0 < e1) {
-        const float *he = HE + ((int64_t)e0 * R + r0) * G::K;
-        for (int k = threadIdx.x; k < nh; k += blockDim.x) Hs[k] = coef(he, k);
+        for (int k = threadIdx.x; k < NS * nh; k += blockDim.x) Hs[slot_of(k)] = coef(e0, k);
     }
     __syncthreads();
     for (int e = e0; e < e1; ++e) {
@@ -398,14 +408,23 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
         float hn[KPT];
         const bool more = e + 1 < e1;
         if (more) {
-            const float *he = HE + ((int64_t)(e + 1) * R + r0) * G::K;
 #pragma unroll
-            for (int t = 0; t < KPT; ++t) hn[t] = coef(he, threadIdx.x + t * blockDim.x);
+            for (int t = 0; t < KPT; ++t) hn[t] = coef(e + 1, threadIdx.x + t * blockDim.x);
         }
         if (rt * 16 < rows) {  // wave-uniform: waves past the last tile only help stage rows
-            c.h[0] = Hs + cur * rb * G::HR + qa * G::HR + G::HL;
+            float *hcur = Hs + cur * NS * hset;
+            c.h[0] = hcur + qa * G::HR + G::HL;
+            if (SPLIT) c.h[NS - 1] = hcur + hset + qa * G::HR + G::HL;
+            float bfa[G::KM][NS][3];
+            legendre_all<LM, NS, 0>(c, bfa);
+            // value from the first row set, the derivative fields from the last
             float bf[G::KM][1][3];
-            legendre_all<LM, 1, 0>(c, bf);
+#pragma unroll
+            for (int kk = 0; kk < G::KM; ++kk) {
+                bf[kk][0][0] = bfa[kk][0][0];
+                bf[kk][0][1] = bfa[kk][NS - 1][1];
+                bf[kk][0][2] = bfa[kk][NS - 1][2];
+            }
 #pragma unroll
             for (int t = 0; t < G::VT; ++t) {
                 float4_t acc[3] = {float4_t{0.f, 0.f, 0.f, 0.f}, float4_t{0.f, 0.f, 0.f, 0.f},
@@ -426,11 +445,11 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
             }
         }
         if (more) {
-            float *hnext = Hs + (cur ^ 1) * rb * G::HR;
+            float *hnext = Hs + (cur ^ 1) * NS * hset;
 #pragma unroll
             for (int t = 0; t < KPT; ++t) {
                 const int k = threadIdx.x + t * blockDim.x;
-                if (k < nh) hnext[k] = hn[t];
+                if (k < NS * nh) hnext[slot_of(k)] = hn[t];
             }
         }
         __syncthreads();  // the next rows are staged; this edge's rows are consumed
@@ -775,37 +794,43 @@ hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
 
 template <int LM>
 hipError_t receiver_fields_lm(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
-                              const int32_t *col, const float *HE, const float *SF, float *S,
-                              hipStream_t s)
+                              const int32_t *col, const float *HE, const float *HEc,
+                              const float *SF, float *S, hipStream_t s)
 {
     using G = Grid<LM>;
+    const int ns = HEc ? 2 : 1;
     int rb = FieldsTiles<LM>::RB;
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorNotSupported;
     const int waves = (rb * G::U + 15) / 16;
     // every staged row element is fetched by some thread's prefetch
-    if ((size_t)rb * G::HR > (size_t)FieldsTiles<LM>::KPT * 64 * waves) return hipErrorNotSupported;
+    if ((size_t)ns * rb * G::HR > (size_t)FieldsTiles<LM>::KPT * 64 * waves)
+        return hipErrorNotSupported;
     const size_t sh = sizeof(float) * (4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB +
-                                       2 * (size_t)rb * G::HR);
+                                       2 * (size_t)ns * rb * G::HR);
     if (sh > 65536) return hipErrorNotSupported;
     const int64_t blocks = N * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_receiver_fields_mfma<LM>), dim3((unsigned)blocks), dim3(64 * waves), sh,
-                       s, tb, R, rb, row_ptr, col, HE, SF, S);
+    if (HEc)
+        hipLaunchKernelGGL((k_receiver_fields_mfma<LM, true>), dim3((unsigned)blocks),
+                           dim3(64 * waves), sh, s, tb, R, rb, row_ptr, col, HE, HEc, SF, S);
+    else
+        hipLaunchKernelGGL((k_receiver_fields_mfma<LM, false>), dim3((unsigned)blocks),
+                           dim3(64 * waves), sh, s, tb, R, rb, row_ptr, col, HE, HEc, SF, S);
     return hipGetLastError();
 }
 
 hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const int32_t *row_ptr, const int32_t *col,
-                                       const float *HE, const float *SF, float *S, float *Ta,
-                                       float *Tb, hipStream_t s)
+                                       const float *HE, const float *HEc, const float *SF,
+                                       float *S, float *Ta, float *Tb, hipStream_t s)
 {
     if (N == 0) return hipSuccess;
     if (!sender_mfma_supported(tb.d)) return hipErrorNotSupported;
     hipError_t e = hipErrorNotSupported;
     switch (tb.d.lmax) {
 #define CGTP_CASE(LMV) \
-    case LMV: e = receiver_fields_lm<LMV>(tb, N, R, row_ptr, col, HE, SF, S, s); break;
+    case LMV: e = receiver_fields_lm<LMV>(tb, N, R, row_ptr, col, HE, HEc, SF, S, s); break;
         CGTP_LMAX_CASES(CGTP_CASE)
 #undef CGTP_CASE
     default: return hipErrorNotSupported;

@@ -131,10 +131,12 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
 // fp32 edge-field receiver on MFMA (fourier_mfma.hip), default grid: the summed grid fields
 // go to S [N][R][2][UVs] and the inverse transforms into Ta, Tb follow. SF in the layout
 // [N][R][3][UVs]. hipErrorNotSupported off the default grid.
+// HEc: NULL, or the edge coefficients of the curl factors (then HE holds the Gaunt factors'
+// and gives the value field, HEc the two derivative fields).
 hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const int32_t *row_ptr, const int32_t *col,
-                                       const float *HE, const float *SF, float *S, float *Ta,
-                                       float *Tb, hipStream_t s);
+                                       const float *HE, const float *HEc, const float *SF,
+                                       float *S, float *Ta, float *Tb, hipStream_t s);
 
 // nu-body on-site grid product (kernels.hip): Tout[b][r][K] = the analysis of the pointwise
 // product of the nu fields synthesised from H.h[t][b][r][K]. The grid of tb must be fine

@@ -138,21 +138,26 @@ bool use_mfma_fields(const cgtp_plan_s *p)
 }
 
 // Workspace of message passing with a general edge field: HI [N][R][K], SF [N][R][3][UVs],
-// HE [E][R][K], Ta, Tb [N][R][K], and S [N][R][2][UVs] for the MFMA receiver.
-Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E)
+// HE [E][R][K], Ta, Tb [N][R][K], S [N][R][2][UVs] for the MFMA receiver, and the
+// concatenated factor blocks. With split factors HI and HE are followed by the curl
+// factors' contractions.
+Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool split = false)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
+    const size_t ns = split ? 2 : 1;
     size_t h = align256(es * (size_t)N * R * p->d.K);
     size_t sf = align256(es * (size_t)N * R * 3 * p->d.UVs);
     size_t he = align256(es * (size_t)E * R * p->d.K);
     size_t sg = use_mfma_fields(p) ? align256(es * (size_t)N * R * 2 * p->d.UVs) : 0;
     Layout l{};
     l.off[0] = 0;
-    l.off[1] = h;
-    l.off[2] = h + sf;
-    l.off[3] = h + sf + he;
+    l.off[1] = ns * h;
+    l.off[2] = ns * h + sf;
+    l.off[3] = l.off[2] + ns * he;
     l.off[4] = l.off[3] + h;
     l.off[5] = l.off[4] + h;
+    l.hf = h;
+    l.rtf = he;
     l.wc = l.off[5] + sg;
     l.total = l.wc + align256(es * (size_t)p->d.L * p->C * R);
     return l;
@@ -550,11 +555,14 @@ int project_blocks(const cgtp_plan_s *p, const Groups &G, int64_t N, const Facto
 // Channel contraction of every group's operand (first when first, else second) into
 // H [rows][G R][K]: one launch per run of consecutive groups that read the same operand slot,
 // with the runs' factor blocks concatenated along the rank into wcat [L][C][n R].
+// side: 0 the group's one contraction (group_block), 1 its Gaunt factors (bg), 2 its curl
+// factors (bc).
 template <typename T>
 hipError_t contract_runs(const cgtp_plan_s *p, const Groups &G, int64_t rows, bool first,
                          const void *const X[2], const void *const fac[4], T *H, T *wcat,
-                         hipStream_t s)
+                         hipStream_t s, int side = 0)
 {
+    auto blk = [&](const Group &g) { return side == 1 ? g.bg : side == 2 ? g.bc : group_block(g); };
     const cgtp::Dims &d = p->d;
     const int C = p->C, R = p->R, Rg = G.n * R;
     const size_t es = sizeof(T);
@@ -564,11 +572,11 @@ hipError_t contract_runs(const cgtp_plan_s *p, const Groups &G, int64_t rows, bo
         int g1 = g0 + 1;
         while (g1 < G.n && (first ? G.g[g1].s1 : G.g[g1].s2) == slot) ++g1;
         const int n = g1 - g0;
-        const T *W = static_cast<const T *>(fac[group_block(G.g[g0])]);
+        const T *W = static_cast<const T *>(fac[blk(G.g[g0])]);
         if (n > 1) {
             for (int gi = g0; gi < g1; ++gi) {
                 hipError_t e = hipMemcpy2DAsync(wcat + (size_t)(gi - g0) * R, es * n * R,
-                                                fac[group_block(G.g[gi])], es * R, es * R,
+                                                fac[blk(G.g[gi])], es * R, es * R,
                                                 (size_t)d.L * C, hipMemcpyDeviceToDevice, s);
                 if (e != hipSuccess) return e;
             }
@@ -703,30 +711,39 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     const cgtp::Dims &d = p->d;
     const int Rg = G.n * p->R;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
-    Layout lay = mpf_layout(p, Rg, N, E);
+    Layout lay = mpf_layout(p, Rg, N, E, G.split);
     T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
     T *SF = reinterpret_cast<T *>(ws + lay.off[1]);
     T *HE = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Ta = reinterpret_cast<T *>(ws + lay.off[3]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[4]);
+    // split: the curl factors' node and edge contractions
+    T *HIc = G.split ? reinterpret_cast<T *>(ws + lay.off[0] + lay.hf) : nullptr;
+    T *HEc = G.split ? reinterpret_cast<T *>(ws + lay.off[2] + lay.rtf) : nullptr;
     StageRec rec;
     int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_FIELDS, 6, s);
     if (st) return st;
     hipError_t e;
     T *wc = reinterpret_cast<T *>(ws + lay.wc);
-    e = contract_runs<T>(p, G, N, false, X2, f.in2, HI, wc, s);
+    e = contract_runs<T>(p, G, N, false, X2, f.in2, HI, wc, s, G.split ? 1 : 0);
+    if (e == hipSuccess && G.split) e = contract_runs<T>(p, G, N, false, X2, f.in2, HIc, wc, s, 2);
     if (e != hipSuccess) return hip_fail(e, "contract node features");
     rec.mark();
-    e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s);
+    // split: the Gaunt factors' contraction gives the sender values, the curl factors' the
+    // two derivative fields, into the same field slots
+    e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s, G.split ? 1 : 7);
+    if (e == hipSuccess && G.split) e = cgtp::launch_sender_fields<T>(tb, N, Rg, HIc, SF, s, 6);
     if (e != hipSuccess) return hip_fail(e, "sender fields");
     rec.mark();
-    e = contract_runs<T>(p, G, E, true, X1, f.in1, HE, wc, s);
+    e = contract_runs<T>(p, G, E, true, X1, f.in1, HE, wc, s, G.split ? 1 : 0);
+    if (e == hipSuccess && G.split) e = contract_runs<T>(p, G, E, true, X1, f.in1, HEc, wc, s, 2);
     if (e != hipSuccess) return hip_fail(e, "contract edge field");
     rec.mark();
     if constexpr (sizeof(T) == 4) {
         if (use_mfma_fields(p)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
-            e = cgtp::launch_receiver_fields_mfma(tb, N, Rg, row_ptr, col, HE, SF, Sg, Ta, Tb, s);
+            e = cgtp::launch_receiver_fields_mfma(tb, N, Rg, row_ptr, col, HE, HEc, SF, Sg, Ta, Tb,
+                                                  s);
             if (e != hipSuccess) return hip_fail(e, "receiver (edge field, mfma)");
             rec.mark();
             return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
@@ -1055,9 +1072,10 @@ int cgtp_workspace_bytes_general(cgtp_plan plan, int op, int64_t n_nodes, int64_
         *bytes = route_onsite(plan, n_nodes, flips & 1, flips & 2, in_blocks).ws;
     else if (op == CGTP_OP_MESSAGE_PASS_GENERAL)
         *bytes = route_mp(plan, n_nodes, n_edges, flips & 2, in_blocks, out_blocks).ws;
-    else if (op == CGTP_OP_MESSAGE_PASS_FIELDS)
-        *bytes = mpf_layout(plan, make_groups(flips & 1, flips & 2, in_blocks, false).n * plan->R,
-                            n_nodes, n_edges).total;
+    else if (op == CGTP_OP_MESSAGE_PASS_FIELDS) {
+        Groups G = make_groups(flips & 1, flips & 2, in_blocks, use_mfma_fields(plan));
+        *bytes = mpf_layout(plan, G.n * plan->R, n_nodes, n_edges, G.split).total;
+    }
     else return fail(CGTP_ERR_ARG, "unknown general op %d", op);
     return CGTP_OK;
 }
@@ -1183,7 +1201,8 @@ int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
     if (n_edges > 0 && (!col || !edge_feat)) return fail(CGTP_ERR_ARG, "NULL edge input");
     if ((out_even && !U_out_even) || (out_odd && !U_out_odd))
         return fail(CGTP_ERR_ARG, "NULL output projection");
-    Groups G = make_groups(edge_flip != nullptr, node_flip != nullptr, in_blocks, false);
+    Groups G = make_groups(edge_flip != nullptr, node_flip != nullptr, in_blocks,
+                           use_mfma_fields(plan));
     const int Rg = G.n * plan->R;
     if ((n_nodes > n_edges ? n_nodes : n_edges) * (int64_t)Rg > 0x7fffffffLL)
         return fail(CGTP_ERR_UNSUPPORTED, "rows * total rank exceeds 2^31 - 1");
@@ -1195,8 +1214,8 @@ int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
         if (st) return st;
     }
     void *ws = nullptr;
-    st = get_workspace(plan, mpf_layout(plan, Rg, n_nodes, n_edges).total, workspace, ws_bytes,
-                       &ws);
+    st = get_workspace(plan, mpf_layout(plan, Rg, n_nodes, n_edges, G.split).total, workspace,
+                       ws_bytes, &ws);
     if (st) return st;
     Factors f = resolve_factors(plan, in_blocks, U_E, U_I, out_blocks, U_out_even, U_out_odd);
     const void *X1[2] = {edge_feat, edge_flip}, *X2[2] = {node_feat, node_flip};
