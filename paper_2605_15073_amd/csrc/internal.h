@@ -101,9 +101,12 @@ hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, 
 
 // fp32 on-site grid stage for lmax <= kOnsiteFoldedMaxL (onsite.hip); returns
 // hipErrorNotSupported above that.
+// HAc, HBc: NULL, or the curl factors' contractions (then HA, HB are the Gaunt factors': the
+// product takes the values of HA, HB and the curl the derivative fields of HAc, HBc).
 constexpr int kOnsiteFoldedMaxL = 14;
 hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
-                                const float *HB, float *Ta, float *Tb, hipStream_t s);
+                                const float *HB, float *Ta, float *Tb, hipStream_t s,
+                                const float *HAc = nullptr, const float *HBc = nullptr);
 
 // Message-passing receiver pass: per receiver, synthesise the edge fields, multiply
 // with the streamed sender fields, sum over the CSR row, then the inverse transforms.

@@ -9,6 +9,11 @@
 // forms the product (Eq. struct-S) and the surface curl (Eq. poisson-S2-x), and
 // accumulates the Fourier analysis (Eq. struct-Tmu) in registers with the same
 // pairing. The Gauss-Legendre analysis across u (Eq. struct-Tlm) goes through LDS.
+//
+// With per-block factors (general parameterization) the Gaunt product takes the values of the
+// Gaunt factors' contractions HA, HB and the surface curl the derivative fields of the curl
+// factors' contractions HAc, HBc; that kernel runs the two in phases through one LDS
+// footprint.
 #include "internal.h"
 
 namespace cgtp {
@@ -162,6 +167,205 @@ hipError_t launch_folded(const Tabs<float> &tb, int64_t B, int R, const float *H
     return hipGetLastError();
 }
 
+// Azimuth sweep of one row at latitude u for the Gaunt product (Eq. struct-S): synthesise
+// A from FA and B from FB at each pair (v, V - v) and add the Fourier analysis (Eq.
+// struct-Tmu) of A B into T. qs row v holds cos(k phi_v) at LM + k and sin(k phi_v) at
+// LM - k.
+template <int LM>
+__device__ __forceinline__ void sweep_product(const float *FA, const float *FB,
+                                              const float *qs, int V, float *T)
+{
+    constexpr int M = 2 * LM + 1;
+    for (int v = 0; 2 * v <= V; ++v) {
+        const bool paired = v != 0 && 2 * v != V;
+        const float *qr = qs + v * M;
+        float aC = FA[LM], aS = 0.f, bC = FB[LM], bS = 0.f;
+#pragma unroll
+        for (int k = 1; k <= LM; ++k) {
+            const float c = qr[LM + k], s = qr[LM - k];
+            aC += c * FA[LM + k];
+            aS += s * FA[LM - k];
+            bC += c * FB[LM + k];
+            bS += s * FB[LM - k];
+        }
+        const float s0 = (aC + aS) * (bC + bS);
+        const float s1 = paired ? (aC - aS) * (bC - bS) : 0.f;
+        const float sP = s0 + s1, sM = s0 - s1;
+        T[LM] += sP;
+#pragma unroll
+        for (int k = 1; k <= LM; ++k) {
+            T[LM + k] += qr[LM + k] * sP;
+            T[LM - k] += qr[LM - k] * sM;
+        }
+    }
+}
+
+// The same sweep for the surface curl (Eq. poisson-S2-x): dA/dphi dB/dx - dA/dx dB/dphi,
+// with the phi-derivatives taken from FA, FB by swapping the cosine and sine halves.
+template <int LM>
+__device__ __forceinline__ void sweep_curl(const float *FA, const float *FxA, const float *FB,
+                                           const float *FxB, const float *qs, int V, float *T)
+{
+    constexpr int M = 2 * LM + 1;
+    for (int v = 0; 2 * v <= V; ++v) {
+        const bool paired = v != 0 && 2 * v != V;
+        const float *qr = qs + v * M;
+        float axC = FxA[LM], axS = 0.f, apC = 0.f, apS = 0.f;
+        float bxC = FxB[LM], bxS = 0.f, bpC = 0.f, bpS = 0.f;
+#pragma unroll
+        for (int k = 1; k <= LM; ++k) {
+            const float c = qr[LM + k], s = qr[LM - k];
+            const float kc = (float)k * c, ks = (float)k * s;
+            axC += c * FxA[LM + k];
+            axS += s * FxA[LM - k];
+            apC += kc * FA[LM - k];
+            apS -= ks * FA[LM + k];
+            bxC += c * FxB[LM + k];
+            bxS += s * FxB[LM - k];
+            bpC += kc * FB[LM - k];
+            bpS -= ks * FB[LM + k];
+        }
+        const float s0 = (apC + apS) * (bxC + bxS) - (axC + axS) * (bpC + bpS);
+        const float s1 =
+            paired ? (apC - apS) * (bxC - bxS) - (axC - axS) * (bpC - bpS) : 0.f;
+        const float sP = s0 + s1, sM = s0 - s1;
+        T[LM] += sP;
+#pragma unroll
+        for (int k = 1; k <= LM; ++k) {
+            T[LM + k] += qr[LM + k] * sP;
+            T[LM - k] += qr[LM - k] * sM;
+        }
+    }
+}
+
+// Per-block factors: phase 0 stages the Gaunt rows HA, HB and writes the product's
+// coefficients to Ta, phase 1 stages the curl rows HAc, HBc into the same LDS and writes the
+// curl's to Tb. One (rank, u) thread per row, as above; Tm holds one product at a time.
+template <int LM>
+__global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int rb,
+                                                      const float *__restrict__ HA,
+                                                      const float *__restrict__ HB,
+                                                      const float *__restrict__ HAc,
+                                                      const float *__restrict__ HBc,
+                                                      float *__restrict__ Ta,
+                                                      float *__restrict__ Tb)
+{
+    constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
+    extern __shared__ float smem[];
+    const int U = tb.d.U, V = tb.d.V;
+    float *qs = smem;              // [V][M]
+    float *ps = qs + V * M;        // [U][P]
+    float *dps = ps + U * P;       // [U][P]
+    float *Hs = dps + U * P;       // [2][rb][K]
+    float *Tm = Hs + 2 * rb * K;   // [rb][M][U]
+
+    const int nrb = (R + rb - 1) / rb;
+    const int64_t b = blockIdx.x / nrb;
+    const int r0 = (int)(blockIdx.x - b * nrb) * rb;
+    const int nr = (R - r0 < rb) ? (R - r0) : rb;
+    for (int k = threadIdx.x; k < V * M; k += blockDim.x) qs[k] = tb.q[k];
+    for (int k = threadIdx.x; k < U * P; k += blockDim.x) {
+        ps[k] = tb.p[k];
+        dps[k] = tb.dp[k];
+    }
+    const int q = threadIdx.x / U, u = threadIdx.x - q * U;
+    const bool active = q < nr;
+    const float *pu = ps + u * P, *dpu = dps + u * P;
+    const float *h1 = Hs + q * K, *h2 = Hs + (rb + q) * K;
+    for (int ph = 0; ph < 2; ++ph) {
+        // the previous phase's sweep has read Hs and its analysis Tm before the barrier
+        // that follows this staging
+        const float *src1 = (ph ? HAc : HA) + (b * R + r0) * (int64_t)K;
+        const float *src2 = (ph ? HBc : HB) + (b * R + r0) * (int64_t)K;
+        for (int k = threadIdx.x; k < nr * K; k += blockDim.x) {
+            Hs[k] = src1[k];
+            Hs[rb * K + k] = src2[k];
+        }
+        __syncthreads();
+        if (active) {
+            float T[M];
+#pragma unroll
+            for (int mi = 0; mi < M; ++mi) T[mi] = 0.f;
+            if (ph == 0) {
+                float FA[M], FB[M];
+#pragma unroll
+                for (int mi = 0; mi < M; ++mi) {
+                    const int m = mi - LM, am = m < 0 ? -m : m;
+                    float f1 = 0.f, f2 = 0.f;
+#pragma unroll
+                    for (int l = am; l <= LM; ++l) {
+                        const float p = pu[l * (l + 1) / 2 + am];
+                        f1 += p * h1[l * l + l + m];
+                        f2 += p * h2[l * l + l + m];
+                    }
+                    FA[mi] = f1;
+                    FB[mi] = f2;
+                }
+                sweep_product<LM>(FA, FB, qs, V, T);
+            } else {
+                float FA[M], FxA[M], FB[M], FxB[M];
+#pragma unroll
+                for (int mi = 0; mi < M; ++mi) {
+                    const int m = mi - LM, am = m < 0 ? -m : m;
+                    float f1 = 0.f, g1 = 0.f, f2 = 0.f, g2 = 0.f;
+#pragma unroll
+                    for (int l = am; l <= LM; ++l) {
+                        const float p = pu[l * (l + 1) / 2 + am], dp = dpu[l * (l + 1) / 2 + am];
+                        const float c1 = h1[l * l + l + m], c2 = h2[l * l + l + m];
+                        f1 += p * c1;
+                        g1 += dp * c1;
+                        f2 += p * c2;
+                        g2 += dp * c2;
+                    }
+                    FA[mi] = f1;
+                    FxA[mi] = g1;
+                    FB[mi] = f2;
+                    FxB[mi] = g2;
+                }
+                sweep_curl<LM>(FA, FxA, FB, FxB, qs, V, T);
+            }
+            float *tm = Tm + q * M * U;
+#pragma unroll
+            for (int mi = 0; mi < M; ++mi) tm[mi * U + u] = T[mi];
+        }
+        __syncthreads();
+        // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
+        float *dst = ph ? Tb : Ta;
+        for (int idx = threadIdx.x; idx < nr * K; idx += blockDim.x) {
+            const int qq = idx / K, k = idx - qq * K;
+            int l = (int)sqrtf((float)k);
+            while (l * l > k) --l;
+            while ((l + 1) * (l + 1) <= k) ++l;
+            const int m = k - l * l - l, am = m < 0 ? -m : m;
+            const float *tm = Tm + qq * M * U + (m + LM) * U;
+            const int pi = l * (l + 1) / 2 + am;
+            float s = 0.f;
+            for (int uu = 0; uu < U; ++uu) s += tb.wq[uu] * ps[uu * P + pi] * tm[uu];
+            dst[(b * R + r0 + qq) * (int64_t)K + k] = s;
+        }
+    }
+}
+
+template <int LM>
+hipError_t launch_split(const Tabs<float> &tb, int64_t B, int R, const float *HA,
+                        const float *HB, const float *HAc, const float *HBc, float *Ta,
+                        float *Tb, hipStream_t s)
+{
+    constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
+    const int U = tb.d.U, V = tb.d.V;
+    int rb = 256 / U;
+    if (rb > R) rb = R;
+    if (rb < 1) return hipErrorInvalidValue;
+    auto lds = [&](int r) { return sizeof(float) * (V * M + 2 * U * P + 2 * r * K + r * M * U); };
+    while (rb > 1 && lds(rb) > 65536) --rb;
+    if (lds(rb) > 65536) return hipErrorInvalidValue;
+    const int threads = (rb * U + 63) / 64 * 64;
+    const int64_t blocks = B * ((R + rb - 1) / rb);
+    hipLaunchKernelGGL((k_onsite_split<LM>), dim3((unsigned)blocks), dim3(threads), lds(rb), s,
+                       tb, R, rb, HA, HB, HAc, HBc, Ta, Tb);
+    return hipGetLastError();
+}
+
 // nu-body product in the folded form (fp32, lmax <= kNbodyFoldedMaxL, NU operands): one
 // thread per (rank, Gauss-Legendre node u) keeps the Legendre coefficients F_t[m] of every
 // operand in registers (Eq. struct-F), sweeps the azimuth in pairs (v, V - v) forming each
@@ -294,12 +498,17 @@ hipError_t launch_nbody_folded_nu(const Tabs<float> &tb, int64_t B, int R, int n
 }  // namespace
 
 hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
-                                const float *HB, float *Ta, float *Tb, hipStream_t s)
+                                const float *HB, float *Ta, float *Tb, hipStream_t s,
+                                const float *HAc, const float *HBc)
 {
     if (B == 0) return hipSuccess;
+    if ((HAc == nullptr) != (HBc == nullptr)) return hipErrorInvalidValue;
+    const bool split = HAc != nullptr;
     switch (tb.d.lmax) {
 #define CGTP_CASE(LMV) \
-    case LMV: return launch_folded<LMV>(tb, B, R, HA, HB, Ta, Tb, s);
+    case LMV: \
+        return split ? launch_split<LMV>(tb, B, R, HA, HB, HAc, HBc, Ta, Tb, s) \
+                     : launch_folded<LMV>(tb, B, R, HA, HB, Ta, Tb, s);
         CGTP_CASE(0) CGTP_CASE(1) CGTP_CASE(2) CGTP_CASE(3) CGTP_CASE(4) CGTP_CASE(5)
         CGTP_CASE(6) CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11)
         CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)

@@ -90,16 +90,25 @@ bool sf_chunked(const cgtp_plan_s *p, int R)
 }
 
 // On-site workspace: HA, HB, Ta, Tb, each [N][R][K] (R: the plan's rank, or the total
-// rank of the groups of the general path).
-Layout onsite_layout(const cgtp_plan_s *p, int R, int64_t N)
+// rank of the groups of the general path), with split factors then HAc, HBc (the curl
+// factors' contractions), and the concatenated factor blocks of a run of groups.
+Layout onsite_layout(const cgtp_plan_s *p, int R, int64_t N, bool split = false)
 {
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
     size_t blk = align256(es * (size_t)N * R * p->d.K);
+    const int nb = split ? 6 : 4;
     Layout l{};
-    for (int i = 0; i < 4; ++i) l.off[i] = i * blk;
-    l.wc = 4 * blk;
-    l.total = 4 * blk + align256(es * (size_t)p->d.L * p->C * R);
+    for (int i = 0; i < 6; ++i) l.off[i] = i * blk;  // HA, HB, Ta, Tb (, HAc, HBc)
+    l.wc = nb * blk;
+    l.total = nb * blk + align256(es * (size_t)p->d.L * p->C * R);
     return l;
+}
+
+// The general on-site call splits its rank groups (one per slot pair, Gaunt and curl
+// factors apart) on the folded kernel: fp32, lmax within its range.
+bool onsite_split_ok(const cgtp_plan_s *p)
+{
+    return p->dtype == CGTP_F32 && p->d.lmax <= cgtp::kOnsiteFoldedMaxL;
 }
 
 // Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],
@@ -600,22 +609,35 @@ int run_onsite_groups(cgtp_plan_s *p, const Groups &G, int64_t N, const void *co
     const cgtp::Dims &d = p->d;
     const int Rg = G.n * p->R;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
-    Layout lay = onsite_layout(p, Rg, N);
+    Layout lay = onsite_layout(p, Rg, N, G.split);
     T *HA = reinterpret_cast<T *>(ws + lay.off[0]);
     T *HB = reinterpret_cast<T *>(ws + lay.off[1]);
     T *Ta = reinterpret_cast<T *>(ws + lay.off[2]);
     T *Tb = reinterpret_cast<T *>(ws + lay.off[3]);
+    T *HAc = G.split ? reinterpret_cast<T *>(ws + lay.off[4]) : nullptr;
+    T *HBc = G.split ? reinterpret_cast<T *>(ws + lay.off[5]) : nullptr;
     StageRec rec;
     int st = rec.begin(p, CGTP_OP_ONSITE_GENERAL, 5, s);
     if (st) return st;
     hipError_t e;
     T *wc = reinterpret_cast<T *>(ws + lay.wc);
-    e = contract_runs<T>(p, G, N, true, X1, f.in1, HA, wc, s);
+    const int side = G.split ? 1 : 0;  // split: Gaunt factors first, then the curl factors
+    e = contract_runs<T>(p, G, N, true, X1, f.in1, HA, wc, s, side);
+    if (e == hipSuccess && G.split) e = contract_runs<T>(p, G, N, true, X1, f.in1, HAc, wc, s, 2);
     if (e != hipSuccess) return hip_fail(e, "contract first operand");
     rec.mark();
-    e = contract_runs<T>(p, G, N, false, X2, f.in2, HB, wc, s);
+    e = contract_runs<T>(p, G, N, false, X2, f.in2, HB, wc, s, side);
+    if (e == hipSuccess && G.split) e = contract_runs<T>(p, G, N, false, X2, f.in2, HBc, wc, s, 2);
     if (e != hipSuccess) return hip_fail(e, "contract second operand");
     rec.mark();
+    if constexpr (sizeof(T) == 4) {
+        if (G.split) {
+            e = cgtp::launch_onsite_folded(tb, N, Rg, HA, HB, Ta, Tb, s, HAc, HBc);
+            if (e != hipSuccess) return hip_fail(e, "onsite grid (split)");
+            rec.mark();
+            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+        }
+    }
     e = cgtp::launch_onsite_grid<T>(tb, N, Rg, HA, HB, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "onsite grid");
     rec.mark();
@@ -813,8 +835,8 @@ GeneralRoute route_onsite(const cgtp_plan_s *p, int64_t N, bool f1, bool f2, int
     if (r.fused) {
         r.ws = onsite_layout(p, p->R, N).total;
     } else {
-        r.G = make_groups(f1, f2, in_blocks, false);
-        r.ws = onsite_layout(p, r.G.n * p->R, N).total;
+        r.G = make_groups(f1, f2, in_blocks, onsite_split_ok(p));
+        r.ws = onsite_layout(p, r.G.n * p->R, N, r.G.split).total;
     }
     return r;
 }

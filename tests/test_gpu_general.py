@@ -141,7 +141,7 @@ def test_onsite_general_workspace_errors_and_stages(cg):
     N = d["A"].shape[0]
     need = cg.workspace_bytes_general(plan, cg.CGTP_OP_ONSITE_GENERAL, N, 0, 3, 4, 2)
     plain = cg.workspace_bytes(plan, cg.CGTP_OP_ONSITE, N)
-    assert need >= 8 * plain - 8 * 4 * 256  # eight rank groups (each buffer 256-aligned)
+    assert need > 2 * plain  # stacked rank groups (their number depends on the lowering)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     _check(_on_gpu(cg, plan, t, workspace=ws), _on_ref(lmax, d), TOL_F32)
     with pytest.raises(cg.CgtpError) as ei:
