@@ -193,6 +193,7 @@ def _mp_ref(lmax, d, receivers=None):
     (3, 6, False, 2, 1),    # one slot, independent Gaunt / curl factors
     (5, 6, True, 1, 2),     # shared factors, per-category output weights
     (6, 9, True, 4, 2),
+    (6, 8, True, 4, 2),     # split groups stacked to 16 ranks
     (7, 16, True, 4, 2),    # MFMA receiver at 4 x 16 ranks
     (8, 16, False, 2, 2),
     (12, 16, True, 2, 1),
