@@ -231,12 +231,17 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
 
     if d is None:
         d = w.make()
+    torch.empty(1, device="cuda")  # the GPU context exists before the plan is timed
+    torch.cuda.synchronize()
+    t_plan = time.perf_counter()
     if w.kind == "nbody":
         nt, nph = cg.nbody_grid(w.lmax, w.nu)
         plan = cg.plan_create(w.lmax, w.C, w.R, n_theta=nt, n_phi=nph,
                               flags=cg.CGTP_TIME_STAGES)
     else:
         plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
+    torch.cuda.synchronize()
+    plan_ms = 1e3 * (time.perf_counter() - t_plan)  # tables built and uploaded, outside every step
     if w.kind == "nbody":
         import numpy as np
 
@@ -335,6 +340,20 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
     stages, calls = cg.stage_times(plan, op)
     assert calls == steps, (calls, steps)
     ms_step = 1e3 * wall / steps
+    # per-step times for the median, from HIP events around single steps after the timed region
+    cur = torch.cuda.current_stream()
+    singles = []
+    for _ in range(min(steps, 20)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(cur)
+        step()
+        e1.record(cur)
+        e1.synchronize()
+        singles.append(e0.elapsed_time(e1))
+    cg.stage_times(plan, op)                     # these steps do not enter the stage averages
+    singles.sort()
+    ms_median = (singles[len(singles) // 2] if len(singles) % 2
+                 else 0.5 * (singles[len(singles) // 2 - 1] + singles[len(singles) // 2]))
     stage_avg = {k: v / steps for k, v in stages.items()}
     dom = max(stage_avg, key=stage_avg.get)
     U, V = grid_dims(w.lmax)
@@ -346,6 +365,8 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         "steps": steps,
         "warmup": warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_median": ms_median,
+        "plan_create_ms": plan_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
