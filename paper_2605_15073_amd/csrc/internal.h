@@ -107,6 +107,9 @@ constexpr int kOnsiteFoldedMaxL = 14;
 hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
                                 const float *HB, float *Ta, float *Tb, hipStream_t s,
                                 const float *HAc = nullptr, const float *HBc = nullptr);
+// Whether the split form (HAc, HBc given) fits this grid: lmax in range and one rank's rows,
+// tables and coefficients within a workgroup's 64 KiB of LDS.
+bool onsite_split_supported(const Dims &d);
 
 // Message-passing receiver pass: per receiver, synthesise the edge fields, multiply
 // with the streamed sender fields, sum over the CSR row, then the inverse transforms.

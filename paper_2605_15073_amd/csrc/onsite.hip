@@ -346,17 +346,24 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
     }
 }
 
+// LDS bytes of k_onsite_split with rb ranks per block: twiddles, both Legendre tables, two
+// staged row sets and the Fourier coefficients of one product.
+size_t split_lds(const Dims &d, int rb)
+{
+    const size_t M = 2 * d.lmax + 1, L = d.lmax + 1, K = L * L, P = L * (L + 1) / 2;
+    return sizeof(float) * (d.V * M + 2 * d.U * P + rb * (2 * K + M * d.U));
+}
+
 template <int LM>
 hipError_t launch_split(const Tabs<float> &tb, int64_t B, int R, const float *HA,
                         const float *HB, const float *HAc, const float *HBc, float *Ta,
                         float *Tb, hipStream_t s)
 {
-    constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
-    const int U = tb.d.U, V = tb.d.V;
+    const int U = tb.d.U;
     int rb = 256 / U;
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorInvalidValue;
-    auto lds = [&](int r) { return sizeof(float) * (V * M + 2 * U * P + 2 * r * K + r * M * U); };
+    auto lds = [&](int r) { return split_lds(tb.d, r); };
     while (rb > 1 && lds(rb) > 65536) --rb;
     if (lds(rb) > 65536) return hipErrorInvalidValue;
     const int threads = (rb * U + 63) / 64 * 64;
@@ -496,6 +503,11 @@ hipError_t launch_nbody_folded_nu(const Tabs<float> &tb, int64_t B, int R, int n
 }
 
 }  // namespace
+
+bool onsite_split_supported(const Dims &d)
+{
+    return d.lmax <= kOnsiteFoldedMaxL && d.U <= 256 && split_lds(d, 1) <= 65536;
+}
 
 hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,
                                 const float *HB, float *Ta, float *Tb, hipStream_t s,

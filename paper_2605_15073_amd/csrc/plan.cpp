@@ -105,10 +105,11 @@ Layout onsite_layout(const cgtp_plan_s *p, int R, int64_t N, bool split = false)
 }
 
 // The general on-site call splits its rank groups (one per slot pair, Gaunt and curl
-// factors apart) on the folded kernel: fp32, lmax within its range.
+// factors apart) on the folded kernel: fp32, lmax within its range and a grid whose tables
+// fit its LDS (a plan with a larger grid override takes the unsplit groups).
 bool onsite_split_ok(const cgtp_plan_s *p)
 {
-    return p->dtype == CGTP_F32 && p->d.lmax <= cgtp::kOnsiteFoldedMaxL;
+    return p->dtype == CGTP_F32 && cgtp::onsite_split_supported(p->d);
 }
 
 // Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],

@@ -93,6 +93,15 @@ def test_onsite_general_vs_oracle(cg, lmax, n, R, flip1, flip2, nin, nout):
     _check(_on_gpu(cg, plan, _dev(d, ONSITE_G)), _on_ref(lmax, d), TOL_F32)
 
 
+def test_onsite_general_large_grid_override(cg):
+    """A plan whose grid override is too large for the split kernel's LDS (lmax 12 on a 76 x 37
+    grid) runs the general call on unsplit groups and the per-thread grid kernel."""
+    lmax = 12
+    d = _on_d(lmax, 6, 4, 4, 316, True, True, 4, 2)
+    plan = cg.plan_create(lmax, 4, 4, n_theta=76, n_phi=37)
+    _check(_on_gpu(cg, plan, _dev(d, ONSITE_G)), _on_ref(lmax, d), TOL_F32)
+
+
 def test_onsite_general_fp64(cg):
     lmax = 3
     d = _on_d(lmax, 16, 4, 5, 311, True, True, 4, 2)
