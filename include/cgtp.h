@@ -253,7 +253,8 @@ int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
  * Rank groups are stacked as in cgtp_onsite_general (up to 8x the plan's rank); query the
  * workspace with cgtp_workspace_bytes_general(CGTP_OP_MESSAGE_PASS_FIELDS). Other
  * arguments, preconditions and errors as in cgtp_message_pass; CGTP_ERR_UNSUPPORTED also
- * when the receiver's LDS staging does not fit (fp64 at the highest degrees). */
+ * when the per-point receiver (fp64, or fp32 on a grid other than the default) meets a grid
+ * of more than 2048 points or LDS staging beyond 64 KiB (fp64 at the highest degrees). */
 int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                              const int32_t *row_ptr, const int32_t *col, const void *edge_feat,
                              const void *edge_flip, const void *node_feat, const void *node_flip,

@@ -774,7 +774,10 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     }
     e = cgtp::launch_receiver_fields<T>(tb, N, Rg, row_ptr, col, HE, SF, Ta, Tb, s);
     if (e == hipErrorNotSupported)
-        return fail(CGTP_ERR_UNSUPPORTED, "edge-field receiver staging exceeds 64 KiB of LDS");
+        return fail(CGTP_ERR_UNSUPPORTED,
+                    "edge-field receiver: a grid of %d points (at most 2048 off the fp32 default "
+                    "grid) or its LDS staging (at most 64 KiB) is out of range",
+                    p->d.UV);
     if (e != hipSuccess) return hip_fail(e, "receiver (edge field)");
     rec.mark();
     return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);

@@ -194,3 +194,34 @@ def test_general_calls_deterministic(cg):
     f = _dev(_f_d(lmax, 40, 8, 8, 714, True, True, 4, 2), FK)
     a, b = _f_gpu(cg, plan, f), _f_gpu(cg, plan, f)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+# grids larger than the defaults, up to the plan's cap of 2816 points: the kernels that assume
+# the default grid hand over to their generic forms, which size their LDS from the plan
+@pytest.mark.parametrize("lmax,R,nt,nph", [
+    (4, 6, 20, 40),
+    (6, 16, 40, 70),     # split groups stacked to 32 ranks, 2800 points
+    (8, 16, 30, 60),     # matrix-core receiver range, off the default grid
+])
+def test_general_mp_grid_override(cg, lmax, R, nt, nph):
+    d = _mp_d(lmax, 40, 4, R, 720 + lmax, True, 4, 2)
+    plan = cg.plan_create(lmax, 4, R, n_theta=nt, n_phi=nph)
+    _check(_mp_gpu(cg, plan, _dev(d, MP_G)), _mp_ref(lmax, d), TOL_F32)
+
+
+# off the default grid the per-point receiver serves grids of up to 2048 points
+@pytest.mark.parametrize("lmax,R,nt,nph", [(3, 5, 16, 30), (6, 8, 32, 64)])
+def test_fields_grid_override(cg, lmax, R, nt, nph):
+    d = _f_d(lmax, 30, 4, R, 724 + lmax, True, True, 4, 2, r_cut=3.0)
+    plan = cg.plan_create(lmax, 4, R, n_theta=nt, n_phi=nph)
+    _check(_f_gpu(cg, plan, _dev(d, FK)), _f_ref(lmax, d), TOL_F32)
+
+
+def test_fields_grid_beyond_per_point_receiver(cg):
+    """More than 2048 points off the default grid: a clear error, nothing launched."""
+    lmax = 6
+    d = _f_d(lmax, 30, 4, 8, 726, True, True, 4, 2, r_cut=3.0)
+    plan = cg.plan_create(lmax, 4, 8, n_theta=40, n_phi=70)
+    with pytest.raises(cg.CgtpError) as ei:
+        _f_gpu(cg, plan, _dev(d, FK))
+    assert ei.value.status == cg.CGTP_ERR_UNSUPPORTED and "2048" in str(ei.value)
