@@ -61,12 +61,14 @@ constexpr int kNS = kTile * kCs / kThreadsC;  // staged elements per thread, per
 
 // OT output rows per block (64 or 128): wave (wo, wc) owns OT / 2 rows x 32 columns, i.e.
 // OT / 32 x 2 MFMA tiles, so a block with OT = 128 stages each X slice once for 128 outputs.
-template <bool WT, int OT>
+// GATHER: input rows [c rows, (c + 1) rows) come from xg.base[c] (each with row stride x_sb
+// and its rows at stride K); rows is a multiple of the slice kCs, so a slice reads one source.
+template <bool WT, int OT, bool GATHER>
 __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     int64_t B, int Cin, int Cout, int K, int tiles_per_group, int otiles,
     const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
     const float *__restrict__ X, int64_t x_sb, float *__restrict__ Y, int64_t y_sb, int64_t y_so,
-    int64_t y_sk, const float *__restrict__ scale, bool accumulate)
+    int64_t y_sk, const float *__restrict__ scale, bool accumulate, XGather xg)
 {
     constexpr int SWo = OT + 16;                 // LDS row stride of Ws[i][o]: 16 mod 32
     constexpr int NW = OT * kCs / kThreadsC;     // staged W elements per thread
@@ -112,13 +114,17 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     const bool c_ok = cg < ncols;
     const int bl = c_ok ? cg / width : 0;
     const int mm = c_ok ? cg - bl * width : 0;
-    const float *xcol = X + (b0 + bl) * x_sb + kofs + mm;
+    const int64_t xoff = (b0 + bl) * x_sb + kofs + mm;
     float wr[NW], xr[kNS];
     auto fetch = [&](int i0) {
+        // the slice's source and its first row there (the whole slice lies in one source)
+        const int src = GATHER ? i0 / xg.rows : 0;
+        const float *xcol = (GATHER ? xg.base[src] : X) + xoff;
+        const int ib = GATHER ? i0 - src * xg.rows : i0;
 #pragma unroll
         for (int s2 = 0; s2 < kNS; ++s2) {
             const int ig = i0 + li + 4 * s2;
-            xr[s2] = (ig < Cin && c_ok) ? xcol[(int64_t)ig * K] : 0.f;
+            xr[s2] = (ig < Cin && c_ok) ? xcol[(int64_t)(ib + li + 4 * s2) * K] : 0.f;
         }
 #pragma unroll
         for (int s2 = 0; s2 < NW; ++s2) {
@@ -389,10 +395,40 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
     const int otiles = (Cout + ot_rows - 1) / ot_rows;
     const int64_t blocks = groups * tiles_per_group * otiles;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-#define CGTP_CONTRACT(WTV, OTV)                                                                 \
-    hipLaunchKernelGGL((k_contract_mfma<WTV, OTV>), dim3((unsigned)blocks), dim3(kThreadsC), 0, \
-                       s, B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, w_si, w_so, X,     \
-                       x_sb, Y, y_sb, y_so, y_sk, scale, accumulate)
+    const XGather none{};
+#define CGTP_CONTRACT(WTV, OTV)                                                                  \
+    hipLaunchKernelGGL((k_contract_mfma<WTV, OTV, false>), dim3((unsigned)blocks),               \
+                       dim3(kThreadsC), 0, s, B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, \
+                       w_si, w_so, X, x_sb, Y, y_sb, y_so, y_sk, scale, accumulate, none)
+    if (w_si == 1) {
+        if (wide) CGTP_CONTRACT(true, 128);
+        else CGTP_CONTRACT(true, 64);
+    } else {
+        if (wide) CGTP_CONTRACT(false, 128);
+        else CGTP_CONTRACT(false, 64);
+    }
+#undef CGTP_CONTRACT
+    return hipGetLastError();
+}
+
+hipError_t launch_contract_gather(int64_t B, int Cout, int K, const float *W, int64_t w_sl,
+                                  int64_t w_si, int64_t w_so, const XGather &xg, int nsrc,
+                                  int64_t x_sb, float *Y, int64_t y_sb, int64_t y_so,
+                                  int64_t y_sk, hipStream_t s)
+{
+    if (B == 0 || Cout == 0 || K == 0 || nsrc == 0) return hipSuccess;
+    if (nsrc > kMaxGather || xg.rows <= 0 || xg.rows % kCs != 0) return hipErrorNotSupported;
+    const int Cin = nsrc * xg.rows;
+    if (x_sb < (int64_t)xg.rows * K) return hipErrorInvalidValue;
+    const int64_t groups = (B + kTile - 1) / kTile;
+    const bool wide = Cout >= 128;
+    const int otiles = (Cout + (wide ? 128 : kTile) - 1) / (wide ? 128 : kTile);
+    const int64_t blocks = groups * K * otiles;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+#define CGTP_CONTRACT(WTV, OTV)                                                                  \
+    hipLaunchKernelGGL((k_contract_mfma<WTV, OTV, true>), dim3((unsigned)blocks),                \
+                       dim3(kThreadsC), 0, s, B, Cin, Cout, K, K, otiles, W, w_sl, w_si, w_so,   \
+                       nullptr, x_sb, Y, y_sb, y_so, y_sk, nullptr, false, xg)
     if (w_si == 1) {
         if (wide) CGTP_CONTRACT(true, 128);
         else CGTP_CONTRACT(true, 64);

@@ -86,6 +86,20 @@ hipError_t launch_contract<double>(int64_t, int, int, int, bool, const double *,
                                    int64_t, const double *, int64_t, double *, int64_t, int64_t,
                                    int64_t, const double *, bool, hipStream_t);
 
+// fp32 contraction whose Cin = nsrc * xg.rows input rows come from nsrc sources: rows
+// [c rows, (c + 1) rows) of node b are xg.base[c] + b * x_sb + i * K (i < rows), otherwise as
+// launch_contract (never accumulating, no scale). rows must be a multiple of 32 and
+// nsrc <= kMaxGather; hipErrorNotSupported otherwise.
+constexpr int kMaxGather = 8;
+struct XGather {
+    const float *base[kMaxGather];
+    int rows;
+};
+hipError_t launch_contract_gather(int64_t B, int Cout, int K, const float *W, int64_t w_sl,
+                                  int64_t w_si, int64_t w_so, const XGather &xg, int nsrc,
+                                  int64_t x_sb, float *Y, int64_t y_sb, int64_t y_so,
+                                  int64_t y_sk, hipStream_t s);
+
 // Node-side synthesis of the three grid fields (A, dA/dx, dA/dphi) of H[b][r][K]:
 // SF[b][r][3][UVs] (Eqs. struct-F, struct-tildeA plus the derivative passes). Only the
 // fields whose bit is set in planes (1: A, 2: dA/dx, 4: dA/dphi) are written.

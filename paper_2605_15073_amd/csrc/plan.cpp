@@ -115,7 +115,9 @@ bool onsite_split_ok(const cgtp_plan_s *p)
 // Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],
 // and, for the MFMA receiver, the summed grid fields S [N][R][2][UVs]. With two node slots,
 // HI and SF hold the natural slot followed by the flipped one. With split factors (general
-// path), HI and Rt hold the Gaunt factors' contraction followed by the curl factors'.
+// path), HI and Rt hold the Gaunt factors' contraction followed by the curl factors'. Last,
+// room for one sector's output weights concatenated over the groups (the general path's
+// gathered projection).
 Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = false,
                  bool split = false)
 {
@@ -133,7 +135,8 @@ Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = f
     l.off[3] = l.off[2] + nrt * rt;
     l.off[4] = l.off[3] + h;
     l.off[5] = l.off[4] + h;
-    l.total = l.off[5] + sg;
+    l.wc = l.off[5] + sg;  // the output weights of a sector's groups, concatenated
+    l.total = l.wc + align256(es * (size_t)p->d.L * p->C * R);
     l.hf = h;
     l.sff = sf;
     l.rtf = rt;
@@ -538,23 +541,52 @@ Factors resolve_factors(const cgtp_plan_s *p, int in_blocks, const void *U1, con
     return f;
 }
 
+// Projection of each output sector (Eqs. cat-alpha-phi, cat-beta-phi): the sum over the
+// groups' products that feed one of its blocks, each with that block's weights. fp32 with
+// R a multiple of 32: one contraction per sector over all of its contributions, the rows
+// gathered from Ta / Tb and the weights concatenated along the rank into wcat [L][C][n R];
+// otherwise one accumulating contraction per contribution.
 template <typename T>
 int project_blocks(const cgtp_plan_s *p, const Groups &G, int64_t N, const Factors &f,
-                   const T *Ta, const T *Tb, void *oe, void *oo, hipStream_t s, StageRec &rec)
+                   const T *Ta, const T *Tb, void *oe, void *oo, T *wcat, hipStream_t s,
+                   StageRec &rec)
 {
-    const int64_t rs = (int64_t)G.n * p->R * p->d.K;  // row stride of Ta / Tb
+    const cgtp::Dims &d = p->d;
+    const int C = p->C, R = p->R;
+    const int64_t rs = (int64_t)G.n * R * d.K;  // row stride of Ta / Tb
+    const size_t es = sizeof(T);
     void *outs[2] = {oe, oo};
     for (int sec = 0; sec < 2; ++sec) {
-        bool first = true;
+        const T *src[2 * kMaxGroups];
+        int blk[2 * kMaxGroups], n = 0;
         for (int cat = 0; cat < 2 && outs[sec]; ++cat) {
             const int b = 2 * cat + sec;
             for (int gi = 0; gi < G.n; ++gi) {
                 if (!feeds(G.g[gi], b)) continue;
-                const T *src = (cat ? Tb : Ta) + (int64_t)gi * p->R * p->d.K;
-                hipError_t e = project<T>(N, p->C, p->R, p->d.K, f.out[b], src, rs, outs[sec],
-                                          !first, s);
-                if (e != hipSuccess) return hip_fail(e, sec ? "project odd" : "project even");
-                first = false;
+                src[n] = (cat ? Tb : Ta) + (int64_t)gi * R * d.K;
+                blk[n++] = b;
+            }
+        }
+        const char *what = sec ? "project odd" : "project even";
+        hipError_t e = hipSuccess;
+        if (sizeof(T) == 4 && n > 1 && n <= cgtp::kMaxGather && R % 32 == 0) {
+            cgtp::XGather xg{};
+            xg.rows = R;
+            for (int c = 0; c < n && e == hipSuccess; ++c) {
+                xg.base[c] = reinterpret_cast<const float *>(src[c]);
+                e = hipMemcpy2DAsync(wcat + (size_t)c * R, es * n * R, f.out[blk[c]], es * R,
+                                     es * R, (size_t)d.L * C, hipMemcpyDeviceToDevice, s);
+            }
+            if (e == hipSuccess)
+                e = cgtp::launch_contract_gather(N, C, d.K, reinterpret_cast<const float *>(wcat),
+                                                 (int64_t)C * n * R, 1, (int64_t)n * R, xg, n, rs,
+                                                 static_cast<float *>(outs[sec]),
+                                                 (int64_t)C * d.K, d.K, 1, s);
+            if (e != hipSuccess) return hip_fail(e, what);
+        } else {
+            for (int c = 0; c < n; ++c) {
+                e = project<T>(N, C, R, d.K, f.out[blk[c]], src[c], rs, outs[sec], c > 0, s);
+                if (e != hipSuccess) return hip_fail(e, what);
             }
         }
         rec.mark();
@@ -636,13 +668,13 @@ int run_onsite_groups(cgtp_plan_s *p, const Groups &G, int64_t N, const void *co
             e = cgtp::launch_onsite_folded(tb, N, Rg, HA, HB, Ta, Tb, s, HAc, HBc);
             if (e != hipSuccess) return hip_fail(e, "onsite grid (split)");
             rec.mark();
-            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
         }
     }
     e = cgtp::launch_onsite_grid<T>(tb, N, Rg, HA, HB, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "onsite grid");
     rec.mark();
-    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
 }
 
 template <typename T>
@@ -655,6 +687,7 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     const bool separated = (p->flags & CGTP_EDGE_SEPARATED) != 0;
     cgtp::Tabs<T> tb = cgtp::bind_tables<T>(d, p->tables);
     Layout lay = mp_layout(p, Rg, N, E, false, G.split);
+    T *wc = reinterpret_cast<T *>(ws + lay.wc);
     T *HI = reinterpret_cast<T *>(ws + lay.off[0]);
     T *SF = reinterpret_cast<T *>(ws + lay.off[1]);
     T *Rt = reinterpret_cast<T *>(ws + lay.off[2]);
@@ -712,14 +745,14 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
                                            SF, nullptr, sf_chunked(p, Rg), Sg, Ta, Tb, s);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
-            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
         }
     }
     e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, Rtc, SF,
                                  nullptr, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "receiver");
     rec.mark();
-    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
 }
 
 // Message passing with two parity-bearing fields (Eq. twoparity-phi): rank groups as for
@@ -769,7 +802,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
                                                   s);
             if (e != hipSuccess) return hip_fail(e, "receiver (edge field, mfma)");
             rec.mark();
-            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
         }
     }
     e = cgtp::launch_receiver_fields<T>(tb, N, Rg, row_ptr, col, HE, SF, Ta, Tb, s);
@@ -780,7 +813,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
                     p->d.UV);
     if (e != hipSuccess) return hip_fail(e, "receiver (edge field)");
     rec.mark();
-    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, s, rec);
+    return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
 }
 
 // nu-body on-site product: one channel contraction per distinct (operand, factor) pair,

@@ -58,6 +58,7 @@ def _ref(lmax, d, rec=None):
     (8, 8, True, True, 2, 2),
     (12, 8, False, False, 4, 2),
     (20, 4, True, True, 1, 1),
+    (3, 32, True, True, 4, 2),    # ranks a multiple of 32: gathered projection
 ])
 def test_fields_vs_oracle(cg, lmax, R, ef, nf, nin, nout):
     d = _d(lmax, 36, 4, R, 500 + lmax, ef, nf, nin, nout)

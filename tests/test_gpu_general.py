@@ -85,6 +85,7 @@ def _on_ref(lmax, d):
     (6, 12, 7, False, True, 4, 1),
     (8, 10, 16, True, True, 2, 1),
     (13, 6, 16, True, True, 4, 2),    # MFMA grid stage
+    (4, 12, 32, True, True, 4, 2),    # ranks a multiple of 32: one gathered projection per sector
     (14, 5, 8, False, True, 2, 2),
 ])
 def test_onsite_general_vs_oracle(cg, lmax, n, R, flip1, flip2, nin, nout):
@@ -204,6 +205,8 @@ def _mp_ref(lmax, d, receivers=None):
     (6, 9, True, 4, 2),
     (6, 8, True, 4, 2),     # split groups stacked to 16 ranks
     (7, 16, True, 4, 2),    # MFMA receiver at 4 x 16 ranks
+    (4, 32, True, 4, 2),    # gathered projection
+    (8, 32, False, 2, 2),   # gathered projection, one node slot
     (8, 16, False, 2, 2),
     (12, 16, True, 2, 1),
     (20, 16, True, 4, 2),
