@@ -382,6 +382,7 @@ __device__ __forceinline__ void load_unit(const T *unit, int64_t e, T &ux, T &uy
 // serves all RB ranks; the 3 RB sender values of a point are loaded before the
 // arithmetic so that their latency overlaps it.
 constexpr int kRecvMaxThreads = 1024;
+constexpr int kRecvEdgeChunk = 16;  // edges whose coefficients a receiver block stages at once
 
 // Raw buffer loads: one descriptor per edge over the sender's rank block; every
 // load of a grid point shares its VGPR byte offset and differs only in a scalar
@@ -464,84 +465,110 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
         jn = __builtin_amdgcn_readfirstlane(col[e0]);
         load_unit(unit, e0, uxn, uyn, uzn);
     }
-    for (int e = e0; e < e1; ++e) {
-        const int64_t j = jn;
-        const T ux = uxn, uy = uyn, uz = uzn;
-        if (e + 1 < e1) {
-            jn = __builtin_amdgcn_readfirstlane(col[e + 1]);
-            load_unit(unit, e + 1, uxn, uyn, uzn);
+    // SPLIT (two coefficient sets per edge): the block's edge coefficients are staged in LDS
+    // kRecvEdgeChunk edges at a time, as Rs[edge][set][l][q] (set 1: the curl's Rtg; ranks
+    // past nr zero), and read from there as broadcasts; one set is read from global memory
+    // as uniform (scalar) loads, which keep the single-set kernels at fewer registers
+    constexpr bool STAGE = SPLIT;
+    constexpr int NSET = SPLIT ? 2 : 1;
+    const int rstride = STAGE ? RB : R;  // between the degrees of one edge's coefficients
+    T *Rs = smem;
+    for (int ec = e0; ec < e1; ec += (STAGE ? kRecvEdgeChunk : e1 - e0)) {
+        const int ne = STAGE ? ((e1 - ec < kRecvEdgeChunk) ? (e1 - ec) : kRecvEdgeChunk)
+                             : e1 - e0;
+        if (STAGE) {
+            __syncthreads();  // the previous chunk is consumed
+            for (int k = threadIdx.x; k < ne * NSET * L * RB; k += blockDim.x) {
+                const int q = k % RB, rest = k / RB;
+                const int l = rest % L, es = rest / L;
+                const int set = es % NSET, ee = es / NSET;
+                const T *src = set ? Rtg : Rt;
+                Rs[k] = (FULL || q < nr) ? src[((int64_t)(ec + ee) * L + l) * R + r0 + q]
+                                         : (T)0;
+            }
+            __syncthreads();
         }
-        const T *rt = Rt + (int64_t)e * L * R + r0;   // Rt[e][l][r0 + q] = rt[l * R + q]
-        const T *rtg = SPLIT ? Rtg + (int64_t)e * L * R + r0 : rt;
-        const int UVs = d.UVs;
-        const __amdgpu_buffer_rsrc_t sfr =
-            make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs, (unsigned)(nr * 3 * UVs * sizeof(T)));
-        const __amdgpu_buffer_rsrc_t sff =
-            make_rsrc((TWO ? SFf : SF) + (j * R + r0) * 3 * (int64_t)UVs,
-                      (unsigned)(nr * 3 * UVs * sizeof(T)));
-        const unsigned fstride = (unsigned)(UVs * sizeof(T));
-#pragma unroll
-        for (int s = 0; s < NPT; ++s) {
-            const int uv = uvs[s];
-            if (uv >= UV) continue;
-            const unsigned voff = (unsigned)(uv * sizeof(T));
-            T fI[RB], fX[RB], fP[RB], gI[RB], gX[RB], gP[RB];
-#pragma unroll
-            for (int q = 0; q < RB; ++q) {
-                // ranks past nr fall outside the descriptor's range and read 0
-                fI[q] = buf_load<T>(sfr, voff, (3 * q) * fstride);
-                fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
-                fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
-                if (TWO) {
-                    gI[q] = buf_load<T>(sff, voff, (3 * q) * fstride);
-                    gX[q] = buf_load<T>(sff, voff, (3 * q + 1) * fstride);
-                    gP[q] = buf_load<T>(sff, voff, (3 * q + 2) * fstride);
-                }
+        for (int e = ec; e < ec + ne; ++e) {
+            const int64_t j = jn;
+            const T ux = uxn, uy = uyn, uz = uzn;
+            if (e + 1 < e1) {
+                jn = __builtin_amdgcn_readfirstlane(col[e + 1]);
+                load_unit(unit, e + 1, uxn, uyn, uzn);
             }
-    const T h = ux * pcp[s] + uy * psp[s];
-            const T t = uz * px[s] + psx[s] * h;
-            T a[RB], g[RB];
+            // rt[l * rstride + q] = Rt[e][l][r0 + q], rtg the same of Rtg
+            const T *rt = STAGE ? Rs + (e - ec) * NSET * L * RB : Rt + (int64_t)e * L * R + r0;
+            const T *rtg = SPLIT ? rt + L * RB : rt;
+            const int UVs = d.UVs;
+            const __amdgpu_buffer_rsrc_t sfr = make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs,
+                                                         (unsigned)(nr * 3 * UVs * sizeof(T)));
+            const __amdgpu_buffer_rsrc_t sff =
+                make_rsrc((TWO ? SFf : SF) + (j * R + r0) * 3 * (int64_t)UVs,
+                          (unsigned)(nr * 3 * UVs * sizeof(T)));
+            const unsigned fstride = (unsigned)(UVs * sizeof(T));
 #pragma unroll
-            for (int q = 0; q < RB; ++q) {
-                a[q] = (FULL || q < nr) ? rt[q] : (T)0;
-                g[q] = 0;
-            }
-            if (lmax >= 1) {
+            for (int s = 0; s < NPT; ++s) {
+                const int uv = uvs[s];
+                if (uv >= UV) continue;
+                const unsigned voff = (unsigned)(uv * sizeof(T));
+                T fI[RB], fX[RB], fP[RB], gI[RB], gX[RB], gP[RB];
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
-                    T c = (FULL || q < nr) ? rt[R + q] : (T)0;
-                    a[q] += c * t;
-                    g[q] = SPLIT ? ((FULL || q < nr) ? rtg[R + q] : (T)0) : c;
+                    // ranks past nr fall outside the descriptor's range and read 0
+                    fI[q] = buf_load<T>(sfr, voff, (3 * q) * fstride);
+                    fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
+                    fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
+                    if (TWO) {
+                        gI[q] = buf_load<T>(sff, voff, (3 * q) * fstride);
+                        gX[q] = buf_load<T>(sff, voff, (3 * q + 1) * fstride);
+                        gP[q] = buf_load<T>(sff, voff, (3 * q + 2) * fstride);
+                    }
                 }
-            }
-            T p0 = 1, p1 = t, d1 = 1;
-            for (int l = 2; l <= lmax; ++l) {
-                const T p2 = tb.rc1[l] * t * p1 - tb.rc2[l] * p0;
-                const T d2 = (T)l * p1 + t * d1;
+        const T h = ux * pcp[s] + uy * psp[s];
+                const T t = uz * px[s] + psx[s] * h;
+                T a[RB], g[RB];
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
-                    T c = (FULL || q < nr) ? rt[l * R + q] : (T)0;
-                    T cg = SPLIT ? ((FULL || q < nr) ? rtg[l * R + q] : (T)0) : c;
-                    a[q] += c * p2;
-                    g[q] += cg * d2;
+                    a[q] = (FULL || q < nr) ? rt[q] : (T)0;
+                    g[q] = 0;
                 }
-                p0 = p1;
-                p1 = p2;
-                d1 = d2;
-            }
-            const T dxt = uz - pxsx[s] * h;
-            const T dpt = psx[s] * (uy * pcp[s] - ux * psp[s]);
+                if (lmax >= 1) {
 #pragma unroll
-            for (int q = 0; q < RB; ++q) {
-                sa[s][q] += a[q] * fI[q];
-                sb[s][q] += g[q] * (dpt * fX[q] - dxt * fP[q]);
-                if (TWO) {
-                    sa[s][q] += g[q] * (dpt * gX[q] - dxt * gP[q]);
-                    sb[s][q] += a[q] * gI[q];
+                    for (int q = 0; q < RB; ++q) {
+                        T c = (FULL || q < nr) ? rt[rstride + q] : (T)0;
+                        a[q] += c * t;
+                        g[q] = SPLIT ? ((FULL || q < nr) ? rtg[rstride + q] : (T)0) : c;
+                    }
+                }
+                T p0 = 1, p1 = t, d1 = 1;
+                for (int l = 2; l <= lmax; ++l) {
+                    const T p2 = tb.rc1[l] * t * p1 - tb.rc2[l] * p0;
+                    const T d2 = (T)l * p1 + t * d1;
+#pragma unroll
+                    for (int q = 0; q < RB; ++q) {
+                        T c = (FULL || q < nr) ? rt[l * rstride + q] : (T)0;
+                        T cg = SPLIT ? ((FULL || q < nr) ? rtg[l * rstride + q] : (T)0) : c;
+                        a[q] += c * p2;
+                        g[q] += cg * d2;
+                    }
+                    p0 = p1;
+                    p1 = p2;
+                    d1 = d2;
+                }
+                const T dxt = uz - pxsx[s] * h;
+                const T dpt = psx[s] * (uy * pcp[s] - ux * psp[s]);
+#pragma unroll
+                for (int q = 0; q < RB; ++q) {
+                    sa[s][q] += a[q] * fI[q];
+                    sb[s][q] += g[q] * (dpt * fX[q] - dxt * fP[q]);
+                    if (TWO) {
+                        sa[s][q] += g[q] * (dpt * gX[q] - dxt * gP[q]);
+                        sb[s][q] += a[q] * gI[q];
+                    }
                 }
             }
         }
     }
+    if (STAGE) __syncthreads();  // the staged coefficients are consumed before the analysis
     // inverse transforms, one rank at a time through LDS
     T *qs = smem;
     T *Sa = qs + d.V * d.M;
@@ -899,16 +926,19 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + 2 * d.M * d.U);
     const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
     const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
+    // LDS: the analysis buffers, or (split) one chunk of staged edge coefficients if larger
 #define CGTP_RECV_TW(RBV, NP, TW, SP)                                                          \
     do {                                                                                       \
         int64_t nb = N * ((R + RBV - 1) / RBV);                                                \
+        const size_t chunk = SP ? sizeof(T) * kRecvEdgeChunk * 2 * d.L * RBV : 0;              \
+        const size_t shc = chunk > sh ? chunk : sh;                                            \
         if (R % RBV == 0)                                                                      \
             hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true, TW, SP>),                   \
-                               dim3((unsigned)nb), dim3(threads), sh, s, tb, R, row_ptr, col,  \
+                               dim3((unsigned)nb), dim3(threads), shc, s, tb, R, row_ptr, col, \
                                unit, Rt, Rtg, SF, SFf, Ta, Tb);                                \
         else                                                                                   \
             hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false, TW, SP>),                  \
-                               dim3((unsigned)nb), dim3(threads), sh, s, tb, R, row_ptr, col,  \
+                               dim3((unsigned)nb), dim3(threads), shc, s, tb, R, row_ptr, col, \
                                unit, Rt, Rtg, SF, SFf, Ta, Tb);                                \
     } while (0)
 #define CGTP_RECV(RBV, NP)                              \
