@@ -116,7 +116,9 @@ int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan);
 int cgtp_plan_grid(cgtp_plan plan, int *n_theta, int *n_phi);
 
 /* Bytes of device workspace an operation needs for n_nodes nodes and n_edges
- * edges (n_edges ignored for CGTP_OP_ONSITE). */
+ * edges (n_edges ignored for CGTP_OP_ONSITE). A caller workspace must start on a
+ * 256-byte boundary (kernels store 16-byte vectors into it); a misaligned one is
+ * rejected with CGTP_ERR_ARG. */
 int cgtp_workspace_bytes(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edges,
                          size_t *bytes);
 

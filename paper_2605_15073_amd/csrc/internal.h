@@ -55,9 +55,17 @@ struct Tabs {
     const T *wpt;   // [P][Ut] wq[u] * p transposed (Gauss-Legendre analysis weights)
     const T *yc;    // [P] sqrt((2l+1)(l^2-m^2)/(2l-1)): (1-x^2) dPt_l^m/dx
                     //     = yc Pt_{l-1}^m - l x Pt_l^m
+    const T *ysyn;  // [KP][3 UVs] for lmax <= kDenseSynthMaxL (else empty): row k = (l, m),
+                    // KP = K rounded up to 4 (rows past K zero); column f UVs + u V + v holds
+                    // Y_k (f = 0), dY_k/dx (f = 1) and dY_k/dphi (f = 2) at grid point (u, v),
+                    // with zeros past UV in each block
 
     Dims d;
 };
+
+// Degrees up to which the plan builds the dense synthesis table ysyn (the sender fields of
+// a row are then one product of its coefficients with that table).
+constexpr int kDenseSynthMaxL = 6;
 
 // Number of T elements of each table region, in the order of Tabs.
 size_t table_elems(const Dims &d);

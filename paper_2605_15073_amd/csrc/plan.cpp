@@ -215,6 +215,8 @@ int check_device(const cgtp_plan_s *p)
 int get_workspace(cgtp_plan_s *p, size_t need, void *ws, size_t ws_bytes, void **out)
 {
     if (ws) {
+        if (reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+            return fail(CGTP_ERR_ARG, "workspace %p is not 256-byte aligned", ws);
         if (ws_bytes < need)
             return fail(CGTP_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
         *out = ws;

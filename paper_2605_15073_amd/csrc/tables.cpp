@@ -165,9 +165,10 @@ static void region_sizes(const Dims &d, size_t *n)
     n[16] = (size_t)d.P * ut;   // dpt
     n[17] = (size_t)d.P * ut;   // wpt
     n[18] = d.P;                // yc
+    n[19] = d.lmax <= kDenseSynthMaxL ? (size_t)(d.K + 3) / 4 * 4 * 3 * d.UVs : 0;  // ysyn
 }
 
-static const int kRegions = 19;
+static const int kRegions = 20;
 
 static size_t round_up(size_t n) { return (n + 63) & ~(size_t)63; }  // 512 B for fp64
 
@@ -233,6 +234,29 @@ void fill_tables(const Dims &d, double *h)
                 h[off[13] + idx] = 0.0;
             }
         }
+    // Dense synthesis table: with k = l^2 + l + m and the real basis Y_k = Pt_l^|m|(x) q_m(phi),
+    // d/dphi maps q_m to -m q_{-m} (cos(m phi) -> -m sin(m phi), sin(|m| phi) -> |m| cos(|m| phi)).
+    if (n[19]) {
+        const size_t ld = 3 * (size_t)d.UVs;
+        for (int l = 0; l <= d.lmax; ++l)
+            for (int m = -l; m <= l; ++m) {
+                const int k = l * l + l + m, am = m < 0 ? -m : m;
+                const int pi = l * (l + 1) / 2 + am;
+                double *row = h + off[19] + (size_t)k * ld;
+                for (int u = 0; u < d.U; ++u) {
+                    const double pv = h[off[4] + (size_t)u * d.P + pi];
+                    const double dv = h[off[5] + (size_t)u * d.P + pi];
+                    for (int v = 0; v < d.V; ++v) {
+                        const double qm = h[off[6] + (size_t)v * d.M + m + d.lmax];
+                        const double qn = h[off[6] + (size_t)v * d.M - m + d.lmax];
+                        const size_t pnt = (size_t)u * d.V + v;
+                        row[pnt] = pv * qm;
+                        row[d.UVs + pnt] = dv * qm;
+                        row[2 * (size_t)d.UVs + pnt] = -m * pv * qn;
+                    }
+                }
+            }
+    }
 }
 
 template <typename T>
@@ -267,6 +291,7 @@ Tabs<T> bind_tables(const Dims &d, const void *dev)
     tb.dpt = ptr[16];
     tb.wpt = ptr[17];
     tb.yc = ptr[18];
+    tb.ysyn = ptr[19];
     tb.d = d;
     return tb;
 }

@@ -167,6 +167,11 @@ def test_onsite_caller_workspace_and_errors(cg):
     with pytest.raises(cg.CgtpError) as ei:
         run_onsite(cg, plan, t, workspace=small)
     assert ei.value.status == cg.CGTP_ERR_WORKSPACE
+    # a workspace off a 256-byte boundary is refused before anything is enqueued
+    big = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(cg.CgtpError) as ei:
+        run_onsite(cg, plan, t, workspace=big[4:])
+    assert ei.value.status == cg.CGTP_ERR_ARG
     empty = {k: (v[:0] if k in ("A", "B") else v) for k, v in t.items()}
     oe, oo = run_onsite(cg, plan, empty)
     assert oe.shape[0] == 0 and oo.shape[0] == 0
