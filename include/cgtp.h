@@ -291,13 +291,14 @@ int cgtp_onsite_nbody(cgtp_plan plan, int64_t n_nodes, int nu, const void *const
  * per-step breakdown (App. D, Table 4). Waits for the recorded events, writes the
  * summed milliseconds of each stage of `op` to ms[0 .. *n_stages) (at most cap
  * entries) and the number of calls to *n_calls, then resets the accumulation.
- * Stages of CGTP_OP_ONSITE: 0 contract A, 1 contract B, 2 grid product+curl and
- * analysis, 3 project even, 4 project odd. Stages of CGTP_OP_MESSAGE_PASS:
+ * Stages of CGTP_OP_ONSITE: 0 contract both operands, 1 grid product+curl and
+ * analysis, 2 project both output slots. Stages of CGTP_OP_MESSAGE_PASS:
  * 0 contract node features, 1 sender grid fields, 2 contract edge radial,
  * 3 receiver pass (edge synthesis, products, neighbour sum, analysis),
  * 4 project even, 5 project odd. CGTP_OP_MESSAGE_PASS_TWO_SLOT has the same six
- * stages, each covering both node slots; CGTP_OP_ONSITE_GENERAL and
- * CGTP_OP_MESSAGE_PASS_GENERAL those of CGTP_OP_ONSITE / CGTP_OP_MESSAGE_PASS, covering
+ * stages, each covering both node slots; CGTP_OP_ONSITE_GENERAL: 0 contract first
+ * operand, 1 contract second operand, 2 grid product+curl and analysis, 3 project even,
+ * 4 project odd; CGTP_OP_MESSAGE_PASS_GENERAL those of CGTP_OP_MESSAGE_PASS; both cover
  * every rank group; CGTP_OP_MESSAGE_PASS_FIELDS: 0 contract node features, 1 sender grid
  * fields, 2 contract edge field, 3 receiver pass, 4 project even, 5 project odd. A
  * skipped stage counts as 0.

@@ -40,8 +40,9 @@ EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_
             "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_message_pass_fields",
             "cgtp_workspace_bytes_nbody", "cgtp_onsite_nbody", "cgtp_stage_times",
             "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables")
-ONSITE_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis", "project_even",
-                 "project_odd")
+ONSITE_STAGES = ("contract_operands", "grid_product_curl_analysis", "project")
+ONSITE_GENERAL_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis",
+                         "project_even", "project_odd")
 MP_STAGES = ("contract_node", "sender_fields", "contract_edge_radial", "receiver",
              "project_even", "project_odd")
 NBODY_STAGES = ("contract_operands", "grid_product_analysis", "project")
@@ -162,7 +163,8 @@ def stage_times(plan: Plan, op: int):
     _check(load_library().cgtp_stage_times(plan.handle, op, ms, 8, ctypes.byref(ns),
                                            ctypes.byref(nc)), "cgtp_stage_times")
     names = (NBODY_STAGES if op == CGTP_OP_ONSITE_NBODY else
-             ONSITE_STAGES if op in (CGTP_OP_ONSITE, CGTP_OP_ONSITE_GENERAL) else MP_STAGES)
+             ONSITE_STAGES if op == CGTP_OP_ONSITE else
+             ONSITE_GENERAL_STAGES if op == CGTP_OP_ONSITE_GENERAL else MP_STAGES)
     return {names[i]: ms[i] for i in range(ns.value)}, nc.value
 
 

@@ -68,7 +68,7 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     int64_t B, int Cin, int Cout, int K, int tiles_per_group, int otiles,
     const float *__restrict__ W, int64_t w_sl, int64_t w_si, int64_t w_so,
     const float *__restrict__ X, int64_t x_sb, float *__restrict__ Y, int64_t y_sb, int64_t y_so,
-    int64_t y_sk, const float *__restrict__ scale, bool accumulate, XGather xg)
+    int64_t y_sk, const float *__restrict__ scale, bool accumulate, XGather xg, Pair2 second)
 {
     constexpr int SWo = OT + 16;                 // LDS row stride of Ws[i][o]: 16 mod 32
     constexpr int NW = OT * kCs / kThreadsC;     // staged W elements per thread
@@ -82,7 +82,14 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
     const int64_t nblk = gridDim.x;
     const int64_t per = nblk / 8, rem = nblk % 8;
     const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
-    const int64_t bid = (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+    int64_t bid = (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+    // a paired launch runs the second problem (same sizes and strides) on blocks past nper
+    if (second.nper > 0 && bid >= second.nper) {
+        bid -= second.nper;
+        W = second.W;
+        X = second.X;
+        Y = second.Y;
+    }
     const int ot = (int)(bid % otiles);
     const int64_t rest = bid / otiles;
     const int t = (int)(rest % tiles_per_group);
@@ -399,7 +406,7 @@ hipError_t launch_contract<float>(int64_t B, int Cin, int Cout, int K, bool kdeg
 #define CGTP_CONTRACT(WTV, OTV)                                                                  \
     hipLaunchKernelGGL((k_contract_mfma<WTV, OTV, false>), dim3((unsigned)blocks),               \
                        dim3(kThreadsC), 0, s, B, Cin, Cout, K, tiles_per_group, otiles, W, w_sl, \
-                       w_si, w_so, X, x_sb, Y, y_sb, y_so, y_sk, scale, accumulate, none)
+                       w_si, w_so, X, x_sb, Y, y_sb, y_so, y_sk, scale, accumulate, none, Pair2{})
     if (w_si == 1) {
         if (wide) CGTP_CONTRACT(true, 128);
         else CGTP_CONTRACT(true, 64);
@@ -428,7 +435,36 @@ hipError_t launch_contract_gather(int64_t B, int Cout, int K, const float *W, in
 #define CGTP_CONTRACT(WTV, OTV)                                                                  \
     hipLaunchKernelGGL((k_contract_mfma<WTV, OTV, true>), dim3((unsigned)blocks),                \
                        dim3(kThreadsC), 0, s, B, Cin, Cout, K, K, otiles, W, w_sl, w_si, w_so,   \
-                       nullptr, x_sb, Y, y_sb, y_so, y_sk, nullptr, false, xg)
+                       nullptr, x_sb, Y, y_sb, y_so, y_sk, nullptr, false, xg, Pair2{})
+    if (w_si == 1) {
+        if (wide) CGTP_CONTRACT(true, 128);
+        else CGTP_CONTRACT(true, 64);
+    } else {
+        if (wide) CGTP_CONTRACT(false, 128);
+        else CGTP_CONTRACT(false, 64);
+    }
+#undef CGTP_CONTRACT
+    return hipGetLastError();
+}
+
+hipError_t launch_contract_pair(int64_t B, int Cin, int Cout, int K, const float *W0,
+                                const float *W1, int64_t w_sl, int64_t w_si, int64_t w_so,
+                                const float *X0, const float *X1, int64_t x_sb, float *Y0,
+                                float *Y1, int64_t y_sb, int64_t y_so, int64_t y_sk, hipStream_t s)
+{
+    if (B == 0 || Cout == 0 || K == 0) return hipSuccess;
+    if (x_sb < (int64_t)Cin * K) return hipErrorInvalidValue;
+    const int64_t groups = (B + kTile - 1) / kTile;
+    const bool wide = Cout >= 128;
+    const int otiles = (Cout + (wide ? 128 : kTile) - 1) / (wide ? 128 : kTile);
+    const int64_t per = groups * K * otiles;  // blocks of one problem
+    if (2 * per > 0x7fffffffLL) return hipErrorInvalidValue;
+    const XGather none{};
+    const Pair2 second{W1, X1, Y1, per};
+#define CGTP_CONTRACT(WTV, OTV)                                                                  \
+    hipLaunchKernelGGL((k_contract_mfma<WTV, OTV, false>), dim3((unsigned)(2 * per)),            \
+                       dim3(kThreadsC), 0, s, B, Cin, Cout, K, K, otiles, W0, w_sl, w_si, w_so,  \
+                       X0, x_sb, Y0, y_sb, y_so, y_sk, nullptr, false, none, second)
     if (w_si == 1) {
         if (wide) CGTP_CONTRACT(true, 128);
         else CGTP_CONTRACT(true, 64);

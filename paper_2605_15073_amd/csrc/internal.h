@@ -108,6 +108,21 @@ hipError_t launch_contract_gather(int64_t B, int Cout, int K, const float *W, in
                                   int64_t x_sb, float *Y, int64_t y_sb, int64_t y_so,
                                   int64_t y_sk, hipStream_t s);
 
+// Two fp32 contractions of the same sizes and strides (never accumulating, no scale) in one
+// launch: Y0 from (W0, X0) and Y1 from (W1, X1), each as launch_contract with kdeg false.
+// Small problems are bound by the latency of their few workgroups; one launch overlaps both.
+struct Pair2 {
+    const float *W;
+    const float *X;
+    float *Y;
+    int64_t nper;  // blocks of the first problem; 0: a single problem
+};
+hipError_t launch_contract_pair(int64_t B, int Cin, int Cout, int K, const float *W0,
+                                const float *W1, int64_t w_sl, int64_t w_si, int64_t w_so,
+                                const float *X0, const float *X1, int64_t x_sb, float *Y0,
+                                float *Y1, int64_t y_sb, int64_t y_so, int64_t y_sk,
+                                hipStream_t s);
+
 // Node-side synthesis of the three grid fields (A, dA/dx, dA/dphi) of H[b][r][K]:
 // SF[b][r][3][UVs] (Eqs. struct-F, struct-tildeA plus the derivative passes). Only the
 // fields whose bit is set in planes (1: A, 2: dA/dx, 4: dA/dphi) are written.

@@ -345,32 +345,37 @@ int run_onsite(cgtp_plan_s *p, int op, int64_t N, const void *A, const void *B, 
     T *Tb = reinterpret_cast<T *>(ws + lay.off[3]);
     const int64_t hs = (int64_t)R * d.K;
     StageRec rec;
-    int st = rec.begin(p, op, 5, s);
+    int st = rec.begin(p, op, 3, s);
     if (st) return st;
     hipError_t e;
-    // Eq. struct-H for both operands (shared when the operands coincide)
-    e = contract_in<T>(N, C, R, d.K, UA, A, HA, hs, s);
-    if (e != hipSuccess) return hip_fail(e, "contract A");
-    rec.mark();
-    const T *HBp = HA;
-    if (!(A == B && UA == UB)) {
-        e = contract_in<T>(N, C, R, d.K, UB, B, HB, hs, s);
-        if (e != hipSuccess) return hip_fail(e, "contract B");
-        HBp = HB;
+    // Eq. struct-H for both operands (shared when the operands coincide); in fp32 the two
+    // contractions run as one launch
+    const bool shared = A == B && UA == UB;
+    const T *HBp = shared ? HA : HB;
+    if (sizeof(T) == 4 && !shared) {
+        e = cgtp::launch_contract_pair(N, C, R, d.K, (const float *)UA, (const float *)UB,
+                                       (int64_t)C * R, R, 1, (const float *)A, (const float *)B,
+                                       (int64_t)C * d.K, (float *)HA, (float *)HB, hs, d.K, 1, s);
+    } else {
+        e = contract_in<T>(N, C, R, d.K, UA, A, HA, hs, s);
+        if (e == hipSuccess && !shared) e = contract_in<T>(N, C, R, d.K, UB, B, HB, hs, s);
     }
+    if (e != hipSuccess) return hip_fail(e, "contract operands");
     rec.mark();
     e = cgtp::launch_onsite_grid<T>(tb, N, R, HA, HBp, Ta, Tb, s);
     if (e != hipSuccess) return hip_fail(e, "onsite grid");
     rec.mark();
-    if (oe) {
-        e = project<T>(N, C, R, d.K, Uoe, Ta, hs, oe, false, s);
-        if (e != hipSuccess) return hip_fail(e, "project even");
+    // Eqs. struct-phi / cat-beta-phi for the slots asked for (both in one fp32 launch)
+    if (sizeof(T) == 4 && oe && oo) {
+        e = cgtp::launch_contract_pair(N, R, C, d.K, (const float *)Uoe, (const float *)Uoo,
+                                       (int64_t)C * R, 1, R, (const float *)Ta, (const float *)Tb,
+                                       hs, (float *)oe, (float *)oo, (int64_t)C * d.K, d.K, 1, s);
+    } else {
+        e = hipSuccess;
+        if (oe) e = project<T>(N, C, R, d.K, Uoe, Ta, hs, oe, false, s);
+        if (e == hipSuccess && oo) e = project<T>(N, C, R, d.K, Uoo, Tb, hs, oo, false, s);
     }
-    rec.mark();
-    if (oo) {
-        e = project<T>(N, C, R, d.K, Uoo, Tb, hs, oo, false, s);
-        if (e != hipSuccess) return hip_fail(e, "project odd");
-    }
+    if (e != hipSuccess) return hip_fail(e, "project");
     rec.mark();
     return CGTP_OK;
 }
@@ -1348,8 +1353,8 @@ int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages,
     if (!(plan->flags & CGTP_TIME_STAGES))
         return fail(CGTP_ERR_ARG, "plan was created without CGTP_TIME_STAGES");
     int ns;
-    if (op == CGTP_OP_ONSITE_NBODY) ns = 3;
-    else if (op == CGTP_OP_ONSITE || op == CGTP_OP_ONSITE_GENERAL) ns = 5;
+    if (op == CGTP_OP_ONSITE_NBODY || op == CGTP_OP_ONSITE) ns = 3;
+    else if (op == CGTP_OP_ONSITE_GENERAL) ns = 5;
     else if (op == CGTP_OP_MESSAGE_PASS || op == CGTP_OP_MESSAGE_PASS_TWO_SLOT ||
              op == CGTP_OP_MESSAGE_PASS_GENERAL || op == CGTP_OP_MESSAGE_PASS_FIELDS)
         ns = 6;

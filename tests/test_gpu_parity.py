@@ -151,6 +151,27 @@ def test_onsite_skip_slots_and_grid_override(cg):
     _check_pair(run_onsite(cg, mn, t3), r3, TOL_F32)
 
 
+def test_onsite_paired_launches_match_single_and_stage_times(cg):
+    """The fp32 call contracts both operands in one launch and projects both output slots in
+    one launch; a call that asks for one slot (or shares the operands) takes the single
+    launches. The paired blocks run the same arithmetic, so the results agree bit for bit."""
+    import torch
+
+    lmax = 5
+    d = inputs.onsite_inputs(70, lmax, 12, 20, seed=14, distinct_out=True)
+    ref = _oracle_onsite(lmax, d)
+    t = to_dev(d, ONSITE_KEYS)
+    plan = cg.plan_create(lmax, 12, 20, flags=cg.CGTP_TIME_STAGES)
+    both = run_onsite(cg, plan, t)
+    _check_pair(both, ref, TOL_F32)
+    even, _ = run_onsite(cg, plan, t, out_odd=False)
+    _, odd = run_onsite(cg, plan, t, out_even=False)
+    assert torch.equal(both[0], even) and torch.equal(both[1], odd)
+    stages, calls = cg.stage_times(plan, cg.CGTP_OP_ONSITE)
+    assert calls == 3 and tuple(stages) == cg.ONSITE_STAGES
+    assert all(v > 0 for v in stages.values())
+
+
 def test_onsite_caller_workspace_and_errors(cg):
     import torch
 
