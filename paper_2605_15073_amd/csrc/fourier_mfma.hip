@@ -64,7 +64,7 @@ struct Grid {
 };
 
 constexpr size_t kLdsTarget = 40 * 1024;  // keeps several workgroups resident per CU
-constexpr int64_t kDenseSynthBlocks = 512;  // persistent dense-synthesis workgroups: two per CU
+constexpr int64_t kDenseSynthBlocks = 512;  // dense-synthesis workgroups if occupancy is unknown
 
 // Largest rank block (<= 16) within the LDS target, else the largest within 64 KiB.
 int pick_rb(int R, size_t fixed, size_t per_rank)
@@ -298,47 +298,42 @@ __global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int 
 //   SF[(b,r)][f UVs + p] = sum_k H[(b,r)][k] ysyn[k][f UVs + p].
 // At these degrees this costs K x 3 UV matrix-core products per row and no Legendre pass
 // on the vector ALUs, which outweighs the separated form's smaller count. The 16-row tiles
-// of rows (b, r) are dealt to persistent workgroups of six waves; wave w owns the column
-// tiles [w CTW, (w + 1) CTW) (half of one field) and holds their B operands (the table)
-// in registers for the whole launch. A row tile (16 K contiguous floats) is loaded once
+// of rows (b, r) are dealt to persistent workgroups of NW waves (12 when the column tiles
+// split evenly that way, so that every SIMD carries three waves between the per-tile
+// barriers; else 6); wave w owns the column tiles [w CTW, (w + 1) CTW) and holds their
+// table operands in registers for the whole launch. A row tile (16 K contiguous floats) is loaded once
 // per workgroup with coalesced loads into a double-buffered LDS tile while the previous
-// one is multiplied; each wave's 16 x 16 CTW result block goes through wave-private LDS
-// and leaves as 16-byte stores of whole row segments.
+// one is multiplied. The product is formed transposed, D[column][row] = table^T H^T, so a
+// lane holds four consecutive columns of one row and stores them as one 16-byte vector.
 template <int LM>
 struct DenseSyn {
     using G = Grid<LM>;
     static constexpr int KP = (G::K + 3) / 4 * 4, KS = KP / 4;  // reduction steps of 4
     static constexpr int NCOL = 3 * G::UVs, CT = NCOL / 16;     // 16-column tiles
-    // six waves per workgroup: UVs is a multiple of 32, so CT = 6 UVs / 32 splits evenly
-    static constexpr int NW = 6, NT = 64 * NW, CTW = CT / NW, WC = 16 * CTW;
+    // UVs is a multiple of 32, so CT = 6 UVs / 32 always splits evenly over six waves
+    static constexpr int NW = CT % 12 == 0 ? 12 : 6, NT = 64 * NW, CTW = CT / NW, WC = 16 * CTW;
     static_assert(CT % NW == 0, "column tiles split evenly over the waves");
     // LDS row stride of a staged A row: KA / 4 odd puts the 16 rows x 4 lane groups of an
     // operand read on distinct banks
     static constexpr int KA = (KP / 4) % 2 ? KP : KP + 4;
     static constexpr int NLA = (16 * G::K + NT - 1) / NT;  // tile loads per thread
-    static constexpr int OS = WC + 4;                      // result rows: 16-byte aligned,
-                                                           // lane groups 16 banks apart
-    static constexpr int NST = 16 * WC / 4 / 64;           // 16-byte stores per lane
-    static_assert((16 * WC / 4) % 64 == 0, "result block is whole 16-byte stores");
 };
 
 template <int LM>
-__global__ __launch_bounds__(384) __attribute__((amdgpu_waves_per_eu(3))) void k_sender_dense(
+__global__ __launch_bounds__(64 * DenseSyn<LM>::NW) __attribute__((amdgpu_waves_per_eu(3))) void k_sender_dense(
     const float *__restrict__ Ys, int64_t rows, const float *__restrict__ H,
     float *__restrict__ SF, int planes)
 {
     using G = Grid<LM>;
     using D = DenseSyn<LM>;
-    __shared__ __align__(16) float as[2][16 * D::KA];       // staged A rows (columns past K stay 0)
-    __shared__ __align__(16) float osh[D::NW][16 * D::OS];  // per-wave result blocks (16-byte reads)
+    __shared__ float as[2][16 * D::KA];  // staged rows of H (columns past K stay 0)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g4 = lane >> 4, n = lane & 15;
-    float *os = osh[wave];
     for (int i = tid; i < 2 * 16 * D::KA; i += D::NT) (&as[0][0])[i] = 0.f;
     const int t0 = wave * D::CTW;
-    const int f = (t0 * 16) / G::UVs;   // the field of this wave's columns
+    const int f = (t0 * 16) / G::UVs;   // the field of this wave's columns (CTW tiles lie in one)
     const bool store = (planes >> f) & 1;
-    // B operand of tile t at reduction step kk: ysyn[4 kk + g][16 (t0 + t) + n]
+    // A operand of column tile t at reduction step kk: ysyn[4 kk + g][16 (t0 + t) + n]
     float bq[D::CTW][D::KS];
 #pragma unroll
     for (int t = 0; t < D::CTW; ++t)
@@ -346,7 +341,8 @@ __global__ __launch_bounds__(384) __attribute__((amdgpu_waves_per_eu(3))) void k
         for (int kk = 0; kk < D::KS; ++kk)
             bq[t][kk] = Ys[(4 * kk + g4) * D::NCOL + (t0 + t) * 16 + n];
     const int64_t ntiles = (rows + 15) / 16, nel = rows * G::K;
-    // row tile rt is H[16 K rt, 16 K (rt + 1)); this thread's elements e = tid + NT s
+    // row tile rt is H[16 K rt, 16 K (rt + 1)); this thread's elements e = tid + NT s, staged
+    // as the B operand H[16 rt + n][4 kk + g]
     float xr[D::NLA];
     auto load = [&](int64_t rt) {
 #pragma unroll
@@ -366,7 +362,6 @@ __global__ __launch_bounds__(384) __attribute__((amdgpu_waves_per_eu(3))) void k
             }
         }
     };
-    __syncthreads();  // the zero fill lands before the first tile
     load(blockIdx.x);
     stage(as[0]);
     __syncthreads();
@@ -383,22 +378,13 @@ __global__ __launch_bounds__(384) __attribute__((amdgpu_waves_per_eu(3))) void k
         for (int kk = 0; kk < D::KS; ++kk)
 #pragma unroll
             for (int t = 0; t < D::CTW; ++t)
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[kk], bq[t][kk], acc[t], 0, 0, 0);
-        // D[row 4 g + j][column 16 t + n] -> os, then whole 16-byte row segments out
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(bq[t][kk], a[kk], acc[t], 0, 0, 0);
+        // D[column 16 t + 4 g + j][row n]: columns 4 g .. 4 g + 3 of row 16 rt + n
+        const int64_t row = rt * 16 + n;
+        if (store && row < rows) {
+            float *dst = SF + row * D::NCOL + t0 * 16 + 4 * g4;
 #pragma unroll
-        for (int t = 0; t < D::CTW; ++t)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) os[(4 * g4 + j) * D::OS + 16 * t + n] = acc[t][j];
-        if (store) {
-#pragma unroll
-            for (int s2 = 0; s2 < D::NST; ++s2) {
-                const int i = lane + 64 * s2;
-                const int rr = i / (D::WC / 4), c4 = i - rr * (D::WC / 4);
-                const int64_t row = rt * 16 + rr;
-                const float4_t v = *reinterpret_cast<const float4_t *>(os + rr * D::OS + 4 * c4);
-                if (row < rows)
-                    *reinterpret_cast<float4_t *>(SF + row * D::NCOL + t0 * 16 + 4 * c4) = v;
-            }
+            for (int t = 0; t < D::CTW; ++t) *reinterpret_cast<float4_t *>(dst + 16 * t) = acc[t];
         }
         // the other buffer was last read before the previous barrier
         stage(as[buf ^ 1]);
@@ -859,7 +845,20 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
     if constexpr (LM >= 1 && LM <= kDenseSynthMaxL) {
         if (!chunked) {
             const int64_t rows = B * R, ntiles = (rows + 15) / 16;
-            const int64_t grid = ntiles < kDenseSynthBlocks ? ntiles : kDenseSynthBlocks;
+            // as many persistent workgroups as the device holds at once
+            static const int64_t resident = [] {
+                int dev = 0, cus = 0, per = 0;
+                if (hipGetDevice(&dev) != hipSuccess ||
+                    hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                        hipSuccess ||
+                    hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                        &per, reinterpret_cast<const void *>(&k_sender_dense<LM>),
+                        64 * DenseSyn<LM>::NW, 0) != hipSuccess ||
+                    cus < 1 || per < 1)
+                    return kDenseSynthBlocks;
+                return (int64_t)cus * per;
+            }();
+            const int64_t grid = ntiles < resident ? ntiles : resident;
             hipLaunchKernelGGL((k_sender_dense<LM>), dim3((unsigned)grid),
                                dim3(64 * DenseSyn<LM>::NW), 0, s, tb.ysyn, rows, H, SF, planes);
             return hipGetLastError();
