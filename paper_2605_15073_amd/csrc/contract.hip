@@ -201,8 +201,10 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
 }
 
 // kdeg contraction (the edge side, Eq. msgpass-tildeR): Y[b][o][l] over the L degree
-// slots of X [B][Cin][L]. A workgroup owns 64 rows b and 64 outputs o for a group of LG
-// degrees, so a row's input block is read once for all of those degrees. The reduction
+// slots of X [B][Cin][L]. A workgroup owns 64 rows b and 64 outputs o for a group of kLG
+// degrees, so a row's input block is read once for all of those degrees (four: with their
+// 64 accumulator registers three waves fit per SIMD, which hides the loads better than
+// seven degrees at two waves, even though a group of 7 then leaves one slot idle). The reduction
 // runs in slices of kCk inputs: each thread prefetches its share of the next slice into
 // registers while the matrix cores work on the current one from LDS. X rows keep their
 // natural (i, l) order in LDS (row stride kSB = 2 mod 32, so the A-operand reads of a
@@ -210,12 +212,12 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
 // its 32 x 32 sub-tile of D[b][o] for every degree of the group (A = X rows, B = W
 // columns, so 16 lanes write 64 contiguous bytes of a row of Y).
 constexpr int kCk = 8;           // reduction slice per LDS stage
-constexpr int kLG = 7;           // degrees per workgroup
-constexpr int kSB = 66;          // LDS row stride of a staged X row (kCk * kLG = 56 used)
+constexpr int kLG = 4;           // degrees per workgroup
+constexpr int kSB = 34;          // LDS row stride of a staged X row (kCk * kLG = 32 used)
 constexpr int kSW = kTile + 16;  // LDS row stride of Ws: lane groups of a half-wave apart
 constexpr int kNX = kTile * kCk * kLG / kThreadsC;  // staged elements per thread and slice
 
-__global__ __launch_bounds__(kThreadsC, 2) void k_contract_kdeg(
+__global__ __launch_bounds__(kThreadsC, 3) void k_contract_kdeg(
     int64_t B, int Cin, int Cout, int L, int otiles, int lgroups, const float *__restrict__ W,
     unsigned w_bytes, int w_sl, int w_si, int w_so, const float *__restrict__ X, int x_sb,
     float *__restrict__ Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
