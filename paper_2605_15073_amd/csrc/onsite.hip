@@ -8,7 +8,11 @@
 // (Eq. struct-tildeA) give A(v) = C + S and A(V - v) = C - S. At both points it
 // forms the product (Eq. struct-S) and the surface curl (Eq. poisson-S2-x), and
 // accumulates the Fourier analysis (Eq. struct-Tmu) in registers with the same
-// pairing. The Gauss-Legendre analysis across u (Eq. struct-Tlm) goes through LDS.
+// pairing. The Gauss-Legendre analysis across u (Eq. struct-Tlm) goes through LDS, one
+// output field at a time, in the space the coefficient rows held (they are dead once the
+// Legendre pass is in registers): the workgroup's LDS is then about half of what both
+// fields' Fourier rows next to the coefficient rows took, so more ranks and workgroups fit
+// per CU.
 //
 // With per-block factors (general parameterization) the Gaunt product takes the values of the
 // Gaunt factors' contractions HA, HB and the surface curl the derivative fields of the curl
@@ -33,8 +37,8 @@ __global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, in
     float *qs = smem;              // [V][M]
     float *ps = qs + V * M;        // [U][P]
     float *dps = ps + U * P;       // [U][P]
-    float *Hs = dps + U * P;       // [2][rb][K]
-    float *Tm = Hs + 2 * rb * K;   // [rb][2][M][U]
+    float *Hs = dps + U * P;       // [2][rb][K], then reused as
+    float *Tm = Hs;                // [rb][M][U]: one field's Fourier rows
 
     const int nrb = (R + rb - 1) / rb;
     const int64_t b = blockIdx.x / nrb;
@@ -55,8 +59,11 @@ __global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, in
 
     const int q = threadIdx.x / U, u = threadIdx.x - q * U;
     const bool active = q < nr;
+    float TA[M], TB[M];
+#pragma unroll
+    for (int mi = 0; mi < M; ++mi) TA[mi] = TB[mi] = 0.f;
+    float FA[M], FxA[M], FB[M], FxB[M];
     if (active) {
-        float FA[M], FxA[M], FB[M], FxB[M];
         const float *h1 = Hs + q * K, *h2 = Hs + (rb + q) * K;
         const float *pu = ps + u * P, *dpu = dps + u * P;
 #pragma unroll
@@ -77,9 +84,9 @@ __global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, in
             FB[mi] = f2;
             FxB[mi] = g2;
         }
-        float TA[M], TB[M];
-#pragma unroll
-        for (int mi = 0; mi < M; ++mi) TA[mi] = TB[mi] = 0.f;
+    }
+    __syncthreads();  // every thread has its coefficients: Hs is free for Tm
+    if (active) {
         for (int v = 0; 2 * v <= V; ++v) {
             const int pv = v == 0 ? 0 : V - v;
             const bool paired = v != 0 && pv != v;
@@ -123,28 +130,30 @@ __global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, in
                 TB[LM - k] += s * sbM;
             }
         }
-        float *tm = Tm + q * 2 * M * U;
-#pragma unroll
-        for (int mi = 0; mi < M; ++mi) {
-            tm[mi * U + u] = TA[mi];
-            tm[(M + mi) * U + u] = TB[mi];
-        }
     }
-    __syncthreads();
-    // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
-    for (int idx = threadIdx.x; idx < 2 * nr * K; idx += blockDim.x) {
-        const int which = idx / (nr * K);
-        const int rem = idx - which * nr * K;
-        const int qq = rem / K, k = rem - qq * K;
-        int l = (int)sqrtf((float)k);
-        while (l * l > k) --l;
-        while ((l + 1) * (l + 1) <= k) ++l;
-        const int m = k - l * l - l, am = m < 0 ? -m : m;
-        const float *tm = Tm + (qq * 2 + which) * M * U + (m + LM) * U;
-        const int pi = l * (l + 1) / 2 + am;
-        float s = 0.f;
-        for (int uu = 0; uu < U; ++uu) s += tb.wq[uu] * ps[uu * P + pi] * tm[uu];
-        (which ? Tb : Ta)[(b * R + r0 + qq) * (int64_t)K + k] = s;
+    // Gauss-Legendre analysis, one field at a time: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u)
+    // Tm[m][u]
+#pragma unroll
+    for (int which = 0; which < 2; ++which) {
+        if (active) {
+            float *tm = Tm + q * M * U;
+#pragma unroll
+            for (int mi = 0; mi < M; ++mi) tm[mi * U + u] = which ? TB[mi] : TA[mi];
+        }
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < nr * K; idx += blockDim.x) {
+            const int qq = idx / K, k = idx - qq * K;
+            int l = (int)sqrtf((float)k);
+            while (l * l > k) --l;
+            while ((l + 1) * (l + 1) <= k) ++l;
+            const int m = k - l * l - l, am = m < 0 ? -m : m;
+            const float *tm = Tm + qq * M * U + (m + LM) * U;
+            const int pi = l * (l + 1) / 2 + am;
+            float s = 0.f;
+            for (int uu = 0; uu < U; ++uu) s += tb.wq[uu] * ps[uu * P + pi] * tm[uu];
+            (which ? Tb : Ta)[(b * R + r0 + qq) * (int64_t)K + k] = s;
+        }
+        __syncthreads();  // Tm is read before the next field overwrites it
     }
 }
 
@@ -157,7 +166,10 @@ hipError_t launch_folded(const Tabs<float> &tb, int64_t B, int R, const float *H
     int rb = 256 / U;
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorInvalidValue;
-    auto lds = [&](int r) { return sizeof(float) * (V * M + 2 * U * P + 2 * r * K + r * 2 * M * U); };
+    auto lds = [&](int r) {
+        const int shared = 2 * r * K > r * M * U ? 2 * r * K : r * M * U;  // Hs, then Tm
+        return sizeof(float) * (V * M + 2 * U * P + shared);
+    };
     while (rb > 1 && lds(rb) > 65536) --rb;
     if (lds(rb) > 65536) return hipErrorInvalidValue;
     const int threads = (rb * U + 63) / 64 * 64;
