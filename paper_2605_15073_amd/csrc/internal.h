@@ -220,7 +220,7 @@ hipError_t launch_analysis_mfma(const Tabs<float> &tb, int64_t B, int R, const f
 // fp32 on-site grid stage on MFMA (fourier_mfma.hip), default grid only: the same
 // contract as launch_onsite_grid. Used from kOnsiteMfmaMinL up; below it the
 // register-resident folded kernel is faster.
-constexpr int kOnsiteMfmaMinL = 13;
+constexpr int kOnsiteMfmaMinL = 15;
 hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const float *HA,
                               const float *HB, float *Ta, float *Tb, hipStream_t s);
 

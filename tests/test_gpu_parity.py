@@ -66,11 +66,12 @@ def test_onsite_lmax_sweep_ragged(cg, lmax, n, C, R):
     _check_pair(run_onsite(cg, plan, to_dev(d, ONSITE_KEYS)), _oracle_onsite(lmax, d), TOL_F32)
 
 
-@pytest.mark.parametrize("lmax,n,C,R", [(2, 9, 5, 17), (6, 7, 8, 33), (12, 5, 6, 19),
-                                        (15, 3, 4, 7), (16, 4, 5, 18), (20, 3, 4, 18),
-                                        (24, 2, 3, 5)])
+@pytest.mark.parametrize("lmax,n,C,R", [(2, 9, 5, 17), (6, 7, 8, 33), (10, 6, 5, 31),
+                                        (12, 5, 6, 19), (14, 3, 4, 23), (15, 3, 4, 7),
+                                        (16, 4, 5, 18), (20, 3, 4, 18), (24, 2, 3, 5)])
 def test_onsite_rank_blocks_and_high_lmax(cg, lmax, n, C, R):
-    # rank counts that leave a partial rank block; lmax >= 15 runs the MFMA grid stage
+    # rank counts that leave a partial rank block; up to lmax 14 the register-resident
+    # folded grid stage runs, from lmax 15 the MFMA one
     d = inputs.onsite_inputs(n, lmax, C, R, seed=300 + lmax, distinct_out=True)
     plan = cg.plan_create(lmax, C, R)
     _check_pair(run_onsite(cg, plan, to_dev(d, ONSITE_KEYS)), _oracle_onsite(lmax, d), TOL_F32)
