@@ -13,7 +13,8 @@
 //   and sums them over l from the transposed Legendre tables (Eq. msgpass-FI), so the
 //   Legendre stage needs no LDS.
 // k_analysis_mfma: inverse transforms (Eqs. msgpass-Tmu, msgpass-Tlm) of the summed grid
-//   fields S [N][R][2][UVs]: rows of S are staged in LDS, then
+//   fields S [N][R][2][UVs]: rows of S are staged in LDS one field at a time (so that a
+//   workgroup's LDS holds more ranks), then
 //     Tm[(q,u)][m] = sum_v S[q][u V + v] q_vm
 //   runs on MFMA and the Gauss-Legendre sum over u reads the weighted transposed
 //   Legendre table with 16-byte loads.
@@ -583,8 +584,8 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
 {
     using G = Grid<LM>;
     extern __shared__ float smem[];
-    float *Ss = smem;                                      // [2][rb U][VS]
-    float *Tm = Ss + (2 * rb * G::U * G::VS + 3) / 4 * 4;  // [rb][2][M][TS], 16-byte aligned
+    float *Ss = smem;                                  // [rb U][VS]: one field's rows at a time
+    float *Tm = Ss + (rb * G::U * G::VS + 3) / 4 * 4;  // [rb][2][M][TS], 16-byte aligned
     const int nrb = (R + rb - 1) / rb;
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
@@ -593,30 +594,9 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
     const int lane = tid & 63, wave = tid >> 6, nw = nt >> 6, g4 = lane >> 4, n = lane & 15;
     const int rows = nr * G::U;
     const int rtiles = (rows + 15) / 16;
-    // stage rows (q, u) of both fields as Ss[f][q U + u][v] (16-byte loads of the stored rows;
-    // columns V .. VP - 1 zero)
-    constexpr int R4 = G::UVs / 4;  // 16-byte words per stored row
-    for (int k = tid; k < 2 * nr * R4; k += nt) {
-        const int qf = k / R4, r = 4 * (k - qf * R4);  // qf = 2 q + f
-        if (r < G::UV) {
-            const float4_t x = *reinterpret_cast<const float4_t *>(
-                S + ((b * R + r0) * 2 + qf) * (int64_t)G::UVs + r);
-            const int q = qf >> 1, f = qf & 1;
-            float *dst = Ss + (f * rb + q) * G::U * G::VS;
-            int u = r / G::V, v = r - u * G::V;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (r + e < G::UV) dst[u * G::VS + v] = x[e];
-                if (++v == G::V) {
-                    v = 0;
-                    ++u;
-                }
-            }
-        }
-    }
     constexpr int pad = G::VP - G::V;
     if (pad > 0)
-        for (int k = tid; k < 2 * rb * G::U * pad; k += nt) {
+        for (int k = tid; k < rb * G::U * pad; k += nt) {
             const int ro = k / pad;
             Ss[ro * G::VS + G::V + (k - ro * pad)] = 0.f;
         }
@@ -635,38 +615,59 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
             const int v = 4 * kk + g4, m = 16 * t + n;
             qb[kk][t] = (v < G::V && m < G::M) ? tb.q[v * G::M + m] : 0.f;
         }
-    __syncthreads();
-    // Tm[(q,u)][m] = sum_v S[(q,u)][v] q_vm for both fields (Eq. msgpass-Tmu)
-    for (int job = wave; job < 2 * rtiles; job += nw) {
-        const int f = job & 1, rt = job >> 1;
-        const int ra = rt * 16 + n;
-        const float *sa = Ss + (f * rb * G::U + (ra < rows ? ra : 0)) * G::VS + g4;
-        float4_t acc[G::MT];
+    constexpr int R4 = G::UVs / 4;  // 16-byte words per stored row
+    for (int f = 0; f < 2; ++f) {
+        // stage rows (q, u) of field f as Ss[q U + u][v] (16-byte loads of the stored rows;
+        // columns V .. VP - 1 stay zero)
+        for (int k = tid; k < nr * R4; k += nt) {
+            const int q = k / R4, r = 4 * (k - q * R4);
+            if (r < G::UV) {
+                const float4_t x = *reinterpret_cast<const float4_t *>(
+                    S + ((b * R + r0 + q) * 2 + f) * (int64_t)G::UVs + r);
+                float *dst = Ss + q * G::U * G::VS;
+                int u = r / G::V, v = r - u * G::V;
 #pragma unroll
-        for (int t = 0; t < G::MT; ++t) acc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < G::KV; ++kk) {
-            const float av = sa[4 * kk];
-#pragma unroll
-            for (int t = 0; t < G::MT; ++t)
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, qb[kk][t], acc[t], 0, 0, 0);
-        }
-#pragma unroll
-        for (int t = 0; t < G::MT; ++t) {
-            const int mi = t * 16 + n;
-            if (mi < G::M) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int ro = rt * 16 + 4 * g4 + j;
-                    if (ro < rows) {
-                        const int qo = ro / G::U, uo = ro - qo * G::U;
-                        Tm[((qo * 2 + f) * G::M + mi) * G::TS + uo] = acc[t][j];
+                for (int e = 0; e < 4; ++e) {
+                    if (r + e < G::UV) dst[u * G::VS + v] = x[e];
+                    if (++v == G::V) {
+                        v = 0;
+                        ++u;
                     }
                 }
             }
         }
+        __syncthreads();
+        // Tm[(q,u)][m] = sum_v S[(q,u)][v] q_vm (Eq. msgpass-Tmu)
+        for (int rt = wave; rt < rtiles; rt += nw) {
+            const int ra = rt * 16 + n;
+            const float *sa = Ss + (ra < rows ? ra : 0) * G::VS + g4;
+            float4_t acc[G::MT];
+#pragma unroll
+            for (int t = 0; t < G::MT; ++t) acc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kk = 0; kk < G::KV; ++kk) {
+                const float av = sa[4 * kk];
+#pragma unroll
+                for (int t = 0; t < G::MT; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, qb[kk][t], acc[t], 0, 0, 0);
+            }
+#pragma unroll
+            for (int t = 0; t < G::MT; ++t) {
+                const int mi = t * 16 + n;
+                if (mi < G::M) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int ro = rt * 16 + 4 * g4 + j;
+                        if (ro < rows) {
+                            const int qo = ro / G::U, uo = ro - qo * G::U;
+                            Tm[((qo * 2 + f) * G::M + mi) * G::TS + uo] = acc[t][j];
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();  // Ss is read before the next field is staged; Tm is complete
     }
-    __syncthreads();
     // Gauss-Legendre analysis of both fields: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
     // (Eq. msgpass-Tlm); one weight row serves both fields
     for (int idx = tid; idx < nr * G::K; idx += nt) {
@@ -877,7 +878,7 @@ hipError_t analysis_lm(const Tabs<float> &tb, int64_t B, int R, const float *S, 
 {
     using G = Grid<LM>;
     const size_t fixed = 3;  // alignment of the Tm region
-    const size_t per_rank = 2 * (size_t)G::U * G::VS + 2 * (size_t)G::M * G::TS;
+    const size_t per_rank = (size_t)G::U * G::VS + 2 * (size_t)G::M * G::TS;
     const int rb = pick_rb(R, fixed, per_rank);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
