@@ -203,7 +203,7 @@ __device__ __forceinline__ void legendre_all(const LaneRows<LM, NOP> &c,
 }
 
 template <int LM>
-__global__ __launch_bounds__(256) void k_sender_mfma(Tabs<float> tb, int R, int rb, int nc,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k_sender_mfma(Tabs<float> tb, int R, int rb, int nc,
                                                      const float *__restrict__ H,
                                                      float *__restrict__ SF, int planes)
 {
