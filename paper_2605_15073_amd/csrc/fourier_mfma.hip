@@ -694,7 +694,7 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
 // ------------------------------------------------------------- on-site grid stage
 
 template <int LM>
-__global__ __launch_bounds__(256) void k_onsite_mfma(Tabs<float> tb, int R, int rb,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(LM <= 16 ? 3 : 1))) void k_onsite_mfma(Tabs<float> tb, int R, int rb,
                                                      const float *__restrict__ HA,
                                                      const float *__restrict__ HB,
                                                      float *__restrict__ Ta,
