@@ -127,15 +127,22 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     // sender fields of edge e (cur) and e + 1 (nxt): the next edge's loads are in flight
     // while this one is computed
     float4_t cI[TPW], cX[TPW], cP[TPW];
+    // lanes whose 4 points all lie past the grid (the padding of the last chunk: up to 18% of
+    // the points at lmax 7-8) load through an offset past the resource, which returns zeros
+    // without a memory request (2^31: past the resource with or without the scalar offsets
+    // below, which stay under 2 UVs x 4 + 192 bytes, and far from wrapping)
+    unsigned vofft[TPW];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) vofft[t] = pw0 + 16 * t + 4 * g < UV ? voff : 0x80000000u;
     auto load_fields = [&](const float *base, int e, float4_t *fI, float4_t *fX, float4_t *fP) {
         const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
         const __amdgpu_buffer_rsrc_t sfr = rsrc(base + j * jstride, sfbytes);
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
             const unsigned so = (unsigned)(t * 16 * 4);
-            fI[t] = bload4(sfr, voff, so);
-            fX[t] = bload4(sfr, voff, so + fstride * 4);
-            fP[t] = bload4(sfr, voff, so + 2 * fstride * 4);
+            fI[t] = bload4(sfr, vofft[t], so);
+            fX[t] = bload4(sfr, vofft[t], so + fstride * 4);
+            fP[t] = bload4(sfr, vofft[t], so + 2 * fstride * 4);
         }
     };
     if (!TWO && e0 < e1) load_fields(sfb, e0, cI, cX, cP);
