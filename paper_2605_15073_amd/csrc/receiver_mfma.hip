@@ -92,6 +92,9 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     const int64_t i = blockIdx.x - (int64_t)rest * NN;
     const int r0 = (rest / nchunks) * kRT;
     const int pw0 = (rest % nchunks) * PC + wave * PW;  // first point of this wave
+    // a wave wholly past the grid (the padding of the last chunk, e.g. at lmax 7, 12, 14, 18)
+    // has nothing to compute or store; waves synchronise only within themselves
+    if (pw0 >= UV) return;
 
     // degrees beyond lmax stay zero in the A operand
     for (int k = lane; k < 2 * 4 * KS * RS; k += 64) Pl[k] = 0.f;
