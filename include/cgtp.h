@@ -305,6 +305,20 @@ int cgtp_onsite_nbody(cgtp_plan plan, int64_t n_nodes, int nu, const void *const
  * Errors: CGTP_ERR_ARG (NULL, flag not set, unknown op), CGTP_ERR_HIP. */
 int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages, int *n_calls);
 
+/* Measurement helper, not part of the method: the read-pattern ceiling of the message-passing
+ * receiver. Replays, for the CSR (row_ptr, col) of cgtp_message_pass, exactly the sender-field
+ * loads of the plan's per-thread receiver (fp32 plans whose receiver is the zonal per-thread
+ * kernel: lmax <= 6 by default, grids of at most 1024 points), in its block order, over
+ * fields [n_nodes][R][3][UVs] (UVs = n_theta * n_phi rounded up to 32; contents arbitrary),
+ * and computes nothing from them; sink is a device float written at most once. Its time is
+ * the floor the receiver's gather pattern sets on the memory path (sender fields are read
+ * once per edge: 12 R n_theta n_phi bytes per edge). Asynchronous on stream.
+ * Errors: CGTP_ERR_ARG (NULL, sizes, fields_bytes too small), CGTP_ERR_UNSUPPORTED (another
+ * receiver), CGTP_ERR_HIP. */
+int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,
+                      const int32_t *col, const void *fields, size_t fields_bytes, void *sink,
+                      void *stream);
+
 /* Release the plan and everything it owns. Synchronises the device first.
  * cgtp_destroy(NULL) is a no-op. */
 int cgtp_destroy(cgtp_plan plan);

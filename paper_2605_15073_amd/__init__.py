@@ -39,7 +39,8 @@ EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_
             "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_workspace_bytes_general",
             "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_message_pass_fields",
             "cgtp_workspace_bytes_nbody", "cgtp_onsite_nbody", "cgtp_stage_times",
-            "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables")
+            "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables",
+            "cgtp_gather_probe")
 ONSITE_STAGES = ("contract_operands", "grid_product_curl_analysis", "project")
 ONSITE_GENERAL_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis",
                          "project_even", "project_odd")
@@ -77,6 +78,7 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_plan_grid.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.cgtp_workspace_bytes.argtypes = [vp, i32, i64, i64, ctypes.POINTER(sz)]
     lib.cgtp_onsite.argtypes = [vp, i64] + [vp] * 8 + [vp, sz, vp]
+    lib.cgtp_gather_probe.argtypes = [vp, i64, i64, vp, vp, vp, sz, vp, vp]
     lib.cgtp_message_pass.argtypes = [vp, i64, i64] + [vp] * 11 + [vp, sz, vp]
     lib.cgtp_message_pass_two_slot.argtypes = [vp, i64, i64] + [vp] * 12 + [vp, sz, vp]
     lib.cgtp_workspace_bytes_general.argtypes = [vp, i32, i64, i64, i32, i32, i32,
@@ -97,6 +99,7 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_last_error.restype = ctypes.c_char_p
     lib.cgtp_host_tables.argtypes = [i32, i32, i32] + [vp] * 5
     for name in ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
+                 "cgtp_gather_probe",
                  "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_stage_times",
                  "cgtp_destroy", "cgtp_host_tables"):
         getattr(lib, name).restype = i32
@@ -222,6 +225,22 @@ def onsite(plan: Plan, A, B, U_A, U_B, U_out_even, U_out_odd, out_even=None, out
                                       _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)),
            "cgtp_onsite")
     return outs[0], outs[1]
+
+
+def gather_probe(plan: Plan, row_ptr, col, fields, sink, stream=None):
+    """cgtp_gather_probe: replay the receiver's sender-field loads over fields (a device
+    buffer of at least N R 3 UVs floats) for the CSR (row_ptr, col); sink: a device float."""
+    torch = _torch()
+    N = row_ptr.shape[0] - 1
+    E = col.shape[0]
+    _want(plan, "row_ptr", row_ptr, (N + 1,), torch.int32)
+    _want(plan, "col", col, (E,), torch.int32)
+    if not fields.is_cuda or not sink.is_cuda:
+        raise ValueError("fields and sink must be device tensors")
+    _check(load_library().cgtp_gather_probe(plan.handle, N, E, _ptr(row_ptr), _ptr(col),
+                                            _ptr(fields), fields.numel() * fields.element_size(),
+                                            _ptr(sink), _stream_handle(stream)),
+           "cgtp_gather_probe")
 
 
 def message_pass(plan: Plan, row_ptr, col, edge_unit, edge_radial, node_feat, U_E, U_I,

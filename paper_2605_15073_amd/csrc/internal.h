@@ -235,4 +235,11 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
                                 const float *Rtg, const float *SF, const float *SFf,
                                 bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s);
 
+// Read-pattern ceiling of the per-thread receiver (kernels.hip): the sender-field loads of
+// k_receiver_zonal (fp32, one grid point per thread, blocks of 8 ranks) over SF
+// [N][R][3][UVs], in its block order, and no arithmetic. hipErrorNotSupported for grids of
+// more than 1024 points.
+hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
+                               const int32_t *col, const float *SF, float *sink, hipStream_t s);
+
 }  // namespace cgtp

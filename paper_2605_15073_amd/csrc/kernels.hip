@@ -592,6 +592,56 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     }
 }
 
+// Read-pattern ceiling of k_receiver_zonal: the same blocks in the same order, the same
+// wave-uniform sender index per edge and the same raw buffer loads of the 3 RB sender
+// values of every grid point, with nothing computed from them but a running sum. sink
+// receives a value only if that sum equals a constant no finite input sums to by chance,
+// which keeps every load live.
+template <int RB>
+__global__ __launch_bounds__(kRecvMaxThreads) void k_gather_probe(
+    int UV, int UVs, int R, const int32_t *__restrict__ row_ptr,
+    const int32_t *__restrict__ col, const float *__restrict__ SF, float *__restrict__ sink)
+{
+    const int nrb = (R + RB - 1) / RB;
+    const int64_t NN = (int64_t)gridDim.x / nrb;
+    const int64_t c = blockIdx.x / NN;
+    const int64_t i = blockIdx.x - c * NN;
+    const int r0 = (int)c * RB;
+    const int nr = (R - r0 < RB) ? (R - r0) : RB;
+    const int uv = threadIdx.x;
+    const unsigned voff = (unsigned)(uv * sizeof(float));
+    const unsigned fstride = (unsigned)(UVs * sizeof(float));
+    float acc = 0.f;
+    const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
+    for (int e = e0; e < e1; ++e) {
+        const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
+        const __amdgpu_buffer_rsrc_t sfr = make_rsrc(SF + (j * R + r0) * 3 * (int64_t)UVs,
+                                                     (unsigned)(nr * 3 * UVs * sizeof(float)));
+        if (uv < UV) {
+#pragma unroll
+            for (int q = 0; q < RB; ++q) {
+                acc += buf_load<float>(sfr, voff, (3 * q) * fstride);
+                acc += buf_load<float>(sfr, voff, (3 * q + 1) * fstride);
+                acc += buf_load<float>(sfr, voff, (3 * q + 2) * fstride);
+            }
+        }
+    }
+    if (acc == -1.2345678e30f) sink[0] = acc;
+}
+
+hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
+                               const int32_t *col, const float *SF, float *sink, hipStream_t s)
+{
+    constexpr int RB = 8;  // the rank block of the fp32 per-thread receiver at one point per thread
+    if (d.UV > kRecvMaxThreads) return hipErrorNotSupported;
+    const int threads = (d.UV + 63) / 64 * 64;
+    const int64_t nb = N * ((R + RB - 1) / RB);
+    if (nb == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_gather_probe<RB>, dim3((unsigned)nb), dim3(threads), 0, s, d.UV, d.UVs,
+                       R, row_ptr, col, SF, sink);
+    return hipGetLastError();
+}
+
 // Separated edge synthesis (Eqs. msgpass-FE, msgpass-AE and the derivative
 // passes): per edge, the real SH of the bond direction, E[k] = Rt_l Y_k(rhat),
 // the Legendre pass and the Fourier pass at every grid point.

@@ -1334,6 +1334,34 @@ int cgtp_onsite_nbody(cgtp_plan plan, int64_t n_nodes, int nu, const void *const
     return run_nbody<float>(plan, n_nodes, nu, X, U, U_out, out, w, s);
 }
 
+int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,
+                      const int32_t *col, const void *fields, size_t fields_bytes, void *sink,
+                      void *stream)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
+    if (n_nodes < 0 || n_edges < 0 || n_edges >= 0x7fffffffLL)
+        return fail(CGTP_ERR_ARG, "bad sizes");
+    if (plan->dtype != CGTP_F32 || use_mfma_receiver(plan, plan->R) ||
+        (plan->flags & CGTP_EDGE_SEPARATED) || plan->d.UV > 1024)
+        return fail(CGTP_ERR_UNSUPPORTED,
+                    "the probe replays the fp32 per-thread zonal receiver (lmax < %d, grids of "
+                    "at most 1024 points)", cgtp::kMfmaRecvMinL);
+    if (n_nodes == 0) return CGTP_OK;
+    if (!row_ptr || !fields || !sink || (n_edges > 0 && !col))
+        return fail(CGTP_ERR_ARG, "NULL argument");
+    const size_t need = sizeof(float) * (size_t)n_nodes * plan->R * 3 * plan->d.UVs;
+    if (fields_bytes < need)
+        return fail(CGTP_ERR_ARG, "fields buffer of %zu bytes, %zu needed", fields_bytes, need);
+    int st = check_device(plan);
+    if (st) return st;
+    hipError_t e = cgtp::launch_gather_probe(plan->d, n_nodes, plan->R, row_ptr, col,
+                                             static_cast<const float *>(fields),
+                                             static_cast<float *>(sink),
+                                             static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? CGTP_OK : hip_fail(e, "gather probe");
+}
+
 int cgtp_destroy(cgtp_plan plan)
 {
     if (!plan) return CGTP_OK;

@@ -283,6 +283,12 @@ WORKLOADS = {
     "onsite_n4096_l12_c128": Workload("onsite_n4096_l12_c128", "onsite", 4096, 12, 128, 128,
                                       seed=3, per_degree=True),
     "mp_5k_l20_c64": Workload("mp_5k_l20_c64", "mp", 5000, 20, 64, 64, seed=4),
+    # the same two message-passing workloads at the cutoff that gives the edge counts quoted
+    # for them (about 301k and 151k directed edges, r_cut = 4.153 A, Z about 30)
+    "mp_10k_l6_c128_rc4153": Workload("mp_10k_l6_c128_rc4153", "mp", 10000, 6, 128, 128,
+                                      seed=2, r_cut=4.153),
+    "mp_5k_l20_c64_rc4153": Workload("mp_5k_l20_c64_rc4153", "mp", 5000, 20, 64, 64, seed=4,
+                                     r_cut=4.153),
     # both node parity slots populated (natural and parity-flipped), Cases A-D of Table 1
     "mp2_10k_l6_c128": Workload("mp2_10k_l6_c128", "mp", 10000, 6, 128, 128, seed=2,
                                 two_slot=True),

@@ -39,3 +39,13 @@ def run_onsite(cg, plan, t, **kw):
 
 def run_mp(cg, plan, t, **kw):
     return cg.message_pass(plan, *(t[k] for k in MP_KEYS), **kw)
+
+
+def sample_rows(n: int, k: int, seed: int):
+    """k distinct rows of [0, n) drawn with a seeded generator over the whole range, always
+    including the first and the last, sorted."""
+    if k >= n:
+        return np.arange(n)
+    rng = np.random.default_rng(seed)
+    inner = rng.choice(np.arange(1, n - 1), max(k - 2, 0), replace=False)
+    return np.unique(np.concatenate([[0, n - 1], inner]))[:max(k, 1)]

@@ -11,7 +11,7 @@ import pytest
 import oracle
 from paper_2605_15073_amd import inputs
 from tests import bruteforce as bf
-from tests.gpu_util import TOL_F32, TOL_F64, rel_err
+from tests.gpu_util import TOL_F32, TOL_F64, rel_err, sample_rows
 from tests.test_gpu_general import _dev, _check
 
 pytestmark = pytest.mark.gpu
@@ -154,7 +154,8 @@ def test_mpf_5k_l6_sampled(cg):
     plan = cg.plan_create(w.lmax, w.C, w.R)
     t = _dev(d, FK)
     gpu = _gpu(cg, plan, t)
-    rec = np.sort(np.random.default_rng(6).choice(w.n, 4, replace=False))
+    rec = sample_rows(w.n, 24, seed=6)
+    assert len(rec) == 24
     _check(gpu, _ref(w.lmax, d, rec), TOL_F32, rows=rec)
     again = _gpu(cg, plan, t)
     assert torch.equal(gpu[0], again[0]) and torch.equal(gpu[1], again[1])

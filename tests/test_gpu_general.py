@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 from paper_2605_15073_amd import inputs
-from tests.gpu_util import TOL_F32, TOL_F64, rel_err
+from tests.gpu_util import TOL_F32, TOL_F64, rel_err, sample_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -174,7 +174,8 @@ def test_onsiteg_n4096_l12_sampled(cg):
     d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R)
     gpu = _on_gpu(cg, plan, _dev(d, ONSITE_G))
-    rows = np.array([0, 1234, w.n - 1])
+    rows = sample_rows(w.n, 24, seed=8)
+    assert len(rows) == 24
     sub = {k: (v[rows] if k in ("A", "B", "A_flip", "B_flip") and v is not None else v)
            for k, v in d.items()}
     _check(gpu, _on_ref(w.lmax, sub), TOL_F32, rows=rows)
@@ -281,7 +282,8 @@ def test_mpg_10k_l6_sampled(cg):
     plan = cg.plan_create(w.lmax, w.C, w.R)
     t = _dev(d, MP_G)
     gpu = _mp_gpu(cg, plan, t)
-    rec = np.sort(np.random.default_rng(5).choice(w.n, 4, replace=False))
+    rec = sample_rows(w.n, 48, seed=5)
+    assert len(rec) == 48
     _check(gpu, _mp_ref(w.lmax, d, rec), TOL_F32, rows=rec)
     again = _mp_gpu(cg, plan, t)
     assert torch.equal(gpu[0], again[0]) and torch.equal(gpu[1], again[1])
