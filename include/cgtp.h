@@ -139,6 +139,24 @@ int cgtp_onsite(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B,
                 const void *U_out_odd, void *out_even, void *out_odd, void *workspace,
                 size_t ws_bytes, void *stream);
 
+/* Size in bytes of the fixed device scratch of cgtp_onsite_noalloc (64 MiB). */
+#define CGTP_NOALLOC_SCRATCH_BYTES 67108864u
+
+/* cgtp_onsite for callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc. Same arguments, results and errors as
+ * cgtp_onsite, except that there is no workspace argument: the workspace is a fixed array of
+ * CGTP_NOALLOC_SCRATCH_BYTES in device memory, one per GPU, resolved by cgtp_plan_create on
+ * the plan's device (the first plan on a device sets it up) and held until the process ends.
+ * The call allocates nothing (no hipMalloc/hipFree, no events: stage times are not recorded
+ * for it). A call whose workspace, cgtp_workspace_bytes(CGTP_OP_ONSITE, n_nodes), exceeds
+ * the scratch returns CGTP_ERR_WORKSPACE before anything is enqueued. Every call on one GPU
+ * shares that GPU's scratch: calls that may overlap on one GPU (several host threads, or
+ * several streams without an ordering between them) race and must be serialised by the
+ * caller. Nothing in the scratch needs to start at zero; it keeps the last call's contents. */
+int cgtp_onsite_noalloc(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B,
+                        const void *U_A, const void *U_B, const void *U_out_even,
+                        const void *U_out_odd, void *out_even, void *out_odd, void *stream);
+
 /* Message passing, Eq. msgpass-parity-start, by the parity-aware pipeline
  * (Eqs. msgpass-tildeR, msgpass-HI, msgpass-FI, msgpass-AI, msgpass-S,
  * cat-beta-curl, msgpass-Tmu, msgpass-Tlm, cat-alpha-phi, cat-beta-phi) for a

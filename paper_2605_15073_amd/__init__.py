@@ -40,7 +40,8 @@ EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_
             "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_message_pass_fields",
             "cgtp_workspace_bytes_nbody", "cgtp_onsite_nbody", "cgtp_stage_times",
             "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables",
-            "cgtp_gather_probe")
+            "cgtp_onsite_noalloc", "cgtp_gather_probe")
+CGTP_NOALLOC_SCRATCH_BYTES = 64 << 20
 ONSITE_STAGES = ("contract_operands", "grid_product_curl_analysis", "project")
 ONSITE_GENERAL_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis",
                          "project_even", "project_odd")
@@ -78,6 +79,7 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_plan_grid.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.cgtp_workspace_bytes.argtypes = [vp, i32, i64, i64, ctypes.POINTER(sz)]
     lib.cgtp_onsite.argtypes = [vp, i64] + [vp] * 8 + [vp, sz, vp]
+    lib.cgtp_onsite_noalloc.argtypes = [vp, i64] + [vp] * 8 + [vp]
     lib.cgtp_gather_probe.argtypes = [vp, i64, i64, vp, vp, vp, sz, vp, vp]
     lib.cgtp_message_pass.argtypes = [vp, i64, i64] + [vp] * 11 + [vp, sz, vp]
     lib.cgtp_message_pass_two_slot.argtypes = [vp, i64, i64] + [vp] * 12 + [vp, sz, vp]
@@ -99,7 +101,7 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_last_error.restype = ctypes.c_char_p
     lib.cgtp_host_tables.argtypes = [i32, i32, i32] + [vp] * 5
     for name in ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
-                 "cgtp_gather_probe",
+                 "cgtp_onsite_noalloc", "cgtp_gather_probe",
                  "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_stage_times",
                  "cgtp_destroy", "cgtp_host_tables"):
         getattr(lib, name).restype = i32
@@ -224,6 +226,33 @@ def onsite(plan: Plan, A, B, U_A, U_B, U_out_even, U_out_odd, out_even=None, out
                                       _ptr(U_out_even), _ptr(U_out_odd), _ptr(outs[0]),
                                       _ptr(outs[1]), ws_ptr, ws_len, _stream_handle(stream)),
            "cgtp_onsite")
+    return outs[0], outs[1]
+
+
+def onsite_noalloc(plan: Plan, A, B, U_A, U_B, U_out_even, U_out_odd, out_even, out_odd,
+                   stream=None):
+    """cgtp_onsite_noalloc: cgtp_onsite on the library's fixed device scratch
+    (CGTP_NOALLOC_SCRATCH_BYTES per GPU). The caller passes the outputs (either may be
+    False to skip that slot); nothing is allocated, here or in the library."""
+    N, C, K = A.shape
+    L = plan.lmax + 1
+    _want(plan, "A", A, (N, plan.channels, L * L))
+    _want(plan, "B", B, A.shape)
+    for nm, U in (("U_A", U_A), ("U_B", U_B)):
+        _want(plan, nm, U, (L, plan.channels, plan.rank))
+    outs = []
+    for nm, o, U in (("out_even", out_even, U_out_even), ("out_odd", out_odd, U_out_odd)):
+        if o is False:
+            outs.append(None)
+            continue
+        _want(plan, nm.replace("out", "U_out"), U, (L, plan.channels, plan.rank))
+        _want(plan, nm, o, A.shape)
+        outs.append(o)
+    _check(load_library().cgtp_onsite_noalloc(plan.handle, N, _ptr(A), _ptr(B), _ptr(U_A),
+                                              _ptr(U_B), _ptr(U_out_even), _ptr(U_out_odd),
+                                              _ptr(outs[0]), _ptr(outs[1]),
+                                              _stream_handle(stream)),
+           "cgtp_onsite_noalloc")
     return outs[0], outs[1]
 
 

@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libcgtp.so")
 SOURCES = ["plan.cpp", "tables.cpp", "contract.hip", "kernels.hip", "onsite.hip", "receiver_mfma.hip", "folded.hip",
-           "fourier_mfma.hip"]
+           "fourier_mfma.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed fp32 VALU ops are disabled for all device code.

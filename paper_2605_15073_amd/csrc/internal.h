@@ -242,4 +242,21 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
 hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
                                const int32_t *col, const float *SF, float *sink, hipStream_t s);
 
+// Status reporting shared by the entry points of every source file: report() stores the
+// detail message returned by cgtp_last_error() on this thread and passes the status through.
+int report(int status, const char *fmt, ...);
+void clear_error();
+
+// The on-site call on a caller-fixed scratch buffer (plan.cpp): the workspace is never
+// grown and no stage events are recorded; CGTP_ERR_WORKSPACE when the scratch is too small.
+int onsite_fixed_scratch(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B,
+                         const void *U_A, const void *U_B, const void *U_out_even,
+                         const void *U_out_odd, void *out_even, void *out_odd, void *scratch,
+                         size_t scratch_bytes, void *stream);
+
+// Resolves the device address of the fixed scratch of cgtp_onsite_noalloc for device dev,
+// which must be current (noalloc.hip). Called by cgtp_plan_create; the result is kept per
+// device and later calls return it.
+hipError_t noalloc_setup(int dev);
+
 }  // namespace cgtp

@@ -333,7 +333,7 @@ hipError_t contract_in(int64_t N, int C, int R, int K, const void *U, const void
 template <typename T>
 int run_onsite(cgtp_plan_s *p, int op, int64_t N, const void *A, const void *B, const void *UA,
                const void *UB, const void *Uoe, const void *Uoo, void *oe, void *oo, char *ws,
-               hipStream_t s)
+               hipStream_t s, bool timed = true)
 {
     const cgtp::Dims &d = p->d;
     const int C = p->C, R = p->R;
@@ -345,7 +345,7 @@ int run_onsite(cgtp_plan_s *p, int op, int64_t N, const void *A, const void *B, 
     T *Tb = reinterpret_cast<T *>(ws + lay.off[3]);
     const int64_t hs = (int64_t)R * d.K;
     StageRec rec;
-    int st = rec.begin(p, op, 3, s);
+    int st = timed ? rec.begin(p, op, 3, s) : CGTP_OK;
     if (st) return st;
     hipError_t e;
     // Eq. struct-H for both operands (shared when the operands coincide); in fp32 the two
@@ -963,6 +963,9 @@ int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan)
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    // the fixed scratch of cgtp_onsite_noalloc is resolved once per device, here, with the
+    // plan's device current; a failure is reported by that entry point, not here
+    (void)cgtp::noalloc_setup(dev);
     size_t n = cgtp::table_elems(d);
     std::vector<double> host(n);
     cgtp::fill_tables(d, host.data());
@@ -1019,11 +1022,17 @@ int cgtp_workspace_bytes(cgtp_plan plan, int op, int64_t n_nodes, int64_t n_edge
     return CGTP_OK;
 }
 
-int cgtp_onsite(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B, const void *U_A,
+}  // extern "C"
+
+namespace {
+
+// Shared by cgtp_onsite and the fixed-scratch entry point. fixed: the workspace is the
+// caller's fixed buffer (never grown by the plan) and no stage events are recorded, so
+// nothing is allocated.
+int onsite_impl(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B, const void *U_A,
                 const void *U_B, const void *U_out_even, const void *U_out_odd, void *out_even,
-                void *out_odd, void *workspace, size_t ws_bytes, void *stream)
+                void *out_odd, void *workspace, size_t ws_bytes, void *stream, bool fixed)
 {
-    g_err[0] = 0;
     if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
     if (n_nodes < 0) return fail(CGTP_ERR_ARG, "n_nodes < 0");
     if (n_nodes == 0) return CGTP_OK;
@@ -1036,14 +1045,57 @@ int cgtp_onsite(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B, c
     int st = check_device(plan);
     if (st) return st;
     void *ws = nullptr;
-    st = get_workspace(plan, onsite_layout(plan, plan->R, n_nodes).total, workspace, ws_bytes, &ws);
+    const size_t need = onsite_layout(plan, plan->R, n_nodes).total;
+    if (fixed && (!workspace || ws_bytes < need))
+        return fail(CGTP_ERR_WORKSPACE,
+                    "%lld nodes need %zu bytes of scratch; the fixed scratch holds %zu",
+                    (long long)n_nodes, need, workspace ? ws_bytes : (size_t)0);
+    st = get_workspace(plan, need, workspace, ws_bytes, &ws);
     if (st) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (plan->dtype == CGTP_F64)
         return run_onsite<double>(plan, CGTP_OP_ONSITE, n_nodes, A, B, U_A, U_B, U_out_even,
-                                  U_out_odd, out_even, out_odd, static_cast<char *>(ws), s);
+                                  U_out_odd, out_even, out_odd, static_cast<char *>(ws), s,
+                                  !fixed);
     return run_onsite<float>(plan, CGTP_OP_ONSITE, n_nodes, A, B, U_A, U_B, U_out_even, U_out_odd,
-                             out_even, out_odd, static_cast<char *>(ws), s);
+                             out_even, out_odd, static_cast<char *>(ws), s, !fixed);
+}
+
+}  // namespace
+
+namespace cgtp {
+
+int onsite_fixed_scratch(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B,
+                         const void *U_A, const void *U_B, const void *U_out_even,
+                         const void *U_out_odd, void *out_even, void *out_odd, void *scratch,
+                         size_t scratch_bytes, void *stream)
+{
+    return onsite_impl(plan, n_nodes, A, B, U_A, U_B, U_out_even, U_out_odd, out_even, out_odd,
+                       scratch, scratch_bytes, stream, true);
+}
+
+int report(int status, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+void clear_error() { g_err[0] = 0; }
+
+}  // namespace cgtp
+
+extern "C" {
+
+int cgtp_onsite(cgtp_plan plan, int64_t n_nodes, const void *A, const void *B, const void *U_A,
+                const void *U_B, const void *U_out_even, const void *U_out_odd, void *out_even,
+                void *out_odd, void *workspace, size_t ws_bytes, void *stream)
+{
+    g_err[0] = 0;
+    return onsite_impl(plan, n_nodes, A, B, U_A, U_B, U_out_even, U_out_odd, out_even, out_odd,
+                       workspace, ws_bytes, stream, false);
 }
 
 namespace {
