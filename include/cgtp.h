@@ -274,7 +274,8 @@ int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
  * workspace with cgtp_workspace_bytes_general(CGTP_OP_MESSAGE_PASS_FIELDS). Other
  * arguments, preconditions and errors as in cgtp_message_pass; CGTP_ERR_UNSUPPORTED also
  * when the per-point receiver (fp64, or fp32 on a grid other than the default) meets a grid
- * of more than 2048 points or LDS staging beyond 64 KiB (fp64 at the highest degrees). */
+ * of more than 2048 points or LDS staging beyond what a workgroup of the device holds (160 KiB
+ * on MI355X; fp64 at the highest degrees). */
 int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
                              const int32_t *row_ptr, const int32_t *col, const void *edge_feat,
                              const void *edge_flip, const void *node_feat, const void *node_flip,
@@ -296,7 +297,7 @@ int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
  * with n_theta >= ((nu + 1) lmax + 2) / 2 (integer division) and n_phi >= (nu + 1) lmax + 1
  * (CGTP_ERR_ARG otherwise, with the sizes in cgtp_last_error). The workspace is
  * cgtp_workspace_bytes_nbody. n_nodes == 0 is a no-op. Errors: CGTP_ERR_ARG,
- * CGTP_ERR_WORKSPACE, CGTP_ERR_UNSUPPORTED (LDS staging over 64 KiB), CGTP_ERR_HIP.
+ * CGTP_ERR_WORKSPACE, CGTP_ERR_UNSUPPORTED (LDS staging beyond a workgroup's), CGTP_ERR_HIP.
  * Stages for cgtp_stage_times (CGTP_OP_ONSITE_NBODY): 0 contract operands, 1 grid product
  * and analysis, 2 project. */
 int cgtp_workspace_bytes_nbody(cgtp_plan plan, int64_t n_nodes, int nu, size_t *bytes);

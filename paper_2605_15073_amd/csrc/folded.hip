@@ -73,12 +73,12 @@ __global__ __launch_bounds__(256) void k_analysis_folded(Tabs<float> tb, int R, 
 }
 
 template <int LM>
-int pick_rb(int U, int R, size_t fixed, size_t per_rank)
+int pick_rb(int U, int R, size_t fixed, size_t per_rank, int lds_max)
 {
     int rb = 256 / U;
     if (rb > 16) rb = 16;
     if (rb > R) rb = R;
-    while (rb > 1 && sizeof(float) * (fixed + rb * per_rank) > 65536) --rb;
+    while (rb > 1 && sizeof(float) * (fixed + rb * per_rank) > (size_t)lds_max) --rb;
     return rb;
 }
 
@@ -89,8 +89,9 @@ hipError_t launch_analysis_lm(const Tabs<float> &tb, int64_t B, int R, const flo
     constexpr int M = 2 * LM + 1, L = LM + 1, P = L * (L + 1) / 2;
     const int U = tb.d.U, V = tb.d.V;
     const size_t fixed = (size_t)V * M + (size_t)U * P;
-    const int rb = pick_rb<LM>(U, R, fixed, (size_t)M * U);
-    if (sizeof(float) * (fixed + rb * (size_t)M * U) > 65536) return hipErrorNotSupported;
+    const int rb = pick_rb<LM>(U, R, fixed, (size_t)M * U, tb.d.lds_max);
+    if (sizeof(float) * (fixed + rb * (size_t)M * U) > (size_t)tb.d.lds_max)
+        return hipErrorNotSupported;
     const int threads = (rb * U + 63) / 64 * 64;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     hipLaunchKernelGGL((k_analysis_folded<LM>), dim3((unsigned)blocks), dim3(threads),

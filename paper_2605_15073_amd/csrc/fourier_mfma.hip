@@ -64,15 +64,17 @@ struct Grid {
     static constexpr int TS = Ut + (Ut % 8 == 0 ? 4 : 0);
 };
 
-constexpr size_t kLdsTarget = 40 * 1024;  // keeps several workgroups resident per CU
+// LDS per workgroup that keeps four workgroups resident on a compute unit
+inline size_t lds_target(const Dims &d) { return (size_t)d.lds_cu / 4; }
 constexpr int64_t kDenseSynthBlocks = 512;  // dense-synthesis workgroups if occupancy is unknown
 
-// Largest rank block (<= 16) within the LDS target, else the largest within 64 KiB.
-int pick_rb(int R, size_t fixed, size_t per_rank)
+// Largest rank block (<= 16) within the LDS target, else the largest within a workgroup's
+// LDS.
+int pick_rb(const Dims &d, int R, size_t fixed, size_t per_rank)
 {
     int rb = R < 16 ? R : 16;
-    while (rb > 1 && sizeof(float) * (fixed + rb * per_rank) > kLdsTarget) --rb;
-    while (rb > 0 && sizeof(float) * (fixed + rb * per_rank) > 65536) --rb;
+    while (rb > 1 && sizeof(float) * (fixed + rb * per_rank) > lds_target(d)) --rb;
+    while (rb > 0 && sizeof(float) * (fixed + rb * per_rank) > (size_t)d.lds_max) --rb;
     return rb;
 }
 
@@ -823,7 +825,7 @@ hipError_t onsite_lm(const Tabs<float> &tb, int64_t B, int R, const float *HA, c
     using G = Grid<LM>;
     const size_t fixed = 4 * (size_t)G::P + (size_t)G::VT * 16 * G::QS + 4;
     const size_t per_rank = 2 * (size_t)G::HR + 2 * (size_t)G::M * G::TS;
-    const int rb = pick_rb(R, fixed, per_rank);
+    const int rb = pick_rb(tb.d, R, fixed, per_rank);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -838,7 +840,7 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
 {
     using G = Grid<LM>;
     const size_t fixed = 4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB;
-    const int rb = pick_rb(R, fixed, G::HR);
+    const int rb = pick_rb(tb.d, R, fixed, G::HR);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -879,7 +881,7 @@ hipError_t analysis_lm(const Tabs<float> &tb, int64_t B, int R, const float *S, 
     using G = Grid<LM>;
     const size_t fixed = 3;  // alignment of the Tm region
     const size_t per_rank = (size_t)G::U * G::VS + 2 * (size_t)G::M * G::TS;
-    const int rb = pick_rb(R, fixed, per_rank);
+    const int rb = pick_rb(tb.d, R, fixed, per_rank);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -933,7 +935,7 @@ hipError_t receiver_fields_lm(const Tabs<float> &tb, int64_t N, int R, const int
         return hipErrorNotSupported;
     const size_t sh = sizeof(float) * (4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB +
                                        2 * (size_t)ns * rb * G::HR);
-    if (sh > 65536) return hipErrorNotSupported;
+    if (sh > (size_t)tb.d.lds_max) return hipErrorNotSupported;
     const int64_t blocks = N * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     if (HEc)

@@ -22,6 +22,9 @@ struct Dims {
     int UV;    // U * V grid points
     int UVs;   // row stride of stored grid fields: UV rounded up to 32 elements, so every
                // row starts on a 128-byte line
+    int lds_max;  // LDS bytes one workgroup may use on the plan's device (queried when the
+                  // plan is created; 64 KiB until then)
+    int lds_cu;   // LDS bytes of one compute unit (the same query)
 };
 
 bool resolve_grid(int lmax, int n_theta, int n_phi, int *U, int *V);
@@ -145,7 +148,7 @@ hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const f
                                 const float *HB, float *Ta, float *Tb, hipStream_t s,
                                 const float *HAc = nullptr, const float *HBc = nullptr);
 // Whether the split form (HAc, HBc given) fits this grid: lmax in range and one rank's rows,
-// tables and coefficients within a workgroup's 64 KiB of LDS.
+// tables and coefficients within a workgroup's LDS.
 bool onsite_split_supported(const Dims &d);
 
 // Message-passing receiver pass: per receiver, synthesise the edge fields, multiply

@@ -238,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void k_onsite_grid(Tabs<T> tb, int R, int
     const Dims &d = tb.d;
     const int64_t br = blockIdx.x;
     const int MU = d.M * d.U;
-    // the Fourier table is staged in LDS unless that would exceed the 64 KiB budget
+    // the Fourier table is staged in LDS unless that would exceed the workgroup's LDS
     T *qs = smem;
     T *H1 = qs + (q_in_lds ? d.V * d.M : 0);
     T *H2 = H1 + d.K;
@@ -289,7 +289,7 @@ hipError_t launch_onsite_grid(const Tabs<T> &tb, int64_t B, int R, const T *HA, 
     }
     const size_t base = 2 * tb.d.K + 4 * tb.d.M * tb.d.U + 2 * tb.d.UV;
     const size_t with_q = base + tb.d.V * tb.d.M;
-    const int q_in_lds = sizeof(T) * with_q <= 65536 ? 1 : 0;
+    const int q_in_lds = sizeof(T) * with_q <= (size_t)tb.d.lds_max ? 1 : 0;
     const size_t sh = sizeof(T) * (q_in_lds ? with_q : base);
     hipLaunchKernelGGL(k_onsite_grid<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R,
                        q_in_lds, HA, HB, Ta, Tb);
@@ -348,9 +348,9 @@ hipError_t launch_nbody_grid(const Tabs<T> &tb, int64_t B, int R, int nu,
     const size_t MU = (size_t)tb.d.M * tb.d.U;
     const size_t base = nu * (tb.d.K + MU) + tb.d.UV + MU;
     const size_t with_q = base + (size_t)tb.d.V * tb.d.M;
-    const int q_in_lds = sizeof(T) * with_q <= 65536 ? 1 : 0;
+    const int q_in_lds = sizeof(T) * with_q <= (size_t)tb.d.lds_max ? 1 : 0;
     const size_t sh = sizeof(T) * (q_in_lds ? with_q : base);
-    if (sh > 65536) return hipErrorNotSupported;
+    if (sh > (size_t)tb.d.lds_max) return hipErrorNotSupported;
     hipLaunchKernelGGL(k_nbody_grid<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s, tb, R, nu,
                        q_in_lds, H, Tout);
     return hipGetLastError();
@@ -902,7 +902,7 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
     if (npt > 3) return hipErrorNotSupported;
     const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
     // ranks per block and table staging: the largest RB whose registers (five values per
-    // rank and point) and LDS (at most 64 KiB; the analysis reuses the edge staging, 2 UV +
+    // rank and point) and LDS (the workgroup's; the analysis reuses the edge staging, 2 UV +
     // 2 MU elements) fit, with the Legendre tables in LDS when they fit too
     const size_t analysis = 2 * (size_t)d.UV + 2 * MU;
     int rb = 0;
@@ -915,11 +915,11 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
         const size_t stage = cand * (2 * (size_t)d.K + 2 * MU);
         const size_t base = (size_t)d.V * d.M + (stage > analysis ? stage : analysis);
         const size_t tabs = 2 * (size_t)d.U * d.P;
-        if (sizeof(T) * (base + tabs) <= 65536) {
+        if (sizeof(T) * (base + tabs) <= (size_t)d.lds_max) {
             rb = cand, lt = true, sh = sizeof(T) * (base + tabs);
             break;
         }
-        if (sizeof(T) * base <= 65536) {
+        if (sizeof(T) * base <= (size_t)d.lds_max) {
             rb = cand, lt = false, sh = sizeof(T) * base;
             break;
         }

@@ -170,8 +170,8 @@ hipError_t launch_folded(const Tabs<float> &tb, int64_t B, int R, const float *H
         const int shared = 2 * r * K > r * M * U ? 2 * r * K : r * M * U;  // Hs, then Tm
         return sizeof(float) * (V * M + 2 * U * P + shared);
     };
-    while (rb > 1 && lds(rb) > 65536) --rb;
-    if (lds(rb) > 65536) return hipErrorInvalidValue;
+    while (rb > 1 && lds(rb) > (size_t)tb.d.lds_max) --rb;
+    if (lds(rb) > (size_t)tb.d.lds_max) return hipErrorInvalidValue;
     const int threads = (rb * U + 63) / 64 * 64;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     hipLaunchKernelGGL((k_onsite_folded<LM>), dim3((unsigned)blocks), dim3(threads), lds(rb), s,
@@ -376,8 +376,8 @@ hipError_t launch_split(const Tabs<float> &tb, int64_t B, int R, const float *HA
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorInvalidValue;
     auto lds = [&](int r) { return split_lds(tb.d, r); };
-    while (rb > 1 && lds(rb) > 65536) --rb;
-    if (lds(rb) > 65536) return hipErrorInvalidValue;
+    while (rb > 1 && lds(rb) > (size_t)tb.d.lds_max) --rb;
+    if (lds(rb) > (size_t)tb.d.lds_max) return hipErrorInvalidValue;
     const int threads = (rb * U + 63) / 64 * 64;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     hipLaunchKernelGGL((k_onsite_split<LM>), dim3((unsigned)blocks), dim3(threads), lds(rb), s,
@@ -492,8 +492,8 @@ hipError_t launch_nbody_folded_lm(const Tabs<float> &tb, int64_t B, int R,
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorNotSupported;
     auto lds = [&](int r) { return sizeof(float) * (V * M + U * P + NU * r * K + r * M * U); };
-    while (rb > 1 && lds(rb) > 65536) --rb;
-    if (lds(rb) > 65536) return hipErrorNotSupported;
+    while (rb > 1 && lds(rb) > (size_t)tb.d.lds_max) --rb;
+    if (lds(rb) > (size_t)tb.d.lds_max) return hipErrorNotSupported;
     const int threads = (rb * U + 63) / 64 * 64;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -518,7 +518,7 @@ hipError_t launch_nbody_folded_nu(const Tabs<float> &tb, int64_t B, int R, int n
 
 bool onsite_split_supported(const Dims &d)
 {
-    return d.lmax <= kOnsiteFoldedMaxL && d.U <= 256 && split_lds(d, 1) <= 65536;
+    return d.lmax <= kOnsiteFoldedMaxL && d.U <= 256 && split_lds(d, 1) <= (size_t)d.lds_max;
 }
 
 hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const float *HA,

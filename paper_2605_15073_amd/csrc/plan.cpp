@@ -816,7 +816,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     if (e == hipErrorNotSupported)
         return fail(CGTP_ERR_UNSUPPORTED,
                     "edge-field receiver: a grid of %d points (at most 2048 off the fp32 default "
-                    "grid) or its LDS staging (at most 64 KiB) is out of range",
+                    "grid) or its LDS staging (beyond a workgroup's LDS) is out of range",
                     p->d.UV);
     if (e != hipSuccess) return hip_fail(e, "receiver (edge field)");
     rec.mark();
@@ -855,7 +855,7 @@ int run_nbody(cgtp_plan_s *p, int64_t N, int nu, const void *const *X, const voi
     rec.mark();
     hipError_t e = cgtp::launch_nbody_grid<T>(tb, N, R, nu, H, Tn, s);
     if (e == hipErrorNotSupported)
-        return fail(CGTP_ERR_UNSUPPORTED, "nu-body grid staging exceeds 64 KiB of LDS");
+        return fail(CGTP_ERR_UNSUPPORTED, "nu-body grid staging exceeds a workgroup's LDS");
     if (e != hipSuccess) return hip_fail(e, "nu-body grid product");
     rec.mark();
     e = project<T>(N, C, R, d.K, Uout, Tn, hs, out, false, s);
@@ -955,14 +955,21 @@ int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan)
                     3 * desc->lmax + 1);
     cgtp::Dims d = cgtp::make_dims(desc->lmax, U, V);
     size_t es = desc->dtype == CGTP_F64 ? 8 : 4;
-    if (max_lds_bytes(d, es) > 65536)
-        return fail(CGTP_ERR_UNSUPPORTED, "grid %d x %d at lmax %d needs %zu B of LDS (> 64 KiB)",
-                    U, V, desc->lmax, max_lds_bytes(d, es));
     if (d.UV > 11 * 256)
         return fail(CGTP_ERR_UNSUPPORTED, "grid of %d points exceeds 2816", d.UV);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    // the LDS of a workgroup and of a compute unit size the kernels' rank blocks
+    e = hipDeviceGetAttribute(&d.lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&d.lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                  dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute(shared memory)");
+    if (max_lds_bytes(d, es) > (size_t)d.lds_max)
+        return fail(CGTP_ERR_UNSUPPORTED,
+                    "grid %d x %d at lmax %d needs %zu B of LDS (the device's workgroups have "
+                    "%d)", U, V, desc->lmax, max_lds_bytes(d, es), d.lds_max);
     // the fixed scratch of cgtp_onsite_noalloc is resolved once per device, here, with the
     // plan's device current; a failure is reported by that entry point, not here
     (void)cgtp::noalloc_setup(dev);

@@ -45,6 +45,8 @@ Dims make_dims(int lmax, int U, int V)
     d.V = V;
     d.UV = U * V;
     d.UVs = (d.UV + 31) / 32 * 32;
+    d.lds_max = 65536;
+    d.lds_cu = 65536;
     return d;
 }
 
