@@ -204,8 +204,10 @@ def load_traffic(workload: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(w, d, budget_s: float = 15.0):
-    """Time the fp64 oracle on a bounded sample of the same workload."""
+def cpu_baseline(w, d, budget_s: float = 15.0, n_fixed: int = 0):
+    """Time the fp64 oracle on a bounded sample of the same workload: the first n nodes or
+    receivers, n chosen to take about budget_s (or n_fixed of them, the whole workload when
+    n_fixed >= its size)."""
     import numpy as np
 
     import oracle
@@ -233,11 +235,14 @@ def cpu_baseline(w, d, budget_s: float = 15.0):
                                  d["U_out_even"], d["U_out_odd"], A_flip=cut("A_flip"),
                                  B_flip=cut("B_flip"))
         unit_name = "nodes"
-    probe = min(w.n, 16)
-    t0 = time.perf_counter()
-    run(probe)
-    tp = time.perf_counter() - t0
-    n = int(min(w.n, max(probe, probe * budget_s / max(tp, 1e-6))))
+    if n_fixed:
+        n = min(w.n, n_fixed)
+    else:
+        probe = min(w.n, 16)
+        t0 = time.perf_counter()
+        run(probe)
+        tp = time.perf_counter() - t0
+        n = int(min(w.n, max(probe, probe * budget_s / max(tp, 1e-6))))
     t0 = time.perf_counter()
     run(n)
     t = time.perf_counter() - t0
@@ -249,7 +254,8 @@ def cpu_baseline(w, d, budget_s: float = 15.0):
 
 # ---------------------------------------------------------------- one workload
 
-def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=False):
+def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=False,
+                   cpu_budget: float = 15.0):
     import torch
 
     import paper_2605_15073_amd as cg
@@ -468,7 +474,7 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
                            "traffic": load_traffic(w.name), "algorithmic_flops": fl}
     else:
         rec["roofline"] = None
-    rec["cpu_baseline"] = cpu_baseline(w, d) if with_cpu else None
+    rec["cpu_baseline"] = cpu_baseline(w, d, cpu_budget) if with_cpu else None
     plan.close()
     return rec
 
@@ -522,11 +528,33 @@ def sweep(path: str, steps: int, warmup: int):
         pts.append(Workload(f"mp_5k_l{lmax}_c64", "mp", 5000, lmax, 64, 64, seed=4))
     with open(path, "w") as f:
         for w in pts:
-            rec = bench_workload(w, steps, warmup, with_cpu=False)
+            # the oracle on a sample of about 2 s of host work next to every point
+            rec = bench_workload(w, steps, warmup, with_cpu=True, cpu_budget=2.0)
             f.write(json.dumps(rec) + "\n")
             f.flush()
             print(f"sweep {w.name}: {rec['ms_per_step']:.3f} ms/step "
                   f"dominant {rec['dominant_kernel']}", flush=True)
+
+
+def cpu_baselines(path: str):
+    """The fp64 oracle on the host cores for the five benchmark workloads: the two smaller
+    on-site ones and the lmax-12 on-site one whole, message passing at lmax 20 on its first
+    64 receivers and at lmax 6 on a sample of about 15 s. One JSON line per workload."""
+    from paper_2605_15073_amd.inputs import WORKLOADS
+
+    plan = [("onsite_n64_l2_c8", 10 ** 9, 0), ("onsite_ace_n2048_l4_c64", 10 ** 9, 0),
+            ("mp_10k_l6_c128", 0, 15.0), ("onsite_n4096_l12_c128", 10 ** 9, 0),
+            ("mp_5k_l20_c64", 64, 0)]
+    with open(path, "w") as f:
+        for name, n_fixed, budget in plan:
+            w = WORKLOADS[name]
+            d = w.make()
+            if w.self_coupled:
+                d = dict(d, B=d["A"])
+            rec = {"workload": name, **cpu_baseline(w, d, budget or 15.0, n_fixed)}
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            print(json.dumps(rec), flush=True)
 
 
 def main():
@@ -537,6 +565,9 @@ def main():
     ap.add_argument("--workload", default="mp_10k_l6_c128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep-out", default=None)
+    ap.add_argument("--cpu-baselines", default=None,
+                    help="time only the fp64 oracle on the five benchmark workloads (whole, "
+                         "or on a stated sample) and write one JSON line each to this file")
     ap.add_argument("--gather-ceiling", action="store_true",
                     help="run only the receiver's read-pattern probe (cgtp_gather_probe) on the "
                          "workload's neighbour list, 5 launches after 2 warm-up launches")
@@ -555,6 +586,9 @@ def main():
         sys.exit(1)
     from paper_2605_15073_amd.inputs import WORKLOADS
 
+    if args.cpu_baselines:
+        cpu_baselines(args.cpu_baselines)
+        return
     if args.copy_bytes:
         n = args.copy_bytes // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
