@@ -58,6 +58,8 @@ struct Tabs {
     const T *wpt;   // [P][Ut] wq[u] * p transposed (Gauss-Legendre analysis weights)
     const T *yc;    // [P] sqrt((2l+1)(l^2-m^2)/(2l-1)): (1-x^2) dPt_l^m/dx
                     //     = yc Pt_{l-1}^m - l x Pt_l^m
+    const T *qd;    // [V][M] the phi-derivative weights of q: column LM + k holds k q[v][LM + k],
+                    // column LM - k holds -k q[v][LM - k] (k >= 1), column LM zero
     const T *ysyn;  // [KP][3 UVs] for lmax <= kDenseSynthMaxL (else empty): row k = (l, m),
                     // KP = K rounded up to 4 (rows past K zero); column f UVs + u V + v holds
                     // Y_k (f = 0), dY_k/dx (f = 1) and dY_k/dphi (f = 2) at grid point (u, v),

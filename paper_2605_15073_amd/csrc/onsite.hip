@@ -24,8 +24,14 @@ namespace cgtp {
 
 namespace {
 
+// qg, qdg: the Fourier factors q_vm [V][M] and their phi-derivative weights as read-only
+// arguments: the azimuth sweep reads one row of each per step, the same for every thread, as
+// scalar loads (operands from scalar registers, no LDS traffic in the sweep).
 template <int LM>
-__global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, int rb,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(LM == 12 || LM == 13 ? 3 : 1)))
+void k_onsite_folded(Tabs<float> tb, int R, int rb,
+                                                       const float *__restrict__ qg,
+                                                       const float *__restrict__ qdg,
                                                        const float *__restrict__ HA,
                                                        const float *__restrict__ HB,
                                                        float *__restrict__ Ta,
@@ -34,8 +40,7 @@ __global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, in
     constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
     extern __shared__ float smem[];
     const int U = tb.d.U, V = tb.d.V;
-    float *qs = smem;              // [V][M]
-    float *ps = qs + V * M;        // [U][P]
+    float *ps = smem;              // [U][P]
     float *dps = ps + U * P;       // [U][P]
     float *Hs = dps + U * P;       // [2][rb][K], then reused as
     float *Tm = Hs;                // [rb][M][U]: one field's Fourier rows
@@ -44,7 +49,6 @@ __global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, in
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
-    for (int k = threadIdx.x; k < V * M; k += blockDim.x) qs[k] = tb.q[k];
     for (int k = threadIdx.x; k < U * P; k += blockDim.x) {
         ps[k] = tb.p[k];
         dps[k] = tb.dp[k];
@@ -90,26 +94,26 @@ __global__ __launch_bounds__(256) void k_onsite_folded(Tabs<float> tb, int R, in
         for (int v = 0; 2 * v <= V; ++v) {
             const int pv = v == 0 ? 0 : V - v;
             const bool paired = v != 0 && pv != v;
-            const float *qr = qs + v * M;
+            const float *qr = qg + v * M, *qdr = qdg + v * M;
             // cosine (C) and sine (S) parts of A, dA/dx, dA/dphi for both operands
             float aC = FA[LM], aS = 0.f, axC = FxA[LM], axS = 0.f, apC = 0.f, apS = 0.f;
             float bC = FB[LM], bS = 0.f, bxC = FxB[LM], bxS = 0.f, bpC = 0.f, bpS = 0.f;
 #pragma unroll
             for (int k = 1; k <= LM; ++k) {
                 const float c = qr[LM + k], s = qr[LM - k];
-                const float kc = (float)k * c, ks = (float)k * s;
+                const float kc = qdr[LM + k], mks = qdr[LM - k];  // k cos, -k sin
                 aC += c * FA[LM + k];
                 aS += s * FA[LM - k];
                 axC += c * FxA[LM + k];
                 axS += s * FxA[LM - k];
                 apC += kc * FA[LM - k];
-                apS -= ks * FA[LM + k];
+                apS += mks * FA[LM + k];
                 bC += c * FB[LM + k];
                 bS += s * FB[LM - k];
                 bxC += c * FxB[LM + k];
                 bxS += s * FxB[LM - k];
                 bpC += kc * FB[LM - k];
-                bpS -= ks * FB[LM + k];
+                bpS += mks * FB[LM + k];
             }
             float sa0 = (aC + aS) * (bC + bS);
             float sb0 = (apC + apS) * (bxC + bxS) - (axC + axS) * (bpC + bpS);
@@ -162,27 +166,28 @@ hipError_t launch_folded(const Tabs<float> &tb, int64_t B, int R, const float *H
                          const float *HB, float *Ta, float *Tb, hipStream_t s)
 {
     constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
-    const int U = tb.d.U, V = tb.d.V;
+    const int U = tb.d.U;
     int rb = 256 / U;
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorInvalidValue;
     auto lds = [&](int r) {
         const int shared = 2 * r * K > r * M * U ? 2 * r * K : r * M * U;  // Hs, then Tm
-        return sizeof(float) * (V * M + 2 * U * P + shared);
+        return sizeof(float) * (2 * U * P + shared);
     };
     while (rb > 1 && lds(rb) > (size_t)tb.d.lds_max) --rb;
     if (lds(rb) > (size_t)tb.d.lds_max) return hipErrorInvalidValue;
     const int threads = (rb * U + 63) / 64 * 64;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     hipLaunchKernelGGL((k_onsite_folded<LM>), dim3((unsigned)blocks), dim3(threads), lds(rb), s,
-                       tb, R, rb, HA, HB, Ta, Tb);
+                       tb, R, rb, tb.q, tb.qd, HA, HB, Ta, Tb);
     return hipGetLastError();
 }
 
 // Azimuth sweep of one row at latitude u for the Gaunt product (Eq. struct-S): synthesise
 // A from FA and B from FB at each pair (v, V - v) and add the Fourier analysis (Eq.
 // struct-Tmu) of A B into T. qs row v holds cos(k phi_v) at LM + k and sin(k phi_v) at
-// LM - k.
+// LM - k: the plan's table, passed down from a read-only kernel argument so that each row is
+// read with scalar loads.
 template <int LM>
 __device__ __forceinline__ void sweep_product(const float *FA, const float *FB,
                                               const float *qs, int V, float *T)
@@ -216,26 +221,27 @@ __device__ __forceinline__ void sweep_product(const float *FA, const float *FB,
 // with the phi-derivatives taken from FA, FB by swapping the cosine and sine halves.
 template <int LM>
 __device__ __forceinline__ void sweep_curl(const float *FA, const float *FxA, const float *FB,
-                                           const float *FxB, const float *qs, int V, float *T)
+                                           const float *FxB, const float *qs, const float *qds,
+                                           int V, float *T)
 {
     constexpr int M = 2 * LM + 1;
     for (int v = 0; 2 * v <= V; ++v) {
         const bool paired = v != 0 && 2 * v != V;
-        const float *qr = qs + v * M;
+        const float *qr = qs + v * M, *qdr = qds + v * M;
         float axC = FxA[LM], axS = 0.f, apC = 0.f, apS = 0.f;
         float bxC = FxB[LM], bxS = 0.f, bpC = 0.f, bpS = 0.f;
 #pragma unroll
         for (int k = 1; k <= LM; ++k) {
             const float c = qr[LM + k], s = qr[LM - k];
-            const float kc = (float)k * c, ks = (float)k * s;
+            const float kc = qdr[LM + k], mks = qdr[LM - k];  // k cos, -k sin
             axC += c * FxA[LM + k];
             axS += s * FxA[LM - k];
             apC += kc * FA[LM - k];
-            apS -= ks * FA[LM + k];
+            apS += mks * FA[LM + k];
             bxC += c * FxB[LM + k];
             bxS += s * FxB[LM - k];
             bpC += kc * FB[LM - k];
-            bpS -= ks * FB[LM + k];
+            bpS += mks * FB[LM + k];
         }
         const float s0 = (apC + apS) * (bxC + bxS) - (axC + axS) * (bpC + bpS);
         const float s1 =
@@ -255,6 +261,8 @@ __device__ __forceinline__ void sweep_curl(const float *FA, const float *FxA, co
 // curl's to Tb. One (rank, u) thread per row, as above; Tm holds one product at a time.
 template <int LM>
 __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int rb,
+                                                      const float *__restrict__ qg,
+                                                      const float *__restrict__ qdg,
                                                       const float *__restrict__ HA,
                                                       const float *__restrict__ HB,
                                                       const float *__restrict__ HAc,
@@ -265,8 +273,7 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
     constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
     extern __shared__ float smem[];
     const int U = tb.d.U, V = tb.d.V;
-    float *qs = smem;              // [V][M]
-    float *ps = qs + V * M;        // [U][P]
+    float *ps = smem;              // [U][P]
     float *dps = ps + U * P;       // [U][P]
     float *Hs = dps + U * P;       // [2][rb][K]
     float *Tm = Hs + 2 * rb * K;   // [rb][M][U]
@@ -275,7 +282,6 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
-    for (int k = threadIdx.x; k < V * M; k += blockDim.x) qs[k] = tb.q[k];
     for (int k = threadIdx.x; k < U * P; k += blockDim.x) {
         ps[k] = tb.p[k];
         dps[k] = tb.dp[k];
@@ -313,7 +319,7 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
                     FA[mi] = f1;
                     FB[mi] = f2;
                 }
-                sweep_product<LM>(FA, FB, qs, V, T);
+                sweep_product<LM>(FA, FB, qg, V, T);
             } else {
                 float FA[M], FxA[M], FB[M], FxB[M];
 #pragma unroll
@@ -334,7 +340,7 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
                     FB[mi] = f2;
                     FxB[mi] = g2;
                 }
-                sweep_curl<LM>(FA, FxA, FB, FxB, qs, V, T);
+                sweep_curl<LM>(FA, FxA, FB, FxB, qg, qdg, V, T);
             }
             float *tm = Tm + q * M * U;
 #pragma unroll
@@ -358,12 +364,12 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
     }
 }
 
-// LDS bytes of k_onsite_split with rb ranks per block: twiddles, both Legendre tables, two
-// staged row sets and the Fourier coefficients of one product.
+// LDS bytes of k_onsite_split with rb ranks per block: both Legendre tables, two staged row
+// sets and the Fourier coefficients of one product.
 size_t split_lds(const Dims &d, int rb)
 {
     const size_t M = 2 * d.lmax + 1, L = d.lmax + 1, K = L * L, P = L * (L + 1) / 2;
-    return sizeof(float) * (d.V * M + 2 * d.U * P + rb * (2 * K + M * d.U));
+    return sizeof(float) * (2 * d.U * P + rb * (2 * K + M * d.U));
 }
 
 template <int LM>
@@ -381,7 +387,7 @@ hipError_t launch_split(const Tabs<float> &tb, int64_t B, int R, const float *HA
     const int threads = (rb * U + 63) / 64 * 64;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     hipLaunchKernelGGL((k_onsite_split<LM>), dim3((unsigned)blocks), dim3(threads), lds(rb), s,
-                       tb, R, rb, HA, HB, HAc, HBc, Ta, Tb);
+                       tb, R, rb, tb.q, tb.qd, HA, HB, HAc, HBc, Ta, Tb);
     return hipGetLastError();
 }
 
@@ -394,14 +400,14 @@ hipError_t launch_split(const Tabs<float> &tb, int64_t B, int R, const float *HA
 // goes through LDS. The grid (U, V) is the plan's, exact for the (NU + 1) lmax integrand.
 template <int LM, int NU>
 __global__ __launch_bounds__(256) void k_nbody_folded(Tabs<float> tb, int R, int rb,
+                                                      const float *__restrict__ qg,
                                                       NbodyOperands<float> H,
                                                       float *__restrict__ Tout)
 {
     constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
     extern __shared__ float smem[];
     const int U = tb.d.U, V = tb.d.V;
-    float *qs = smem;              // [V][M]
-    float *ps = qs + V * M;        // [U][P]
+    float *ps = smem;              // [U][P]
     float *Hs = ps + U * P;        // [NU][rb][K]
     float *Tm = Hs + NU * rb * K;  // [rb][M][U]
 
@@ -409,7 +415,6 @@ __global__ __launch_bounds__(256) void k_nbody_folded(Tabs<float> tb, int R, int
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
-    for (int k = threadIdx.x; k < V * M; k += blockDim.x) qs[k] = tb.q[k];
     for (int k = threadIdx.x; k < U * P; k += blockDim.x) ps[k] = tb.p[k];
 #pragma unroll
     for (int t = 0; t < NU; ++t) {
@@ -440,7 +445,7 @@ __global__ __launch_bounds__(256) void k_nbody_folded(Tabs<float> tb, int R, int
         for (int v = 0; 2 * v <= V; ++v) {
             const int pv = v == 0 ? 0 : V - v;
             const bool paired = v != 0 && pv != v;
-            const float *qr = qs + v * M;
+            const float *qr = qg + v * M;
             float p0 = 1.f, p1 = 1.f;  // the product at v and at V - v
 #pragma unroll
             for (int t = 0; t < NU; ++t) {
@@ -487,18 +492,18 @@ hipError_t launch_nbody_folded_lm(const Tabs<float> &tb, int64_t B, int R,
                                   const NbodyOperands<float> &H, float *Tout, hipStream_t s)
 {
     constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
-    const int U = tb.d.U, V = tb.d.V;
+    const int U = tb.d.U;
     int rb = 256 / U;
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorNotSupported;
-    auto lds = [&](int r) { return sizeof(float) * (V * M + U * P + NU * r * K + r * M * U); };
+    auto lds = [&](int r) { return sizeof(float) * (U * P + NU * r * K + r * M * U); };
     while (rb > 1 && lds(rb) > (size_t)tb.d.lds_max) --rb;
     if (lds(rb) > (size_t)tb.d.lds_max) return hipErrorNotSupported;
     const int threads = (rb * U + 63) / 64 * 64;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     hipLaunchKernelGGL((k_nbody_folded<LM, NU>), dim3((unsigned)blocks), dim3(threads), lds(rb),
-                       s, tb, R, rb, H, Tout);
+                       s, tb, R, rb, tb.q, H, Tout);
     return hipGetLastError();
 }
 

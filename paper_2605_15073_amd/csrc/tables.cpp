@@ -168,9 +168,10 @@ static void region_sizes(const Dims &d, size_t *n)
     n[17] = (size_t)d.P * ut;   // wpt
     n[18] = d.P;                // yc
     n[19] = d.lmax <= kDenseSynthMaxL ? (size_t)(d.K + 3) / 4 * 4 * 3 * d.UVs : 0;  // ysyn
+    n[20] = (size_t)d.V * d.M;  // qd
 }
 
-static const int kRegions = 20;
+static const int kRegions = 21;
 
 static size_t round_up(size_t n) { return (n + 63) & ~(size_t)63; }  // 512 B for fp64
 
@@ -236,6 +237,13 @@ void fill_tables(const Dims &d, double *h)
                 h[off[13] + idx] = 0.0;
             }
         }
+    // phi-derivative weights of the Fourier factors (real basis: d/dphi maps cos(k phi) to
+    // -k sin(k phi) and sin(k phi) to k cos(k phi))
+    for (int v = 0; v < d.V; ++v)
+        for (int k = 1; k <= d.lmax; ++k) {
+            h[off[20] + (size_t)v * d.M + d.lmax + k] = k * h[off[6] + (size_t)v * d.M + d.lmax + k];
+            h[off[20] + (size_t)v * d.M + d.lmax - k] = -k * h[off[6] + (size_t)v * d.M + d.lmax - k];
+        }
     // Dense synthesis table: with k = l^2 + l + m and the real basis Y_k = Pt_l^|m|(x) q_m(phi),
     // d/dphi maps q_m to -m q_{-m} (cos(m phi) -> -m sin(m phi), sin(|m| phi) -> |m| cos(|m| phi)).
     if (n[19]) {
@@ -294,6 +302,7 @@ Tabs<T> bind_tables(const Dims &d, const void *dev)
     tb.wpt = ptr[17];
     tb.yc = ptr[18];
     tb.ysyn = ptr[19];
+    tb.qd = ptr[20];
     tb.d = d;
     return tb;
 }
