@@ -16,8 +16,8 @@
 //
 // With per-block factors (general parameterization) the Gaunt product takes the values of the
 // Gaunt factors' contractions HA, HB and the surface curl the derivative fields of the curl
-// factors' contractions HAc, HBc; that kernel runs the two in phases through one LDS
-// footprint.
+// factors' contractions HAc, HBc; that kernel sweeps the two one after the other, with both
+// output rows in registers and the same LDS reuse.
 #include "internal.h"
 
 namespace cgtp {
@@ -256,27 +256,27 @@ __device__ __forceinline__ void sweep_curl(const float *FA, const float *FxA, co
     }
 }
 
-// Per-block factors: phase 0 stages the Gaunt rows HA, HB and writes the product's
-// coefficients to Ta, phase 1 stages the curl rows HAc, HBc into the same LDS and writes the
-// curl's to Tb. One (rank, u) thread per row, as above; Tm holds one product at a time.
+// Per-block factors: the workgroup stages the Gaunt rows HA, HB and the curl rows HAc, HBc
+// once; each (rank, u) thread sweeps the surface curl from the second pair (values and
+// x-derivatives), then the Gaunt product from the first (values only: the smaller register set
+// while the curl's Fourier row is held), keeping both Fourier rows in registers. Once every thread has its coefficients the staged rows are dead and their LDS
+// holds one output field's Fourier rows at a time for the Gauss-Legendre analysis, as in
+// k_onsite_folded.
 template <int LM>
-__global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int rb,
-                                                      const float *__restrict__ qg,
-                                                      const float *__restrict__ qdg,
-                                                      const float *__restrict__ HA,
-                                                      const float *__restrict__ HB,
-                                                      const float *__restrict__ HAc,
-                                                      const float *__restrict__ HBc,
-                                                      float *__restrict__ Ta,
-                                                      float *__restrict__ Tb)
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(LM >= 11 && LM <= 13 ? 3 : 1)))
+void k_onsite_split(Tabs<float> tb, int R, int rb, const float *__restrict__ qg,
+                    const float *__restrict__ qdg, const float *__restrict__ HA,
+                    const float *__restrict__ HB, const float *__restrict__ HAc,
+                    const float *__restrict__ HBc, float *__restrict__ Ta,
+                    float *__restrict__ Tb)
 {
     constexpr int M = 2 * LM + 1, L = LM + 1, K = L * L, P = L * (L + 1) / 2;
     extern __shared__ float smem[];
     const int U = tb.d.U, V = tb.d.V;
     float *ps = smem;              // [U][P]
     float *dps = ps + U * P;       // [U][P]
-    float *Hs = dps + U * P;       // [2][rb][K]
-    float *Tm = Hs + 2 * rb * K;   // [rb][M][U]
+    float *Hs = dps + U * P;       // [4][rb][K]: HA, HB, HAc, HBc rows, then reused as
+    float *Tm = Hs;                // [rb][M][U]: one field's Fourier rows
 
     const int nrb = (R + rb - 1) / rb;
     const int64_t b = blockIdx.x / nrb;
@@ -286,69 +286,76 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
         ps[k] = tb.p[k];
         dps[k] = tb.dp[k];
     }
+    const int64_t row0 = (b * R + r0) * (int64_t)K;
+    for (int k = threadIdx.x; k < nr * K; k += blockDim.x) {
+        Hs[k] = HA[row0 + k];
+        Hs[rb * K + k] = HB[row0 + k];
+        Hs[2 * rb * K + k] = HAc[row0 + k];
+        Hs[3 * rb * K + k] = HBc[row0 + k];
+    }
+    __syncthreads();
+
     const int q = threadIdx.x / U, u = threadIdx.x - q * U;
     const bool active = q < nr;
-    const float *pu = ps + u * P, *dpu = dps + u * P;
-    const float *h1 = Hs + q * K, *h2 = Hs + (rb + q) * K;
-    for (int ph = 0; ph < 2; ++ph) {
-        // the previous phase's sweep has read Hs and its analysis Tm before the barrier
-        // that follows this staging
-        const float *src1 = (ph ? HAc : HA) + (b * R + r0) * (int64_t)K;
-        const float *src2 = (ph ? HBc : HB) + (b * R + r0) * (int64_t)K;
-        for (int k = threadIdx.x; k < nr * K; k += blockDim.x) {
-            Hs[k] = src1[k];
-            Hs[rb * K + k] = src2[k];
-        }
-        __syncthreads();
-        if (active) {
-            float T[M];
+    float TA[M], TB[M];
 #pragma unroll
-            for (int mi = 0; mi < M; ++mi) T[mi] = 0.f;
-            if (ph == 0) {
-                float FA[M], FB[M];
+    for (int mi = 0; mi < M; ++mi) TA[mi] = TB[mi] = 0.f;
+    if (active) {
+        const float *pu = ps + u * P, *dpu = dps + u * P;
+        {
+            const float *h1 = Hs + (2 * rb + q) * K, *h2 = Hs + (3 * rb + q) * K;
+            float FA[M], FxA[M], FB[M], FxB[M];
 #pragma unroll
-                for (int mi = 0; mi < M; ++mi) {
-                    const int m = mi - LM, am = m < 0 ? -m : m;
-                    float f1 = 0.f, f2 = 0.f;
+            for (int mi = 0; mi < M; ++mi) {
+                const int m = mi - LM, am = m < 0 ? -m : m;
+                float f1 = 0.f, g1 = 0.f, f2 = 0.f, g2 = 0.f;
 #pragma unroll
-                    for (int l = am; l <= LM; ++l) {
-                        const float p = pu[l * (l + 1) / 2 + am];
-                        f1 += p * h1[l * l + l + m];
-                        f2 += p * h2[l * l + l + m];
-                    }
-                    FA[mi] = f1;
-                    FB[mi] = f2;
+                for (int l = am; l <= LM; ++l) {
+                    const float p = pu[l * (l + 1) / 2 + am], dp = dpu[l * (l + 1) / 2 + am];
+                    const float c1 = h1[l * l + l + m], c2 = h2[l * l + l + m];
+                    f1 += p * c1;
+                    g1 += dp * c1;
+                    f2 += p * c2;
+                    g2 += dp * c2;
                 }
-                sweep_product<LM>(FA, FB, qg, V, T);
-            } else {
-                float FA[M], FxA[M], FB[M], FxB[M];
-#pragma unroll
-                for (int mi = 0; mi < M; ++mi) {
-                    const int m = mi - LM, am = m < 0 ? -m : m;
-                    float f1 = 0.f, g1 = 0.f, f2 = 0.f, g2 = 0.f;
-#pragma unroll
-                    for (int l = am; l <= LM; ++l) {
-                        const float p = pu[l * (l + 1) / 2 + am], dp = dpu[l * (l + 1) / 2 + am];
-                        const float c1 = h1[l * l + l + m], c2 = h2[l * l + l + m];
-                        f1 += p * c1;
-                        g1 += dp * c1;
-                        f2 += p * c2;
-                        g2 += dp * c2;
-                    }
-                    FA[mi] = f1;
-                    FxA[mi] = g1;
-                    FB[mi] = f2;
-                    FxB[mi] = g2;
-                }
-                sweep_curl<LM>(FA, FxA, FB, FxB, qg, qdg, V, T);
+                FA[mi] = f1;
+                FxA[mi] = g1;
+                FB[mi] = f2;
+                FxB[mi] = g2;
             }
+            sweep_curl<LM>(FA, FxA, FB, FxB, qg, qdg, V, TB);
+        }
+        {
+            const float *h1 = Hs + q * K, *h2 = Hs + (rb + q) * K;
+            float FA[M], FB[M];
+#pragma unroll
+            for (int mi = 0; mi < M; ++mi) {
+                const int m = mi - LM, am = m < 0 ? -m : m;
+                float f1 = 0.f, f2 = 0.f;
+#pragma unroll
+                for (int l = am; l <= LM; ++l) {
+                    const float p = pu[l * (l + 1) / 2 + am];
+                    f1 += p * h1[l * l + l + m];
+                    f2 += p * h2[l * l + l + m];
+                }
+                FA[mi] = f1;
+                FB[mi] = f2;
+            }
+            sweep_product<LM>(FA, FB, qg, V, TA);
+        }
+    }
+    __syncthreads();  // every thread has its Fourier rows: Hs is free for Tm
+    // Gauss-Legendre analysis, one field at a time: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u)
+    // Tm[m][u]
+#pragma unroll
+    for (int which = 0; which < 2; ++which) {
+        if (active) {
             float *tm = Tm + q * M * U;
 #pragma unroll
-            for (int mi = 0; mi < M; ++mi) tm[mi * U + u] = T[mi];
+            for (int mi = 0; mi < M; ++mi) tm[mi * U + u] = which ? TB[mi] : TA[mi];
         }
         __syncthreads();
-        // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
-        float *dst = ph ? Tb : Ta;
+        float *dst = which ? Tb : Ta;
         for (int idx = threadIdx.x; idx < nr * K; idx += blockDim.x) {
             const int qq = idx / K, k = idx - qq * K;
             int l = (int)sqrtf((float)k);
@@ -361,15 +368,17 @@ __global__ __launch_bounds__(256) void k_onsite_split(Tabs<float> tb, int R, int
             for (int uu = 0; uu < U; ++uu) s += tb.wq[uu] * ps[uu * P + pi] * tm[uu];
             dst[(b * R + r0 + qq) * (int64_t)K + k] = s;
         }
+        __syncthreads();  // Tm is read before the next field overwrites it
     }
 }
 
-// LDS bytes of k_onsite_split with rb ranks per block: both Legendre tables, two staged row
-// sets and the Fourier coefficients of one product.
+// LDS bytes of k_onsite_split with rb ranks per block: both Legendre tables and the four
+// staged row sets, whose space then holds one field's Fourier rows.
 size_t split_lds(const Dims &d, int rb)
 {
     const size_t M = 2 * d.lmax + 1, L = d.lmax + 1, K = L * L, P = L * (L + 1) / 2;
-    return sizeof(float) * (2 * d.U * P + rb * (2 * K + M * d.U));
+    const size_t rows = 4 * K > M * d.U ? 4 * K : M * d.U;
+    return sizeof(float) * (2 * d.U * P + rb * rows);
 }
 
 template <int LM>
