@@ -128,13 +128,31 @@ __device__ __forceinline__ void stage_rows(const float *src, float *dst, int nr)
 // in l, started by adding seed = Pt_|m|^|m|(x) at l = |m| (seed 0 for the padding orders
 // |m| > lmax). Below l = |m| a lane carries zeros. The loop is unrolled from the lowest
 // |m| of the step, so every table offset is a constant.
+// Degrees a lane visits at reduction step kk (orders 4 kk - lmax .. 4 kk - lmax + 3):
+// l = a0(kk) .. lmax, the lowest |m| of the step upwards; base(kk) counts the (step, degree)
+// pairs of the steps before kk.
+template <int LM>
+struct LegendreSteps {
+    static constexpr int a0(int kk)
+    {
+        const int lo = 4 * kk - LM, hi = lo + 3;
+        return (lo <= 0 && hi >= 0) ? 0 : (lo > 0 ? lo : -hi);
+    }
+    static constexpr int base(int kk)
+    {
+        int b = 0;
+        for (int k = 0; k < kk; ++k) b += LM - a0(k) + 1;
+        return b;
+    }
+    static constexpr int N = base(Grid<LM>::KM);
+};
+
 template <int LM, int KK, int NOP>
 __device__ __forceinline__ void legendre_step(const float4_t *cf, const float *const *h, float seed,
                                               float x, float r, int m, float *fa, float *fx,
                                               float *fn)
 {
-    constexpr int lo = 4 * KK - LM, hi = lo + 3;
-    constexpr int A0 = (lo <= 0 && hi >= 0) ? 0 : (lo > 0 ? lo : -hi);
+    constexpr int A0 = LegendreSteps<LM>::a0(KK);
     const int am = m < 0 ? (-m < LM ? -m : LM) : (m < LM ? m : LM);
     const float4_t *ca = cf + am;
     float p1 = 0.f, p2 = 0.f;
@@ -201,6 +219,71 @@ __device__ __forceinline__ void legendre_all(const LaneRows<LM, NOP> &c,
         // line code would otherwise hold every step's operands in registers at once
         __builtin_amdgcn_sched_barrier(0);
         legendre_all<LM, NOP, KK + 1>(c, bf);
+    }
+}
+
+// The functions legendre_step forms, tabulated for one lane and every step: pv[base(KK) + l -
+// a0(KK)] = Pt_l^|m|(x) and dv[...] = dPt_l^|m|/dx at the step's order m (zero below l = |m|),
+// by the same recurrence and arithmetic. They depend on the lane's node and orders only, so a
+// lane that runs the Legendre pass once per edge forms them once.
+template <int LM, int KK>
+__device__ __forceinline__ void legendre_tabulate(const float4_t *cf, const float *seed, float x,
+                                                  float r, int g4,
+                                                  float (&pv)[LegendreSteps<LM>::N],
+                                                  float (&dv)[LegendreSteps<LM>::N])
+{
+    if constexpr (KK < Grid<LM>::KM) {
+        constexpr int A0 = LegendreSteps<LM>::a0(KK), B = LegendreSteps<LM>::base(KK);
+        const int m = 4 * KK + g4 - LM;
+        const int am = m < 0 ? (-m < LM ? -m : LM) : (m < LM ? m : LM);
+        const float4_t *ca = cf + am;
+        float p1 = 0.f, p2 = 0.f;
+#pragma unroll
+        for (int l = A0; l <= LM; ++l) {
+            const float4_t c = ca[l * (l + 1) / 2];
+            const float inj = (l == am) ? seed[KK] : 0.f;
+            const float p = c[0] * (x * p1 - c[1] * p2) + inj;
+            pv[B + l - A0] = p;
+            dv[B + l - A0] = (c[2] * p1 - (float)l * x * p) * r;
+            p2 = p1;
+            p1 = p;
+        }
+        legendre_tabulate<LM, KK + 1>(cf, seed, x, r, g4, pv, dv);
+    }
+}
+
+// legendre_all over tabulated functions (legendre_tabulate): the same sums in the same order.
+template <int LM, int NOP, int KK>
+__device__ __forceinline__ void legendre_all_tab(const float *const *h, int g4,
+                                                 const float (&pv)[LegendreSteps<LM>::N],
+                                                 const float (&dv)[LegendreSteps<LM>::N],
+                                                 float (&bf)[Grid<LM>::KM][NOP][3])
+{
+    if constexpr (KK < Grid<LM>::KM) {
+        constexpr int A0 = LegendreSteps<LM>::a0(KK), B = LegendreSteps<LM>::base(KK);
+        const int m = 4 * KK + g4 - LM;
+        float fa[NOP], fx[NOP], fn[NOP];
+#pragma unroll
+        for (int o = 0; o < NOP; ++o) fa[o] = fx[o] = fn[o] = 0.f;
+#pragma unroll
+        for (int l = A0; l <= LM; ++l) {
+            const float p = pv[B + l - A0], d = dv[B + l - A0];
+#pragma unroll
+            for (int o = 0; o < NOP; ++o) {
+                const float cp = h[o][l * l + l + m];
+                fa[o] += p * cp;
+                fx[o] += d * cp;
+                fn[o] += p * h[o][l * l + l - m];
+            }
+        }
+#pragma unroll
+        for (int o = 0; o < NOP; ++o) {
+            bf[KK][o][0] = fa[o];
+            bf[KK][o][1] = fx[o];
+            bf[KK][o][2] = (float)m * fn[o];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        legendre_all_tab<LM, NOP, KK + 1>(h, g4, pv, dv, bf);
     }
 }
 
@@ -405,8 +488,28 @@ template <int LM>
 struct FieldsTiles {
     using G = Grid<LM>;
     static constexpr int RB = (64 / G::U) < 1 ? 1 : ((64 / G::U) < 16 ? (64 / G::U) : 16);
-    static constexpr int KPT = 8;  // prefetched coefficients per thread and edge, at most
+    // prefetched coefficients per thread, edge and row set: rb rows of HR elements over
+    // 64 ceil(rb U / 16) >= 4 rb U threads
+    static constexpr int KPT = (G::HR + 4 * G::U - 1) / (4 * G::U);
 };
+
+// Raw buffer resource over [base, base + bytes): loads past the end return 0 without a memory
+// request.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t fields_rsrc(const void *base, unsigned bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ float fields_load(__amdgpu_buffer_rsrc_t rs, unsigned voff,
+                                             unsigned soff)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0));
+}
+
+// A byte offset past every resource here, also with the scalar offsets added (which stay far
+// below 2^31): such loads return 0.
+constexpr unsigned kFieldsOutside = 0x80000000u;
 
 // Receiver for a general per-edge field (two parity-bearing fields, Eq. twoparity-phi):
 // a workgroup owns one receiver and rb ranks, one wave per 16-row tile of rows (rank q,
@@ -417,7 +520,9 @@ struct FieldsTiles {
 // msgpass-S and cat-beta-curl; 16 lanes read 64 contiguous bytes of a row). A lane requests
 // its sender fields and its share of the next edge's coefficient rows when the edge starts,
 // so both arrive while it computes; the rows are double-buffered in LDS (one barrier per
-// edge). The products accumulate in registers over the CSR row; the sums go to
+// edge). Both are buffer loads whose per-lane byte offsets are fixed over the CSR row and
+// computed once (rows and columns past the block read 0 from past the resource); only the
+// wave-uniform resources change per edge. The products accumulate in registers over the CSR row; the sums go to
 // S [N][R][2][UVs] for k_analysis_mfma. Blocks run rank block by rank block, all receivers
 // inside one, so the memory-side cache serves a rank slice of the sender fields.
 // SPLIT: the value field comes from the rows HE (Gaunt factors) and the two derivative
@@ -472,56 +577,91 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
         const int qo = ro / G::U, uo = ro - qo * G::U;
         off[j] = ro < rows ? qo * 3 * G::UVs + uo * G::V : -1;
     }
+    // sender-field byte offsets of D row j at v = 16 t + n: tile t at the scalar offset 64 t,
+    // the last tile (whose columns may pass V) with offsets of its own
+    constexpr int VL = G::V - 16 * (G::VT - 1);  // valid columns of the last tile
+    unsigned foff[4], flast[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        foff[j] = off[j] >= 0 ? (unsigned)(off[j] + n) * 4u : kFieldsOutside;
+        flast[j] = off[j] >= 0 && n < VL ? foff[j] : kFieldsOutside;
+    }
+    const unsigned fbytes = (unsigned)(nr * 3 * G::UVs * 4);
+    // staged element kk = tid + t blockDim of a row set is element ii = kk % HR - HL of
+    // margin-padded row q = kk / HR: coefficient q K + ii of the edge's rank block, or a
+    // margin (0)
+    unsigned hoff[KPT];
+#pragma unroll
+    for (int t = 0; t < KPT; ++t) {
+        const int kk = threadIdx.x + t * blockDim.x;
+        const int q = kk / G::HR, ii = kk - q * G::HR - G::HL;
+        hoff[t] = kk < nh && ii >= 0 && ii < G::K ? (unsigned)(q * G::K + ii) * 4u
+                                                   : kFieldsOutside;
+    }
+    const unsigned hbytes = (unsigned)(nr * G::K * 4);
+    auto fetch_rows = [&](int64_t e, float (&hv)[NS][KPT]) {
+#pragma unroll
+        for (int set = 0; set < NS; ++set) {
+            const __amdgpu_buffer_rsrc_t rs =
+                fields_rsrc((set ? HEc : HE) + (e * R + r0) * G::K, hbytes);
+#pragma unroll
+            for (int t = 0; t < KPT; ++t) hv[set][t] = fields_load(rs, hoff[t], 0);
+        }
+    };
+    auto store_rows = [&](float *buf, const float (&hv)[NS][KPT]) {
+#pragma unroll
+        for (int set = 0; set < NS; ++set)
+#pragma unroll
+            for (int t = 0; t < KPT; ++t) {
+                const int kk = threadIdx.x + t * blockDim.x;
+                if (kk < nh) buf[set * hset + kk] = hv[set][t];
+            }
+    };
     float4_t sa[G::VT], sb[G::VT];
 #pragma unroll
     for (int t = 0; t < G::VT; ++t) sa[t] = sb[t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
-    // staged element k of an edge: row set k / nh, then the margin-padded row element
-    // q HR + HL + i of that set
-    auto coef = [&](int64_t e, int k) -> float {
-        const int set = (SPLIT && k >= nh) ? 1 : 0;
-        const int kk = k - set * nh;
-        const int q = kk / G::HR, ii = kk - q * G::HR - G::HL;
-        const float *he = (set ? HEc : HE) + (e * R + r0) * G::K;
-        return (k < NS * nh && ii >= 0 && ii < G::K) ? he[q * G::K + ii] : 0.f;
-    };
-    auto slot_of = [&](int k) { return (SPLIT && k >= nh) ? hset + (k - nh) : k; };
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     if (e0 < e1) {
-        for (int k = threadIdx.x; k < NS * nh; k += blockDim.x) Hs[slot_of(k)] = coef(e0, k);
+        float h0[NS][KPT];
+        fetch_rows(e0, h0);
+        store_rows(Hs, h0);
     }
     __syncthreads();
+    // small lmax: the lane's Legendre functions in registers, formed once for the CSR row
+    constexpr int NT = LegendreSteps<LM>::N;
+    constexpr bool TAB = 2 * NT <= 44;
+    float pvt[NT], dvt[NT];
+    if constexpr (TAB) legendre_tabulate<LM, 0>(cf, seed, c.x, c.r, g4, pvt, dvt);
     for (int e = e0; e < e1; ++e) {
         const int cur = (e - e0) & 1;
         const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
         // this edge's sender fields at the lane's D rows and columns
-        const float *sfj = SF + (j * R + r0) * 3 * (int64_t)G::UVs;
+        const __amdgpu_buffer_rsrc_t sfr = fields_rsrc(SF + (j * R + r0) * 3 * (int64_t)G::UVs,
+                                                       fbytes);
         float fI[G::VT][4], fX[G::VT][4], fP[G::VT][4];
 #pragma unroll
         for (int t = 0; t < G::VT; ++t) {
-            const int v = t * 16 + n;
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-                const bool ok = off[jj] >= 0 && v < G::V;
-                const float *f = sfj + (ok ? off[jj] + v : 0);
-                fI[t][jj] = ok ? f[0] : 0.f;
-                fX[t][jj] = ok ? f[G::UVs] : 0.f;
-                fP[t][jj] = ok ? f[2 * G::UVs] : 0.f;
+                const unsigned vo = t == G::VT - 1 ? flast[jj] : foff[jj];
+                const unsigned so = (unsigned)(t * 16 * 4);
+                fI[t][jj] = fields_load(sfr, vo, so);
+                fX[t][jj] = fields_load(sfr, vo, so + G::UVs * 4);
+                fP[t][jj] = fields_load(sfr, vo, so + 2 * G::UVs * 4);
             }
         }
         // the next edge's coefficient rows, stored after this edge's Legendre pass
-        float hn[KPT];
+        float hn[NS][KPT];
         const bool more = e + 1 < e1;
-        if (more) {
-#pragma unroll
-            for (int t = 0; t < KPT; ++t) hn[t] = coef(e + 1, threadIdx.x + t * blockDim.x);
-        }
+        if (more) fetch_rows(e + 1, hn);
         if (rt * 16 < rows) {  // wave-uniform: waves past the last tile only help stage rows
             float *hcur = Hs + cur * NS * hset;
             c.h[0] = hcur + qa * G::HR + G::HL;
             if (SPLIT) c.h[NS - 1] = hcur + hset + qa * G::HR + G::HL;
             float bfa[G::KM][NS][3];
-            legendre_all<LM, NS, 0>(c, bfa);
+            if constexpr (TAB) legendre_all_tab<LM, NS, 0>(c.h, g4, pvt, dvt, bfa);
+            else legendre_all<LM, NS, 0>(c, bfa);
             // value from the first row set, the derivative fields from the last
             float bf[G::KM][1][3];
 #pragma unroll
@@ -549,14 +689,7 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
                 }
             }
         }
-        if (more) {
-            float *hnext = Hs + (cur ^ 1) * NS * hset;
-#pragma unroll
-            for (int t = 0; t < KPT; ++t) {
-                const int k = threadIdx.x + t * blockDim.x;
-                if (k < NS * nh) hnext[slot_of(k)] = hn[t];
-            }
-        }
+        if (more) store_rows(Hs + (cur ^ 1) * NS * hset, hn);
         __syncthreads();  // the next rows are staged; this edge's rows are consumed
     }
     float *Sr = S + (i * R + r0) * 2 * (int64_t)G::UVs;
@@ -930,8 +1063,10 @@ hipError_t receiver_fields_lm(const Tabs<float> &tb, int64_t N, int R, const int
     if (rb > R) rb = R;
     if (rb < 1) return hipErrorNotSupported;
     const int waves = (rb * G::U + 15) / 16;
-    // every staged row element is fetched by some thread's prefetch
-    if ((size_t)ns * rb * G::HR > (size_t)FieldsTiles<LM>::KPT * 64 * waves)
+    // every staged row element is fetched by some thread's prefetch, and the buffer offsets of
+    // a rank block's coefficients and sender fields stay below 2^31
+    if ((size_t)rb * G::HR > (size_t)FieldsTiles<LM>::KPT * 64 * waves ||
+        (size_t)rb * 3 * G::UVs * 4 >= (size_t)kFieldsOutside)
         return hipErrorNotSupported;
     const size_t sh = sizeof(float) * (4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB +
                                        2 * (size_t)ns * rb * G::HR);
