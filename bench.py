@@ -30,6 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_RECV_MIN_L = 7            # fp32 message passing: the MFMA receiver from this lmax on
 FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector (and matrix) peak
 CSRC = os.path.join(ROOT, "paper_2605_15073_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
@@ -56,9 +57,10 @@ def grid_dims(lmax: int):
 
 def receiver_bytes(lmax: int, R: int, N: int, E: int, slots: int = 1, planes: int = 0,
                    rt_blocks: int = 1, t_fields: int = 2) -> int:
-    """HBM bytes the receiver pass must move (fp32): per edge the sender grid fields the
-    couplings read (value A for a Gaunt coupling, dA/dx and dA/dphi for a curl coupling:
-    3 R UV per node slot when both categories share the factors), the edge radial
+    """Bytes the receiver pass must move (fp32): per edge the sender grid fields the
+    couplings read (planes R UV floats: the value A for a Gaunt coupling and, for a curl
+    coupling, dA/dx and dA/dphi, or nothing more when the curl's derivatives are moved onto
+    the analysis; default 3 per node slot), the edge radial
     coefficients (R L per distinct edge factor block), the unit vector and the sender
     index; per receiver the row pointer and the analysed fields (R K each)."""
     U, V = grid_dims(lmax)
@@ -448,8 +450,12 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
                 rt_blocks=1 if w.in_blocks == 1 else len(live),
                 t_fields=len(live) if w.out_blocks == 2 else 2)
         else:
-            alg = receiver_bytes(w.lmax, w.R, w.n, E, 2 if w.two_slot else 1)
-            comp = compulsory_receiver_bytes(w.lmax, w.R, w.n, E, 6 if w.two_slot else 3)
+            # the zonal receiver (lmax < MFMA_RECV_MIN_L) takes the curl in the moved-derivative
+            # form and reads one plane per node slot; the MFMA receiver reads three
+            per_slot = 1 if w.lmax < MFMA_RECV_MIN_L else 3
+            slots = 2 if w.two_slot else 1
+            alg = receiver_bytes(w.lmax, w.R, w.n, E, slots, planes=per_slot * slots)
+            comp = compulsory_receiver_bytes(w.lmax, w.R, w.n, E, per_slot * slots)
         traffic = load_traffic(w.name)
         # The receiver reads each sender's grid fields once per edge (about 52 times per
         # sender). Those gathers are served by the memory-side cache and the fabric into L2,
@@ -488,8 +494,8 @@ def probe_ok(w) -> bool:
 def gather_ceiling(plan, w, t, E, reps: int = 5):
     """Time cgtp_gather_probe (the receiver's sender-field loads alone, same blocks and order)
     on the workload's CSR over a zero-filled field buffer of the receiver's layout, with HIP
-    events on the stream it runs on. Returns the bytes the receiver gathers per launch (12 R U V
-    per edge), the mean launch time and their ratio."""
+    events on the stream it runs on. Returns the bytes the receiver gathers per launch (the
+    value plane: 4 R U V per edge), the mean launch time and their ratio."""
     import torch
 
     import paper_2605_15073_amd as cg
@@ -508,7 +514,7 @@ def gather_ceiling(plan, w, t, E, reps: int = 5):
     e1.record(cur)
     e1.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    gathered = 4 * E * 3 * w.R * U * V
+    gathered = 4 * E * w.R * U * V
     del fields
     return {"pattern": "per-edge sender-field loads of the zonal receiver",
             "bytes": gathered, "ms": ms, "GBs": gathered / (ms / 1e3) / 1e9}

@@ -330,8 +330,10 @@ int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages,
  * kernel: lmax <= 6 by default, grids of at most 1024 points), in its block order, over
  * fields [n_nodes][R][3][UVs] (UVs = n_theta * n_phi rounded up to 32; contents arbitrary),
  * and computes nothing from them; sink is a device float written at most once. Its time is
- * the floor the receiver's gather pattern sets on the memory path (sender fields are read
- * once per edge: 12 R n_theta n_phi bytes per edge). Asynchronous on stream.
+ * the floor the receiver's gather pattern sets on the memory path. That receiver takes the
+ * surface curl with both derivatives moved onto the analysis (integration by parts on the
+ * sphere), so it reads only the value plane (plane 0) of each sender rank, once per edge:
+ * 4 R n_theta n_phi bytes per edge. Asynchronous on stream.
  * Errors: CGTP_ERR_ARG (NULL, sizes, fields_bytes too small), CGTP_ERR_UNSUPPORTED (another
  * receiver), CGTP_ERR_HIP. */
 int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,

@@ -711,16 +711,23 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
 
 // ------------------------------------------------------ inverse transforms (MP)
 
-template <int LM>
+// Grid fields per (node, rank) of S for k_analysis_mfma: MODE 0 the summed Gaunt product and
+// surface curl (into Ta, Tb); MODE 1 the Gaunt sum into Ta and the curl's moved-derivative
+// pair (S1, S2 of analysis_moved) into Tb; MODE 2 (two node slots) a value sum and a moved
+// pair for each of Ta and Tb.
+constexpr int analysis_fields(int mode) { return mode == 0 ? 2 : mode == 1 ? 3 : 6; }
+
+template <int LM, int MODE>
 __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, int rb,
                                                        const float *__restrict__ S,
                                                        float *__restrict__ Ta,
                                                        float *__restrict__ Tb)
 {
     using G = Grid<LM>;
+    constexpr int NF = analysis_fields(MODE);
     extern __shared__ float smem[];
     float *Ss = smem;                                  // [rb U][VS]: one field's rows at a time
-    float *Tm = Ss + (rb * G::U * G::VS + 3) / 4 * 4;  // [rb][2][M][TS], 16-byte aligned
+    float *Tm = Ss + (rb * G::U * G::VS + 3) / 4 * 4;  // [rb][NF][M][TS], 16-byte aligned
     const int nrb = (R + rb - 1) / rb;
     const int64_t b = blockIdx.x / nrb;
     const int r0 = (int)(blockIdx.x - b * nrb) * rb;
@@ -737,7 +744,7 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
         }
     constexpr int tpad = G::Ut - G::U;
     if (tpad > 0)
-        for (int k = tid; k < nr * 2 * G::M * tpad; k += nt) {
+        for (int k = tid; k < nr * NF * G::M * tpad; k += nt) {
             const int ro = k / tpad;
             Tm[ro * G::TS + G::U + (k - ro * tpad)] = 0.f;
         }
@@ -751,14 +758,14 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
             qb[kk][t] = (v < G::V && m < G::M) ? tb.q[v * G::M + m] : 0.f;
         }
     constexpr int R4 = G::UVs / 4;  // 16-byte words per stored row
-    for (int f = 0; f < 2; ++f) {
+    for (int f = 0; f < NF; ++f) {
         // stage rows (q, u) of field f as Ss[q U + u][v] (16-byte loads of the stored rows;
         // columns V .. VP - 1 stay zero)
         for (int k = tid; k < nr * R4; k += nt) {
             const int q = k / R4, r = 4 * (k - q * R4);
             if (r < G::UV) {
                 const float4_t x = *reinterpret_cast<const float4_t *>(
-                    S + ((b * R + r0 + q) * 2 + f) * (int64_t)G::UVs + r);
+                    S + ((b * R + r0 + q) * NF + f) * (int64_t)G::UVs + r);
                 float *dst = Ss + q * G::U * G::VS;
                 int u = r / G::V, v = r - u * G::V;
 #pragma unroll
@@ -795,7 +802,7 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
                         const int ro = rt * 16 + 4 * g4 + j;
                         if (ro < rows) {
                             const int qo = ro / G::U, uo = ro - qo * G::U;
-                            Tm[((qo * 2 + f) * G::M + mi) * G::TS + uo] = acc[t][j];
+                            Tm[((qo * NF + f) * G::M + mi) * G::TS + uo] = acc[t][j];
                         }
                     }
                 }
@@ -803,23 +810,42 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
         }
         __syncthreads();  // Ss is read before the next field is staged; Tm is complete
     }
-    // Gauss-Legendre analysis of both fields: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u]
-    // (Eq. msgpass-Tlm); one weight row serves both fields
+    // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u] (Eq.
+    // msgpass-Tlm) of each value field; a moved-derivative pair (F1, F2) adds
+    // -m sum_u w_u (2 pi / V) Pt_l^|m|(x_u) F1[-m][u] - sum_u w_u (2 pi / V) dPt_l^|m|/dx(x_u) F2[m][u]
     for (int idx = tid; idx < nr * G::K; idx += nt) {
         const int q = idx / G::K, k = idx - q * G::K;
         const int l = (int)sqrtf((float)k + 0.5f);  // exact for k < 2^20
         const int m = k - l * l - l, am = m < 0 ? -m : m;
-        const float4_t *w4 =
-            reinterpret_cast<const float4_t *>(tb.wpt + (l * (l + 1) / 2 + am) * G::Ut);
-        const float4_t *ta4 = reinterpret_cast<const float4_t *>(Tm + ((q * 2) * G::M + m + LM) * G::TS);
-        const float4_t *tb4 =
-            reinterpret_cast<const float4_t *>(Tm + ((q * 2 + 1) * G::M + m + LM) * G::TS);
-        float s0 = 0.f, s1 = 0.f;
+        const int pi = l * (l + 1) / 2 + am;
+        const float4_t *w4 = reinterpret_cast<const float4_t *>(tb.wpt + pi * G::Ut);
+        const float4_t *wd4 = reinterpret_cast<const float4_t *>(tb.wdpt + pi * G::Ut);
+        auto row = [&](int f, int mm) {
+            return reinterpret_cast<const float4_t *>(Tm + ((q * NF + f) * G::M + mm + LM) * G::TS);
+        };
+        auto dot = [&](const float4_t *w, const float4_t *x) {
+            float sum = 0.f;
 #pragma unroll
-        for (int c = 0; c < G::Ut / 4; ++c) {
-            const float4_t w = w4[c], x0 = ta4[c], x1 = tb4[c];
-            s0 += w[0] * x0[0] + w[1] * x0[1] + w[2] * x0[2] + w[3] * x0[3];
-            s1 += w[0] * x1[0] + w[1] * x1[1] + w[2] * x1[2] + w[3] * x1[3];
+            for (int c = 0; c < G::Ut / 4; ++c) {
+                const float4_t a = w[c], y = x[c];
+                sum += a[0] * y[0] + a[1] * y[1] + a[2] * y[2] + a[3] * y[3];
+            }
+            return sum;
+        };
+        const float fm = (float)m;
+        // the moved pair's term, formed alike in every mode: a zero flipped slot (mode 2)
+        // then gives exactly the one-slot result (mode 1)
+        auto curl = [&](int f1) { return -fm * dot(w4, row(f1, -m)) - dot(wd4, row(f1 + 1, m)); };
+        float s0, s1;
+        if constexpr (MODE == 0) {
+            s0 = dot(w4, row(0, m));
+            s1 = dot(w4, row(1, m));
+        } else if constexpr (MODE == 1) {
+            s0 = dot(w4, row(0, m));
+            s1 = curl(1);
+        } else {
+            s0 = dot(w4, row(0, m)) + curl(1);
+            s1 = dot(w4, row(3, m)) + curl(4);
         }
         Ta[(b * R + r0 + q) * (int64_t)G::K + k] = s0;
         Tb[(b * R + r0 + q) * (int64_t)G::K + k] = s1;
@@ -1009,18 +1035,24 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
 
 template <int LM>
 hipError_t analysis_lm(const Tabs<float> &tb, int64_t B, int R, const float *S, float *Ta,
-                       float *Tb, hipStream_t s)
+                       float *Tb, hipStream_t s, int mode)
 {
     using G = Grid<LM>;
     const size_t fixed = 3;  // alignment of the Tm region
-    const size_t per_rank = (size_t)G::U * G::VS + 2 * (size_t)G::M * G::TS;
+    const size_t per_rank =
+        (size_t)G::U * G::VS + (size_t)analysis_fields(mode) * G::M * G::TS;
     const int rb = pick_rb(tb.d, R, fixed, per_rank);
     if (rb < 1) return hipErrorNotSupported;
     const int64_t blocks = B * ((R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_analysis_mfma<LM>), dim3((unsigned)blocks),
-                       dim3(64 * waves_for(rb * G::U)), sizeof(float) * (fixed + rb * per_rank), s,
-                       tb, R, rb, S, Ta, Tb);
+    const dim3 grid((unsigned)blocks), block(64 * waves_for(rb * G::U));
+    const size_t sh = sizeof(float) * (fixed + rb * per_rank);
+    if (mode == 0)
+        hipLaunchKernelGGL((k_analysis_mfma<LM, 0>), grid, block, sh, s, tb, R, rb, S, Ta, Tb);
+    else if (mode == 1)
+        hipLaunchKernelGGL((k_analysis_mfma<LM, 1>), grid, block, sh, s, tb, R, rb, S, Ta, Tb);
+    else
+        hipLaunchKernelGGL((k_analysis_mfma<LM, 2>), grid, block, sh, s, tb, R, rb, S, Ta, Tb);
     return hipGetLastError();
 }
 
@@ -1118,13 +1150,13 @@ hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
 }
 
 hipError_t launch_analysis_mfma(const Tabs<float> &tb, int64_t B, int R, const float *S, float *Ta,
-                                float *Tb, hipStream_t s)
+                                float *Tb, hipStream_t s, int mode)
 {
     if (B == 0) return hipSuccess;
-    if (!default_grid(tb.d)) return hipErrorNotSupported;
+    if (!default_grid(tb.d) || mode < 0 || mode > 2) return hipErrorNotSupported;
     switch (tb.d.lmax) {
 #define CGTP_CASE(LMV) \
-    case LMV: return analysis_lm<LMV>(tb, B, R, S, Ta, Tb, s);
+    case LMV: return analysis_lm<LMV>(tb, B, R, S, Ta, Tb, s, mode);
         CGTP_LMAX_CASES(CGTP_CASE)
 #undef CGTP_CASE
     default: return hipErrorNotSupported;

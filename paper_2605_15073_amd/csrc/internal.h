@@ -56,6 +56,7 @@ struct Tabs {
     const T *pt;    // [P][Ut] p transposed, Ut = U rounded up to 4, zero padded
     const T *dpt;   // [P][Ut] dp transposed
     const T *wpt;   // [P][Ut] wq[u] * p transposed (Gauss-Legendre analysis weights)
+    const T *wdpt;  // [P][Ut] wq[u] * dp transposed
     const T *yc;    // [P] sqrt((2l+1)(l^2-m^2)/(2l-1)): (1-x^2) dPt_l^m/dx
                     //     = yc Pt_{l-1}^m - l x Pt_l^m
     const T *qd;    // [V][M] the phi-derivative weights of q: column LM + k holds k q[v][LM + k],
@@ -160,11 +161,15 @@ bool onsite_split_supported(const Dims &d);
 // field, one node slot).
 // SFf: NULL, or the sender fields of the parity-flipped node slot (two-slot message
 // passing; not with the separated edge field).
+// values_only: the curl in the moved-derivative form, which reads only the value plane of the
+// sender fields (the others need not be written); not with the separated edge field or Rtg.
+// Sg (fp32, values_only, default grid): the summed fields go to Sg [N][R][3][UVs] ([6] with
+// SFf) and the MFMA analysis follows; NULL: the analysis runs inside the receiver.
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
                            const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
-                           hipStream_t s);
+                           hipStream_t s, bool values_only = false, T *Sg = nullptr);
 
 // Receiver pass for a general per-edge field (two parity-bearing fields): HE [E][R][K] are
 // the edge field's channel-contracted coefficients (edge e = row_ptr order), SF the sender
@@ -220,8 +225,12 @@ inline int sf_chunks(const Dims &d) { return (d.UV + kSfChunk - 1) / kSfChunk; }
 bool sender_mfma_supported(const Dims &d);
 hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
                               bool chunked, hipStream_t s, int planes = 7);
+// Inverse transforms on MFMA of the summed grid fields S [B][R][NF][UVs] into Ta, Tb
+// (default grid): mode 0, NF = 2 (Gaunt product, surface curl); mode 1, NF = 3 (Gaunt sum;
+// the curl's moved-derivative pair S1, S2); mode 2, NF = 6 (per output a value sum and a
+// moved pair, two node slots). hipErrorNotSupported off the default grid.
 hipError_t launch_analysis_mfma(const Tabs<float> &tb, int64_t B, int R, const float *S,
-                                float *Ta, float *Tb, hipStream_t s);
+                                float *Ta, float *Tb, hipStream_t s, int mode = 0);
 // fp32 on-site grid stage on MFMA (fourier_mfma.hip), default grid only: the same
 // contract as launch_onsite_grid. Used from kOnsiteMfmaMinL up; below it the
 // register-resident folded kernel is faster.
@@ -232,17 +241,22 @@ hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
 // fp32 receiver pass with the edge synthesis on MFMA (receiver_mfma.hip): writes the
 // summed grid fields to S [N][R][2][UVs] and then runs the inverse transforms into
 // Ta, Tb. Requires R % 16 == 0.
-constexpr int kMfmaRecvMinL = 7;  // below this the per-thread SIMT receiver is used
+constexpr int kMfmaRecvMinL = 7;  // three-plane form: below this the per-thread SIMT receiver
 bool receiver_mfma_supported(const Dims &d, int R);
-size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R);
+// S [N][R][planes][UVs]: 2 planes, or with values_only 3 (6 with SFf).
+size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R, int planes);
+// values_only (not with Rtg; default grid): the moved-derivative curl, reading only the value
+// plane of SF (and SFf); every lmax. Otherwise lmax >= kMfmaRecvMinL.
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
                                 const float *Rtg, const float *SF, const float *SFf,
-                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s);
+                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s,
+                                bool values_only = false);
 
 // Read-pattern ceiling of the per-thread receiver (kernels.hip): the sender-field loads of
-// k_receiver_zonal (fp32, one grid point per thread, blocks of 8 ranks) over SF
-// [N][R][3][UVs], in its block order, and no arithmetic. hipErrorNotSupported for grids of
+// k_receiver_zonal in its value-only form (fp32, one grid point per thread, blocks of 16
+// ranks when they divide R, else 8; plane 0 of SF [N][R][3][UVs]), in its block order, and no
+// arithmetic. hipErrorNotSupported for grids of
 // more than 1024 points.
 hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
                                const int32_t *col, const float *SF, float *sink, hipStream_t s);

@@ -149,6 +149,53 @@ __device__ void analysis2(const Tabs<T> &tb, const T *q, const T *S1, const T *S
     }
 }
 
+// Quadrature analysis of the curl product in the moved-derivative form, plus a value field:
+// Sv, S1, S2 [UV] on chip (Sv may be null, and S1, S2 both null), through Tm scratch
+// [3][M][U]; writes
+//   out[l, m] = sum_u wq_u [ Pt_l^|m|(x_u) (Fv[m][u] - m F1[-m][u]) - dPt_l^|m|/dx(x_u) F2[m][u] ]
+// with F_f[m][u] = sum_v q_vm S_f[u][v]. The first term is the analysis of Sv (Eqs.
+// struct-Tmu, struct-Tlm). The others are the analysis of the surface curl of Eq.
+// poisson-S2-x after moving both derivatives onto the test function: on the sphere, with
+// {f, g} = f_phi g_x - f_x g_phi, the integral of Y {A, B} equals that of B {Y, A}, and the
+// grid integrates both exactly, so with S1 = sum_j B_j dA_j/dx and S2 = sum_j B_j dA_j/dphi
+// the curl's coefficient is the analysis of S1 against dY/dphi minus that of S2 against dY/dx.
+// dY_lm/dphi = Pt_l^|m| times the order-swapped Fourier factor -m q_{-m}.
+template <typename T>
+__device__ void analysis_moved(const Tabs<T> &tb, const T *q, const T *Sv, const T *S1,
+                               const T *S2, T *Tm, T *out)
+{
+    const Dims &d = tb.d;
+    const int MU = d.M * d.U;
+    const bool hv = Sv != nullptr, hc = S1 != nullptr;
+    const int f0 = hv ? 0 : 1, f1 = hc ? 3 : 1;  // the fields present: f0 <= f < f1
+    for (int idx = threadIdx.x; idx < (f1 - f0) * MU; idx += blockDim.x) {
+        const int f = f0 + idx / MU, rem = idx - (f - f0) * MU;
+        const int mi = rem / d.U, u = rem - mi * d.U;
+        const T *S = (f == 0 ? Sv : f == 1 ? S1 : S2) + u * d.V;
+        T s = 0;
+        for (int v = 0; v < d.V; ++v) s += q[v * d.M + mi] * S[v];
+        Tm[f * MU + rem] = s;
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < d.K; k += blockDim.x) {
+        const int l = degree_of(k), m = k - l * l - l, am = m < 0 ? -m : m;
+        const T *tv = Tm + (m + d.lmax) * d.U;
+        const T *t1 = Tm + MU + (d.lmax - m) * d.U;
+        const T *t2 = Tm + 2 * MU + (m + d.lmax) * d.U;
+        const int pi = l * (l + 1) / 2 + am;
+        const T fm = (T)m;
+        T s = 0;
+        for (int u = 0; u < d.U; ++u) {
+            const T p = tb.p[(size_t)u * d.P + pi];
+            T t = 0;
+            if (hv) t += p * tv[u];
+            if (hc) t += -fm * p * t1[u] - tb.dp[(size_t)u * d.P + pi] * t2[u];
+            s += tb.wq[u] * t;
+        }
+        out[k] = s;
+    }
+}
+
 // Copy the [V][M] Fourier table into LDS (callers synchronise afterwards).
 template <typename T>
 __device__ __forceinline__ void stage_q(const Tabs<T> &tb, T *qs)
@@ -371,7 +418,10 @@ __device__ __forceinline__ void load_unit(const T *unit, int64_t e, T &ux, T &uy
     ux = unit[3 * e];
     uy = unit[3 * e + 1];
     uz = unit[3 * e + 2];
-    T inv = (T)1 / sqrt(ux * ux + uy * uy + uz * uz);
+    // renormalised: fp32 by the hardware reciprocal square root (within 1 ulp), fp64 exactly
+    T inv;
+    if constexpr (sizeof(T) == 4) inv = __builtin_amdgcn_rsqf(ux * ux + uy * uy + uz * uz);
+    else inv = (T)1 / sqrt(ux * ux + uy * uy + uz * uz);
     ux *= inv;
     uy *= inv;
     uz *= inv;
@@ -414,11 +464,16 @@ __device__ __forceinline__ double buf_load<double>(__amdgpu_buffer_rsrc_t rs, un
 // Table 1 its Gaunt product then feeds Tb and its curl product Ta.
 // SPLIT: the curl product takes the edge coefficients Rtg (its own CP factors) for the
 // derivative sum g, the Gaunt product Rt for the value sum a.
-template <typename T, int RB, int NPT, bool FULL, bool TWO, bool SPLIT>
+// VAL (not with SPLIT): the curl product in the moved-derivative form of analysis_moved. The
+// senders then only need their value plane (plane 0 of each rank's three): per point and
+// rank the block accumulates the Gaunt sum a B and the two sums B dA/dx, B dA/dphi of the
+// edge field's derivatives, and reads a third of the sender bytes.
+template <typename T, int RB, int NPT, bool FULL, bool TWO, bool SPLIT, bool VAL>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
     const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ Rtg,
-    const T *__restrict__ SF, const T *__restrict__ SFf, T *__restrict__ Ta, T *__restrict__ Tb)
+    const T *__restrict__ SF, const T *__restrict__ SFf, T *__restrict__ Ta, T *__restrict__ Tb,
+    T *__restrict__ Sg)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
@@ -449,11 +504,14 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
         pcp[s] = tb.cphi[v];
         psp[s] = tb.sphi[v];
     }
-    T sa[NPT][RB], sb[NPT][RB];
+    static_assert(!(VAL && SPLIT), "the moved-derivative form takes one set of edge coefficients");
+    // VAL: sa, sb the Gaunt sums into Ta, Tb; (ca1, ca2) the moved curl sums into Ta (the
+    // flipped slot's, TWO), (cb1, cb2) into Tb (the natural slot's)
+    T sa[NPT][RB], sb[NPT][RB], ca1[NPT][RB], ca2[NPT][RB], cb1[NPT][RB], cb2[NPT][RB];
 #pragma unroll
     for (int s = 0; s < NPT; ++s)
 #pragma unroll
-        for (int q = 0; q < RB; ++q) sa[s][q] = sb[s][q] = 0;
+        for (int q = 0; q < RB; ++q) sa[s][q] = sb[s][q] = ca1[s][q] = ca2[s][q] = cb1[s][q] = cb2[s][q] = 0;
 
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     // the next edge's sender index and direction are fetched one iteration ahead
@@ -515,12 +573,16 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
                 for (int q = 0; q < RB; ++q) {
                     // ranks past nr fall outside the descriptor's range and read 0
                     fI[q] = buf_load<T>(sfr, voff, (3 * q) * fstride);
-                    fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
-                    fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
+                    if (!VAL) {
+                        fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
+                        fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
+                    }
                     if (TWO) {
                         gI[q] = buf_load<T>(sff, voff, (3 * q) * fstride);
-                        gX[q] = buf_load<T>(sff, voff, (3 * q + 1) * fstride);
-                        gP[q] = buf_load<T>(sff, voff, (3 * q + 2) * fstride);
+                        if (!VAL) {
+                            gX[q] = buf_load<T>(sff, voff, (3 * q + 1) * fstride);
+                            gP[q] = buf_load<T>(sff, voff, (3 * q + 2) * fstride);
+                        }
                     }
                 }
         const T h = ux * pcp[s] + uy * psp[s];
@@ -558,23 +620,91 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
                 const T dpt = psx[s] * (uy * pcp[s] - ux * psp[s]);
 #pragma unroll
                 for (int q = 0; q < RB; ++q) {
-                    sa[s][q] += a[q] * fI[q];
-                    sb[s][q] += g[q] * (dpt * fX[q] - dxt * fP[q]);
-                    if (TWO) {
-                        sa[s][q] += g[q] * (dpt * gX[q] - dxt * gP[q]);
-                        sb[s][q] += a[q] * gI[q];
+                    if (VAL) {
+                        // dA/dx = g dxt and dA/dphi = g dpt of the edge field
+                        sa[s][q] += a[q] * fI[q];
+                        const T gf = g[q] * fI[q];
+                        cb1[s][q] += dxt * gf;
+                        cb2[s][q] += dpt * gf;
+                        if (TWO) {
+                            sb[s][q] += a[q] * gI[q];
+                            const T gg = g[q] * gI[q];
+                            ca1[s][q] += dxt * gg;
+                            ca2[s][q] += dpt * gg;
+                        }
+                    } else {
+                        sa[s][q] += a[q] * fI[q];
+                        sb[s][q] += g[q] * (dpt * fX[q] - dxt * fP[q]);
+                        if (TWO) {
+                            sa[s][q] += g[q] * (dpt * gX[q] - dxt * gP[q]);
+                            sb[s][q] += a[q] * gI[q];
+                        }
                     }
                 }
             }
         }
     }
     if (STAGE) __syncthreads();  // the staged coefficients are consumed before the analysis
+    if (VAL && Sg) {
+        // the sums go to Sg [N][R][NF][UVs] for the MFMA analysis: (Gaunt sum into Ta, moved
+        // curl pair into Tb), or with two slots (value sum, moved pair) for Ta, then for Tb
+        constexpr int NF = TWO ? 6 : 3;
+        const int UVs = d.UVs;
+#pragma unroll
+        for (int q = 0; q < RB; ++q) {
+            if (!FULL && q >= nr) break;
+            T *o = Sg + (i * R + r0 + q) * NF * (int64_t)UVs;
+#pragma unroll
+            for (int s = 0; s < NPT; ++s) {
+                const int uv = uvs[s];
+                if (uv >= UV) continue;
+                o[uv] = sa[s][q];
+                if (TWO) {
+                    o[UVs + uv] = ca1[s][q];
+                    o[2 * UVs + uv] = ca2[s][q];
+                    o[3 * UVs + uv] = sb[s][q];
+                    o[4 * UVs + uv] = cb1[s][q];
+                    o[5 * UVs + uv] = cb2[s][q];
+                } else {
+                    o[UVs + uv] = cb1[s][q];
+                    o[2 * UVs + uv] = cb2[s][q];
+                }
+            }
+        }
+        return;
+    }
     // inverse transforms, one rank at a time through LDS
     T *qs = smem;
     T *Sa = qs + d.V * d.M;
     T *Sb = Sa + UV;
     T *Tm = Sb + UV;
     stage_q(tb, qs);
+    if (VAL) {
+        // one output at a time: its value sum (if any) and moved curl pair (if any)
+        T *S1 = Sb + UV, *Tm3 = S1 + UV;
+#pragma unroll
+        for (int q = 0; q < RB; ++q) {
+            if (q >= nr) break;
+            const int64_t br = i * R + r0 + q;
+#pragma unroll
+            for (int o = 0; o < 2; ++o) {
+                const bool hv = o == 0 || TWO, hc = o == 1 || TWO;
+#pragma unroll
+                for (int s = 0; s < NPT; ++s) {
+                    if (uvs[s] < UV) {
+                        Sa[uvs[s]] = o ? sb[s][q] : sa[s][q];
+                        S1[uvs[s]] = o ? cb1[s][q] : ca1[s][q];
+                        Sb[uvs[s]] = o ? cb2[s][q] : ca2[s][q];
+                    }
+                }
+                __syncthreads();
+                analysis_moved(tb, qs, hv ? Sa : (const T *)nullptr, hc ? S1 : (const T *)nullptr,
+                               hc ? Sb : (const T *)nullptr, Tm3, (o ? Tb : Ta) + br * d.K);
+                __syncthreads();
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int q = 0; q < RB; ++q) {
         if (q >= nr) break;
@@ -592,9 +722,10 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     }
 }
 
-// Read-pattern ceiling of k_receiver_zonal: the same blocks in the same order, the same
-// wave-uniform sender index per edge and the same raw buffer loads of the 3 RB sender
-// values of every grid point, with nothing computed from them but a running sum. sink
+// Read-pattern ceiling of k_receiver_zonal in its value-only form (the moved-derivative curl):
+// the same blocks in the same order, the same wave-uniform sender index per edge and the
+// same raw buffer loads of the RB sender values of every grid point, with nothing computed
+// from them but a running sum. sink
 // receives a value only if that sum equals a constant no finite input sums to by chance,
 // which keeps every load live.
 template <int RB>
@@ -619,11 +750,7 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_gather_probe(
                                                      (unsigned)(nr * 3 * UVs * sizeof(float)));
         if (uv < UV) {
 #pragma unroll
-            for (int q = 0; q < RB; ++q) {
-                acc += buf_load<float>(sfr, voff, (3 * q) * fstride);
-                acc += buf_load<float>(sfr, voff, (3 * q + 1) * fstride);
-                acc += buf_load<float>(sfr, voff, (3 * q + 2) * fstride);
-            }
+            for (int q = 0; q < RB; ++q) acc += buf_load<float>(sfr, voff, (3 * q) * fstride);
         }
     }
     if (acc == -1.2345678e30f) sink[0] = acc;
@@ -632,13 +759,19 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_gather_probe(
 hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
                                const int32_t *col, const float *SF, float *sink, hipStream_t s)
 {
-    constexpr int RB = 8;  // the rank block of the fp32 per-thread receiver at one point per thread
+    // the rank block of the fp32 value-only receiver at one point per thread: 16 ranks when
+    // they divide R, else 8
     if (d.UV > kRecvMaxThreads) return hipErrorNotSupported;
     const int threads = (d.UV + 63) / 64 * 64;
-    const int64_t nb = N * ((R + RB - 1) / RB);
+    const int rb = R % 16 == 0 ? 16 : 8;
+    const int64_t nb = N * ((R + rb - 1) / rb);
     if (nb == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_gather_probe<RB>, dim3((unsigned)nb), dim3(threads), 0, s, d.UV, d.UVs,
-                       R, row_ptr, col, SF, sink);
+    if (rb == 16)
+        hipLaunchKernelGGL(k_gather_probe<16>, dim3((unsigned)nb), dim3(threads), 0, s, d.UV,
+                           d.UVs, R, row_ptr, col, SF, sink);
+    else
+        hipLaunchKernelGGL(k_gather_probe<8>, dim3((unsigned)nb), dim3(threads), 0, s, d.UV,
+                           d.UVs, R, row_ptr, col, SF, sink);
     return hipGetLastError();
 }
 
@@ -960,12 +1093,14 @@ template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
                            const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
-                           hipStream_t s)
+                           hipStream_t s, bool values_only, T *Sg)
 {
     int64_t blocks = N * R;
     if (blocks == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (SFf && Rtg) return hipErrorNotSupported;
+    if (values_only && (separated || Rtg)) return hipErrorInvalidValue;
+    if (Sg && (!values_only || sizeof(T) != 4)) return hipErrorInvalidValue;
     if (separated) {
         if (SFf || Rtg) return hipErrorNotSupported;
         size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + d.K + 2 * d.M * d.U);
@@ -973,29 +1108,37 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb);
         return hipGetLastError();
     }
-    size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + 2 * d.M * d.U);
+    // the analysis buffers: two grid fields and two Fourier row sets, three of each with
+    // values_only
+    // (none when the analysis follows on MFMA)
+    const int nf = values_only ? 3 : 2;
+    size_t sh = Sg ? 0 : sizeof(T) * (d.V * d.M + nf * d.UV + nf * d.M * d.U);
     const int npt = (d.UV + kRecvMaxThreads - 1) / kRecvMaxThreads;
     const int threads = ((d.UV + npt - 1) / npt + 63) / 64 * 64;
     // LDS: the analysis buffers, or (split) one chunk of staged edge coefficients if larger
-#define CGTP_RECV_TW(RBV, NP, TW, SP)                                                          \
+#define CGTP_RECV_TW(RBV, NP, TW, SP, VL)                                                      \
     do {                                                                                       \
         int64_t nb = N * ((R + RBV - 1) / RBV);                                                \
         const size_t chunk = SP ? sizeof(T) * kRecvEdgeChunk * 2 * d.L * RBV : 0;              \
         const size_t shc = chunk > sh ? chunk : sh;                                            \
+        if (shc > (size_t)d.lds_max) return hipErrorNotSupported;                              \
         if (R % RBV == 0)                                                                      \
-            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true, TW, SP>),                   \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true, TW, SP, VL>),               \
                                dim3((unsigned)nb), dim3(threads), shc, s, tb, R, row_ptr, col, \
-                               unit, Rt, Rtg, SF, SFf, Ta, Tb);                                \
+                               unit, Rt, Rtg, SF, SFf, Ta, Tb, Sg);                            \
         else                                                                                   \
-            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false, TW, SP>),                  \
+            hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false, TW, SP, VL>),              \
                                dim3((unsigned)nb), dim3(threads), shc, s, tb, R, row_ptr, col, \
-                               unit, Rt, Rtg, SF, SFf, Ta, Tb);                                \
+                               unit, Rt, Rtg, SF, SFf, Ta, Tb, Sg);                            \
     } while (0)
-#define CGTP_RECV(RBV, NP)                              \
-    do {                                                \
-        if (SFf) CGTP_RECV_TW(RBV, NP, true, false);    \
-        else if (Rtg) CGTP_RECV_TW(RBV, NP, false, true); \
-        else CGTP_RECV_TW(RBV, NP, false, false);       \
+#define CGTP_RECV(RBV, NP)                                                  \
+    do {                                                                    \
+        if (values_only) {                                                  \
+            if (SFf) CGTP_RECV_TW(RBV, NP, true, false, true);              \
+            else CGTP_RECV_TW(RBV, NP, false, false, true);                 \
+        } else if (SFf) CGTP_RECV_TW(RBV, NP, true, false, false);          \
+        else if (Rtg) CGTP_RECV_TW(RBV, NP, false, true, false);            \
+        else CGTP_RECV_TW(RBV, NP, false, false, false);                    \
     } while (0)
     // ranks per block: sized so the per-thread accumulators and in-flight loads fit in
     // registers without spilling (fp64 values take two registers)
@@ -1006,7 +1149,11 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     else CGTP_RECV(2, 3);
 #undef CGTP_RECV
 #undef CGTP_RECV_TW
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !Sg) return e;
+    if constexpr (sizeof(T) == 4)
+        return launch_analysis_mfma(tb, N, R, Sg, Ta, Tb, s, SFf ? 2 : 1);
+    return hipErrorInvalidValue;
 }
 
 #define CGTP_INSTANTIATE(T)                                                                      \
@@ -1016,7 +1163,8 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                                               const T *, T *, T *, hipStream_t);                 \
     template hipError_t launch_receiver<T>(const Tabs<T> &, bool, int64_t, int, const int32_t *, \
                                            const int32_t *, const T *, const T *, const T *,     \
-                                           const T *, const T *, T *, T *, hipStream_t);         \
+                                           const T *, const T *, T *, T *, hipStream_t, bool,    \
+                                           T *);                                                 \
     template hipError_t launch_receiver_fields<T>(const Tabs<T> &, int64_t, int, const int32_t *, \
                                                   const int32_t *, const T *, const T *, T *, T *, \
                                                   hipStream_t);                                   \

@@ -74,19 +74,41 @@ struct Layout {
     size_t wc = 0;           // concatenated factor blocks of a run of rank groups [L][C][R]
 };
 
-// Receiver on MFMA: fp32, zonal edge field, R a multiple of 16, lmax high enough that the
-// per-thread recurrence sums would make the SIMT receiver compute-bound.
-bool use_mfma_receiver(const cgtp_plan_s *p, int R)
+// Receiver on MFMA in its values-only form (the moved-derivative curl: only the senders'
+// value plane is read): fp32, zonal edge field, shared factors (split: no), R a multiple of
+// 16, the default grid (for the MFMA analysis of its moved planes); every lmax.
+bool mfma_values_only(const cgtp_plan_s *p, int R, bool split)
 {
-    return p->dtype == CGTP_F32 && !(p->flags & CGTP_EDGE_SEPARATED) &&
-           p->d.lmax >= cgtp::kMfmaRecvMinL && cgtp::receiver_mfma_supported(p->d, R);
+    return p->dtype == CGTP_F32 && !split && !(p->flags & CGTP_EDGE_SEPARATED) &&
+           cgtp::receiver_mfma_supported(p->d, R) && cgtp::sender_mfma_supported(p->d);
+}
+
+// Receiver on MFMA: the values-only form above, else (three sender planes) fp32, zonal edge
+// field, R a multiple of 16, lmax high enough that the per-thread recurrence sums would make
+// the SIMT receiver compute-bound.
+bool use_mfma_receiver(const cgtp_plan_s *p, int R, bool split = false)
+{
+    return mfma_values_only(p, R, split) ||
+           (p->dtype == CGTP_F32 && !(p->flags & CGTP_EDGE_SEPARATED) &&
+            p->d.lmax >= cgtp::kMfmaRecvMinL && cgtp::receiver_mfma_supported(p->d, R));
+}
+
+// Whether the receiver takes the curl in the moved-derivative form (senders then write only
+// their value plane): shared factors and the zonal edge field, on the per-thread receiver or
+// on the MFMA one in its values-only form.
+bool values_only_form(const cgtp_plan_s *p, int R, bool split)
+{
+    if (split || (p->flags & CGTP_EDGE_SEPARATED)) return false;
+    return !use_mfma_receiver(p, R, split) || mfma_values_only(p, R, split);
 }
 
 // The MFMA receiver reads the sender fields in 64-point chunks when the MFMA sender writes
-// them (fp32, default grid).
-bool sf_chunked(const cgtp_plan_s *p, int R)
+// them (fp32, default grid, from kMfmaRecvMinL on; below it the dense sender writes the plain
+// layout).
+bool sf_chunked(const cgtp_plan_s *p, int R, bool split = false)
 {
-    return use_mfma_receiver(p, R) && cgtp::sender_mfma_supported(p->d);
+    return use_mfma_receiver(p, R, split) && p->d.lmax >= cgtp::kMfmaRecvMinL &&
+           cgtp::sender_mfma_supported(p->d);
 }
 
 // On-site workspace: HA, HB, Ta, Tb, each [N][R][K] (R: the plan's rank, or the total
@@ -112,8 +134,17 @@ bool onsite_split_ok(const cgtp_plan_s *p)
     return p->dtype == CGTP_F32 && cgtp::onsite_split_supported(p->d);
 }
 
+// The zonal receiver (values-only form: shared factors, fp32, default grid) hands its summed
+// fields to the MFMA analysis through S [N][R][3][UVs] ([6] with two node slots).
+bool zonal_mfma_analysis(const cgtp_plan_s *p, int R, bool split)
+{
+    return p->dtype == CGTP_F32 && !split && !(p->flags & CGTP_EDGE_SEPARATED) &&
+           !use_mfma_receiver(p, R, split) && cgtp::sender_mfma_supported(p->d);
+}
+
 // Message-passing workspace: HI [N][R][K], SF [N][R][3][UVs], Rt [E][L][R], Ta, Tb [N][R][K],
-// and, for the MFMA receiver, the summed grid fields S [N][R][2][UVs]. With two node slots,
+// and the summed grid fields S: [N][R][2][UVs] for the MFMA receiver, [N][R][3 or 6][UVs] for
+// the zonal one handing over to the MFMA analysis. With two node slots,
 // HI and SF hold the natural slot followed by the flipped one. With split factors (general
 // path), HI and Rt hold the Gaunt factors' contraction followed by the curl factors'. Last,
 // room for one sector's output weights concatenated over the groups (the general path's
@@ -124,10 +155,15 @@ Layout mp_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool two = f
     size_t es = p->dtype == CGTP_F64 ? 8 : 4;
     const size_t nh = (two || split) ? 2 : 1, nsf = two ? 2 : 1, nrt = split ? 2 : 1;
     size_t h = align256(es * (size_t)N * R * p->d.K);
-    const size_t sf_pts = sf_chunked(p, R) ? (size_t)cgtp::sf_chunks(p->d) * cgtp::kSfChunk : p->d.UVs;
+    const size_t sf_pts = sf_chunked(p, R, split) ? (size_t)cgtp::sf_chunks(p->d) * cgtp::kSfChunk : p->d.UVs;
     size_t sf = align256(es * (size_t)N * R * 3 * sf_pts);
     size_t rt = align256(es * (size_t)E * R * p->d.L);
-    size_t sg = use_mfma_receiver(p, R) ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, R)) : 0;
+    const int sg_planes = values_only_form(p, R, split) ? (two ? 6 : 3) : 2;
+    size_t sg = use_mfma_receiver(p, R, split)
+                    ? align256(es * cgtp::receiver_mfma_ws_elems(p->d, N, R, sg_planes))
+                : zonal_mfma_analysis(p, R, split)
+                    ? align256(es * (size_t)N * R * sg_planes * p->d.UVs)
+                    : 0;
     Layout l{};
     l.off[0] = 0;
     l.off[1] = nh * h;
@@ -400,6 +436,9 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
     T *HIf = two ? reinterpret_cast<T *>(ws + lay.off[0] + lay.hf) : nullptr;
     T *SFf = two ? reinterpret_cast<T *>(ws + lay.off[1] + lay.sff) : nullptr;
     const int64_t hs = (int64_t)R * d.K;
+    // the zonal receiver takes the curl in the moved-derivative form: the senders' value plane
+    // is all it reads
+    const bool values_only = values_only_form(p, R, false);
     StageRec rec;
     int st = rec.begin(p, op, 6, s);
     if (st) return st;
@@ -413,13 +452,14 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
     rec.mark();
     for (int slot = 0; slot < (two ? 2 : 1); ++slot) {
         T *h = slot ? HIf : HI, *sf = slot ? SFf : SF;
+        const int planes = values_only ? 1 : 7;
         if constexpr (sizeof(T) == 4) {
             if (sf_chunked(p, R))
                 e = cgtp::launch_sender_mfma(tb, N, R, h, sf, true, s);
             else
-                e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s);
+                e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s, planes);
         } else {
-            e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s);
+            e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s, planes);
         }
         if (e != hipSuccess) return hip_fail(e, "sender fields");
     }
@@ -435,14 +475,20 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
         if (use_mfma_receiver(p, R)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
             e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt,
-                                           nullptr, SF, SFf, sf_chunked(p, R), Sg, Ta, Tb, s);
+                                           nullptr, SF, SFf, sf_chunked(p, R), Sg, Ta, Tb, s,
+                                           values_only);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
             goto projections;
         }
     }
-    e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt, nullptr,
-                                 SF, SFf, Ta, Tb, s);
+    {
+        T *Sz = values_only && zonal_mfma_analysis(p, R, false)
+                    ? reinterpret_cast<T *>(ws + lay.off[5])
+                    : nullptr;
+        e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt,
+                                     nullptr, SF, SFf, Ta, Tb, s, values_only, Sz);
+    }
     if (e != hipSuccess) return hip_fail(e, "receiver");
     rec.mark();
 projections:
@@ -719,11 +765,13 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     rec.mark();
     // split: the Gaunt factors' contraction gives the sender values, the curl factors' the
     // two derivative fields, into the same field slots
+    // the zonal receiver with shared factors takes the moved-derivative curl (value planes)
+    const bool values_only = values_only_form(p, Rg, G.split);
     for (int pass = 0; pass < (G.split ? 2 : 1); ++pass) {
         const T *h = pass ? HIc : HI;
-        const int planes = G.split ? (pass ? 6 : 1) : 7;
+        const int planes = G.split ? (pass ? 6 : 1) : (values_only ? 1 : 7);
         if constexpr (sizeof(T) == 4) {
-            if (sf_chunked(p, Rg))
+            if (sf_chunked(p, Rg, G.split))
                 e = cgtp::launch_sender_mfma(tb, N, Rg, h, SF, true, s, planes);
             else
                 e = cgtp::launch_sender_fields<T>(tb, N, Rg, h, SF, s, planes);
@@ -746,17 +794,21 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     }
     rec.mark();
     if constexpr (sizeof(T) == 4) {
-        if (use_mfma_receiver(p, Rg)) {
+        if (use_mfma_receiver(p, Rg, G.split)) {
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
             e = cgtp::launch_receiver_mfma(tb, N, Rg, row_ptr, col, (const float *)unit, Rt, Rtc,
-                                           SF, nullptr, sf_chunked(p, Rg), Sg, Ta, Tb, s);
+                                           SF, nullptr, sf_chunked(p, Rg, G.split), Sg, Ta, Tb, s,
+                                           values_only);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             rec.mark();
             return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
         }
     }
+    T *Sz = values_only && zonal_mfma_analysis(p, Rg, G.split)
+                ? reinterpret_cast<T *>(ws + lay.off[5])
+                : nullptr;
     e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, Rtc, SF,
-                                 nullptr, Ta, Tb, s);
+                                 nullptr, Ta, Tb, s, values_only, Sz);
     if (e != hipSuccess) return hip_fail(e, "receiver");
     rec.mark();
     return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);

@@ -13,6 +13,11 @@
 // registers. The summed grid fields go to S [N][R][2][UVs]; the folded analysis
 // (k_analysis_rows when it does not fit)
 // then runs the inverse transforms (Eqs. msgpass-Tmu, msgpass-Tlm).
+// With VAL the surface curl takes the moved-derivative form (integration by parts on the
+// sphere: the curl's coefficient is the analysis of S1 = sum_j B_j dA_j/dx against dY/dphi
+// minus that of S2 = sum_j B_j dA_j/dphi against dY/dx): a lane reads only the value plane of
+// its sender fields and accumulates the Gaunt sum a B and the pair (S1, S2); S is then
+// [N][R][3][UVs] (six planes with two node slots) for the MFMA analysis in its moved modes.
 #include "internal.h"
 
 namespace cgtp {
@@ -54,7 +59,8 @@ __device__ __forceinline__ void wave_sync()
 // product S_beta's. The next edge is prefetched only with one slot (registers).
 // SPLIT: the curl product's edge coefficients are Rtg (its own CP factors): the derivative
 // sum g multiplies P' with those, the value sum a P with Rt.
-template <int WPB, int LM, bool TWO, bool SPLIT>
+// VAL (not with SPLIT): value planes only, moved-derivative curl (above).
+template <int WPB, int LM, bool TWO, bool SPLIT, bool VAL>
 __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
                                                             const int32_t *__restrict__ row_ptr,
                                                             const int32_t *__restrict__ col,
@@ -107,11 +113,15 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
 
     // D[row = point 4 g + j][col = rank n]: a lane holds 4 consecutive points of one
     // rank, so its sender values are 16-byte loads and its S values 16-byte stores.
-    float4_t sa[TPW], sb[TPW];
+    // VAL: sa, sb the Gaunt sums into S_alpha, S_beta; (ca1, ca2) the moved curl pair into
+    // S_alpha (the flipped slot's, TWO), (cb1, cb2) into S_beta (the natural slot's)
+    static_assert(!(VAL && SPLIT), "the moved-derivative form takes one set of edge coefficients");
+    float4_t sa[TPW], sb[TPW], ca1[TPW], ca2[TPW], cb1[TPW], cb2[TPW];
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
         sa[t] = float4_t{0.f, 0.f, 0.f, 0.f};
         sb[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+        ca1[t] = ca2[t] = cb1[t] = cb2[t] = float4_t{0.f, 0.f, 0.f, 0.f};
     }
     // lane's points: pw0 + 16 t + 4 g + (0..3); lane's rank: r0 + n. The sender fields are
     // either SF [N][R][3][UVs] (a sender's 16-rank block is [16][3][UVs]) or, with sf_nc
@@ -144,8 +154,10 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
         for (int t = 0; t < TPW; ++t) {
             const unsigned so = (unsigned)(t * 16 * 4);
             fI[t] = bload4(sfr, vofft[t], so);
-            fX[t] = bload4(sfr, vofft[t], so + fstride * 4);
-            fP[t] = bload4(sfr, vofft[t], so + 2 * fstride * 4);
+            if (!VAL) {
+                fX[t] = bload4(sfr, vofft[t], so + fstride * 4);
+                fP[t] = bload4(sfr, vofft[t], so + 2 * fstride * 4);
+            }
         }
     };
     if (!TWO && e0 < e1) load_fields(sfb, e0, cI, cX, cP);
@@ -158,8 +170,10 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
 #pragma unroll
             for (int t = 0; t < TPW; ++t) {
                 fI[t] = cI[t];
-                fX[t] = cX[t];
-                fP[t] = cP[t];
+                if (!VAL) {
+                    fX[t] = cX[t];
+                    fP[t] = cP[t];
+                }
             }
             if (e + 1 < e1) load_fields(sfb, e + 1, cI, cX, cP);
         }
@@ -221,29 +235,61 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
             for (int jj = 0; jj < 4; ++jj) {
                 const int pl = 16 * t + 4 * g + jj;
                 const float dxt = dxs[pl], dpt = dps[pl];
-                sa[t][jj] += a[jj] * fI[t][jj];
-                sb[t][jj] += gg[jj] * (dpt * fX[t][jj] - dxt * fP[t][jj]);
-                if (TWO) {
-                    sa[t][jj] += gg[jj] * (dpt * hX[t][jj] - dxt * hP[t][jj]);
-                    sb[t][jj] += a[jj] * hI[t][jj];
+                if (VAL) {
+                    // dA/dx = g dxt and dA/dphi = g dpt of the edge field
+                    sa[t][jj] += a[jj] * fI[t][jj];
+                    const float gf = gg[jj] * fI[t][jj];
+                    cb1[t][jj] += dxt * gf;
+                    cb2[t][jj] += dpt * gf;
+                    if (TWO) {
+                        sb[t][jj] += a[jj] * hI[t][jj];
+                        const float gh = gg[jj] * hI[t][jj];
+                        ca1[t][jj] += dxt * gh;
+                        ca2[t][jj] += dpt * gh;
+                    }
+                } else {
+                    sa[t][jj] += a[jj] * fI[t][jj];
+                    sb[t][jj] += gg[jj] * (dpt * fX[t][jj] - dxt * fP[t][jj]);
+                    if (TWO) {
+                        sa[t][jj] += gg[jj] * (dpt * hX[t][jj] - dxt * hP[t][jj]);
+                        sb[t][jj] += a[jj] * hI[t][jj];
+                    }
                 }
             }
         }
     }
-    // S[i][r0 + n][0 / 1][p .. p + 3]
+    // S[i][r0 + n][plane][p .. p + 3]: planes (S_alpha, S_beta), or with VAL the Gaunt sum and
+    // moved pair (sa, cb1, cb2), with two slots (sa, ca1, ca2, sb, cb1, cb2)
+    constexpr int NF = VAL ? (TWO ? 6 : 3) : 2;
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
         const int p = pw0 + 16 * t + 4 * g;
-        float *o = S + ((i * R + r0 + n) * 2) * (int64_t)UVs + p;
+        float *o = S + ((i * R + r0 + n) * NF) * (int64_t)UVs + p;
+        float4_t pl[NF];
+        if (!VAL) {
+            pl[0] = sa[t];
+            pl[1] = sb[t];
+        } else if (!TWO) {
+            pl[0] = sa[t];
+            pl[1] = cb1[t];
+            pl[2] = cb2[t];
+        } else {
+            pl[0] = sa[t];
+            pl[1] = ca1[t];
+            pl[2] = ca2[t];
+            pl[3] = sb[t];
+            pl[4] = cb1[t];
+            pl[5] = cb2[t];
+        }
         if (p + 3 < UV) {
-            *reinterpret_cast<float4_t *>(o) = sa[t];
-            *reinterpret_cast<float4_t *>(o + UVs) = sb[t];
+#pragma unroll
+            for (int f = 0; f < NF; ++f) *reinterpret_cast<float4_t *>(o + f * UVs) = pl[f];
         } else {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj)
                 if (p + jj < UV) {
-                    o[jj] = sa[t][jj];
-                    o[UVs + jj] = sb[t][jj];
+#pragma unroll
+                    for (int f = 0; f < NF; ++f) o[f * UVs + jj] = pl[f][jj];
                 }
         }
     }
@@ -310,20 +356,22 @@ bool receiver_mfma_supported(const Dims &d, int R)
     return R % kRT == 0 && d.L <= 32;
 }
 
-size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R)
+size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R, int planes)
 {
-    return (size_t)N * R * 2 * d.UVs;
+    return (size_t)N * R * planes * d.UVs;
 }
 
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
                                 const int32_t *col, const float *unit, const float *Rt,
                                 const float *Rtg, const float *SF, const float *SFf,
-                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s)
+                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s,
+                                bool values_only)
 {
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
     if (SFf && Rtg) return hipErrorNotSupported;
+    if (values_only && Rtg) return hipErrorInvalidValue;
     constexpr int WPB = 2, PW = 64, PC = WPB * PW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
@@ -332,30 +380,37 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     static_assert(PW == kSfChunk, "a receiver wave reads one chunk of the chunked layout");
     const int sf_nc = sf_chunked ? sf_chunks(d) : 0;
+#define CGTP_LAUNCH(LMV, TW, SP, VL)                                                            \
+    hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, TW, SP, VL>), dim3((unsigned)blocks),         \
+                       dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt, Rtg, SF,  \
+                       SFf, sf_nc, S)
     switch (d.lmax) {
-#define CGTP_CASE(LMV)                                                                          \
-    case LMV:                                                                                   \
-        if (SFf)                                                                                \
-            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, true, false>), dim3((unsigned)blocks), \
-                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt,   \
-                               Rtg, SF, SFf, sf_nc, S);                                         \
-        else if (Rtg)                                                                           \
-            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, false, true>), dim3((unsigned)blocks), \
-                               dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt,   \
-                               Rtg, SF, SFf, sf_nc, S);                                         \
-        else                                                                                    \
-            hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, false, false>),                       \
-                               dim3((unsigned)blocks), dim3(64 * WPB), sh, s, tb, R, nchunks,   \
-                               row_ptr, col, unit, Rt, Rtg, SF, SFf, sf_nc, S);                 \
+#define CGTP_CASE(LMV)                                                 \
+    case LMV:                                                          \
+        if (values_only) {                                             \
+            if (SFf) CGTP_LAUNCH(LMV, true, false, true);              \
+            else CGTP_LAUNCH(LMV, false, false, true);                 \
+        } else if (LMV < kMfmaRecvMinL) {                              \
+            return hipErrorNotSupported;                               \
+        } else if (SFf) {                                              \
+            CGTP_LAUNCH(LMV, true, false, false);                      \
+        } else if (Rtg) {                                              \
+            CGTP_LAUNCH(LMV, false, true, false);                      \
+        } else {                                                       \
+            CGTP_LAUNCH(LMV, false, false, false);                     \
+        }                                                              \
         break;
+        CGTP_CASE(0) CGTP_CASE(1) CGTP_CASE(2) CGTP_CASE(3) CGTP_CASE(4) CGTP_CASE(5) CGTP_CASE(6)
         CGTP_CASE(7) CGTP_CASE(8) CGTP_CASE(9) CGTP_CASE(10) CGTP_CASE(11) CGTP_CASE(12) CGTP_CASE(13) CGTP_CASE(14)
         CGTP_CASE(15) CGTP_CASE(16) CGTP_CASE(17) CGTP_CASE(18) CGTP_CASE(19) CGTP_CASE(20)
         CGTP_CASE(21) CGTP_CASE(22) CGTP_CASE(23) CGTP_CASE(24)
 #undef CGTP_CASE
+#undef CGTP_LAUNCH
     default: return hipErrorNotSupported;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (values_only) return launch_analysis_mfma(tb, N, R, S, Ta, Tb, s, SFf ? 2 : 1);
     e = launch_analysis_mfma(tb, N, R, S, Ta, Tb, s);
     if (e != hipErrorNotSupported) return e;
     e = launch_analysis_folded(tb, N, R, S, Ta, Tb, s);

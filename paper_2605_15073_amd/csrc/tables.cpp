@@ -169,9 +169,10 @@ static void region_sizes(const Dims &d, size_t *n)
     n[18] = d.P;                // yc
     n[19] = d.lmax <= kDenseSynthMaxL ? (size_t)(d.K + 3) / 4 * 4 * 3 * d.UVs : 0;  // ysyn
     n[20] = (size_t)d.V * d.M;  // qd
+    n[21] = (size_t)d.P * ut;   // wdpt
 }
 
-static const int kRegions = 21;
+static const int kRegions = 22;
 
 static size_t round_up(size_t n) { return (n + 63) & ~(size_t)63; }  // 512 B for fp64
 
@@ -221,6 +222,7 @@ void fill_tables(const Dims &d, double *h)
             h[off[15] + (size_t)i * ut + u] = pv;
             h[off[16] + (size_t)i * ut + u] = h[off[5] + (size_t)u * d.P + i];
             h[off[17] + (size_t)i * ut + u] = h[off[3] + u] * pv;
+            h[off[21] + (size_t)i * ut + u] = h[off[3] + u] * h[off[5] + (size_t)u * d.P + i];
         }
     for (int l = 0; l <= d.lmax; ++l)
         for (int m = 0; m <= l; ++m) {
@@ -303,6 +305,7 @@ Tabs<T> bind_tables(const Dims &d, const void *dev)
     tb.yc = ptr[18];
     tb.ysyn = ptr[19];
     tb.qd = ptr[20];
+    tb.wdpt = ptr[21];
     tb.d = d;
     return tb;
 }

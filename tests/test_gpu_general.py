@@ -263,7 +263,8 @@ def test_mp_general_workspace_and_errors(cg):
     plan = cg.plan_create(lmax, 3, 4)
     N, E = d["node_feat"].shape[0], d["n_edges"]
     need = cg.workspace_bytes_general(plan, cg.CGTP_OP_MESSAGE_PASS_GENERAL, N, E, 2, 4, 2)
-    assert need > cg.workspace_bytes(plan, cg.CGTP_OP_MESSAGE_PASS_TWO_SLOT, N, E)
+    # the rank groups (two slot pairs, split factors) need more than the one-slot call
+    assert need > cg.workspace_bytes(plan, cg.CGTP_OP_MESSAGE_PASS, N, E)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     _check(_mp_gpu(cg, plan, t, workspace=ws), _mp_ref(lmax, d), TOL_F32)
     with pytest.raises(cg.CgtpError) as ei:
