@@ -30,7 +30,6 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
-MFMA_RECV_MIN_L = 7            # fp32 message passing: the MFMA receiver from this lmax on
 FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 vector (and matrix) peak
 CSRC = os.path.join(ROOT, "paper_2605_15073_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
@@ -450,9 +449,9 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
                 rt_blocks=1 if w.in_blocks == 1 else len(live),
                 t_fields=len(live) if w.out_blocks == 2 else 2)
         else:
-            # the zonal receiver (lmax < MFMA_RECV_MIN_L) takes the curl in the moved-derivative
-            # form and reads one plane per node slot; the MFMA receiver reads three
-            per_slot = 1 if w.lmax < MFMA_RECV_MIN_L else 3
+            # with shared factors the receivers take the curl in the moved-derivative form and
+            # read one plane (the sender values) per node slot
+            per_slot = 1
             slots = 2 if w.two_slot else 1
             alg = receiver_bytes(w.lmax, w.R, w.n, E, slots, planes=per_slot * slots)
             comp = compulsory_receiver_bytes(w.lmax, w.R, w.n, E, per_slot * slots)
@@ -486,8 +485,8 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
 
 
 def probe_ok(w) -> bool:
-    """The read-pattern probe replays the fp32 per-thread zonal receiver (lmax <= 6, one node
-    slot, shared factors)."""
+    """The read-pattern probe replays the fp32 message-passing receiver in its values-only form
+    on the plain sender layout (lmax <= 6, one node slot, shared factors)."""
     return w.kind == "mp" and not w.general and not w.two_slot and w.lmax <= 6
 
 
@@ -516,7 +515,7 @@ def gather_ceiling(plan, w, t, E, reps: int = 5):
     ms = e0.elapsed_time(e1) / reps
     gathered = 4 * E * w.R * U * V
     del fields
-    return {"pattern": "per-edge sender-field loads of the zonal receiver",
+    return {"pattern": "per-edge sender value-plane loads of the receiver",
             "bytes": gathered, "ms": ms, "GBs": gathered / (ms / 1e3) / 1e9}
 
 

@@ -313,27 +313,29 @@ int cgtp_onsite_nbody(cgtp_plan plan, int64_t n_nodes, int nu, const void *const
  * Stages of CGTP_OP_ONSITE: 0 contract both operands, 1 grid product+curl and
  * analysis, 2 project both output slots. Stages of CGTP_OP_MESSAGE_PASS:
  * 0 contract node features, 1 sender grid fields, 2 contract edge radial,
- * 3 receiver pass (edge synthesis, products, neighbour sum, analysis),
- * 4 project even, 5 project odd. CGTP_OP_MESSAGE_PASS_TWO_SLOT has the same six
+ * 3 receiver pass (edge synthesis, products, neighbour sum), 4 analysis of the summed grid
+ * fields (0 where the receiver runs it itself: fp64, grids off the default one),
+ * 5 project even, 6 project odd. CGTP_OP_MESSAGE_PASS_TWO_SLOT has the same seven
  * stages, each covering both node slots; CGTP_OP_ONSITE_GENERAL: 0 contract first
  * operand, 1 contract second operand, 2 grid product+curl and analysis, 3 project even,
  * 4 project odd; CGTP_OP_MESSAGE_PASS_GENERAL those of CGTP_OP_MESSAGE_PASS; both cover
  * every rank group; CGTP_OP_MESSAGE_PASS_FIELDS: 0 contract node features, 1 sender grid
- * fields, 2 contract edge field, 3 receiver pass, 4 project even, 5 project odd. A
- * skipped stage counts as 0.
+ * fields, 2 contract edge field, 3 receiver pass, 4 analysis, 5 project even, 6 project odd.
+ * A skipped stage counts as 0.
  * Errors: CGTP_ERR_ARG (NULL, flag not set, unknown op), CGTP_ERR_HIP. */
 int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages, int *n_calls);
 
 /* Measurement helper, not part of the method: the read-pattern ceiling of the message-passing
  * receiver. Replays, for the CSR (row_ptr, col) of cgtp_message_pass, exactly the sender-field
- * loads of the plan's per-thread receiver (fp32 plans whose receiver is the zonal per-thread
- * kernel: lmax <= 6 by default, grids of at most 1024 points), in its block order, over
- * fields [n_nodes][R][3][UVs] (UVs = n_theta * n_phi rounded up to 32; contents arbitrary),
- * and computes nothing from them; sink is a device float written at most once. Its time is
- * the floor the receiver's gather pattern sets on the memory path. That receiver takes the
- * surface curl with both derivatives moved onto the analysis (integration by parts on the
- * sphere), so it reads only the value plane (plane 0) of each sender rank, once per edge:
- * 4 R n_theta n_phi bytes per edge. Asynchronous on stream.
+ * loads of the plan's receiver, in its block order, over fields [n_nodes][R][3][UVs]
+ * (UVs = n_theta * n_phi rounded up to 32; contents arbitrary), and computes nothing from them;
+ * sink is a device float written at most once. Its time is the floor the receiver's gather
+ * pattern sets on the memory path. The receivers take the surface curl with both derivatives
+ * moved onto the analysis (integration by parts on the sphere), so they read only the value
+ * plane (plane 0) of each sender rank, once per edge: 4 R n_theta n_phi bytes per edge.
+ * Supported for fp32 plans whose receiver is the MFMA one on the plain sender layout (the
+ * default grid below lmax 7, R a multiple of 16) or the per-thread one (grids of at most 1024
+ * points). Asynchronous on stream.
  * Errors: CGTP_ERR_ARG (NULL, sizes, fields_bytes too small), CGTP_ERR_UNSUPPORTED (another
  * receiver), CGTP_ERR_HIP. */
 int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,

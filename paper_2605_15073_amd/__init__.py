@@ -45,7 +45,7 @@ CGTP_NOALLOC_SCRATCH_BYTES = 64 << 20
 ONSITE_STAGES = ("contract_operands", "grid_product_curl_analysis", "project")
 ONSITE_GENERAL_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis",
                          "project_even", "project_odd")
-MP_STAGES = ("contract_node", "sender_fields", "contract_edge_radial", "receiver",
+MP_STAGES = ("contract_node", "sender_fields", "contract_edge_radial", "receiver", "analysis",
              "project_even", "project_odd")
 NBODY_STAGES = ("contract_operands", "grid_product_analysis", "project")
 

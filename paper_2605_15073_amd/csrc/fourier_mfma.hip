@@ -1117,7 +1117,7 @@ hipError_t receiver_fields_lm(const Tabs<float> &tb, int64_t N, int R, const int
 hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const int32_t *row_ptr, const int32_t *col,
                                        const float *HE, const float *HEc, const float *SF,
-                                       float *S, float *Ta, float *Tb, hipStream_t s)
+                                       float *S, float *Ta, float *Tb, hipStream_t s, bool analyse)
 {
     if (N == 0) return hipSuccess;
     if (!sender_mfma_supported(tb.d)) return hipErrorNotSupported;
@@ -1129,7 +1129,7 @@ hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
 #undef CGTP_CASE
     default: return hipErrorNotSupported;
     }
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || !analyse) return e;
     e = launch_analysis_mfma(tb, N, R, S, Ta, Tb, s);
     if (e != hipErrorNotSupported) return e;
     return launch_analysis_folded(tb, N, R, S, Ta, Tb, s);

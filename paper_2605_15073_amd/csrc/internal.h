@@ -169,7 +169,8 @@ template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
                            const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
-                           hipStream_t s, bool values_only = false, T *Sg = nullptr);
+                           hipStream_t s, bool values_only = false, T *Sg = nullptr,
+                           bool analyse = true);
 
 // Receiver pass for a general per-edge field (two parity-bearing fields): HE [E][R][K] are
 // the edge field's channel-contracted coefficients (edge e = row_ptr order), SF the sender
@@ -189,7 +190,8 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
 hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const int32_t *row_ptr, const int32_t *col,
                                        const float *HE, const float *HEc, const float *SF,
-                                       float *S, float *Ta, float *Tb, hipStream_t s);
+                                       float *S, float *Ta, float *Tb, hipStream_t s,
+                                       bool analyse = true);
 
 // nu-body on-site grid product (kernels.hip): Tout[b][r][K] = the analysis of the pointwise
 // product of the nu fields synthesised from H.h[t][b][r][K]. The grid of tb must be fine
@@ -251,7 +253,11 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
                                 const int32_t *col, const float *unit, const float *Rt,
                                 const float *Rtg, const float *SF, const float *SFf,
                                 bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s,
-                                bool values_only = false);
+                                bool values_only = false, bool analyse = true);
+// The inverse transforms of the summed grid fields S of a receiver (analyse = false above)
+// into Ta, Tb: mode as launch_analysis_mfma; mode 0 also off the default grid.
+hipError_t launch_summed_analysis(const Tabs<float> &tb, int64_t N, int R, const float *S,
+                                  float *Ta, float *Tb, hipStream_t s, int mode);
 
 // Read-pattern ceiling of the per-thread receiver (kernels.hip): the sender-field loads of
 // k_receiver_zonal in its value-only form (fp32, one grid point per thread, blocks of 16
@@ -260,6 +266,11 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
 // more than 1024 points.
 hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
                                const int32_t *col, const float *SF, float *sink, hipStream_t s);
+// The same for the MFMA receiver in its values-only form on the plain sender layout
+// (receiver_mfma.hip): its blocks, block order and 16-byte value-plane loads.
+hipError_t launch_gather_probe_mfma(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
+                                    const int32_t *col, const float *SF, float *sink,
+                                    hipStream_t s);
 
 // Status reporting shared by the entry points of every source file: report() stores the
 // detail message returned by cgtp_last_error() on this thread and passes the status through.

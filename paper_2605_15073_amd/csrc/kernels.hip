@@ -1093,7 +1093,7 @@ template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
                            const int32_t *row_ptr, const int32_t *col, const T *unit,
                            const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
-                           hipStream_t s, bool values_only, T *Sg)
+                           hipStream_t s, bool values_only, T *Sg, bool analyse)
 {
     int64_t blocks = N * R;
     if (blocks == 0) return hipSuccess;
@@ -1150,7 +1150,7 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
 #undef CGTP_RECV
 #undef CGTP_RECV_TW
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !Sg) return e;
+    if (e != hipSuccess || !Sg || !analyse) return e;
     if constexpr (sizeof(T) == 4)
         return launch_analysis_mfma(tb, N, R, Sg, Ta, Tb, s, SFf ? 2 : 1);
     return hipErrorInvalidValue;
@@ -1164,7 +1164,7 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     template hipError_t launch_receiver<T>(const Tabs<T> &, bool, int64_t, int, const int32_t *, \
                                            const int32_t *, const T *, const T *, const T *,     \
                                            const T *, const T *, T *, T *, hipStream_t, bool,    \
-                                           T *);                                                 \
+                                           T *, bool);                                           \
     template hipError_t launch_receiver_fields<T>(const Tabs<T> &, int64_t, int, const int32_t *, \
                                                   const int32_t *, const T *, const T *, T *, T *, \
                                                   hipStream_t);                                   \

@@ -9,7 +9,7 @@
 #include "internal.h"
 
 namespace {
-constexpr int kMaxStages = 6;
+constexpr int kMaxStages = 7;
 constexpr int kNumOps = 7;  // CGTP_OP_ONSITE .. CGTP_OP_ONSITE_NBODY
 // HIP events bracketing the kernel stages of one call (CGTP_TIME_STAGES).
 struct EventSet {
@@ -440,7 +440,7 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
     // is all it reads
     const bool values_only = values_only_form(p, R, false);
     StageRec rec;
-    int st = rec.begin(p, op, 6, s);
+    int st = rec.begin(p, op, 7, s);
     if (st) return st;
     hipError_t e;
     // Eq. msgpass-HI, then the node-side forward transforms (Eqs. msgpass-FI, msgpass-AI),
@@ -455,7 +455,7 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
         const int planes = values_only ? 1 : 7;
         if constexpr (sizeof(T) == 4) {
             if (sf_chunked(p, R))
-                e = cgtp::launch_sender_mfma(tb, N, R, h, sf, true, s);
+                e = cgtp::launch_sender_mfma(tb, N, R, h, sf, true, s, planes);
             else
                 e = cgtp::launch_sender_fields<T>(tb, N, R, h, sf, s, planes);
         } else {
@@ -471,27 +471,39 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
                                  separated ? nullptr : tb.cl, false, s);
     if (e != hipSuccess) return hip_fail(e, "contract edge radial");
     rec.mark();
-    if constexpr (sizeof(T) == 4) {
-        if (use_mfma_receiver(p, R)) {
-            float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
-            e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt,
-                                           nullptr, SF, SFf, sf_chunked(p, R), Sg, Ta, Tb, s,
-                                           values_only);
-            if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
-            rec.mark();
-            goto projections;
-        }
-    }
     {
-        T *Sz = values_only && zonal_mfma_analysis(p, R, false)
-                    ? reinterpret_cast<T *>(ws + lay.off[5])
-                    : nullptr;
-        e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt,
-                                     nullptr, SF, SFf, Ta, Tb, s, values_only, Sz);
+        // the receiver pass (stage 3); the inverse transforms of its summed fields S (stage 4)
+        // when they run as a kernel of their own, else inside the receiver (the stage is empty)
+        T *Sg = reinterpret_cast<T *>(ws + lay.off[5]);
+        int amode = -1;  // analysis mode of S (launch_analysis_mfma), -1: none
+        bool mfma = false;
+        if constexpr (sizeof(T) == 4) {
+            mfma = use_mfma_receiver(p, R);
+            if (mfma) {
+                e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt,
+                                               nullptr, SF, SFf, sf_chunked(p, R), Sg, Ta, Tb, s,
+                                               values_only, false);
+                if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
+                amode = values_only ? (two ? 2 : 1) : 0;
+            }
+        }
+        if (!mfma) {
+            const bool hand_over = values_only && zonal_mfma_analysis(p, R, false);
+            e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt,
+                                         nullptr, SF, SFf, Ta, Tb, s, values_only,
+                                         hand_over ? Sg : nullptr, false);
+            if (e != hipSuccess) return hip_fail(e, "receiver");
+            if (hand_over) amode = two ? 2 : 1;
+        }
+        rec.mark();
+        if constexpr (sizeof(T) == 4) {
+            if (amode >= 0) {
+                e = cgtp::launch_summed_analysis(tb, N, R, Sg, Ta, Tb, s, amode);
+                if (e != hipSuccess) return hip_fail(e, "analysis");
+            }
+        }
+        rec.mark();
     }
-    if (e != hipSuccess) return hip_fail(e, "receiver");
-    rec.mark();
-projections:
     if (oe) {
         e = project<T>(N, C, R, d.K, Uoe, Ta, hs, oe, false, s);
         if (e != hipSuccess) return hip_fail(e, "project even");
@@ -750,7 +762,7 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     T *HIc = G.split ? reinterpret_cast<T *>(ws + lay.off[0] + lay.hf) : nullptr;
     T *Rtc = G.split ? reinterpret_cast<T *>(ws + lay.off[2] + lay.rtf) : nullptr;
     StageRec rec;
-    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_GENERAL, 6, s);
+    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_GENERAL, 7, s);
     if (st) return st;
     hipError_t e;
     for (int gi = 0; gi < G.n; ++gi) {
@@ -793,23 +805,36 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
         }
     }
     rec.mark();
+    // the receiver pass (stage 3), then the inverse transforms of its summed fields S (stage 4)
+    // when they run as a kernel of their own
+    T *Sg = reinterpret_cast<T *>(ws + lay.off[5]);
+    int amode = -1;  // analysis mode of S (launch_analysis_mfma), -1: none
+    bool mfma = false;
     if constexpr (sizeof(T) == 4) {
-        if (use_mfma_receiver(p, Rg, G.split)) {
-            float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
+        mfma = use_mfma_receiver(p, Rg, G.split);
+        if (mfma) {
             e = cgtp::launch_receiver_mfma(tb, N, Rg, row_ptr, col, (const float *)unit, Rt, Rtc,
                                            SF, nullptr, sf_chunked(p, Rg, G.split), Sg, Ta, Tb, s,
-                                           values_only);
+                                           values_only, false);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
-            rec.mark();
-            return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
+            amode = values_only ? 1 : 0;
         }
     }
-    T *Sz = values_only && zonal_mfma_analysis(p, Rg, G.split)
-                ? reinterpret_cast<T *>(ws + lay.off[5])
-                : nullptr;
-    e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, Rtc, SF,
-                                 nullptr, Ta, Tb, s, values_only, Sz);
-    if (e != hipSuccess) return hip_fail(e, "receiver");
+    if (!mfma) {
+        const bool hand_over = values_only && zonal_mfma_analysis(p, Rg, G.split);
+        e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, Rtc,
+                                     SF, nullptr, Ta, Tb, s, values_only, hand_over ? Sg : nullptr,
+                                     false);
+        if (e != hipSuccess) return hip_fail(e, "receiver");
+        if (hand_over) amode = 1;
+    }
+    rec.mark();
+    if constexpr (sizeof(T) == 4) {
+        if (amode >= 0) {
+            e = cgtp::launch_summed_analysis(tb, N, Rg, Sg, Ta, Tb, s, amode);
+            if (e != hipSuccess) return hip_fail(e, "analysis");
+        }
+    }
     rec.mark();
     return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
 }
@@ -836,7 +861,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     T *HIc = G.split ? reinterpret_cast<T *>(ws + lay.off[0] + lay.hf) : nullptr;
     T *HEc = G.split ? reinterpret_cast<T *>(ws + lay.off[2] + lay.rtf) : nullptr;
     StageRec rec;
-    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_FIELDS, 6, s);
+    int st = rec.begin(p, CGTP_OP_MESSAGE_PASS_FIELDS, 7, s);
     if (st) return st;
     hipError_t e;
     T *wc = reinterpret_cast<T *>(ws + lay.wc);
@@ -856,10 +881,14 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     rec.mark();
     if constexpr (sizeof(T) == 4) {
         if (use_mfma_fields(p)) {
+            // the receiver pass (stage 3), then the inverse transforms of its sums (stage 4)
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
             e = cgtp::launch_receiver_fields_mfma(tb, N, Rg, row_ptr, col, HE, HEc, SF, Sg, Ta, Tb,
-                                                  s);
+                                                  s, false);
             if (e != hipSuccess) return hip_fail(e, "receiver (edge field, mfma)");
+            rec.mark();
+            e = cgtp::launch_summed_analysis(tb, N, Rg, Sg, Ta, Tb, s, 0);
+            if (e != hipSuccess) return hip_fail(e, "analysis");
             rec.mark();
             return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
         }
@@ -872,6 +901,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
                     p->d.UV);
     if (e != hipSuccess) return hip_fail(e, "receiver (edge field)");
     rec.mark();
+    rec.mark();  // the analysis ran inside the receiver
     return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
 }
 
@@ -1453,11 +1483,16 @@ int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
     if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
     if (n_nodes < 0 || n_edges < 0 || n_edges >= 0x7fffffffLL)
         return fail(CGTP_ERR_ARG, "bad sizes");
-    if (plan->dtype != CGTP_F32 || use_mfma_receiver(plan, plan->R) ||
-        (plan->flags & CGTP_EDGE_SEPARATED) || plan->d.UV > 1024)
+    // the receiver of cgtp_message_pass on this plan: the MFMA one in its values-only form on
+    // the plain sender layout, or the per-thread zonal one
+    const bool mfma = use_mfma_receiver(plan, plan->R);
+    const bool mfma_plain = mfma && mfma_values_only(plan, plan->R, false) && !sf_chunked(plan, plan->R);
+    if (plan->dtype != CGTP_F32 || (plan->flags & CGTP_EDGE_SEPARATED) || (mfma && !mfma_plain) ||
+        (!mfma && plan->d.UV > 1024))
         return fail(CGTP_ERR_UNSUPPORTED,
-                    "the probe replays the fp32 per-thread zonal receiver (lmax < %d, grids of "
-                    "at most 1024 points)", cgtp::kMfmaRecvMinL);
+                    "the probe replays the fp32 message-passing receiver in its values-only form "
+                    "(MFMA below lmax %d on the default grid, else per-thread on grids of at "
+                    "most 1024 points)", cgtp::kMfmaRecvMinL);
     if (n_nodes == 0) return CGTP_OK;
     if (!row_ptr || !fields || !sink || (n_edges > 0 && !col))
         return fail(CGTP_ERR_ARG, "NULL argument");
@@ -1466,10 +1501,15 @@ int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
         return fail(CGTP_ERR_ARG, "fields buffer of %zu bytes, %zu needed", fields_bytes, need);
     int st = check_device(plan);
     if (st) return st;
-    hipError_t e = cgtp::launch_gather_probe(plan->d, n_nodes, plan->R, row_ptr, col,
-                                             static_cast<const float *>(fields),
-                                             static_cast<float *>(sink),
-                                             static_cast<hipStream_t>(stream));
+    hipError_t e =
+        mfma_plain ? cgtp::launch_gather_probe_mfma(plan->d, n_nodes, plan->R, row_ptr, col,
+                                                    static_cast<const float *>(fields),
+                                                    static_cast<float *>(sink),
+                                                    static_cast<hipStream_t>(stream))
+                   : cgtp::launch_gather_probe(plan->d, n_nodes, plan->R, row_ptr, col,
+                                               static_cast<const float *>(fields),
+                                               static_cast<float *>(sink),
+                                               static_cast<hipStream_t>(stream));
     return e == hipSuccess ? CGTP_OK : hip_fail(e, "gather probe");
 }
 
@@ -1496,7 +1536,7 @@ int cgtp_stage_times(cgtp_plan plan, int op, double *ms, int cap, int *n_stages,
     else if (op == CGTP_OP_ONSITE_GENERAL) ns = 5;
     else if (op == CGTP_OP_MESSAGE_PASS || op == CGTP_OP_MESSAGE_PASS_TWO_SLOT ||
              op == CGTP_OP_MESSAGE_PASS_GENERAL || op == CGTP_OP_MESSAGE_PASS_FIELDS)
-        ns = 6;
+        ns = 7;
     else return fail(CGTP_ERR_ARG, "unknown op %d", op);
     int status = drain_timers(plan);
     for (int k = 0; k < ns && k < cap; ++k) ms[k] = plan->stage_acc[op][k];

@@ -295,6 +295,47 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     }
 }
 
+// Read-pattern ceiling of k_receiver_mfma in its values-only form on the plain sender layout
+// [N][R][3][UVs]: the same blocks in the same order, the same wave-uniform sender index per
+// edge and the same 16-byte loads of the value plane (one per 16-point tile and lane), with
+// nothing computed from them but a running sum; sink receives a value only if that sum equals
+// a constant no finite input sums to by chance, which keeps every load live.
+template <int WPB>
+__global__ __launch_bounds__(64 * WPB) void k_gather_probe_mfma(int UV, int UVs, int R,
+                                                                int nchunks,
+                                                                const int32_t *__restrict__ row_ptr,
+                                                                const int32_t *__restrict__ col,
+                                                                const float *__restrict__ SF,
+                                                                float *__restrict__ sink)
+{
+    constexpr int TPW = 4, PW = 16 * TPW, PC = WPB * PW;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, n = lane & 15;
+    const int64_t NN = (int64_t)gridDim.x / ((int64_t)(R / kRT) * nchunks);
+    const int rest = (int)(blockIdx.x / NN);
+    const int64_t i = blockIdx.x - (int64_t)rest * NN;
+    const int r0 = (rest / nchunks) * kRT;
+    const int pw0 = (rest % nchunks) * PC + wave * PW;
+    if (pw0 >= UV) return;
+    const unsigned voff = (unsigned)((n * 3 * UVs + pw0 + 4 * g) * 4);
+    unsigned vofft[TPW];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) vofft[t] = pw0 + 16 * t + 4 * g < UV ? voff : 0x80000000u;
+    const float *sfb = SF + (int64_t)r0 * 3 * UVs;
+    const int64_t jstride = (int64_t)R * 3 * UVs;
+    const unsigned sfbytes = (unsigned)(kRT * 3 * UVs * 4);
+    float4_t acc = float4_t{0.f, 0.f, 0.f, 0.f};
+    const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
+    for (int e = e0; e < e1; ++e) {
+        const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
+        const __amdgpu_buffer_rsrc_t sfr = rsrc(sfb + j * jstride, sfbytes);
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) acc += bload4(sfr, vofft[t], (unsigned)(t * 16 * 4));
+    }
+    const float sum = acc[0] + acc[1] + acc[2] + acc[3];
+    if (sum == -1.2345678e30f) sink[0] = sum;
+}
+
 // Inverse transforms of stored grid fields S [B][R][2][UVs] -> Ta, Tb [B][R][K]:
 // one workgroup per (node, block of ranks), one rank at a time through LDS.
 __global__ __launch_bounds__(256) void k_analysis_rows(Tabs<float> tb, int R, int rb,
@@ -356,6 +397,21 @@ bool receiver_mfma_supported(const Dims &d, int R)
     return R % kRT == 0 && d.L <= 32;
 }
 
+hipError_t launch_gather_probe_mfma(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
+                                    const int32_t *col, const float *SF, float *sink,
+                                    hipStream_t s)
+{
+    if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
+    constexpr int WPB = 2, PC = WPB * 64;  // as launch_receiver_mfma
+    const int nchunks = (d.UV + PC - 1) / PC;
+    const int64_t blocks = N * (R / kRT) * nchunks;
+    if (blocks == 0) return hipSuccess;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_gather_probe_mfma<WPB>), dim3((unsigned)blocks), dim3(64 * WPB), 0, s,
+                       d.UV, d.UVs, R, nchunks, row_ptr, col, SF, sink);
+    return hipGetLastError();
+}
+
 size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R, int planes)
 {
     return (size_t)N * R * planes * d.UVs;
@@ -365,7 +421,7 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
                                 const int32_t *col, const float *unit, const float *Rt,
                                 const float *Rtg, const float *SF, const float *SFf,
                                 bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s,
-                                bool values_only)
+                                bool values_only, bool analyse)
 {
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
@@ -409,9 +465,17 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     default: return hipErrorNotSupported;
     }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if (values_only) return launch_analysis_mfma(tb, N, R, S, Ta, Tb, s, SFf ? 2 : 1);
-    e = launch_analysis_mfma(tb, N, R, S, Ta, Tb, s);
+    if (e != hipSuccess || !analyse) return e;
+    return launch_summed_analysis(tb, N, R, S, Ta, Tb, s, values_only ? (SFf ? 2 : 1) : 0);
+}
+
+hipError_t launch_summed_analysis(const Tabs<float> &tb, int64_t N, int R, const float *S,
+                                  float *Ta, float *Tb, hipStream_t s, int mode)
+{
+    if (N == 0) return hipSuccess;
+    const Dims &d = tb.d;
+    if (mode != 0) return launch_analysis_mfma(tb, N, R, S, Ta, Tb, s, mode);
+    hipError_t e = launch_analysis_mfma(tb, N, R, S, Ta, Tb, s);
     if (e != hipErrorNotSupported) return e;
     e = launch_analysis_folded(tb, N, R, S, Ta, Tb, s);
     if (e != hipErrorNotSupported) return e;

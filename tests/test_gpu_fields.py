@@ -143,7 +143,7 @@ def test_fields_workspace_errors_and_stages(cg):
     assert ei.value.status == cg.CGTP_ERR_WORKSPACE
     _check(_gpu(cg, plan, t), ref, TOL_F32)
     stages, calls = cg.stage_times(plan, op)
-    assert calls == 2 and len(stages) == 6 and all(v >= 0 for v in stages.values())
+    assert calls == 2 and len(stages) == 7 and all(v >= 0 for v in stages.values())
 
 
 def test_mpf_5k_l6_sampled(cg):

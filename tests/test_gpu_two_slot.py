@@ -157,7 +157,7 @@ def test_two_slot_stage_times(cg):
     for _ in range(2):
         _run2(cg, plan, t)
     stages, calls = cg.stage_times(plan, cg.CGTP_OP_MESSAGE_PASS_TWO_SLOT)
-    assert calls == 2 and len(stages) == 6 and all(v >= 0 for v in stages.values())
+    assert calls == 2 and len(stages) == 7 and all(v >= 0 for v in stages.values())
     assert cg.stage_times(plan, cg.CGTP_OP_MESSAGE_PASS)[1] == 0
 
 
