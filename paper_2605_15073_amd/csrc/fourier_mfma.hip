@@ -391,13 +391,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 // per workgroup with coalesced loads into a double-buffered LDS tile while the previous
 // one is multiplied. The product is formed transposed, D[column][row] = table^T H^T, so a
 // lane holds four consecutive columns of one row and stores them as one 16-byte vector.
-template <int LM>
+// V1: the value field only (the first UVs columns; the receivers that take the curl in its
+// moved-derivative form read nothing else).
+constexpr int dense_waves(int ct)
+{
+    for (int nw = 12; nw > 1; --nw)
+        if (ct % nw == 0 && nw != 11 && nw != 9 && nw != 7) return nw;
+    return 1;
+}
+
+template <int LM, bool V1 = false>
 struct DenseSyn {
     using G = Grid<LM>;
     static constexpr int KP = (G::K + 3) / 4 * 4, KS = KP / 4;  // reduction steps of 4
-    static constexpr int NCOL = 3 * G::UVs, CT = NCOL / 16;     // 16-column tiles
-    // UVs is a multiple of 32, so CT = 6 UVs / 32 always splits evenly over six waves
-    static constexpr int NW = CT % 12 == 0 ? 12 : 6, NT = 64 * NW, CTW = CT / NW, WC = 16 * CTW;
+    static constexpr int NCOL = 3 * G::UVs;                     // table and output row length
+    static constexpr int CT = (V1 ? G::UVs : NCOL) / 16;        // computed 16-column tiles
+    // the largest wave count up to 12 that splits the tiles evenly (UVs is a multiple of 32:
+    // CT is even, and a multiple of 6 for all three fields)
+    static constexpr int NW = dense_waves(CT), NT = 64 * NW, CTW = CT / NW, WC = 16 * CTW;
     static_assert(CT % NW == 0, "column tiles split evenly over the waves");
     // LDS row stride of a staged A row: KA / 4 odd puts the 16 rows x 4 lane groups of an
     // operand read on distinct banks
@@ -405,13 +416,13 @@ struct DenseSyn {
     static constexpr int NLA = (16 * G::K + NT - 1) / NT;  // tile loads per thread
 };
 
-template <int LM>
-__global__ __launch_bounds__(64 * DenseSyn<LM>::NW) __attribute__((amdgpu_waves_per_eu(3))) void k_sender_dense(
+template <int LM, bool V1>
+__global__ __launch_bounds__((64 * DenseSyn<LM, V1>::NW)) __attribute__((amdgpu_waves_per_eu(3))) void k_sender_dense(
     const float *__restrict__ Ys, int64_t rows, const float *__restrict__ H,
     float *__restrict__ SF, int planes)
 {
     using G = Grid<LM>;
-    using D = DenseSyn<LM>;
+    using D = DenseSyn<LM, V1>;
     __shared__ float as[2][16 * D::KA];  // staged rows of H (columns past K stay 0)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g4 = lane >> 4, n = lane & 15;
@@ -993,6 +1004,31 @@ hipError_t onsite_lm(const Tabs<float> &tb, int64_t B, int R, const float *HA, c
     return hipGetLastError();
 }
 
+// The dense synthesis as persistent workgroups, as many as the device holds at once.
+template <int LM, bool V1>
+hipError_t launch_dense(const Tabs<float> &tb, int64_t rows, const float *H, float *SF, int planes,
+                        hipStream_t s)
+{
+    using D = DenseSyn<LM, V1>;
+    const int64_t ntiles = (rows + 15) / 16;
+    static const int64_t resident = [] {
+        int dev = 0, cus = 0, per = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per, reinterpret_cast<const void *>(&k_sender_dense<LM, V1>), 64 * D::NW, 0) !=
+                hipSuccess ||
+            cus < 1 || per < 1)
+            return kDenseSynthBlocks;
+        return (int64_t)cus * per;
+    }();
+    const int64_t grid = ntiles < resident ? ntiles : resident;
+    hipLaunchKernelGGL((k_sender_dense<LM, V1>), dim3((unsigned)grid), dim3(64 * D::NW), 0, s,
+                       tb.ysyn, rows, H, SF, planes);
+    return hipGetLastError();
+}
+
 template <int LM>
 hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, float *SF,
                      bool chunked, hipStream_t s, int planes)
@@ -1006,24 +1042,8 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
     if (chunked && R % 16 != 0) return hipErrorInvalidValue;
     if constexpr (LM >= 1 && LM <= kDenseSynthMaxL) {
         if (!chunked) {
-            const int64_t rows = B * R, ntiles = (rows + 15) / 16;
-            // as many persistent workgroups as the device holds at once
-            static const int64_t resident = [] {
-                int dev = 0, cus = 0, per = 0;
-                if (hipGetDevice(&dev) != hipSuccess ||
-                    hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
-                        hipSuccess ||
-                    hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                        &per, reinterpret_cast<const void *>(&k_sender_dense<LM>),
-                        64 * DenseSyn<LM>::NW, 0) != hipSuccess ||
-                    cus < 1 || per < 1)
-                    return kDenseSynthBlocks;
-                return (int64_t)cus * per;
-            }();
-            const int64_t grid = ntiles < resident ? ntiles : resident;
-            hipLaunchKernelGGL((k_sender_dense<LM>), dim3((unsigned)grid),
-                               dim3(64 * DenseSyn<LM>::NW), 0, s, tb.ysyn, rows, H, SF, planes);
-            return hipGetLastError();
+            if (planes == 1) return launch_dense<LM, true>(tb, B * R, H, SF, planes, s);
+            return launch_dense<LM, false>(tb, B * R, H, SF, planes, s);
         }
     }
     const int nc = chunked ? sf_chunks(tb.d) : 0;
