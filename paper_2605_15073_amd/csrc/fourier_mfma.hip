@@ -393,8 +393,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
 // lane holds four consecutive columns of one row and stores them as one 16-byte vector.
 // V1: the value field only (the first UVs columns; the receivers that take the curl in its
 // moved-derivative form read nothing else).
-constexpr int dense_waves(int ct)
+// Waves per workgroup. All three fields: 12 when the column tiles split evenly that way,
+// else 6 (UVs is a multiple of 32, so CT = 6 UVs / 32 splits over six), either way a whole
+// number of a wave's tiles per field, so a wave's tiles lie in one field (its store mask is
+// per field). The value field alone: the largest even split up to 12.
+constexpr int dense_waves(int ct, bool v1)
 {
+    if (!v1) return ct % 12 == 0 ? 12 : 6;
     for (int nw = 12; nw > 1; --nw)
         if (ct % nw == 0 && nw != 11 && nw != 9 && nw != 7) return nw;
     return 1;
@@ -406,10 +411,9 @@ struct DenseSyn {
     static constexpr int KP = (G::K + 3) / 4 * 4, KS = KP / 4;  // reduction steps of 4
     static constexpr int NCOL = 3 * G::UVs;                     // table and output row length
     static constexpr int CT = (V1 ? G::UVs : NCOL) / 16;        // computed 16-column tiles
-    // the largest wave count up to 12 that splits the tiles evenly (UVs is a multiple of 32:
-    // CT is even, and a multiple of 6 for all three fields)
-    static constexpr int NW = dense_waves(CT), NT = 64 * NW, CTW = CT / NW, WC = 16 * CTW;
+    static constexpr int NW = dense_waves(CT, V1), NT = 64 * NW, CTW = CT / NW, WC = 16 * CTW;
     static_assert(CT % NW == 0, "column tiles split evenly over the waves");
+    static_assert(V1 || (G::UVs / 16) % CTW == 0, "a wave's column tiles lie in one field");
     // LDS row stride of a staged A row: KA / 4 odd puts the 16 rows x 4 lane groups of an
     // operand read on distinct banks
     static constexpr int KA = (KP / 4) % 2 ? KP : KP + 4;
