@@ -773,24 +773,48 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
             qb[kk][t] = (v < G::V && m < G::M) ? tb.q[v * G::M + m] : 0.f;
         }
     constexpr int R4 = G::UVs / 4;  // 16-byte words per stored row
-    for (int f = 0; f < NF; ++f) {
-        // stage rows (q, u) of field f as Ss[q U + u][v] (16-byte loads of the stored rows;
-        // columns V .. VP - 1 stay zero)
-        for (int k = tid; k < nr * R4; k += nt) {
-            const int q = k / R4, r = 4 * (k - q * R4);
-            if (r < G::UV) {
-                const float4_t x = *reinterpret_cast<const float4_t *>(
-                    S + ((b * R + r0 + q) * NF + f) * (int64_t)G::UVs + r);
-                float *dst = Ss + q * G::U * G::VS;
-                int u = r / G::V, v = r - u * G::V;
+    // A thread's 16-byte words k = tid + j nt of a field; the first kPre of them are loaded
+    // into registers one field ahead, so their latency overlaps the previous field's products.
+    constexpr int kPre = 4;
+    auto word = [&](int f, int k) {
+        const int q = k / R4, r = 4 * (k - q * R4);
+        return *reinterpret_cast<const float4_t *>(S + ((b * R + r0 + q) * NF + f) * (int64_t)G::UVs + r);
+    };
+    // rows (q, u) of a field as Ss[q U + u][v]; columns V .. VP - 1 stay zero
+    auto put = [&](int k, const float4_t &x) {
+        const int q = k / R4, r = 4 * (k - q * R4);
+        float *dst = Ss + q * G::U * G::VS;
+        int u = r / G::V, v = r - u * G::V;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    if (r + e < G::UV) dst[u * G::VS + v] = x[e];
-                    if (++v == G::V) {
-                        v = 0;
-                        ++u;
-                    }
-                }
+        for (int e = 0; e < 4; ++e) {
+            if (r + e < G::UV) dst[u * G::VS + v] = x[e];
+            if (++v == G::V) {
+                v = 0;
+                ++u;
+            }
+        }
+    };
+    auto live = [&](int k) { return k < nr * R4 && 4 * (k % R4) < G::UV; };
+    float4_t pre[kPre];
+#pragma unroll
+    for (int j = 0; j < kPre; ++j) {
+        const int k = tid + j * nt;
+        if (live(k)) pre[j] = word(0, k);
+    }
+    for (int f = 0; f < NF; ++f) {
+        // stage field f: the prefetched words, then any further ones directly
+#pragma unroll
+        for (int j = 0; j < kPre; ++j) {
+            const int k = tid + j * nt;
+            if (live(k)) put(k, pre[j]);
+        }
+        for (int k = tid + kPre * nt; k < nr * R4; k += nt)
+            if (live(k)) put(k, word(f, k));
+        if (f + 1 < NF) {
+#pragma unroll
+            for (int j = 0; j < kPre; ++j) {
+                const int k = tid + j * nt;
+                if (live(k)) pre[j] = word(f + 1, k);
             }
         }
         __syncthreads();
