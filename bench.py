@@ -106,11 +106,12 @@ def live_blocks(flip1: bool, flip2: bool):
 
 
 def general_receiver_bytes(w, N: int, E: int) -> int:
-    """Algorithmic receiver bytes of general message passing: one grid field per Gaunt
-    block, two per curl block; one edge factor per block (one when shared); one analysed
-    field per block with per-category weights (two otherwise)."""
+    """Algorithmic receiver bytes of general message passing: one grid field per block (the
+    sender values its factors give: the curl takes its derivatives on the analysis side); one
+    edge factor per block (one when shared); one analysed field per block with per-category
+    weights (two otherwise)."""
     live = live_blocks(False, w.two_slot)
-    planes = sum(1 if b < 2 else 2 for b in live)
+    planes = len(live)
     rt = 1 if w.in_blocks == 1 else len(live)
     tf = len(live) if w.out_blocks == 2 else 2
     return receiver_bytes(w.lmax, w.R, N, E, planes=planes, rt_blocks=rt, t_fields=tf)
@@ -445,7 +446,7 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
             alg = general_receiver_bytes(w, w.n, E)
             live = live_blocks(False, w.two_slot)
             comp = compulsory_receiver_bytes(
-                w.lmax, w.R, w.n, E, planes=sum(1 if b < 2 else 2 for b in live),
+                w.lmax, w.R, w.n, E, planes=len(live),
                 rt_blocks=1 if w.in_blocks == 1 else len(live),
                 t_fields=len(live) if w.out_blocks == 2 else 2)
         else:

@@ -355,6 +355,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
                             if (planes & 1) o[t * 16] = acc[0][t][j];
                             if (planes & 2) o[G::UVs + t * 16] = acc[1][t][j];
                             if (planes & 4) o[2 * G::UVs + t * 16] = acc[2][t][j];
+                            if (planes & 8) o[G::UVs + t * 16] = acc[0][t][j];
                         }
                     }
                 } else {  // SF [R/16][nc][B][16][3][64]
@@ -370,6 +371,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
                             if (planes & 1) o[0] = acc[0][t][j];
                             if (planes & 2) o[kSfChunk] = acc[1][t][j];
                             if (planes & 4) o[2 * kSfChunk] = acc[2][t][j];
+                            if (planes & 8) o[kSfChunk] = acc[0][t][j];
                         }
                     }
                 }
@@ -433,7 +435,9 @@ __global__ __launch_bounds__((64 * DenseSyn<LM, V1>::NW)) __attribute__((amdgpu_
     for (int i = tid; i < 2 * 16 * D::KA; i += D::NT) (&as[0][0])[i] = 0.f;
     const int t0 = wave * D::CTW;
     const int f = (t0 * 16) / G::UVs;   // the field of this wave's columns (CTW tiles lie in one)
-    const bool store = (planes >> f) & 1;
+    // V1: the value field, into plane 0 (planes bit 0) or plane 1 (bit 3)
+    const bool store = V1 ? (planes & 9) != 0 : ((planes >> f) & 1) != 0;
+    const int pofs = V1 && (planes & 8) ? G::UVs : 0;
     // A operand of column tile t at reduction step kk: ysyn[4 kk + g][16 (t0 + t) + n]
     float bq[D::CTW][D::KS];
 #pragma unroll
@@ -483,7 +487,7 @@ __global__ __launch_bounds__((64 * DenseSyn<LM, V1>::NW)) __attribute__((amdgpu_
         // D[column 16 t + 4 g + j][row n]: columns 4 g .. 4 g + 3 of row 16 rt + n
         const int64_t row = rt * 16 + n;
         if (store && row < rows) {
-            float *dst = SF + row * D::NCOL + t0 * 16 + 4 * g4;
+            float *dst = SF + row * D::NCOL + pofs + t0 * 16 + 4 * g4;
 #pragma unroll
             for (int t = 0; t < D::CTW; ++t) *reinterpret_cast<float4_t *>(dst + 16 * t) = acc[t];
         }
@@ -1070,7 +1074,7 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
     if (chunked && R % 16 != 0) return hipErrorInvalidValue;
     if constexpr (LM >= 1 && LM <= kDenseSynthMaxL) {
         if (!chunked) {
-            if (planes == 1) return launch_dense<LM, true>(tb, B * R, H, SF, planes, s);
+            if (planes == 1 || planes == 8) return launch_dense<LM, true>(tb, B * R, H, SF, planes, s);
             return launch_dense<LM, false>(tb, B * R, H, SF, planes, s);
         }
     }

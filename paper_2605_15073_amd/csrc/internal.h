@@ -131,7 +131,8 @@ hipError_t launch_contract_pair(int64_t B, int Cin, int Cout, int K, const float
 
 // Node-side synthesis of the three grid fields (A, dA/dx, dA/dphi) of H[b][r][K]:
 // SF[b][r][3][UVs] (Eqs. struct-F, struct-tildeA plus the derivative passes). Only the
-// fields whose bit is set in planes (1: A, 2: dA/dx, 4: dA/dphi) are written.
+// fields whose bit is set in planes (1: A, 2: dA/dx, 4: dA/dphi) are written; bit 8 writes A
+// into plane 1 (the curl factors' values of the moved-derivative form with per-block factors).
 template <typename T>
 hipError_t launch_sender_fields(const Tabs<T> &tb, int64_t B, int R, const T *H, T *SF,
                                 hipStream_t s, int planes = 7);

@@ -205,7 +205,7 @@ __device__ __forceinline__ void stage_q(const Tabs<T> &tb, T *qs)
 
 // ---------------------------------------------------------------------------
 // Sender (node-side) grid fields: SF[b][r][0..2][UV] = (A, dA/dx, dA/dphi); only the fields
-// whose bit is set in `planes` are stored.
+// whose bit is set in `planes` are stored (bit 8: A into plane 1).
 // One block per (node, rb consecutive ranks): the Legendre pass of all rb ranks,
 // then every thread writes the three fields of its grid points for each rank.
 // ---------------------------------------------------------------------------
@@ -242,6 +242,7 @@ __global__ __launch_bounds__(kThreads) void k_sender_fields(Tabs<T> tb, int R, i
             if (planes & 1) o[0] = a;
             if (planes & 2) o[d.UVs] = ax;
             if (planes & 4) o[2 * d.UVs] = ap;
+            if (planes & 8) o[d.UVs] = a;
         }
     }
 }
@@ -464,10 +465,10 @@ __device__ __forceinline__ double buf_load<double>(__amdgpu_buffer_rsrc_t rs, un
 // Table 1 its Gaunt product then feeds Tb and its curl product Ta.
 // SPLIT: the curl product takes the edge coefficients Rtg (its own CP factors) for the
 // derivative sum g, the Gaunt product Rt for the value sum a.
-// VAL (not with SPLIT): the curl product in the moved-derivative form of analysis_moved. The
-// senders then only need their value plane (plane 0 of each rank's three): per point and
-// rank the block accumulates the Gaunt sum a B and the two sums B dA/dx, B dA/dphi of the
-// edge field's derivatives, and reads a third of the sender bytes.
+// VAL: the curl product in the moved-derivative form of analysis_moved. The senders then
+// only need their value plane (plane 0 of each rank's three; with SPLIT the curl factors'
+// values in plane 1): per point and rank the block accumulates the Gaunt sum a B and the two
+// sums B dA/dx, B dA/dphi of the edge field's derivatives.
 template <typename T, int RB, int NPT, bool FULL, bool TWO, bool SPLIT, bool VAL>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
@@ -504,7 +505,6 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
         pcp[s] = tb.cphi[v];
         psp[s] = tb.sphi[v];
     }
-    static_assert(!(VAL && SPLIT), "the moved-derivative form takes one set of edge coefficients");
     // VAL: sa, sb the Gaunt sums into Ta, Tb; (ca1, ca2) the moved curl sums into Ta (the
     // flipped slot's, TWO), (cb1, cb2) into Tb (the natural slot's)
     T sa[NPT][RB], sb[NPT][RB], ca1[NPT][RB], ca2[NPT][RB], cb1[NPT][RB], cb2[NPT][RB];
@@ -573,10 +573,8 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
                 for (int q = 0; q < RB; ++q) {
                     // ranks past nr fall outside the descriptor's range and read 0
                     fI[q] = buf_load<T>(sfr, voff, (3 * q) * fstride);
-                    if (!VAL) {
-                        fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
-                        fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
-                    }
+                    if (!VAL || SPLIT) fX[q] = buf_load<T>(sfr, voff, (3 * q + 1) * fstride);
+                    if (!VAL) fP[q] = buf_load<T>(sfr, voff, (3 * q + 2) * fstride);
                     if (TWO) {
                         gI[q] = buf_load<T>(sff, voff, (3 * q) * fstride);
                         if (!VAL) {
@@ -623,7 +621,8 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
                     if (VAL) {
                         // dA/dx = g dxt and dA/dphi = g dpt of the edge field
                         sa[s][q] += a[q] * fI[q];
-                        const T gf = g[q] * fI[q];
+                        // SPLIT: the curl takes the curl factors' values (plane 1)
+                        const T gf = g[q] * (SPLIT ? fX[q] : fI[q]);
                         cb1[s][q] += dxt * gf;
                         cb2[s][q] += dpt * gf;
                         if (TWO) {
@@ -1099,7 +1098,7 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     if (blocks == 0) return hipSuccess;
     const Dims &d = tb.d;
     if (SFf && Rtg) return hipErrorNotSupported;
-    if (values_only && (separated || Rtg)) return hipErrorInvalidValue;
+    if (values_only && separated) return hipErrorInvalidValue;
     if (Sg && (!values_only || sizeof(T) != 4)) return hipErrorInvalidValue;
     if (separated) {
         if (SFf || Rtg) return hipErrorNotSupported;
@@ -1135,6 +1134,7 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     do {                                                                    \
         if (values_only) {                                                  \
             if (SFf) CGTP_RECV_TW(RBV, NP, true, false, true);              \
+            else if (Rtg) CGTP_RECV_TW(RBV, NP, false, true, true);         \
             else CGTP_RECV_TW(RBV, NP, false, false, true);                 \
         } else if (SFf) CGTP_RECV_TW(RBV, NP, true, false, false);          \
         else if (Rtg) CGTP_RECV_TW(RBV, NP, false, true, false);            \

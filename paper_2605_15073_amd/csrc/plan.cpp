@@ -75,11 +75,13 @@ struct Layout {
 };
 
 // Receiver on MFMA in its values-only form (the moved-derivative curl: only the senders'
-// value plane is read): fp32, zonal edge field, shared factors (split: no), R a multiple of
-// 16, the default grid (for the MFMA analysis of its moved planes); every lmax.
+// values are read, plane 0, and with per-block factors (split) the curl factors' values in
+// plane 1): fp32, zonal edge field, R a multiple of 16, the default grid (for the MFMA
+// analysis of its moved planes); every lmax.
 bool mfma_values_only(const cgtp_plan_s *p, int R, bool split)
 {
-    return p->dtype == CGTP_F32 && !split && !(p->flags & CGTP_EDGE_SEPARATED) &&
+    (void)split;
+    return p->dtype == CGTP_F32 && !(p->flags & CGTP_EDGE_SEPARATED) &&
            cgtp::receiver_mfma_supported(p->d, R) && cgtp::sender_mfma_supported(p->d);
 }
 
@@ -94,11 +96,11 @@ bool use_mfma_receiver(const cgtp_plan_s *p, int R, bool split = false)
 }
 
 // Whether the receiver takes the curl in the moved-derivative form (senders then write only
-// their value plane): shared factors and the zonal edge field, on the per-thread receiver or
-// on the MFMA one in its values-only form.
+// their values): the zonal edge field, on the per-thread receiver or on the MFMA one in its
+// values-only form.
 bool values_only_form(const cgtp_plan_s *p, int R, bool split)
 {
-    if (split || (p->flags & CGTP_EDGE_SEPARATED)) return false;
+    if (p->flags & CGTP_EDGE_SEPARATED) return false;
     return !use_mfma_receiver(p, R, split) || mfma_values_only(p, R, split);
 }
 
@@ -134,11 +136,11 @@ bool onsite_split_ok(const cgtp_plan_s *p)
     return p->dtype == CGTP_F32 && cgtp::onsite_split_supported(p->d);
 }
 
-// The zonal receiver (values-only form: shared factors, fp32, default grid) hands its summed
-// fields to the MFMA analysis through S [N][R][3][UVs] ([6] with two node slots).
+// The zonal receiver (values-only form, fp32, default grid) hands its summed fields to the
+// MFMA analysis through S [N][R][3][UVs] ([6] with two node slots).
 bool zonal_mfma_analysis(const cgtp_plan_s *p, int R, bool split)
 {
-    return p->dtype == CGTP_F32 && !split && !(p->flags & CGTP_EDGE_SEPARATED) &&
+    return p->dtype == CGTP_F32 && !(p->flags & CGTP_EDGE_SEPARATED) &&
            !use_mfma_receiver(p, R, split) && cgtp::sender_mfma_supported(p->d);
 }
 
@@ -775,13 +777,14 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
         if (e != hipSuccess) return hip_fail(e, "contract node features");
     }
     rec.mark();
-    // split: the Gaunt factors' contraction gives the sender values, the curl factors' the
-    // two derivative fields, into the same field slots
-    // the zonal receiver with shared factors takes the moved-derivative curl (value planes)
+    // split: the Gaunt factors' contraction gives the sender values (plane 0); the curl
+    // factors' give the two derivative fields (planes 1, 2), or in the moved-derivative form
+    // their values (plane 1)
     const bool values_only = values_only_form(p, Rg, G.split);
     for (int pass = 0; pass < (G.split ? 2 : 1); ++pass) {
         const T *h = pass ? HIc : HI;
-        const int planes = G.split ? (pass ? 6 : 1) : (values_only ? 1 : 7);
+        const int planes =
+            G.split ? (pass ? (values_only ? 8 : 6) : 1) : (values_only ? 1 : 7);
         if constexpr (sizeof(T) == 4) {
             if (sf_chunked(p, Rg, G.split))
                 e = cgtp::launch_sender_mfma(tb, N, Rg, h, SF, true, s, planes);

@@ -59,7 +59,8 @@ __device__ __forceinline__ void wave_sync()
 // product S_beta's. The next edge is prefetched only with one slot (registers).
 // SPLIT: the curl product's edge coefficients are Rtg (its own CP factors): the derivative
 // sum g multiplies P' with those, the value sum a P with Rt.
-// VAL (not with SPLIT): value planes only, moved-derivative curl (above).
+// VAL: value planes only, moved-derivative curl (above). With SPLIT the senders carry the
+// Gaunt factors' values in plane 0 and the curl factors' in plane 1.
 template <int WPB, int LM, bool TWO, bool SPLIT, bool VAL>
 __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
                                                             const int32_t *__restrict__ row_ptr,
@@ -115,7 +116,6 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     // rank, so its sender values are 16-byte loads and its S values 16-byte stores.
     // VAL: sa, sb the Gaunt sums into S_alpha, S_beta; (ca1, ca2) the moved curl pair into
     // S_alpha (the flipped slot's, TWO), (cb1, cb2) into S_beta (the natural slot's)
-    static_assert(!(VAL && SPLIT), "the moved-derivative form takes one set of edge coefficients");
     float4_t sa[TPW], sb[TPW], ca1[TPW], ca2[TPW], cb1[TPW], cb2[TPW];
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
@@ -154,10 +154,8 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
         for (int t = 0; t < TPW; ++t) {
             const unsigned so = (unsigned)(t * 16 * 4);
             fI[t] = bload4(sfr, vofft[t], so);
-            if (!VAL) {
-                fX[t] = bload4(sfr, vofft[t], so + fstride * 4);
-                fP[t] = bload4(sfr, vofft[t], so + 2 * fstride * 4);
-            }
+            if (!VAL || SPLIT) fX[t] = bload4(sfr, vofft[t], so + fstride * 4);
+            if (!VAL) fP[t] = bload4(sfr, vofft[t], so + 2 * fstride * 4);
         }
     };
     if (!TWO && e0 < e1) load_fields(sfb, e0, cI, cX, cP);
@@ -170,10 +168,8 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
 #pragma unroll
             for (int t = 0; t < TPW; ++t) {
                 fI[t] = cI[t];
-                if (!VAL) {
-                    fX[t] = cX[t];
-                    fP[t] = cP[t];
-                }
+                if (!VAL || SPLIT) fX[t] = cX[t];
+                if (!VAL) fP[t] = cP[t];
             }
             if (e + 1 < e1) load_fields(sfb, e + 1, cI, cX, cP);
         }
@@ -238,7 +234,8 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
                 if (VAL) {
                     // dA/dx = g dxt and dA/dphi = g dpt of the edge field
                     sa[t][jj] += a[jj] * fI[t][jj];
-                    const float gf = gg[jj] * fI[t][jj];
+                    // SPLIT: the curl takes the curl factors' values (plane 1)
+                    const float gf = gg[jj] * (SPLIT ? fX[t][jj] : fI[t][jj]);
                     cb1[t][jj] += dxt * gf;
                     cb2[t][jj] += dpt * gf;
                     if (TWO) {
@@ -427,7 +424,7 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     const Dims &d = tb.d;
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
     if (SFf && Rtg) return hipErrorNotSupported;
-    if (values_only && Rtg) return hipErrorInvalidValue;
+    if (values_only && SFf && Rtg) return hipErrorInvalidValue;
     constexpr int WPB = 2, PW = 64, PC = WPB * PW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
@@ -445,6 +442,7 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     case LMV:                                                          \
         if (values_only) {                                             \
             if (SFf) CGTP_LAUNCH(LMV, true, false, true);              \
+            else if (Rtg) CGTP_LAUNCH(LMV, false, true, true);         \
             else CGTP_LAUNCH(LMV, false, false, true);                 \
         } else if (LMV < kMfmaRecvMinL) {                              \
             return hipErrorNotSupported;                               \
