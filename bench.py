@@ -256,8 +256,25 @@ def cpu_baseline(w, d, budget_s: float = 15.0, n_fixed: int = 0):
 
 # ---------------------------------------------------------------- one workload
 
+def set_order(plan, w, d, use_order: bool):
+    """Message passing: compute the receiver order of the workload's graph on the host
+    (cgtp_receiver_order, once per graph, before any timed step) and set it on the plan.
+    Returns (kind, host ms) for the bench line."""
+    import paper_2605_15073_amd as cg
+
+    if w.kind not in ("mp", "mp_fields"):
+        return None, None
+    if not use_order:
+        return "identity", None
+    t0 = time.perf_counter()
+    o = cg.receiver_order(d["row_ptr"], d["col"], d.get("edge_unit"))
+    ms = 1e3 * (time.perf_counter() - t0)
+    cg.set_receiver_order(plan, o)
+    return ("hilbert" if d.get("edge_unit") is not None else "breadth_first"), ms
+
+
 def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=False,
-                   cpu_budget: float = 15.0):
+                   cpu_budget: float = 15.0, use_order: bool = True):
     import torch
 
     import paper_2605_15073_amd as cg
@@ -275,6 +292,7 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
         plan = cg.plan_create(w.lmax, w.C, w.R, flags=cg.CGTP_TIME_STAGES)
     torch.cuda.synchronize()
     plan_ms = 1e3 * (time.perf_counter() - t_plan)  # tables built and uploaded, outside every step
+    order_kind, order_ms = set_order(plan, w, d, use_order)
     if w.kind == "nbody":
         import numpy as np
 
@@ -412,6 +430,8 @@ def bench_workload(w, steps: int, warmup: int, with_cpu: bool, d=None, quiet=Fal
                    + ("_general" if w.general else "_two_slot" if w.two_slot else ""),
                    "nodes": w.n, "edges": E, "lmax": w.lmax, "channels": w.C, "rank": w.R,
                    "grid": f"{U}x{V}", "seed": w.seed},
+        "receiver_order": order_kind,
+        "receiver_order_host_ms": order_ms,
         "stages_ms": {k: round(v, 4) for k, v in stage_avg.items()},
         "dominant_kernel": dom,
     }
@@ -577,6 +597,9 @@ def main():
     ap.add_argument("--gather-ceiling", action="store_true",
                     help="run only the receiver's read-pattern probe (cgtp_gather_probe) on the "
                          "workload's neighbour list, 5 launches after 2 warm-up launches")
+    ap.add_argument("--no-receiver-order", action="store_true",
+                    help="message passing: run the receivers in node order instead of the "
+                         "locality order of cgtp_receiver_order")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="run only a plain device-to-device copy of this many bytes (3 times), "
                          "the calibration kernel for the HBM byte counters")
@@ -614,16 +637,18 @@ def main():
         d = w.make()
         t = to_dev(d, ("row_ptr", "col"))
         plan = cg.plan_create(w.lmax, w.C, w.R)
+        order_kind, _ = set_order(plan, w, d, not args.no_receiver_order)
         ceil = gather_ceiling(plan, w, t, int(d["n_edges"]))
         plan.close()
         print(json.dumps({"workload": w.name, "edges": int(d["n_edges"]),
-                          "gather_ceiling": ceil}), flush=True)
+                          "receiver_order": order_kind, "gather_ceiling": ceil}), flush=True)
         return
     if args.sweep_out:
         sweep(args.sweep_out, max(3, args.steps // 4), args.warmup)
         return
     w = WORKLOADS[args.workload]
-    rec = bench_workload(w, args.steps, args.warmup, with_cpu=not args.no_cpu_baseline)
+    rec = bench_workload(w, args.steps, args.warmup, with_cpu=not args.no_cpu_baseline,
+                         use_order=not args.no_receiver_order)
     print(json.dumps(rec), flush=True)
 
 

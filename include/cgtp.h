@@ -342,6 +342,33 @@ int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
                       const int32_t *col, const void *fields, size_t fields_bytes, void *sink,
                       void *stream);
 
+/* Scheduling aid, not an operation of the paper: the order in which the message-passing
+ * receivers run. The neighbour sum of a receiver (Eq. msgpass-S) is the same whatever order
+ * the receivers are processed in, so the outputs of every message-passing call are bitwise
+ * the same with or without an order; a locality-preserving one lets the receivers that run at
+ * the same time share their senders, whose grid fields then stay in the GPU's L2.
+ *
+ * cgtp_receiver_order (host only, no GPU needed) computes such an order for the CSR of a
+ * message-passing call: row_ptr[n_nodes + 1], col[n_edges] and edge_vec[n_edges][3] are HOST
+ * arrays, order[n_nodes] a host array it fills with a permutation of 0 .. n_nodes - 1.
+ * edge_vec is the edge direction of cgtp_message_pass (or the displacement vector); positions
+ * are rebuilt from it along a breadth-first spanning tree of each connected component, and
+ * the nodes sorted by component, then by the Hilbert index of the rebuilt position. edge_vec
+ * may be NULL (e.g. for cgtp_message_pass_fields): the order is then the breadth-first
+ * discovery order. Deterministic. Cost O(n_edges + n_nodes log n_nodes) on one host thread;
+ * compute it once per graph. Errors: CGTP_ERR_ARG (NULL, sizes), CGTP_ERR_CSR (row_ptr not
+ * non-decreasing from 0 to n_edges, or col out of range).
+ *
+ * cgtp_plan_set_receiver_order copies order[n_nodes] (a HOST array, checked to be a
+ * permutation) to device memory the plan owns; from then on every message-passing call and
+ * cgtp_gather_probe on the plan runs its receivers in that order and must pass exactly
+ * n_nodes nodes (CGTP_ERR_ARG otherwise). order NULL or n_nodes 0 clears it (the identity).
+ * Synchronises the device. Errors: CGTP_ERR_ARG (NULL plan, not a permutation, wrong
+ * device), CGTP_ERR_HIP (allocation or copy). */
+int cgtp_receiver_order(int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,
+                        const int32_t *col, const float *edge_vec, int32_t *order);
+int cgtp_plan_set_receiver_order(cgtp_plan plan, int64_t n_nodes, const int32_t *order);
+
 /* Release the plan and everything it owns. Synchronises the device first.
  * cgtp_destroy(NULL) is a no-op. */
 int cgtp_destroy(cgtp_plan plan);

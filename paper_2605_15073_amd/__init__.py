@@ -11,6 +11,8 @@ from __future__ import annotations
 import ctypes
 import os
 
+import numpy as np
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libcgtp.so")
 
@@ -40,7 +42,8 @@ EXPORTED = ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_
             "cgtp_onsite_general", "cgtp_message_pass_general", "cgtp_message_pass_fields",
             "cgtp_workspace_bytes_nbody", "cgtp_onsite_nbody", "cgtp_stage_times",
             "cgtp_destroy", "cgtp_status_string", "cgtp_last_error", "cgtp_host_tables",
-            "cgtp_onsite_noalloc", "cgtp_gather_probe")
+            "cgtp_onsite_noalloc", "cgtp_gather_probe", "cgtp_receiver_order",
+            "cgtp_plan_set_receiver_order")
 CGTP_NOALLOC_SCRATCH_BYTES = 64 << 20
 ONSITE_STAGES = ("contract_operands", "grid_product_curl_analysis", "project")
 ONSITE_GENERAL_STAGES = ("contract_a", "contract_b", "grid_product_curl_analysis",
@@ -100,10 +103,13 @@ def load_library(path: str = LIB_PATH):
     lib.cgtp_last_error.argtypes = []
     lib.cgtp_last_error.restype = ctypes.c_char_p
     lib.cgtp_host_tables.argtypes = [i32, i32, i32] + [vp] * 5
+    lib.cgtp_receiver_order.argtypes = [i64, i64, vp, vp, vp, vp]
+    lib.cgtp_plan_set_receiver_order.argtypes = [vp, i64, vp]
     for name in ("cgtp_plan_create", "cgtp_plan_grid", "cgtp_workspace_bytes", "cgtp_onsite",
                  "cgtp_onsite_noalloc", "cgtp_gather_probe",
                  "cgtp_message_pass", "cgtp_message_pass_two_slot", "cgtp_stage_times",
-                 "cgtp_destroy", "cgtp_host_tables"):
+                 "cgtp_destroy", "cgtp_host_tables", "cgtp_receiver_order",
+                 "cgtp_plan_set_receiver_order"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib
@@ -254,6 +260,44 @@ def onsite_noalloc(plan: Plan, A, B, U_A, U_B, U_out_even, U_out_odd, out_even, 
                                               _stream_handle(stream)),
            "cgtp_onsite_noalloc")
     return outs[0], outs[1]
+
+
+def _host(a, dtype):
+    """A contiguous numpy array of dtype on the host (from numpy or a torch tensor)."""
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().numpy()
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def receiver_order(row_ptr, col, edge_vec=None):
+    """cgtp_receiver_order on the host: a locality-preserving permutation of the receivers
+    of the CSR (row_ptr [N+1], col [E]), from the edge vectors [E, 3] if given, else the
+    breadth-first order. Returns an int32 numpy array [N]."""
+    rp = _host(row_ptr, np.int32)
+    cl = _host(col, np.int32)
+    N, E = rp.shape[0] - 1, cl.shape[0]
+    ev = None if edge_vec is None else _host(edge_vec, np.float32)
+    if ev is not None and ev.shape != (E, 3):
+        raise ValueError(f"edge_vec: expected shape ({E}, 3), got {ev.shape}")
+    out = np.empty(N, dtype=np.int32)
+    vp = ctypes.c_void_p
+    _check(load_library().cgtp_receiver_order(
+        N, E, vp(rp.ctypes.data), vp(cl.ctypes.data),
+        None if ev is None else vp(ev.ctypes.data), vp(out.ctypes.data)), "cgtp_receiver_order")
+    return out
+
+
+def set_receiver_order(plan: Plan, order=None) -> None:
+    """cgtp_plan_set_receiver_order: run the plan's message-passing receivers in this order
+    (a permutation of the N nodes; None restores the identity)."""
+    lib = load_library()
+    if order is None:
+        _check(lib.cgtp_plan_set_receiver_order(plan.handle, 0, None),
+               "cgtp_plan_set_receiver_order")
+        return
+    o = _host(order, np.int32)
+    _check(lib.cgtp_plan_set_receiver_order(plan.handle, o.shape[0], ctypes.c_void_p(o.ctypes.data)),
+           "cgtp_plan_set_receiver_order")
 
 
 def gather_probe(plan: Plan, row_ptr, col, fields, sink, stream=None):

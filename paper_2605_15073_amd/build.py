@@ -11,9 +11,12 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libcgtp.so")
-SOURCES = ["plan.cpp", "tables.cpp", "contract.hip", "kernels.hip", "onsite.hip", "receiver_mfma.hip", "folded.hip",
+SOURCES = ["plan.cpp", "tables.cpp", "order.cpp", "contract.hip", "kernels.hip", "onsite.hip", "receiver_mfma.hip", "folded.hip",
            "fourier_mfma.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+# Per-source flags. The receiver's matrix-core results feed vector ALU products at once:
+# accumulating them in VGPRs (not AccVGPRs) saves a copy per result element and registers.
+SOURCE_FLAGS = {"receiver_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 # Packed fp32 VALU ops are disabled for all device code.
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -28,7 +31,7 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(src_obj):
         src, obj = src_obj
-        cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC, *FLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)

@@ -542,15 +542,17 @@ constexpr unsigned kFieldsOutside = 0x80000000u;
 // edge). Both are buffer loads whose per-lane byte offsets are fixed over the CSR row and
 // computed once (rows and columns past the block read 0 from past the resource); only the
 // wave-uniform resources change per edge. The products accumulate in registers over the CSR row; the sums go to
-// S [N][R][2][UVs] for k_analysis_mfma. Blocks run rank block by rank block, all receivers
-// inside one, so the memory-side cache serves a rank slice of the sender fields.
+// S [N][R][2][UVs] for k_analysis_mfma. Blocks run in the receiver block order (recv_block),
+// rank block by rank block.
 // SPLIT: the value field comes from the rows HE (Gaunt factors) and the two derivative
 // fields from the rows HEc (curl factors); both row sets are staged and the Legendre pass
 // runs over both.
 template <int LM, bool SPLIT>
 __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, int R, int rb,
+                                                              int64_t N,
                                                               const int32_t *__restrict__ row_ptr,
                                                               const int32_t *__restrict__ col,
+                                                              const int32_t *__restrict__ order,
                                                               const float *__restrict__ HE,
                                                               const float *__restrict__ HEc,
                                                               const float *__restrict__ SF,
@@ -563,11 +565,9 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
     float4_t *cf = reinterpret_cast<float4_t *>(smem);  // [P] recurrence coefficients
     float *qs = smem + 4 * G::P;                         // [4 KM][QB]: q_vm as [m][v]
     float *Hs = qs + 4 * G::KM * G::QB;                  // [2][NS][rb][HR] this / the next edge
-    const int nrb = (R + rb - 1) / rb;
-    const int64_t NN = (int64_t)gridDim.x / nrb;
-    const int cb = (int)(blockIdx.x / NN);
-    const int64_t i = blockIdx.x - (int64_t)cb * NN;
-    const int r0 = cb * rb;
+    int64_t slice, i;
+    if (!recv_block(N, order, slice, i)) return;
+    const int r0 = (int)slice * rb;
     const int nr = (R - r0 < rb) ? (R - r0) : rb;
     const int nh = nr * G::HR;          // staged elements of one row set
     const int hset = rb * G::HR;        // LDS stride of a row set
@@ -1138,8 +1138,8 @@ hipError_t launch_sender_mfma(const Tabs<float> &tb, int64_t B, int R, const flo
 
 template <int LM>
 hipError_t receiver_fields_lm(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
-                              const int32_t *col, const float *HE, const float *HEc,
-                              const float *SF, float *S, hipStream_t s)
+                              const int32_t *col, const int32_t *order, const float *HE,
+                              const float *HEc, const float *SF, float *S, hipStream_t s)
 {
     using G = Grid<LM>;
     const int ns = HEc ? 2 : 1;
@@ -1155,28 +1155,31 @@ hipError_t receiver_fields_lm(const Tabs<float> &tb, int64_t N, int R, const int
     const size_t sh = sizeof(float) * (4 * (size_t)G::P + 4 * (size_t)G::KM * G::QB +
                                        2 * (size_t)ns * rb * G::HR);
     if (sh > (size_t)tb.d.lds_max) return hipErrorNotSupported;
-    const int64_t blocks = N * ((R + rb - 1) / rb);
+    const int64_t blocks = recv_blocks(N, (R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     if (HEc)
         hipLaunchKernelGGL((k_receiver_fields_mfma<LM, true>), dim3((unsigned)blocks),
-                           dim3(64 * waves), sh, s, tb, R, rb, row_ptr, col, HE, HEc, SF, S);
+                           dim3(64 * waves), sh, s, tb, R, rb, N, row_ptr, col, order, HE, HEc,
+                           SF, S);
     else
         hipLaunchKernelGGL((k_receiver_fields_mfma<LM, false>), dim3((unsigned)blocks),
-                           dim3(64 * waves), sh, s, tb, R, rb, row_ptr, col, HE, HEc, SF, S);
+                           dim3(64 * waves), sh, s, tb, R, rb, N, row_ptr, col, order, HE, HEc,
+                           SF, S);
     return hipGetLastError();
 }
 
 hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const int32_t *row_ptr, const int32_t *col,
-                                       const float *HE, const float *HEc, const float *SF,
-                                       float *S, float *Ta, float *Tb, hipStream_t s, bool analyse)
+                                       const int32_t *order, const float *HE, const float *HEc,
+                                       const float *SF, float *S, float *Ta, float *Tb,
+                                       hipStream_t s, bool analyse)
 {
     if (N == 0) return hipSuccess;
     if (!sender_mfma_supported(tb.d)) return hipErrorNotSupported;
     hipError_t e = hipErrorNotSupported;
     switch (tb.d.lmax) {
 #define CGTP_CASE(LMV) \
-    case LMV: e = receiver_fields_lm<LMV>(tb, N, R, row_ptr, col, HE, HEc, SF, S, s); break;
+    case LMV: e = receiver_fields_lm<LMV>(tb, N, R, row_ptr, col, order, HE, HEc, SF, S, s); break;
         CGTP_LMAX_CASES(CGTP_CASE)
 #undef CGTP_CASE
     default: return hipErrorNotSupported;

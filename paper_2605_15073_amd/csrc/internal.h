@@ -155,9 +155,37 @@ hipError_t launch_onsite_folded(const Tabs<float> &tb, int64_t B, int R, const f
 // tables and coefficients within a workgroup's LDS.
 bool onsite_split_supported(const Dims &d);
 
+// Block order of the receiver passes. Their work is split into slices (a rank block, and a
+// chunk of grid points where a pass has them) times receivers. Slices run one after another
+// and inside a slice all receivers, so blocks in flight read one slice of the sender fields.
+// The hardware hands the blocks of a launch to the kXcds XCDs in turn (block b to XCD
+// b mod kXcds); here XCD x takes the x-th of kXcds contiguous spans of the receiver sequence of
+// each slice. order[pos] gives the receiver at sequence position pos (NULL: the identity);
+// under a locality-preserving order (cgtp_receiver_order) the receivers one XCD runs at once
+// are close in space, share most of their senders, and those senders' fields stay in that
+// XCD's L2 instead of being fetched again for every edge.
+constexpr int kXcds = 8;
+__host__ __device__ inline int64_t recv_span(int64_t N) { return (N + kXcds - 1) / kXcds; }
+// Blocks of a receiver launch with `slices` slices (at most kXcds - 1 idle per slice).
+inline int64_t recv_blocks(int64_t N, int64_t slices) { return kXcds * recv_span(N) * slices; }
+// This block's slice and receiver; false for the idle blocks past the last receiver.
+__device__ inline bool recv_block(int64_t N, const int32_t *order, int64_t &slice, int64_t &i)
+{
+    const int64_t m = recv_span(N);
+    const int64_t b = blockIdx.x;
+    const int64_t k = b / kXcds;
+    slice = k / m;
+    const int64_t pos = (b - k * kXcds) * m + (k - slice * m);
+    if (pos >= N) return false;
+    i = order ? (int64_t)order[pos] : pos;
+    return true;
+}
+
 // Message-passing receiver pass: per receiver, synthesise the edge fields, multiply
 // with the streamed sender fields, sum over the CSR row, then the inverse transforms.
 // Rt is the edge-radial contraction in the layout [E][L][R].
+// order: the receiver sequence of the block order above (NULL: the identity); every
+// receiver pass below takes it.
 // Rtg: NULL, or separate edge coefficients of the curl product (same layout; zonal edge
 // field, one node slot).
 // SFf: NULL, or the sender fields of the parity-flipped node slot (two-slot message
@@ -168,8 +196,9 @@ bool onsite_split_supported(const Dims &d);
 // SFf) and the MFMA analysis follows; NULL: the analysis runs inside the receiver.
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
-                           const int32_t *row_ptr, const int32_t *col, const T *unit,
-                           const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
+                           const int32_t *row_ptr, const int32_t *col, const int32_t *order,
+                           const T *unit, const T *Rt, const T *Rtg, const T *SF, const T *SFf,
+                           T *Ta, T *Tb,
                            hipStream_t s, bool values_only = false, T *Sg = nullptr,
                            bool analyse = true);
 
@@ -180,8 +209,8 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
 // hipErrorNotSupported when the LDS staging does not fit (fp64 at the highest degrees).
 template <typename T>
 hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int32_t *row_ptr,
-                                  const int32_t *col, const T *HE, const T *SF, T *Ta, T *Tb,
-                                  hipStream_t s);
+                                  const int32_t *col, const int32_t *order, const T *HE,
+                                  const T *SF, T *Ta, T *Tb, hipStream_t s);
 
 // fp32 edge-field receiver on MFMA (fourier_mfma.hip), default grid: the summed grid fields
 // go to S [N][R][2][UVs] and the inverse transforms into Ta, Tb follow. SF in the layout
@@ -190,9 +219,9 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
 // and gives the value field, HEc the two derivative fields).
 hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const int32_t *row_ptr, const int32_t *col,
-                                       const float *HE, const float *HEc, const float *SF,
-                                       float *S, float *Ta, float *Tb, hipStream_t s,
-                                       bool analyse = true);
+                                       const int32_t *order, const float *HE, const float *HEc,
+                                       const float *SF, float *S, float *Ta, float *Tb,
+                                       hipStream_t s, bool analyse = true);
 
 // nu-body on-site grid product (kernels.hip): Tout[b][r][K] = the analysis of the pointwise
 // product of the nu fields synthesised from H.h[t][b][r][K]. The grid of tb must be fine
@@ -251,10 +280,10 @@ size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R, int planes);
 // values_only (not with Rtg; default grid): the moved-derivative curl, reading only the value
 // plane of SF (and SFf); every lmax. Otherwise lmax >= kMfmaRecvMinL.
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
-                                const int32_t *col, const float *unit, const float *Rt,
-                                const float *Rtg, const float *SF, const float *SFf,
-                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s,
-                                bool values_only = false, bool analyse = true);
+                                const int32_t *col, const int32_t *order, const float *unit,
+                                const float *Rt, const float *Rtg, const float *SF,
+                                const float *SFf, bool sf_chunked, float *S, float *Ta, float *Tb,
+                                hipStream_t s, bool values_only = false, bool analyse = true);
 // The inverse transforms of the summed grid fields S of a receiver (analyse = false above)
 // into Ta, Tb: mode as launch_analysis_mfma; mode 0 also off the default grid.
 hipError_t launch_summed_analysis(const Tabs<float> &tb, int64_t N, int R, const float *S,
@@ -266,12 +295,13 @@ hipError_t launch_summed_analysis(const Tabs<float> &tb, int64_t N, int R, const
 // arithmetic. hipErrorNotSupported for grids of
 // more than 1024 points.
 hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
-                               const int32_t *col, const float *SF, float *sink, hipStream_t s);
+                               const int32_t *col, const int32_t *order, const float *SF,
+                               float *sink, hipStream_t s);
 // The same for the MFMA receiver in its values-only form on the plain sender layout
 // (receiver_mfma.hip): its blocks, block order and 16-byte value-plane loads.
 hipError_t launch_gather_probe_mfma(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
-                                    const int32_t *col, const float *SF, float *sink,
-                                    hipStream_t s);
+                                    const int32_t *col, const int32_t *order, const float *SF,
+                                    float *sink, hipStream_t s);
 
 // Status reporting shared by the entry points of every source file: report() stores the
 // detail message returned by cgtp_last_error() on this thread and passes the status through.

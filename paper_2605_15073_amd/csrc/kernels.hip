@@ -471,7 +471,8 @@ __device__ __forceinline__ double buf_load<double>(__amdgpu_buffer_rsrc_t rs, un
 // sums B dA/dx, B dA/dphi of the edge field's derivatives.
 template <typename T, int RB, int NPT, bool FULL, bool TWO, bool SPLIT, bool VAL>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
-    Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    Tabs<T> tb, int R, int64_t N, const int32_t *__restrict__ row_ptr,
+    const int32_t *__restrict__ col, const int32_t *__restrict__ order,
     const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ Rtg,
     const T *__restrict__ SF, const T *__restrict__ SFf, T *__restrict__ Ta, T *__restrict__ Tb,
     T *__restrict__ Sg)
@@ -480,13 +481,9 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
     T *smem = reinterpret_cast<T *>(smem_raw);
     const Dims &d = tb.d;
     const int UV = d.UV, L = d.L, lmax = d.lmax;
-    const int nrb = (R + RB - 1) / RB;
-    // Block order: rank blocks in turn, and inside one, all receivers. Blocks in flight then
-    // read the same rank slice of the sender fields, which the memory-side cache keeps
-    // across receivers.
-    const int64_t NN = (int64_t)gridDim.x / nrb;
-    const int64_t c = blockIdx.x / NN;
-    const int64_t i = blockIdx.x - c * NN;
+    // Block order (recv_block): the slices are the rank blocks.
+    int64_t c, i;
+    if (!recv_block(N, order, c, i)) return;
     const int r0 = (int)c * RB;
     // FULL: R is a multiple of RB, so every rank of the block exists (no guards)
     const int nr = FULL ? RB : ((R - r0 < RB) ? (R - r0) : RB);
@@ -729,13 +726,12 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_zonal(
 // which keeps every load live.
 template <int RB>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_gather_probe(
-    int UV, int UVs, int R, const int32_t *__restrict__ row_ptr,
-    const int32_t *__restrict__ col, const float *__restrict__ SF, float *__restrict__ sink)
+    int UV, int UVs, int R, int64_t N, const int32_t *__restrict__ row_ptr,
+    const int32_t *__restrict__ col, const int32_t *__restrict__ order,
+    const float *__restrict__ SF, float *__restrict__ sink)
 {
-    const int nrb = (R + RB - 1) / RB;
-    const int64_t NN = (int64_t)gridDim.x / nrb;
-    const int64_t c = blockIdx.x / NN;
-    const int64_t i = blockIdx.x - c * NN;
+    int64_t c, i;
+    if (!recv_block(N, order, c, i)) return;
     const int r0 = (int)c * RB;
     const int nr = (R - r0 < RB) ? (R - r0) : RB;
     const int uv = threadIdx.x;
@@ -756,21 +752,23 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_gather_probe(
 }
 
 hipError_t launch_gather_probe(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
-                               const int32_t *col, const float *SF, float *sink, hipStream_t s)
+                               const int32_t *col, const int32_t *order, const float *SF,
+                               float *sink, hipStream_t s)
 {
     // the rank block of the fp32 value-only receiver at one point per thread: 16 ranks when
     // they divide R, else 8
     if (d.UV > kRecvMaxThreads) return hipErrorNotSupported;
     const int threads = (d.UV + 63) / 64 * 64;
     const int rb = R % 16 == 0 ? 16 : 8;
-    const int64_t nb = N * ((R + rb - 1) / rb);
-    if (nb == 0) return hipSuccess;
+    if (N == 0 || R == 0) return hipSuccess;
+    const int64_t nb = recv_blocks(N, (R + rb - 1) / rb);
+    if (nb > 0x7fffffffLL) return hipErrorInvalidValue;
     if (rb == 16)
         hipLaunchKernelGGL(k_gather_probe<16>, dim3((unsigned)nb), dim3(threads), 0, s, d.UV,
-                           d.UVs, R, row_ptr, col, SF, sink);
+                           d.UVs, R, N, row_ptr, col, order, SF, sink);
     else
         hipLaunchKernelGGL(k_gather_probe<8>, dim3((unsigned)nb), dim3(threads), 0, s, d.UV,
-                           d.UVs, R, row_ptr, col, SF, sink);
+                           d.UVs, R, N, row_ptr, col, order, SF, sink);
     return hipGetLastError();
 }
 
@@ -817,16 +815,19 @@ __device__ void edge_sh(const Tabs<T> &tb, T ux, T uy, T uz, T *Y)
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_receiver_separated(
-    Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    Tabs<T> tb, int R, int64_t N, const int32_t *__restrict__ row_ptr,
+    const int32_t *__restrict__ col, const int32_t *__restrict__ order,
     const T *__restrict__ unit, const T *__restrict__ Rt, const T *__restrict__ SF,
     T *__restrict__ Ta, T *__restrict__ Tb)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
     const Dims &d = tb.d;
-    const int64_t br = blockIdx.x;
-    const int64_t i = br / R;
-    const int r = (int)(br - i * R);
+    // Block order (recv_block): the slices are the ranks.
+    int64_t rr, i;
+    if (!recv_block(N, order, rr, i)) return;
+    const int r = (int)rr;
+    const int64_t br = i * R + r;
     const int MU = d.M * d.U;
     T *qs = smem;
     T *Sa = qs + d.V * d.M;
@@ -878,17 +879,16 @@ constexpr int kFieldsKpt = 8;  // staged coefficients per thread and edge, at mo
 
 template <typename T, int RB, int NPT, bool FULL, bool LT>
 __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_fields(
-    Tabs<T> tb, int R, const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+    Tabs<T> tb, int R, int64_t N, const int32_t *__restrict__ row_ptr,
+    const int32_t *__restrict__ col, const int32_t *__restrict__ order,
     const T *__restrict__ HE, const T *__restrict__ SF, T *__restrict__ Ta, T *__restrict__ Tb)
 {
     extern __shared__ unsigned char smem_raw[];
     T *smem = reinterpret_cast<T *>(smem_raw);
     const Dims &d = tb.d;
     const int UV = d.UV, UVs = d.UVs, K = d.K, MU = d.M * d.U, lmax = d.lmax, P = d.P;
-    const int nrb = (R + RB - 1) / RB;
-    const int64_t NN = (int64_t)gridDim.x / nrb;
-    const int64_t c = blockIdx.x / NN;
-    const int64_t i = blockIdx.x - c * NN;
+    int64_t c, i;
+    if (!recv_block(N, order, c, i)) return;
     const int r0 = (int)c * RB;
     const int nr = FULL ? RB : ((R - r0 < RB) ? (R - r0) : RB);
     const int nk = nr * K;  // staged coefficients of one edge
@@ -1024,8 +1024,8 @@ __global__ __launch_bounds__(kRecvMaxThreads) void k_receiver_fields(
 
 template <typename T>
 hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int32_t *row_ptr,
-                                  const int32_t *col, const T *HE, const T *SF, T *Ta, T *Tb,
-                                  hipStream_t s)
+                                  const int32_t *col, const int32_t *order, const T *HE,
+                                  const T *SF, T *Ta, T *Tb, hipStream_t s)
 {
     if (N == 0 || R == 0) return hipSuccess;
     const Dims &d = tb.d;
@@ -1057,18 +1057,18 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
         }
     }
     if (rb == 0) return hipErrorNotSupported;
-    const int64_t blocks = N * ((R + rb - 1) / rb);
+    const int64_t blocks = recv_blocks(N, (R + rb - 1) / rb);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
 #define CGTP_FIELDS(RBV, NP, LTV)                                                              \
     do {                                                                                       \
         if (R % RBV == 0)                                                                      \
             hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, true, LTV>),                     \
-                               dim3((unsigned)blocks), dim3(threads), sh, s, tb, R, row_ptr,   \
-                               col, HE, SF, Ta, Tb);                                           \
+                               dim3((unsigned)blocks), dim3(threads), sh, s, tb, R, N,         \
+                               row_ptr, col, order, HE, SF, Ta, Tb);                           \
         else                                                                                   \
             hipLaunchKernelGGL((k_receiver_fields<T, RBV, NP, false, LTV>),                    \
-                               dim3((unsigned)blocks), dim3(threads), sh, s, tb, R, row_ptr,   \
-                               col, HE, SF, Ta, Tb);                                           \
+                               dim3((unsigned)blocks), dim3(threads), sh, s, tb, R, N,         \
+                               row_ptr, col, order, HE, SF, Ta, Tb);                           \
     } while (0)
 #define CGTP_FIELDS_LT(RBV, NP)                          \
     do {                                                 \
@@ -1090,12 +1090,13 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
 
 template <typename T>
 hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
-                           const int32_t *row_ptr, const int32_t *col, const T *unit,
-                           const T *Rt, const T *Rtg, const T *SF, const T *SFf, T *Ta, T *Tb,
-                           hipStream_t s, bool values_only, T *Sg, bool analyse)
+                           const int32_t *row_ptr, const int32_t *col, const int32_t *order,
+                           const T *unit, const T *Rt, const T *Rtg, const T *SF, const T *SFf,
+                           T *Ta, T *Tb, hipStream_t s, bool values_only, T *Sg, bool analyse)
 {
-    int64_t blocks = N * R;
-    if (blocks == 0) return hipSuccess;
+    if (N == 0 || R == 0) return hipSuccess;
+    const int64_t blocks = recv_blocks(N, R);
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     const Dims &d = tb.d;
     if (SFf && Rtg) return hipErrorNotSupported;
     if (values_only && separated) return hipErrorInvalidValue;
@@ -1104,7 +1105,7 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
         if (SFf || Rtg) return hipErrorNotSupported;
         size_t sh = sizeof(T) * (d.V * d.M + 2 * d.UV + d.K + 2 * d.M * d.U);
         hipLaunchKernelGGL(k_receiver_separated<T>, dim3((unsigned)blocks), dim3(kThreads), sh, s,
-                           tb, R, row_ptr, col, unit, Rt, SF, Ta, Tb);
+                           tb, R, N, row_ptr, col, order, unit, Rt, SF, Ta, Tb);
         return hipGetLastError();
     }
     // the analysis buffers: two grid fields and two Fourier row sets, three of each with
@@ -1117,18 +1118,19 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     // LDS: the analysis buffers, or (split) one chunk of staged edge coefficients if larger
 #define CGTP_RECV_TW(RBV, NP, TW, SP, VL)                                                      \
     do {                                                                                       \
-        int64_t nb = N * ((R + RBV - 1) / RBV);                                                \
+        const int64_t nb = recv_blocks(N, (R + RBV - 1) / RBV);                                \
+        if (nb > 0x7fffffffLL) return hipErrorInvalidValue;                                    \
         const size_t chunk = SP ? sizeof(T) * kRecvEdgeChunk * 2 * d.L * RBV : 0;              \
         const size_t shc = chunk > sh ? chunk : sh;                                            \
         if (shc > (size_t)d.lds_max) return hipErrorNotSupported;                              \
         if (R % RBV == 0)                                                                      \
             hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, true, TW, SP, VL>),               \
-                               dim3((unsigned)nb), dim3(threads), shc, s, tb, R, row_ptr, col, \
-                               unit, Rt, Rtg, SF, SFf, Ta, Tb, Sg);                            \
+                               dim3((unsigned)nb), dim3(threads), shc, s, tb, R, N, row_ptr,   \
+                               col, order, unit, Rt, Rtg, SF, SFf, Ta, Tb, Sg);                \
         else                                                                                   \
             hipLaunchKernelGGL((k_receiver_zonal<T, RBV, NP, false, TW, SP, VL>),              \
-                               dim3((unsigned)nb), dim3(threads), shc, s, tb, R, row_ptr, col, \
-                               unit, Rt, Rtg, SF, SFf, Ta, Tb, Sg);                            \
+                               dim3((unsigned)nb), dim3(threads), shc, s, tb, R, N, row_ptr,   \
+                               col, order, unit, Rt, Rtg, SF, SFf, Ta, Tb, Sg);                \
     } while (0)
 #define CGTP_RECV(RBV, NP)                                                  \
     do {                                                                    \
@@ -1162,12 +1164,12 @@ hipError_t launch_receiver(const Tabs<T> &tb, bool separated, int64_t N, int R,
     template hipError_t launch_onsite_grid<T>(const Tabs<T> &, int64_t, int, const T *,          \
                                               const T *, T *, T *, hipStream_t);                 \
     template hipError_t launch_receiver<T>(const Tabs<T> &, bool, int64_t, int, const int32_t *, \
-                                           const int32_t *, const T *, const T *, const T *,     \
-                                           const T *, const T *, T *, T *, hipStream_t, bool,    \
-                                           T *, bool);                                           \
+                                           const int32_t *, const int32_t *, const T *,          \
+                                           const T *, const T *, const T *, const T *, T *, T *, \
+                                           hipStream_t, bool, T *, bool);                        \
     template hipError_t launch_receiver_fields<T>(const Tabs<T> &, int64_t, int, const int32_t *, \
-                                                  const int32_t *, const T *, const T *, T *, T *, \
-                                                  hipStream_t);                                   \
+                                                  const int32_t *, const int32_t *, const T *,    \
+                                                  const T *, T *, T *, hipStream_t);              \
     template hipError_t launch_nbody_grid<T>(const Tabs<T> &, int64_t, int, int,                  \
                                              const NbodyOperands<T> &, T *, hipStream_t);
 

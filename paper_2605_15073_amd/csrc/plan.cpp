@@ -32,6 +32,8 @@ struct cgtp_plan_s {
     size_t timers_used;
     double stage_acc[kNumOps][kMaxStages];  // drained sums per op (CGTP_OP_*)
     int stage_calls[kNumOps];
+    int32_t *order;      // receiver sequence of the message-passing passes (plan-owned device
+    int64_t order_n;     // copy of cgtp_plan_set_receiver_order's), NULL: the identity
 };
 
 namespace {
@@ -236,6 +238,15 @@ void nbody_min_grid(int lmax, int nu, int *U, int *V)
     *U = (deg + 2) / 2;
     if (*U < 1) *U = 1;
     *V = deg + 1;
+}
+
+// A receiver order set on the plan must be for the call's node count.
+int check_order(const cgtp_plan_s *p, int64_t n_nodes)
+{
+    if (p->order && p->order_n != n_nodes)
+        return fail(CGTP_ERR_ARG, "the plan's receiver order is for %lld nodes, the call has %lld",
+                    (long long)p->order_n, (long long)n_nodes);
+    return CGTP_OK;
 }
 
 int check_device(const cgtp_plan_s *p)
@@ -482,18 +493,18 @@ int run_mp(cgtp_plan_s *p, int op, int64_t N, int64_t E, const int32_t *row_ptr,
         if constexpr (sizeof(T) == 4) {
             mfma = use_mfma_receiver(p, R);
             if (mfma) {
-                e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, (const float *)unit, Rt,
-                                               nullptr, SF, SFf, sf_chunked(p, R), Sg, Ta, Tb, s,
-                                               values_only, false);
+                e = cgtp::launch_receiver_mfma(tb, N, R, row_ptr, col, p->order,
+                                               (const float *)unit, Rt, nullptr, SF, SFf,
+                                               sf_chunked(p, R), Sg, Ta, Tb, s, values_only, false);
                 if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
                 amode = values_only ? (two ? 2 : 1) : 0;
             }
         }
         if (!mfma) {
             const bool hand_over = values_only && zonal_mfma_analysis(p, R, false);
-            e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, (const T *)unit, Rt,
-                                         nullptr, SF, SFf, Ta, Tb, s, values_only,
-                                         hand_over ? Sg : nullptr, false);
+            e = cgtp::launch_receiver<T>(tb, separated, N, R, row_ptr, col, p->order,
+                                         (const T *)unit, Rt, nullptr, SF, SFf, Ta, Tb, s,
+                                         values_only, hand_over ? Sg : nullptr, false);
             if (e != hipSuccess) return hip_fail(e, "receiver");
             if (hand_over) amode = two ? 2 : 1;
         }
@@ -816,18 +827,18 @@ int run_mp_groups(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     if constexpr (sizeof(T) == 4) {
         mfma = use_mfma_receiver(p, Rg, G.split);
         if (mfma) {
-            e = cgtp::launch_receiver_mfma(tb, N, Rg, row_ptr, col, (const float *)unit, Rt, Rtc,
-                                           SF, nullptr, sf_chunked(p, Rg, G.split), Sg, Ta, Tb, s,
-                                           values_only, false);
+            e = cgtp::launch_receiver_mfma(tb, N, Rg, row_ptr, col, p->order, (const float *)unit,
+                                           Rt, Rtc, SF, nullptr, sf_chunked(p, Rg, G.split), Sg, Ta,
+                                           Tb, s, values_only, false);
             if (e != hipSuccess) return hip_fail(e, "receiver (mfma)");
             amode = values_only ? 1 : 0;
         }
     }
     if (!mfma) {
         const bool hand_over = values_only && zonal_mfma_analysis(p, Rg, G.split);
-        e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, (const T *)unit, Rt, Rtc,
-                                     SF, nullptr, Ta, Tb, s, values_only, hand_over ? Sg : nullptr,
-                                     false);
+        e = cgtp::launch_receiver<T>(tb, separated, N, Rg, row_ptr, col, p->order,
+                                     (const T *)unit, Rt, Rtc, SF, nullptr, Ta, Tb, s, values_only,
+                                     hand_over ? Sg : nullptr, false);
         if (e != hipSuccess) return hip_fail(e, "receiver");
         if (hand_over) amode = 1;
     }
@@ -886,8 +897,8 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
         if (use_mfma_fields(p)) {
             // the receiver pass (stage 3), then the inverse transforms of its sums (stage 4)
             float *Sg = reinterpret_cast<float *>(ws + lay.off[5]);
-            e = cgtp::launch_receiver_fields_mfma(tb, N, Rg, row_ptr, col, HE, HEc, SF, Sg, Ta, Tb,
-                                                  s, false);
+            e = cgtp::launch_receiver_fields_mfma(tb, N, Rg, row_ptr, col, p->order, HE, HEc, SF,
+                                                  Sg, Ta, Tb, s, false);
             if (e != hipSuccess) return hip_fail(e, "receiver (edge field, mfma)");
             rec.mark();
             e = cgtp::launch_summed_analysis(tb, N, Rg, Sg, Ta, Tb, s, 0);
@@ -896,7 +907,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
             return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);
         }
     }
-    e = cgtp::launch_receiver_fields<T>(tb, N, Rg, row_ptr, col, HE, SF, Ta, Tb, s);
+    e = cgtp::launch_receiver_fields<T>(tb, N, Rg, row_ptr, col, p->order, HE, SF, Ta, Tb, s);
     if (e == hipErrorNotSupported)
         return fail(CGTP_ERR_UNSUPPORTED,
                     "edge-field receiver: a grid of %d points (at most 2048 off the fp32 default "
@@ -1090,6 +1101,8 @@ int cgtp_plan_create(const cgtp_desc *desc, cgtp_plan *plan)
     p->own_ws = nullptr;
     p->own_ws_bytes = 0;
     p->timers_used = 0;
+    p->order = nullptr;
+    p->order_n = 0;
     *plan = p;
     return CGTP_OK;
 }
@@ -1221,6 +1234,7 @@ int message_pass_impl(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
         return fail(CGTP_ERR_UNSUPPORTED,
                     "two node slots are built for the zonal edge field, not CGTP_EDGE_SEPARATED");
     int st = check_device(plan);
+    if (!st) st = check_order(plan, n_nodes);
     if (st) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (plan->flags & CGTP_VALIDATE_CSR) {
@@ -1361,6 +1375,7 @@ int cgtp_message_pass_general(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
     if (n_nodes * (int64_t)Rg > 0x7fffffffLL)
         return fail(CGTP_ERR_UNSUPPORTED, "n_nodes * total rank exceeds 2^31 - 1");
     int st = check_device(plan);
+    if (!st) st = check_order(plan, n_nodes);
     if (st) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (plan->flags & CGTP_VALIDATE_CSR) {
@@ -1417,6 +1432,7 @@ int cgtp_message_pass_fields(cgtp_plan plan, int64_t n_nodes, int64_t n_edges,
     if ((n_nodes > n_edges ? n_nodes : n_edges) * (int64_t)Rg > 0x7fffffffLL)
         return fail(CGTP_ERR_UNSUPPORTED, "rows * total rank exceeds 2^31 - 1");
     int st = check_device(plan);
+    if (!st) st = check_order(plan, n_nodes);
     if (st) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (plan->flags & CGTP_VALIDATE_CSR) {
@@ -1503,17 +1519,64 @@ int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
     if (fields_bytes < need)
         return fail(CGTP_ERR_ARG, "fields buffer of %zu bytes, %zu needed", fields_bytes, need);
     int st = check_device(plan);
+    if (!st) st = check_order(plan, n_nodes);
     if (st) return st;
     hipError_t e =
         mfma_plain ? cgtp::launch_gather_probe_mfma(plan->d, n_nodes, plan->R, row_ptr, col,
+                                                    plan->order,
                                                     static_cast<const float *>(fields),
                                                     static_cast<float *>(sink),
                                                     static_cast<hipStream_t>(stream))
                    : cgtp::launch_gather_probe(plan->d, n_nodes, plan->R, row_ptr, col,
-                                               static_cast<const float *>(fields),
+                                               plan->order, static_cast<const float *>(fields),
                                                static_cast<float *>(sink),
                                                static_cast<hipStream_t>(stream));
     return e == hipSuccess ? CGTP_OK : hip_fail(e, "gather probe");
+}
+
+int cgtp_plan_set_receiver_order(cgtp_plan plan, int64_t n_nodes, const int32_t *order)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(CGTP_ERR_ARG, "plan is NULL");
+    if (n_nodes < 0 || n_nodes >= 0x7fffffffLL) return fail(CGTP_ERR_ARG, "bad n_nodes");
+    int st = check_device(plan);
+    if (st) return st;
+    if (!order || n_nodes == 0) {  // back to the identity
+        if (plan->order) {
+            hipError_t e = hipDeviceSynchronize();  // calls in flight may still read it
+            (void)hipFree(plan->order);
+            plan->order = nullptr;
+            plan->order_n = 0;
+            if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+        }
+        return CGTP_OK;
+    }
+    std::vector<unsigned char> seen((size_t)n_nodes, 0);
+    for (int64_t k = 0; k < n_nodes; ++k) {
+        const int32_t v = order[k];
+        if (v < 0 || v >= n_nodes || seen[(size_t)v])
+            return fail(CGTP_ERR_ARG, "order is not a permutation of the %lld nodes (order[%lld] = %d)",
+                        (long long)n_nodes, (long long)k, v);
+        seen[(size_t)v] = 1;
+    }
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+    if (plan->order) {
+        (void)hipFree(plan->order);
+        plan->order = nullptr;
+        plan->order_n = 0;
+    }
+    int32_t *dev = nullptr;
+    e = hipMalloc(&dev, sizeof(int32_t) * (size_t)n_nodes);
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(receiver order)");
+    e = hipMemcpy(dev, order, sizeof(int32_t) * (size_t)n_nodes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(dev);
+        return hip_fail(e, "hipMemcpy(receiver order)");
+    }
+    plan->order = dev;
+    plan->order_n = n_nodes;
+    return CGTP_OK;
 }
 
 int cgtp_destroy(cgtp_plan plan)
@@ -1522,6 +1585,7 @@ int cgtp_destroy(cgtp_plan plan)
     hipError_t e = hipDeviceSynchronize();
     if (plan->own_ws) (void)hipFree(plan->own_ws);
     if (plan->tables) (void)hipFree(plan->tables);
+    if (plan->order) (void)hipFree(plan->order);
     for (EventSet &es : plan->timers)
         for (int i = 0; i <= kMaxStages; ++i) (void)hipEventDestroy(es.ev[i]);
     delete plan;

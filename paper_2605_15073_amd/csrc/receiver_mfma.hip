@@ -49,6 +49,15 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Waves per SIMD the register allocation of k_receiver_mfma aims at (values-only form): 4 with
+// one set of sums at lmax 3 to 7 (where it needs no spill), else 3, and 2 with six sums (two
+// node slots) or two coefficient sets above lmax 12 (which would spill at 3).
+template <bool VAL, bool TWO, bool SPLIT>
+constexpr int kRecvWaves(int lm)
+{
+    return !VAL ? 1 : TWO ? 2 : SPLIT ? (lm > 12 ? 2 : 3) : (lm >= 3 && lm <= 7 ? 4 : 3);
+}
+
 // LM is lmax: the recurrence is unrolled with compile-time coefficients. A workgroup
 // is WPB waves; each wave owns PW = 64 grid points, one per lane: per edge a lane runs
 // the Legendre recurrence for P_l and P_l' at its own point (both in the same lane) into
@@ -56,15 +65,18 @@ __device__ __forceinline__ void wave_sync()
 // [L x 16 ranks] edge coefficients on the matrix cores.
 // TWO: the senders carry a second, parity-flipped node slot SFf (same layout as SF); by
 // Table 1 its curl product then feeds S_alpha's slot (natural parity) and its Gaunt
-// product S_beta's. The next edge is prefetched only with one slot (registers).
+// product S_beta's. Its six sums keep it at 2 waves per SIMD.
 // SPLIT: the curl product's edge coefficients are Rtg (its own CP factors): the derivative
 // sum g multiplies P' with those, the value sum a P with Rt.
 // VAL: value planes only, moved-derivative curl (above). With SPLIT the senders carry the
 // Gaunt factors' values in plane 0 and the curl factors' in plane 1.
 template <int WPB, int LM, bool TWO, bool SPLIT, bool VAL>
-__global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
+__global__ __launch_bounds__(64 * WPB)
+__attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_receiver_mfma(Tabs<float> tb, int R, int nchunks,
+                                                            int64_t N,
                                                             const int32_t *__restrict__ row_ptr,
                                                             const int32_t *__restrict__ col,
+                                                            const int32_t *__restrict__ order,
                                                             const float *__restrict__ unit,
                                                             const float *__restrict__ Rt,
                                                             const float *__restrict__ Rtg,
@@ -91,12 +103,10 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     float *dxs = Dl + 4 * KS * RS;      // [PW]
     float *dps = dxs + PW;              // [PW]
 
-    // Block order: (rank tile, point chunk) slices run one after another, and inside a slice
-    // all receivers. Blocks in flight then read one slice of the sender fields, which the
-    // memory-side cache keeps across receivers.
-    const int64_t NN = (int64_t)gridDim.x / ((int64_t)(R / kRT) * nchunks);
-    const int rest = (int)(blockIdx.x / NN);
-    const int64_t i = blockIdx.x - (int64_t)rest * NN;
+    // Block order (recv_block): the slices are (rank tile, point chunk) pairs.
+    int64_t slice, i;
+    if (!recv_block(N, order, slice, i)) return;
+    const int rest = (int)slice;
     const int r0 = (rest / nchunks) * kRT;
     const int pw0 = (rest % nchunks) * PC + wave * PW;  // first point of this wave
     // a wave wholly past the grid (the padding of the last chunk, e.g. at lmax 7, 12, 14, 18)
@@ -130,16 +140,13 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     const int fstride = sf_nc ? kSfChunk : UVs;  // field stride, elements
     const unsigned voff = sf_nc ? (unsigned)((n * 3 * kSfChunk + 4 * g) * 4)
                                 : (unsigned)((n * 3 * UVs + pw0 + 4 * g) * 4);
-    const int64_t sfo = sf_nc ? ((int64_t)(r0 / kRT) * sf_nc + pw0 / kSfChunk) * NN * (kRT * 3 * kSfChunk)
+    const int64_t sfo = sf_nc ? ((int64_t)(r0 / kRT) * sf_nc + pw0 / kSfChunk) * N * (kRT * 3 * kSfChunk)
                               : (int64_t)r0 * 3 * UVs;
     const float *sfb = SF + sfo;
     const float *sfbf = (TWO ? SFf : SF) + sfo;
     const int64_t jstride = sf_nc ? (int64_t)kRT * 3 * kSfChunk : (int64_t)R * 3 * UVs;
     const unsigned sfbytes = (unsigned)(kRT * 3 * fstride * 4);
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
-    // sender fields of edge e (cur) and e + 1 (nxt): the next edge's loads are in flight
-    // while this one is computed
-    float4_t cI[TPW], cX[TPW], cP[TPW];
     // lanes whose 4 points all lie past the grid (the padding of the last chunk: up to 18% of
     // the points at lmax 7-8) load through an offset past the resource, which returns zeros
     // without a memory request (2^31: past the resource with or without the scalar offsets
@@ -147,8 +154,29 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
     unsigned vofft[TPW];
 #pragma unroll
     for (int t = 0; t < TPW; ++t) vofft[t] = pw0 + 16 * t + 4 * g < UV ? voff : 0x80000000u;
-    auto load_fields = [&](const float *base, int e, float4_t *fI, float4_t *fX, float4_t *fP) {
-        const int64_t j = __builtin_amdgcn_readfirstlane(col[e]);
+    // Edge data in batches of 64 edges: lane k holds the sender index and the normalised
+    // direction of edge eb + k, read out per edge with readlane, so no per-edge load of them
+    // sits on the critical path.
+    int colv = 0;
+    float uxv = 0.f, uyv = 0.f, uzv = 1.f;
+    auto load_batch = [&](int eb) {
+        const int e = eb + lane;
+        if (e < e1) {
+            colv = col[e];
+            const float x = unit[3 * (int64_t)e], y = unit[3 * (int64_t)e + 1],
+                        z = unit[3 * (int64_t)e + 2];
+            // renormalised by the hardware reciprocal square root (within 1 ulp)
+            const float inv = __builtin_amdgcn_rsqf(x * x + y * y + z * z);
+            uxv = x * inv;
+            uyv = y * inv;
+            uzv = z * inv;
+        }
+    };
+    auto lane_f = [](float v, int k) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), k));
+    };
+    auto load_fields = [&](const float *base, int k, float4_t *fI, float4_t *fX, float4_t *fP) {
+        const int64_t j = __builtin_amdgcn_readlane(colv, k);
         const __amdgpu_buffer_rsrc_t sfr = rsrc(base + j * jstride, sfbytes);
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
@@ -158,35 +186,47 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
             if (!VAL) fP[t] = bload4(sfr, vofft[t], so + 2 * fstride * 4);
         }
     };
-    if (!TWO && e0 < e1) load_fields(sfb, e0, cI, cX, cP);
-    for (int e = e0; e < e1; ++e) {
-        float4_t fI[TPW], fX[TPW], fP[TPW], hI[TPW], hX[TPW], hP[TPW];
-        if (TWO) {
-            load_fields(sfb, e, fI, fX, fP);
-            load_fields(sfbf, e, hI, hX, hP);
-        } else {
-#pragma unroll
-            for (int t = 0; t < TPW; ++t) {
-                fI[t] = cI[t];
-                if (!VAL || SPLIT) fX[t] = cX[t];
-                if (!VAL) fP[t] = cP[t];
-            }
-            if (e + 1 < e1) load_fields(sfb, e + 1, cI, cX, cP);
-        }
-        float ux = unit[3 * (int64_t)e], uy = unit[3 * (int64_t)e + 1], uz = unit[3 * (int64_t)e + 2];
-        const float inv = 1.f / sqrtf(ux * ux + uy * uy + uz * uz);
-        ux *= inv;
-        uy *= inv;
-        uz *= inv;
-        // B operand: Rt[e][4 kk + g][r0 + n]
+    // B operand: Rt[e][4 kk + g][r0 + n] (and Rtg's with SPLIT)
+    auto load_b = [&](int e, float *bv, float *bg) {
         const float *rte = Rt + (int64_t)e * L * R + r0 + n;
         const float *rtg = SPLIT ? Rtg + (int64_t)e * L * R + r0 + n : rte;
-        float Bv[KS], Bg[KS];
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
             const int l = 4 * kk + g;
-            Bv[kk] = l <= LM ? rte[l * R] : 0.f;
-            Bg[kk] = SPLIT ? (l <= LM ? rtg[l * R] : 0.f) : Bv[kk];
+            bv[kk] = l <= LM ? rte[l * R] : 0.f;
+            if (SPLIT) bg[kk] = l <= LM ? rtg[l * R] : 0.f;
+        }
+    };
+    // A wave loads an edge's sender fields when the edge starts and hides their latency behind
+    // the other waves of its SIMD: prefetching them an edge ahead would take the registers of
+    // a wave (4 waves per SIMD in the values-only form at low degrees, 3 with the prefetch,
+    // which measured slower). At low degrees (PRE_B) the next edge's B operand, a few
+    // registers, is loaded one edge ahead.
+    constexpr bool PRE_B = KS <= 2 && !TWO && !SPLIT;
+    float nBv[KS], nBg[KS];
+    if (e0 < e1) {
+        load_batch(e0);
+        if (PRE_B) load_b(e0, nBv, nBg);
+    }
+    for (int e = e0; e < e1; ++e) {
+        const int k = (e - e0) & 63;
+        float4_t fI[TPW], fX[TPW], fP[TPW], hI[TPW], hX[TPW], hP[TPW];
+        float Bv[KS], Bg[KS];
+        if (PRE_B) {
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) Bv[kk] = Bg[kk] = nBv[kk];
+        } else {
+            load_b(e, Bv, Bg);
+            if (!SPLIT)
+#pragma unroll
+                for (int kk = 0; kk < KS; ++kk) Bg[kk] = Bv[kk];
+        }
+        const float ux = lane_f(uxv, k), uy = lane_f(uyv, k), uz = lane_f(uzv, k);
+        load_fields(sfb, k, fI, fX, fP);
+        if (TWO) load_fields(sfbf, k, hI, hX, hP);
+        if (e + 1 < e1) {
+            if (k == 63) load_batch(e + 1);
+            if (PRE_B) load_b(e + 1, nBv, nBg);
         }
         wave_sync();  // this wave is done reading the previous edge's P, P'
         {
@@ -227,10 +267,12 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
                 a = __builtin_amdgcn_mfma_f32_16x16x4f32(ap, Bv[kk], a, 0, 0, 0);
                 gg = __builtin_amdgcn_mfma_f32_16x16x4f32(ad, Bg[kk], gg, 0, 0, 0);
             }
+            // this lane's 4 points' dt/dx and dt/dphi: one 16-byte LDS read each
+            const float4_t dx4 = *reinterpret_cast<const float4_t *>(dxs + 16 * t + 4 * g);
+            const float4_t dp4 = *reinterpret_cast<const float4_t *>(dps + 16 * t + 4 * g);
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-                const int pl = 16 * t + 4 * g + jj;
-                const float dxt = dxs[pl], dpt = dps[pl];
+                const float dxt = dx4[jj], dpt = dp4[jj];
                 if (VAL) {
                     // dA/dx = g dxt and dA/dphi = g dpt of the edge field
                     sa[t][jj] += a[jj] * fI[t][jj];
@@ -299,18 +341,19 @@ __global__ __launch_bounds__(64 * WPB) void k_receiver_mfma(Tabs<float> tb, int 
 // a constant no finite input sums to by chance, which keeps every load live.
 template <int WPB>
 __global__ __launch_bounds__(64 * WPB) void k_gather_probe_mfma(int UV, int UVs, int R,
-                                                                int nchunks,
+                                                                int nchunks, int64_t N,
                                                                 const int32_t *__restrict__ row_ptr,
                                                                 const int32_t *__restrict__ col,
+                                                                const int32_t *__restrict__ order,
                                                                 const float *__restrict__ SF,
                                                                 float *__restrict__ sink)
 {
     constexpr int TPW = 4, PW = 16 * TPW, PC = WPB * PW;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, n = lane & 15;
-    const int64_t NN = (int64_t)gridDim.x / ((int64_t)(R / kRT) * nchunks);
-    const int rest = (int)(blockIdx.x / NN);
-    const int64_t i = blockIdx.x - (int64_t)rest * NN;
+    int64_t slice, i;
+    if (!recv_block(N, order, slice, i)) return;
+    const int rest = (int)slice;
     const int r0 = (rest / nchunks) * kRT;
     const int pw0 = (rest % nchunks) * PC + wave * PW;
     if (pw0 >= UV) return;
@@ -395,17 +438,17 @@ bool receiver_mfma_supported(const Dims &d, int R)
 }
 
 hipError_t launch_gather_probe_mfma(const Dims &d, int64_t N, int R, const int32_t *row_ptr,
-                                    const int32_t *col, const float *SF, float *sink,
-                                    hipStream_t s)
+                                    const int32_t *col, const int32_t *order, const float *SF,
+                                    float *sink, hipStream_t s)
 {
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
     constexpr int WPB = 2, PC = WPB * 64;  // as launch_receiver_mfma
     const int nchunks = (d.UV + PC - 1) / PC;
-    const int64_t blocks = N * (R / kRT) * nchunks;
-    if (blocks == 0) return hipSuccess;
+    if (N == 0) return hipSuccess;
+    const int64_t blocks = recv_blocks(N, (int64_t)(R / kRT) * nchunks);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     hipLaunchKernelGGL((k_gather_probe_mfma<WPB>), dim3((unsigned)blocks), dim3(64 * WPB), 0, s,
-                       d.UV, d.UVs, R, nchunks, row_ptr, col, SF, sink);
+                       d.UV, d.UVs, R, nchunks, N, row_ptr, col, order, SF, sink);
     return hipGetLastError();
 }
 
@@ -415,10 +458,10 @@ size_t receiver_mfma_ws_elems(const Dims &d, int64_t N, int R, int planes)
 }
 
 hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const int32_t *row_ptr,
-                                const int32_t *col, const float *unit, const float *Rt,
-                                const float *Rtg, const float *SF, const float *SFf,
-                                bool sf_chunked, float *S, float *Ta, float *Tb, hipStream_t s,
-                                bool values_only, bool analyse)
+                                const int32_t *col, const int32_t *order, const float *unit,
+                                const float *Rt, const float *Rtg, const float *SF,
+                                const float *SFf, bool sf_chunked, float *S, float *Ta, float *Tb,
+                                hipStream_t s, bool values_only, bool analyse)
 {
     if (N == 0) return hipSuccess;
     const Dims &d = tb.d;
@@ -429,14 +472,14 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
     const size_t sh = sizeof(float) * WPB * (2 * 4 * KS * (PW + 16) + 2 * PW);
-    const int64_t blocks = N * (R / kRT) * nchunks;
+    const int64_t blocks = recv_blocks(N, (int64_t)(R / kRT) * nchunks);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     static_assert(PW == kSfChunk, "a receiver wave reads one chunk of the chunked layout");
     const int sf_nc = sf_chunked ? sf_chunks(d) : 0;
 #define CGTP_LAUNCH(LMV, TW, SP, VL)                                                            \
     hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, TW, SP, VL>), dim3((unsigned)blocks),         \
-                       dim3(64 * WPB), sh, s, tb, R, nchunks, row_ptr, col, unit, Rt, Rtg, SF,  \
-                       SFf, sf_nc, S)
+                       dim3(64 * WPB), sh, s, tb, R, nchunks, N, row_ptr, col, order, unit, Rt, \
+                       Rtg, SF, SFf, sf_nc, S)
     switch (d.lmax) {
 #define CGTP_CASE(LMV)                                                 \
     case LMV:                                                          \
