@@ -574,7 +574,8 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
     stage_q<LM>(tb, qs, 4 * G::KM, G::QB, false);
     stage_coefs<LM>(tb, cf);
 
-    const int lane = threadIdx.x & 63, rt = threadIdx.x >> 6;  // this wave's row tile
+    const int lane = threadIdx.x & 63;
+    const int rt = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // this wave's row tile (uniform)
     const int g4 = lane >> 4, n = lane & 15;
     const int rows = nr * G::U;
     // this lane's A row (qa, ua) and its Legendre seeds; its four D rows 16 rt + 4 g + j

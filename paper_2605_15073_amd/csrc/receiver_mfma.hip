@@ -93,7 +93,8 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
     constexpr int RS = PW + 16;
     const Dims &d = tb.d;
     const int UV = d.UV, UVs = d.UVs;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the wave index, uniform across the wave (so the buffer resources built from it are too)
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, n = lane & 15;
     // wave-private LDS: P_l and P_l' at the wave's points, then dt/dx and dt/dphi
     extern __shared__ float smem[];
@@ -349,7 +350,8 @@ __global__ __launch_bounds__(64 * WPB) void k_gather_probe_mfma(int UV, int UVs,
                                                                 float *__restrict__ sink)
 {
     constexpr int TPW = 4, PW = 16 * TPW, PC = WPB * PW;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // the wave index, uniform across the wave (so the buffer resources built from it are too)
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, n = lane & 15;
     int64_t slice, i;
     if (!recv_block(N, order, slice, i)) return;
