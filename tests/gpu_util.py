@@ -49,3 +49,18 @@ def sample_rows(n: int, k: int, seed: int):
     rng = np.random.default_rng(seed)
     inner = rng.choice(np.arange(1, n - 1), max(k - 2, 0), replace=False)
     return np.unique(np.concatenate([[0, n - 1], inner]))[:max(k, 1)]
+
+
+def bench_order(cg, plan, d):
+    """Set on plan the receiver order bench.py uses for the graph of d (cgtp_receiver_order
+    from the edge directions when the inputs have them)."""
+    cg.set_receiver_order(plan, cg.receiver_order(d["row_ptr"], d["col"], d.get("edge_unit")))
+
+
+def same_without_order(cg, plan, run, got):
+    """run(plan) in node order equals got (computed under a receiver order) bit for bit."""
+    import torch
+
+    cg.set_receiver_order(plan, None)
+    base = run(plan)
+    assert all(torch.equal(a, b) for a, b in zip(base, got))

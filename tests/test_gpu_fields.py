@@ -11,7 +11,7 @@ import pytest
 import oracle
 from paper_2605_15073_amd import inputs
 from tests import bruteforce as bf
-from tests.gpu_util import TOL_F32, TOL_F64, rel_err, sample_rows
+from tests.gpu_util import TOL_F32, TOL_F64, bench_order, rel_err, same_without_order, sample_rows
 from tests.test_gpu_general import _dev, _check
 
 pytestmark = pytest.mark.gpu
@@ -153,6 +153,7 @@ def test_mpf_5k_l6_sampled(cg):
     w = inputs.WORKLOADS["mpf_5k_l6_c64"]
     d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R)
+    bench_order(cg, plan, d)
     t = _dev(d, FK)
     gpu = _gpu(cg, plan, t)
     rec = sample_rows(w.n, 24, seed=6)
@@ -160,3 +161,4 @@ def test_mpf_5k_l6_sampled(cg):
     _check(gpu, _ref(w.lmax, d, rec), TOL_F32, rows=rec)
     again = _gpu(cg, plan, t)
     assert torch.equal(gpu[0], again[0]) and torch.equal(gpu[1], again[1])
+    same_without_order(cg, plan, lambda p: _gpu(cg, p, t), gpu)

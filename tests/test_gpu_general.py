@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 from paper_2605_15073_amd import inputs
-from tests.gpu_util import TOL_F32, TOL_F64, rel_err, sample_rows
+from tests.gpu_util import TOL_F32, TOL_F64, bench_order, rel_err, same_without_order, sample_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -281,6 +281,7 @@ def test_mpg_10k_l6_sampled(cg):
     w = inputs.WORKLOADS["mpg_10k_l6_c128"]
     d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R)
+    bench_order(cg, plan, d)
     t = _dev(d, MP_G)
     gpu = _mp_gpu(cg, plan, t)
     rec = sample_rows(w.n, 48, seed=5)
@@ -288,3 +289,4 @@ def test_mpg_10k_l6_sampled(cg):
     _check(gpu, _mp_ref(w.lmax, d, rec), TOL_F32, rows=rec)
     again = _mp_gpu(cg, plan, t)
     assert torch.equal(gpu[0], again[0]) and torch.equal(gpu[1], again[1])
+    same_without_order(cg, plan, lambda p: _mp_gpu(cg, p, t), gpu)

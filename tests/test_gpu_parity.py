@@ -11,8 +11,8 @@ import pytest
 import oracle
 from paper_2605_15073_amd import inputs
 from tests import bruteforce as bf
-from tests.gpu_util import (MP_KEYS, ONSITE_KEYS, TOL_F32, TOL_F64, rel_err, run_mp, run_onsite,
-                            sample_rows, to_dev)
+from tests.gpu_util import (MP_KEYS, ONSITE_KEYS, TOL_F32, TOL_F64, bench_order, rel_err, run_mp,
+                            run_onsite, same_without_order, sample_rows, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -316,6 +316,7 @@ def test_mp_10k_l6_sampled(cg):
     w = inputs.WORKLOADS["mp_10k_l6_c128"]
     d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R)
+    bench_order(cg, plan, d)  # the launch configuration bench.py times
     t = to_dev(d, MP_KEYS)
     gpu = run_mp(cg, plan, t)
     rec = sample_rows(w.n, 160, seed=1)
@@ -323,6 +324,7 @@ def test_mp_10k_l6_sampled(cg):
     _check_pair(gpu, _oracle_mp(w.lmax, d, rec), TOL_F32, nodes=rec)
     again = run_mp(cg, plan, t)
     assert torch.equal(gpu[0], again[0]) and torch.equal(gpu[1], again[1])
+    same_without_order(cg, plan, lambda p: run_mp(cg, p, t), gpu)
 
 
 _L20 = {}
@@ -335,7 +337,10 @@ def _mp_5k_l20(cg):
         w = inputs.WORKLOADS["mp_5k_l20_c64"]
         d = w.make()
         plan = cg.plan_create(w.lmax, w.C, w.R)
-        ge, go = run_mp(cg, plan, to_dev(d, MP_KEYS))
+        bench_order(cg, plan, d)
+        t = to_dev(d, MP_KEYS)
+        ge, go = run_mp(cg, plan, t)
+        same_without_order(cg, plan, lambda p: run_mp(cg, p, t), (ge, go))
         _L20["run"] = (w, d, ge.cpu().numpy(), go.cpu().numpy())
         plan.close()
     return _L20["run"]

@@ -13,7 +13,8 @@ import pytest
 import oracle
 from paper_2605_15073_amd import inputs
 from tests import bruteforce as bf
-from tests.gpu_util import MP_KEYS, TOL_F32, TOL_F64, rel_err, run_mp, sample_rows, to_dev
+from tests.gpu_util import (MP_KEYS, TOL_F32, TOL_F64, bench_order, rel_err, run_mp,
+                            same_without_order, sample_rows, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -167,6 +168,7 @@ def test_mp2_10k_l6_sampled(cg):
     w = inputs.WORKLOADS["mp2_10k_l6_c128"]
     d = w.make()
     plan = cg.plan_create(w.lmax, w.C, w.R)
+    bench_order(cg, plan, d)
     t = to_dev(d, KEYS2)
     gpu = _run2(cg, plan, t)
     rec = sample_rows(w.n, 128, seed=3)
@@ -174,6 +176,7 @@ def test_mp2_10k_l6_sampled(cg):
     _check(gpu, _oracle2(w.lmax, d, rec), TOL_F32, nodes=rec)
     again = _run2(cg, plan, t)
     assert torch.equal(gpu[0], again[0]) and torch.equal(gpu[1], again[1])
+    same_without_order(cg, plan, lambda p: _run2(cg, p, t), gpu)
 
 
 _L20 = {}
@@ -186,7 +189,10 @@ def _mp2_5k_l20(cg):
         w = inputs.WORKLOADS["mp2_5k_l20_c64"]
         d = w.make()
         plan = cg.plan_create(w.lmax, w.C, w.R)
-        ge, go = _run2(cg, plan, to_dev(d, KEYS2))
+        bench_order(cg, plan, d)
+        t = to_dev(d, KEYS2)
+        ge, go = _run2(cg, plan, t)
+        same_without_order(cg, plan, lambda p: _run2(cg, p, t), (ge, go))
         _L20["run"] = (w, d, ge.cpu().numpy(), go.cpu().numpy())
         plan.close()
     return _L20["run"]
