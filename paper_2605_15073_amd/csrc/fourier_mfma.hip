@@ -127,7 +127,8 @@ __device__ __forceinline__ void stage_rows(const float *src, float *dst, int nr)
 // (Eq. msgpass-FI and its x-derivative). The functions come from the three-term recurrence
 // in l, started by adding seed = Pt_|m|^|m|(x) at l = |m| (seed 0 for the padding orders
 // |m| > lmax). Below l = |m| a lane carries zeros. The loop is unrolled from the lowest
-// |m| of the step, so every table offset is a constant.
+// |m| of the step, so every table offset is a constant. VO: the values fa alone (fx, fn
+// untouched).
 // Degrees a lane visits at reduction step kk (orders 4 kk - lmax .. 4 kk - lmax + 3):
 // l = a0(kk) .. lmax, the lowest |m| of the step upwards; base(kk) counts the (step, degree)
 // pairs of the steps before kk.
@@ -147,7 +148,7 @@ struct LegendreSteps {
     static constexpr int N = base(Grid<LM>::KM);
 };
 
-template <int LM, int KK, int NOP>
+template <int LM, int KK, int NOP, bool VO = false>
 __device__ __forceinline__ void legendre_step(const float4_t *cf, const float *const *h, float seed,
                                               float x, float r, int m, float *fa, float *fx,
                                               float *fn)
@@ -161,13 +162,15 @@ __device__ __forceinline__ void legendre_step(const float4_t *cf, const float *c
         const float4_t c = ca[l * (l + 1) / 2];
         const float inj = (l == am) ? seed : 0.f;
         const float pv = c[0] * (x * p1 - c[1] * p2) + inj;
-        const float dv = (c[2] * p1 - (float)l * x * pv) * r;
 #pragma unroll
         for (int o = 0; o < NOP; ++o) {
             const float cp = h[o][l * l + l + m];
             fa[o] += pv * cp;
-            fx[o] += dv * cp;
-            fn[o] += pv * h[o][l * l + l - m];
+            if constexpr (!VO) {
+                const float dv = (c[2] * p1 - (float)l * x * pv) * r;
+                fx[o] += dv * cp;
+                fn[o] += pv * h[o][l * l + l - m];
+            }
         }
         p2 = p1;
         p1 = pv;
@@ -189,7 +192,8 @@ __device__ __forceinline__ void load_seeds(const Tabs<float> &tb, int g4, int ua
 // ---------------------------------------------------------------- sender fields
 
 // Legendre pass of all reduction steps of one lane for NOP operands: bf[kk][o][f] holds
-// F, dF/dx and m F[-m] (the d/dphi slot swap) of operand o at order m = 4 kk + g - lmax.
+// F, dF/dx and m F[-m] (the d/dphi slot swap) of operand o at order m = 4 kk + g - lmax
+// (VO: F alone, in f = 0).
 template <int LM, int NOP>
 struct LaneRows {
     const float4_t *cf;
@@ -199,7 +203,7 @@ struct LaneRows {
     int g4;
 };
 
-template <int LM, int NOP, int KK>
+template <int LM, int NOP, int KK, bool VO = false>
 __device__ __forceinline__ void legendre_all(const LaneRows<LM, NOP> &c,
                                              float (&bf)[Grid<LM>::KM][NOP][3])
 {
@@ -208,17 +212,19 @@ __device__ __forceinline__ void legendre_all(const LaneRows<LM, NOP> &c,
         float fa[NOP], fx[NOP], fn[NOP];
 #pragma unroll
         for (int o = 0; o < NOP; ++o) fa[o] = fx[o] = fn[o] = 0.f;
-        legendre_step<LM, KK, NOP>(c.cf, c.h, c.seed[KK], c.x, c.r, m, fa, fx, fn);
+        legendre_step<LM, KK, NOP, VO>(c.cf, c.h, c.seed[KK], c.x, c.r, m, fa, fx, fn);
 #pragma unroll
         for (int o = 0; o < NOP; ++o) {
             bf[KK][o][0] = fa[o];
-            bf[KK][o][1] = fx[o];
-            bf[KK][o][2] = (float)m * fn[o];
+            if constexpr (!VO) {
+                bf[KK][o][1] = fx[o];
+                bf[KK][o][2] = (float)m * fn[o];
+            }
         }
         // keep the scheduler from hoisting the next step's loads over this one: the straight
         // line code would otherwise hold every step's operands in registers at once
         __builtin_amdgcn_sched_barrier(0);
-        legendre_all<LM, NOP, KK + 1>(c, bf);
+        legendre_all<LM, NOP, KK + 1, VO>(c, bf);
     }
 }
 
@@ -287,7 +293,7 @@ __device__ __forceinline__ void legendre_all_tab(const float *const *h, int g4,
     }
 }
 
-template <int LM>
+template <int LM, bool V1>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k_sender_mfma(Tabs<float> tb, int R, int rb, int nc,
                                                      const float *__restrict__ H,
                                                      float *__restrict__ SF, int planes)
@@ -325,8 +331,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
         c.x = tb.x[ua];
         c.r = 1.f / (sxu * sxu);
         c.g4 = g4;
+        // V1: the value field alone (planes 1 and 8), without the derivative passes
+        constexpr int NFD = V1 ? 1 : 3;
         float bf[G::KM][1][3];
-        legendre_all<LM, 1, 0>(c, bf);
+        legendre_all<LM, 1, 0, V1>(c, bf);
         // Fourier pass: D[(q,u)][v] = sum_m F[(q,u)][m] q_vm, one v tile at a time
         float4_t acc[3][G::VT];
 #pragma unroll
@@ -336,7 +344,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
             for (int kk = 0; kk < G::KM; ++kk) {
                 const float bq = qs[(4 * kk + g4) * G::QB + t * 16 + n];
 #pragma unroll
-                for (int f = 0; f < 3; ++f)
+                for (int f = 0; f < NFD; ++f)
                     acc[f][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[kk][0][f], bq, acc[f][t],
                                                                      0, 0, 0);
             }
@@ -353,8 +361,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
                     for (int t = 0; t < G::VT; ++t) {
                         if (t * 16 + n < G::V) {
                             if (planes & 1) o[t * 16] = acc[0][t][j];
-                            if (planes & 2) o[G::UVs + t * 16] = acc[1][t][j];
-                            if (planes & 4) o[2 * G::UVs + t * 16] = acc[2][t][j];
+                            if (!V1 && (planes & 2)) o[G::UVs + t * 16] = acc[1][t][j];
+                            if (!V1 && (planes & 4)) o[2 * G::UVs + t * 16] = acc[2][t][j];
                             if (planes & 8) o[G::UVs + t * 16] = acc[0][t][j];
                         }
                     }
@@ -369,8 +377,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k
                             float *o = SF + ((((int64_t)(r >> 4) * nc + c) * nb + b) * 16 + (r & 15)) *
                                                 3 * kSfChunk + pp;
                             if (planes & 1) o[0] = acc[0][t][j];
-                            if (planes & 2) o[kSfChunk] = acc[1][t][j];
-                            if (planes & 4) o[2 * kSfChunk] = acc[2][t][j];
+                            if (!V1 && (planes & 2)) o[kSfChunk] = acc[1][t][j];
+                            if (!V1 && (planes & 4)) o[2 * kSfChunk] = acc[2][t][j];
                             if (planes & 8) o[kSfChunk] = acc[0][t][j];
                         }
                     }
@@ -1080,9 +1088,14 @@ hipError_t sender_lm(const Tabs<float> &tb, int64_t B, int R, const float *H, fl
         }
     }
     const int nc = chunked ? sf_chunks(tb.d) : 0;
-    hipLaunchKernelGGL((k_sender_mfma<LM>), dim3((unsigned)blocks), dim3(64 * waves_for(rb * G::U)),
-                       sizeof(float) * (fixed + rb * (size_t)G::HR), s, tb, R, rb, nc, H, SF,
-                       planes);
+    const dim3 grid((unsigned)blocks), block(64 * waves_for(rb * G::U));
+    const size_t sh = sizeof(float) * (fixed + rb * (size_t)G::HR);
+    if ((planes & ~9) == 0)  // the value field alone (planes 0 and/or 1)
+        hipLaunchKernelGGL((k_sender_mfma<LM, true>), grid, block, sh, s, tb, R, rb, nc, H, SF,
+                           planes);
+    else
+        hipLaunchKernelGGL((k_sender_mfma<LM, false>), grid, block, sh, s, tb, R, rb, nc, H, SF,
+                           planes);
     return hipGetLastError();
 }
 
