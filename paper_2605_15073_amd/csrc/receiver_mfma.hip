@@ -50,12 +50,15 @@ __device__ __forceinline__ void wave_sync()
 }
 
 // Waves per SIMD the register allocation of k_receiver_mfma aims at (values-only form): 4 with
-// one set of sums at lmax 3 to 7 (where it needs no spill), else 3, and 2 with six sums (two
-// node slots) or two coefficient sets above lmax 12 (which would spill at 3).
+// one set of sums at lmax 3 to 7 (where it needs no spill), else 3 (2 at lmax 24), and 2 with
+// six sums (two node slots) or two coefficient sets above lmax 12 (which would spill at 3).
 template <bool VAL, bool TWO, bool SPLIT>
 constexpr int kRecvWaves(int lm)
 {
-    return !VAL ? 1 : TWO ? 2 : SPLIT ? (lm > 12 ? 2 : 3) : (lm >= 3 && lm <= 7 ? 4 : 3);
+    return !VAL ? 1
+           : TWO ? 2
+           : SPLIT ? (lm > 12 ? 2 : 3)
+                   : (lm >= 3 && lm <= 7 ? 4 : lm >= 24 ? 2 : 3);
 }
 
 // LM is lmax: the recurrence is unrolled with compile-time coefficients. A workgroup
@@ -89,6 +92,10 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
     constexpr int PC = WPB * PW;     // grid points per workgroup
     constexpr int L = LM + 1;
     constexpr int KS = (L + 3) / 4;  // K steps of 4 degrees
+    // P_0' = 0: when lmax is a multiple of 4 the derivative sum starts at degree DO = 1 and
+    // takes one K step fewer (KSG) than the value sum; its LDS row j holds degree j + DO
+    constexpr int DO = (LM > 0 && LM % 4 == 0) ? 1 : 0;
+    constexpr int KSG = (L - DO + 3) / 4;
     // LDS row stride: the rows read by lane groups g and g + 1 land in different bank halves
     constexpr int RS = PW + 16;
     const Dims &d = tb.d;
@@ -187,7 +194,8 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
             if (!VAL) fP[t] = bload4(sfr, vofft[t], so + 2 * fstride * 4);
         }
     };
-    // B operand: Rt[e][4 kk + g][r0 + n] (and Rtg's with SPLIT)
+    // B operands: Rt[e][4 kk + g][r0 + n] for the value sum; for the derivative sum the rows
+    // from degree DO on, of Rtg with SPLIT (else the same as the value sum's when DO = 0)
     auto load_b = [&](int e, float *bv, float *bg) {
         const float *rte = Rt + (int64_t)e * L * R + r0 + n;
         const float *rtg = SPLIT ? Rtg + (int64_t)e * L * R + r0 + n : rte;
@@ -195,7 +203,13 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
         for (int kk = 0; kk < KS; ++kk) {
             const int l = 4 * kk + g;
             bv[kk] = l <= LM ? rte[l * R] : 0.f;
-            if (SPLIT) bg[kk] = l <= LM ? rtg[l * R] : 0.f;
+        }
+        if (SPLIT || DO) {
+#pragma unroll
+            for (int kk = 0; kk < KSG; ++kk) {
+                const int l = 4 * kk + g + DO;
+                bg[kk] = l <= LM ? rtg[l * R] : 0.f;
+            }
         }
     };
     // A wave loads an edge's sender fields when the edge starts and hides their latency behind
@@ -215,10 +229,12 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
         float Bv[KS], Bg[KS];
         if (PRE_B) {
 #pragma unroll
-            for (int kk = 0; kk < KS; ++kk) Bv[kk] = Bg[kk] = nBv[kk];
+            for (int kk = 0; kk < KS; ++kk) Bv[kk] = nBv[kk];
+#pragma unroll
+            for (int kk = 0; kk < KSG; ++kk) Bg[kk] = DO ? nBg[kk] : nBv[kk];
         } else {
             load_b(e, Bv, Bg);
-            if (!SPLIT)
+            if (!SPLIT && !DO)
 #pragma unroll
                 for (int kk = 0; kk < KS; ++kk) Bg[kk] = Bv[kk];
         }
@@ -237,10 +253,10 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
             const float t = uz * rx + rsx * h;
             float p0v = 1.f, p1v = t, d1 = 1.f;
             Pl[lane] = 1.f;
-            Dl[lane] = 0.f;
+            if (!DO) Dl[lane] = 0.f;
             if (LM >= 1) {
                 Pl[RS + lane] = t;
-                Dl[RS + lane] = 1.f;
+                Dl[(1 - DO) * RS + lane] = 1.f;
             }
 #pragma unroll
             for (int l = 2; l <= LM; ++l) {
@@ -248,7 +264,7 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
                 const float p2 = c1 * t * p1v - c2 * p0v;
                 const float d2 = (float)l * p1v + t * d1;
                 Pl[l * RS + lane] = p2;
-                Dl[l * RS + lane] = d2;
+                Dl[(l - DO) * RS + lane] = d2;
                 p0v = p1v;
                 p1v = p2;
                 d1 = d2;
@@ -259,14 +275,17 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
         wave_sync();
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
-            // A operand: P_{4 kk + g}(t_p) at point p = 16 t + n (rows are points)
+            // A operands: P_{4 kk + g}(t_p) and P'_{4 kk + g + DO}(t_p) at point p = 16 t + n
+            // (rows are points)
             float4_t a = float4_t{0.f, 0.f, 0.f, 0.f}, gg = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kk = 0; kk < KS; ++kk) {
                 const float ap = Pl[(4 * kk + g) * RS + 16 * t + n];
-                const float ad = Dl[(4 * kk + g) * RS + 16 * t + n];
                 a = __builtin_amdgcn_mfma_f32_16x16x4f32(ap, Bv[kk], a, 0, 0, 0);
-                gg = __builtin_amdgcn_mfma_f32_16x16x4f32(ad, Bg[kk], gg, 0, 0, 0);
+                if (kk < KSG) {
+                    const float ad = Dl[(4 * kk + g) * RS + 16 * t + n];
+                    gg = __builtin_amdgcn_mfma_f32_16x16x4f32(ad, Bg[kk], gg, 0, 0, 0);
+                }
             }
             // this lane's 4 points' dt/dx and dt/dphi: one 16-byte LDS read each
             const float4_t dx4 = *reinterpret_cast<const float4_t *>(dxs + 16 * t + 4 * g);
