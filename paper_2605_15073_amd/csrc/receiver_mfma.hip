@@ -489,17 +489,22 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     if (!receiver_mfma_supported(d, R)) return hipErrorNotSupported;
     if (SFf && Rtg) return hipErrorNotSupported;
     if (values_only && SFf && Rtg) return hipErrorInvalidValue;
-    constexpr int WPB = 2, PW = 64, PC = WPB * PW;
+    // Waves per workgroup: two (128 grid points); one with two node slots up to lmax 8, whose
+    // six sums leave two waves per SIMD (there more, smaller workgroups measured 2.8% faster
+    // at lmax 6, but 4% slower at lmax 20 and 2.6% slower with one slot).
+    constexpr int PW = 64;
+    const int wpb = SFf && d.lmax <= 8 ? 1 : 2, PC = wpb * PW;
     const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
-    const size_t sh = sizeof(float) * WPB * (2 * 4 * KS * (PW + 16) + 2 * PW);
+    const size_t sh = sizeof(float) * wpb * (2 * 4 * KS * (PW + 16) + 2 * PW);
     const int64_t blocks = recv_blocks(N, (int64_t)(R / kRT) * nchunks);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     static_assert(PW == kSfChunk, "a receiver wave reads one chunk of the chunked layout");
     const int sf_nc = sf_chunked ? sf_chunks(d) : 0;
 #define CGTP_LAUNCH(LMV, TW, SP, VL)                                                            \
-    hipLaunchKernelGGL((k_receiver_mfma<WPB, LMV, TW, SP, VL>), dim3((unsigned)blocks),         \
-                       dim3(64 * WPB), sh, s, tb, R, nchunks, N, row_ptr, col, order, unit, Rt, \
+    hipLaunchKernelGGL((k_receiver_mfma<TW && LMV <= 8 ? 1 : 2, LMV, TW, SP, VL>),            \
+                       dim3((unsigned)blocks),                                                  \
+                       dim3(64 * wpb), sh, s, tb, R, nchunks, N, row_ptr, col, order, unit, Rt, \
                        Rtg, SF, SFf, sf_nc, S)
     switch (d.lmax) {
 #define CGTP_CASE(LMV)                                                 \
