@@ -543,18 +543,23 @@ constexpr unsigned kFieldsOutside = 0x80000000u;
 // node u). Per edge each wave synthesises its rows of the edge field's grid fields exactly
 // as k_sender_mfma does for a node (the Legendre sums formed in the A-operand registers, the
 // Fourier product on MFMA; columns v) and each lane multiplies its D values, rows
-// 16 rt + 4 g + j at v = 16 t + n, with the sender fields at the same (q, u, v) (Eqs.
-// msgpass-S and cat-beta-curl; 16 lanes read 64 contiguous bytes of a row). A lane requests
-// its sender fields and its share of the next edge's coefficient rows when the edge starts,
+// 16 rt + 4 g + j at v = 16 t + n, with the sender values at the same (q, u, v) (Eq.
+// msgpass-S; 16 lanes read 64 contiguous bytes of a row). The surface curl takes the
+// moved-derivative form (integration by parts on the sphere, as k_receiver_mfma): the edge
+// field's x- and phi-derivatives times the sender values are summed into S1, S2, which the
+// analysis takes against dY/dphi and dY/dx, so the senders' derivative fields are never
+// read. A lane requests its sender values and its share of the next edge's coefficient rows
+// when the edge starts,
 // so both arrive while it computes; the rows are double-buffered in LDS (one barrier per
 // edge). Both are buffer loads whose per-lane byte offsets are fixed over the CSR row and
 // computed once (rows and columns past the block read 0 from past the resource); only the
-// wave-uniform resources change per edge. The products accumulate in registers over the CSR row; the sums go to
-// S [N][R][2][UVs] for k_analysis_mfma. Blocks run in the receiver block order (recv_block),
-// rank block by rank block.
+// wave-uniform resources change per edge. The products accumulate in registers over the CSR
+// row; the sums (S^alpha, S1, S2) go to S [N][R][3][UVs] for k_analysis_mfma in its moved
+// mode. Blocks run in the receiver block order (recv_block), rank block by rank block.
 // SPLIT: the value field comes from the rows HE (Gaunt factors) and the two derivative
 // fields from the rows HEc (curl factors); both row sets are staged and the Legendre pass
-// runs over both.
+// runs over both. The senders then carry the Gaunt factors' values in plane 0 and the curl
+// factors' in plane 1, which the derivative fields multiply.
 template <int LM, bool SPLIT>
 __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, int R, int rb,
                                                               int64_t N,
@@ -645,9 +650,9 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
                 if (kk < nh) buf[set * hset + kk] = hv[set][t];
             }
     };
-    float4_t sa[G::VT], sb[G::VT];
+    float4_t sa[G::VT], s1[G::VT], s2[G::VT];
 #pragma unroll
-    for (int t = 0; t < G::VT; ++t) sa[t] = sb[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < G::VT; ++t) sa[t] = s1[t] = s2[t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
     const int e0 = row_ptr[i], e1 = row_ptr[i + 1];
     if (e0 < e1) {
@@ -667,7 +672,8 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
         // this edge's sender fields at the lane's D rows and columns
         const __amdgpu_buffer_rsrc_t sfr = fields_rsrc(SF + (j * R + r0) * 3 * (int64_t)G::UVs,
                                                        fbytes);
-        float fI[G::VT][4], fX[G::VT][4], fP[G::VT][4];
+        // the sender values (plane 0); SPLIT: the curl factors' values too (plane 1)
+        float fI[G::VT][4], fC[G::VT][4];
 #pragma unroll
         for (int t = 0; t < G::VT; ++t) {
 #pragma unroll
@@ -675,8 +681,7 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
                 const unsigned vo = t == G::VT - 1 ? flast[jj] : foff[jj];
                 const unsigned so = (unsigned)(t * 16 * 4);
                 fI[t][jj] = fields_load(sfr, vo, so);
-                fX[t][jj] = fields_load(sfr, vo, so + G::UVs * 4);
-                fP[t][jj] = fields_load(sfr, vo, so + 2 * G::UVs * 4);
+                fC[t][jj] = SPLIT ? fields_load(sfr, vo, so + G::UVs * 4) : fI[t][jj];
             }
         }
         // the next edge's coefficient rows, stored after this edge's Legendre pass
@@ -710,17 +715,20 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
                         acc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(bf[kk][0][f], bq, acc[f], 0,
                                                                       0, 0);
                 }
+                // the Gaunt sum and the curl's moved-derivative pair: the edge field's x- and
+                // phi-derivatives times the sender values
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) {
                     sa[t][jj] += acc[0][jj] * fI[t][jj];
-                    sb[t][jj] += acc[2][jj] * fX[t][jj] - acc[1][jj] * fP[t][jj];
+                    s1[t][jj] += acc[1][jj] * fC[t][jj];
+                    s2[t][jj] += acc[2][jj] * fC[t][jj];
                 }
             }
         }
         if (more) store_rows(Hs + (cur ^ 1) * NS * hset, hn);
         __syncthreads();  // the next rows are staged; this edge's rows are consumed
     }
-    float *Sr = S + (i * R + r0) * 2 * (int64_t)G::UVs;
+    float *Sr = S + (i * R + r0) * 3 * (int64_t)G::UVs;
 #pragma unroll
     for (int t = 0; t < G::VT; ++t) {
         const int v = t * 16 + n;
@@ -730,9 +738,10 @@ __global__ __launch_bounds__(512) void k_receiver_fields_mfma(Tabs<float> tb, in
             if (off[jj] < 0) continue;
             const int ro = rt * 16 + 4 * g4 + jj;
             const int qo = ro / G::U, uo = ro - qo * G::U;
-            float *o = Sr + qo * 2 * G::UVs + uo * G::V + v;
+            float *o = Sr + qo * 3 * G::UVs + uo * G::V + v;
             o[0] = sa[t][jj];
-            o[G::UVs] = sb[t][jj];
+            o[G::UVs] = s1[t][jj];
+            o[2 * G::UVs] = s2[t][jj];
         }
     }
 }
@@ -1199,9 +1208,7 @@ hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
     default: return hipErrorNotSupported;
     }
     if (e != hipSuccess || !analyse) return e;
-    e = launch_analysis_mfma(tb, N, R, S, Ta, Tb, s);
-    if (e != hipErrorNotSupported) return e;
-    return launch_analysis_folded(tb, N, R, S, Ta, Tb, s);
+    return launch_analysis_mfma(tb, N, R, S, Ta, Tb, s, 1);
 }
 
 hipError_t launch_onsite_mfma(const Tabs<float> &tb, int64_t B, int R, const float *HA,

@@ -212,11 +212,14 @@ hipError_t launch_receiver_fields(const Tabs<T> &tb, int64_t N, int R, const int
                                   const int32_t *col, const int32_t *order, const T *HE,
                                   const T *SF, T *Ta, T *Tb, hipStream_t s);
 
-// fp32 edge-field receiver on MFMA (fourier_mfma.hip), default grid: the summed grid fields
-// go to S [N][R][2][UVs] and the inverse transforms into Ta, Tb follow. SF in the layout
-// [N][R][3][UVs]. hipErrorNotSupported off the default grid.
+// fp32 edge-field receiver on MFMA (fourier_mfma.hip), default grid, with the curl in the
+// moved-derivative form: the summed grid fields (S^alpha, S1, S2) go to S [N][R][3][UVs] and
+// the inverse transforms (launch_analysis_mfma mode 1) into Ta, Tb follow. SF in the layout
+// [N][R][3][UVs], of which only the sender values (plane 0) are read.
+// hipErrorNotSupported off the default grid.
 // HEc: NULL, or the edge coefficients of the curl factors (then HE holds the Gaunt factors'
-// and gives the value field, HEc the two derivative fields).
+// and gives the value field, HEc the two derivative fields, which multiply the curl factors'
+// sender values in plane 1 of SF).
 hipError_t launch_receiver_fields_mfma(const Tabs<float> &tb, int64_t N, int R,
                                        const int32_t *row_ptr, const int32_t *col,
                                        const int32_t *order, const float *HE, const float *HEc,

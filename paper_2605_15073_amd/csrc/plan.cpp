@@ -201,7 +201,8 @@ Layout mpf_layout(const cgtp_plan_s *p, int R, int64_t N, int64_t E, bool split 
     size_t h = align256(es * (size_t)N * R * p->d.K);
     size_t sf = align256(es * (size_t)N * R * 3 * p->d.UVs);
     size_t he = align256(es * (size_t)E * R * p->d.K);
-    size_t sg = use_mfma_fields(p) ? align256(es * (size_t)N * R * 2 * p->d.UVs) : 0;
+    // the MFMA edge-field receiver's sums: the Gaunt sum and the curl's moved pair
+    size_t sg = use_mfma_fields(p) ? align256(es * (size_t)N * R * 3 * p->d.UVs) : 0;
     Layout l{};
     l.off[0] = 0;
     l.off[1] = ns * h;
@@ -883,10 +884,14 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
     if (e == hipSuccess && G.split) e = contract_runs<T>(p, G, N, false, X2, f.in2, HIc, wc, s, 2);
     if (e != hipSuccess) return hip_fail(e, "contract node features");
     rec.mark();
-    // split: the Gaunt factors' contraction gives the sender values, the curl factors' the
-    // two derivative fields, into the same field slots
-    e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s, G.split ? 1 : 7);
-    if (e == hipSuccess && G.split) e = cgtp::launch_sender_fields<T>(tb, N, Rg, HIc, SF, s, 6);
+    // The MFMA receiver takes the curl in the moved-derivative form and reads sender values
+    // only: plane 0, and with split factors the curl factors' values in plane 1. The
+    // per-thread receiver reads all three fields; split: the Gaunt factors' contraction gives
+    // the sender values, the curl factors' the two derivative fields.
+    const bool moved = sizeof(T) == 4 && use_mfma_fields(p);
+    e = cgtp::launch_sender_fields<T>(tb, N, Rg, HI, SF, s, moved || G.split ? 1 : 7);
+    if (e == hipSuccess && G.split)
+        e = cgtp::launch_sender_fields<T>(tb, N, Rg, HIc, SF, s, moved ? 8 : 6);
     if (e != hipSuccess) return hip_fail(e, "sender fields");
     rec.mark();
     e = contract_runs<T>(p, G, E, true, X1, f.in1, HE, wc, s, G.split ? 1 : 0);
@@ -901,7 +906,7 @@ int run_mp_fields(cgtp_plan_s *p, const Groups &G, int64_t N, int64_t E, const i
                                                   Sg, Ta, Tb, s, false);
             if (e != hipSuccess) return hip_fail(e, "receiver (edge field, mfma)");
             rec.mark();
-            e = cgtp::launch_summed_analysis(tb, N, Rg, Sg, Ta, Tb, s, 0);
+            e = cgtp::launch_summed_analysis(tb, N, Rg, Sg, Ta, Tb, s, 1);
             if (e != hipSuccess) return hip_fail(e, "analysis");
             rec.mark();
             return project_blocks<T>(p, G, N, f, Ta, Tb, oe, oo, wc, s, rec);

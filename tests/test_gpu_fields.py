@@ -54,7 +54,7 @@ def _ref(lmax, d, rec=None):
     (2, 6, True, True, 4, 2),
     (3, 6, False, False, 1, 1),   # one slot each, shared factors
     (4, 5, True, False, 2, 1),
-    (5, 6, True, True, 4, 2),     # split factors: the curl pass writes only the derivative planes
+    (5, 6, True, True, 4, 2),     # split factors: the curl pass writes the curl values to plane 1
     (6, 9, False, True, 1, 2),
     (8, 8, True, True, 2, 2),
     (12, 8, False, False, 4, 2),
