@@ -49,15 +49,24 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Waves per SIMD the register allocation of k_receiver_mfma aims at (values-only form): 4 with
-// one set of sums at lmax 3 to 7 (where it needs no spill), else 3 (2 at lmax 24), and 2 with
-// six sums (two node slots) or two coefficient sets above lmax 12 (which would spill at 3).
+// Wave-private LDS of k_receiver_mfma in floats: P_l rows (4 KS) and P_l' rows (4 KSG) of 64
+// points, then dt/dx and dt/dphi at those points.
+constexpr int recv_lds_floats(int lm)
+{
+    const int ks = (lm + 4) / 4, ksg = (lm + 1 - ((lm > 0 && lm % 4 == 0) ? 1 : 0) + 3) / 4;
+    return 4 * (ks + ksg) * 64 + 2 * 64;
+}
+
+// Waves per SIMD the register allocation of k_receiver_mfma aims at (values-only form), at
+// least: 4 with one set of sums at lmax 3 to 7 (where it needs no spill), else 3 (2 at lmax
+// 24), and 2 with six sums (two node slots) or two coefficient sets from lmax 9 (which would
+// spill at 3).
 template <bool VAL, bool TWO, bool SPLIT>
 constexpr int kRecvWaves(int lm)
 {
     return !VAL ? 1
            : TWO ? 2
-           : SPLIT ? (lm > 12 ? 2 : 3)
+           : SPLIT ? (lm >= 9 ? 2 : 3)
                    : (lm >= 3 && lm <= 7 ? 4 : lm >= 24 ? 2 : 3);
 }
 
@@ -96,8 +105,9 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
     // takes one K step fewer (KSG) than the value sum; its LDS row j holds degree j + DO
     constexpr int DO = (LM > 0 && LM % 4 == 0) ? 1 : 0;
     constexpr int KSG = (L - DO + 3) / 4;
-    // LDS row stride: the rows read by lane groups g and g + 1 land in different bank halves
-    constexpr int RS = PW + 16;
+    // LDS rows of 64 points; point p of row j sits at column p ^ 16 (j & 3), so the rows that
+    // lane groups g = 0..3 read at once (j = 4 kk + g) land on four different groups of 16 banks
+    constexpr int RS = PW;
     const Dims &d = tb.d;
     const int UV = d.UV, UVs = d.UVs;
     // the wave index, uniform across the wave (so the buffer resources built from it are too)
@@ -105,11 +115,12 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
     const int g = lane >> 4, n = lane & 15;
     // wave-private LDS: P_l and P_l' at the wave's points, then dt/dx and dt/dphi
     extern __shared__ float smem[];
-    constexpr int wstride = 2 * 4 * KS * RS + 2 * PW;
+    constexpr int wstride = recv_lds_floats(LM);
     float *Pl = smem + wave * wstride;  // [4 KS][RS]
-    float *Dl = Pl + 4 * KS * RS;       // [4 KS][RS]
-    float *dxs = Dl + 4 * KS * RS;      // [PW]
+    float *Dl = Pl + 4 * KS * RS;       // [4 KSG][RS]
+    float *dxs = Dl + 4 * KSG * RS;     // [PW]
     float *dps = dxs + PW;              // [PW]
+    auto slot = [](int j, int p) { return j * RS + (p ^ ((j & 3) << 4)); };
 
     // Block order (recv_block): the slices are (rank tile, point chunk) pairs.
     int64_t slice, i;
@@ -122,7 +133,7 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
     if (pw0 >= UV) return;
 
     // degrees beyond lmax stay zero in the A operand
-    for (int k = lane; k < 2 * 4 * KS * RS; k += 64) Pl[k] = 0.f;
+    for (int k = lane; k < 4 * (KS + KSG) * RS; k += 64) Pl[k] = 0.f;
     // this lane's recurrence point (points past the grid compute on point 0, never stored)
     const int pr = pw0 + lane;
     const int prc = pr < UV ? pr : 0;
@@ -252,19 +263,19 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
             const float h = ux * rcp + uy * rsp;
             const float t = uz * rx + rsx * h;
             float p0v = 1.f, p1v = t, d1 = 1.f;
-            Pl[lane] = 1.f;
-            if (!DO) Dl[lane] = 0.f;
+            Pl[slot(0, lane)] = 1.f;
+            if (!DO) Dl[slot(0, lane)] = 0.f;
             if (LM >= 1) {
-                Pl[RS + lane] = t;
-                Dl[(1 - DO) * RS + lane] = 1.f;
+                Pl[slot(1, lane)] = t;
+                Dl[slot(1 - DO, lane)] = 1.f;
             }
 #pragma unroll
             for (int l = 2; l <= LM; ++l) {
                 const float c1 = (float)(2 * l - 1) / (float)l, c2 = (float)(l - 1) / (float)l;
                 const float p2 = c1 * t * p1v - c2 * p0v;
                 const float d2 = (float)l * p1v + t * d1;
-                Pl[l * RS + lane] = p2;
-                Dl[(l - DO) * RS + lane] = d2;
+                Pl[slot(l, lane)] = p2;
+                Dl[slot(l - DO, lane)] = d2;
                 p0v = p1v;
                 p1v = p2;
                 d1 = d2;
@@ -280,10 +291,10 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
             float4_t a = float4_t{0.f, 0.f, 0.f, 0.f}, gg = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kk = 0; kk < KS; ++kk) {
-                const float ap = Pl[(4 * kk + g) * RS + 16 * t + n];
+                const float ap = Pl[slot(4 * kk + g, 16 * t + n)];
                 a = __builtin_amdgcn_mfma_f32_16x16x4f32(ap, Bv[kk], a, 0, 0, 0);
                 if (kk < KSG) {
-                    const float ad = Dl[(4 * kk + g) * RS + 16 * t + n];
+                    const float ad = Dl[slot(4 * kk + g, 16 * t + n)];
                     gg = __builtin_amdgcn_mfma_f32_16x16x4f32(ad, Bg[kk], gg, 0, 0, 0);
                 }
             }
@@ -494,9 +505,8 @@ hipError_t launch_receiver_mfma(const Tabs<float> &tb, int64_t N, int R, const i
     // at lmax 6, but 4% slower at lmax 20 and 2.6% slower with one slot).
     constexpr int PW = 64;
     const int wpb = SFf && d.lmax <= 8 ? 1 : 2, PC = wpb * PW;
-    const int KS = (d.L + 3) / 4;
     const int nchunks = (d.UV + PC - 1) / PC;
-    const size_t sh = sizeof(float) * wpb * (2 * 4 * KS * (PW + 16) + 2 * PW);
+    const size_t sh = sizeof(float) * wpb * (size_t)recv_lds_floats(d.lmax);
     const int64_t blocks = recv_blocks(N, (int64_t)(R / kRT) * nchunks);
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     static_assert(PW == kSfChunk, "a receiver wave reads one chunk of the chunked layout");
