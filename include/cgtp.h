@@ -363,8 +363,10 @@ int cgtp_gather_probe(cgtp_plan plan, int64_t n_nodes, int64_t n_edges, const in
  * permutation) to device memory the plan owns; from then on every message-passing call and
  * cgtp_gather_probe on the plan runs its receivers in that order and must pass exactly
  * n_nodes nodes (CGTP_ERR_ARG otherwise). order NULL or n_nodes 0 clears it (the identity).
- * Synchronises the device. Errors: CGTP_ERR_ARG (NULL plan, not a permutation, wrong
- * device), CGTP_ERR_HIP (allocation or copy). */
+ * Synchronises the device. Setting or clearing an order frees the previous device copy, so
+ * a HIP graph captured from calls under that order must not be replayed afterwards.
+ * Errors: CGTP_ERR_ARG (NULL plan, not a permutation, wrong device), CGTP_ERR_HIP
+ * (allocation or copy). */
 int cgtp_receiver_order(int64_t n_nodes, int64_t n_edges, const int32_t *row_ptr,
                         const int32_t *col, const float *edge_vec, int32_t *order);
 int cgtp_plan_set_receiver_order(cgtp_plan plan, int64_t n_nodes, const int32_t *order);
