@@ -203,7 +203,7 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
 // kdeg contraction (the edge side, Eq. msgpass-tildeR): Y[b][o][l] over the L degree
 // slots of X [B][Cin][L]. A workgroup owns 64 rows b and 64 outputs o for a group of kLG
 // degrees, so a row's input block is read once for all of those degrees (four: with their
-// 64 accumulator registers three waves fit per SIMD, which hides the loads better than
+// 64 accumulator registers four waves fit per SIMD, which hides the loads better than
 // seven degrees at two waves, even though a group of 7 then leaves one slot idle). The reduction
 // runs in slices of kCk inputs: each thread prefetches its share of the next slice into
 // registers while the matrix cores work on the current one from LDS. X rows keep their
@@ -217,7 +217,7 @@ constexpr int kSB = 34;          // LDS row stride of a staged X row (kCk * kLG 
 constexpr int kSW = kTile + 16;  // LDS row stride of Ws: lane groups of a half-wave apart
 constexpr int kNX = kTile * kCk * kLG / kThreadsC;  // staged elements per thread and slice
 
-__global__ __launch_bounds__(kThreadsC, 3) void k_contract_kdeg(
+__global__ __launch_bounds__(kThreadsC, 4) void k_contract_kdeg(
     int64_t B, int Cin, int Cout, int L, int otiles, int lgroups, const float *__restrict__ W,
     unsigned w_bytes, int w_sl, int w_si, int w_so, const float *__restrict__ X, int x_sb,
     float *__restrict__ Y, int64_t y_sb, int64_t y_so, int64_t y_sk,
@@ -253,36 +253,28 @@ __global__ __launch_bounds__(kThreadsC, 3) void k_contract_kdeg(
     const __amdgpu_buffer_rsrc_t xs =
         rsrc(X + b0 * (int64_t)x_sb, (unsigned)(((int64_t)(nb - 1) * x_sb + (int64_t)Cin * L) * 4));
     const __amdgpu_buffer_rsrc_t ws = rsrc(W, w_bytes);
-    // Staged elements of this thread, k = tid + 256 s. X: row b = k / (kCk kLG), slot
-    // r = k % (kCk kLG) = i kLG + l of the row's slice (consecutive threads read consecutive
-    // slots of a row); their offsets at i0 = 0 and LDS positions are fixed over the
-    // reduction. W: output o = tid % 64 for the wave-uniform (l, i) pairs p = wave + 4 s,
-    // l = p / kCk, i = p % kCk.
-    unsigned xoff[kNX];
-    int xlds[kNX];
-#pragma unroll
-    for (int s2 = 0; s2 < kNX; ++s2) {
-        const int k = tid + kThreadsC * s2;
-        const int b = k / (kCk * kLG), r = k - b * (kCk * kLG);
-        const int i = r / kLG, l = r - i * kLG;
-        xoff[s2] = l < nl && b < nb ? (unsigned)(b * x_sb + i * L + l0 + l) * 4u : kOutside;
-        xlds[s2] = b * kSB + r;
-    }
+    // Staged elements of this thread, k = tid + 256 s. X: row b = k / (kCk kLG) = tid / 32 +
+    // 8 s, slot r = k % (kCk kLG) = tid % 32 = i kLG + l of the row's slice (consecutive
+    // threads read consecutive slots of a row): one base offset, rows 8 apart. Rows past the
+    // group's last lie past the resource and read 0. W: output o = tid % 64 for the
+    // wave-uniform (l, i) pairs p = wave + 4 s, l = p / kCk, i = p % kCk.
+    static_assert(kThreadsC % (kCk * kLG) == 0, "a thread keeps its slot over s");
+    constexpr int kRowStep = kThreadsC / (kCk * kLG);
+    const int xi = (tid % (kCk * kLG)) / kLG, xl = tid % kLG;
+    const bool x_ok = xl < nl;
+    const unsigned xbase = (unsigned)((tid / (kCk * kLG)) * x_sb + xi * L + l0 + xl) * 4u;
+    const unsigned xstep = (unsigned)(kRowStep * x_sb) * 4u;
+    const int xlds = (tid / (kCk * kLG)) * kSB + tid % (kCk * kLG);
     const bool full_i = Cin % kCk == 0;  // every slice has kCk inputs
     const bool o_ok = o0 + (tid & 63) < Cout;
     const unsigned wcol = (unsigned)((o0 + (tid & 63)) * w_so) * 4u;
     float xr[kNX], wr[kNX];
     auto fetch = [&](int i0) {
         const unsigned di = (unsigned)(i0 * L) * 4u;
+        const bool ok = x_ok && (full_i || i0 + xi < Cin);
 #pragma unroll
         for (int s2 = 0; s2 < kNX; ++s2) {
-            unsigned xo = xoff[s2] == kOutside ? kOutside : xoff[s2] + di;
-            if (!full_i) {
-                const int k = tid + kThreadsC * s2;
-                const int i = (k % (kCk * kLG)) / kLG;
-                if (i0 + i >= Cin) xo = kOutside;
-            }
-            xr[s2] = bload(xs, xo);
+            xr[s2] = bload(xs, ok ? xbase + s2 * xstep + di : kOutside);
             const int p = wave + 4 * s2, lw = p / kCk, iw = p % kCk;  // wave-uniform
             const unsigned wo4 = (o_ok && lw < nl && i0 + iw < Cin)
                                      ? wcol + (unsigned)((l0 + lw) * w_sl + (i0 + iw) * w_si) * 4u
@@ -295,7 +287,7 @@ __global__ __launch_bounds__(kThreadsC, 3) void k_contract_kdeg(
         __syncthreads();  // the previous slice is consumed
 #pragma unroll
         for (int s2 = 0; s2 < kNX; ++s2) {
-            Xs[xlds[s2]] = xr[s2];
+            Xs[xlds + s2 * kRowStep * kSB] = xr[s2];
             const int p = wave + 4 * s2;
             Ws[p / kCk][p % kCk][tid & 63] = wr[s2];
         }
