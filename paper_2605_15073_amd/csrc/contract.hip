@@ -207,8 +207,9 @@ __global__ __launch_bounds__(kThreadsC) void k_contract_mfma(
 // seven degrees at two waves, even though a group of 7 then leaves one slot idle). The reduction
 // runs in slices of kCk inputs: each thread prefetches its share of the next slice into
 // registers while the matrix cores work on the current one from LDS. X rows keep their
-// natural (i, l) order in LDS (row stride kSB = 2 mod 32, so the A-operand reads of a
-// half-wave hit distinct banks); W is staged as Ws[l][i][o]. Wave (wb, wo) accumulates
+// natural (i, l) order in LDS (row stride kSB = 2 mod 32: the A-operand reads of a half-wave
+// meet at most two to a bank, the fewest any padded stride gives, since the two lane groups
+// of a half-wave read slots 4 apart); W is staged as Ws[l][i][o]. Wave (wb, wo) accumulates
 // its 32 x 32 sub-tile of D[b][o] for every degree of the group (A = X rows, B = W
 // columns, so 16 lanes write 64 contiguous bytes of a row of Y).
 constexpr int kCk = 8;           // reduction slice per LDS stage

@@ -424,9 +424,9 @@ struct DenseSyn {
     static constexpr int NW = dense_waves(CT, V1), NT = 64 * NW, CTW = CT / NW, WC = 16 * CTW;
     static_assert(CT % NW == 0, "column tiles split evenly over the waves");
     static_assert(V1 || (G::UVs / 16) % CTW == 0, "a wave's column tiles lie in one field");
-    // LDS row stride of a staged A row: KA / 4 odd puts the 16 rows x 4 lane groups of an
-    // operand read on distinct banks
-    static constexpr int KA = (KP / 4) % 2 ? KP : KP + 4;
+    // LDS row stride of a staged A row: KA / 2 odd (KP is a multiple of 4) puts the 16 rows x
+    // 2 lane groups of each 32-lane half of an operand read on distinct banks
+    static constexpr int KA = KP + 2;
     static constexpr int NLA = (16 * G::K + NT - 1) / NT;  // tile loads per thread
 };
 

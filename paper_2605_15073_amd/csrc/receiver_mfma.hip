@@ -105,8 +105,10 @@ __attribute__((amdgpu_waves_per_eu(kRecvWaves<VAL, TWO, SPLIT>(LM)))) void k_rec
     // takes one K step fewer (KSG) than the value sum; its LDS row j holds degree j + DO
     constexpr int DO = (LM > 0 && LM % 4 == 0) ? 1 : 0;
     constexpr int KSG = (L - DO + 3) / 4;
-    // LDS rows of 64 points; point p of row j sits at column p ^ 16 (j & 3), so the rows that
-    // lane groups g = 0..3 read at once (j = 4 kk + g) land on four different groups of 16 banks
+    // LDS rows of 64 points; point p of row j sits at column p ^ 16 (j & 3). A 64-lane LDS
+    // read is served as two halves of 32 lanes over the 32 banks: the two rows a half reads at
+    // once (lane groups g = 2 h, 2 h + 1 at j = 4 kk + g) then fall on different halves of the
+    // banks, and the recurrence's writes of one row stay a permutation of them
     constexpr int RS = PW;
     const Dims &d = tb.d;
     const int UV = d.UV, UVs = d.UVs;
