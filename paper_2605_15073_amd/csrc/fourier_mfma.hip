@@ -874,42 +874,99 @@ __global__ __launch_bounds__(256) void k_analysis_mfma(Tabs<float> tb, int R, in
     // Gauss-Legendre analysis: T[k] = sum_u w_u (2 pi / V) Pt_l^|m|(x_u) Tm[m][u] (Eq.
     // msgpass-Tlm) of each value field; a moved-derivative pair (F1, F2) adds
     // -m sum_u w_u (2 pi / V) Pt_l^|m|(x_u) F1[-m][u] - sum_u w_u (2 pi / V) dPt_l^|m|/dx(x_u) F2[m][u]
-    for (int idx = tid; idx < nr * G::K; idx += nt) {
-        const int q = idx / G::K, k = idx - q * G::K;
-        const int l = (int)sqrtf((float)k + 0.5f);  // exact for k < 2^20
-        const int m = k - l * l - l, am = m < 0 ? -m : m;
-        const int pi = l * (l + 1) / 2 + am;
-        const float4_t *w4 = reinterpret_cast<const float4_t *>(tb.wpt + pi * G::Ut);
-        const float4_t *wd4 = reinterpret_cast<const float4_t *>(tb.wdpt + pi * G::Ut);
-        auto row = [&](int f, int mm) {
-            return reinterpret_cast<const float4_t *>(Tm + ((q * NF + f) * G::M + mm + LM) * G::TS);
-        };
-        auto dot = [&](const float4_t *w, const float4_t *x) {
-            float sum = 0.f;
+    // Up to lmax 7 (at most 12 GL nodes and K <= 64) a thread keeps one (l, m) and its weight
+    // rows in registers over the ranks it serves, nt / K rank groups side by side (the threads
+    // past them idle in this phase); above, where the rows cost more registers and K nears the
+    // workgroup size, threads take (rank, k) pairs in turn, which keeps them evenly loaded.
+    constexpr bool HOLD = G::Ut <= 12;
+    if constexpr (HOLD) {
+        constexpr int NC = G::Ut / 4;
+        const int gq = G::K < nt ? nt / G::K : 1;
+        for (int kq = tid; kq < G::K * gq; kq += nt) {
+            const int q0 = kq / G::K, k = kq - q0 * G::K;
+            // sqrt(k + 1/2) lies at least 1/(4 (l + 1)) from an integer, far more than the
+            // hardware square root's error at these k
+            const int l = (int)__builtin_amdgcn_sqrtf((float)k + 0.5f);
+            const int m = k - l * l - l, am = m < 0 ? -m : m;
+            const int pi = l * (l + 1) / 2 + am;
+            const float4_t *w4 = reinterpret_cast<const float4_t *>(tb.wpt + pi * G::Ut);
+            const float4_t *wd4 = reinterpret_cast<const float4_t *>(tb.wdpt + pi * G::Ut);
+            float4_t wv[NC], wdv[NC];  // the weighted Legendre row and its x-derivative
 #pragma unroll
-            for (int c = 0; c < G::Ut / 4; ++c) {
-                const float4_t a = w[c], y = x[c];
-                sum += a[0] * y[0] + a[1] * y[1] + a[2] * y[2] + a[3] * y[3];
+            for (int c = 0; c < NC; ++c) {
+                wv[c] = w4[c];
+                if (MODE != 0) wdv[c] = wd4[c];
             }
-            return sum;
-        };
-        const float fm = (float)m;
-        // the moved pair's term, formed alike in every mode: a zero flipped slot (mode 2)
-        // then gives exactly the one-slot result (mode 1)
-        auto curl = [&](int f1) { return -fm * dot(w4, row(f1, -m)) - dot(wd4, row(f1 + 1, m)); };
-        float s0, s1;
-        if constexpr (MODE == 0) {
-            s0 = dot(w4, row(0, m));
-            s1 = dot(w4, row(1, m));
-        } else if constexpr (MODE == 1) {
-            s0 = dot(w4, row(0, m));
-            s1 = curl(1);
-        } else {
-            s0 = dot(w4, row(0, m)) + curl(1);
-            s1 = dot(w4, row(3, m)) + curl(4);
+            const float fm = (float)m;
+            for (int q = q0; q < nr; q += gq) {
+                auto row = [&](int f, int mm) {
+                    return reinterpret_cast<const float4_t *>(Tm + ((q * NF + f) * G::M + mm + LM) * G::TS);
+                };
+                auto dot = [&](const float4_t *w, const float4_t *x) {
+                    float sum = 0.f;
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) {
+                        const float4_t a = w[c], y = x[c];
+                        sum += a[0] * y[0] + a[1] * y[1] + a[2] * y[2] + a[3] * y[3];
+                    }
+                    return sum;
+                };
+                // the moved pair's term, formed alike in every mode: a zero flipped slot (mode
+                // 2) then gives exactly the one-slot result (mode 1)
+                auto curl = [&](int f1) { return -fm * dot(wv, row(f1, -m)) - dot(wdv, row(f1 + 1, m)); };
+                float s0, s1;
+                if constexpr (MODE == 0) {
+                    s0 = dot(wv, row(0, m));
+                    s1 = dot(wv, row(1, m));
+                } else if constexpr (MODE == 1) {
+                    s0 = dot(wv, row(0, m));
+                    s1 = curl(1);
+                } else {
+                    s0 = dot(wv, row(0, m)) + curl(1);
+                    s1 = dot(wv, row(3, m)) + curl(4);
+                }
+                Ta[(b * R + r0 + q) * (int64_t)G::K + k] = s0;
+                Tb[(b * R + r0 + q) * (int64_t)G::K + k] = s1;
+            }
         }
-        Ta[(b * R + r0 + q) * (int64_t)G::K + k] = s0;
-        Tb[(b * R + r0 + q) * (int64_t)G::K + k] = s1;
+    } else {
+        for (int idx = tid; idx < nr * G::K; idx += nt) {
+            const int q = idx / G::K, k = idx - q * G::K;
+            const int l = (int)sqrtf((float)k + 0.5f);  // exact for k < 2^20
+            const int m = k - l * l - l, am = m < 0 ? -m : m;
+            const int pi = l * (l + 1) / 2 + am;
+            const float4_t *w4 = reinterpret_cast<const float4_t *>(tb.wpt + pi * G::Ut);
+            const float4_t *wd4 = reinterpret_cast<const float4_t *>(tb.wdpt + pi * G::Ut);
+            auto row = [&](int f, int mm) {
+                return reinterpret_cast<const float4_t *>(Tm + ((q * NF + f) * G::M + mm + LM) * G::TS);
+            };
+            auto dot = [&](const float4_t *w, const float4_t *x) {
+                float sum = 0.f;
+#pragma unroll
+                for (int c = 0; c < G::Ut / 4; ++c) {
+                    const float4_t a = w[c], y = x[c];
+                    sum += a[0] * y[0] + a[1] * y[1] + a[2] * y[2] + a[3] * y[3];
+                }
+                return sum;
+            };
+            const float fm = (float)m;
+            // the moved pair's term, formed alike in every mode: a zero flipped slot (mode 2)
+            // then gives exactly the one-slot result (mode 1)
+            auto curl = [&](int f1) { return -fm * dot(w4, row(f1, -m)) - dot(wd4, row(f1 + 1, m)); };
+            float s0, s1;
+            if constexpr (MODE == 0) {
+                s0 = dot(w4, row(0, m));
+                s1 = dot(w4, row(1, m));
+            } else if constexpr (MODE == 1) {
+                s0 = dot(w4, row(0, m));
+                s1 = curl(1);
+            } else {
+                s0 = dot(w4, row(0, m)) + curl(1);
+                s1 = dot(w4, row(3, m)) + curl(4);
+            }
+            Ta[(b * R + r0 + q) * (int64_t)G::K + k] = s0;
+            Tb[(b * R + r0 + q) * (int64_t)G::K + k] = s1;
+        }
     }
 }
 
